@@ -1,0 +1,255 @@
+"""Python face of the C ABI: the same six calls, taking torch tensors.
+
+Each function checks device / dtype / contiguity, turns tensors into device
+pointers, passes torch's current HIP stream and raises DrError on a non-OK
+status.  Workspaces are allocated with torch when the caller passes none.
+No arithmetic of the method happens here.
+"""
+
+import ctypes
+
+import torch
+
+from . import _lib
+from ._lib import DrLayer, check
+
+_DTYPES = {torch.float32: _lib.DR_F32, torch.bfloat16: _lib.DR_BF16}
+
+
+def _stream(stream):
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _dev(t, name, dtype=None):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+def _contig(t, name):
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _workspace(nbytes, device, workspace):
+    if nbytes == 0:
+        return None, 0
+    if workspace is None:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    if workspace.numel() * workspace.element_size() < nbytes:
+        raise ValueError("workspace too small")
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def _goff_array(goff):
+    arr = (ctypes.c_int64 * len(goff))(*[int(v) for v in goff])
+    return arr
+
+
+def make_layer_array(layers):
+    """Host array of dr_layer descriptors from dicts of device tensors.
+
+    Each dict: x [N, T, d_in], dy [N, T, d_out] (row stride may exceed d),
+    p_in [k_in, d_in], p_out [k_out, d_out], col_offset.
+    """
+    arr = (DrLayer * len(layers))()
+    for i, L in enumerate(layers):
+        x, dy, p_in, p_out = L["x"], L["dy"], L["p_in"], L["p_out"]
+        for t, nm in ((x, "x"), (dy, "dy")):
+            if t.numel() > 0 and (t.stride(-1) != 1 or t.stride(0) != t.shape[1] * t.stride(1)):
+                raise ValueError(f"{nm} must be [N][T][ld] with unit element stride")
+        _contig(p_in, "p_in")
+        _contig(p_out, "p_out")
+        arr[i] = DrLayer(x.data_ptr(), max(x.stride(1), x.shape[2]), dy.data_ptr(), max(dy.stride(1), dy.shape[2]),
+                         p_in.data_ptr(), p_out.data_ptr(),
+                         x.shape[2], dy.shape[2], p_in.shape[0], p_out.shape[0], int(L["col_offset"]))
+    return arr
+
+
+def dr_sketch_workspace_size(layers, N, T, dtype):
+    arr = make_layer_array(layers)
+    return _lib.load().dr_sketch_workspace_size(arr, len(layers), N, T, _DTYPES[dtype])
+
+
+def dr_sketch_grads(layers, N, T, lengths, S, workspace=None, stream=None):
+    """S[i, off_l + a*k_in + b] = sum_{t<len_i} (P_out dy_{i,t})[a] (P_in x_{i,t})[b]."""
+    lib = _lib.load()
+    dtype = layers[0]["x"].dtype
+    if dtype not in _DTYPES:
+        raise ValueError("x must be float32 or bfloat16")
+    for L in layers:
+        for nm in ("x", "dy", "p_in", "p_out"):
+            _dev(L[nm], nm, dtype)
+    _dev(S, "S", torch.float32)
+    if S.dim() != 2 or S.stride(1) != 1:
+        raise ValueError("S must be [N][ldS] with unit column stride")
+    if lengths is not None:
+        _dev(lengths, "lengths", torch.int32)
+        _contig(lengths, "lengths")
+    arr = make_layer_array(layers)
+    nbytes = lib.dr_sketch_workspace_size(arr, len(layers), N, T, _DTYPES[dtype])
+    ws, wsb = _workspace(nbytes, S.device, workspace)
+    check("dr_sketch_grads", lib.dr_sketch_grads(arr, len(layers), N, T, _ptr(lengths), _DTYPES[dtype], _ptr(S),
+                                                 S.stride(0), _ptr(ws), wsb, _stream(stream)))
+    return S
+
+
+def dr_gram_workspace_size(n, m, goff, dtype):
+    return _lib.load().dr_gram_workspace_size(n, m, _goff_array(goff), len(goff) - 1, _DTYPES[dtype])
+
+
+def dr_gram(G, Gt, goff, K, s, t2, workspace=None, stream=None):
+    """Per group: K_p = G_p G_p^T, s_p = G_p gbar_p, t2_p = |gbar_p|^2 (gbar = target mean)."""
+    lib = _lib.load()
+    dtype = Gt.dtype
+    _dev(Gt, "Gt", dtype)
+    n, m = G.shape[0], Gt.shape[0]
+    if n > 0:
+        _dev(G, "G", dtype)
+    for t, nm in ((K, "K"), (s, "s"), (t2, "t2")):
+        _dev(t, nm, torch.float32)
+        _contig(t, nm)
+    P = len(goff) - 1
+    ga = _goff_array(goff)
+    nbytes = lib.dr_gram_workspace_size(n, m, ga, P, _DTYPES[dtype])
+    ws, wsb = _workspace(nbytes, Gt.device, workspace)
+    check("dr_gram", lib.dr_gram(_ptr(G), n, G.stride(0) if n > 0 else 0, _ptr(Gt), m, Gt.stride(0),
+                                 _DTYPES[dtype], ga, P, _ptr(K), _ptr(s), _ptr(t2), _ptr(ws), wsb,
+                                 _stream(stream)))
+
+
+def dr_project_span(K, s, t2, lam, mode, w, lam_eff, resid2, info, stream=None):
+    """(K_p + lam_eff_p I) w_p = s_p per group."""
+    lib = _lib.load()
+    P = t2.shape[0]
+    n = s.shape[-1] if s.numel() > 0 else 0
+    for t, nm in ((K, "K"), (s, "s"), (t2, "t2"), (w, "w"), (lam_eff, "lam_eff"), (resid2, "resid2")):
+        _dev(t, nm, torch.float32)
+        _contig(t, nm)
+    _dev(info, "info", torch.int32)
+    check("dr_project_span", lib.dr_project_span(_ptr(K), _ptr(s), _ptr(t2), n, P, float(lam), int(mode), _ptr(w),
+                                                 _ptr(lam_eff), _ptr(resid2), _ptr(info), None, 0,
+                                                 _stream(stream)))
+
+
+def dr_project_cone(K, s, t2, max_iter, kkt_tol, w, resid2, iters, kkt, info, stream=None):
+    """w_p = argmin_{w >= 0} 1/2 w^T K_p w - s_p^T w per group."""
+    lib = _lib.load()
+    P = t2.shape[0]
+    n = s.shape[-1] if s.numel() > 0 else 0
+    for t, nm in ((K, "K"), (s, "s"), (t2, "t2"), (w, "w"), (resid2, "resid2"), (kkt, "kkt")):
+        _dev(t, nm, torch.float32)
+        _contig(t, nm)
+    for t, nm in ((iters, "iters"), (info, "info")):
+        _dev(t, nm, torch.int32)
+    check("dr_project_cone", lib.dr_project_cone(_ptr(K), _ptr(s), _ptr(t2), n, P, int(max_iter), float(kkt_tol),
+                                                 _ptr(w), _ptr(resid2), _ptr(iters), _ptr(kkt), _ptr(info), None,
+                                                 0, _stream(stream)))
+
+
+def dr_select_topk(s, k, idx, w, info, stream=None):
+    """idx_p = the k largest s_p (ties -> lowest index), ascending; w_p = 1/k on idx_p."""
+    lib = _lib.load()
+    P, n = s.shape
+    _dev(s, "s", torch.float32)
+    _contig(s, "s")
+    _dev(idx, "idx", torch.int32)
+    _dev(info, "info", torch.int32)
+    if w is not None:
+        _dev(w, "w", torch.float32)
+    check("dr_select_topk", lib.dr_select_topk(_ptr(s), n, P, int(k), _ptr(idx), _ptr(w), _ptr(info),
+                                               _stream(stream)))
+
+
+def dr_combine_workspace_size(n, goff):
+    return _lib.load().dr_combine_workspace_size(n, _goff_array(goff), len(goff) - 1)
+
+
+def dr_combine(G, goff, w, u, workspace=None, stream=None):
+    """u[cols_p] = G[:, cols_p]^T w_p per group."""
+    lib = _lib.load()
+    dtype = G.dtype
+    n = G.shape[0]
+    if n > 0:
+        _dev(G, "G", dtype)
+    _dev(w, "w", torch.float32)
+    _dev(u, "u", torch.float32)
+    P = len(goff) - 1
+    ga = _goff_array(goff)
+    nbytes = lib.dr_combine_workspace_size(n, ga, P)
+    ws, wsb = _workspace(nbytes, u.device, workspace)
+    check("dr_combine", lib.dr_combine(_ptr(G), n, G.stride(0) if n > 0 else 0, _DTYPES[dtype], ga, P, _ptr(w),
+                                       _ptr(u), _ptr(ws), wsb, _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+# allocating conveniences (outputs created with torch on the inputs' device)
+# ---------------------------------------------------------------------------
+
+def sketch(layers, lengths=None, stream=None):
+    N, T = layers[0]["x"].shape[:2]
+    kt = max(int(L["col_offset"]) + L["p_in"].shape[0] * L["p_out"].shape[0] for L in layers)
+    S = torch.empty(N, kt, dtype=torch.float32, device=layers[0]["x"].device)
+    return dr_sketch_grads(layers, N, T, lengths, S, stream=stream)
+
+
+def gram(G, Gt, goff=None, stream=None):
+    if goff is None:
+        goff = [0, Gt.shape[1]]
+    P, n = len(goff) - 1, G.shape[0]
+    dev = Gt.device
+    K = torch.empty(P, n, n, dtype=torch.float32, device=dev)
+    s = torch.empty(P, n, dtype=torch.float32, device=dev)
+    t2 = torch.empty(P, dtype=torch.float32, device=dev)
+    dr_gram(G, Gt, goff, K, s, t2, stream=stream)
+    return K, s, t2
+
+
+def project_span(K, s, t2, lam, mode=_lib.DR_RIDGE_REL_TRACE, stream=None):
+    P, n = s.shape
+    dev = t2.device
+    w = torch.empty(P, n, dtype=torch.float32, device=dev)
+    lam_eff = torch.empty(P, dtype=torch.float32, device=dev)
+    resid2 = torch.empty(P, dtype=torch.float32, device=dev)
+    info = torch.empty(P, dtype=torch.int32, device=dev)
+    dr_project_span(K, s, t2, lam, mode, w, lam_eff, resid2, info, stream=stream)
+    return w, lam_eff, resid2, info
+
+
+def project_cone(K, s, t2, max_iter, kkt_tol=0.0, stream=None):
+    P, n = s.shape
+    dev = t2.device
+    w = torch.empty(P, n, dtype=torch.float32, device=dev)
+    resid2 = torch.empty(P, dtype=torch.float32, device=dev)
+    iters = torch.empty(P, dtype=torch.int32, device=dev)
+    kkt = torch.empty(P, dtype=torch.float32, device=dev)
+    info = torch.empty(P, dtype=torch.int32, device=dev)
+    dr_project_cone(K, s, t2, max_iter, kkt_tol, w, resid2, iters, kkt, info, stream=stream)
+    return w, resid2, iters, kkt, info
+
+
+def select_topk(s, k, with_weights=True, stream=None):
+    P, n = s.shape
+    dev = s.device
+    idx = torch.empty(P, k, dtype=torch.int32, device=dev)
+    w = torch.empty(P, n, dtype=torch.float32, device=dev) if with_weights else None
+    info = torch.empty(P, dtype=torch.int32, device=dev)
+    dr_select_topk(s, k, idx, w, info, stream=stream)
+    return idx, w, info
+
+
+def combine(G, w, goff=None, stream=None):
+    if goff is None:
+        goff = [0, G.shape[1]]
+    u = torch.zeros(goff[-1], dtype=torch.float32, device=w.device)
+    dr_combine(G, goff, w, u, stream=stream)
+    return u

@@ -1,0 +1,336 @@
+// Target mean, Gram matrix and alignment scores per parameter group (dr_gram).
+//
+// Per group p (a column range of the sketch matrix, Sec. 3.3.3):
+//   gbar_p = mean of the m target rows            (Sec. 3.2)
+//   K_p    = G_p G_p^T                             (redundancy term, Sec. 3.3.2)
+//   s_p    = G_p gbar_p,  t2_p = ||gbar_p||^2      (alignment scores)
+//
+// Kernels
+//   target_mean_kernel : gbar in fp32 (fp64 sum over the m rows).
+//   gram_tile_kernel   : one 64x64 tile of K_p over one chunk of the group's
+//                        columns (lower-triangle tile pairs only), on MFMA
+//                        (bf16 16x16x32 or fp32 16x16x4, fp32 accumulate).
+//                        Operands stream from memory straight into registers.
+//   gram_reduce_kernel : sums the chunk partials of a tile in chunk order and
+//                        writes the lower triangle and its mirror, so K is
+//                        exactly symmetric.
+//   score_kernel       : s_p[i] = <G_p[i], gbar_p> and t2_p (row n := gbar),
+//                        fp64 accumulation, fixed-order block reduction.
+// No atomics: results are deterministic.
+
+#include "common.h"
+
+namespace dr {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kTile = 64;
+constexpr int kMaxGroups = 128;   // groups per launch (more groups -> more launches)
+constexpr int kTargetWGs = 1024;
+
+struct GramArgs {
+  const unsigned char* G;
+  long long ldG;
+  int n;
+  long long goff[kMaxGroups + 1];   // absolute column offsets of this launch's groups
+  int P;
+  int NT, pairs, CK, maxchunks;
+  float* partial;                   // [P][pairs][maxchunks][kTile*kTile]
+};
+
+template <bool BF16>
+struct GTr;
+template <>
+struct GTr<true> {
+  static constexpr int ES = 2, EPV = 8, KV = 32;   // KV: columns per 16-byte vector per lane group
+};
+template <>
+struct GTr<false> {
+  static constexpr int ES = 4, EPV = 4, KV = 16;
+};
+
+template <bool BF16>
+__device__ __forceinline__ f32x4 mma_v(u32x4 a, u32x4 b, f32x4 c) {
+  if constexpr (BF16) {
+    return mma_bf16(a, b, c);
+  } else {
+    c = mma_f32(__uint_as_float(a.x), __uint_as_float(b.x), c);
+    c = mma_f32(__uint_as_float(a.y), __uint_as_float(b.y), c);
+    c = mma_f32(__uint_as_float(a.z), __uint_as_float(b.z), c);
+    c = mma_f32(__uint_as_float(a.w), __uint_as_float(b.w), c);
+    return c;
+  }
+}
+
+__device__ __forceinline__ void pair_to_tiles(int q, int& I, int& J) {
+  int i = (int)((sqrtf(8.f * q + 1.f) - 1.f) * 0.5f);
+  while ((i + 1) * (i + 2) / 2 <= q) ++i;
+  while (i * (i + 1) / 2 > q) --i;
+  I = i;
+  J = q - i * (i + 1) / 2;
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(kThreads, 2) void gram_tile_kernel(GramArgs a) {
+  using E = GTr<BF16>;
+  constexpr int NV = 2;              // vectors per row-block per step
+  constexpr int STEP = NV * 4 * E::EPV;   // columns per step (4 lane groups)
+  const int chunk = blockIdx.x, q = blockIdx.y, p = blockIdx.z;
+  const long long g0 = a.goff[p], g1 = a.goff[p + 1];
+  const long long c0 = g0 + (long long)chunk * a.CK;
+  if (c0 >= g1) return;
+  const long long c1 = c0 + a.CK < g1 ? c0 + a.CK : g1;
+  int I, J;
+  pair_to_tiles(q, I, J);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int wr = wave >> 1, wc = wave & 1;
+
+  int rowA[2], rowB[2];
+  bool okA[2], okB[2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    rowA[b] = I * kTile + wr * 32 + b * 16 + lr;
+    rowB[b] = J * kTile + wc * 32 + b * 16 + lr;
+    okA[b] = rowA[b] < a.n;
+    okB[b] = rowB[b] < a.n;
+  }
+
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto load = [&](long long cs, u32x4 (&va)[2][NV], u32x4 (&vb)[2][NV]) {
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const long long c = cs + (long long)v * 4 * E::EPV + lg * E::EPV;
+      const bool cok = c < c1;
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        va[b][v] = (okA[b] && cok)
+                       ? *reinterpret_cast<const u32x4*>(a.G + ((long long)rowA[b] * a.ldG + c) * E::ES)
+                       : u32x4{0u, 0u, 0u, 0u};
+        vb[b][v] = (okB[b] && cok)
+                       ? *reinterpret_cast<const u32x4*>(a.G + ((long long)rowB[b] * a.ldG + c) * E::ES)
+                       : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+  };
+
+  u32x4 va[2][NV], vb[2][NV], na[2][NV], nb[2][NV];
+  load(c0, va, vb);
+  for (long long cs = c0; cs < c1; cs += STEP) {
+    const bool more = cs + STEP < c1;
+    if (more) load(cs + STEP, na, nb);
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = mma_v<BF16>(va[i][v], vb[j][v], acc[i][j]);
+    if (more) {
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          va[b][v] = na[b][v];
+          vb[b][v] = nb[b][v];
+        }
+    }
+  }
+
+  float* out = a.partial + (((long long)p * a.pairs + q) * a.maxchunks + chunk) * (kTile * kTile);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        out[(wr * 32 + i * 16 + lg * 4 + r) * kTile + wc * 32 + j * 16 + lr] = acc[i][j][r];
+}
+
+__global__ __launch_bounds__(kThreads) void gram_reduce_kernel(GramArgs a, float* K, long long pbase) {
+  const int q = blockIdx.x, p = blockIdx.y;
+  const long long width = a.goff[p + 1] - a.goff[p];
+  const int nvalid = (int)((width + a.CK - 1) / a.CK);
+  int I, J;
+  pair_to_tiles(q, I, J);
+  const float* src = a.partial + ((long long)p * a.pairs + q) * a.maxchunks * (kTile * kTile);
+  float* Kp = K + (pbase + p) * (long long)a.n * a.n;
+  for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
+    const int r = I * kTile + e / kTile, c = J * kTile + e % kTile;
+    if (r >= a.n || c >= a.n || c > r) continue;
+    float acc = 0.f;
+    for (int ch = 0; ch < nvalid; ++ch) acc += src[(long long)ch * (kTile * kTile) + e];
+    Kp[(long long)r * a.n + c] = acc;
+    Kp[(long long)c * a.n + r] = acc;
+  }
+}
+
+// gbar[c] = (1/m) sum_j Gt[j][c] for c in [c_lo, c_hi)
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void target_mean_kernel(const unsigned char* Gt, long long ldGt, int m,
+                                                               long long c_lo, long long c_hi, float* gbar) {
+  const long long c = c_lo + (long long)blockIdx.x * kThreads + threadIdx.x;
+  if (c >= c_hi) return;
+  double acc = 0.0;
+  for (int j = 0; j < m; ++j) {
+    float v;
+    if constexpr (BF16) {
+      const unsigned short h = reinterpret_cast<const unsigned short*>(Gt)[(long long)j * ldGt + c];
+      v = __uint_as_float((unsigned)h << 16);
+    } else {
+      v = reinterpret_cast<const float*>(Gt)[(long long)j * ldGt + c];
+    }
+    acc += (double)v;
+  }
+  gbar[c] = (float)(acc / (double)m);
+}
+
+// s[p][i] = <G[i][cols_p], gbar[cols_p]> for i < n; row n gives t2[p] = <gbar, gbar>.
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void score_kernel(GramArgs a, const float* gbar, float* s, float* t2,
+                                                         long long pbase) {
+  const int i = blockIdx.x, p = blockIdx.y;
+  const long long g0 = a.goff[p], g1 = a.goff[p + 1];
+  double acc = 0.0;
+  if (i < a.n) {
+    const unsigned char* row = a.G + (long long)i * a.ldG * GTr<BF16>::ES;
+    for (long long c = g0 + threadIdx.x; c < g1; c += kThreads) {
+      float v;
+      if constexpr (BF16)
+        v = __uint_as_float((unsigned)reinterpret_cast<const unsigned short*>(row)[c] << 16);
+      else
+        v = reinterpret_cast<const float*>(row)[c];
+      acc += (double)v * (double)gbar[c];
+    }
+  } else {
+    for (long long c = g0 + threadIdx.x; c < g1; c += kThreads) acc += (double)gbar[c] * (double)gbar[c];
+  }
+  __shared__ double red[kThreads];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int w = kThreads / 2; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    if (i < a.n)
+      s[(pbase + p) * (long long)a.n + i] = (float)red[0];
+    else
+      t2[pbase + p] = (float)red[0];
+  }
+}
+
+struct GramPlan {
+  int NT, pairs, CK, maxchunks;
+  size_t gbar_bytes, partial_bytes;
+};
+
+// Chunk length: a multiple of 256 columns, shrunk until a launch has about
+// kTargetWGs workgroups; identical for every launch of a call.
+GramPlan gram_plan(int64_t n, const int64_t* goff, int P) {
+  GramPlan g;
+  g.NT = (int)((n + kTile - 1) / kTile);
+  g.pairs = g.NT * (g.NT + 1) / 2;
+  int64_t maxw = 0;
+  for (int p = 0; p < P; ++p) maxw = goff[p + 1] - goff[p] > maxw ? goff[p + 1] - goff[p] : maxw;
+  const int gp = P < kMaxGroups ? P : kMaxGroups;
+  int64_t ck = align_up((size_t)(maxw > 0 ? maxw : 1), 256);
+  while (ck > 256 && (int64_t)g.pairs * gp * ((maxw + ck - 1) / ck) < kTargetWGs) ck = align_up((size_t)(ck / 2), 256);
+  g.CK = (int)ck;
+  g.maxchunks = (int)((maxw + ck - 1) / ck);
+  if (g.maxchunks < 1) g.maxchunks = 1;
+  g.gbar_bytes = align_up((size_t)(goff[P] > 0 ? goff[P] : 1) * sizeof(float), 256);
+  g.partial_bytes = (size_t)gp * g.pairs * g.maxchunks * kTile * kTile * sizeof(float);
+  if (n == 0) g.partial_bytes = 0;
+  return g;
+}
+
+dr_status gram_validate(const void* G, int64_t n, int64_t ldG, const void* Gt, int64_t m, int64_t ldGt,
+                        dr_dtype dtype, const int64_t* goff, int P, float* K, float* s, float* t2) {
+  if (dtype != DR_BF16 && dtype != DR_F32) return DR_ERR_DTYPE;
+  if (!goff || P < 1 || n < 0 || m < 1 || n > (1 << 20)) return DR_ERR_ARG;
+  if (goff[0] < 0) return DR_ERR_ARG;
+  for (int p = 0; p < P; ++p)
+    if (goff[p + 1] < goff[p]) return DR_ERR_ARG;
+  const int64_t vec = dtype == DR_BF16 ? 8 : 4;
+  if (ldGt < goff[P] || ldGt % vec || !Gt || !aligned16(Gt) || !t2) return DR_ERR_ARG;
+  if (n > 0) {
+    if (ldG < goff[P] || ldG % vec || !G || !aligned16(G) || !K || !s) return DR_ERR_ARG;
+    for (int p = 0; p <= P; ++p)
+      if (goff[p] % vec) return DR_ERR_ARG;
+  }
+  return DR_OK;
+}
+
+}  // namespace
+}  // namespace dr
+
+extern "C" size_t dr_gram_workspace_size(int64_t n, int64_t m, const int64_t* goff, int P, dr_dtype dtype) {
+  (void)m;
+  (void)dtype;
+  if (!goff || P < 1 || n < 0) return 0;
+  dr::GramPlan g = dr::gram_plan(n, goff, P);
+  return g.gbar_bytes + g.partial_bytes;
+}
+
+extern "C" dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* Gt, int64_t m, int64_t ldGt,
+                             dr_dtype dtype, const int64_t* goff, int P, float* K, float* s, float* t2,
+                             void* workspace, size_t ws_bytes, void* stream) {
+  using namespace dr;
+  dr_status st = gram_validate(G, n, ldG, Gt, m, ldGt, dtype, goff, P, K, s, t2);
+  if (st != DR_OK) return st;
+  GramPlan g = gram_plan(n, goff, P);
+  if (!workspace || ws_bytes < g.gbar_bytes + g.partial_bytes) return DR_ERR_WORKSPACE;
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  const bool bf = dtype == DR_BF16;
+  float* gbar = static_cast<float*>(workspace);
+  float* partial = reinterpret_cast<float*>(static_cast<unsigned char*>(workspace) + g.gbar_bytes);
+
+  const long long c_lo = goff[0], c_hi = goff[P];
+  if (c_hi > c_lo) {
+    const int blocks = (int)((c_hi - c_lo + kThreads - 1) / kThreads);
+    if (bf)
+      hipLaunchKernelGGL(target_mean_kernel<true>, dim3(blocks), dim3(kThreads), 0, hs,
+                         static_cast<const unsigned char*>(Gt), (long long)ldGt, (int)m, c_lo, c_hi, gbar);
+    else
+      hipLaunchKernelGGL(target_mean_kernel<false>, dim3(blocks), dim3(kThreads), 0, hs,
+                         static_cast<const unsigned char*>(Gt), (long long)ldGt, (int)m, c_lo, c_hi, gbar);
+    if ((st = launch_status()) != DR_OK) return st;
+  }
+
+  for (int p0 = 0; p0 < P; p0 += kMaxGroups) {
+    const int gp = P - p0 < kMaxGroups ? P - p0 : kMaxGroups;
+    GramArgs a = {};
+    a.G = static_cast<const unsigned char*>(G);
+    a.ldG = ldG;
+    a.n = (int)n;
+    for (int p = 0; p <= gp; ++p) a.goff[p] = goff[p0 + p];
+    a.P = gp;
+    a.NT = g.NT;
+    a.pairs = g.pairs;
+    a.CK = g.CK;
+    a.maxchunks = g.maxchunks;
+    a.partial = partial;
+    if (n > 0) {
+      dim3 grid(g.maxchunks, g.pairs, gp);
+      if (bf)
+        hipLaunchKernelGGL(gram_tile_kernel<true>, grid, dim3(kThreads), 0, hs, a);
+      else
+        hipLaunchKernelGGL(gram_tile_kernel<false>, grid, dim3(kThreads), 0, hs, a);
+      if ((st = launch_status()) != DR_OK) return st;
+      hipLaunchKernelGGL(gram_reduce_kernel, dim3(g.pairs, gp), dim3(kThreads), 0, hs, a, K, (long long)p0);
+      if ((st = launch_status()) != DR_OK) return st;
+    }
+    if (bf)
+      hipLaunchKernelGGL(score_kernel<true>, dim3(n + 1, gp), dim3(kThreads), 0, hs, a, gbar, s, t2, (long long)p0);
+    else
+      hipLaunchKernelGGL(score_kernel<false>, dim3(n + 1, gp), dim3(kThreads), 0, hs, a, gbar, s, t2, (long long)p0);
+    if ((st = launch_status()) != DR_OK) return st;
+  }
+  return DR_OK;
+}

@@ -1,0 +1,412 @@
+// Projection of the mean target gradient onto the feasible set spanned by
+// the general-data gradients, in Gram form (Eq. (proj), Sec. 3.3.1):
+//   span:  (K + lam_eff I) w = s                 (dr_project_span)
+//   cone:  min_{w >= 0} 1/2 w^T K w - s^T w      (dr_project_cone)
+// One workgroup per group p.  Both report resid2 = ||gbar - G^T w||^2 =
+// t2 - 2 s.w + w.K.w without touching G.
+//
+// span_small_kernel (n <= 256): the lower triangle of K + lam_eff I is held
+// packed in LDS (fp32, at most 129 KiB) and factored right-looking by the
+// whole workgroup; forward / back substitution run on fp64 vectors; two
+// steps of iterative refinement recompute s - (K + lam_eff I) w in fp64
+// from the fp32 K read from global memory, which brings the solution to
+// fp64-level accuracy whenever cond(K + lam_eff I) * 2^-24 < 1.
+//
+// cone_pg_kernel (n <= 256): projected gradient on the Jacobi-scaled
+// problem, written on the unscaled variable: with r_i = K_ii^-1/2,
+//   w_i <- max(0, w_i - r_i^2 (K w - s)_i / Lhat),  Lhat = max_i sum_j r_i |K_ij| r_j,
+// which is exactly w~ <- max(0, w~ - (K~ w~ - s~)/Lhat) for w~ = w / r.
+// K stays in registers as the exact fp32 input (rows split over a
+// power-of-two group of lanes within one wave); w and all sums are fp64.
+
+#include "common.h"
+
+namespace dr {
+namespace {
+
+constexpr int kSpanThreads = 1024;
+constexpr int kSpanMaxN = 256;
+constexpr int kConeThreads = 1024;
+constexpr int kConeMaxN = 256;
+
+__device__ __forceinline__ int tri(int i, int j) { return i * (i + 1) / 2 + j; }   // j <= i
+
+// block-wide fp64 sum over kSpanThreads / kConeThreads threads (fixed order)
+template <int NT>
+__device__ double block_sum(double v, double* scratch) {
+  const int tid = threadIdx.x;
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_down(v, off, 64);
+  if ((tid & 63) == 0) scratch[tid >> 6] = v;
+  __syncthreads();
+  double r = 0.0;
+  if (tid == 0) {
+    for (int w = 0; w < NT / 64; ++w) r += scratch[w];
+    scratch[NT / 64] = r;
+  }
+  __syncthreads();
+  r = scratch[NT / 64];
+  __syncthreads();
+  return r;
+}
+
+__global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K, const float* s, const float* t2,
+                                                                  int n, float lambda, int mode, float* w,
+                                                                  float* lam_eff_out, float* resid2, int* info) {
+  __shared__ float Lp[kSpanMaxN * (kSpanMaxN + 1) / 2];
+  __shared__ double x[kSpanMaxN], y[kSpanMaxN], r[kSpanMaxN];
+  __shared__ double scratch[kSpanThreads / 64 + 1];
+  __shared__ int flag;
+  const int p = blockIdx.x, tid = threadIdx.x;
+  const float* Kp = K + (long long)p * n * n;
+  const float* sp = s + (long long)p * n;
+
+  // non-finite inputs and the trace
+  double tr = 0.0;
+  int bad = 0;
+  for (int i = tid; i < n; i += kSpanThreads) {
+    tr += (double)Kp[(long long)i * n + i];
+    if (!isfinite(sp[i])) bad = 1;
+  }
+  for (int e = tid; e < n * n; e += kSpanThreads)
+    if (!isfinite(Kp[e])) bad = 1;
+  if (tid == 0) flag = 0;
+  __syncthreads();
+  if (bad) flag = 1;
+  tr = block_sum<kSpanThreads>(tr, scratch);
+  const bool nonfinite = flag != 0;
+  __syncthreads();
+
+  const float lam = mode == DR_RIDGE_REL_TRACE ? (float)((double)lambda * tr / (double)n) : lambda;
+  if (nonfinite || (mode == DR_RIDGE_REL_TRACE && tr == 0.0)) {
+    for (int i = tid; i < n; i += kSpanThreads) w[(long long)p * n + i] = 0.f;
+    if (tid == 0) {
+      lam_eff_out[p] = nonfinite ? 0.f : lam;
+      resid2[p] = t2[p];
+      info[p] = nonfinite ? DR_INFO_NONFINITE : 0;
+    }
+    return;
+  }
+
+  for (int e = tid; e < n * (n + 1) / 2; e += kSpanThreads) {
+    int i = (int)((sqrtf(8.f * e + 1.f) - 1.f) * 0.5f);
+    while (tri(i + 1, 0) <= e) ++i;
+    while (tri(i, 0) > e) --i;
+    const int j = e - tri(i, 0);
+    float v = Kp[(long long)i * n + j];
+    if (i == j) v += lam;
+    Lp[e] = v;
+  }
+  if (tid == 0) flag = 0;
+  __syncthreads();
+
+  // right-looking Cholesky, column by column
+  for (int j = 0; j < n; ++j) {
+    if (tid == 0) {
+      const float d = Lp[tri(j, j)];
+      if (!(d > 0.f))
+        flag = j + 1;
+      else
+        Lp[tri(j, j)] = sqrtf(d);
+    }
+    __syncthreads();
+    if (flag) break;
+    const float ljj = Lp[tri(j, j)];
+    for (int i = j + 1 + tid; i < n; i += kSpanThreads) Lp[tri(i, j)] /= ljj;
+    __syncthreads();
+    const int m = n - 1 - j;
+    const int cnt = m * (m + 1) / 2;
+    for (int e = tid; e < cnt; e += kSpanThreads) {
+      int rr = (int)((sqrtf(8.f * e + 1.f) - 1.f) * 0.5f);
+      while (tri(rr + 1, 0) <= e) ++rr;
+      while (tri(rr, 0) > e) --rr;
+      const int cc = e - tri(rr, 0);
+      const int i = j + 1 + rr, k = j + 1 + cc;
+      Lp[tri(i, k)] -= Lp[tri(i, j)] * Lp[tri(k, j)];
+    }
+    __syncthreads();
+  }
+  if (flag) {
+    for (int i = tid; i < n; i += kSpanThreads) w[(long long)p * n + i] = 0.f;
+    if (tid == 0) {
+      lam_eff_out[p] = lam;
+      resid2[p] = t2[p];
+      info[p] = flag;
+    }
+    return;
+  }
+
+  // solve (L L^T) z = rhs in place (rhs in y on entry, z in y on exit)
+  auto chol_solve = [&]() {
+    for (int j = 0; j < n; ++j) {
+      if (tid == 0) y[j] /= (double)Lp[tri(j, j)];
+      __syncthreads();
+      const double yj = y[j];
+      for (int i = j + 1 + tid; i < n; i += kSpanThreads) y[i] -= (double)Lp[tri(i, j)] * yj;
+      __syncthreads();
+    }
+    for (int j = n - 1; j >= 0; --j) {
+      if (tid == 0) y[j] /= (double)Lp[tri(j, j)];
+      __syncthreads();
+      const double yj = y[j];
+      for (int i = tid; i < j; i += kSpanThreads) y[i] -= (double)Lp[tri(j, i)] * yj;
+      __syncthreads();
+    }
+  };
+
+  for (int i = tid; i < n; i += kSpanThreads) {
+    y[i] = (double)sp[i];
+    x[i] = 0.0;
+  }
+  __syncthreads();
+  chol_solve();
+  for (int i = tid; i < n; i += kSpanThreads) x[i] = y[i];
+  __syncthreads();
+
+  // iterative refinement with fp64 residuals of the fp32 K
+  for (int it = 0; it < 2; ++it) {
+    for (int i = tid; i < n; i += kSpanThreads) {
+      const float* Ki = Kp + (long long)i * n;
+      double acc = (double)sp[i] - (double)lam * x[i];
+      for (int j = 0; j < n; ++j) acc -= (double)Ki[j] * x[j];
+      r[i] = acc;
+    }
+    __syncthreads();
+    for (int i = tid; i < n; i += kSpanThreads) y[i] = r[i];
+    __syncthreads();
+    chol_solve();
+    for (int i = tid; i < n; i += kSpanThreads) x[i] += y[i];
+    __syncthreads();
+  }
+
+  // resid2 = t2 - 2 s.x + x.K.x
+  double part = 0.0;
+  for (int i = tid; i < n; i += kSpanThreads) {
+    const float* Ki = Kp + (long long)i * n;
+    double kx = 0.0;
+    for (int j = 0; j < n; ++j) kx += (double)Ki[j] * x[j];
+    part += x[i] * kx - 2.0 * (double)sp[i] * x[i];
+  }
+  const double q = block_sum<kSpanThreads>(part, scratch);
+  for (int i = tid; i < n; i += kSpanThreads) w[(long long)p * n + i] = (float)x[i];
+  if (tid == 0) {
+    lam_eff_out[p] = lam;
+    resid2[p] = (float)((double)t2[p] + q);
+    info[p] = 0;
+  }
+}
+
+// MAXC: K entries held per thread (columns part, part + tpr, ...)
+template <int MAXC>
+__global__ __launch_bounds__(kConeThreads) void cone_pg_kernel(const float* K, const float* s, const float* t2, int n,
+                                                               int max_iter, float kkt_tol, float* w, float* resid2,
+                                                               int* iters, float* kkt, int* info) {
+  __shared__ double wbuf[2][kConeMaxN];
+  __shared__ double rsc[kConeMaxN];
+  __shared__ double scratch[kConeThreads / 64 + 1];
+  __shared__ int flag;
+  const int p = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+  const float* Kp = K + (long long)p * n * n;
+  const float* sp = s + (long long)p * n;
+
+  // lanes per row: a power of two <= 64 with rows * tpr <= kConeThreads
+  int npad = 1;
+  while (npad < n) npad <<= 1;
+  int tpr = kConeThreads / npad;
+  if (tpr > 64) tpr = 64;
+  const int row = tid / tpr, part = tid % tpr;
+  const bool has_row = row < n;
+
+  if (tid == 0) flag = 0;
+  __syncthreads();
+  int bad = 0;
+  for (int e = tid; e < n * n; e += kConeThreads)
+    if (!isfinite(Kp[e])) bad = 1;
+  for (int i = tid; i < n; i += kConeThreads)
+    if (!isfinite(sp[i])) bad = 1;
+  if (bad) flag = 1;
+  for (int i = tid; i < n; i += kConeThreads) {
+    const float d = Kp[(long long)i * n + i];
+    rsc[i] = d > 0.f ? 1.0 / sqrt((double)d) : 0.0;
+    wbuf[0][i] = 0.0;
+  }
+  __syncthreads();
+  if (flag) {
+    for (int i = tid; i < n; i += kConeThreads) w[(long long)p * n + i] = 0.f;
+    if (tid == 0) {
+      resid2[p] = t2[p];
+      iters[p] = 0;
+      kkt[p] = 0.f;
+      info[p] = DR_INFO_NONFINITE;
+    }
+    return;
+  }
+
+  // this thread's slice of row `row`: columns part, part + tpr, ...
+  // MAXC > 0: the slice lives in registers; MAXC == 0: it is re-read from
+  // global memory (L2-resident) every iteration (n > 128)
+  constexpr int KREG = MAXC > 0 ? MAXC : 1;
+  float kr[KREG];
+  double lrow = 0.0;
+  if constexpr (MAXC > 0) {
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+      const int j = part + c * tpr;
+      kr[c] = (has_row && j < n) ? Kp[(long long)row * n + j] : 0.f;
+      if (has_row && j < n) lrow += fabs((double)kr[c]) * rsc[j];
+    }
+  } else {
+    kr[0] = 0.f;
+    if (has_row)
+      for (int j = part; j < n; j += tpr) lrow += fabs((double)Kp[(long long)row * n + j]) * rsc[j];
+  }
+  for (int off = tpr / 2; off > 0; off >>= 1) lrow += __shfl_xor(lrow, off, 64);
+  double lmax = has_row ? lrow * rsc[row] : 0.0;
+  for (int off = 32; off > 0; off >>= 1) lmax = fmax(lmax, __shfl_xor(lmax, off, 64));
+  if (lane == 0) scratch[tid >> 6] = lmax;
+  double sabs = 0.0;
+  for (int i = 0; i < n; ++i) sabs = fmax(sabs, fabs(rsc[i] * (double)sp[i]));
+  __syncthreads();
+  double Lhat = 0.0;
+  for (int q = 0; q < kConeThreads / 64; ++q) Lhat = fmax(Lhat, scratch[q]);
+  __syncthreads();
+  const double den = sabs > 0.0 ? sabs : 2.2250738585072014e-308;
+  const double ri = has_row ? rsc[row] : 0.0;
+  const double si = has_row ? (double)sp[row] : 0.0;
+
+  int it = 0, cur = 0;
+  double rho = 0.0, gi = 0.0;
+  while (true) {
+    const double* wc = wbuf[cur];
+    double acc = 0.0;
+    if constexpr (MAXC > 0) {
+#pragma unroll
+      for (int c = 0; c < MAXC; ++c) {
+        const int j = part + c * tpr;
+        if (j < n) acc += (double)kr[c] * wc[j];
+      }
+    } else {
+      if (has_row)
+        for (int j = part; j < n; j += tpr) acc += (double)Kp[(long long)row * n + j] * wc[j];
+    }
+    for (int off = tpr / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    gi = acc - si;                        // (K w - s)_row
+    const double wi = has_row ? wc[row] : 0.0;
+    // scaled KKT residual |min(w~_i, g~_i)|
+    double v = 0.0;
+    if (has_row && ri > 0.0) v = fabs(fmin(wi / ri, ri * gi));
+    for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
+    if (lane == 0) scratch[tid >> 6] = v;
+    __syncthreads();
+    double vmax = 0.0;
+    for (int q = 0; q < kConeThreads / 64; ++q) vmax = fmax(vmax, scratch[q]);
+    rho = vmax / den;
+    if ((kkt_tol > 0.f && rho <= (double)kkt_tol) || it >= max_iter || Lhat == 0.0) break;
+    if (has_row && part == 0) {
+      const double nw = wi - ri * ri * gi / Lhat;
+      wbuf[cur ^ 1][row] = nw > 0.0 ? nw : 0.0;
+    }
+    __syncthreads();
+    cur ^= 1;
+    ++it;
+  }
+
+  // resid2 = t2 - s.w + w.(K w - s)
+  __syncthreads();   // every wave has read the last residual maxima
+  double contrib = 0.0;
+  if (has_row && part == 0) {
+    const double wi = wbuf[cur][row];
+    contrib = wi * gi - si * wi;
+    w[(long long)p * n + row] = (float)wi;
+  }
+  const double q = block_sum<kConeThreads>(contrib, scratch);
+  if (tid == 0) {
+    resid2[p] = (float)((double)t2[p] + q);
+    iters[p] = it;
+    kkt[p] = (float)rho;
+    info[p] = (kkt_tol > 0.f && rho > (double)kkt_tol) ? DR_INFO_NOT_CONVERGED : 0;
+  }
+}
+
+__global__ void empty_group_kernel(const float* t2, int P, float* lam_eff, float* resid2, int32_t* iters, float* kkt,
+                                   int32_t* info) {
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= P) return;
+  if (lam_eff) lam_eff[p] = 0.f;
+  resid2[p] = t2[p];
+  if (iters) iters[p] = 0;
+  if (kkt) kkt[p] = 0.f;
+  info[p] = 0;
+}
+
+}  // namespace
+}  // namespace dr
+
+extern "C" size_t dr_span_workspace_size(int64_t n, int P) {
+  (void)n;
+  (void)P;
+  return 0;
+}
+
+extern "C" size_t dr_cone_workspace_size(int64_t n, int P) {
+  (void)n;
+  (void)P;
+  return 0;
+}
+
+extern "C" dr_status dr_project_span(const float* K, const float* s, const float* t2, int64_t n, int P, float lambda,
+                                     dr_ridge_mode mode, float* w, float* lam_eff, float* resid2, int32_t* info,
+                                     void* workspace, size_t ws_bytes, void* stream) {
+  using namespace dr;
+  (void)workspace;
+  (void)ws_bytes;
+  if (n < 0 || P < 0) return DR_ERR_ARG;
+  if (mode != DR_RIDGE_ABS && mode != DR_RIDGE_REL_TRACE) return DR_ERR_ARG;
+  if (!(lambda >= 0.f) || !(lambda <= 3.4e38f)) return DR_ERR_ARG;
+  if (P == 0) return DR_OK;
+  if (!t2 || !lam_eff || !resid2 || !info) return DR_ERR_ARG;
+  if (n > 0 && (!K || !s || !w)) return DR_ERR_ARG;
+  if (n > kSpanMaxN) return DR_ERR_UNSUPPORTED;
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  if (n == 0) {
+    hipLaunchKernelGGL(empty_group_kernel, dim3((P + 255) / 256), dim3(256), 0, hs, t2, P, lam_eff, resid2,
+                       (int32_t*)nullptr, (float*)nullptr, info);
+    return launch_status();
+  }
+  hipLaunchKernelGGL(span_small_kernel, dim3(P), dim3(kSpanThreads), 0, hs, K, s, t2, (int)n, lambda, (int)mode, w,
+                     lam_eff, resid2, info);
+  return launch_status();
+}
+
+extern "C" dr_status dr_project_cone(const float* K, const float* s, const float* t2, int64_t n, int P, int max_iter,
+                                     float kkt_tol, float* w, float* resid2, int32_t* iters, float* kkt, int32_t* info,
+                                     void* workspace, size_t ws_bytes, void* stream) {
+  using namespace dr;
+  (void)workspace;
+  (void)ws_bytes;
+  if (n < 0 || P < 0 || max_iter < 0 || !(kkt_tol == kkt_tol)) return DR_ERR_ARG;
+  if (P == 0) return DR_OK;
+  if (!t2 || !resid2 || !iters || !kkt || !info) return DR_ERR_ARG;
+  if (n > 0 && (!K || !s || !w)) return DR_ERR_ARG;
+  if (n > kConeMaxN) return DR_ERR_UNSUPPORTED;
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  if (n == 0) {
+    hipLaunchKernelGGL(empty_group_kernel, dim3((P + 255) / 256), dim3(256), 0, hs, t2, P, (float*)nullptr, resid2,
+                       iters, kkt, info);
+    return launch_status();
+  }
+  int npad = 1;
+  while (npad < n) npad <<= 1;
+  int tpr = kConeThreads / npad;
+  if (tpr > 64) tpr = 64;
+  const int cols = (npad + tpr - 1) / tpr;
+  if (cols <= 4)
+    hipLaunchKernelGGL(cone_pg_kernel<4>, dim3(P), dim3(kConeThreads), 0, hs, K, s, t2, (int)n, max_iter, kkt_tol, w,
+                       resid2, iters, kkt, info);
+  else if (cols <= 16)
+    hipLaunchKernelGGL(cone_pg_kernel<16>, dim3(P), dim3(kConeThreads), 0, hs, K, s, t2, (int)n, max_iter, kkt_tol, w,
+                       resid2, iters, kkt, info);
+  else
+    hipLaunchKernelGGL(cone_pg_kernel<0>, dim3(P), dim3(kConeThreads), 0, hs, K, s, t2, (int)n, max_iter, kkt_tol, w,
+                       resid2, iters, kkt, info);
+  return launch_status();
+}

@@ -1,0 +1,137 @@
+"""The C ABI library loads on a host without a GPU, exports every symbol the
+header declares, and rejects invalid arguments before any HIP call."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2605_07063_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dr_api.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2605_07063_amd import build
+        build.build()
+    return _lib.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w]+\*?\s+\*?(dr_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported_and_bound(lib):
+    names = declared_functions()
+    assert len(names) >= 12
+    for nm in names:
+        assert hasattr(lib, nm), nm
+        assert nm in _lib.SIGNATURES, f"{nm} missing from the Python binding"
+    assert set(_lib.SIGNATURES) == set(names)
+
+
+def test_version_and_status_strings(lib):
+    assert lib.dr_abi_version() == 1
+    for code in range(9):
+        assert lib.dr_status_string(code)
+    assert lib.dr_status_string(0) == b"ok"
+
+
+FAKE = 0x1000_0000   # 16-byte aligned, never dereferenced: validation fails first
+
+
+def layer(**kw):
+    d = dict(x=FAKE, ldx=256, dy=FAKE, lddy=256, p_in=FAKE, p_out=FAKE, d_in=256, d_out=256, k_in=16, k_out=16,
+             col_offset=0)
+    d.update(kw)
+    return _lib.DrLayer(**d)
+
+
+def sketch_call(lib, layers, N=4, T=8, dtype=_lib.DR_F32, S=FAKE, ldS=256, ws=None, wsb=0):
+    arr = (_lib.DrLayer * max(1, len(layers)))(*layers)
+    return lib.dr_sketch_grads(arr, len(layers), N, T, None, dtype, S, ldS, ws, wsb, None)
+
+
+def test_sketch_argument_errors(lib):
+    E = _lib
+    assert sketch_call(lib, []) == E.DR_ERR_ARG
+    assert sketch_call(lib, [layer(k_in=48)]) == E.DR_ERR_ARG
+    assert sketch_call(lib, [layer(k_out=8)]) == E.DR_ERR_ARG
+    assert sketch_call(lib, [layer()], dtype=7) == E.DR_ERR_DTYPE
+    assert sketch_call(lib, [layer(d_in=254, ldx=256)]) == E.DR_ERR_ARG        # not a multiple of 4
+    assert sketch_call(lib, [layer(ldx=128)]) == E.DR_ERR_ARG                   # ld < d
+    assert sketch_call(lib, [layer(x=FAKE + 4)]) == E.DR_ERR_ARG                # misaligned
+    assert sketch_call(lib, [layer(col_offset=250)]) == E.DR_ERR_ARG            # block beyond ldS
+    assert sketch_call(lib, [layer()], N=-1) == E.DR_ERR_ARG
+    assert sketch_call(lib, [layer()], S=None) == E.DR_ERR_ARG
+    assert sketch_call(lib, [layer(d_in=12, ldx=12)], dtype=E.DR_BF16) == E.DR_ERR_ARG   # bf16 needs multiples of 8
+    assert sketch_call(lib, [layer()], N=0) == E.DR_OK                          # nothing to do, no HIP call
+
+
+def test_sketch_workspace_query_and_check(lib):
+    layers = [layer(d_in=2048, d_out=2048, ldx=2048, lddy=2048, k_in=64, k_out=64, col_offset=4096 * i)
+              for i in range(8)]
+    arr = (_lib.DrLayer * 8)(*layers)
+    ws = lib.dr_sketch_workspace_size(arr, 8, 72, 512, _lib.DR_BF16)
+    assert ws > 0 and ws % 4 == 0
+    assert ws == lib.dr_sketch_workspace_size(arr, 8, 72, 512, _lib.DR_BF16)   # deterministic plan
+    st = lib.dr_sketch_grads(arr, 8, 72, 512, None, _lib.DR_BF16, FAKE, 32768, None, 0, None)
+    assert st == _lib.DR_ERR_WORKSPACE
+    st = lib.dr_sketch_grads(arr, 8, 72, 512, None, _lib.DR_BF16, FAKE, 32768, FAKE, ws - 1, None)
+    assert st == _lib.DR_ERR_WORKSPACE
+
+
+def goff(*v):
+    return (ctypes.c_int64 * len(v))(*v)
+
+
+def test_gram_argument_errors(lib):
+    E = _lib
+    g = goff(0, 64)
+    call = lambda **kw: lib.dr_gram(kw.get("G", FAKE), kw.get("n", 8), kw.get("ldG", 64), kw.get("Gt", FAKE),
+                                    kw.get("m", 2), kw.get("ldGt", 64), kw.get("dtype", E.DR_F32),
+                                    kw.get("goff", g), kw.get("P", 1), FAKE, FAKE, FAKE, kw.get("ws", FAKE),
+                                    kw.get("wsb", 1 << 30), None)
+    assert call(P=0) == E.DR_ERR_ARG
+    assert call(m=0) == E.DR_ERR_ARG
+    assert call(ldG=32) == E.DR_ERR_ARG
+    assert call(goff=goff(8, 4), P=1) == E.DR_ERR_ARG
+    assert call(goff=goff(0, 6), P=1) == E.DR_ERR_ARG          # group edge not a multiple of 4
+    assert call(dtype=3) == E.DR_ERR_DTYPE
+    assert call(ws=None) == E.DR_ERR_WORKSPACE
+    assert call(wsb=16) == E.DR_ERR_WORKSPACE
+    assert lib.dr_gram_workspace_size(64, 8, goff(0, 32768), 1, E.DR_F32) > 0
+
+
+def test_solver_and_select_argument_errors(lib):
+    E = _lib
+    span = lambda n=8, P=1, lam=0.0, mode=0: lib.dr_project_span(FAKE, FAKE, FAKE, n, P, lam, mode, FAKE, FAKE,
+                                                                 FAKE, FAKE, None, 0, None)
+    assert span(n=-1) == E.DR_ERR_ARG
+    assert span(lam=-1.0) == E.DR_ERR_ARG
+    assert span(lam=float("nan")) == E.DR_ERR_ARG
+    assert span(mode=5) == E.DR_ERR_ARG
+    assert span(n=257) == E.DR_ERR_UNSUPPORTED
+    assert span(P=0) == E.DR_OK
+    cone = lambda n=8, P=1, it=10, tol=0.0: lib.dr_project_cone(FAKE, FAKE, FAKE, n, P, it, tol, FAKE, FAKE, FAKE,
+                                                                FAKE, FAKE, None, 0, None)
+    assert cone(it=-1) == E.DR_ERR_ARG
+    assert cone(n=300) == E.DR_ERR_UNSUPPORTED
+    assert cone(tol=float("nan")) == E.DR_ERR_ARG
+    assert cone(P=0) == E.DR_OK
+    top = lambda n=8, P=1, k=2: lib.dr_select_topk(FAKE, n, P, k, FAKE, None, FAKE, None)
+    assert top(k=9) == E.DR_ERR_ARG
+    assert top(k=-1) == E.DR_ERR_ARG
+    assert top(P=0) == E.DR_OK
+    g = goff(0, 64)
+    assert lib.dr_combine(FAKE, 8, 64, 9, g, 1, FAKE, FAKE, None, 0, None) == E.DR_ERR_DTYPE
+    assert lib.dr_combine(FAKE, 8, 32, E.DR_F32, g, 1, FAKE, FAKE, None, 0, None) == E.DR_ERR_ARG
+    need = lib.dr_combine_workspace_size(8, g, 1)
+    assert need > 0
+    assert lib.dr_combine(FAKE, 8, 64, E.DR_F32, g, 1, FAKE, FAKE, None, 0, None) == E.DR_ERR_WORKSPACE

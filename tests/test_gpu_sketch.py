@@ -1,0 +1,139 @@
+"""GPU parity of dr_sketch_grads against the oracle's explicit gradients."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2605_07063_amd import api, workloads
+from gpu_helpers import TOL_SKETCH_BF16, TOL_SKETCH_F32, block_errors, host64, layers_to_host
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def run_case(layers, lens, N, T, tol, rows=None):
+    S = api.sketch(layers, lens)
+    torch.cuda.synchronize()
+    S_gpu = host64(S)
+    hl = layers_to_host(layers)
+    lens_h = None if lens is None else lens.cpu().numpy()
+    rows = list(range(N)) if rows is None else rows
+    S_ref = oracle.sketch_ref(hl, lens_h, rows=rows)
+    errs = block_errors(S_gpu, S_ref, layers, rows)
+    assert np.isfinite(errs).all(), "NaN / inf leaked or a zero block is non-zero"
+    assert errs.max() <= tol, f"max block error {errs.max():.3e} > {tol}"
+    return S, errs
+
+
+def custom_layers(specs, N, T, dtype, lens, nan_padding, seed=0):
+    """specs: list of (d_in, d_out, k_in, k_out)."""
+    g = torch.Generator(device=DEV)
+    g.manual_seed(1234 + seed)
+    out, off = [], 0
+    for (di, do, ki, ko) in specs:
+        x = torch.randn(N, T, di, generator=g, device=DEV).to(dtype)
+        dy = torch.randn(N, T, do, generator=g, device=DEV).to(dtype)
+        if nan_padding:
+            mask = torch.arange(T, device=DEV)[None, :] >= lens[:, None]
+            x[mask] = float("nan")
+            dy[mask] = float("nan")
+        p_in = (torch.randn(ki, di, generator=g, device=DEV) / ki ** 0.5).to(dtype)
+        p_out = (torch.randn(ko, do, generator=g, device=DEV) / ko ** 0.5).to(dtype)
+        out.append(dict(x=x, dy=dy, p_in=p_in, p_out=p_out, col_offset=off))
+        off += ki * ko
+    return out
+
+
+def test_tiny_config_fp32_all_rows():
+    cfg = workloads.CONFIGS["tiny"]
+    layers, lens, _ = workloads.sketch_inputs(cfg, DEV)
+    N = cfg["n"] + cfg["m"]
+    _, errs = run_case(layers, lens, N, cfg["T"], TOL_SKETCH_F32)
+    print(f"tiny fp32 max block rel err {errs.max():.2e}")
+
+
+@pytest.mark.parametrize("dtype,tol", [(torch.bfloat16, TOL_SKETCH_BF16), (torch.float32, TOL_SKETCH_F32)])
+def test_ragged_lengths_nan_padding_mixed_kappa_and_dim_tails(dtype, tol):
+    N, T = 11, 300                      # 3 token tiles, ragged tail; split-T reduction path
+    lens = torch.tensor([0, 1, 2, 127, 128, 129, 255, 256, 299, 300, 77], dtype=torch.int32, device=DEV)
+    specs = [(200, 136, 64, 64), (128, 264, 16, 32), (72, 64, 32, 16), (264, 40, 64, 16)]
+    layers = custom_layers(specs, N, T, dtype, lens, nan_padding=True)
+    _, errs = run_case(layers, lens, N, T, tol)
+    print(f"{dtype} ragged max block rel err {errs.max():.2e}")
+
+
+def test_single_chunk_path_and_many_layers():
+    # N * layers >= 2048 units with T <= 128: one chunk per example, no reduction kernel
+    N, T = 128, 100
+    lens = torch.randint(0, T + 1, (N,), dtype=torch.int32, device=DEV)
+    specs = [(64, 64, 16, 16)] * 18     # > 16 layers: two launches
+    layers = custom_layers(specs, N, T, torch.bfloat16, lens, nan_padding=True, seed=3)
+    run_case(layers, lens, N, T, TOL_SKETCH_BF16, rows=list(range(0, N, 9)))
+
+
+def test_null_lengths_means_full_and_determinism():
+    N, T = 5, 260
+    lens_full = torch.full((N,), T, dtype=torch.int32, device=DEV)
+    layers = custom_layers([(256, 128, 32, 32)], N, T, torch.bfloat16, lens_full, nan_padding=False, seed=5)
+    S1 = api.sketch(layers, None)
+    S2 = api.sketch(layers, lens_full)
+    S3 = api.sketch(layers, None)
+    torch.cuda.synchronize()
+    assert torch.equal(S1, S2)
+    assert torch.equal(S1, S3)
+    run_case(layers, None, N, T, TOL_SKETCH_BF16)
+
+
+def test_lengths_outside_range_are_clamped_and_T_zero():
+    N, T = 4, 64
+    lens = torch.tensor([-5, 0, 64, 1000], dtype=torch.int32, device=DEV)
+    layers = custom_layers([(64, 64, 16, 16)], N, T, torch.float32, lens.clamp(0, T), nan_padding=True, seed=7)
+    S = api.sketch(layers, lens)
+    torch.cuda.synchronize()
+    ref = oracle.sketch_ref(layers_to_host(layers), lens.clamp(0, T).cpu().numpy())
+    assert np.all(host64(S)[:2] == 0.0)
+    np.testing.assert_allclose(host64(S)[2:], ref[2:], rtol=1e-5, atol=1e-5 * np.abs(ref).max())
+    layers0 = custom_layers([(64, 64, 16, 16)], N, 0, torch.float32, torch.zeros(N, dtype=torch.int32, device=DEV),
+                            nan_padding=False)
+    S0 = torch.full((N, 256), 7.0, device=DEV)
+    api.dr_sketch_grads(layers0, N, 0, None, S0)
+    torch.cuda.synchronize()
+    assert torch.all(S0 == 0.0)
+
+
+def test_small_config_full_size_sampled():
+    """The benchmark workload (8 layers 2048x2048, 72 examples, T=512, ragged),
+    launched exactly as the benchmark launches it; oracle on sampled blocks."""
+    cfg = workloads.CONFIGS["small"]
+    layers, lens, _ = workloads.sketch_inputs(cfg, DEV, nan_padding=True)
+    N = cfg["n"] + cfg["m"]
+    S = api.sketch(layers, lens)
+    torch.cuda.synchronize()
+    S_gpu = host64(S)
+    rows = [0, 17, 63, 64, 71]
+    sub = [layers[0], layers[5]]
+    ref = oracle.sketch_ref(layers_to_host(sub, rows), lens.cpu().numpy()[rows])
+    errs = block_errors(S_gpu[rows], ref, sub, range(len(rows)))
+    assert errs.max() <= TOL_SKETCH_BF16, errs.max()
+    assert np.isfinite(S_gpu).all()
+    print(f"small full-size sampled max block rel err {errs.max():.2e}")
+
+
+def test_long_context_full_size_sampled():
+    """16 layers 4096x4096 at T=4096 (heavy-tailed, 30 % padded): two layers
+    run, sampled examples checked against the explicit-gradient oracle."""
+    cfg = workloads.CONFIGS["long"]
+    layers, lens, _ = workloads.sketch_inputs(cfg, DEV, layers=[0, 15], nan_padding=True)
+    N = cfg["n"] + cfg["m"]
+    S = api.sketch(layers, lens)
+    torch.cuda.synchronize()
+    S_gpu = host64(S)
+    lh = lens.cpu().numpy()
+    padded = [int(i) for i in np.flatnonzero(lh < cfg["T"])][:1]
+    rows = sorted(set([0] + padded))
+    ref = oracle.sketch_ref(layers_to_host(layers, rows), lh[rows])
+    errs = block_errors(S_gpu[rows], ref, layers, range(len(rows)))
+    assert errs.max() <= TOL_SKETCH_BF16, errs.max()
+    assert np.isfinite(S_gpu).all()
+    print(f"long full-size sampled max block rel err {errs.max():.2e}")
