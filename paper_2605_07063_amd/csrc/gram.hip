@@ -13,9 +13,12 @@
 //                        Operands stream from memory straight into registers.
 //   gram_reduce_kernel : sums the chunk partials of a tile in chunk order and
 //                        writes the lower triangle and its mirror, so K is
-//                        exactly symmetric.
-//   score_kernel       : s_p[i] = <G_p[i], gbar_p> and t2_p (row n := gbar),
-//                        fp64 accumulation, fixed-order block reduction.
+//                        exactly symmetric.  For fp32 sketches the target
+//                        mean joins the tiles as row n, so the same pass
+//                        yields s_p (row n) and t2_p (element (n, n)).
+//   score_kernel       : bf16 sketches only: s_p[i] = <G_p[i], gbar_p> and
+//                        t2_p against the fp32 mean, fp64 accumulation,
+//                        fixed-order block reduction.
 // No atomics: results are deterministic.
 
 #include "common.h"
@@ -32,6 +35,8 @@ struct GramArgs {
   const unsigned char* G;
   long long ldG;
   int n;
+  int rows;                         // rows of the Gram problem: n, or n + 1 with gbar as row n
+  const float* gbar;                // [cols] by absolute column (row n when rows == n + 1)
   long long goff[kMaxGroups + 1];   // absolute column offsets of this launch's groups
   int P;
   int NT, pairs, CK, maxchunks;
@@ -89,12 +94,19 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_kernel(GramArgs a) {
 
   int rowA[2], rowB[2];
   bool okA[2], okB[2];
+  const unsigned char* baseA[2];
+  const unsigned char* baseB[2];
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
     rowA[b] = I * kTile + wr * 32 + b * 16 + lr;
     rowB[b] = J * kTile + wc * 32 + b * 16 + lr;
-    okA[b] = rowA[b] < a.n;
-    okB[b] = rowB[b] < a.n;
+    okA[b] = rowA[b] < a.rows;
+    okB[b] = rowB[b] < a.rows;
+    // row n of the augmented problem is the fp32 target mean (fp32 path only)
+    baseA[b] = rowA[b] < a.n ? a.G + (long long)rowA[b] * a.ldG * E::ES
+                             : reinterpret_cast<const unsigned char*>(a.gbar);
+    baseB[b] = rowB[b] < a.n ? a.G + (long long)rowB[b] * a.ldG * E::ES
+                             : reinterpret_cast<const unsigned char*>(a.gbar);
   }
 
   f32x4 acc[2][2];
@@ -110,12 +122,10 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_kernel(GramArgs a) {
       const bool cok = c < c1;
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
-        va[b][v] = (okA[b] && cok)
-                       ? *reinterpret_cast<const u32x4*>(a.G + ((long long)rowA[b] * a.ldG + c) * E::ES)
-                       : u32x4{0u, 0u, 0u, 0u};
-        vb[b][v] = (okB[b] && cok)
-                       ? *reinterpret_cast<const u32x4*>(a.G + ((long long)rowB[b] * a.ldG + c) * E::ES)
-                       : u32x4{0u, 0u, 0u, 0u};
+        va[b][v] = (okA[b] && cok) ? *reinterpret_cast<const u32x4*>(baseA[b] + c * E::ES)
+                                   : u32x4{0u, 0u, 0u, 0u};
+        vb[b][v] = (okB[b] && cok) ? *reinterpret_cast<const u32x4*>(baseB[b] + c * E::ES)
+                                   : u32x4{0u, 0u, 0u, 0u};
       }
     }
   };
@@ -152,21 +162,38 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_kernel(GramArgs a) {
         out[(wr * 32 + i * 16 + lg * 4 + r) * kTile + wc * 32 + j * 16 + lr] = acc[i][j][r];
 }
 
-__global__ __launch_bounds__(kThreads) void gram_reduce_kernel(GramArgs a, float* K, long long pbase) {
+// One thread per element of a 64x64 tile: sums the chunk partials in chunk
+// order and writes K (lower triangle and its mirror) and, for the augmented
+// fp32 problem, s (row n) and t2 (element (n, n)).
+__global__ __launch_bounds__(kThreads) void gram_reduce_kernel(GramArgs a, float* K, float* s, float* t2,
+                                                               long long pbase) {
   const int q = blockIdx.x, p = blockIdx.y;
+  const int e = blockIdx.z * kThreads + threadIdx.x;
   const long long width = a.goff[p + 1] - a.goff[p];
   const int nvalid = (int)((width + a.CK - 1) / a.CK);
   int I, J;
   pair_to_tiles(q, I, J);
-  const float* src = a.partial + ((long long)p * a.pairs + q) * a.maxchunks * (kTile * kTile);
-  float* Kp = K + (pbase + p) * (long long)a.n * a.n;
-  for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
-    const int r = I * kTile + e / kTile, c = J * kTile + e % kTile;
-    if (r >= a.n || c >= a.n || c > r) continue;
-    float acc = 0.f;
-    for (int ch = 0; ch < nvalid; ++ch) acc += src[(long long)ch * (kTile * kTile) + e];
+  const int r = I * kTile + e / kTile, c = J * kTile + e % kTile;
+  if (r >= a.rows || c > r) return;
+  const float* src = a.partial + ((long long)p * a.pairs + q) * a.maxchunks * (kTile * kTile) + e;
+  float acc = 0.f;
+  int ch = 0;
+  for (; ch + 8 <= nvalid; ch += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = src[(long long)(ch + u) * (kTile * kTile)];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc += v[u];
+  }
+  for (; ch < nvalid; ++ch) acc += src[(long long)ch * (kTile * kTile)];
+  if (r < a.n) {
+    float* Kp = K + (pbase + p) * (long long)a.n * a.n;
     Kp[(long long)r * a.n + c] = acc;
     Kp[(long long)c * a.n + r] = acc;
+  } else if (c < a.n) {
+    s[(pbase + p) * (long long)a.n + c] = acc;
+  } else {
+    t2[pbase + p] = acc;
   }
 }
 
@@ -226,15 +253,18 @@ __global__ __launch_bounds__(kThreads) void score_kernel(GramArgs a, const float
 }
 
 struct GramPlan {
+  int64_t rows;
   int NT, pairs, CK, maxchunks;
   size_t gbar_bytes, partial_bytes;
 };
 
 // Chunk length: a multiple of 256 columns, shrunk until a launch has about
 // kTargetWGs workgroups; identical for every launch of a call.
-GramPlan gram_plan(int64_t n, const int64_t* goff, int P) {
+GramPlan gram_plan(int64_t n, const int64_t* goff, int P, dr_dtype dtype) {
   GramPlan g;
-  g.NT = (int)((n + kTile - 1) / kTile);
+  // fp32 sketches: gbar joins as row n, so s and t2 come out of the same pass
+  const int64_t rows = dtype == DR_F32 ? n + 1 : n;
+  g.NT = (int)((rows + kTile - 1) / kTile);
   g.pairs = g.NT * (g.NT + 1) / 2;
   int64_t maxw = 0;
   for (int p = 0; p < P; ++p) maxw = goff[p + 1] - goff[p] > maxw ? goff[p + 1] - goff[p] : maxw;
@@ -246,7 +276,8 @@ GramPlan gram_plan(int64_t n, const int64_t* goff, int P) {
   if (g.maxchunks < 1) g.maxchunks = 1;
   g.gbar_bytes = align_up((size_t)(goff[P] > 0 ? goff[P] : 1) * sizeof(float), 256);
   g.partial_bytes = (size_t)gp * g.pairs * g.maxchunks * kTile * kTile * sizeof(float);
-  if (n == 0) g.partial_bytes = 0;
+  if (rows == 0) g.partial_bytes = 0;
+  g.rows = rows;
   return g;
 }
 
@@ -272,9 +303,9 @@ dr_status gram_validate(const void* G, int64_t n, int64_t ldG, const void* Gt, i
 
 extern "C" size_t dr_gram_workspace_size(int64_t n, int64_t m, const int64_t* goff, int P, dr_dtype dtype) {
   (void)m;
-  (void)dtype;
+  if (dtype != DR_BF16 && dtype != DR_F32) return 0;
   if (!goff || P < 1 || n < 0) return 0;
-  dr::GramPlan g = dr::gram_plan(n, goff, P);
+  dr::GramPlan g = dr::gram_plan(n, goff, P, dtype);
   return g.gbar_bytes + g.partial_bytes;
 }
 
@@ -284,7 +315,7 @@ extern "C" dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* 
   using namespace dr;
   dr_status st = gram_validate(G, n, ldG, Gt, m, ldGt, dtype, goff, P, K, s, t2);
   if (st != DR_OK) return st;
-  GramPlan g = gram_plan(n, goff, P);
+  GramPlan g = gram_plan(n, goff, P, dtype);
   if (!workspace || ws_bytes < g.gbar_bytes + g.partial_bytes) return DR_ERR_WORKSPACE;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   const bool bf = dtype == DR_BF16;
@@ -309,6 +340,8 @@ extern "C" dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* 
     a.G = static_cast<const unsigned char*>(G);
     a.ldG = ldG;
     a.n = (int)n;
+    a.rows = (int)g.rows;
+    a.gbar = gbar;
     for (int p = 0; p <= gp; ++p) a.goff[p] = goff[p0 + p];
     a.P = gp;
     a.NT = g.NT;
@@ -316,21 +349,22 @@ extern "C" dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* 
     a.CK = g.CK;
     a.maxchunks = g.maxchunks;
     a.partial = partial;
-    if (n > 0) {
+    if (g.rows > 0) {
       dim3 grid(g.maxchunks, g.pairs, gp);
       if (bf)
         hipLaunchKernelGGL(gram_tile_kernel<true>, grid, dim3(kThreads), 0, hs, a);
       else
         hipLaunchKernelGGL(gram_tile_kernel<false>, grid, dim3(kThreads), 0, hs, a);
       if ((st = launch_status()) != DR_OK) return st;
-      hipLaunchKernelGGL(gram_reduce_kernel, dim3(g.pairs, gp), dim3(kThreads), 0, hs, a, K, (long long)p0);
+      hipLaunchKernelGGL(gram_reduce_kernel, dim3(g.pairs, gp, kTile * kTile / kThreads), dim3(kThreads), 0, hs, a,
+                         K, s, t2, (long long)p0);
       if ((st = launch_status()) != DR_OK) return st;
     }
-    if (bf)
+    if (bf) {
+      // bf16 sketches: s and t2 against the fp32 target mean in a separate pass
       hipLaunchKernelGGL(score_kernel<true>, dim3(n + 1, gp), dim3(kThreads), 0, hs, a, gbar, s, t2, (long long)p0);
-    else
-      hipLaunchKernelGGL(score_kernel<false>, dim3(n + 1, gp), dim3(kThreads), 0, hs, a, gbar, s, t2, (long long)p0);
-    if ((st = launch_status()) != DR_OK) return st;
+      if ((st = launch_status()) != DR_OK) return st;
+    }
   }
   return DR_OK;
 }

@@ -12,16 +12,19 @@
 // fp32-MFMA operand layout once token 4*(l/16)+j is read as the reduction
 // index l/16 of the j-th product.
 //
-// Work decomposition: a work unit is (layer, example, chunk of tokens); a
-// 256-thread workgroup owns one unit and walks it in 128-token tiles, each
-// of its four waves owning 32 tokens of the tile.  The x / dy rows stream
-// from HBM straight into registers (each element is used by one wave only);
-// the projector chunk shared by the four waves is staged once per step in
-// LDS (double buffered, one barrier per step).  Rows at or beyond the valid
-// length are never loaded (zero-filled), so padding may hold any bits.
-// The four per-wave partial sketches are summed through LDS in a fixed
-// order; with more than one chunk per example a second kernel sums the
-// chunk partials in chunk order.  No atomics: results are deterministic.
+// Two kernels do the work.  sketch_packed_kernel (below) is the main path:
+// the valid tokens are packed into full 128-token tiles and streamed
+// HBM -> LDS by DMA through a three-stage ring.  sketch_kernel, the general
+// fallback (d not a whole number of 64-element steps, or offsets beyond
+// 32 bits), works on (layer, example, chunk of tokens) units: a 256-thread
+// workgroup owns one unit and walks it in 128-token tiles, each of its four
+// waves owning 32 tokens; x / dy rows stream from HBM straight into
+// registers, the projector chunk shared by the four waves is staged in LDS
+// (double buffered, one barrier per step), rows at or beyond the valid
+// length are never loaded.  In both, the four per-wave partial sketches
+// are summed through LDS in a fixed order and multi-part results are summed
+// by a second kernel in a fixed order.  No atomics: results are
+// deterministic, and padding may hold any bits.
 
 #include "common.h"
 
@@ -318,39 +321,534 @@ __global__ __launch_bounds__(kThreads, 2) void sketch_kernel(SketchArgs a) {
       for (int q = 0; q < 4; ++q) out[(o * 16 + lg * 4 + q) * KIN + i * 16 + lr] = Sacc[o][i][q];
 }
 
-// Sum the chunk partials of every (layer, example) in chunk order.
+
+// ---------------------------------------------------------------------------
+// Packed-token streaming kernel (the main path).
+//
+// The valid tokens of every layer are taken in example order, as if the
+// padded batch were packed: position p = cum[i] + t is token t < len_i of
+// example i.  A workgroup owns one 128-token tile of packed positions of one
+// layer, so every tile is full (up to the last one of the layer) whatever
+// the length mix, and padding is never addressed.  A tile may hold the end
+// of one example and the start of the next: stage 2 then runs once per
+// example of the tile with the other examples' rows masked out of Y.  An
+// example that lies inside one tile is written to S directly; an example
+// spread over several tiles leaves one partial per tile (slot 0 if it is
+// the tile's first example, else slot 1) that sketch_packed_reduce_kernel
+// sums in tile order.
+//
+// Data movement: x / dy rows and projector chunks go HBM -> LDS with the
+// buffer-to-LDS DMA (16 bytes per lane, no registers held while in flight)
+// through a three-stage ring, so two steps of loads are outstanding while
+// the current step computes.  Waits are explicit (vmcnt counts this wave's
+// outstanding DMAs); the barrier is a bare s_barrier after lgkmcnt(0), so no
+// fence drains the ring.
+//
+// LDS layout of a stage: every 16-row operand block (16 token rows of x or
+// dy, or 16 projector rows) occupies 2 KiB as two halves of 8 rows x 128 B.
+// One DMA instruction fills one half: lane l moves 16 bytes of row l/8, so
+// each instruction reads eight whole 128-byte row segments from HBM.  The
+// 16-byte slot of segment g of row r (r = 0..15 within the block) is
+// g ^ (r % 8) ^ (r / 8); with that swizzle the MFMA operand reads
+// (ds_read_b128, lane = row % 16 + 16 * reduction slice) hit all 64 banks
+// exactly once per 16-lane phase.  x / dy DMAs are marked non-temporal: each
+// element is read once.
+
+#define DR_WAIT_VM(n) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory")
+#define DR_LDS_SYNC() asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory")
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+constexpr unsigned kOobOffset = 0xFFFFFFF0u;   // outside every descriptor: reads as zeros
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// aux: cache policy of the load (2 = non-temporal on gfx950)
+template <int AUX>
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, unsigned char* lds_block, unsigned voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds_block, 16, voff, 0, 0, AUX);
+}
+constexpr int kAuxStream = 2;
+
+// 16 bytes of a swizzled 16-row block: row lr, 16-byte segment seg
+__device__ __forceinline__ u32x4 swz_read(const unsigned char* blk, int lr, int seg) {
+  return *reinterpret_cast<const u32x4*>(blk + (lr >> 3) * 1024 + (lr & 7) * 128 + ((seg ^ (lr & 7) ^ (lr >> 3)) * 16));
+}
+
+struct PackArgs {
+  LayerArg L[kMaxLayersPerLaunch];
+  int num_layers;
+  int N, T;
+  int max_tiles;        // tiles per layer for N * T packed positions
+  const int* cum;       // [N + 1] exclusive prefix of the clamped lengths
+  const int* tile_ex;   // [max_tiles] example holding the first position of each tile
+  float* S;
+  long long ldS;
+  float* partial;       // [num_layers][max_tiles][2][KOUT * KIN]
+};
+
+// Exclusive prefix of the clamped lengths and the first example of each
+// tile (one workgroup; N is small next to the streamed data).
+__global__ __launch_bounds__(1024) void sketch_plan_kernel(const int* len, int N, int T, int max_tiles, int* cum,
+                                                           int* tile_ex) {
+  __shared__ int wsum[17];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int per = (N + 1023) / 1024;
+  const int i0 = tid * per, i1 = i0 + per < N ? i0 + per : N;
+  int loc = 0;
+  for (int i = i0; i < i1; ++i) {
+    int l = len ? len[i] : T;
+    loc += l < 0 ? 0 : (l > T ? T : l);
+  }
+  int inc = loc;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int v = __shfl_up(inc, off, 64);
+    if (lane >= off) inc += v;
+  }
+  if (lane == 63) wsum[wave] = inc;
+  __syncthreads();
+  if (tid == 0) {
+    int run = 0;
+    for (int w = 0; w < 16; ++w) {
+      const int v = wsum[w];
+      wsum[w] = run;
+      run += v;
+    }
+    wsum[16] = run;
+  }
+  __syncthreads();
+  int base = wsum[wave] + inc - loc;
+  for (int i = i0; i < i1; ++i) {
+    cum[i] = base;
+    int l = len ? len[i] : T;
+    base += l < 0 ? 0 : (l > T ? T : l);
+  }
+  if (tid == 0) cum[N] = wsum[16];
+  __syncthreads();
+  for (int tt = tid; tt < max_tiles; tt += 1024) {
+    const int p = tt * kTokTile;
+    int lo = 0, hi = N;   // last e with cum[e] <= p
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (cum[mid] <= p)
+        lo = mid;
+      else
+        hi = mid - 1;
+    }
+    tile_ex[tt] = lo;
+  }
+}
+
+template <bool BF16, int KIN, int KOUT>
+__global__ __launch_bounds__(kThreads, 2) void sketch_packed_kernel(PackArgs a) {
+  using E = Tr<BF16>;
+  constexpr int NSUB = 2;                   // MFMA operand vectors per row per step
+  constexpr int KC = NSUB * E::KSUB;        // 64 bf16 / 32 fp32 elements per step
+  constexpr int KP = KIN > KOUT ? KIN : KOUT;
+  constexpr int TI = KIN / 16, TO = KOUT / 16, TPM = KP / 16;
+  constexpr int XBLK = kWaves * 2 * NSUB;   // 16 x blocks of 1 KiB
+  constexpr int PBLK = 2 * TPM > 4 ? 2 * TPM : 4;
+  constexpr int NPW = PBLK / kWaves;        // projector DMAs per wave per stage
+  constexpr int NDMA = 2 * NSUB + NPW;      // DMAs per wave per stage
+  constexpr int STAGE = (XBLK + PBLK) * 1024;
+  constexpr int NST = 3;
+  constexpr int LDS_R = 2 * KOUT * KIN * 4;
+  constexpr int LDS_BYTES = NST * STAGE > LDS_R ? NST * STAGE : LDS_R;
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[LDS_BYTES];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4, hr = lane >> 3;
+  const int li = blockIdx.x / a.max_tiles;
+  const int tile = blockIdx.x - li * a.max_tiles;
+  const int total = a.cum[a.N];
+  const int p0 = tile * kTokTile;
+  if (p0 >= total) return;
+  const LayerArg& L = a.L[li];
+  const int e0 = a.tile_ex[tile];
+  const int* cum = a.cum;
+
+  // example (relative to e0) and token of a packed position, -1 past the end
+  auto locate = [&](int p, int& rel, int& tok) {
+    if (p >= total) {
+      rel = -1;
+      tok = 0;
+      return;
+    }
+    int e = e0;
+    while (cum[e + 1] <= p) ++e;
+    rel = e - e0;
+    tok = p - cum[e];
+  };
+  // byte offsets of this lane's DMA rows (rb, half) from the tile's base example
+  unsigned offx[2][2], offd[2][2];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      int rel, tok;
+      locate(p0 + wave * kTokWave + rb * 16 + h * 8 + hr, rel, tok);
+      const long long row = (long long)rel * a.T + tok;
+      offx[rb][h] = rel < 0 ? kOobOffset : (unsigned)(row * L.ldx * E::ES);
+      offd[rb][h] = rel < 0 ? kOobOffset : (unsigned)(row * L.lddy * E::ES);
+    }
+  int e_last;
+  {
+    int rel, tok;
+    locate((p0 + kTokTile < total ? p0 + kTokTile : total) - 1, rel, tok);
+    e_last = e0 + rel;
+  }
+
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(L.x + (long long)e0 * a.T * L.ldx * E::ES, kOobOffset);
+  const __amdgpu_buffer_rsrc_t rd = make_rsrc(L.dy + (long long)e0 * a.T * L.lddy * E::ES, kOobOffset);
+  const __amdgpu_buffer_rsrc_t rpi = make_rsrc(L.p_in, (unsigned)(KIN * L.d_in * E::ES));
+  const __amdgpu_buffer_rsrc_t rpo = make_rsrc(L.p_out, (unsigned)(KOUT * L.d_out * E::ES));
+  const int nsx = L.d_in / KC, nsd = L.d_out / KC;
+  const int nsteps = nsx + nsd;
+  const unsigned seg = (unsigned)((lane & 7) ^ hr);
+
+  // issue every DMA of step s into ring stage st
+  auto issue = [&](int s, int st) {
+    const int pass = s < nsx ? 0 : 1;
+    const unsigned k0 = (unsigned)((pass == 0 ? s : s - nsx) * KC);
+    unsigned char* sb = lds + st * STAGE;
+    const __amdgpu_buffer_rsrc_t rr = pass == 0 ? rx : rd;
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const unsigned ro = pass == 0 ? offx[rb][h] : offd[rb][h];
+        const unsigned off = ro == kOobOffset ? kOobOffset : ro + (k0 + (seg ^ (unsigned)h) * E::EPV) * E::ES;
+        dma16<kAuxStream>(rr, sb + ((wave * 2 + rb) * 2 + h) * 1024, off);
+      }
+    const __amdgpu_buffer_rsrc_t rp = pass == 0 ? rpi : rpo;
+    const unsigned dp = (unsigned)(pass == 0 ? L.d_in : L.d_out);
+#pragma unroll
+    for (int j = 0; j < NPW; ++j) {
+      const int b = wave + j * kWaves;          // projector half block (column tile, half)
+      const int ct = b >> 1, h = b & 1;
+      const unsigned row = (unsigned)(ct * 16 + h * 8 + hr);
+      // blocks past the projector's tiles and rows past k_in / k_out fall
+      // outside the descriptor's range and fill with zeros
+      const unsigned off = ct < TPM ? (row * dp + k0 + (seg ^ (unsigned)h) * E::EPV) * E::ES : kOobOffset;
+      dma16<0>(rp, sb + (XBLK + b) * 1024, off);
+    }
+  };
+
+  f32x4 Y[2][TI], D[2][TO];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb) {
+#pragma unroll
+    for (int c = 0; c < TI; ++c) Y[rb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < TO; ++c) D[rb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  issue(0, 0);
+  if (nsteps > 1) issue(1, 1);
+  int st = 0;
+  for (int s = 0; s < nsteps; ++s) {
+    if (s + 1 < nsteps)
+      DR_WAIT_VM(NDMA);
+    else
+      DR_WAIT_VM(0);
+    DR_LDS_SYNC();
+    if (s + 2 < nsteps) issue(s + 2, st == 0 ? 2 : st - 1);
+    const unsigned char* sb = lds + st * STAGE;
+    // operand (row lr, reduction slice lg of sub-step sub) = segment sub*4 + lg
+    u32x4 xf[2][NSUB];
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int sub = 0; sub < NSUB; ++sub) xf[rb][sub] = swz_read(sb + (wave * 2 + rb) * 2048, lr, sub * 4 + lg);
+    if (s < nsx) {
+#pragma unroll
+      for (int sub = 0; sub < NSUB; ++sub)
+#pragma unroll
+        for (int c = 0; c < TI; ++c) {
+          const u32x4 b = swz_read(sb + (XBLK + 2 * c) * 1024, lr, sub * 4 + lg);
+#pragma unroll
+          for (int rb = 0; rb < 2; ++rb) Y[rb][c] = mma_vec<BF16>(xf[rb][sub], b, Y[rb][c]);
+        }
+    } else {
+#pragma unroll
+      for (int sub = 0; sub < NSUB; ++sub)
+#pragma unroll
+        for (int c = 0; c < TO; ++c) {
+          const u32x4 b = swz_read(sb + (XBLK + 2 * c) * 1024, lr, sub * 4 + lg);
+#pragma unroll
+          for (int rb = 0; rb < 2; ++rb) D[rb][c] = mma_vec<BF16>(xf[rb][sub], b, D[rb][c]);
+        }
+    }
+    st = st == 2 ? 0 : st + 1;
+  }
+  DR_LDS_SYNC();
+
+  // stage 2 once per example of the tile, the other examples' rows masked
+  float* red = reinterpret_cast<float*>(lds);
+  constexpr int SW = KOUT * KIN;
+  // packed position of the first row this lane holds in the MFMA outputs
+  // (rows rbase + rb*16 + j, j < 4)
+  const int rbase = p0 + wave * kTokWave + lg * 4;
+  for (int e = e0; e <= e_last; ++e) {
+    const int ce = cum[e], ce1 = cum[e + 1];
+    if (ce1 == ce) continue;   // empty examples are written by the reduction kernel
+    f32x4 Sacc[TO][TI];
+#pragma unroll
+    for (int o = 0; o < TO; ++o)
+#pragma unroll
+      for (int i = 0; i < TI; ++i) Sacc[o][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int wlo = p0 + wave * kTokWave, whi = wlo + kTokWave;   // this wave's rows
+    if (ce <= wlo && ce1 >= whi) {
+      // every row of the wave belongs to e
+#pragma unroll
+      for (int o = 0; o < TO; ++o)
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+          for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) Sacc[o][i] = mma_f32(D[rb][o][j], Y[rb][i][j], Sacc[o][i]);
+    } else if (ce < whi && ce1 > wlo) {
+      // rows of other examples are masked out of Y
+#pragma unroll
+      for (int o = 0; o < TO; ++o)
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+          for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int pr = rbase + rb * 16 + j;
+              Sacc[o][i] = mma_f32(D[rb][o][j], (pr >= ce && pr < ce1) ? Y[rb][i][j] : 0.f, Sacc[o][i]);
+            }
+    }
+    // (w0 + w2) + (w1 + w3) through LDS, in a fixed order
+    auto put = [&](int region) {
+#pragma unroll
+      for (int o = 0; o < TO; ++o)
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) red[region * SW + ((o * TI + i) * 4 + q) * 64 + lane] = Sacc[o][i][q];
+    };
+    auto add = [&](int region) {
+#pragma unroll
+      for (int o = 0; o < TO; ++o)
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) Sacc[o][i][q] += red[region * SW + ((o * TI + i) * 4 + q) * 64 + lane];
+    };
+    if (wave >= 2) put(wave - 2);
+    DR_LDS_SYNC();
+    if (wave < 2) add(wave);
+    DR_LDS_SYNC();
+    if (wave == 1) put(0);
+    DR_LDS_SYNC();
+    if (wave == 0) {
+      add(0);
+      const bool inside = ce >= p0 && ce1 <= p0 + kTokTile;
+      float* out = inside ? a.S + (long long)e * a.ldS + L.col_offset
+                          : a.partial + (((long long)li * a.max_tiles + tile) * 2 + (e == e0 ? 0 : 1)) * SW;
+#pragma unroll
+      for (int o = 0; o < TO; ++o)
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) out[(o * 16 + lg * 4 + q) * KIN + i * 16 + lr] = Sacc[o][i][q];
+    }
+    DR_LDS_SYNC();
+  }
+}
+
+// Examples spread over several tiles: sum their per-tile partials in tile
+// order; empty examples get zeros.  Four workgroups per (layer, example),
+// one float4 of the sketch block per thread.
+constexpr int kReduceSplit = 4;
+
+template <int KIN, int KOUT>
+__global__ __launch_bounds__(kThreads) void sketch_packed_reduce_kernel(PackArgs a) {
+  constexpr int V4 = KOUT * KIN / 4;
+  constexpr int PER = (V4 + kReduceSplit * kThreads - 1) / (kReduceSplit * kThreads);
+  const int part = blockIdx.x % kReduceSplit;
+  const int pair = blockIdx.x / kReduceSplit;
+  const int li = pair / a.N, e = pair % a.N;
+  const int ce = a.cum[e], ce1 = a.cum[e + 1];
+  const int t0 = ce / kTokTile, t1 = (ce1 - 1) / kTokTile;
+  if (ce1 > ce && t0 == t1) return;   // written by its only tile
+  float* out = a.S + (long long)e * a.ldS + a.L[li].col_offset;
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e4 = (part * PER + u) * kThreads + threadIdx.x;
+    if (e4 >= V4) break;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (ce1 > ce) {
+      for (int tt = t0; tt <= t1; ++tt) {
+        const int slot = a.tile_ex[tt] == e ? 0 : 1;
+        acc += reinterpret_cast<const f32x4*>(a.partial + (((long long)li * a.max_tiles + tt) * 2 + slot) *
+                                                              (KOUT * KIN))[e4];
+      }
+    }
+    out[4 * e4 + 0] = acc[0];
+    out[4 * e4 + 1] = acc[1];
+    out[4 * e4 + 2] = acc[2];
+    out[4 * e4 + 3] = acc[3];
+  }
+}
+
+// Sum the chunk partials of every (layer, example) in chunk order (register
+// kernel path): four workgroups per (layer, example), one float4 per thread.
 template <int KIN, int KOUT>
 __global__ __launch_bounds__(kThreads) void sketch_reduce_kernel(SketchArgs a) {
-  const int li = blockIdx.x / a.N;
-  const int ex = blockIdx.x % a.N;
+  constexpr int V4 = KOUT * KIN / 4;
+  constexpr int PER = (V4 + kReduceSplit * kThreads - 1) / (kReduceSplit * kThreads);
+  const int part = blockIdx.x % kReduceSplit;
+  const int pair = blockIdx.x / kReduceSplit;
+  const int li = pair / a.N, ex = pair % a.N;
   int len = a.T;
   if (a.len) {
     len = a.len[ex];
     len = len < 0 ? 0 : (len > a.T ? a.T : len);
   }
   const int nvalid = (len + a.chunk_tokens - 1) / a.chunk_tokens;
-  const float* p = a.partial + (long long)(li * a.N + ex) * a.nchunks * (KOUT * KIN);
+  const f32x4* p = reinterpret_cast<const f32x4*>(a.partial + (long long)(li * a.N + ex) * a.nchunks * (KOUT * KIN));
   float* out = a.S + (long long)ex * a.ldS + a.L[li].col_offset;
-  for (int e = threadIdx.x; e < KOUT * KIN; e += kThreads) {
-    float acc = 0.f;
-    for (int c = 0; c < nvalid; ++c) acc += p[(long long)c * (KOUT * KIN) + e];
-    out[e] = acc;
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e4 = (part * PER + u) * kThreads + threadIdx.x;
+    if (e4 >= V4) break;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    int c = 0;
+    for (; c + 4 <= nvalid; c += 4) {
+      f32x4 v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = p[(long long)(c + q) * V4 + e4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc += v[q];
+    }
+    for (; c < nvalid; ++c) acc += p[(long long)c * V4 + e4];
+    out[4 * e4 + 0] = acc[0];
+    out[4 * e4 + 1] = acc[1];
+    out[4 * e4 + 2] = acc[2];
+    out[4 * e4 + 3] = acc[3];
   }
 }
 
+// ---------------------------------------------------------------------------
+// Host side: planning and dispatch.
+
+bool valid_k(int64_t k) { return k == 16 || k == 32 || k == 64; }
+
+// Layers are grouped into launches of at most kMaxLayersPerLaunch
+// consecutive layers with equal (k_in, k_out).  A launch takes the packed
+// path when d_in and d_out are whole numbers of steps and every byte offset
+// a tile can form (at most min(N, 128) examples from its first one) fits in
+// 32 bits; otherwise the register kernel runs over (layer, example, chunk)
+// units whose chunk length is halved (in whole tiles) until the launch has
+// at least kTargetUnits units.
+struct Launch {
+  int first, count, kin, kout, chunk, nchunks;
+  bool packed;
+};
+
+struct Plan {
+  int nlaunch;
+  int max_tiles;
+  size_t off_cum, off_tiles, off_partial, bytes;
+};
+
+int64_t packed_tiles(int64_t N, int64_t T) { return (N * T + kTokTile - 1) / kTokTile; }
+
+bool packed_ok(const dr_layer* layers, int first, int count, int64_t N, int64_t T, dr_dtype dtype) {
+  const int64_t kc = dtype == DR_BF16 ? 64 : 32;
+  const int64_t es = dtype == DR_BF16 ? 2 : 4;
+  const int64_t span = (N < kTokTile ? N : kTokTile) * T + kTokTile;
+  for (int j = first; j < first + count; ++j) {
+    const dr_layer& L = layers[j];
+    if (L.d_in % kc || L.d_out % kc) return false;
+    const int64_t ld = L.ldx > L.lddy ? L.ldx : L.lddy;
+    if ((uint64_t)span * (uint64_t)ld * (uint64_t)es >= (uint64_t)kOobOffset) return false;
+  }
+  return true;
+}
+
+Plan plan(const dr_layer* layers, int num_layers, int64_t N, int64_t T, dr_dtype dtype, Launch* out) {
+  Plan pl = {};
+  size_t need = 0;
+  bool any_packed = false;
+  const int64_t mt = packed_tiles(N, T);
+  int i = 0;
+  while (i < num_layers) {
+    int j = i + 1;
+    while (j < num_layers && j - i < kMaxLayersPerLaunch && layers[j].k_in == layers[i].k_in &&
+           layers[j].k_out == layers[i].k_out)
+      ++j;
+    Launch l = {};
+    l.first = i;
+    l.count = j - i;
+    l.kin = (int)layers[i].k_in;
+    l.kout = (int)layers[i].k_out;
+    l.packed = packed_ok(layers, i, l.count, N, T, dtype);
+    if (l.packed) {
+      any_packed = true;
+      l.chunk = kTokTile;
+      l.nchunks = 1;
+      const size_t b = (size_t)l.count * mt * 2 * l.kin * l.kout * sizeof(float);
+      if (b > need) need = b;
+    } else {
+      int64_t tiles = (T + kTokTile - 1) / kTokTile;
+      if (tiles < 1) tiles = 1;
+      int64_t chunk_tiles = tiles;
+      while (chunk_tiles > 1 && (int64_t)l.count * N * ((tiles + chunk_tiles - 1) / chunk_tiles) < kTargetUnits)
+        chunk_tiles = (chunk_tiles + 1) / 2;
+      l.chunk = (int)(chunk_tiles * kTokTile);
+      l.nchunks = (int)((tiles + chunk_tiles - 1) / chunk_tiles);
+      if (l.nchunks > 1) {
+        const size_t b = (size_t)l.count * N * l.nchunks * l.kin * l.kout * sizeof(float);
+        if (b > need) need = b;
+      }
+    }
+    if (out) out[pl.nlaunch] = l;
+    ++pl.nlaunch;
+    i = j;
+  }
+  pl.max_tiles = (int)mt;
+  if (any_packed) {
+    pl.off_cum = 0;
+    pl.off_tiles = align_up((size_t)(N + 1) * sizeof(int), 256);
+    pl.off_partial = pl.off_tiles + align_up((size_t)(mt > 0 ? mt : 1) * sizeof(int), 256);
+  } else {
+    pl.off_cum = pl.off_tiles = pl.off_partial = 0;
+  }
+  pl.bytes = (need > 0 || any_packed) && N > 0 ? pl.off_partial + need : 0;
+  return pl;
+}
+
 template <bool BF16, int KIN, int KOUT>
-void launch_t(const SketchArgs& a, int units, hipStream_t st) {
+void launch_t(const Launch& l, const SketchArgs& a, const PackArgs& pa, hipStream_t st) {
+  if (l.packed) {
+    if (pa.max_tiles > 0)
+      hipLaunchKernelGGL((sketch_packed_kernel<BF16, KIN, KOUT>), dim3(l.count * pa.max_tiles), dim3(kThreads), 0, st,
+                         pa);
+    hipLaunchKernelGGL((sketch_packed_reduce_kernel<KIN, KOUT>), dim3(l.count * pa.N * kReduceSplit), dim3(kThreads),
+                       0, st, pa);
+    return;
+  }
+  const int units = l.count * a.N * l.nchunks;
   hipLaunchKernelGGL((sketch_kernel<BF16, KIN, KOUT>), dim3(units), dim3(kThreads), 0, st, a);
   if (a.nchunks > 1)
-    hipLaunchKernelGGL((sketch_reduce_kernel<KIN, KOUT>), dim3(a.num_layers * a.N), dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((sketch_reduce_kernel<KIN, KOUT>), dim3(a.num_layers * a.N * kReduceSplit), dim3(kThreads), 0,
+                       st, a);
 }
 
 template <bool BF16>
-void launch_k(const SketchArgs& a, int units, int kin, int kout, hipStream_t st) {
-#define DR_SK(I, O)                                        \
-  if (kin == I && kout == O) {                             \
-    launch_t<BF16, I, O>(a, units, st);                    \
-    return;                                                \
+void launch_k(const Launch& l, const SketchArgs& a, const PackArgs& pa, hipStream_t st) {
+#define DR_SK(I, O)                               \
+  if (l.kin == I && l.kout == O) {                \
+    launch_t<BF16, I, O>(l, a, pa, st);           \
+    return;                                       \
   }
   DR_SK(16, 16) DR_SK(16, 32) DR_SK(16, 64)
   DR_SK(32, 16) DR_SK(32, 32) DR_SK(32, 64)
@@ -358,53 +856,11 @@ void launch_k(const SketchArgs& a, int units, int kin, int kout, hipStream_t st)
 #undef DR_SK
 }
 
-bool valid_k(int64_t k) { return k == 16 || k == 32 || k == 64; }
-
-// Launch plan: layers are grouped into launches of at most
-// kMaxLayersPerLaunch consecutive layers with equal (k_in, k_out); the chunk
-// length is halved (in whole tiles) until a launch has >= kTargetUnits units.
-struct Launch {
-  int first, count, kin, kout, chunk, nchunks;
-};
-
-int plan(const dr_layer* layers, int num_layers, int64_t N, int64_t T, Launch* out, size_t* ws) {
-  int nl = 0;
-  size_t need = 0;
-  int i = 0;
-  while (i < num_layers) {
-    int j = i + 1;
-    while (j < num_layers && j - i < kMaxLayersPerLaunch && layers[j].k_in == layers[i].k_in &&
-           layers[j].k_out == layers[i].k_out)
-      ++j;
-    Launch l;
-    l.first = i;
-    l.count = j - i;
-    l.kin = (int)layers[i].k_in;
-    l.kout = (int)layers[i].k_out;
-    int64_t tiles = (T + kTokTile - 1) / kTokTile;
-    if (tiles < 1) tiles = 1;
-    int64_t chunk_tiles = tiles;
-    while (chunk_tiles > 1 && (int64_t)l.count * N * ((tiles + chunk_tiles - 1) / chunk_tiles) < kTargetUnits)
-      chunk_tiles = (chunk_tiles + 1) / 2;
-    l.chunk = (int)(chunk_tiles * kTokTile);
-    l.nchunks = (int)((tiles + chunk_tiles - 1) / chunk_tiles);
-    if (l.nchunks > 1) {
-      size_t b = (size_t)l.count * N * l.nchunks * l.kin * l.kout * sizeof(float);
-      if (b > need) need = b;
-    }
-    if (out) out[nl] = l;
-    ++nl;
-    i = j;
-  }
-  if (ws) *ws = need;
-  return nl;
-}
-
 dr_status validate(const dr_layer* layers, int num_layers, int64_t N, int64_t T, dr_dtype dtype,
                    const float* S, int64_t ldS) {
   if (dtype != DR_BF16 && dtype != DR_F32) return DR_ERR_DTYPE;
   if (!layers || num_layers < 1 || N < 0 || T < 0) return DR_ERR_ARG;
-  if (N > (1 << 24) || T > (1 << 24)) return DR_ERR_ARG;
+  if (N > (1 << 24) || T > (1 << 24) || N * T > (1LL << 31) - kTokTile) return DR_ERR_ARG;
   const int64_t vec = dtype == DR_BF16 ? 8 : 4;
   if (N > 0 && !S) return DR_ERR_ARG;
   for (int l = 0; l < num_layers; ++l) {
@@ -427,13 +883,11 @@ dr_status validate(const dr_layer* layers, int num_layers, int64_t N, int64_t T,
 
 extern "C" size_t dr_sketch_workspace_size(const dr_layer* layers, int num_layers, int64_t N, int64_t T,
                                            dr_dtype dtype) {
-  (void)dtype;
   if (!layers || num_layers < 1 || N < 0 || T < 0) return 0;
+  if (dtype != DR_BF16 && dtype != DR_F32) return 0;
   for (int l = 0; l < num_layers; ++l)
     if (!dr::valid_k(layers[l].k_in) || !dr::valid_k(layers[l].k_out)) return 0;
-  size_t ws = 0;
-  dr::plan(layers, num_layers, N, T, nullptr, &ws);
-  return ws;
+  return dr::plan(layers, num_layers, N, T, dtype, nullptr).bytes;
 }
 
 extern "C" dr_status dr_sketch_grads(const dr_layer* layers, int num_layers, int64_t N, int64_t T,
@@ -442,45 +896,60 @@ extern "C" dr_status dr_sketch_grads(const dr_layer* layers, int num_layers, int
   using namespace dr;
   dr_status st = validate(layers, num_layers, N, T, dtype, S, ldS);
   if (st != DR_OK) return st;
-  size_t need = 0;
-  const int nlaunch = plan(layers, num_layers, N, T, nullptr, &need);
-  if (need > 0 && (!workspace || ws_bytes < need)) return DR_ERR_WORKSPACE;
+  const Plan pl = plan(layers, num_layers, N, T, dtype, nullptr);
+  if (pl.bytes > 0 && (!workspace || ws_bytes < pl.bytes)) return DR_ERR_WORKSPACE;
   if (N == 0) return DR_OK;
-  Launch* plan_buf = new Launch[nlaunch];
-  plan(layers, num_layers, N, T, plan_buf, nullptr);
+  Launch* lv = new Launch[pl.nlaunch];
+  plan(layers, num_layers, N, T, dtype, lv);
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
-  for (int q = 0; q < nlaunch; ++q) {
-    const Launch& l = plan_buf[q];
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  bool planned = false;
+  for (int q = 0; q < pl.nlaunch && st == DR_OK; ++q) {
+    const Launch& l = lv[q];
     SketchArgs a = {};
+    PackArgs pa = {};
     for (int j = 0; j < l.count; ++j) {
       const dr_layer& L = layers[l.first + j];
-      a.L[j].x = static_cast<const unsigned char*>(L.x);
-      a.L[j].dy = static_cast<const unsigned char*>(L.dy);
-      a.L[j].p_in = static_cast<const unsigned char*>(L.p_in);
-      a.L[j].p_out = static_cast<const unsigned char*>(L.p_out);
-      a.L[j].ldx = L.ldx;
-      a.L[j].lddy = L.lddy;
-      a.L[j].d_in = (int)L.d_in;
-      a.L[j].d_out = (int)L.d_out;
-      a.L[j].col_offset = L.col_offset;
+      LayerArg la;
+      la.x = static_cast<const unsigned char*>(L.x);
+      la.dy = static_cast<const unsigned char*>(L.dy);
+      la.p_in = static_cast<const unsigned char*>(L.p_in);
+      la.p_out = static_cast<const unsigned char*>(L.p_out);
+      la.ldx = L.ldx;
+      la.lddy = L.lddy;
+      la.d_in = (int)L.d_in;
+      la.d_out = (int)L.d_out;
+      la.col_offset = L.col_offset;
+      a.L[j] = la;
+      pa.L[j] = la;
     }
-    a.num_layers = l.count;
-    a.N = (int)N;
-    a.T = (int)T;
+    a.num_layers = pa.num_layers = l.count;
+    a.N = pa.N = (int)N;
+    a.T = pa.T = (int)T;
     a.chunk_tokens = l.chunk;
     a.nchunks = l.nchunks;
     a.len = len;
-    a.S = S;
-    a.ldS = ldS;
-    a.partial = static_cast<float*>(workspace);
-    const int units = l.count * (int)N * l.nchunks;
+    a.S = pa.S = S;
+    a.ldS = pa.ldS = ldS;
+    a.partial = reinterpret_cast<float*>(ws);
+    if (l.packed) {
+      pa.max_tiles = pl.max_tiles;
+      pa.cum = reinterpret_cast<const int*>(ws + pl.off_cum);
+      pa.tile_ex = reinterpret_cast<const int*>(ws + pl.off_tiles);
+      pa.partial = reinterpret_cast<float*>(ws + pl.off_partial);
+      if (!planned) {
+        hipLaunchKernelGGL(sketch_plan_kernel, dim3(1), dim3(1024), 0, hs, len, (int)N, (int)T, pl.max_tiles,
+                           reinterpret_cast<int*>(ws + pl.off_cum), reinterpret_cast<int*>(ws + pl.off_tiles));
+        if ((st = launch_status()) != DR_OK) break;
+        planned = true;
+      }
+    }
     if (dtype == DR_BF16)
-      launch_k<true>(a, units, l.kin, l.kout, hs);
+      launch_k<true>(l, a, pa, hs);
     else
-      launch_k<false>(a, units, l.kin, l.kout, hs);
+      launch_k<false>(l, a, pa, hs);
     st = launch_status();
-    if (st != DR_OK) break;
   }
-  delete[] plan_buf;
+  delete[] lv;
   return st;
 }

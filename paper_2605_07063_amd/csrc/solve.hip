@@ -12,6 +12,11 @@
 // from the fp32 K read from global memory, which brings the solution to
 // fp64-level accuracy whenever cond(K + lam_eff I) * 2^-24 < 1.
 //
+// span_wave_kernel / cone_wave_kernel (n <= 64): the same two methods in a
+// single 64-lane wave, fully in fp64 (no refinement needed), with no block
+// barriers -- the solves of the tiny, small-block and long-context
+// workloads are latency bound and this is their fast path.
+//
 // cone_pg_kernel (n <= 256): projected gradient on the Jacobi-scaled
 // problem, written on the unscaled variable: with r_i = K_ii^-1/2,
 //   w_i <- max(0, w_i - r_i^2 (K w - s)_i / Lhat),  Lhat = max_i sum_j r_i |K_ij| r_j,
@@ -327,6 +332,228 @@ __global__ __launch_bounds__(kConeThreads) void cone_pg_kernel(const float* K, c
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// Single-wave solvers for n <= 64 (one 64-lane wave per group, lane i owns
+// row i, everything in fp64 on the exact fp32 inputs; no block barriers).
+
+constexpr int kWaveN = 64;
+
+__device__ __forceinline__ double wave_sum(double v) {
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+__device__ __forceinline__ double wave_max(double v) {
+  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
+  return v;
+}
+
+typedef __attribute__((ext_vector_type(2))) double f64x2;
+
+// Cholesky of K + lam I in fp64: lane i keeps row i of the factor in
+// registers; each column of L is published once through LDS and read back
+// as a broadcast, so the trailing update is a run of register FMAs.  NM is
+// the padded size (16, 32 or 64); lanes >= n hold zero rows.
+template <int NM>
+__global__ __launch_bounds__(kWaveN) void span_wave_kernel(const float* K, const float* s, const float* t2, int n,
+                                                           float lambda, int mode, float* w, float* lam_eff_out,
+                                                           float* resid2, int* info) {
+  __shared__ __attribute__((aligned(16))) double col[NM];
+  __shared__ double Lr[NM][NM + 1];
+  const int p = blockIdx.x, i = threadIdx.x;
+  const float* Kp = K + (long long)p * n * n;
+  const float* sp = s + (long long)p * n;
+  const bool own = i < n;
+  double a[NM];
+  bool bad = own && !isfinite(sp[i]);
+#pragma unroll
+  for (int k = 0; k < NM; ++k) {
+    const float v = (own && k < n) ? Kp[(long long)i * n + k] : 0.f;
+    bad |= !isfinite(v);
+    a[k] = (double)v;
+  }
+  double kii = 0.0;
+#pragma unroll
+  for (int k = 0; k < NM; ++k)
+    if (k == i) kii = a[k];
+  const double tr = wave_sum(own ? kii : 0.0);
+  const bool nonfinite = __any(bad);
+  const float lam = mode == DR_RIDGE_REL_TRACE ? (float)((double)lambda * tr / (double)n) : lambda;
+  if (nonfinite || (mode == DR_RIDGE_REL_TRACE && tr == 0.0)) {
+    if (own) w[(long long)p * n + i] = 0.f;
+    if (i == 0) {
+      lam_eff_out[p] = nonfinite ? 0.f : lam;
+      resid2[p] = t2[p];
+      info[p] = nonfinite ? DR_INFO_NONFINITE : 0;
+    }
+    return;
+  }
+#pragma unroll
+  for (int k = 0; k < NM; ++k)
+    if (k == i && own) a[k] += (double)lam;
+
+  int bad_pivot = 0;
+#pragma unroll
+  for (int j = 0; j < NM; ++j) {
+    if (j < n && bad_pivot == 0) {
+      const double d = __shfl(a[j], j, 64);        // the pivot, from lane j
+      if (!(d > 0.0)) {
+        bad_pivot = j + 1;
+      } else {
+        const double ljj = sqrt(d);
+        const double lij = i > j ? a[j] / ljj : (i == j ? ljj : 0.0);
+        a[j] = i >= j ? lij : a[j];
+        col[i] = i > j ? lij : 0.0;
+        __syncthreads();
+        // a[k] -= L_ij L_kj for k > j (entries above the diagonal are never
+        // read); an odd first column alone, then pairs of columns
+        const int k1 = (j + 1) & 1 ? j + 2 : j + 1;
+        if (((j + 1) & 1) && j + 1 < NM) a[j + 1] -= lij * col[j + 1];
+#pragma unroll
+        for (int k = k1; k < NM; k += 2) {
+          const f64x2 lk = *reinterpret_cast<const f64x2*>(&col[k]);
+          a[k] -= lij * lk.x;
+          a[k + 1] -= lij * lk.y;
+        }
+        __syncthreads();
+      }
+    }
+  }
+  if (bad_pivot) {
+    if (own) w[(long long)p * n + i] = 0.f;
+    if (i == 0) {
+      lam_eff_out[p] = lam;
+      resid2[p] = t2[p];
+      info[p] = bad_pivot;
+    }
+    return;
+  }
+  // L y = s (lane i holds y_i and row i of L)
+  double y = own ? (double)sp[i] : 0.0;
+#pragma unroll
+  for (int j = 0; j < NM; ++j) {
+    if (j < n) {
+      if (i == j) y /= a[j];
+      const double yj = __shfl(y, j, 64);
+      if (i > j && own) y -= a[j] * yj;
+    }
+  }
+  // L^T x = y: rows of L through LDS so lane i can read L_ji
+#pragma unroll
+  for (int k = 0; k < NM; ++k) Lr[i][k] = a[k];
+  __syncthreads();
+  for (int j = n - 1; j >= 0; --j) {
+    if (i == j) y /= Lr[j][j];
+    const double xj = __shfl(y, j, 64);
+    if (i < j) y -= Lr[j][i] * xj;
+  }
+  const double x = own ? y : 0.0;
+  // resid2 = t2 - 2 s.x + x.K.x with the fp32 K (no ridge)
+  col[i] = x;
+  __syncthreads();
+  double kx = 0.0;
+#pragma unroll
+  for (int k = 0; k < NM; k += 2) {
+    const f64x2 xk = *reinterpret_cast<const f64x2*>(&col[k]);
+    const float k0 = (own && k < n) ? Kp[(long long)i * n + k] : 0.f;
+    const float k1 = (own && k + 1 < n) ? Kp[(long long)i * n + k + 1] : 0.f;
+    kx += (double)k0 * xk.x + (double)k1 * xk.y;
+  }
+  const double q = wave_sum(own ? x * kx - 2.0 * (double)sp[i] * x : 0.0);
+  if (own) w[(long long)p * n + i] = (float)x;
+  if (i == 0) {
+    lam_eff_out[p] = lam;
+    resid2[p] = (float)((double)t2[p] + q);
+    info[p] = 0;
+  }
+}
+
+// Jacobi-preconditioned projected gradient, one wave: lane i keeps row i of
+// the fp32 K in registers and w_i in fp64; each step publishes w through
+// LDS (double buffered) and reads it back as broadcast pairs.
+template <int NM>
+__global__ __launch_bounds__(kWaveN) void cone_wave_kernel(const float* K, const float* s, const float* t2, int n,
+                                                           int max_iter, float kkt_tol, float* w, float* resid2,
+                                                           int* iters, float* kkt, int* info) {
+  __shared__ __attribute__((aligned(16))) double wb[2][kWaveN];
+  __shared__ __attribute__((aligned(16))) double rs[kWaveN];
+  const int p = blockIdx.x, i = threadIdx.x;
+  const float* Kp = K + (long long)p * n * n;
+  const float* sp = s + (long long)p * n;
+  const bool own = i < n;
+  float kr[NM];
+  bool bad = own && !isfinite(sp[i]);
+  double kii = 0.0;
+#pragma unroll
+  for (int j = 0; j < NM; ++j) {
+    kr[j] = (own && j < n) ? Kp[(long long)i * n + j] : 0.f;
+    bad |= !isfinite(kr[j]);
+    if (j == i) kii = (double)kr[j];
+  }
+  const double si = own ? (double)sp[i] : 0.0;
+  const double ri = kii > 0.0 ? 1.0 / sqrt(kii) : 0.0;
+  rs[i] = ri;
+  wb[0][i] = 0.0;
+  __syncthreads();
+  if (__any(bad)) {
+    if (own) w[(long long)p * n + i] = 0.f;
+    if (i == 0) {
+      resid2[p] = t2[p];
+      iters[p] = 0;
+      kkt[p] = 0.f;
+      info[p] = DR_INFO_NONFINITE;
+    }
+    return;
+  }
+  double lrow = 0.0;
+#pragma unroll
+  for (int j = 0; j < NM; ++j) lrow += fabs((double)kr[j]) * rs[j];
+  const double Lhat = wave_max(own ? lrow * ri : 0.0);
+  const double den0 = wave_max(own ? fabs(ri * si) : 0.0);
+  const double den = den0 > 0.0 ? den0 : 2.2250738585072014e-308;
+  const double step = ri * ri / (Lhat > 0.0 ? Lhat : 1.0);
+  const bool check_each = kkt_tol > 0.f;
+
+  int it = 0, cur = 0;
+  double rho = 0.0, g = 0.0, wi = 0.0;
+  while (true) {
+    double wv[NM];
+#pragma unroll
+    for (int j = 0; j < NM; j += 2) {
+      const f64x2 v = *reinterpret_cast<const f64x2*>(&wb[cur][j]);
+      wv[j] = v.x;
+      wv[j + 1] = v.y;
+    }
+    double acc0 = 0.0, acc1 = 0.0;
+#pragma unroll
+    for (int j = 0; j < NM; j += 2) {
+      acc0 += (double)kr[j] * wv[j];
+      acc1 += (double)kr[j + 1] * wv[j + 1];
+    }
+    g = (acc0 + acc1) - si;
+    const bool last = it >= max_iter || Lhat == 0.0;
+    if (check_each || last) {
+      const double v = (own && ri > 0.0) ? fabs(fmin(wi / ri, ri * g)) : 0.0;
+      rho = wave_max(v) / den;
+      if ((check_each && rho <= (double)kkt_tol) || last) break;
+    }
+    const double nw = wi - step * g;
+    wi = nw > 0.0 ? nw : 0.0;
+    wb[cur ^ 1][i] = own ? wi : 0.0;
+    __syncthreads();
+    cur ^= 1;
+    ++it;
+  }
+  const double q = wave_sum(own ? wi * g - si * wi : 0.0);
+  if (own) w[(long long)p * n + i] = (float)wi;
+  if (i == 0) {
+    resid2[p] = (float)((double)t2[p] + q);
+    iters[p] = it;
+    kkt[p] = (float)rho;
+    info[p] = (kkt_tol > 0.f && rho > (double)kkt_tol) ? DR_INFO_NOT_CONVERGED : 0;
+  }
+}
+
 __global__ void empty_group_kernel(const float* t2, int P, float* lam_eff, float* resid2, int32_t* iters, float* kkt,
                                    int32_t* info) {
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
@@ -372,8 +599,18 @@ extern "C" dr_status dr_project_span(const float* K, const float* s, const float
                        (int32_t*)nullptr, (float*)nullptr, info);
     return launch_status();
   }
-  hipLaunchKernelGGL(span_small_kernel, dim3(P), dim3(kSpanThreads), 0, hs, K, s, t2, (int)n, lambda, (int)mode, w,
-                     lam_eff, resid2, info);
+  if (n <= 16)
+    hipLaunchKernelGGL(span_wave_kernel<16>, dim3(P), dim3(kWaveN), 0, hs, K, s, t2, (int)n, lambda, (int)mode, w,
+                       lam_eff, resid2, info);
+  else if (n <= 32)
+    hipLaunchKernelGGL(span_wave_kernel<32>, dim3(P), dim3(kWaveN), 0, hs, K, s, t2, (int)n, lambda, (int)mode, w,
+                       lam_eff, resid2, info);
+  else if (n <= kWaveN)
+    hipLaunchKernelGGL(span_wave_kernel<64>, dim3(P), dim3(kWaveN), 0, hs, K, s, t2, (int)n, lambda, (int)mode, w,
+                       lam_eff, resid2, info);
+  else
+    hipLaunchKernelGGL(span_small_kernel, dim3(P), dim3(kSpanThreads), 0, hs, K, s, t2, (int)n, lambda, (int)mode,
+                       w, lam_eff, resid2, info);
   return launch_status();
 }
 
@@ -392,6 +629,18 @@ extern "C" dr_status dr_project_cone(const float* K, const float* s, const float
   if (n == 0) {
     hipLaunchKernelGGL(empty_group_kernel, dim3((P + 255) / 256), dim3(256), 0, hs, t2, P, (float*)nullptr, resid2,
                        iters, kkt, info);
+    return launch_status();
+  }
+  if (n <= kWaveN) {
+    if (n <= 16)
+      hipLaunchKernelGGL(cone_wave_kernel<16>, dim3(P), dim3(kWaveN), 0, hs, K, s, t2, (int)n, max_iter, kkt_tol, w,
+                         resid2, iters, kkt, info);
+    else if (n <= 32)
+      hipLaunchKernelGGL(cone_wave_kernel<32>, dim3(P), dim3(kWaveN), 0, hs, K, s, t2, (int)n, max_iter, kkt_tol, w,
+                         resid2, iters, kkt, info);
+    else
+      hipLaunchKernelGGL(cone_wave_kernel<64>, dim3(P), dim3(kWaveN), 0, hs, K, s, t2, (int)n, max_iter, kkt_tol, w,
+                         resid2, iters, kkt, info);
     return launch_status();
   }
   int npad = 1;

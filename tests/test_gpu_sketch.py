@@ -137,3 +137,23 @@ def test_long_context_full_size_sampled():
     assert errs.max() <= TOL_SKETCH_BF16, errs.max()
     assert np.isfinite(S_gpu).all()
     print(f"long full-size sampled max block rel err {errs.max():.2e}")
+
+
+@pytest.mark.parametrize("dtype,tol", [(torch.bfloat16, TOL_SKETCH_BF16), (torch.float32, TOL_SKETCH_F32)])
+def test_many_short_examples_share_a_token_tile(dtype, tol):
+    """Packed tiles holding many examples each (lengths 0..16): the per-example
+    masking of stage 2 and the head / tail partials of split examples."""
+    N, T = 300, 16
+    g = torch.Generator(device=DEV)
+    g.manual_seed(77)
+    lens = torch.randint(0, T + 1, (N,), generator=g, device=DEV, dtype=torch.int32)
+    layers = custom_layers([(64, 128, 32, 64), (128, 64, 16, 16)], N, T, dtype, lens, nan_padding=True, seed=11)
+    _, errs = run_case(layers, lens, N, T, tol, rows=list(range(0, N, 7)) + [N - 1])
+    print(f"{dtype} short examples max block rel err {errs.max():.2e}")
+
+
+def test_lengths_on_tile_boundaries():
+    N, T = 9, 384
+    lens = torch.tensor([128, 128, 256, 0, 64, 64, 384, 1, 127], dtype=torch.int32, device=DEV)
+    layers = custom_layers([(128, 64, 64, 32)], N, T, torch.bfloat16, lens, nan_padding=True, seed=13)
+    run_case(layers, lens, N, T, TOL_SKETCH_BF16)
