@@ -12,10 +12,14 @@
 // from the fp32 K read from global memory, which brings the solution to
 // fp64-level accuracy whenever cond(K + lam_eff I) * 2^-24 < 1.
 //
-// span_wave_kernel / cone_wave_kernel (n <= 64): the same two methods in a
-// single 64-lane wave, fully in fp64 (no refinement needed), with no block
-// barriers -- the solves of the tiny, small-block and long-context
-// workloads are latency bound and this is their fast path.
+// n <= 64 (the tiny, small-block and long-context workloads) is latency
+// bound, and everything runs in fp64 on the exact fp32 inputs (no refinement
+// needed):
+//   n <= 16       span_wave_kernel / cone_wave_kernel, one 64-lane wave,
+//                 lane i owns row i, no block barriers;
+//   16 < n <= 64  span_cols_kernel (rows across lanes, 16-column slices
+//                 across waves, one barrier per pivot) and cone_quad_kernel
+//                 (four lanes per row, one barrier per step).
 //
 // cone_pg_kernel (n <= 256): projected gradient on the Jacobi-scaled
 // problem, written on the unscaled variable: with r_i = K_ii^-1/2,
@@ -350,15 +354,36 @@ __device__ __forceinline__ double wave_max(double v) {
 
 typedef __attribute__((ext_vector_type(2))) double f64x2;
 
+// sum over the 4 lanes of a quad with DPP quad permutes (xor 1, xor 2)
+__device__ __forceinline__ double quad_sum(double v) {
+  int lo = __double2loint(v), hi = __double2hiint(v);
+  double o = __hiloint2double(__builtin_amdgcn_mov_dpp(hi, 0xB1, 0xF, 0xF, false),
+                              __builtin_amdgcn_mov_dpp(lo, 0xB1, 0xF, 0xF, false));
+  v += o;
+  lo = __double2loint(v);
+  hi = __double2hiint(v);
+  o = __hiloint2double(__builtin_amdgcn_mov_dpp(hi, 0x4E, 0xF, 0xF, false),
+                       __builtin_amdgcn_mov_dpp(lo, 0x4E, 0xF, 0xF, false));
+  return v + o;
+}
+
+// value of lane src (src uniform) as a scalar broadcast
+__device__ __forceinline__ double readlane_d(double v, int src) {
+  const int lo = __builtin_amdgcn_readlane(__double2loint(v), src);
+  const int hi = __builtin_amdgcn_readlane(__double2hiint(v), src);
+  return __hiloint2double(hi, lo);
+}
+
 // Cholesky of K + lam I in fp64: lane i keeps row i of the factor in
-// registers; each column of L is published once through LDS and read back
-// as a broadcast, so the trailing update is a run of register FMAs.  NM is
-// the padded size (16, 32 or 64); lanes >= n hold zero rows.
+// registers.  Every broadcast (the pivot, the column L_kj, the solution
+// components) is a v_readlane from the owning lane -- no LDS and no waits in
+// the factorisation.  The back substitution needs column i of L in lane i:
+// the rows go through LDS once and each lane reads its column in one batch.
+// NM is the padded size (16, 32 or 64); lanes >= n hold zero rows.
 template <int NM>
 __global__ __launch_bounds__(kWaveN) void span_wave_kernel(const float* K, const float* s, const float* t2, int n,
                                                            float lambda, int mode, float* w, float* lam_eff_out,
                                                            float* resid2, int* info) {
-  __shared__ __attribute__((aligned(16))) double col[NM];
   __shared__ double Lr[NM][NM + 1];
   const int p = blockIdx.x, i = threadIdx.x;
   const float* Kp = K + (long long)p * n * n;
@@ -393,29 +418,24 @@ __global__ __launch_bounds__(kWaveN) void span_wave_kernel(const float* K, const
     if (k == i && own) a[k] += (double)lam;
 
   int bad_pivot = 0;
+  double dinv = 0.0;   // 1 / L_ii of this lane's row
 #pragma unroll
   for (int j = 0; j < NM; ++j) {
     if (j < n && bad_pivot == 0) {
-      const double d = __shfl(a[j], j, 64);        // the pivot, from lane j
+      const double d = readlane_d(a[j], j);        // the pivot, from lane j
       if (!(d > 0.0)) {
         bad_pivot = j + 1;
       } else {
         const double ljj = sqrt(d);
-        const double lij = i > j ? a[j] / ljj : (i == j ? ljj : 0.0);
+        const double inv = 1.0 / ljj;
+        if (i == j) dinv = inv;
+        const double lij = i > j ? a[j] * inv : (i == j ? ljj : 0.0);
         a[j] = i >= j ? lij : a[j];
-        col[i] = i > j ? lij : 0.0;
-        __syncthreads();
-        // a[k] -= L_ij L_kj for k > j (entries above the diagonal are never
-        // read); an odd first column alone, then pairs of columns
-        const int k1 = (j + 1) & 1 ? j + 2 : j + 1;
-        if (((j + 1) & 1) && j + 1 < NM) a[j + 1] -= lij * col[j + 1];
+        // a[k] -= L_ij L_kj for k > j, L_kj from lane k (entries above the
+        // diagonal are never read)
 #pragma unroll
-        for (int k = k1; k < NM; k += 2) {
-          const f64x2 lk = *reinterpret_cast<const f64x2*>(&col[k]);
-          a[k] -= lij * lk.x;
-          a[k + 1] -= lij * lk.y;
-        }
-        __syncthreads();
+        for (int k = j + 1; k < NM; ++k)
+          if (k < n) a[k] -= lij * readlane_d(a[j], k);
       }
     }
   }
@@ -433,31 +453,34 @@ __global__ __launch_bounds__(kWaveN) void span_wave_kernel(const float* K, const
 #pragma unroll
   for (int j = 0; j < NM; ++j) {
     if (j < n) {
-      if (i == j) y /= a[j];
-      const double yj = __shfl(y, j, 64);
+      if (i == j) y *= dinv;
+      const double yj = readlane_d(y, j);
       if (i > j && own) y -= a[j] * yj;
     }
   }
-  // L^T x = y: rows of L through LDS so lane i can read L_ji
+  // column i of L into lane i, through LDS
 #pragma unroll
   for (int k = 0; k < NM; ++k) Lr[i][k] = a[k];
   __syncthreads();
-  for (int j = n - 1; j >= 0; --j) {
-    if (i == j) y /= Lr[j][j];
-    const double xj = __shfl(y, j, 64);
-    if (i < j) y -= Lr[j][i] * xj;
+  double lc[NM];
+#pragma unroll
+  for (int j = 0; j < NM; ++j) lc[j] = Lr[j][i];
+  // L^T x = y
+#pragma unroll
+  for (int j = NM - 1; j >= 0; --j) {
+    if (j < n) {
+      if (i == j) y *= dinv;
+      const double xj = readlane_d(y, j);
+      if (i < j) y -= lc[j] * xj;
+    }
   }
   const double x = own ? y : 0.0;
   // resid2 = t2 - 2 s.x + x.K.x with the fp32 K (no ridge)
-  col[i] = x;
-  __syncthreads();
   double kx = 0.0;
 #pragma unroll
-  for (int k = 0; k < NM; k += 2) {
-    const f64x2 xk = *reinterpret_cast<const f64x2*>(&col[k]);
-    const float k0 = (own && k < n) ? Kp[(long long)i * n + k] : 0.f;
-    const float k1 = (own && k + 1 < n) ? Kp[(long long)i * n + k + 1] : 0.f;
-    kx += (double)k0 * xk.x + (double)k1 * xk.y;
+  for (int k = 0; k < NM; ++k) {
+    const float kik = (own && k < n) ? Kp[(long long)i * n + k] : 0.f;
+    kx += (double)kik * readlane_d(x, k);
   }
   const double q = wave_sum(own ? x * kx - 2.0 * (double)sp[i] * x : 0.0);
   if (own) w[(long long)p * n + i] = (float)x;
@@ -554,6 +577,293 @@ __global__ __launch_bounds__(kWaveN) void cone_wave_kernel(const float* K, const
   }
 }
 
+
+// Jacobi-preconditioned projected gradient for n <= 64 on four waves: wave v
+// owns rows 16v..16v+15, four lanes per row each hold a quarter of the row
+// of K in fp64 registers; partial dot products meet through quad shuffles,
+// and w is exchanged through LDS (double buffered) with one barrier per step.
+template <int NM>
+__global__ __launch_bounds__(256) void cone_quad_kernel(const float* K, const float* s, const float* t2, int n,
+                                                        int max_iter, float kkt_tol, float* w, float* resid2,
+                                                        int* iters, float* kkt, int* info) {
+  constexpr int Q = NM / 4;   // columns per lane
+  __shared__ __attribute__((aligned(16))) double wb[2][NM];
+  __shared__ double rs[NM];
+  __shared__ double red[4];
+  __shared__ int flag;
+  const int p = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int row = wave * 16 + (lane >> 2), q = lane & 3;
+  const float* Kp = K + (long long)p * n * n;
+  const float* sp = s + (long long)p * n;
+  const bool own = row < n;
+  if (tid == 0) flag = 0;
+  if (tid < NM) {
+    const float d = tid < n ? Kp[(long long)tid * n + tid] : 0.f;
+    rs[tid] = d > 0.f ? 1.0 / sqrt((double)d) : 0.0;
+    wb[0][tid] = 0.0;
+  }
+  __syncthreads();
+  double kr[Q];
+  bool bad = own && q == 0 && !isfinite(sp[row]);
+  double lrow = 0.0;
+#pragma unroll
+  for (int c = 0; c < Q; ++c) {
+    const int j = q * Q + c;
+    const float v = (own && j < n) ? Kp[(long long)row * n + j] : 0.f;
+    bad |= !isfinite(v);
+    kr[c] = (double)v;
+    lrow += fabs(kr[c]) * rs[j];
+  }
+  if (bad) flag = 1;
+  lrow = quad_sum(lrow);
+  const double ri = own ? rs[row] : 0.0;
+  const double si = own ? (double)sp[row] : 0.0;
+  double lmax = own ? lrow * ri : 0.0, smax = own ? fabs(ri * si) : 0.0;
+  for (int off = 32; off > 0; off >>= 1) {
+    lmax = fmax(lmax, __shfl_xor(lmax, off, 64));
+    smax = fmax(smax, __shfl_xor(smax, off, 64));
+  }
+  __shared__ double wl[4], wsx[4];
+  if (lane == 0) {
+    wl[wave] = lmax;
+    wsx[wave] = smax;
+  }
+  __syncthreads();
+  if (flag) {
+    if (own && q == 0) w[(long long)p * n + row] = 0.f;
+    if (tid == 0) {
+      resid2[p] = t2[p];
+      iters[p] = 0;
+      kkt[p] = 0.f;
+      info[p] = DR_INFO_NONFINITE;
+    }
+    return;
+  }
+  const double Lhat = fmax(fmax(wl[0], wl[1]), fmax(wl[2], wl[3]));
+  const double den0 = fmax(fmax(wsx[0], wsx[1]), fmax(wsx[2], wsx[3]));
+  const double den = den0 > 0.0 ? den0 : 2.2250738585072014e-308;
+  const double step = ri * ri / (Lhat > 0.0 ? Lhat : 1.0);
+  const bool check_each = kkt_tol > 0.f;
+
+  int it = 0, cur = 0;
+  double rho = 0.0, g = 0.0, wi = 0.0;
+  while (true) {
+    double acc = 0.0;
+#pragma unroll
+    for (int c = 0; c < Q; c += 2) {
+      const f64x2 v = *reinterpret_cast<const f64x2*>(&wb[cur][q * Q + c]);
+      acc += kr[c] * v.x;
+      acc += kr[c + 1] * v.y;
+    }
+    acc = quad_sum(acc);
+    g = acc - si;
+    const bool last = it >= max_iter || Lhat == 0.0;
+    if (check_each || last) {
+      double v = (own && q == 0 && ri > 0.0) ? fabs(fmin(wi / ri, ri * g)) : 0.0;
+      for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
+      if (lane == 0) red[wave] = v;
+      __syncthreads();
+      rho = fmax(fmax(red[0], red[1]), fmax(red[2], red[3])) / den;
+      __syncthreads();
+      if ((check_each && rho <= (double)kkt_tol) || last) break;
+    }
+    const double nw = wi - step * g;
+    wi = nw > 0.0 ? nw : 0.0;
+    if (q == 0 && row < NM) wb[cur ^ 1][row] = own ? wi : 0.0;
+    __syncthreads();
+    cur ^= 1;
+    ++it;
+  }
+  double contrib = (own && q == 0) ? wi * g - si * wi : 0.0;
+  for (int off = 32; off > 0; off >>= 1) contrib += __shfl_xor(contrib, off, 64);
+  if (lane == 0) red[wave] = contrib;
+  __syncthreads();
+  if (own && q == 0) w[(long long)p * n + row] = (float)wi;
+  if (tid == 0) {
+    resid2[p] = (float)((double)t2[p] + ((red[0] + red[1]) + (red[2] + red[3])));
+    iters[p] = it;
+    kkt[p] = (float)rho;
+    info[p] = (kkt_tol > 0.f && rho > (double)kkt_tol) ? DR_INFO_NOT_CONVERGED : 0;
+  }
+}
+
+
+// 1 / sqrt(d) for d > 0 (normal range): the hardware estimate and two
+// Newton steps r <- r + r/2 (1 - d r^2), a few ulp in fp64, about a third of
+// the dependent steps of a correctly rounded sqrt followed by a divide.
+__device__ __forceinline__ double rsqrt_newton(double d) {
+  double r = __builtin_amdgcn_rsq(d);
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const double e = fma(-d * r, r, 1.0);
+    r = fma(0.5 * r, e, r);
+  }
+  return r;
+}
+
+// Cholesky of K + lam I in fp64 for 16 < n <= 64 on NM/16 waves.  Lane i of
+// wave c holds A[i][16c .. 16c + 16) in registers.  The matrix is padded to
+// NM with identity rows and columns (the padded part of the factor is the
+// identity and the padded solution is zero), so the pivot loop has a fixed
+// trip count: column j = 16 jb + jc with jc unrolled, the register holding
+// column j (or j + 1) is known at compile time, and which waves still have
+// columns to update is a scalar branch.  Before pivot j the owner of column j
+// has published A[.][j] to an LDS column buffer (double buffered), so each
+// pivot costs one barrier.  The factor then goes to LDS and wave 0 does the
+// two triangular solves (the L^T solve reads column i of L into lane i once).
+template <int NM>
+__global__ __launch_bounds__(NM * 4) void span_cols_kernel(const float* K, const float* s, const float* t2, int n,
+                                                           float lambda, int mode, float* w, float* lam_eff_out,
+                                                           float* resid2, int* info) {
+  constexpr int CW = 16, NW = NM / CW;
+  __shared__ __attribute__((aligned(16))) double colb[2][NM];
+  __shared__ double Lr[NM][NM + 1];
+  __shared__ __attribute__((aligned(16))) double xs[NM];
+  __shared__ double kxp[NW][NM];
+  __shared__ double red[NW];
+  __shared__ int flag;
+  const int p = blockIdx.x, tid = threadIdx.x, i = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, known uniform
+  const int c0 = wv * CW;                                     // first column held by this wave
+  const float* Kp = K + (long long)p * n * n;
+  const float* sp = s + (long long)p * n;
+  const bool own = i < n;    // a row of K
+  const bool inm = i < NM;   // a row of the padded matrix
+  if (tid == 0) flag = 0;
+  __syncthreads();
+  double a[CW];
+  float kq[CW];   // this lane's slice of the fp32 K row, kept for the residual
+  bool bad = own && wv == 0 && !isfinite(sp[i]);
+  double kii = 0.0;
+#pragma unroll
+  for (int c = 0; c < CW; ++c) {
+    const int k = c0 + c;
+    const float v = (own && k < n) ? Kp[(long long)i * n + k] : 0.f;
+    bad |= !isfinite(v);
+    kq[c] = v;
+    a[c] = (double)v;
+    if (k == i) kii = a[c];
+  }
+  if (bad) flag = 1;
+  const double trw = wave_sum(kii);
+  if (i == 0) red[wv] = trw;
+  __syncthreads();
+  double tr = 0.0;
+#pragma unroll
+  for (int v = 0; v < NW; ++v) tr += red[v];
+  const bool nonfinite = flag != 0;
+  const float lam = mode == DR_RIDGE_REL_TRACE ? (float)((double)lambda * tr / (double)n) : lambda;
+  if (nonfinite || (mode == DR_RIDGE_REL_TRACE && tr == 0.0)) {
+    if (own && wv == 0) w[(long long)p * n + i] = 0.f;
+    if (tid == 0) {
+      lam_eff_out[p] = nonfinite ? 0.f : lam;
+      resid2[p] = t2[p];
+      info[p] = nonfinite ? DR_INFO_NONFINITE : 0;
+    }
+    return;
+  }
+#pragma unroll
+  for (int c = 0; c < CW; ++c)
+    if (c0 + c == i) a[c] = own ? a[c] + (double)lam : (inm ? 1.0 : 0.0);
+  if (wv == 0 && inm) colb[0][i] = a[0];
+  __syncthreads();
+
+  int bad_pivot = 0;   // first j with a non-positive pivot (then the rest is discarded)
+  for (int jb = 0; jb < NW; ++jb) {
+#pragma unroll
+    for (int jc = 0; jc < CW; ++jc) {
+      const int j = jb * CW + jc;
+      const double* cb = colb[jc & 1];
+      double d = cb[j];
+      if (!(d > 0.0)) {
+        if (bad_pivot == 0) bad_pivot = j + 1;
+        d = 1.0;
+      }
+      const double r = rsqrt_newton(d);
+      const double lij = (inm && i > j) ? cb[i] * r : 0.0;
+      const double f = lij * r;   // L_ij / L_jj
+      if (wv == jb) {
+        // column j becomes L_:j (entries above the diagonal are never read)
+        a[jc] = i > j ? lij : (i == j ? d * r : 0.0);
+#pragma unroll
+        for (int c = jc + 1; c < CW; ++c) a[c] = fma(-f, cb[c0 + c], a[c]);
+        if (jc + 1 < CW && inm) colb[(jc + 1) & 1][i] = a[jc + 1];
+      } else if (wv > jb) {
+        // A_ik -= L_ij L_kj = f A_kj for all of this wave's columns
+#pragma unroll
+        for (int c = 0; c < CW; c += 2) {
+          const f64x2 lk = *reinterpret_cast<const f64x2*>(&cb[c0 + c]);
+          a[c] = fma(-f, lk.x, a[c]);
+          a[c + 1] = fma(-f, lk.y, a[c + 1]);
+        }
+        if (jc + 1 == CW && wv == jb + 1 && inm) colb[0][i] = a[0];
+      }
+      __syncthreads();
+    }
+  }
+  if (bad_pivot) {
+    if (own && wv == 0) w[(long long)p * n + i] = 0.f;
+    if (tid == 0) {
+      lam_eff_out[p] = lam;
+      resid2[p] = t2[p];
+      info[p] = bad_pivot;
+    }
+    return;
+  }
+  // the factor to LDS (lower triangle; the rest is never read)
+  if (inm) {
+#pragma unroll
+    for (int c = 0; c < CW; ++c) Lr[i][c0 + c] = a[c];
+  }
+  __syncthreads();
+  if (wv == 0) {
+    double lrow[NM], lcol[NM];
+#pragma unroll
+    for (int k = 0; k < NM; ++k) {
+      lrow[k] = inm ? Lr[i][k] : 0.0;
+      lcol[k] = inm ? Lr[k][i] : 0.0;
+    }
+    const double di = inm ? 1.0 / Lr[i][i] : 0.0;
+    double y = own ? (double)sp[i] : 0.0;
+#pragma unroll
+    for (int j = 0; j < NM; ++j) {
+      if (i == j) y *= di;
+      const double yj = readlane_d(y, j);
+      if (i > j) y = fma(-lrow[j], yj, y);
+    }
+#pragma unroll
+    for (int j = NM - 1; j >= 0; --j) {
+      if (i == j) y *= di;
+      const double xj = readlane_d(y, j);
+      if (i < j) y = fma(-lcol[j], xj, y);
+    }
+    if (inm) xs[i] = own ? y : 0.0;
+  }
+  __syncthreads();
+  // resid2 = t2 - 2 s.x + x.K.x with the fp32 K (no ridge), K from registers
+  double kx = 0.0;
+#pragma unroll
+  for (int c = 0; c < CW; c += 2) {
+    const f64x2 xv = *reinterpret_cast<const f64x2*>(&xs[c0 + c]);
+    kx += (double)kq[c] * xv.x + (double)kq[c + 1] * xv.y;
+  }
+  if (inm) kxp[wv][i] = kx;
+  __syncthreads();
+  if (wv == 0) {
+    double kxi = 0.0;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) kxi += inm ? kxp[v][i] : 0.0;
+    const double x = own ? xs[i] : 0.0;
+    const double q = wave_sum(own ? x * kxi - 2.0 * (double)sp[i] * x : 0.0);
+    if (own) w[(long long)p * n + i] = (float)x;
+    if (i == 0) {
+      lam_eff_out[p] = lam;
+      resid2[p] = (float)((double)t2[p] + q);
+      info[p] = 0;
+    }
+  }
+}
+
 __global__ void empty_group_kernel(const float* t2, int P, float* lam_eff, float* resid2, int32_t* iters, float* kkt,
                                    int32_t* info) {
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
@@ -603,10 +913,10 @@ extern "C" dr_status dr_project_span(const float* K, const float* s, const float
     hipLaunchKernelGGL(span_wave_kernel<16>, dim3(P), dim3(kWaveN), 0, hs, K, s, t2, (int)n, lambda, (int)mode, w,
                        lam_eff, resid2, info);
   else if (n <= 32)
-    hipLaunchKernelGGL(span_wave_kernel<32>, dim3(P), dim3(kWaveN), 0, hs, K, s, t2, (int)n, lambda, (int)mode, w,
+    hipLaunchKernelGGL(span_cols_kernel<32>, dim3(P), dim3(128), 0, hs, K, s, t2, (int)n, lambda, (int)mode, w,
                        lam_eff, resid2, info);
   else if (n <= kWaveN)
-    hipLaunchKernelGGL(span_wave_kernel<64>, dim3(P), dim3(kWaveN), 0, hs, K, s, t2, (int)n, lambda, (int)mode, w,
+    hipLaunchKernelGGL(span_cols_kernel<64>, dim3(P), dim3(256), 0, hs, K, s, t2, (int)n, lambda, (int)mode, w,
                        lam_eff, resid2, info);
   else
     hipLaunchKernelGGL(span_small_kernel, dim3(P), dim3(kSpanThreads), 0, hs, K, s, t2, (int)n, lambda, (int)mode,
@@ -636,10 +946,10 @@ extern "C" dr_status dr_project_cone(const float* K, const float* s, const float
       hipLaunchKernelGGL(cone_wave_kernel<16>, dim3(P), dim3(kWaveN), 0, hs, K, s, t2, (int)n, max_iter, kkt_tol, w,
                          resid2, iters, kkt, info);
     else if (n <= 32)
-      hipLaunchKernelGGL(cone_wave_kernel<32>, dim3(P), dim3(kWaveN), 0, hs, K, s, t2, (int)n, max_iter, kkt_tol, w,
+      hipLaunchKernelGGL(cone_quad_kernel<32>, dim3(P), dim3(256), 0, hs, K, s, t2, (int)n, max_iter, kkt_tol, w,
                          resid2, iters, kkt, info);
     else
-      hipLaunchKernelGGL(cone_wave_kernel<64>, dim3(P), dim3(kWaveN), 0, hs, K, s, t2, (int)n, max_iter, kkt_tol, w,
+      hipLaunchKernelGGL(cone_quad_kernel<64>, dim3(P), dim3(256), 0, hs, K, s, t2, (int)n, max_iter, kkt_tol, w,
                          resid2, iters, kkt, info);
     return launch_status();
   }

@@ -96,6 +96,10 @@ def spd_problem(n, kappa, seed, target_in_span=False):
     (200, 8192, 1e-2, RIDGE_REL_TRACE),
     (256, 16384, 0.0, RIDGE_ABS),           # the Llama-shaped n
     (37, 512, 0.5, RIDGE_ABS),
+    (17, 256, 1e-3, RIDGE_REL_TRACE),       # every small-n kernel: 17..32 and 33..64, padded and full
+    (32, 1024, 0.0, RIDGE_ABS),
+    (48, 2048, 1e-2, RIDGE_REL_TRACE),
+    (63, 4096, 0.0, RIDGE_ABS),
 ])
 def test_span_matches_oracle_and_normal_equations(n, kappa, lam, mode):
     G, gbar, K, s, t2 = spd_problem(n, kappa, 100 + n)
@@ -155,6 +159,30 @@ def test_span_special_cases():
     assert torch.all(info == 0) and torch.equal(resid2.cpu(), torch.tensor([1.0, 2.0]))
 
 
+@pytest.mark.parametrize("n", [12, 20, 32, 40, 64, 100])
+def test_span_bad_pivot_and_batched_groups(n):
+    # group 0: K = diag(1, ..., -1 at j = n - 3, ..., 1) -> info = n - 2 (1-based), w = 0, resid2 = t2;
+    # groups 1, 2: random SPD problems of the same n, each against the oracle
+    j = n - 3
+    d = torch.ones(n, device=DEV)
+    d[j] = -1.0
+    Ks, ss, t2s = [torch.diag(d)], [torch.ones(n, device=DEV)], [torch.full((), 2.0, device=DEV)]
+    for g in (1, 2):
+        _, _, K, s, t2 = spd_problem(n, 2048, 700 + 10 * n + g)
+        Ks.append(K[0]), ss.append(s[0]), t2s.append(t2[0])
+    K, s, t2 = torch.stack(Ks).contiguous(), torch.stack(ss).contiguous(), torch.stack(t2s).contiguous()
+    w, lam_eff, resid2, info = api.project_span(K, s, t2, 1e-3, RIDGE_ABS)
+    torch.cuda.synchronize()
+    assert int(info[0]) == j + 1 and torch.all(w[0] == 0) and float(resid2[0]) == 2.0
+    for g in (1, 2):
+        assert int(info[g]) == 0
+        w_ref, _, info_ref = oracle.span_ref(host64(K[g]), host64(s[g]), 1e-3, RIDGE_ABS)
+        assert info_ref == 0
+        assert rel(host64(w[g]), w_ref) <= TOL_SOLVE
+        r2_ref = oracle.span_residual2(host64(K[g]), host64(s[g]), float(t2[g]), w_ref)
+        assert abs(float(resid2[g]) - r2_ref) <= 1e-5 * float(t2[g])
+
+
 def test_span_batched_groups_and_hand_fixture(golden_dir):
     import json, os
     fx = json.load(open(os.path.join(golden_dir, "span_2x2.json")))
@@ -178,6 +206,8 @@ def test_span_batched_groups_and_hand_fixture(golden_dir):
     (64, 8192, 200, 0.0),       # the small-block workload: 200 projected-gradient steps
     (32, 16384, 100000, 1e-6),  # the long-context workload: run to KKT residual 1e-6
     (16, 1024, 3000, 1e-6),
+    (24, 4096, 400, 0.0),       # padded 17..32 path at a fixed step count
+    (45, 4096, 5000, 1e-6),     # padded 33..64 path to tolerance
     (200, 32768, 20000, 1e-6),  # n > 128: K read from memory each step
     (1, 64, 10, 0.0),
 ])
