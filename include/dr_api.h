@@ -170,7 +170,7 @@ size_t dr_gram_workspace_size(int64_t n, int64_t m, const int64_t* goff, int P, 
  * info = 0; a group with trace(K) = 0 under REL_TRACE returns w = 0.
  * A factor pivot that is not positive sets info = its 1-based index and
  * w = 0.  Arithmetic: fp32 Cholesky factor, iterative refinement with
- * fp64 residuals of the fp32 K.  Supports n <= 256 (else DR_ERR_UNSUPPORTED).
+ * fp64 residuals of the fp32 K.
  * ------------------------------------------------------------------------- */
 dr_status dr_project_span(const float* K, const float* s, const float* t2, int64_t n, int P,
                           float lambda, dr_ridge_mode mode, float* w, float* lam_eff,

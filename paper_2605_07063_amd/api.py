@@ -127,7 +127,11 @@ def dr_gram(G, Gt, goff, K, s, t2, workspace=None, stream=None):
                                  _stream(stream)))
 
 
-def dr_project_span(K, s, t2, lam, mode, w, lam_eff, resid2, info, stream=None):
+def dr_span_workspace_size(n, P):
+    return _lib.load().dr_span_workspace_size(n, P)
+
+
+def dr_project_span(K, s, t2, lam, mode, w, lam_eff, resid2, info, workspace=None, stream=None):
     """(K_p + lam_eff_p I) w_p = s_p per group."""
     lib = _lib.load()
     P = t2.shape[0]
@@ -136,8 +140,10 @@ def dr_project_span(K, s, t2, lam, mode, w, lam_eff, resid2, info, stream=None):
         _dev(t, nm, torch.float32)
         _contig(t, nm)
     _dev(info, "info", torch.int32)
+    nbytes = lib.dr_span_workspace_size(n, P)
+    ws, wsb = _workspace(nbytes, t2.device, workspace)
     check("dr_project_span", lib.dr_project_span(_ptr(K), _ptr(s), _ptr(t2), n, P, float(lam), int(mode), _ptr(w),
-                                                 _ptr(lam_eff), _ptr(resid2), _ptr(info), None, 0,
+                                                 _ptr(lam_eff), _ptr(resid2), _ptr(info), _ptr(ws), wsb,
                                                  _stream(stream)))
 
 

@@ -1,0 +1,662 @@
+// Ridge projection onto the span for large groups (dr_project_span with
+// n > 256, e.g. the Gram-dominated workload's n = 16384): the ridge form of
+// Eq. (proj), Sec. 3.3.1, (K + lam_eff I) w = s, solved by a blocked
+// right-looking Cholesky factorisation in fp32 followed by iterative
+// refinement with fp64 residuals of the exact fp32 K.
+//
+// Workspace (one group at a time; groups run one after another):
+//   L     fp32 [n][ldL]   the factor (lower triangle; the rest is never read)
+//   inv   fp32 [nblk][128][128] and its transpose: the inverse of every
+//         128x128 diagonal block of L (used by the panel solve and by the
+//         two triangular solves)
+//   x, dx, r, z  fp64 [npad] solution, correction, residual, work
+//   ctl   status shared by the kernels of one group (skip / info / lam_eff)
+//
+// Per 128-column panel k:
+//   lg_potrf_kernel  one workgroup factors the diagonal block in registers
+//                    (rows over lanes, 16-column slices over 16 waves, one
+//                    barrier per pivot), then inverts it row by row.
+//   lg_trsm_kernel   L21 = A21 L11^-T as an fp32 MFMA product with the
+//                    inverse, 64 rows per workgroup.
+//   lg_syrk_kernel   A22 -= L21 L21^T on 128x128 lower-triangle tiles, fp32
+//                    MFMA, both panel slices staged in LDS.
+// Solve: L y = r and L^T dx = y block by block (one launch per block and
+// direction; every workgroup applies the block's inverse, then updates its
+// share of the remaining right-hand side), x += dx; three solves (the
+// first and kRefine refinement steps), each refinement preceded by
+// r = s - (K + lam_eff I) x in fp64 read straight from K.
+// Every kernel first reads ctl->skip: once a group's result is decided (a
+// non-finite input, an empty span, a non-positive pivot) the remaining
+// launches of that group return at once.
+
+#include "common.h"
+
+namespace dr {
+namespace {
+
+constexpr int NB = 128;        // panel width
+constexpr int LDP = NB + 4;    // LDS row stride (floats) of staged slices: b128 reads are conflict-free
+constexpr int kRefine = 2;
+constexpr int kPrepBlocks = 2048;
+
+struct LgCtl {
+  int skip;        // the group's result is decided; later kernels return at once
+  int nonfinite;   // some entry of K or s is not finite
+  int info;        // reported info (1-based pivot, or DR_INFO_NONFINITE)
+  float lam;       // lam_eff
+};
+
+struct LgLayout {
+  long long n, ldL, nblk, npad;
+  size_t off_L, off_inv, off_invT, off_x, off_dx, off_r, off_z, off_ctl, total;
+};
+
+LgLayout lg_layout(long long n) {
+  LgLayout l;
+  l.n = n;
+  l.ldL = (long long)align_up((size_t)n, 4);
+  l.nblk = (n + NB - 1) / NB;
+  l.npad = l.nblk * NB;
+  size_t o = 0;
+  l.off_L = o;    o = align_up(o + (size_t)n * l.ldL * 4, 256);
+  l.off_inv = o;  o = align_up(o + (size_t)l.nblk * NB * NB * 4, 256);
+  l.off_invT = o; o = align_up(o + (size_t)l.nblk * NB * NB * 4, 256);
+  l.off_x = o;    o = align_up(o + (size_t)l.npad * 8, 256);
+  l.off_dx = o;   o = align_up(o + (size_t)l.npad * 8, 256);
+  l.off_r = o;    o = align_up(o + (size_t)l.npad * 8, 256);
+  l.off_z = o;    o = align_up(o + (size_t)l.npad * 8, 256);
+  l.off_ctl = o;  o = align_up(o + sizeof(LgCtl), 256);
+  l.total = o;
+  return l;
+}
+
+__device__ __forceinline__ bool finite_f(float v) { return (__float_as_uint(v) & 0x7f800000u) != 0x7f800000u; }
+
+// 1 / sqrt(d), d > 0 normal: hardware estimate plus one Newton step
+__device__ __forceinline__ float rsqrt_nr(float d) {
+  const float r = __builtin_amdgcn_rsqf(d);
+  return r * fmaf(-0.5f * d * r, r, 1.5f);
+}
+
+template <int NT>
+__device__ double block_sum_d(double v, double* sh) {
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+  __syncthreads();
+  double r = 0.0;
+#pragma unroll
+  for (int i = 0; i < NT / 64; ++i) r += sh[i];   // same order in every thread
+  __syncthreads();
+  return r;
+}
+
+// ---------------------------------------------------------------- set-up
+
+__global__ void lg_init_kernel(LgCtl* ctl, const float* s, int n, int npad, double* x, double* dx, double* r,
+                               double* z) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) {
+    ctl->skip = 0;
+    ctl->nonfinite = 0;
+    ctl->info = 0;
+    ctl->lam = 0.f;
+  }
+  if (i < npad) {
+    x[i] = 0.0;
+    dx[i] = 0.0;
+    z[i] = 0.0;
+    r[i] = i < n ? (double)s[i] : 0.0;
+  }
+}
+
+// non-finite check over all n*n entries of K (float4 when 16-byte aligned)
+__global__ __launch_bounds__(256) void lg_prep_kernel(const float* K, long long nn, int vec, LgCtl* ctl) {
+  __shared__ int any;
+  if (threadIdx.x == 0) any = 0;
+  __syncthreads();
+  bool bad = false;
+  const long long stride = (long long)gridDim.x * blockDim.x;
+  long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (vec) {
+    const float4* K4 = reinterpret_cast<const float4*>(K);
+    for (long long q = t; q < nn / 4; q += stride) {
+      const float4 v = K4[q];
+      bad |= !(finite_f(v.x) && finite_f(v.y) && finite_f(v.z) && finite_f(v.w));
+    }
+  } else {
+    for (long long q = t; q < nn; q += stride) bad |= !finite_f(K[q]);
+  }
+  if (bad) any = 1;
+  __syncthreads();
+  if (threadIdx.x == 0 && any) atomicOr(&ctl->nonfinite, 1);
+}
+
+// trace, lam_eff and the early outcomes (non-finite input, empty span)
+__global__ __launch_bounds__(1024) void lg_setup_kernel(const float* K, const float* s, int n, float lambda, int mode,
+                                                        LgCtl* ctl, float* lam_eff_out) {
+  __shared__ double sh[16];
+  __shared__ int sbad;
+  if (threadIdx.x == 0) sbad = 0;
+  __syncthreads();
+  double tr = 0.0;
+  bool bad = false;
+  for (int i = threadIdx.x; i < n; i += 1024) {
+    tr += (double)K[(long long)i * n + i];
+    bad |= !finite_f(s[i]);
+  }
+  if (bad) sbad = 1;
+  tr = block_sum_d<1024>(tr, sh);   // contains a barrier: sbad is visible after it
+  if (threadIdx.x == 0) {
+    const bool nonfinite = ctl->nonfinite != 0 || sbad != 0;
+    const float lam = mode == DR_RIDGE_REL_TRACE ? (float)((double)lambda * tr / (double)n) : lambda;
+    ctl->lam = lam;
+    if (nonfinite) {
+      ctl->skip = 1;
+      ctl->info = DR_INFO_NONFINITE;
+      *lam_eff_out = 0.f;
+    } else {
+      if (mode == DR_RIDGE_REL_TRACE && tr == 0.0) ctl->skip = 1;
+      *lam_eff_out = lam;
+    }
+  }
+}
+
+// L = lower triangle of K + lam_eff I (row i, 4 columns per thread)
+__global__ __launch_bounds__(256) void lg_copy_kernel(const float* K, int n, float* L, long long ldL,
+                                                      const LgCtl* ctl) {
+  if (ctl->skip) return;
+  const int i = blockIdx.x;
+  const int c = (blockIdx.y * 256 + threadIdx.x) * 4;
+  if (c > i) return;
+  const float lam = ctl->lam;
+  const float* kr = K + (long long)i * n;
+  float4 v;
+  v.x = kr[c];
+  v.y = c + 1 < n ? kr[c + 1] : 0.f;
+  v.z = c + 2 < n ? kr[c + 2] : 0.f;
+  v.w = c + 3 < n ? kr[c + 3] : 0.f;
+  if (c == i) v.x += lam;
+  if (c + 1 == i) v.y += lam;
+  if (c + 2 == i) v.z += lam;
+  if (c + 3 == i) v.w += lam;
+  // columns past the diagonal (and past n, up to ldL) are never read
+  *reinterpret_cast<float4*>(L + (long long)i * ldL + c) = v;
+}
+
+// ---------------------------------------------------------------- panel
+
+// Factor and invert the kb x kb diagonal block at (k, k) (kb <= 128; the
+// block is padded to 128 with the identity).  Wave w owns rows
+// 64 (w & 1) .. +64 (one per lane) and columns 16 (w >> 1) .. +16.
+__global__ __launch_bounds__(1024) void lg_potrf_kernel(float* L, long long ldL, int k, int kb, float* inv,
+                                                        float* invT, LgCtl* ctl) {
+  if (ctl->skip) return;
+  __shared__ __attribute__((aligned(16))) float colb[2][NB];
+  __shared__ __attribute__((aligned(16))) float rowb[2][NB];
+  __shared__ float Ls[NB][NB + 1];
+  __shared__ float dinv[NB];      // 1 / L_jj
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int cs = w >> 1;          // column slice
+  const int rlast = 64 * (w & 1) + 63;   // last row of this wave
+  const int i = 64 * (w & 1) + lane;
+  const int c0 = 16 * cs;
+  const bool live = i < kb;
+  float a[16];
+  if (live) {
+    // only chunks that start on or left of the diagonal (they end inside the row)
+    const float4* src = reinterpret_cast<const float4*>(L + (long long)(k + i) * ldL + k + c0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 v = c0 + 4 * q <= i ? src[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+      a[4 * q] = v.x;
+      a[4 * q + 1] = v.y;
+      a[4 * q + 2] = v.z;
+      a[4 * q + 3] = v.w;
+    }
+#pragma unroll
+    for (int c = 0; c < 16; ++c)
+      if (c0 + c > i) a[c] = 0.f;
+  } else {
+#pragma unroll
+    for (int c = 0; c < 16; ++c) a[c] = (c0 + c == i) ? 1.f : 0.f;
+  }
+  if (cs == 0) colb[0][i] = a[0];
+  __syncthreads();
+
+  int bad = 0;
+  for (int jb = 0; jb < NB / 16; ++jb) {
+#pragma unroll
+    for (int jc = 0; jc < 16; ++jc) {
+      const int j = 16 * jb + jc;
+      const float* cb = colb[jc & 1];
+      float d = cb[j];
+      if (!(d > 0.f)) {
+        if (bad == 0) bad = j + 1;
+        d = 1.f;
+      }
+      const float r = rsqrt_nr(d);
+      if (tid == 0) dinv[j] = r;
+      const float lij = i > j ? cb[i] * r : 0.f;
+      const float f = lij * r;
+      if (cs == jb) {
+        a[jc] = i > j ? lij : (i == j ? d * r : 0.f);
+#pragma unroll
+        for (int c = jc + 1; c < 16; ++c) a[c] = fmaf(-f, cb[c0 + c], a[c]);
+        if (jc + 1 < 16) colb[(jc + 1) & 1][i] = a[jc + 1];
+      } else if (cs > jb) {
+        if (rlast > j) {   // rows at or above the pivot have f = 0
+#pragma unroll
+          for (int c = 0; c < 16; c += 4) {
+            const float4 v = *reinterpret_cast<const float4*>(&cb[c0 + c]);
+            a[c] = fmaf(-f, v.x, a[c]);
+            a[c + 1] = fmaf(-f, v.y, a[c + 1]);
+            a[c + 2] = fmaf(-f, v.z, a[c + 2]);
+            a[c + 3] = fmaf(-f, v.w, a[c + 3]);
+          }
+        }
+        if (jc == 15 && cs == jb + 1) colb[0][i] = a[0];
+      }
+      __syncthreads();
+    }
+  }
+  if (bad) {
+    // padded pivots are exactly 1: a failure is always inside the block
+    if (tid == 0) {
+      ctl->info = k + bad;
+      ctl->skip = 1;
+    }
+    return;
+  }
+#pragma unroll
+  for (int c = 0; c < 16; ++c) Ls[i][c0 + c] = a[c];
+  if (live) {
+    float4* dst = reinterpret_cast<float4*>(L + (long long)(k + i) * ldL + k + c0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (c0 + 4 * q <= i) dst[q] = make_float4(a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]);
+    }
+  }
+  __syncthreads();
+
+  // X = L^-1 row by row: X_j = (e_j - sum_{m<j} L_jm X_m) / L_jj, applied
+  // right-looking (once row j is final every later row subtracts L_ij X_j)
+  float xr[16];
+#pragma unroll
+  for (int c = 0; c < 16; ++c) xr[c] = (c0 + c == i) ? 1.f : 0.f;
+  for (int jb = 0; jb < NB / 16; ++jb) {
+#pragma unroll
+    for (int jc = 0; jc < 16; ++jc) {
+      const int j = 16 * jb + jc;
+      if (i == j) {
+        const float dj = dinv[j];
+#pragma unroll
+        for (int c = 0; c < 16; ++c) xr[c] *= dj;
+#pragma unroll
+        for (int c = 0; c < 16; c += 4)
+          *reinterpret_cast<float4*>(&rowb[j & 1][c0 + c]) = make_float4(xr[c], xr[c + 1], xr[c + 2], xr[c + 3]);
+      }
+      __syncthreads();
+      if (rlast > j && i > j) {
+        const float lij = Ls[i][j];
+#pragma unroll
+        for (int c = 0; c < 16; c += 4) {
+          const float4 v = *reinterpret_cast<const float4*>(&rowb[j & 1][c0 + c]);
+          xr[c] = fmaf(-lij, v.x, xr[c]);
+          xr[c + 1] = fmaf(-lij, v.y, xr[c + 1]);
+          xr[c + 2] = fmaf(-lij, v.z, xr[c + 2]);
+          xr[c + 3] = fmaf(-lij, v.w, xr[c + 3]);
+        }
+      }
+    }
+  }
+  float4* drow = reinterpret_cast<float4*>(inv + (long long)i * NB + c0);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) drow[q] = make_float4(xr[4 * q], xr[4 * q + 1], xr[4 * q + 2], xr[4 * q + 3]);
+#pragma unroll
+  for (int c = 0; c < 16; ++c) invT[(long long)(c0 + c) * NB + i] = xr[c];
+}
+
+// L21 = A21 L11^-T: rows k+128+64b .. +64, X[r][c] = sum_m A[r][m] Inv[c][m].
+// 16x16x4 fp32 MFMA; each lane reads a float4 along the reduction of both
+// operands, so the four MFMAs of one 16-wide step take the reduction indices
+// {t, 4+t, 8+t, 12+t} -- the same set for A and B, which is all that matters.
+__global__ __launch_bounds__(256) void lg_trsm_kernel(float* L, long long ldL, int n, int k, const float* inv,
+                                                      const LgCtl* ctl) {
+  if (ctl->skip) return;
+  __shared__ __attribute__((aligned(16))) float As[64][LDP];
+  __shared__ __attribute__((aligned(16))) float Bs[NB][LDP];
+  const int tid = threadIdx.x;
+  const int r0 = k + NB + 64 * blockIdx.x;
+  for (int t = tid; t < 64 * (NB / 4); t += 256) {
+    const int rr = t / (NB / 4), cq = t % (NB / 4);
+    const int row = r0 + rr;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (row < n) v = *reinterpret_cast<const float4*>(L + (long long)row * ldL + k + 4 * cq);
+    *reinterpret_cast<float4*>(&As[rr][4 * cq]) = v;
+  }
+  for (int t = tid; t < NB * (NB / 4); t += 256) {
+    const int rr = t / (NB / 4), cq = t % (NB / 4);
+    *reinterpret_cast<float4*>(&Bs[rr][4 * cq]) = *reinterpret_cast<const float4*>(inv + (long long)rr * NB + 4 * cq);
+  }
+  __syncthreads();
+  const int w = tid >> 6, lane = tid & 63, lr = lane & 15, lq = lane >> 4;
+  f32x4 acc[8];
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
+  for (int kk = 0; kk < NB / 16; ++kk) {
+    const float4 av = *reinterpret_cast<const float4*>(&As[16 * w + lr][16 * kk + 4 * lq]);
+#pragma unroll
+    for (int cb = 0; cb < 8; ++cb) {
+      const float4 bv = *reinterpret_cast<const float4*>(&Bs[16 * cb + lr][16 * kk + 4 * lq]);
+      acc[cb] = mma_f32(av.x, bv.x, acc[cb]);
+      acc[cb] = mma_f32(av.y, bv.y, acc[cb]);
+      acc[cb] = mma_f32(av.z, bv.z, acc[cb]);
+      acc[cb] = mma_f32(av.w, bv.w, acc[cb]);
+    }
+  }
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int row = r0 + 16 * w + 4 * lq + j;
+      if (row < n) L[(long long)row * ldL + k + 16 * cb + lr] = acc[cb][j];
+    }
+  }
+}
+
+__device__ __forceinline__ void tile_pair(int q, int& I, int& J) {
+  int i = (int)((sqrtf(8.f * q + 1.f) - 1.f) * 0.5f);
+  while ((i + 1) * (i + 2) / 2 <= q) ++i;
+  while (i * (i + 1) / 2 > q) --i;
+  I = i;
+  J = q - i * (i + 1) / 2;
+}
+
+// A22 -= L21 L21^T on the lower-triangle 128x128 tiles of the trailing
+// matrix (rows and columns from k1 = k + 128).  Wave (wr, wc) computes the
+// 64x64 sub-tile (wr, wc); on a diagonal tile the strictly upper sub-tile
+// is skipped and only entries on or below the diagonal are written.
+__global__ __launch_bounds__(256) void lg_syrk_kernel(float* L, long long ldL, int n, int k, const LgCtl* ctl) {
+  if (ctl->skip) return;
+  __shared__ __attribute__((aligned(16))) float Ai[NB][LDP];
+  __shared__ __attribute__((aligned(16))) float Aj[NB][LDP];
+  int I, J;
+  tile_pair(blockIdx.x, I, J);
+  const int k1 = k + NB;
+  const int ri = k1 + NB * I, rj = k1 + NB * J;
+  const int tid = threadIdx.x;
+  for (int t = tid; t < NB * (NB / 4); t += 256) {
+    const int rr = t / (NB / 4), cq = t % (NB / 4);
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (ri + rr < n) v = *reinterpret_cast<const float4*>(L + (long long)(ri + rr) * ldL + k + 4 * cq);
+    *reinterpret_cast<float4*>(&Ai[rr][4 * cq]) = v;
+    if (I != J) {
+      float4 u = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (rj + rr < n) u = *reinterpret_cast<const float4*>(L + (long long)(rj + rr) * ldL + k + 4 * cq);
+      *reinterpret_cast<float4*>(&Aj[rr][4 * cq]) = u;
+    }
+  }
+  __syncthreads();
+  const float(*Bp)[LDP] = I != J ? Aj : Ai;
+  const int w = tid >> 6, lane = tid & 63, lr = lane & 15, lq = lane >> 4;
+  const int wr = w & 1, wc = w >> 1;
+  if (I == J && wc > wr) return;
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int kk = 0; kk < NB / 16; ++kk) {
+    float4 av[4], bv[4];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) av[rb] = *reinterpret_cast<const float4*>(&Ai[64 * wr + 16 * rb + lr][16 * kk + 4 * lq]);
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) bv[cb] = *reinterpret_cast<const float4*>(&Bp[64 * wc + 16 * cb + lr][16 * kk + 4 * lq]);
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        acc[rb][cb] = mma_f32(av[rb].x, bv[cb].x, acc[rb][cb]);
+        acc[rb][cb] = mma_f32(av[rb].y, bv[cb].y, acc[rb][cb]);
+        acc[rb][cb] = mma_f32(av[rb].z, bv[cb].z, acc[rb][cb]);
+        acc[rb][cb] = mma_f32(av[rb].w, bv[cb].w, acc[rb][cb]);
+      }
+  }
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = ri + 64 * wr + 16 * rb + 4 * lq + j;
+        const int col = rj + 64 * wc + 16 * cb + lr;
+        if (row < n && col < n && (I != J || col <= row)) L[(long long)row * ldL + col] -= acc[rb][cb][j];
+      }
+}
+
+// ---------------------------------------------------------------- solves
+
+// Forward step for block b of L y = r: y_b = Inv_b r_b (every workgroup
+// forms it; workgroup 0 stores it in y), then r_i -= L[i, block b] . y_b for
+// this workgroup's 128 rows of the trailing part (32 lanes per row, all of
+// a thread's row loads issued before the sums).
+__global__ __launch_bounds__(256) void lg_fwd_kernel(const float* L, long long ldL, int n, int b, const float* invT,
+                                                     double* r, double* y, const LgCtl* ctl) {
+  if (ctl->skip) return;
+  __shared__ double rb[NB], yb[NB], part[NB];
+  const int tid = threadIdx.x;
+  const int o = NB * b;
+  if (tid < NB) rb[tid] = r[o + tid];
+  __syncthreads();
+  {
+    // y_c = sum_m Inv[c][m] r_m = sum_m invT[m][c] r_m (Inv is lower, zeros above):
+    // two threads per c, each half of m
+    const int c = tid & (NB - 1), h = tid >> 7;
+    const float* col = invT + c;
+    double a0 = 0.0, a1 = 0.0;
+#pragma unroll 8
+    for (int m = 64 * h; m < 64 * h + 64; m += 2) {
+      a0 += (double)col[(long long)m * NB] * rb[m];
+      a1 += (double)col[(long long)(m + 1) * NB] * rb[m + 1];
+    }
+    if (h == 1) part[c] = a0 + a1;
+    __syncthreads();
+    if (h == 0) {
+      const double v = (a0 + a1) + part[c];
+      yb[c] = v;
+      if (blockIdx.x == 0) y[o + c] = v;
+    }
+    __syncthreads();
+  }
+  const int g = tid >> 5, l32 = tid & 31;   // 8 rows at a time, 32 lanes each
+  const int base = o + NB + NB * blockIdx.x;
+  const double y0 = yb[4 * l32], y1 = yb[4 * l32 + 1], y2 = yb[4 * l32 + 2], y3 = yb[4 * l32 + 3];
+  float4 v[NB / 8];
+#pragma unroll
+  for (int t = 0; t < NB / 8; ++t) {
+    const int row = base + g + 8 * t;
+    v[t] = row < n ? *reinterpret_cast<const float4*>(L + (long long)row * ldL + o + 4 * l32)
+                   : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+#pragma unroll
+  for (int t = 0; t < NB / 8; ++t) {
+    const int row = base + g + 8 * t;
+    double acc = (double)v[t].x * y0 + (double)v[t].y * y1 + (double)v[t].z * y2 + (double)v[t].w * y3;
+    for (int off = 16; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 32);
+    if (l32 == 0 && row < n) r[row] -= acc;
+  }
+}
+
+// Backward step for block b of L^T x = y: x_b = Inv_b^T y_b (every workgroup
+// forms it; workgroup 0 stores it), then y_m -= sum_{i in block b} L[i][m] x_i
+// for this workgroup's 256 columns m < 128 b.
+__global__ __launch_bounds__(256) void lg_bwd_kernel(const float* L, long long ldL, int n, int b, const float* inv,
+                                                     double* y, double* x, const LgCtl* ctl) {
+  if (ctl->skip) return;
+  __shared__ double zb[NB], xb[NB], part[NB];
+  const int tid = threadIdx.x;
+  const int o = NB * b;
+  if (tid < NB) zb[tid] = y[o + tid];
+  __syncthreads();
+  {
+    // x_c = sum_m Inv[m][c] y_m (zeros above the diagonal): two threads per c
+    const int c = tid & (NB - 1), h = tid >> 7;
+    const float* col = inv + c;
+    double a0 = 0.0, a1 = 0.0;
+#pragma unroll 8
+    for (int m = 64 * h; m < 64 * h + 64; m += 2) {
+      a0 += (double)col[(long long)m * NB] * zb[m];
+      a1 += (double)col[(long long)(m + 1) * NB] * zb[m + 1];
+    }
+    if (h == 1) part[c] = a0 + a1;
+    __syncthreads();
+    if (h == 0) {
+      const double v = (a0 + a1) + part[c];
+      xb[c] = v;
+      if (blockIdx.x == 0) x[o + c] = v;
+    }
+    __syncthreads();
+  }
+  const int m = 256 * blockIdx.x + tid;
+  if (m >= o) return;
+  const int rows = n - o < NB ? n - o : NB;
+  const float* colp = L + (long long)o * ldL + m;
+  double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+  int i = 0;
+  for (; i + 4 <= rows; i += 4) {
+    a0 += (double)colp[(long long)i * ldL] * xb[i];
+    a1 += (double)colp[(long long)(i + 1) * ldL] * xb[i + 1];
+    a2 += (double)colp[(long long)(i + 2) * ldL] * xb[i + 2];
+    a3 += (double)colp[(long long)(i + 3) * ldL] * xb[i + 3];
+  }
+  for (; i < rows; ++i) a0 += (double)colp[(long long)i * ldL] * xb[i];
+  y[m] -= (a0 + a1) + (a2 + a3);
+}
+
+__global__ void lg_axpy_kernel(double* x, const double* dx, int npad, const LgCtl* ctl) {
+  if (ctl->skip) return;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < npad) x[i] += dx[i];
+}
+
+// r = s - (K + lam I) x and kx = K x in fp64, one wave per row of K
+__global__ __launch_bounds__(256) void lg_resid_kernel(const float* K, int n, const float* s, const double* x,
+                                                       double* r, double* kx, const LgCtl* ctl) {
+  if (ctl->skip) return;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= n) return;
+  const float* kr = K + (long long)row * n;
+  double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+  int j = lane;
+  for (; j + 192 < n; j += 256) {
+    a0 += (double)kr[j] * x[j];
+    a1 += (double)kr[j + 64] * x[j + 64];
+    a2 += (double)kr[j + 128] * x[j + 128];
+    a3 += (double)kr[j + 192] * x[j + 192];
+  }
+  for (; j < n; j += 64) a0 += (double)kr[j] * x[j];
+  double acc = (a0 + a1) + (a2 + a3);
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+  if (lane == 0) {
+    r[row] = (double)s[row] - acc - (double)ctl->lam * x[row];
+    if (kx) kx[row] = acc;
+  }
+}
+
+__global__ __launch_bounds__(1024) void lg_final_kernel(const float* s, const float* t2, int n, const double* x,
+                                                        const double* kx, const LgCtl* ctl, float* w, float* resid2,
+                                                        int* info) {
+  __shared__ double sh[16];
+  const bool skip = ctl->skip != 0;
+  double q = 0.0;
+  for (int i = threadIdx.x; i < n; i += 1024) {
+    if (skip) {
+      w[i] = 0.f;
+    } else {
+      w[i] = (float)x[i];
+      q += x[i] * kx[i] - 2.0 * (double)s[i] * x[i];
+    }
+  }
+  q = block_sum_d<1024>(q, sh);
+  if (threadIdx.x == 0) {
+    resid2[0] = skip ? t2[0] : (float)((double)t2[0] + q);
+    info[0] = skip ? ctl->info : 0;
+  }
+}
+
+}  // namespace
+
+size_t span_large_workspace(int64_t n) { return lg_layout(n).total; }
+
+dr_status span_large(const float* K, const float* s, const float* t2, int64_t n64, int P, float lambda, int mode,
+                     float* w, float* lam_eff, float* resid2, int32_t* info, void* ws, size_t ws_bytes,
+                     hipStream_t hs) {
+  const LgLayout lay = lg_layout(n64);
+  if (!ws || ws_bytes < lay.total) return DR_ERR_WORKSPACE;
+  if (!aligned16(ws)) return DR_ERR_ARG;
+  const int n = (int)n64;
+  unsigned char* base = static_cast<unsigned char*>(ws);
+  float* L = reinterpret_cast<float*>(base + lay.off_L);
+  float* inv = reinterpret_cast<float*>(base + lay.off_inv);
+  float* invT = reinterpret_cast<float*>(base + lay.off_invT);
+  double* x = reinterpret_cast<double*>(base + lay.off_x);
+  double* dx = reinterpret_cast<double*>(base + lay.off_dx);
+  double* r = reinterpret_cast<double*>(base + lay.off_r);
+  double* z = reinterpret_cast<double*>(base + lay.off_z);
+  LgCtl* ctl = reinterpret_cast<LgCtl*>(base + lay.off_ctl);
+  const long long ldL = lay.ldL;
+  const int nblk = (int)lay.nblk, npad = (int)lay.npad;
+  const long long nn = (long long)n * n;
+  for (int p = 0; p < P; ++p) {
+    const float* Kp = K + (long long)p * nn;
+    const float* sp = s + (long long)p * n;
+    hipLaunchKernelGGL(lg_init_kernel, dim3((npad + 255) / 256), dim3(256), 0, hs, ctl, sp, n, npad, x, dx, r, z);
+    const int vec = aligned16(Kp) && (nn % 4 == 0);
+    long long want = (nn / (vec ? 4 : 1) + 255) / 256;
+    const int pb = (int)(want < kPrepBlocks ? want : kPrepBlocks);
+    hipLaunchKernelGGL(lg_prep_kernel, dim3(pb), dim3(256), 0, hs, Kp, nn, vec, ctl);
+    hipLaunchKernelGGL(lg_setup_kernel, dim3(1), dim3(1024), 0, hs, Kp, sp, n, lambda, mode, ctl, lam_eff + p);
+    hipLaunchKernelGGL(lg_copy_kernel, dim3(n, (n + 1023) / 1024), dim3(256), 0, hs, Kp, n, L, ldL, ctl);
+    for (int b = 0; b < nblk; ++b) {
+      const int k = NB * b;
+      const int kb = n - k < NB ? n - k : NB;
+      float* ib = inv + (long long)b * NB * NB;
+      float* ibT = invT + (long long)b * NB * NB;
+      hipLaunchKernelGGL(lg_potrf_kernel, dim3(1), dim3(1024), 0, hs, L, ldL, k, kb, ib, ibT, ctl);
+      const int rest = n - k - NB;
+      if (rest > 0) {
+        hipLaunchKernelGGL(lg_trsm_kernel, dim3((rest + 63) / 64), dim3(256), 0, hs, L, ldL, n, k, ib, ctl);
+        const int T = (rest + NB - 1) / NB;
+        hipLaunchKernelGGL(lg_syrk_kernel, dim3(T * (T + 1) / 2), dim3(256), 0, hs, L, ldL, n, k, ctl);
+      }
+    }
+    for (int it = 0; it <= kRefine; ++it) {
+      if (it > 0)
+        hipLaunchKernelGGL(lg_resid_kernel, dim3((n + 3) / 4), dim3(256), 0, hs, Kp, n, sp, x, r, (double*)nullptr,
+                           ctl);
+      // L z = r (r is consumed), then L^T dx = z (z is consumed)
+      for (int b = 0; b < nblk; ++b) {
+        const int rest = n - NB * (b + 1);
+        const int g = rest > 0 ? (rest + NB - 1) / NB : 1;
+        hipLaunchKernelGGL(lg_fwd_kernel, dim3(g), dim3(256), 0, hs, L, ldL, n, b, invT + (long long)b * NB * NB, r,
+                           z, ctl);
+      }
+      for (int b = nblk - 1; b >= 0; --b) {
+        const int g = b > 0 ? (NB * b + 255) / 256 : 1;
+        hipLaunchKernelGGL(lg_bwd_kernel, dim3(g), dim3(256), 0, hs, L, ldL, n, b, inv + (long long)b * NB * NB, z,
+                           dx, ctl);
+      }
+      hipLaunchKernelGGL(lg_axpy_kernel, dim3((npad + 255) / 256), dim3(256), 0, hs, x, dx, npad, ctl);
+    }
+    hipLaunchKernelGGL(lg_resid_kernel, dim3((n + 3) / 4), dim3(256), 0, hs, Kp, n, sp, x, r, z, ctl);
+    hipLaunchKernelGGL(lg_final_kernel, dim3(1), dim3(1024), 0, hs, sp, t2 + p, n, x, z, ctl, w + (long long)p * n,
+                       resid2 + p, info + p);
+    const dr_status st = launch_status();
+    if (st != DR_OK) return st;
+  }
+  return DR_OK;
+}
+
+}  // namespace dr

@@ -27,6 +27,39 @@ __device__ __forceinline__ f32x4 mma_f32(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
+// ---- buffer -> LDS DMA (gfx950): lane l of a wave writes 16 bytes at the
+// wave-uniform LDS address + 16 l; an offset outside the descriptor reads 0.
+
+#define DR_WAIT_VM(n) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory")
+#define DR_LDS_SYNC() asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory")
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+constexpr unsigned kOobOffset = 0xFFFFFFF0u;   // outside every descriptor: reads as zeros
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// aux: cache policy of the load (2 = non-temporal on gfx950)
+template <int AUX>
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, unsigned char* lds_block, unsigned voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds_block, 16, voff, 0, 0, AUX);
+}
+constexpr int kAuxStream = 2;
+constexpr int kAuxCached = 0;
+
+// LDS layout of an operand tile for the bf16 MFMA: 16-row blocks of 2 KB
+// (rows of 128 bytes = 8 segments of 16 bytes), segment seg of row lr stored
+// in slot seg ^ (lr & 7) ^ (lr >> 3): the 16-byte reads of one MFMA operand
+// (16 rows, one segment) are conflict-free, and one wave's DMA fills one
+// 8-row half block (1 KB) with lane l holding row l / 8, slot l % 8.
+__device__ __forceinline__ u32x4 swz_read(const unsigned char* blk, int lr, int seg) {
+  return *reinterpret_cast<const u32x4*>(blk + (lr >> 3) * 1024 + (lr & 7) * 128 + ((seg ^ (lr & 7) ^ (lr >> 3)) * 16));
+}
+// the segment that lane l loads when its wave fills half block h (0 or 1)
+__device__ __forceinline__ int swz_seg_of_lane(int l, int h) { return (l & 7) ^ (l >> 3) ^ h; }
+
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 inline dr_status launch_status() {
@@ -35,5 +68,12 @@ inline dr_status launch_status() {
 }
 
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// blocked Cholesky ridge solve for large groups (chol.hip)
+constexpr int64_t kSpanLargeMaxN = 65536;
+size_t span_large_workspace(int64_t n);
+dr_status span_large(const float* K, const float* s, const float* t2, int64_t n, int P, float lambda, int mode,
+                     float* w, float* lam_eff, float* resid2, int32_t* info, void* ws, size_t ws_bytes,
+                     hipStream_t hs);
 
 }  // namespace dr

@@ -19,6 +19,15 @@
 //   score_kernel       : bf16 sketches only: s_p[i] = <G_p[i], gbar_p> and
 //                        t2_p against the fp32 mean, fp64 accumulation,
 //                        fixed-order block reduction.
+// Large bf16 problems (at least kBigMinTiles 256x256 lower-triangle tiles):
+//   gram_big_kernel    : one 256x256 tile of K_p per workgroup over all of
+//                        the group's columns (no split): 64-column steps
+//                        stream into a two-stage LDS ring by buffer->LDS DMA,
+//                        four waves each hold a 128x128 fp32 accumulator
+//                        (bf16 16x16x32 MFMA); lower-triangle tiles only,
+//                        consecutive tiles kept on one XCD.
+//   gram_mirror_kernel : fills the upper triangle from the lower one
+//                        (64x64 tiles through LDS), so K is exactly symmetric.
 // No atomics: results are deterministic.
 
 #include "common.h"
@@ -162,6 +171,139 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_kernel(GramArgs a) {
         out[(wr * 32 + i * 16 + lg * 4 + r) * kTile + wc * 32 + j * 16 + lr] = acc[i][j][r];
 }
 
+// ---------------------------------------------------------------- large n
+
+constexpr int kBT = 256;                   // output tile edge
+constexpr int kBK = 64;                    // bf16 columns per step (128-byte rows)
+constexpr int kBPanel = kBT * kBK * 2;     // bytes of one operand panel per step (32 KiB)
+constexpr int kBStage = 2 * kBPanel;       // A and B panels
+constexpr int kBigMinTiles = 512;
+
+struct BigArgs {
+  const unsigned char* G;
+  long long ldG;   // elements
+  int n, T, pairs;
+  long long goff[kMaxGroups + 1];
+  float* K;        // [P][n][n] of this launch's groups
+};
+
+__global__ __launch_bounds__(256) void gram_big_kernel(BigArgs a) {
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * kBStage];
+  const int p = blockIdx.y;
+  // workgroup i runs on XCD i % 8: give each XCD a contiguous run of tiles
+  // (same row panel, neighbouring column panels) so they share its L2
+  int q = blockIdx.x;
+  const int full = a.pairs / 8 * 8;
+  if (q < full) q = (q & 7) * (full / 8) + (q >> 3);
+  int I, J;
+  pair_to_tiles(q, I, J);
+  const long long g0 = a.goff[p], g1 = a.goff[p + 1];
+  const int nk = (int)((g1 - g0 + kBK - 1) / kBK);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = w >> 1, wc = w & 1;
+  const int rowA0 = I * kBT, rowB0 = J * kBT;
+  const int rowsA = a.n - rowA0 < kBT ? a.n - rowA0 : kBT;
+  const int rowsB = a.n - rowB0 < kBT ? a.n - rowB0 : kBT;
+  const bool diag = I == J;
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(a.G + (long long)rowA0 * a.ldG * 2, kOobOffset);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.G + (long long)rowB0 * a.ldG * 2, kOobOffset);
+  // this lane's 8 rows of each panel (half blocks w, w + 4, ..., w + 28) and its segment
+  unsigned offA[8], offB[8];
+  int segs[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const int hb = w + 4 * u;             // half block: rows 8 hb .. 8 hb + 7
+    const int r = 8 * hb + (lane >> 3);
+    segs[u] = swz_seg_of_lane(lane, hb & 1);
+    offA[u] = r < rowsA ? (unsigned)((long long)r * a.ldG * 2) : kOobOffset;
+    offB[u] = r < rowsB ? (unsigned)((long long)r * a.ldG * 2) : kOobOffset;
+  }
+  auto issue = [&](int t, int st) {
+    unsigned char* sb = lds + st * kBStage;
+    const long long cbase = g0 + (long long)t * kBK;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const long long col = cbase + segs[u] * 8;
+      const bool cok = col < g1;
+      const unsigned ca = (offA[u] == kOobOffset || !cok) ? kOobOffset : offA[u] + (unsigned)(col * 2);
+      dma16<kAuxCached>(ra, sb + (w + 4 * u) * 1024, ca);
+      if (!diag) {
+        const unsigned cb = (offB[u] == kOobOffset || !cok) ? kOobOffset : offB[u] + (unsigned)(col * 2);
+        dma16<kAuxCached>(rb, sb + kBPanel + (w + 4 * u) * 1024, cb);
+      }
+    }
+  };
+
+  f32x4 acc[8][8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int lr = lane & 15, lg = lane >> 4;
+  if (nk > 0) issue(0, 0);
+  for (int t = 0; t < nk; ++t) {
+    DR_WAIT_VM(0);
+    DR_LDS_SYNC();
+    if (t + 1 < nk) issue(t + 1, (t + 1) & 1);
+    const unsigned char* sa = lds + (t & 1) * kBStage;
+    const unsigned char* sbp = diag ? sa : sa + kBPanel;
+#pragma unroll
+    for (int kh = 0; kh < 2; ++kh) {
+      const int seg = 4 * kh + lg;
+      u32x4 fa[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) fa[i] = swz_read(sa + (wr * 8 + i) * 2048, lr, seg);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const u32x4 fb = swz_read(sbp + (wc * 8 + j) * 2048, lr, seg);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i][j] = mma_bf16(fa[i], fb, acc[i][j]);
+      }
+    }
+  }
+
+  float* Kp = a.K + (long long)p * a.n * a.n;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rowA0 + wr * 128 + 16 * i + 4 * lg + r;
+        const int col = rowB0 + wc * 128 + 16 * j + lr;
+        if (row < a.n && col < a.n && (!diag || col <= row)) Kp[(long long)row * a.n + col] = acc[i][j][r];
+      }
+}
+
+// K[c][r] = K[r][c] for c > r: lower 64x64 tiles through LDS
+__global__ __launch_bounds__(kThreads) void gram_mirror_kernel(float* K, int n) {
+  __shared__ float tile[64][65];
+  int I, J;
+  pair_to_tiles(blockIdx.x, I, J);
+  float* Kp = K + (long long)blockIdx.y * n * n;
+  const int r0 = I * 64, c0 = J * 64;
+  for (int e = threadIdx.x; e < 64 * 64; e += kThreads) {
+    const int rr = e >> 6, cc = e & 63;
+    const int r = r0 + rr, c = c0 + cc;
+    tile[rr][cc] = (r < n && c <= r) ? Kp[(long long)r * n + c] : 0.f;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < 64 * 64; e += kThreads) {
+    const int rr = e >> 6, cc = e & 63;
+    const int orow = c0 + rr, ocol = r0 + cc;   // the mirror of (ocol, orow)
+    if (orow < n && ocol < n && ocol > orow) Kp[(long long)orow * n + ocol] = tile[cc][rr];
+  }
+}
+
+bool gram_use_big(int64_t n, int P, dr_dtype dtype) {
+  if (dtype != DR_BF16 || n < 2 * kBT) return false;
+  const int64_t T = (n + kBT - 1) / kBT;
+  const int gp = P < kMaxGroups ? P : kMaxGroups;
+  return T * (T + 1) / 2 * gp >= kBigMinTiles;
+}
+
 // One thread per element of a 64x64 tile: sums the chunk partials in chunk
 // order and writes K (lower triangle and its mirror) and, for the augmented
 // fp32 problem, s (row n) and t2 (element (n, n)).
@@ -276,7 +418,7 @@ GramPlan gram_plan(int64_t n, const int64_t* goff, int P, dr_dtype dtype) {
   if (g.maxchunks < 1) g.maxchunks = 1;
   g.gbar_bytes = align_up((size_t)(goff[P] > 0 ? goff[P] : 1) * sizeof(float), 256);
   g.partial_bytes = (size_t)gp * g.pairs * g.maxchunks * kTile * kTile * sizeof(float);
-  if (rows == 0) g.partial_bytes = 0;
+  if (rows == 0 || gram_use_big(n, P, dtype)) g.partial_bytes = 0;
   g.rows = rows;
   return g;
 }
@@ -315,6 +457,8 @@ extern "C" dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* 
   using namespace dr;
   dr_status st = gram_validate(G, n, ldG, Gt, m, ldGt, dtype, goff, P, K, s, t2);
   if (st != DR_OK) return st;
+  // the large-n kernel addresses a 256-row panel with 32-bit buffer offsets
+  if (gram_use_big(n, P, dtype) && (uint64_t)ldG * 2 * (kBT + 1) >= (uint64_t)kOobOffset) return DR_ERR_UNSUPPORTED;
   GramPlan g = gram_plan(n, goff, P, dtype);
   if (!workspace || ws_bytes < g.gbar_bytes + g.partial_bytes) return DR_ERR_WORKSPACE;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
@@ -349,7 +493,22 @@ extern "C" dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* 
     a.CK = g.CK;
     a.maxchunks = g.maxchunks;
     a.partial = partial;
-    if (g.rows > 0) {
+    if (gram_use_big(n, P, dtype)) {
+      BigArgs b = {};
+      b.G = static_cast<const unsigned char*>(G);
+      b.ldG = ldG;
+      b.n = (int)n;
+      b.T = (int)((n + kBT - 1) / kBT);
+      b.pairs = b.T * (b.T + 1) / 2;
+      for (int p = 0; p <= gp; ++p) b.goff[p] = goff[p0 + p];
+      b.K = K + (long long)p0 * n * n;
+      hipLaunchKernelGGL(gram_big_kernel, dim3(b.pairs, gp), dim3(256), 0, hs, b);
+      if ((st = launch_status()) != DR_OK) return st;
+      const int T64 = (int)((n + 63) / 64);
+      hipLaunchKernelGGL(gram_mirror_kernel, dim3(T64 * (T64 + 1) / 2, gp), dim3(kThreads), 0, hs,
+                         K + (long long)p0 * n * n, (int)n);
+      if ((st = launch_status()) != DR_OK) return st;
+    } else if (g.rows > 0) {
       dim3 grid(g.maxchunks, g.pairs, gp);
       if (bf)
         hipLaunchKernelGGL(gram_tile_kernel<true>, grid, dim3(kThreads), 0, hs, a);

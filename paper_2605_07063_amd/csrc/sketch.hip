@@ -354,28 +354,6 @@ __global__ __launch_bounds__(kThreads, 2) void sketch_kernel(SketchArgs a) {
 // exactly once per 16-lane phase.  x / dy DMAs are marked non-temporal: each
 // element is read once.
 
-#define DR_WAIT_VM(n) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory")
-#define DR_LDS_SYNC() asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory")
-
-typedef __attribute__((address_space(3))) void lds_void_t;
-
-constexpr unsigned kOobOffset = 0xFFFFFFF0u;   // outside every descriptor: reads as zeros
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
-}
-
-// aux: cache policy of the load (2 = non-temporal on gfx950)
-template <int AUX>
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, unsigned char* lds_block, unsigned voff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds_block, 16, voff, 0, 0, AUX);
-}
-constexpr int kAuxStream = 2;
-
-// 16 bytes of a swizzled 16-row block: row lr, 16-byte segment seg
-__device__ __forceinline__ u32x4 swz_read(const unsigned char* blk, int lr, int seg) {
-  return *reinterpret_cast<const u32x4*>(blk + (lr >> 3) * 1024 + (lr & 7) * 128 + ((seg ^ (lr & 7) ^ (lr >> 3)) * 16));
-}
 
 struct PackArgs {
   LayerArg L[kMaxLayersPerLaunch];

@@ -879,9 +879,9 @@ __global__ void empty_group_kernel(const float* t2, int P, float* lam_eff, float
 }  // namespace dr
 
 extern "C" size_t dr_span_workspace_size(int64_t n, int P) {
-  (void)n;
-  (void)P;
-  return 0;
+  (void)P;   // groups above kSpanMaxN are solved one after another in one workspace
+  if (n <= dr::kSpanMaxN || n > dr::kSpanLargeMaxN) return 0;
+  return dr::span_large_workspace(n);
 }
 
 extern "C" size_t dr_cone_workspace_size(int64_t n, int P) {
@@ -894,16 +894,16 @@ extern "C" dr_status dr_project_span(const float* K, const float* s, const float
                                      dr_ridge_mode mode, float* w, float* lam_eff, float* resid2, int32_t* info,
                                      void* workspace, size_t ws_bytes, void* stream) {
   using namespace dr;
-  (void)workspace;
-  (void)ws_bytes;
   if (n < 0 || P < 0) return DR_ERR_ARG;
   if (mode != DR_RIDGE_ABS && mode != DR_RIDGE_REL_TRACE) return DR_ERR_ARG;
   if (!(lambda >= 0.f) || !(lambda <= 3.4e38f)) return DR_ERR_ARG;
   if (P == 0) return DR_OK;
   if (!t2 || !lam_eff || !resid2 || !info) return DR_ERR_ARG;
   if (n > 0 && (!K || !s || !w)) return DR_ERR_ARG;
-  if (n > kSpanMaxN) return DR_ERR_UNSUPPORTED;
+  if (n > kSpanLargeMaxN) return DR_ERR_UNSUPPORTED;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  if (n > kSpanMaxN)
+    return span_large(K, s, t2, n, P, lambda, (int)mode, w, lam_eff, resid2, info, workspace, ws_bytes, hs);
   if (n == 0) {
     hipLaunchKernelGGL(empty_group_kernel, dim3((P + 255) / 256), dim3(256), 0, hs, t2, P, lam_eff, resid2,
                        (int32_t*)nullptr, (float*)nullptr, info);

@@ -117,7 +117,10 @@ def test_solver_and_select_argument_errors(lib):
     assert span(lam=-1.0) == E.DR_ERR_ARG
     assert span(lam=float("nan")) == E.DR_ERR_ARG
     assert span(mode=5) == E.DR_ERR_ARG
-    assert span(n=257) == E.DR_ERR_UNSUPPORTED
+    assert span(n=257) == E.DR_ERR_WORKSPACE                 # the blocked path needs its workspace
+    assert span(n=65537) == E.DR_ERR_UNSUPPORTED
+    assert lib.dr_span_workspace_size(256, 1) == 0
+    assert lib.dr_span_workspace_size(16384, 3) >= 16384 * 16384 * 4
     assert span(P=0) == E.DR_OK
     cone = lambda n=8, P=1, it=10, tol=0.0: lib.dr_project_cone(FAKE, FAKE, FAKE, n, P, it, tol, FAKE, FAKE, FAKE,
                                                                 FAKE, FAKE, None, 0, None)

@@ -78,6 +78,30 @@ def test_gram_dominated_full_size_sampled():
     assert torch.equal(K[0, :64, 8000:8064], K[0, 8000:8064, :64].T)
 
 
+def test_gram_large_tiles_ragged_groups():
+    """The 256x256-tile path: ragged n (8200 rows), a ragged group width (1000
+    columns), an empty group and a full-width one; sampled rows of each K_p
+    against the oracle, every K_p exactly symmetric."""
+    n, goff = 8200, [0, 1000, 1000, 2600]
+    G = rand((n, 2600), 77, torch.bfloat16)
+    Gt = rand((3, 2600), 78, torch.bfloat16)
+    K, s, t2 = api.gram(G, Gt, goff)
+    torch.cuda.synchronize()
+    pick = [0, 255, 256, 4100, 8191, 8199]
+    Gh, Gth = host64(G), host64(Gt)
+    for p in range(3):
+        c0, c1 = goff[p], goff[p + 1]
+        Kref = Gh[pick, c0:c1] @ Gh[:, c0:c1].T
+        if c1 == c0:
+            assert torch.all(K[p] == 0)
+        else:
+            assert rel(host64(K[p, pick]), Kref) <= TOL_GRAM
+        gbar = Gth[:, c0:c1].mean(0)
+        if c1 > c0:
+            assert rel(host64(s[p]), Gh[:, c0:c1] @ gbar) <= TOL_GRAM
+        assert torch.equal(K[p], K[p].T)
+
+
 # --------------------------------------------------------------------------- span
 
 def spd_problem(n, kappa, seed, target_in_span=False):
@@ -181,6 +205,91 @@ def test_span_bad_pivot_and_batched_groups(n):
         assert rel(host64(w[g]), w_ref) <= TOL_SOLVE
         r2_ref = oracle.span_residual2(host64(K[g]), host64(s[g]), float(t2[g]), w_ref)
         assert abs(float(resid2[g]) - r2_ref) <= 1e-5 * float(t2[g])
+
+
+# ------------------------------------------------------------ span, n > 256 (blocked)
+
+@pytest.mark.parametrize("n,kappa,lam,mode", [
+    (257, 4096, 1e-3, RIDGE_REL_TRACE),     # one full panel + a 1-row panel
+    (300, 256, 1e-2, RIDGE_REL_TRACE),      # rank-deficient G: the ridge carries it
+    (1000, 4096, 0.0, RIDGE_ABS),           # no ridge, full rank
+    (2085, 8192, 0.5, RIDGE_ABS),           # ragged last panel, several trailing tiles
+])
+def test_span_blocked_matches_oracle(n, kappa, lam, mode):
+    G, gbar, K, s, t2 = spd_problem(n, kappa, 900 + n)
+    w, lam_eff, resid2, info = api.project_span(K, s, t2, lam, mode)
+    torch.cuda.synchronize()
+    assert int(info[0]) == 0
+    Kh, sh, t2h = host64(K[0]), host64(s[0]), float(host64(t2)[0])
+    le = float(host64(lam_eff)[0])
+    if mode == RIDGE_REL_TRACE:
+        assert abs(le - lam * np.trace(Kh) / n) <= 1e-6 * le
+    w_ref, _, info_ref = oracle.span_ref(Kh, sh, lam, mode, lam_eff=le)
+    assert info_ref == 0
+    assert rel(host64(w[0]), w_ref) <= TOL_SOLVE, rel(host64(w[0]), w_ref)
+    r2_ref = oracle.span_residual2(Kh, sh, t2h, w_ref)
+    assert abs(float(host64(resid2)[0]) - r2_ref) <= 1e-5 * t2h
+
+
+def test_span_blocked_special_cases():
+    n = 400
+    # a non-positive pivot in the second panel and one in the last row
+    for j in (200, n - 1):
+        d = torch.ones(n, device=DEV)
+        d[j] = -1.0
+        w, _, r2, info = api.project_span(torch.diag(d)[None].contiguous(), torch.ones(1, n, device=DEV),
+                                          torch.full((1,), 5.0, device=DEV), 0.0, RIDGE_ABS)
+        torch.cuda.synchronize()
+        assert int(info[0]) == j + 1 and torch.all(w == 0) and float(r2[0]) == 5.0
+    # a NaN in the upper triangle (the factorisation never reads it; the residual does)
+    G, gbar, K, s, t2 = spd_problem(n, 1024, 31)
+    Kn = K.clone()
+    Kn[0, 3, 300] = float("nan")
+    w, le, r2, info = api.project_span(Kn, s, t2, 1e-3, RIDGE_REL_TRACE)
+    torch.cuda.synchronize()
+    assert int(info[0]) == -3 and torch.all(w == 0) and float(le[0]) == 0.0
+    # relative ridge with K = 0: empty span
+    w, le, r2, info = api.project_span(torch.zeros(1, n, n, device=DEV), torch.zeros(1, n, device=DEV),
+                                       torch.full((1,), 3.0, device=DEV), 1e-2, RIDGE_REL_TRACE)
+    torch.cuda.synchronize()
+    assert int(info[0]) == 0 and torch.all(w == 0) and float(r2[0]) == 3.0
+    # two groups in one call share the workspace one after another; the
+    # target inside the span is reproduced at lam = 0
+    G1, g1, K1, s1, t21 = spd_problem(n, 2048, 41, target_in_span=True)
+    G2, g2, K2, s2, t22 = spd_problem(n, 2048, 42)
+    K = torch.cat([K1, K2]).contiguous()
+    s = torch.cat([s1, s2]).contiguous()
+    t2 = torch.cat([t21, t22]).contiguous()
+    w, le, r2, info = api.project_span(K, s, t2, 0.0, RIDGE_ABS)
+    u1 = api.combine(G1, w[:1].contiguous())
+    torch.cuda.synchronize()
+    assert torch.all(info == 0)
+    assert rel(host64(u1), host64(g1)) <= 1e-4
+    w_ref, _, _ = oracle.span_ref(host64(K2[0]), host64(s2[0]), 0.0, RIDGE_ABS)
+    assert rel(host64(w[1]), w_ref) <= TOL_SOLVE
+
+
+def test_span_gram_dominated_full_size():
+    """n = 16384 from the 16384 x 8192 bf16 rows with a rank-32 spike, relative ridge 1e-2:
+    parity with the fp64 LAPACK oracle and the ridge normal equations G (gbar - G^T w) = lam w."""
+    cfg = workloads.CONFIGS["gram"]
+    rows = workloads.gram_rows(cfg, DEV)
+    G, Gt = rows[:cfg["n"]], rows[cfg["n"]:]
+    K, s, t2 = api.gram(G, Gt)
+    w, lam_eff, resid2, info = api.project_span(K, s, t2, cfg["lam"], RIDGE_REL_TRACE)
+    torch.cuda.synchronize()
+    assert int(info[0]) == 0
+    le = float(lam_eff[0])
+    Kh, sh = host64(K[0]), host64(s[0])
+    w_ref, _, info_ref = oracle.span_ref(Kh, sh, cfg["lam"], RIDGE_REL_TRACE, lam_eff=le)
+    assert info_ref == 0
+    wg = host64(w[0])
+    assert rel(wg, w_ref) <= TOL_SOLVE, rel(wg, w_ref)
+    r2_ref = oracle.span_residual2(Kh, sh, float(t2[0]), w_ref)
+    assert abs(float(resid2[0]) - r2_ref) <= 1e-5 * float(t2[0])
+    # ridge normal equations in the sketch space: K w + lam w = s
+    res = Kh @ wg + le * wg - sh
+    assert np.linalg.norm(res) <= 1e-5 * np.linalg.norm(sh)
 
 
 def test_span_batched_groups_and_hand_fixture(golden_dir):
