@@ -23,9 +23,9 @@
 //   gram_big_kernel    : one 256x256 tile of K_p per workgroup over all of
 //                        the group's columns (no split): 64-column steps
 //                        stream into a two-stage LDS ring by buffer->LDS DMA,
-//                        four waves each hold a 128x128 fp32 accumulator
+//                        eight waves each hold a 128x64 fp32 accumulator
 //                        (bf16 16x16x32 MFMA); lower-triangle tiles only,
-//                        consecutive tiles kept on one XCD.
+//                        scheduled in 4x8-tile chunks, one per XCD at a time.
 //   gram_mirror_kernel : fills the upper triangle from the lower one
 //                        (64x64 tiles through LDS), so K is exactly symmetric.
 // No atomics: results are deterministic.
@@ -187,80 +187,95 @@ struct BigArgs {
   float* K;        // [P][n][n] of this launch's groups
 };
 
-__global__ __launch_bounds__(256) void gram_big_kernel(BigArgs a) {
+__global__ __launch_bounds__(512) void gram_big_kernel(BigArgs a) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * kBStage];
   const int p = blockIdx.y;
-  // workgroup i runs on XCD i % 8: give each XCD a contiguous run of tiles
-  // (same row panel, neighbouring column panels) so they share its L2
-  int q = blockIdx.x;
-  const int full = a.pairs / 8 * 8;
-  if (q < full) q = (q & 7) * (full / 8) + (q >> 3);
+  // Workgroup i runs on XCD i % 8, and an XCD's 32 CUs take its workgroups
+  // in order.  The lower-triangle tiles are grouped in chunks of 4 tile rows
+  // x 8 tile columns (bands of 4 rows, 8 columns at a time); XCD x runs
+  // chunks x, x + 8, ... one whole chunk at a time, so the 32 concurrent
+  // tiles of an XCD read 12 distinct panels through its L2 rather than ~34.
   int I, J;
-  pair_to_tiles(q, I, J);
+  {
+    const int x = blockIdx.x & 7, sl = blockIdx.x >> 3;
+    const int ci = (sl >> 5) * 8 + x, r = sl & 31;
+    int band = 0, acc = 0;
+    for (;; ++band) {
+      if (4 * band >= a.T) return;   // past the last chunk
+      const int rows_end = 4 * band + 4 < a.T ? 4 * band + 4 : a.T;
+      const int nc = (rows_end + 7) / 8;
+      if (ci < acc + nc) break;
+      acc += nc;
+    }
+    I = 4 * band + (r >> 3);
+    J = 8 * (ci - acc) + (r & 7);
+    if (I >= a.T || J > I) return;
+  }
   const long long g0 = a.goff[p], g1 = a.goff[p + 1];
   const int nk = (int)((g1 - g0 + kBK - 1) / kBK);
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wr = w >> 1, wc = w & 1;
+  const int wr = w >> 2, wc = w & 3;   // 128-row half, 64-column quarter of the tile
   const int rowA0 = I * kBT, rowB0 = J * kBT;
   const int rowsA = a.n - rowA0 < kBT ? a.n - rowA0 : kBT;
   const int rowsB = a.n - rowB0 < kBT ? a.n - rowB0 : kBT;
   const bool diag = I == J;
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(a.G + (long long)rowA0 * a.ldG * 2, kOobOffset);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.G + (long long)rowB0 * a.ldG * 2, kOobOffset);
-  // this lane's 8 rows of each panel (half blocks w, w + 4, ..., w + 28) and its segment
-  unsigned offA[8], offB[8];
-  int segs[8];
+  // this lane's 4 rows of each panel (half blocks w, w + 8, w + 16, w + 24) and its segment
+  unsigned offA[4], offB[4];
+  int segs[4];
 #pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const int hb = w + 4 * u;             // half block: rows 8 hb .. 8 hb + 7
+  for (int u = 0; u < 4; ++u) {
+    const int hb = w + 8 * u;             // half block: rows 8 hb .. 8 hb + 7
     const int r = 8 * hb + (lane >> 3);
     segs[u] = swz_seg_of_lane(lane, hb & 1);
     offA[u] = r < rowsA ? (unsigned)((long long)r * a.ldG * 2) : kOobOffset;
     offB[u] = r < rowsB ? (unsigned)((long long)r * a.ldG * 2) : kOobOffset;
   }
+  // straight-line issue (no branches around the loads keeps the accumulators
+  // in place): a diagonal tile loads its panel twice, and the step after the
+  // last one loads zeros (every column is past the group) into the free stage
   auto issue = [&](int t, int st) {
     unsigned char* sb = lds + st * kBStage;
     const long long cbase = g0 + (long long)t * kBK;
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < 4; ++u) {
       const long long col = cbase + segs[u] * 8;
       const bool cok = col < g1;
       const unsigned ca = (offA[u] == kOobOffset || !cok) ? kOobOffset : offA[u] + (unsigned)(col * 2);
-      dma16<kAuxCached>(ra, sb + (w + 4 * u) * 1024, ca);
-      if (!diag) {
-        const unsigned cb = (offB[u] == kOobOffset || !cok) ? kOobOffset : offB[u] + (unsigned)(col * 2);
-        dma16<kAuxCached>(rb, sb + kBPanel + (w + 4 * u) * 1024, cb);
-      }
+      const unsigned cb = (offB[u] == kOobOffset || !cok) ? kOobOffset : offB[u] + (unsigned)(col * 2);
+      dma16<kAuxCached>(ra, sb + (w + 8 * u) * 1024, ca);
+      dma16<kAuxCached>(rb, sb + kBPanel + (w + 8 * u) * 1024, cb);
     }
   };
 
-  f32x4 acc[8][8];
+  f32x4 acc[8][4];
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int lr = lane & 15, lg = lane >> 4;
-  if (nk > 0) issue(0, 0);
+  issue(0, 0);
   for (int t = 0; t < nk; ++t) {
     DR_WAIT_VM(0);
     DR_LDS_SYNC();
-    if (t + 1 < nk) issue(t + 1, (t + 1) & 1);
+    issue(t + 1, (t + 1) & 1);
     const unsigned char* sa = lds + (t & 1) * kBStage;
-    const unsigned char* sbp = diag ? sa : sa + kBPanel;
+    const unsigned char* sbp = sa + kBPanel;
 #pragma unroll
     for (int kh = 0; kh < 2; ++kh) {
       const int seg = 4 * kh + lg;
-      u32x4 fa[8];
+      u32x4 fa[8], fb[4];
 #pragma unroll
       for (int i = 0; i < 8; ++i) fa[i] = swz_read(sa + (wr * 8 + i) * 2048, lr, seg);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const u32x4 fb = swz_read(sbp + (wc * 8 + j) * 2048, lr, seg);
+      for (int j = 0; j < 4; ++j) fb[j] = swz_read(sbp + (wc * 4 + j) * 2048, lr, seg);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) acc[i][j] = mma_bf16(fa[i], fb, acc[i][j]);
-      }
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i][j] = mma_bf16(fa[i], fb[j], acc[i][j]);
     }
   }
 
@@ -268,11 +283,11 @@ __global__ __launch_bounds__(256) void gram_big_kernel(BigArgs a) {
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = rowA0 + wr * 128 + 16 * i + 4 * lg + r;
-        const int col = rowB0 + wc * 128 + 16 * j + lr;
+        const int col = rowB0 + wc * 64 + 16 * j + lr;
         if (row < a.n && col < a.n && (!diag || col <= row)) Kp[(long long)row * a.n + col] = acc[i][j][r];
       }
 }
@@ -502,7 +517,9 @@ extern "C" dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* 
       b.pairs = b.T * (b.T + 1) / 2;
       for (int p = 0; p <= gp; ++p) b.goff[p] = goff[p0 + p];
       b.K = K + (long long)p0 * n * n;
-      hipLaunchKernelGGL(gram_big_kernel, dim3(b.pairs, gp), dim3(256), 0, hs, b);
+      int chunks = 0;
+      for (int band = 0; 4 * band < b.T; ++band) chunks += ((4 * band + 4 < b.T ? 4 * band + 4 : b.T) + 7) / 8;
+      hipLaunchKernelGGL(gram_big_kernel, dim3((chunks + 7) / 8 * 256, gp), dim3(512), 0, hs, b);
       if ((st = launch_status()) != DR_OK) return st;
       const int T64 = (int)((n + 63) / 64);
       hipLaunchKernelGGL(gram_mirror_kernel, dim3(T64 * (T64 + 1) / 2, gp), dim3(kThreads), 0, hs,
