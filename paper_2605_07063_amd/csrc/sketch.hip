@@ -104,7 +104,7 @@ __global__ __launch_bounds__(kThreads, 2) void sketch_kernel(SketchArgs a) {
   constexpr int TI = KIN / 16, TO = KOUT / 16;
   constexpr int PVEC = KP * (ROWB / 16) / kThreads;   // projector vectors per thread per step
   constexpr int LDS_P = 2 * KP * RS;
-  constexpr int LDS_R = 2 * KOUT * KIN * 4;
+  constexpr int LDS_R = kWaves * KOUT * KIN * 4;   // stage-2 partial sums, one region per wave
   constexpr int LDS_BYTES = LDS_P > LDS_R ? LDS_P : LDS_R;
   static_assert(PVEC >= 1 && PVEC * kThreads * 16 == KP * ROWB, "projector staging");
   __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
@@ -355,13 +355,21 @@ __global__ __launch_bounds__(kThreads, 2) void sketch_kernel(SketchArgs a) {
 // element is read once.
 
 
+// The packed positions [0, total) of a layer are split into WL ranges of
+// R positions (R >= 128, computed on the device from total), one range per
+// workgroup, each walked in up to KS tiles of 128 positions.  With WL =
+// ceil(N T / 128) (R = 128, KS = 1) this is one tile per workgroup; for
+// launches too small to fill the chip several times over, WL is chosen so
+// that every workgroup of the launch is resident at once and each streams
+// the same number of tokens, which removes the partly filled last round.
 struct PackArgs {
   LayerArg L[kMaxLayersPerLaunch];
   int num_layers;
   int N, T;
-  int max_tiles;        // tiles per layer for N * T packed positions
-  const int* cum;       // [N + 1] exclusive prefix of the clamped lengths
-  const int* tile_ex;   // [max_tiles] example holding the first position of each tile
+  int WL, KS;           // workgroups per layer, tiles per workgroup (upper bound)
+  int max_tiles;        // WL * KS: tile slots per layer
+  const int* cum;       // [N + 2]: exclusive prefix of the clamped lengths, then R
+  const int* tile_ex;   // [max_tiles] example holding the first position of each tile, -1 if empty
   float* S;
   long long ldS;
   float* partial;       // [num_layers][max_tiles][2][KOUT * KIN]
@@ -369,7 +377,7 @@ struct PackArgs {
 
 // Exclusive prefix of the clamped lengths and the first example of each
 // tile (one workgroup; N is small next to the streamed data).
-__global__ __launch_bounds__(1024) void sketch_plan_kernel(const int* len, int N, int T, int max_tiles, int* cum,
+__global__ __launch_bounds__(1024) void sketch_plan_kernel(const int* len, int N, int T, int WL, int KS, int* cum,
                                                            int* tile_ex) {
   __shared__ int wsum[17];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -403,10 +411,22 @@ __global__ __launch_bounds__(1024) void sketch_plan_kernel(const int* len, int N
     int l = len ? len[i] : T;
     base += l < 0 ? 0 : (l > T ? T : l);
   }
-  if (tid == 0) cum[N] = wsum[16];
+  const int total = wsum[16];
+  const int share = (total + WL - 1) / WL;
+  const int R = share > kTokTile ? share : kTokTile;   // positions per workgroup
+  if (tid == 0) {
+    cum[N] = total;
+    cum[N + 1] = R;
+  }
   __syncthreads();
-  for (int tt = tid; tt < max_tiles; tt += 1024) {
-    const int p = tt * kTokTile;
+  for (int tt = tid; tt < WL * KS; tt += 1024) {
+    const int w = tt / KS, k = tt - w * KS;
+    const int p = w * R + k * kTokTile;
+    const int hi_w = w * R + R < total ? w * R + R : total;
+    if (p >= hi_w) {
+      tile_ex[tt] = -1;
+      continue;
+    }
     int lo = 0, hi = N;   // last e with cum[e] <= p
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
@@ -417,6 +437,15 @@ __global__ __launch_bounds__(1024) void sketch_plan_kernel(const int* len, int N
     }
     tile_ex[tt] = lo;
   }
+}
+
+// two fp32 values -> their bf16 truncations (hi, low half first) and the
+// bf16 truncations of the remainders (lo)
+__device__ __forceinline__ uint2 split_pack(float a, float b) {
+  const unsigned ua = __float_as_uint(a), ub = __float_as_uint(b);
+  const float ra = a - __uint_as_float(ua & 0xffff0000u);
+  const float rb = b - __uint_as_float(ub & 0xffff0000u);
+  return make_uint2((ua >> 16) | (ub & 0xffff0000u), (__float_as_uint(ra) >> 16) | (__float_as_uint(rb) & 0xffff0000u));
 }
 
 template <bool BF16, int KIN, int KOUT>
@@ -432,32 +461,51 @@ __global__ __launch_bounds__(kThreads, 2) void sketch_packed_kernel(PackArgs a) 
   constexpr int NDMA = 2 * NSUB + NPW;      // DMAs per wave per stage
   constexpr int STAGE = (XBLK + PBLK) * 1024;
   constexpr int NST = 3;
-  constexpr int LDS_R = 2 * KOUT * KIN * 4;
-  constexpr int LDS_BYTES = NST * STAGE > LDS_R ? NST * STAGE : LDS_R;
+  constexpr int LDS_R = kWaves * KOUT * KIN * 4;   // stage-2 partial sums, one region per wave
+  // the ring (or the stage-2 partial sums), then the tile's prefix entries
+  constexpr int LDS_MAIN = NST * STAGE > LDS_R ? NST * STAGE : LDS_R;
+  constexpr int LDS_BYTES = LDS_MAIN + 1024;
   __shared__ __attribute__((aligned(1024))) unsigned char lds[LDS_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4, hr = lane >> 3;
-  const int li = blockIdx.x / a.max_tiles;
-  const int tile = blockIdx.x - li * a.max_tiles;
+  const int li = blockIdx.x / a.WL;
+  const int wg = blockIdx.x - li * a.WL;
   const int total = a.cum[a.N];
-  const int p0 = tile * kTokTile;
-  if (p0 >= total) return;
+  const int R = a.cum[a.N + 1];
+  const int r_lo = wg * R;
+  const int r_hi = r_lo + R < total ? r_lo + R : total;
   const LayerArg& L = a.L[li];
-  const int e0 = a.tile_ex[tile];
   const int* cum = a.cum;
+  for (int kt = 0; kt < a.KS; ++kt) {
+  const int p0 = r_lo + kt * kTokTile;
+  const int pend = p0 + kTokTile < r_hi ? p0 + kTokTile : r_hi;   // this tile's positions: [p0, pend)
+  if (p0 >= pend) break;
+  const int tile = wg * a.KS + kt;
+  const int e0 = a.tile_ex[tile];
+  // cum[e0 .. e0 + 128] staged once in LDS.  A tile holds at most 128
+  // non-empty examples; runs of empty ones in between can only push an
+  // example past the staged range, which then reads cum from memory.
+  int* tcum = reinterpret_cast<int*>(lds + LDS_MAIN);   // kTokTile + 1 entries
+  __syncthreads();   // the previous tile is done with tcum and the ring
+  {
+    const int r = tid;
+    if (r <= kTokTile && e0 + r <= a.N) tcum[r] = cum[e0 + r];
+  }
+  __syncthreads();
+  auto cumat = [&](int r) { return r <= kTokTile ? tcum[r] : cum[e0 + r]; };
 
-  // example (relative to e0) and token of a packed position, -1 past the end
+  // example (relative to e0) and token of a packed position, -1 past the tile
   auto locate = [&](int p, int& rel, int& tok) {
-    if (p >= total) {
+    if (p >= pend) {
       rel = -1;
       tok = 0;
       return;
     }
-    int e = e0;
-    while (cum[e + 1] <= p) ++e;
-    rel = e - e0;
-    tok = p - cum[e];
+    int r = 0;
+    while (cumat(r + 1) <= p) ++r;
+    rel = r;
+    tok = p - cumat(r);
   };
   // byte offsets of this lane's DMA rows (rb, half) from the tile's base example
   unsigned offx[2][2], offd[2][2];
@@ -474,7 +522,7 @@ __global__ __launch_bounds__(kThreads, 2) void sketch_packed_kernel(PackArgs a) 
   int e_last;
   {
     int rel, tok;
-    locate((p0 + kTokTile < total ? p0 + kTokTile : total) - 1, rel, tok);
+    locate(pend - 1, rel, tok);
     e_last = e0 + rel;
   }
 
@@ -526,72 +574,114 @@ __global__ __launch_bounds__(kThreads, 2) void sketch_packed_kernel(PackArgs a) 
   issue(0, 0);
   if (nsteps > 1) issue(1, 1);
   int st = 0;
-  for (int s = 0; s < nsteps; ++s) {
-    if (s + 1 < nsteps)
-      DR_WAIT_VM(NDMA);
-    else
-      DR_WAIT_VM(0);
-    DR_LDS_SYNC();
-    if (s + 2 < nsteps) issue(s + 2, st == 0 ? 2 : st - 1);
-    const unsigned char* sb = lds + st * STAGE;
-    // operand (row lr, reduction slice lg of sub-step sub) = segment sub*4 + lg
-    u32x4 xf[2][NSUB];
+  // steps [s0, s1) of one pass accumulate into ACC (Y for x, D for dy); the
+  // two passes are separate loops so each accumulates in place
+  auto pass_steps = [&](int s0, int s1, auto& ACC) {
+    constexpr int NC = sizeof(ACC[0]) / sizeof(f32x4);
+    for (int s = s0; s < s1; ++s) {
+      if (s + 1 < nsteps)
+        DR_WAIT_VM(NDMA);
+      else
+        DR_WAIT_VM(0);
+      DR_LDS_SYNC();
+      if (s + 2 < nsteps) issue(s + 2, st == 0 ? 2 : st - 1);
+      const unsigned char* sb = lds + st * STAGE;
+      // operand (row lr, reduction slice lg of sub-step sub) = segment sub*4 + lg
+      u32x4 xf[2][NSUB];
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
+      for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-      for (int sub = 0; sub < NSUB; ++sub) xf[rb][sub] = swz_read(sb + (wave * 2 + rb) * 2048, lr, sub * 4 + lg);
-    if (s < nsx) {
-#pragma unroll
-      for (int sub = 0; sub < NSUB; ++sub)
-#pragma unroll
-        for (int c = 0; c < TI; ++c) {
-          const u32x4 b = swz_read(sb + (XBLK + 2 * c) * 1024, lr, sub * 4 + lg);
-#pragma unroll
-          for (int rb = 0; rb < 2; ++rb) Y[rb][c] = mma_vec<BF16>(xf[rb][sub], b, Y[rb][c]);
-        }
-    } else {
+        for (int sub = 0; sub < NSUB; ++sub) xf[rb][sub] = swz_read(sb + (wave * 2 + rb) * 2048, lr, sub * 4 + lg);
 #pragma unroll
       for (int sub = 0; sub < NSUB; ++sub)
 #pragma unroll
-        for (int c = 0; c < TO; ++c) {
+        for (int c = 0; c < NC; ++c) {
           const u32x4 b = swz_read(sb + (XBLK + 2 * c) * 1024, lr, sub * 4 + lg);
 #pragma unroll
-          for (int rb = 0; rb < 2; ++rb) D[rb][c] = mma_vec<BF16>(xf[rb][sub], b, D[rb][c]);
+          for (int rb = 0; rb < 2; ++rb) ACC[rb][c] = mma_vec<BF16>(xf[rb][sub], b, ACC[rb][c]);
         }
+      st = st == 2 ? 0 : st + 1;
     }
-    st = st == 2 ? 0 : st + 1;
-  }
+  };
+  pass_steps(0, nsx, Y);
+  pass_steps(nsx, nsteps, D);
   DR_LDS_SYNC();
 
-  // stage 2 once per example of the tile, the other examples' rows masked
+  // stage 2 once per example of the tile, the other examples' rows masked.
+  // Each wave writes its partial sums to its own LDS region one 16-row
+  // block of the output at a time (few live registers), then all threads
+  // add the four regions in the fixed order (w0 + w2) + (w1 + w3).
   float* red = reinterpret_cast<float*>(lds);
   constexpr int SW = KOUT * KIN;
   // packed position of the first row this lane holds in the MFMA outputs
   // (rows rbase + rb*16 + j, j < 4)
   const int rbase = p0 + wave * kTokWave + lg * 4;
+  const int wlo = p0 + wave * kTokWave, whi = wlo + kTokWave;   // this wave's rows
+  // bf16 sketches: each fp32 stage-1 output v is split as hi + lo with hi =
+  // v truncated to bf16 and lo = (v - hi) truncated to bf16, and
+  // sum_t D Y ~ Dh Yh + Dh Yl + Dl Yh (relative error about 3 * 2^-16 per
+  // product).  One 16x16x32 bf16 MFMA then covers the wave's 32 rows: lane
+  // group g holds rows {4g + j, 16 + 4g + j}, which become the 8 consecutive
+  // reduction indices of its operand, for D and Y alike.
+  u32x4 Dh[TO], Dl[TO];
+  if constexpr (BF16) {
+#pragma unroll
+    for (int o = 0; o < TO; ++o) {
+      { const uint2 s_ = split_pack(D[0][o][0], D[0][o][1]); Dh[o].x = s_.x; Dl[o].x = s_.y; }
+      { const uint2 s_ = split_pack(D[0][o][2], D[0][o][3]); Dh[o].y = s_.x; Dl[o].y = s_.y; }
+      { const uint2 s_ = split_pack(D[1][o][0], D[1][o][1]); Dh[o].z = s_.x; Dl[o].z = s_.y; }
+      { const uint2 s_ = split_pack(D[1][o][2], D[1][o][3]); Dh[o].w = s_.x; Dl[o].w = s_.y; }
+    }
+  }
   for (int e = e0; e <= e_last; ++e) {
-    const int ce = cum[e], ce1 = cum[e + 1];
+    const int ce = cumat(e - e0), ce1 = cumat(e - e0 + 1);
     if (ce1 == ce) continue;   // empty examples are written by the reduction kernel
-    f32x4 Sacc[TO][TI];
+    const bool all_e = ce <= wlo && ce1 >= whi;   // every row of the wave belongs to e
+    const bool some_e = ce < whi && ce1 > wlo;
+    if constexpr (BF16) {
+      u32x4 Yh[TI], Yl[TI];
 #pragma unroll
-    for (int o = 0; o < TO; ++o)
+      for (int i = 0; i < TI; ++i) {
+        float y[2][4];
 #pragma unroll
-      for (int i = 0; i < TI; ++i) Sacc[o][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int wlo = p0 + wave * kTokWave, whi = wlo + kTokWave;   // this wave's rows
-    if (ce <= wlo && ce1 >= whi) {
-      // every row of the wave belongs to e
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int pr = rbase + rb * 16 + j;
+            y[rb][j] = (all_e || (pr >= ce && pr < ce1)) ? Y[rb][i][j] : 0.f;
+          }
+        { const uint2 s_ = split_pack(y[0][0], y[0][1]); Yh[i].x = s_.x; Yl[i].x = s_.y; }
+        { const uint2 s_ = split_pack(y[0][2], y[0][3]); Yh[i].y = s_.x; Yl[i].y = s_.y; }
+        { const uint2 s_ = split_pack(y[1][0], y[1][1]); Yh[i].z = s_.x; Yl[i].z = s_.y; }
+        { const uint2 s_ = split_pack(y[1][2], y[1][3]); Yh[i].w = s_.x; Yl[i].w = s_.y; }
+      }
 #pragma unroll
       for (int o = 0; o < TO; ++o)
+#pragma unroll
+        for (int i = 0; i < TI; ++i) {
+          f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+          if (some_e) {
+            acc = mma_bf16(Dh[o], Yh[i], acc);
+            acc = mma_bf16(Dh[o], Yl[i], acc);
+            acc = mma_bf16(Dl[o], Yh[i], acc);
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) red[wave * SW + ((o * TI + i) * 4 + q) * 64 + lane] = acc[q];
+        }
+    } else {
+#pragma unroll
+    for (int o = 0; o < TO; ++o) {
+      f32x4 Sacc[TI];
+#pragma unroll
+      for (int i = 0; i < TI; ++i) Sacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (all_e) {
 #pragma unroll
         for (int i = 0; i < TI; ++i)
 #pragma unroll
           for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) Sacc[o][i] = mma_f32(D[rb][o][j], Y[rb][i][j], Sacc[o][i]);
-    } else if (ce < whi && ce1 > wlo) {
-      // rows of other examples are masked out of Y
-#pragma unroll
-      for (int o = 0; o < TO; ++o)
+            for (int j = 0; j < 4; ++j) Sacc[i] = mma_f32(D[rb][o][j], Y[rb][i][j], Sacc[i]);
+      } else if (some_e) {
 #pragma unroll
         for (int i = 0; i < TI; ++i)
 #pragma unroll
@@ -599,46 +689,29 @@ __global__ __launch_bounds__(kThreads, 2) void sketch_packed_kernel(PackArgs a) 
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
               const int pr = rbase + rb * 16 + j;
-              Sacc[o][i] = mma_f32(D[rb][o][j], (pr >= ce && pr < ce1) ? Y[rb][i][j] : 0.f, Sacc[o][i]);
+              Sacc[i] = mma_f32(D[rb][o][j], (pr >= ce && pr < ce1) ? Y[rb][i][j] : 0.f, Sacc[i]);
             }
+      }
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) red[wave * SW + ((o * TI + i) * 4 + q) * 64 + lane] = Sacc[i][q];
     }
-    // (w0 + w2) + (w1 + w3) through LDS, in a fixed order
-    auto put = [&](int region) {
-#pragma unroll
-      for (int o = 0; o < TO; ++o)
-#pragma unroll
-        for (int i = 0; i < TI; ++i)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) red[region * SW + ((o * TI + i) * 4 + q) * 64 + lane] = Sacc[o][i][q];
-    };
-    auto add = [&](int region) {
-#pragma unroll
-      for (int o = 0; o < TO; ++o)
-#pragma unroll
-        for (int i = 0; i < TI; ++i)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) Sacc[o][i][q] += red[region * SW + ((o * TI + i) * 4 + q) * 64 + lane];
-    };
-    if (wave >= 2) put(wave - 2);
+    }
     DR_LDS_SYNC();
-    if (wave < 2) add(wave);
-    DR_LDS_SYNC();
-    if (wave == 1) put(0);
-    DR_LDS_SYNC();
-    if (wave == 0) {
-      add(0);
-      const bool inside = ce >= p0 && ce1 <= p0 + kTokTile;
-      float* out = inside ? a.S + (long long)e * a.ldS + L.col_offset
-                          : a.partial + (((long long)li * a.max_tiles + tile) * 2 + (e == e0 ? 0 : 1)) * SW;
-#pragma unroll
-      for (int o = 0; o < TO; ++o)
-#pragma unroll
-        for (int i = 0; i < TI; ++i)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) out[(o * 16 + lg * 4 + q) * KIN + i * 16 + lr] = Sacc[o][i][q];
+    const bool inside = ce >= p0 && ce1 <= pend;
+    float* out = inside ? a.S + (long long)e * a.ldS + L.col_offset
+                        : a.partial + (((long long)li * a.max_tiles + tile) * 2 + (e == e0 ? 0 : 1)) * SW;
+    for (int k = tid; k < SW; k += kThreads) {
+      const float v = (red[k] + red[2 * SW + k]) + (red[SW + k] + red[3 * SW + k]);
+      const int l = k & 63, oiq = k >> 6;           // (o * TI + i) * 4 + q
+      const int q = oiq & 3, oi = oiq >> 2;
+      const int o = oi / TI, i = oi - o * TI;
+      out[(o * 16 + (l >> 4) * 4 + q) * KIN + i * 16 + (l & 15)] = v;
     }
     DR_LDS_SYNC();
   }
+  }   // tiles of this workgroup
 }
 
 // Examples spread over several tiles: sum their per-tile partials in tile
@@ -654,7 +727,10 @@ __global__ __launch_bounds__(kThreads) void sketch_packed_reduce_kernel(PackArgs
   const int pair = blockIdx.x / kReduceSplit;
   const int li = pair / a.N, e = pair % a.N;
   const int ce = a.cum[e], ce1 = a.cum[e + 1];
-  const int t0 = ce / kTokTile, t1 = (ce1 - 1) / kTokTile;
+  const int R = a.cum[a.N + 1];
+  // tile slot of a position: workgroup p / R, tile (p mod R) / 128 within it
+  const int t0 = (ce / R) * a.KS + (ce % R) / kTokTile;
+  const int t1 = ((ce1 - 1) / R) * a.KS + ((ce1 - 1) % R) / kTokTile;
   if (ce1 > ce && t0 == t1) return;   // written by its only tile
   float* out = a.S + (long long)e * a.ldS + a.L[li].col_offset;
 #pragma unroll
@@ -664,6 +740,7 @@ __global__ __launch_bounds__(kThreads) void sketch_packed_reduce_kernel(PackArgs
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
     if (ce1 > ce) {
       for (int tt = t0; tt <= t1; ++tt) {
+        if (a.tile_ex[tt] < 0) continue;   // slot past the end of a workgroup's range
         const int slot = a.tile_ex[tt] == e ? 0 : 1;
         acc += reinterpret_cast<const f32x4*>(a.partial + (((long long)li * a.max_tiles + tt) * 2 + slot) *
                                                               (KOUT * KIN))[e4];
@@ -733,9 +810,18 @@ struct Launch {
 
 struct Plan {
   int nlaunch;
-  int max_tiles;
+  int WL, KS, max_tiles;
   size_t off_cum, off_tiles, off_partial, bytes;
 };
+
+// resident packed workgroups per CU (LDS-bound) times the CU count
+int resident_slots() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                              hipSuccess || cus < 1)
+    cus = 256;
+  return 2 * cus;
+}
 
 int64_t packed_tiles(int64_t N, int64_t T) { return (N * T + kTokTile - 1) / kTokTile; }
 
@@ -757,6 +843,31 @@ Plan plan(const dr_layer* layers, int num_layers, int64_t N, int64_t T, dr_dtype
   size_t need = 0;
   bool any_packed = false;
   const int64_t mt = packed_tiles(N, T);
+  // balanced ranges when the largest packed launch has at most 8 tiles per
+  // resident workgroup slot (else one tile per workgroup)
+  int lmax = 0;
+  for (int i0 = 0; i0 < num_layers;) {
+    int j0 = i0 + 1;
+    while (j0 < num_layers && j0 - i0 < kMaxLayersPerLaunch && layers[j0].k_in == layers[i0].k_in &&
+           layers[j0].k_out == layers[i0].k_out)
+      ++j0;
+    if (packed_ok(layers, i0, j0 - i0, N, T, dtype) && j0 - i0 > lmax) lmax = j0 - i0;
+    i0 = j0;
+  }
+  int64_t WL = mt, KS = 1;
+  if (lmax > 0 && mt > 0) {
+    const int64_t slots = resident_slots();
+    if ((int64_t)lmax * mt <= 8 * slots) {
+      WL = slots / lmax;
+      if (WL < 1) WL = 1;
+      if (WL > mt) WL = mt;
+      const int64_t share = (N * T + WL - 1) / WL;   // upper bound of R
+      KS = (share + kTokTile - 1) / kTokTile;
+    }
+  }
+  pl.WL = (int)WL;
+  pl.KS = (int)KS;
+  const int64_t slots_per_layer = WL * KS;
   int i = 0;
   while (i < num_layers) {
     int j = i + 1;
@@ -773,7 +884,7 @@ Plan plan(const dr_layer* layers, int num_layers, int64_t N, int64_t T, dr_dtype
       any_packed = true;
       l.chunk = kTokTile;
       l.nchunks = 1;
-      const size_t b = (size_t)l.count * mt * 2 * l.kin * l.kout * sizeof(float);
+      const size_t b = (size_t)l.count * slots_per_layer * 2 * l.kin * l.kout * sizeof(float);
       if (b > need) need = b;
     } else {
       int64_t tiles = (T + kTokTile - 1) / kTokTile;
@@ -792,11 +903,11 @@ Plan plan(const dr_layer* layers, int num_layers, int64_t N, int64_t T, dr_dtype
     ++pl.nlaunch;
     i = j;
   }
-  pl.max_tiles = (int)mt;
+  pl.max_tiles = (int)slots_per_layer;
   if (any_packed) {
     pl.off_cum = 0;
-    pl.off_tiles = align_up((size_t)(N + 1) * sizeof(int), 256);
-    pl.off_partial = pl.off_tiles + align_up((size_t)(mt > 0 ? mt : 1) * sizeof(int), 256);
+    pl.off_tiles = align_up((size_t)(N + 2) * sizeof(int), 256);
+    pl.off_partial = pl.off_tiles + align_up((size_t)(slots_per_layer > 0 ? slots_per_layer : 1) * sizeof(int), 256);
   } else {
     pl.off_cum = pl.off_tiles = pl.off_partial = 0;
   }
@@ -808,8 +919,7 @@ template <bool BF16, int KIN, int KOUT>
 void launch_t(const Launch& l, const SketchArgs& a, const PackArgs& pa, hipStream_t st) {
   if (l.packed) {
     if (pa.max_tiles > 0)
-      hipLaunchKernelGGL((sketch_packed_kernel<BF16, KIN, KOUT>), dim3(l.count * pa.max_tiles), dim3(kThreads), 0, st,
-                         pa);
+      hipLaunchKernelGGL((sketch_packed_kernel<BF16, KIN, KOUT>), dim3(l.count * pa.WL), dim3(kThreads), 0, st, pa);
     hipLaunchKernelGGL((sketch_packed_reduce_kernel<KIN, KOUT>), dim3(l.count * pa.N * kReduceSplit), dim3(kThreads),
                        0, st, pa);
     return;
@@ -911,12 +1021,14 @@ extern "C" dr_status dr_sketch_grads(const dr_layer* layers, int num_layers, int
     a.ldS = pa.ldS = ldS;
     a.partial = reinterpret_cast<float*>(ws);
     if (l.packed) {
+      pa.WL = pl.WL;
+      pa.KS = pl.KS;
       pa.max_tiles = pl.max_tiles;
       pa.cum = reinterpret_cast<const int*>(ws + pl.off_cum);
       pa.tile_ex = reinterpret_cast<const int*>(ws + pl.off_tiles);
       pa.partial = reinterpret_cast<float*>(ws + pl.off_partial);
       if (!planned) {
-        hipLaunchKernelGGL(sketch_plan_kernel, dim3(1), dim3(1024), 0, hs, len, (int)N, (int)T, pl.max_tiles,
+        hipLaunchKernelGGL(sketch_plan_kernel, dim3(1), dim3(1024), 0, hs, len, (int)N, (int)T, pl.WL, pl.KS,
                            reinterpret_cast<int*>(ws + pl.off_cum), reinterpret_cast<int*>(ws + pl.off_tiles));
         if ((st = launch_status()) != DR_OK) break;
         planned = true;
