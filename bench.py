@@ -36,11 +36,17 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle's sketch sample")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run three 1 GiB device-to-device copies first (known bytes, to scale HBM counters)")
+    ap.add_argument("--summarize-profiles", nargs=3, metavar=("KT_DIR", "FETCH_DIR", "WRITE_DIR"),
+                    help="write the profiles/ summaries from the csv output of a rocprofv3 kernel-trace run "
+                         "and the FETCH_SIZE / WRITE_SIZE counter runs of this script (no GPU needed)")
     return ap.parse_args()
 
 
 def main():
     args = parse()
+    if args.summarize_profiles:
+        summarize_profiles(*args.summarize_profiles)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
               "(the per-GPU share is the single-GPU workload; see the design notes on sharding)",
@@ -207,20 +213,124 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+SKETCH_SOURCES = ["paper_2605_07063_amd/csrc/sketch.hip", "paper_2605_07063_amd/csrc/common.h"]
+SKETCH_KERNELS = ("sketch_plan_kernel", "sketch_packed_kernel", "sketch_packed_reduce_kernel")
+KT_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_kt -o small -- "
+          "python -u bench.py --steps 50 --warmup 10 --no-cpu-baseline")
+PMC_CMD = ("rocprofv3 --pmc {c} --output-format csv -d gpurun_out/prof_{d} -o small -- "
+           "python -u bench.py --steps 5 --warmup 2 --no-cpu-baseline --copy-calibration")
+SUM_CMD = "python bench.py --summarize-profiles gpurun_out/prof_kt gpurun_out/prof_fetch gpurun_out/prof_write"
+
+
+def sketch_sources_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in SKETCH_SOURCES:
+        h.update(open(os.path.join(ROOT, rel), "rb").read())
+    return h.hexdigest()
+
+
 def measured_traffic():
     """HBM bytes per sketch call from the committed rocprofv3 FETCH_SIZE /
     WRITE_SIZE passes (scaled by a known-size copy), or None when the kernel
-    source has changed since those counters were taken."""
-    import hashlib
+    sources have changed since those counters were taken."""
     path = os.path.join(ROOT, "profiles", "sketch_small_block_traffic.json")
     try:
         rec = json.load(open(path))
-        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+        sha = sketch_sources_sha()
     except (OSError, ValueError, KeyError):
         return None
-    if hashlib.sha256(src).hexdigest() != rec.get("source_sha256"):
+    if sha != rec.get("sources_sha256"):
         return None
     return rec["traffic_bytes_per_call"]
+
+
+def _short_name(name):
+    import re
+    n = re.sub(r"\(anonymous namespace\)::", "", name).replace("dr::", "")
+    if n.startswith("void "):
+        n = n[5:]
+    return n.split("(")[0].strip()
+
+
+def summarize_profiles(kt_dir, fetch_dir, write_dir):
+    """profiles/ summaries (kernel trace, HBM traffic, the traffic record
+    bench.py reads) from rocprofv3 csv output of this script's commands."""
+    import csv
+    import glob
+
+    def one(pattern, d):
+        f = sorted(glob.glob(os.path.join(d, "**", pattern), recursive=True))
+        if not f:
+            raise SystemExit(f"no {pattern} under {d}")
+        return f[0]
+
+    stats = list(csv.DictReader(open(one("*_kernel_stats.csv", kt_dir))))
+    tot = sum(float(r["TotalDurationNs"]) for r in stats)
+    rows, sk_avg = [], 0.0
+    for r in stats:
+        nm = _short_name(r["Name"])
+        ours = not r["Name"].startswith(("void at::", "at::", "__amd"))
+        if nm.startswith(SKETCH_KERNELS):
+            sk_avg += float(r["AverageNs"]) / 1e3
+        rows.append(f"| `{nm}`{'' if ours else ' (input generation, untimed)'} | {int(r['Calls'])} | "
+                    f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+                    f"{float(r['MaxNs']) / 1e3:.2f} | {100 * float(r['TotalDurationNs']) / tot:.1f}% |")
+    kt = ["# Kernel trace: small-block workload, bench step", "",
+          "Command (repository root on the GPU box, `TMPDIR=/tmp`), summarised by", "",
+          "```", KT_CMD, SUM_CMD, "```", "",
+          "60 calls per kernel of the step = 10 warmup + 50 timed steps. Durations in microseconds.", "",
+          "| Kernel | Calls | Avg (us) | Min | Max | Share |", "|---|---|---|---|---|---|"] + rows + [
+          "", f"The sketch call (`dr_sketch_grads`) = {' + '.join(SKETCH_KERNELS)} = **{sk_avg:.1f} us** per call "
+          "(average kernel durations; bench.py's HIP-event time of the same call also spans the launch gaps)."]
+    open(os.path.join(ROOT, "profiles", "small_block_kernel_trace.md"), "w").write("\n".join(kt) + "\n")
+
+    def counters(d, cname):
+        recs = list(csv.DictReader(open(one("*_counter_collection.csv", d))))
+        per = {}
+        for r in recs:
+            if r["Counter_Name"] != cname:
+                continue
+            per.setdefault(_short_name(r["Kernel_Name"]), []).append(float(r["Counter_Value"]))
+        return per
+
+    fetch, write = counters(fetch_dir, "FETCH_SIZE"), counters(write_dir, "WRITE_SIZE")
+    copy = "rocclr_copyBuffer"
+    ck = [k for k in fetch if copy in k]
+    # three 1 GiB copies: each reads and writes 1,048,576 KiB
+    f_cal = max(fetch[ck[0]]) if ck else None
+    w_cal = max(write[[k for k in write if copy in k][0]]) if ck else None
+    ffac = 1048576.0 / f_cal if f_cal else 1.0
+    wfac = 1048576.0 / w_cal if w_cal else 1.0
+    lines, sk_bytes = [], 0.0
+    for k in fetch:
+        if copy in k or k.startswith(("at::", "void at::")):
+            continue
+        fa = sum(fetch[k]) / len(fetch[k])
+        wa = sum(write.get(k, [0.0])) / max(1, len(write.get(k, [0.0])))
+        lines.append(f"| `{k}` | {len(fetch[k])} | {fa:,.1f} | {fa * ffac * 1024 / 1e6:,.1f} MB | {wa:,.1f} | "
+                     f"{wa * wfac * 1024 / 1e6:,.1f} MB |")
+        if k.startswith(SKETCH_KERNELS):
+            sk_bytes += (fa * ffac + wa * wfac) * 1024
+    tr = ["# HBM traffic: small-block workload, bench step", "",
+          "Two counter passes, each in its own run (`TMPDIR=/tmp`), summarised by the last command:", "", "```",
+          PMC_CMD.format(c="FETCH_SIZE", d="fetch"), PMC_CMD.format(c="WRITE_SIZE", d="write"), SUM_CMD, "```", "",
+          "Calibration: `--copy-calibration` makes three 1 GiB device-to-device copies (1,048,576 KiB read and "
+          "written).",
+          f"- FETCH_SIZE reads {f_cal:,.1f} KiB for such a copy: scale factor **{ffac:.4f}**." if f_cal else
+          "- no copy kernel found: FETCH_SIZE unscaled.",
+          f"- WRITE_SIZE reads {w_cal:,.1f} KiB: scale factor **{wfac:.4f}**." if w_cal else
+          "- no copy kernel found: WRITE_SIZE unscaled.", "",
+          "| Kernel | dispatches | FETCH_SIZE (KiB, raw avg) | fetched (scaled) | WRITE_SIZE (KiB avg) | "
+          "written (scaled) |", "|---|---|---|---|---|---|"] + lines + [
+          "", f"Sketch call total (plan + packed + reduce kernels): **{sk_bytes / 1e9:.4f} GB** of HBM traffic "
+          "per call."]
+    open(os.path.join(ROOT, "profiles", "small_block_hbm_traffic.md"), "w").write("\n".join(tr) + "\n")
+    rec = {"kernel": "dr_sketch_grads", "workload": "small-block", "sources": SKETCH_SOURCES,
+           "sources_sha256": sketch_sources_sha(), "traffic_bytes_per_call": sk_bytes,
+           "fetch_factor": ffac, "write_factor": wfac}
+    json.dump(rec, open(os.path.join(ROOT, "profiles", "sketch_small_block_traffic.json"), "w"), indent=1)
+    print(f"sketch call {sk_avg:.1f} us, {sk_bytes / 1e9:.4f} GB per call")
 
 
 def cpu_baseline(layers, lens, S, K, s, t2, n, m, k_top, lam, cfg, budget_s):

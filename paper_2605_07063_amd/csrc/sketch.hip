@@ -6,15 +6,19 @@
 // second-stage projector).  G_i is never formed: per token tile
 //   stage 1:  Y = X P_in^T  [tokens x k_in],  D = dY P_out^T  [tokens x k_out]
 //             (bf16 or fp32 MFMA, fp32 accumulate, contraction over d)
-//   stage 2:  S += D^T Y    [k_out x k_in]  (fp32 MFMA, contraction over tokens)
+//   stage 2:  S += D^T Y    [k_out x k_in]  (contraction over tokens)
 // The stage-1 accumulators feed stage 2 straight from registers: the MFMA
 // output layout (token 4*(l/16)+j, column l%16 in register j) is exactly the
 // fp32-MFMA operand layout once token 4*(l/16)+j is read as the reduction
-// index l/16 of the j-th product.
+// index l/16 of the j-th product.  On the bf16 path stage 2 instead runs
+// as three bf16 MFMAs on hi/lo bf16 splits of D and Y (Dh Yh + Dh Yl +
+// Dl Yh), one MFMA per 32 rows.
 //
 // Two kernels do the work.  sketch_packed_kernel (below) is the main path:
-// the valid tokens are packed into full 128-token tiles and streamed
-// HBM -> LDS by DMA through a three-stage ring.  sketch_kernel, the general
+// the valid tokens are packed into 128-token tiles and streamed HBM -> LDS
+// by DMA through a three-stage ring; a workgroup walks a range of tiles
+// (one tile, or an equal share of the layer's tokens when the launch is too
+// small to fill the chip many times over).  sketch_kernel, the general
 // fallback (d not a whole number of 64-element steps, or offsets beyond
 // 32 bits), works on (layer, example, chunk of tokens) units: a 256-thread
 // workgroup owns one unit and walks it in 128-token tiles, each of its four

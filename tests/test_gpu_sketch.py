@@ -139,6 +139,25 @@ def test_long_context_full_size_sampled():
     print(f"long full-size sampled max block rel err {errs.max():.2e}")
 
 
+def test_llama_block_full_size_sampled():
+    """One Llama-3-8B-shaped block at full size (q, k, v, o, gate, up, down;
+    272 examples x 1024 tokens, bf16 N(0, 0.02^2), 32 x 32 sketches) in one
+    call -- the one-tile-per-workgroup schedule over 7 x 2176 tiles; two
+    examples checked against the explicit-gradient oracle on every map."""
+    cfg = workloads.CONFIGS["llama"]
+    layers, lens, ktot = workloads.sketch_inputs(cfg, DEV, layers=range(7))
+    assert ktot == 7 * 32 * 32
+    S = api.sketch(layers, lens)
+    torch.cuda.synchronize()
+    S_gpu = host64(S)
+    assert np.isfinite(S_gpu).all()
+    rows = [0, 271]
+    ref = oracle.sketch_ref(layers_to_host(layers, rows), lens.cpu().numpy()[rows])
+    errs = block_errors(S_gpu[rows], ref, layers, range(len(rows)))
+    assert errs.max() <= TOL_SKETCH_BF16, errs.max()
+    print(f"llama block full-size sampled max block rel err {errs.max():.2e}")
+
+
 @pytest.mark.parametrize("dtype,tol", [(torch.bfloat16, TOL_SKETCH_BF16), (torch.float32, TOL_SKETCH_F32)])
 def test_many_short_examples_share_a_token_tile(dtype, tol):
     """Packed tiles holding many examples each (lengths 0..16): the per-example
