@@ -50,15 +50,18 @@ constexpr int kAuxStream = 2;
 constexpr int kAuxCached = 0;
 
 // LDS layout of an operand tile for the bf16 MFMA: 16-row blocks of 2 KB
-// (rows of 128 bytes = 8 segments of 16 bytes), segment seg of row lr stored
-// in slot seg ^ (lr & 7) ^ (lr >> 3): the 16-byte reads of one MFMA operand
-// (16 rows, one segment) are conflict-free, and one wave's DMA fills one
-// 8-row half block (1 KB) with lane l holding row l / 8, slot l % 8.
-__device__ __forceinline__ u32x4 swz_read(const unsigned char* blk, int lr, int seg) {
-  return *reinterpret_cast<const u32x4*>(blk + (lr >> 3) * 1024 + (lr & 7) * 128 + ((seg ^ (lr & 7) ^ (lr >> 3)) * 16));
+// (rows of 128 bytes = 8 segments of 16 bytes), segment seg of row r stored
+// in slot seg ^ ((r >> 1) & 7).  The 16-byte reads of one MFMA operand (16
+// rows, one segment per group of 16 lanes) then fall on distinct banks, and
+// one wave's DMA fills one 8-row half block (1 KB) with lane l holding row
+// l / 8, slot l % 8.  (The LDS serves 32 lanes of a 16-byte read at a time:
+// rows with equal r mod 4 must get distinct slots across two segments, and
+// measured bank-conflict counts are zero for this layout.)
+__device__ __forceinline__ u32x4 swz_read(const unsigned char* blk, int r, int seg) {
+  return *reinterpret_cast<const u32x4*>(blk + r * 128 + ((seg ^ ((r >> 1) & 7)) * 16));
 }
 // the segment that lane l loads when its wave fills half block h (0 or 1)
-__device__ __forceinline__ int swz_seg_of_lane(int l, int h) { return (l & 7) ^ (l >> 3) ^ h; }
+__device__ __forceinline__ int swz_seg_of_lane(int l, int h) { return (l & 7) ^ (4 * h + (l >> 4)); }
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 

@@ -264,19 +264,23 @@ __global__ __launch_bounds__(512) void gram_big_kernel(BigArgs a) {
     issue(t + 1, (t + 1) & 1);
     const unsigned char* sa = lds + (t & 1) * kBStage;
     const unsigned char* sbp = sa + kBPanel;
+    // both 32-column halves' fragments are read up front, so the second
+    // half's reads are in flight during the first half's MFMAs
+    u32x4 fa[2][8], fb[2][4];
 #pragma unroll
     for (int kh = 0; kh < 2; ++kh) {
       const int seg = 4 * kh + lg;
-      u32x4 fa[8], fb[4];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) fa[i] = swz_read(sa + (wr * 8 + i) * 2048, lr, seg);
+      for (int i = 0; i < 8; ++i) fa[kh][i] = swz_read(sa + (wr * 8 + i) * 2048, lr, seg);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) fb[j] = swz_read(sbp + (wc * 4 + j) * 2048, lr, seg);
+      for (int j = 0; j < 4; ++j) fb[kh][j] = swz_read(sbp + (wc * 4 + j) * 2048, lr, seg);
+    }
+#pragma unroll
+    for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int i = 0; i < 8; ++i) acc[i][j] = mma_bf16(fa[i], fb[j], acc[i][j]);
-    }
+        for (int i = 0; i < 8; ++i) acc[i][j] = mma_bf16(fa[kh][i], fb[kh][j], acc[i][j]);
   }
 
   float* Kp = a.K + (long long)p * a.n * a.n;
@@ -382,14 +386,23 @@ __global__ __launch_bounds__(kThreads) void score_kernel(GramArgs a, const float
   const long long g0 = a.goff[p], g1 = a.goff[p + 1];
   double acc = 0.0;
   if (i < a.n) {
+    // 16-byte loads: group edges are multiples of 8 (bf16) / 4 (fp32)
+    // elements and rows are 16-byte aligned
     const unsigned char* row = a.G + (long long)i * a.ldG * GTr<BF16>::ES;
-    for (long long c = g0 + threadIdx.x; c < g1; c += kThreads) {
-      float v;
-      if constexpr (BF16)
-        v = __uint_as_float((unsigned)reinterpret_cast<const unsigned short*>(row)[c] << 16);
-      else
-        v = reinterpret_cast<const float*>(row)[c];
-      acc += (double)v * (double)gbar[c];
+    constexpr int V = GTr<BF16>::EPV;
+    for (long long c = g0 + (long long)threadIdx.x * V; c < g1; c += (long long)kThreads * V) {
+      const u32x4 q = *reinterpret_cast<const u32x4*>(row + c * GTr<BF16>::ES);
+      const float4 g4a = *reinterpret_cast<const float4*>(gbar + c);
+      if constexpr (BF16) {
+        const float4 g4b = *reinterpret_cast<const float4*>(gbar + c + 4);
+        acc += (double)__uint_as_float(q.x << 16) * (double)g4a.x + (double)__uint_as_float(q.x & 0xffff0000u) * (double)g4a.y;
+        acc += (double)__uint_as_float(q.y << 16) * (double)g4a.z + (double)__uint_as_float(q.y & 0xffff0000u) * (double)g4a.w;
+        acc += (double)__uint_as_float(q.z << 16) * (double)g4b.x + (double)__uint_as_float(q.z & 0xffff0000u) * (double)g4b.y;
+        acc += (double)__uint_as_float(q.w << 16) * (double)g4b.z + (double)__uint_as_float(q.w & 0xffff0000u) * (double)g4b.w;
+      } else {
+        acc += (double)__uint_as_float(q.x) * (double)g4a.x + (double)__uint_as_float(q.y) * (double)g4a.y;
+        acc += (double)__uint_as_float(q.z) * (double)g4a.z + (double)__uint_as_float(q.w) * (double)g4a.w;
+      }
     }
   } else {
     for (long long c = g0 + threadIdx.x; c < g1; c += kThreads) acc += (double)gbar[c] * (double)gbar[c];

@@ -536,7 +536,7 @@ __global__ __launch_bounds__(kThreads, 2) void sketch_packed_kernel(PackArgs a) 
   const __amdgpu_buffer_rsrc_t rpo = make_rsrc(L.p_out, (unsigned)(KOUT * L.d_out * E::ES));
   const int nsx = L.d_in / KC, nsd = L.d_out / KC;
   const int nsteps = nsx + nsd;
-  const unsigned seg = (unsigned)((lane & 7) ^ hr);
+  const unsigned seg0 = (unsigned)swz_seg_of_lane(lane, 0), seg1 = (unsigned)swz_seg_of_lane(lane, 1);
 
   // issue every DMA of step s into ring stage st
   auto issue = [&](int s, int st) {
@@ -549,7 +549,7 @@ __global__ __launch_bounds__(kThreads, 2) void sketch_packed_kernel(PackArgs a) 
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const unsigned ro = pass == 0 ? offx[rb][h] : offd[rb][h];
-        const unsigned off = ro == kOobOffset ? kOobOffset : ro + (k0 + (seg ^ (unsigned)h) * E::EPV) * E::ES;
+        const unsigned off = ro == kOobOffset ? kOobOffset : ro + (k0 + (h ? seg1 : seg0) * E::EPV) * E::ES;
         dma16<kAuxStream>(rr, sb + ((wave * 2 + rb) * 2 + h) * 1024, off);
       }
     const __amdgpu_buffer_rsrc_t rp = pass == 0 ? rpi : rpo;
@@ -561,7 +561,7 @@ __global__ __launch_bounds__(kThreads, 2) void sketch_packed_kernel(PackArgs a) 
       const unsigned row = (unsigned)(ct * 16 + h * 8 + hr);
       // blocks past the projector's tiles and rows past k_in / k_out fall
       // outside the descriptor's range and fill with zeros
-      const unsigned off = ct < TPM ? (row * dp + k0 + (seg ^ (unsigned)h) * E::EPV) * E::ES : kOobOffset;
+      const unsigned off = ct < TPM ? (row * dp + k0 + (h ? seg1 : seg0) * E::EPV) * E::ES : kOobOffset;
       dma16<0>(rp, sb + (XBLK + b) * 1024, off);
     }
   };
