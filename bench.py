@@ -33,6 +33,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--groups", choices=["global", "layer"], default="global",
+                    help="one group over all sketch columns (default), or one group per layer (P = 8)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle's sketch sample")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run three 1 GiB device-to-device copies first (known bytes, to scale HBM counters)")
@@ -72,23 +74,25 @@ def main():
     S = torch.empty(N, ktot, dtype=torch.float32, device=dev)
     sk_ws = torch.empty(max(1, api.dr_sketch_workspace_size(layers, N, T, torch.bfloat16)), dtype=torch.uint8,
                         device=dev)
-    goff = [0, ktot]
-    K = torch.empty(1, n, n, device=dev)
-    s = torch.empty(1, n, device=dev)
-    t2 = torch.empty(1, device=dev)
+    # groups: one over the concatenated sketch, or one per layer (layer-wise mode)
+    goff = [0, ktot] if args.groups == "global" else [int(L["col_offset"]) for L in layers] + [ktot]
+    P = len(goff) - 1
+    K = torch.empty(P, n, n, device=dev)
+    s = torch.empty(P, n, device=dev)
+    t2 = torch.empty(P, device=dev)
     gr_ws = torch.empty(max(1, api.dr_gram_workspace_size(n, m, goff, torch.float32)), dtype=torch.uint8, device=dev)
-    wc = torch.empty(1, n, device=dev)
-    r2c = torch.empty(1, device=dev)
-    itc = torch.empty(1, dtype=torch.int32, device=dev)
-    kktc = torch.empty(1, device=dev)
-    infoc = torch.empty(1, dtype=torch.int32, device=dev)
-    ws_ = torch.empty(1, n, device=dev)
-    le = torch.empty(1, device=dev)
-    r2s = torch.empty(1, device=dev)
-    infos = torch.empty(1, dtype=torch.int32, device=dev)
-    idx = torch.empty(1, k_top, dtype=torch.int32, device=dev)
-    wt = torch.empty(1, n, device=dev)
-    infot = torch.empty(1, dtype=torch.int32, device=dev)
+    wc = torch.empty(P, n, device=dev)
+    r2c = torch.empty(P, device=dev)
+    itc = torch.empty(P, dtype=torch.int32, device=dev)
+    kktc = torch.empty(P, device=dev)
+    infoc = torch.empty(P, dtype=torch.int32, device=dev)
+    ws_ = torch.empty(P, n, device=dev)
+    le = torch.empty(P, device=dev)
+    r2s = torch.empty(P, device=dev)
+    infos = torch.empty(P, dtype=torch.int32, device=dev)
+    idx = torch.empty(P, k_top, dtype=torch.int32, device=dev)
+    wt = torch.empty(P, n, device=dev)
+    infot = torch.empty(P, dtype=torch.int32, device=dev)
     u = torch.empty(ktot, device=dev)
     cb_ws = torch.empty(max(1, api.dr_combine_workspace_size(n, goff)), dtype=torch.uint8, device=dev)
 
@@ -154,7 +158,7 @@ def main():
     # Gram end to the last projection's end (the three overlap)
     proj_wall = float(np.mean([max(events[i][2].elapsed_time(events[i][j]) for j in (4, 6, 8))
                                + events[i][1].elapsed_time(events[i][2]) for i in range(args.steps)]))
-    if int(infoc[0]) != 0 or int(infos[0]) != 0 or int(infot[0]) != 0:
+    if bool((infoc != 0).any()) or bool((infos != 0).any()) or bool((infot != 0).any()):
         raise RuntimeError("a projection reported a non-zero info code")
 
     # algorithmic bytes of one sketch call: valid tokens' x and dy rows, the
@@ -191,6 +195,7 @@ def main():
                         "iterations + ridge span + top-32 + combine on the same Gram",
             "layers": 8, "d_in": 2048, "d_out": 2048, "n": n, "m": m, "seq_len": T, "sketch": "64x64",
             "valid_tokens": int(lh.sum()), "accumulate": "fp32", "solver_arithmetic": "fp64 on fp32 K",
+            "groups": "one over all columns" if P == 1 else f"{P} (one per layer)",
         },
         "projection_steps_per_s": 1e3 / proj_ms,
         "projection_ms": proj_ms,
@@ -209,7 +214,7 @@ def main():
     }
 
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(layers, lens, S, K, s, t2, n, m, k_top, lam, cfg, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(layers, lens, S, K, s, t2, n, m, k_top, lam, cfg, args.cpu_seconds, goff)
     print(json.dumps(out), flush=True)
 
 
@@ -333,7 +338,7 @@ def summarize_profiles(kt_dir, fetch_dir, write_dir):
     print(f"sketch call {sk_avg:.1f} us, {sk_bytes / 1e9:.4f} GB per call")
 
 
-def cpu_baseline(layers, lens, S, K, s, t2, n, m, k_top, lam, cfg, budget_s):
+def cpu_baseline(layers, lens, S, K, s, t2, n, m, k_top, lam, cfg, budget_s, goff):
     """The oracle, as it stands, on the host cores: explicit-gradient sketches
     on a bounded sample of (example, layer) blocks of the same inputs
     (extrapolated linearly to all 72 x 8 blocks), then Gram, cone, span,
@@ -376,20 +381,22 @@ def cpu_baseline(layers, lens, S, K, s, t2, n, m, k_top, lam, cfg, budget_s):
     t_sketch_full = t_sk * len(blocks) / done
     Sg = f64(S)
     t0 = time.perf_counter()
-    Kr, sr, t2r = oracle.gram_ref(Sg[:n], Sg[n:])
+    Kr, sr, t2r = oracle.gram_ref(Sg[:n], Sg[n:], goff)
     t_gram = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    wc = oracle.nnls_active_set(Kr[0], sr[0])
-    t_cone = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    oracle.span_ref(Kr[0], sr[0], lam, 1)
-    t_span = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    oracle.topk_ref(sr[0], k_top)
-    t_top = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    oracle.combine_ref(Sg[:n], wc)
-    t_comb = time.perf_counter() - t0
+    t_cone = t_span = t_top = t_comb = 0.0
+    for p in range(len(goff) - 1):
+        t0 = time.perf_counter()
+        wc = oracle.nnls_active_set(Kr[p], sr[p])
+        t_cone += time.perf_counter() - t0
+        t0 = time.perf_counter()
+        oracle.span_ref(Kr[p], sr[p], lam, 1)
+        t_span += time.perf_counter() - t0
+        t0 = time.perf_counter()
+        oracle.topk_ref(sr[p], k_top)
+        t_top += time.perf_counter() - t0
+        t0 = time.perf_counter()
+        oracle.combine_ref(Sg[:n, goff[p]:goff[p + 1]], wc)
+        t_comb += time.perf_counter() - t0
     t_step = t_sketch_full + t_gram + t_cone + t_span + t_top + t_comb
     cpu_model = ""
     try:

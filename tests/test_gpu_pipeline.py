@@ -70,3 +70,78 @@ def test_small_block_workload_end_to_end_with_all_projections():
     wsr, _, _ = oracle.span_ref(Kh, sh, 1e-3, RIDGE_REL_TRACE, lam_eff=float(le[0]))
     assert int(infos[0]) == 0 and rel(host64(ws[0]), wsr) <= TOL_SOLVE
     assert np.array_equal(idx[0].cpu().numpy(), oracle.topk_ref(host64(s[0]), n // 2))
+
+
+def test_small_block_layerwise_groups():
+    """Layer-wise mode (one group per layer, P = 8 groups of 4096 columns) on
+    the benchmark's sketches: batched Gram, cone, span, top-k and combine,
+    every group against the oracle on the GPU's own sketches."""
+    cfg = workloads.CONFIGS["small"]
+    n, m = cfg["n"], cfg["m"]
+    layers, lens, kt = workloads.sketch_inputs(cfg, DEV)
+    goff = [int(L["col_offset"]) for L in layers] + [kt]
+    P = len(layers)
+    S = api.sketch(layers, lens)
+    K, s, t2 = api.gram(S[:n], S[n:], goff)
+    wc, r2c, itc, kktc, infoc = api.project_cone(K, s, t2, cfg["iters"], 0.0)
+    ws, le, r2s, infos = api.project_span(K, s, t2, 1e-3, RIDGE_REL_TRACE)
+    idx, wt, infot = api.select_topk(s, n // 2)
+    u = api.combine(S[:n], wc, goff)
+    torch.cuda.synchronize()
+    Sg = host64(S)
+    K_ref, s_ref, t2_ref = oracle.gram_ref(Sg[:n], Sg[n:], goff)
+    u_h = host64(u)
+    for p in range(P):
+        Kh, sh = host64(K[p]), host64(s[p])
+        assert rel(Kh, K_ref[p]) <= TOL_GRAM and rel(sh, s_ref[p]) <= TOL_GRAM
+        assert int(infoc[p]) == 0 and int(infos[p]) == 0 and int(infot[p]) == 0
+        w_ref = oracle.nnls_active_set(Kh, sh)
+        assert rel(host64(wc[p]), w_ref) <= TOL_SOLVE
+        wsr, _, _ = oracle.span_ref(Kh, sh, 1e-3, RIDGE_REL_TRACE, lam_eff=float(le[p]))
+        assert rel(host64(ws[p]), wsr) <= TOL_SOLVE
+        assert np.array_equal(idx[p].cpu().numpy(), oracle.topk_ref(sh, n // 2))
+        c0, c1 = goff[p], goff[p + 1]
+        assert rel(u_h[c0:c1], oracle.combine_ref(Sg[:n, c0:c1], w_ref)) <= TOL_SOLVE
+
+
+def test_llama_shaped_layerwise_projection():
+    """Layer-wise mode at the Llama-shaped scale: 224 groups (one per matrix)
+    of 1024 sketch columns, n = 256 general + 16 target rows; the Gram runs
+    as two launches of at most 128 groups; span at lam = 0 and top-64 on
+    every group, sampled groups against the oracle."""
+    n, m, P, width = 256, 16, 224, 1024
+    g = torch.Generator(device=DEV)
+    g.manual_seed(4242)
+    rows = torch.randn(n + m, P * width, generator=g, device=DEV)
+    goff = [p * width for p in range(P + 1)]
+    K, s, t2 = api.gram(rows[:n], rows[n:], goff)
+    w, le, r2, info = api.project_span(K, s, t2, 0.0, 0)
+    idx, wt, infot = api.select_topk(s, 64)
+    torch.cuda.synchronize()
+    assert torch.all(info == 0) and torch.all(infot == 0)
+    Rh = host64(rows)
+    for p in (0, 127, 128, 223):
+        c0, c1 = goff[p], goff[p + 1]
+        K_ref, s_ref, _ = oracle.gram_ref(Rh[:n, c0:c1], Rh[n:, c0:c1])
+        assert rel(host64(K[p]), K_ref[0]) <= TOL_GRAM and rel(host64(s[p]), s_ref[0]) <= TOL_GRAM
+        w_ref, _, info_ref = oracle.span_ref(host64(K[p]), host64(s[p]), 0.0, 0)
+        assert info_ref == 0 and rel(host64(w[p]), w_ref) <= TOL_SOLVE
+        assert np.array_equal(idx[p].cpu().numpy(), oracle.topk_ref(host64(s[p]), 64))
+
+
+def test_long_context_layerwise_cone():
+    """Long-context layer-wise mode: 16 groups with n = 32 general rows, cone
+    to KKT residual 1e-6 in every group."""
+    n, m, P, width = 32, 4, 16, 4096
+    g = torch.Generator(device=DEV)
+    g.manual_seed(777)
+    rows = torch.randn(n + m, P * width, generator=g, device=DEV)
+    rows[n:] += 0.3 * rows[: m]   # targets partly aligned with some general rows
+    goff = [p * width for p in range(P + 1)]
+    K, s, t2 = api.gram(rows[:n], rows[n:], goff)
+    w, r2, it, kkt, info = api.project_cone(K, s, t2, 100000, 1e-6)
+    torch.cuda.synchronize()
+    for p in range(P):
+        assert int(info[p]) == 0 and float(kkt[p]) <= 1e-6
+        w_ref = oracle.nnls_active_set(host64(K[p]), host64(s[p]))
+        assert rel(host64(w[p]), w_ref) <= TOL_SOLVE
