@@ -19,7 +19,7 @@
 //   lg_trsm_kernel   L21 = A21 L11^-T as an fp32 MFMA product with the
 //                    inverse, 64 rows per workgroup.
 //   lg_syrk_kernel   A22 -= L21 L21^T on 128x128 lower-triangle tiles, fp32
-//                    MFMA, both panel slices staged in LDS.
+//                    MFMA, the panel slices streamed through LDS in chunks.
 // Solve: L y = r and L^T dx = y block by block (one launch per block and
 // direction; every workgroup applies the block's inverse, then updates its
 // share of the remaining right-hand side), x += dx; three solves (the
@@ -375,64 +375,111 @@ __device__ __forceinline__ void tile_pair(int q, int& I, int& J) {
 }
 
 // A22 -= L21 L21^T on the lower-triangle 128x128 tiles of the trailing
-// matrix (rows and columns from k1 = k + 128).  Wave (wr, wc) computes the
-// 64x64 sub-tile (wr, wc); on a diagonal tile the strictly upper sub-tile
-// is skipped and only entries on or below the diagonal are written.
-__global__ __launch_bounds__(256) void lg_syrk_kernel(float* L, long long ldL, int n, int k, const LgCtl* ctl) {
+// matrix (rows and columns from k1 = k + 128).  The 128-column panel slices
+// of both tile rows stream through LDS in four 32-column chunks (buffer ->
+// LDS DMA, double buffered, 32 KiB per chunk, so two workgroups share a
+// CU), in the conflict-free operand layout of the bf16 kernels (a 32-float
+// row is 8 segments of 4 floats).  The tile of A22 is read into registers
+// before the products and updated at the end.  Wave (wr, wc) computes the
+// 64x64 sub-tile (wr, wc) with fp32 16x16x4 MFMA; each lane's 4-float
+// segment feeds 4 MFMAs (reduction indices {t, 4 + t, 8 + t, 12 + t}, the
+// same set for both operands).  On a diagonal tile the strictly upper
+// sub-tile is skipped and only entries on or below the diagonal are written.
+constexpr int SY_CH = 32;                 // panel columns per chunk
+constexpr int SY_PANEL = NB * SY_CH * 4;  // bytes of one tile row's chunk (16 KiB)
+
+__global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL, int n, int k, const LgCtl* ctl) {
   if (ctl->skip) return;
-  __shared__ __attribute__((aligned(16))) float Ai[NB][LDP];
-  __shared__ __attribute__((aligned(16))) float Aj[NB][LDP];
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * 2 * SY_PANEL];
   int I, J;
   tile_pair(blockIdx.x, I, J);
   const int k1 = k + NB;
   const int ri = k1 + NB * I, rj = k1 + NB * J;
-  const int tid = threadIdx.x;
-  for (int t = tid; t < NB * (NB / 4); t += 256) {
-    const int rr = t / (NB / 4), cq = t % (NB / 4);
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (ri + rr < n) v = *reinterpret_cast<const float4*>(L + (long long)(ri + rr) * ldL + k + 4 * cq);
-    *reinterpret_cast<float4*>(&Ai[rr][4 * cq]) = v;
-    if (I != J) {
-      float4 u = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (rj + rr < n) u = *reinterpret_cast<const float4*>(L + (long long)(rj + rr) * ldL + k + 4 * cq);
-      *reinterpret_cast<float4*>(&Aj[rr][4 * cq]) = u;
-    }
-  }
-  __syncthreads();
-  const float(*Bp)[LDP] = I != J ? Aj : Ai;
-  const int w = tid >> 6, lane = tid & 63, lr = lane & 15, lq = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wr = w & 1, wc = w >> 1;
-  if (I == J && wc > wr) return;
+  const bool diag = I == J;
+  const bool active = !(diag && wc > wr);
+  const int lr = lane & 15, lg = lane >> 4;
+  // this lane's C entries (rows 4 lg + q of each 16-row block, column lr),
+  // loaded during the last two chunks
+  f32x4 c[4][4];
+  auto load_c = [&]() {
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int row = ri + 64 * wr + 16 * rb + 4 * lg + q;
+          const int col = rj + 64 * wc + 16 * cb + lr;
+          c[rb][cb][q] = (row < n && col < n) ? L[(long long)row * ldL + col] : 0.f;
+        }
+  };
+  // DMA of one chunk: wave w fills half blocks w, w + 4, w + 8, w + 12 of each panel
+  const __amdgpu_buffer_rsrc_t rsi = make_rsrc(L + (long long)ri * ldL, kOobOffset);
+  const __amdgpu_buffer_rsrc_t rsj = make_rsrc(L + (long long)rj * ldL, kOobOffset);
+  unsigned offi[4], offj[4];
+  int segs[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int hb = w + 4 * u;
+    const int r = 8 * hb + (lane >> 3);
+    segs[u] = swz_seg_of_lane(lane, hb & 1);
+    offi[u] = ri + r < n ? (unsigned)((long long)r * ldL * 4) : kOobOffset;
+    offj[u] = rj + r < n ? (unsigned)((long long)r * ldL * 4) : kOobOffset;
+  }
+  auto issue = [&](int ch, int st) {
+    unsigned char* sb = lds + st * 2 * SY_PANEL;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const unsigned cofs = (unsigned)((k + SY_CH * ch + 4 * segs[u]) * 4);
+      dma16<kAuxCached>(rsi, sb + (w + 4 * u) * 1024, offi[u] == kOobOffset ? kOobOffset : offi[u] + cofs);
+      dma16<kAuxCached>(rsj, sb + SY_PANEL + (w + 4 * u) * 1024, offj[u] == kOobOffset ? kOobOffset : offj[u] + cofs);
+    }
+  };
   f32x4 acc[4][4];
 #pragma unroll
   for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int kk = 0; kk < NB / 16; ++kk) {
-    float4 av[4], bv[4];
+  issue(0, 0);
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb) av[rb] = *reinterpret_cast<const float4*>(&Ai[64 * wr + 16 * rb + lr][16 * kk + 4 * lq]);
+  for (int ch = 0; ch < NB / SY_CH; ++ch) {
+    DR_WAIT_VM(0);
+    DR_LDS_SYNC();
+    if (ch + 1 < NB / SY_CH) issue(ch + 1, (ch + 1) & 1);
+    if (ch == NB / SY_CH - 2 && active) load_c();
+    if (active) {
+      const unsigned char* sa = lds + (ch & 1) * 2 * SY_PANEL;
+      const unsigned char* sbp = sa + SY_PANEL;
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) bv[cb] = *reinterpret_cast<const float4*>(&Bp[64 * wc + 16 * cb + lr][16 * kk + 4 * lq]);
+      for (int sub = 0; sub < 2; ++sub) {
+        const int seg = 4 * sub + lg;
+        f32x4 fa[4], fb[4];
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
+        for (int rb = 0; rb < 4; ++rb) fa[rb] = __builtin_bit_cast(f32x4, swz_read(sa + (4 * wr + rb) * 2048, lr, seg));
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb) {
-        acc[rb][cb] = mma_f32(av[rb].x, bv[cb].x, acc[rb][cb]);
-        acc[rb][cb] = mma_f32(av[rb].y, bv[cb].y, acc[rb][cb]);
-        acc[rb][cb] = mma_f32(av[rb].z, bv[cb].z, acc[rb][cb]);
-        acc[rb][cb] = mma_f32(av[rb].w, bv[cb].w, acc[rb][cb]);
+        for (int cb = 0; cb < 4; ++cb) fb[cb] = __builtin_bit_cast(f32x4, swz_read(sbp + (4 * wc + cb) * 2048, lr, seg));
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+          for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) acc[rb][cb] = mma_f32(fa[rb][t], fb[cb][t], acc[rb][cb]);
       }
+    }
   }
+  if (!active) return;
 #pragma unroll
   for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int row = ri + 64 * wr + 16 * rb + 4 * lq + j;
+      for (int q = 0; q < 4; ++q) {
+        const int row = ri + 64 * wr + 16 * rb + 4 * lg + q;
         const int col = rj + 64 * wc + 16 * cb + lr;
-        if (row < n && col < n && (I != J || col <= row)) L[(long long)row * ldL + col] -= acc[rb][cb][j];
+        if (row < n && col < n && (!diag || col <= row)) L[(long long)row * ldL + col] = c[rb][cb][q] - acc[rb][cb][q];
       }
 }
 
