@@ -485,41 +485,53 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
 
 // ---------------------------------------------------------------- solves
 
+// y_c = sum_m M[m][c] v_m for a 128x128 block M staged in LDS (row-major,
+// thread pairs split m); every thread of the workgroup takes part, the
+// result lands in out[] (LDS).  M is lower- or upper-triangular with zeros
+// elsewhere, so the sum runs over all m.
+__device__ __forceinline__ void block_matvec_T(const float* Ms, const double* v, double* part, double* out) {
+  const int tid = threadIdx.x;
+  const int c = tid & (NB - 1), h = tid >> 7;
+  double a0 = 0.0, a1 = 0.0;
+#pragma unroll 8
+  for (int m = 64 * h; m < 64 * h + 64; m += 2) {
+    a0 += (double)Ms[m * NB + c] * v[m];
+    a1 += (double)Ms[(m + 1) * NB + c] * v[m + 1];
+  }
+  if (h == 1) part[c] = a0 + a1;
+  __syncthreads();
+  if (h == 0) out[c] = (a0 + a1) + part[c];
+  __syncthreads();
+}
+
+// stage a 128x128 fp32 block (row stride ld floats) into LDS: 16 float4 per thread, all in flight
+__device__ __forceinline__ void stage_block(float* dst, const float* src, long long ld, int rows_valid) {
+  const int tid = threadIdx.x;
+  float4 v[16];
+#pragma unroll
+  for (int u = 0; u < 16; ++u) {
+    const int e = tid + 256 * u;   // float4 index: row e / 32, column 4 (e % 32)
+    const int r = e >> 5, c4 = e & 31;
+    v[u] = r < rows_valid ? *reinterpret_cast<const float4*>(src + (long long)r * ld + 4 * c4)
+                          : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+#pragma unroll
+  for (int u = 0; u < 16; ++u) reinterpret_cast<float4*>(dst)[tid + 256 * u] = v[u];
+}
+
 // Forward step for block b of L y = r: y_b = Inv_b r_b (every workgroup
-// forms it; workgroup 0 stores it in y), then r_i -= L[i, block b] . y_b for
-// this workgroup's 128 rows of the trailing part (32 lanes per row, all of
-// a thread's row loads issued before the sums).
+// forms it from the staged inverse; workgroup 0 stores it in y), then
+// r_i -= L[i, block b] . y_b for this workgroup's 128 rows of the trailing
+// part (32 lanes per row; the row loads are issued first).
 __global__ __launch_bounds__(256) void lg_fwd_kernel(const float* L, long long ldL, int n, int b, const float* invT,
                                                      double* r, double* y, const LgCtl* ctl) {
   if (ctl->skip) return;
+  __shared__ __attribute__((aligned(16))) float Ms[NB * NB];
   __shared__ double rb[NB], yb[NB], part[NB];
   const int tid = threadIdx.x;
   const int o = NB * b;
-  if (tid < NB) rb[tid] = r[o + tid];
-  __syncthreads();
-  {
-    // y_c = sum_m Inv[c][m] r_m = sum_m invT[m][c] r_m (Inv is lower, zeros above):
-    // two threads per c, each half of m
-    const int c = tid & (NB - 1), h = tid >> 7;
-    const float* col = invT + c;
-    double a0 = 0.0, a1 = 0.0;
-#pragma unroll 8
-    for (int m = 64 * h; m < 64 * h + 64; m += 2) {
-      a0 += (double)col[(long long)m * NB] * rb[m];
-      a1 += (double)col[(long long)(m + 1) * NB] * rb[m + 1];
-    }
-    if (h == 1) part[c] = a0 + a1;
-    __syncthreads();
-    if (h == 0) {
-      const double v = (a0 + a1) + part[c];
-      yb[c] = v;
-      if (blockIdx.x == 0) y[o + c] = v;
-    }
-    __syncthreads();
-  }
   const int g = tid >> 5, l32 = tid & 31;   // 8 rows at a time, 32 lanes each
   const int base = o + NB + NB * blockIdx.x;
-  const double y0 = yb[4 * l32], y1 = yb[4 * l32 + 1], y2 = yb[4 * l32 + 2], y3 = yb[4 * l32 + 3];
   float4 v[NB / 8];
 #pragma unroll
   for (int t = 0; t < NB / 8; ++t) {
@@ -527,6 +539,12 @@ __global__ __launch_bounds__(256) void lg_fwd_kernel(const float* L, long long l
     v[t] = row < n ? *reinterpret_cast<const float4*>(L + (long long)row * ldL + o + 4 * l32)
                    : make_float4(0.f, 0.f, 0.f, 0.f);
   }
+  stage_block(Ms, invT, NB, NB);   // invT[m][c] = Inv_b[c][m]
+  if (tid < NB) rb[tid] = r[o + tid];
+  __syncthreads();
+  block_matvec_T(Ms, rb, part, yb);
+  if (blockIdx.x == 0 && tid < NB) y[o + tid] = yb[tid];
+  const double y0 = yb[4 * l32], y1 = yb[4 * l32 + 1], y2 = yb[4 * l32 + 2], y3 = yb[4 * l32 + 3];
 #pragma unroll
   for (int t = 0; t < NB / 8; ++t) {
     const int row = base + g + 8 * t;
@@ -536,50 +554,29 @@ __global__ __launch_bounds__(256) void lg_fwd_kernel(const float* L, long long l
   }
 }
 
-// Backward step for block b of L^T x = y: x_b = Inv_b^T y_b (every workgroup
-// forms it; workgroup 0 stores it), then y_m -= sum_{i in block b} L[i][m] x_i
-// for this workgroup's 256 columns m < 128 b.
+// Backward step for block b of L^T x = y: x_b = Inv_b^T y_b (every
+// workgroup forms it; workgroup 0 stores it), then y_m -= sum_{i in block b}
+// L[i][m] x_i for this workgroup's 128 columns m < 128 b, with the 128x128
+// block of L staged in LDS.
 __global__ __launch_bounds__(256) void lg_bwd_kernel(const float* L, long long ldL, int n, int b, const float* inv,
                                                      double* y, double* x, const LgCtl* ctl) {
   if (ctl->skip) return;
-  __shared__ double zb[NB], xb[NB], part[NB];
+  __shared__ __attribute__((aligned(16))) float Ms[NB * NB];
+  __shared__ double zb[NB], xb[NB], part[NB], sums[NB];
   const int tid = threadIdx.x;
   const int o = NB * b;
+  const int rows = n - o < NB ? n - o : NB;
+  stage_block(Ms, inv, NB, NB);    // inv[m][c] = Inv_b[m][c]: x_c = sum_m inv[m][c] y_m
   if (tid < NB) zb[tid] = y[o + tid];
   __syncthreads();
-  {
-    // x_c = sum_m Inv[m][c] y_m (zeros above the diagonal): two threads per c
-    const int c = tid & (NB - 1), h = tid >> 7;
-    const float* col = inv + c;
-    double a0 = 0.0, a1 = 0.0;
-#pragma unroll 8
-    for (int m = 64 * h; m < 64 * h + 64; m += 2) {
-      a0 += (double)col[(long long)m * NB] * zb[m];
-      a1 += (double)col[(long long)(m + 1) * NB] * zb[m + 1];
-    }
-    if (h == 1) part[c] = a0 + a1;
-    __syncthreads();
-    if (h == 0) {
-      const double v = (a0 + a1) + part[c];
-      xb[c] = v;
-      if (blockIdx.x == 0) x[o + c] = v;
-    }
-    __syncthreads();
-  }
-  const int m = 256 * blockIdx.x + tid;
-  if (m >= o) return;
-  const int rows = n - o < NB ? n - o : NB;
-  const float* colp = L + (long long)o * ldL + m;
-  double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
-  int i = 0;
-  for (; i + 4 <= rows; i += 4) {
-    a0 += (double)colp[(long long)i * ldL] * xb[i];
-    a1 += (double)colp[(long long)(i + 1) * ldL] * xb[i + 1];
-    a2 += (double)colp[(long long)(i + 2) * ldL] * xb[i + 2];
-    a3 += (double)colp[(long long)(i + 3) * ldL] * xb[i + 3];
-  }
-  for (; i < rows; ++i) a0 += (double)colp[(long long)i * ldL] * xb[i];
-  y[m] -= (a0 + a1) + (a2 + a3);
+  block_matvec_T(Ms, zb, part, xb);
+  if (blockIdx.x == 0 && tid < NB) x[o + tid] = xb[tid];
+  const int m0 = NB * blockIdx.x;
+  if (m0 >= o) return;   // (uniform) block 0 has no columns to the left
+  stage_block(Ms, L + (long long)o * ldL + m0, ldL, rows);   // rows o .. o + rows, columns m0 .. m0 + 128
+  __syncthreads();
+  block_matvec_T(Ms, xb, part, sums);   // sums_c = sum_i L[o + i][m0 + c] x_i
+  if (tid < NB) y[m0 + tid] -= sums[tid];
 }
 
 __global__ void lg_axpy_kernel(double* x, const double* dx, int npad, const LgCtl* ctl) {
@@ -691,7 +688,7 @@ dr_status span_large(const float* K, const float* s, const float* t2, int64_t n6
                            z, ctl);
       }
       for (int b = nblk - 1; b >= 0; --b) {
-        const int g = b > 0 ? (NB * b + 255) / 256 : 1;
+        const int g = b > 0 ? b : 1;
         hipLaunchKernelGGL(lg_bwd_kernel, dim3(g), dim3(256), 0, hs, L, ldL, n, b, inv + (long long)b * NB * NB, z,
                            dx, ctl);
       }
