@@ -20,6 +20,8 @@ written for a reader who checks it against the paper by eye:
 * ``cone``    -- Eq. (proj) onto the convex cone of the general-data
   gradients (non-negative least squares, exact active-set solver).
 * ``topk``    -- the top-k rule of Sec. 3.3.2 with lowest-index tie break.
+* ``update``  -- the weighted assembly of the update in parameter space
+  (Sec. 4.2, post-hoc assembly from the retained pairs).
 * ``brute``   -- exhaustive enumeration for tiny inputs.
 
 Parity status of every function is stated in its module header.
@@ -31,6 +33,7 @@ from .gram import gram_ref
 from .span import ridge_lambda, span_ref, span_residual2, combine_ref
 from .cone import nnls_active_set, cone_ref, cone_kkt_residual, cone_pg_replay
 from .topk import topk_ref
+from .update import update_ref
 from . import brute
 
 __all__ = [
@@ -39,5 +42,5 @@ __all__ = [
     "gram_ref",
     "ridge_lambda", "span_ref", "span_residual2", "combine_ref",
     "nnls_active_set", "cone_ref", "cone_kkt_residual", "cone_pg_replay",
-    "topk_ref", "brute",
+    "topk_ref", "update_ref", "brute",
 ]

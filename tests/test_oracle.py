@@ -406,3 +406,90 @@ def test_topk_is_exact_subset_projection_when_gram_is_scaled_identity(seed):
     np.testing.assert_allclose(K[0], 4.0 * np.eye(n), atol=1e-12)
     S_exact, _ = brute.subset_projection(G, gbar, k)
     np.testing.assert_array_equal(oracle.topk_ref(s[0], k), S_exact)
+
+
+# --------------------------------------------------------------------------
+# Update assembly oracle
+# --------------------------------------------------------------------------
+
+def test_update_hand_fixture(golden_dir):
+    fx = _load(golden_dir, "update_hand.json")
+    x = np.array([[[_num(v) for v in r] for r in ex] for ex in fx["x"]])
+    dy = np.array([[[_num(v) for v in r] for r in ex] for ex in fx["dy"]])
+    for c in fx["cases"]:
+        (U,) = oracle.update_ref([dict(x=x, dy=dy)], c["w"], fx["lengths"])
+        np.testing.assert_array_equal(U, np.array(c["U"], dtype=float))
+
+
+@pytest.mark.parametrize("seed", [0, 3])
+def test_update_one_hot_and_unit_weights_match_autograd(seed):
+    x, dy, lens, per_ex, wgrad = _linear_layer_batch(seed)
+    N = x.shape[0]
+    x = x.copy(); dy = dy.copy()
+    for i in range(N):
+        x[i, lens[i]:] = np.nan
+        dy[i, lens[i]:] = np.nan
+    layer = dict(x=x, dy=dy)
+    for i in range(N):
+        (U,) = oracle.update_ref([layer], np.eye(N)[i], lens)
+        np.testing.assert_allclose(U, per_ex[i], rtol=1e-12, atol=1e-12)
+    (U,) = oracle.update_ref([layer], np.ones(N), lens)
+    np.testing.assert_allclose(U, wgrad, rtol=1e-12, atol=1e-12)
+
+
+def test_update_subset_mean_is_the_gradient_of_the_subset_mean_loss():
+    """u = g_S (Sec. 3.3.2): with w = 1/k on S the assembled update equals
+    autograd's weight gradient of (1/k) sum_{i in S} loss_i."""
+    g = torch.Generator().manual_seed(21)
+    N, T, d_in, d_out = 6, 5, 4, 3
+    x = torch.randn(N, T, d_in, generator=g, dtype=torch.float64)
+    W = torch.randn(d_out, d_in, generator=g, dtype=torch.float64)
+    c = torch.randn(N, T, d_out, generator=g, dtype=torch.float64)
+    lens = torch.tensor([5, 2, 0, 4, 1, 3])
+    mask = (torch.arange(T)[None, :] < lens[:, None]).to(torch.float64)
+    e = (x @ W.T).requires_grad_(True)
+    per_example_loss = (mask[..., None] * torch.sin(e - c) ** 2).sum(dim=(1, 2))
+    (dy,) = torch.autograd.grad(per_example_loss.sum(), e)
+    S = [0, 3, 4]
+    Wg = W.clone().requires_grad_(True)
+    loss_S = (mask[..., None] * torch.sin(x @ Wg.T - c) ** 2).sum(dim=(1, 2))[S].mean()
+    loss_S.backward()
+    w = np.zeros(N)
+    w[S] = 1.0 / len(S)
+    (U,) = oracle.update_ref([dict(x=x.numpy(), dy=dy.numpy())], w, lens.numpy())
+    np.testing.assert_allclose(U, Wg.grad.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_update_sketch_equals_weighted_sum_of_sketches_per_group():
+    """P_out U_l P_in^T = sum_i w_{g(l),i} S_i^(l): sketching is linear, so
+    the sketch of the assembled update is the same weighted sum of the
+    (separately pinned) per-example sketches.  Two layers in two groups,
+    NaN padding, a NaN row with weight 0 and NaN target rows after n."""
+    rng = np.random.default_rng(8)
+    n, m, T = 5, 2, 6
+    N = n + m
+    lens = np.array([6, 3, 0, 1, 5, 6, 6])
+    dims = [(7, 5, 3, 2), (4, 6, 2, 3)]
+    layers = []
+    for d_in, d_out, k_in, k_out in dims:
+        x = rng.standard_normal((N, T, d_in))
+        dy = rng.standard_normal((N, T, d_out))
+        for i in range(N):
+            x[i, lens[i]:] = np.nan
+            dy[i, lens[i]:] = np.nan
+        x[1] = np.nan
+        dy[1] = np.nan
+        x[n:] = np.nan
+        layers.append(dict(x=x, dy=dy, p_in=rng.standard_normal((k_in, d_in)),
+                           p_out=rng.standard_normal((k_out, d_out))))
+    w = rng.standard_normal((2, n))
+    w[:, 1] = 0.0
+    w[1, 3] = 0.0
+    U = oracle.update_ref(layers, w, lens, group_of_layer=[1, 0])
+    for li, (L, g) in enumerate(zip(layers, [1, 0])):
+        assert np.all(np.isfinite(U[li]))
+        rows = [i for i in range(n) if w[g, i] != 0.0]
+        S = oracle.sketch_ref([L], lens, rows=rows)
+        want = sum(w[g, i] * S[i] for i in rows)
+        got = (L["p_out"] @ U[li] @ L["p_in"].T).reshape(-1)
+        np.testing.assert_allclose(got, want, rtol=1e-11, atol=1e-11)
