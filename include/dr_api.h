@@ -228,6 +228,47 @@ dr_status dr_combine(const void* G, int64_t n, int64_t ldG, dr_dtype dtype, cons
                      void* stream);
 size_t dr_combine_workspace_size(int64_t n, const int64_t* goff, int P);
 
+/* ---------------------------------------------------------------------------
+ * dr_assemble_update -- the update in full parameter space, assembled from
+ * the retained pairs once the weights are known (Sec. 4.2: the post-hoc
+ * assembly step of the Global Subset Update algorithm and the per-layer
+ * assembly of the Layer-Wise Subset Update algorithm).  For every layer l
+ *   U_l = sum_{i < n, w[g_l][i] != 0} w[g_l][i] * sum_{t < len[i]} dy_{i,t} x_{i,t}^T
+ * a d_out x d_in matrix.  Top-k weights (1/k on S, dr_select_topk) give the
+ * subset mean g_S of Sec. 3.3.2; span or cone weights give u = G^T w of
+ * Eq. (proj) in parameter space.  Examples with weight 0 and padded tokens
+ * t >= len[i] are never read (they may hold any bits, NaN included).
+ *
+ * Arithmetic: DR_BF16 inputs on bf16 MFMA with fp32 accumulation, each
+ * example's sum scaled by its weight in fp32; DR_F32 inputs on fp32 MFMA.
+ *
+ * Arguments
+ *   layers      (host) num_layers descriptors; x, ldx, dy, lddy, d_in, d_out
+ *               are used (p_in, p_out, k_*, col_offset are ignored).  The
+ *               first n examples of x / dy are the weighted ones (target rows
+ *               after them never enter).
+ *   n, T        weighted examples and padded length, n >= 0, T >= 0.
+ *   len         device int32 [n] (clamped to [0, T]) or NULL (= all T).
+ *   dtype       DR_BF16 or DR_F32 (x and dy share it).
+ *   w, P, ldw   device fp32 weights [P][ldw], P >= 1, ldw >= n.
+ *   group_of_layer  (host) int32 [num_layers] in [0, P): the weight row of
+ *               each layer (group-wise mode, Sec. 3.3.3), or NULL (= row 0).
+ *   U, u_offset fp32 output; layer l's block is U + u_offset[l] (host int64),
+ *               row-major [d_out][d_in].  Blocks must not overlap.  Every
+ *               element of every block is written (zeros if no example has a
+ *               non-zero weight).
+ *   workspace   at least dr_update_workspace_size() bytes.
+ * Requirements (else DR_ERR_ARG): d_in, d_out, ldx, lddy multiples of 8
+ *   (bf16) or 4 (f32); x, dy 16-byte aligned.  One example's rows must span
+ *   less than 4 GiB (T * ld * element size), else DR_ERR_UNSUPPORTED.
+ * ------------------------------------------------------------------------- */
+dr_status dr_assemble_update(const dr_layer* layers, int num_layers, int64_t n, int64_t T,
+                             const int32_t* len, dr_dtype dtype, const float* w, int P, int64_t ldw,
+                             const int32_t* group_of_layer, float* U, const int64_t* u_offset,
+                             void* workspace, size_t ws_bytes, void* stream);
+size_t dr_update_workspace_size(const dr_layer* layers, int num_layers, int64_t n, int64_t T,
+                                dr_dtype dtype);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,4 +1,4 @@
-"""Python face of the C ABI: the same six calls, taking torch tensors.
+"""Python face of the C ABI: the same calls, taking torch tensors.
 
 Each function checks device / dtype / contiguity, turns tensors into device
 pointers, passes torch's current HIP stream and raises DrError on a non-OK
@@ -197,6 +197,57 @@ def dr_combine(G, goff, w, u, workspace=None, stream=None):
                                        _ptr(u), _ptr(ws), wsb, _stream(stream)))
 
 
+def make_update_layer_array(layers):
+    """Host dr_layer descriptors for dr_assemble_update: dicts with x [N, T, d_in]
+    and dy [N, T, d_out] (projector fields are not used by the call)."""
+    arr = (DrLayer * len(layers))()
+    for i, L in enumerate(layers):
+        x, dy = L["x"], L["dy"]
+        for t, nm in ((x, "x"), (dy, "dy")):
+            if t.numel() > 0 and (t.stride(-1) != 1 or t.stride(0) != t.shape[1] * t.stride(1)):
+                raise ValueError(f"{nm} must be [N][T][ld] with unit element stride")
+        arr[i] = DrLayer(x.data_ptr(), max(x.stride(1), x.shape[2]), dy.data_ptr(), max(dy.stride(1), dy.shape[2]),
+                         None, None, x.shape[2], dy.shape[2], 0, 0, 0)
+    return arr
+
+
+def dr_update_workspace_size(layers, n, T, dtype):
+    arr = make_update_layer_array(layers)
+    return _lib.load().dr_update_workspace_size(arr, len(layers), n, T, _DTYPES[dtype])
+
+
+def dr_assemble_update(layers, n, T, lengths, w, U, u_offset, group_of_layer=None, workspace=None, stream=None):
+    """U[u_offset[l]:] (as [d_out][d_in]) = sum_{i<n, w[g_l][i] != 0} w[g_l][i] sum_{t<len_i} dy_{i,t} x_{i,t}^T."""
+    lib = _lib.load()
+    dtype = layers[0]["x"].dtype
+    if dtype not in _DTYPES:
+        raise ValueError("x must be float32 or bfloat16")
+    for L in layers:
+        for nm in ("x", "dy"):
+            _dev(L[nm], nm, dtype)
+    _dev(U, "U", torch.float32)
+    _contig(U, "U")
+    _dev(w, "w", torch.float32)
+    if w.dim() == 1:
+        w = w.unsqueeze(0)
+    if w.dim() != 2 or w.stride(1) != 1:
+        raise ValueError("w must be [P][ldw] with unit column stride")
+    if lengths is not None:
+        _dev(lengths, "lengths", torch.int32)
+        _contig(lengths, "lengths")
+    arr = make_update_layer_array(layers)
+    offs = _goff_array(u_offset)
+    gol = None
+    if group_of_layer is not None:
+        gol = (ctypes.c_int32 * len(layers))(*[int(v) for v in group_of_layer])
+    nbytes = lib.dr_update_workspace_size(arr, len(layers), n, T, _DTYPES[dtype])
+    ws, wsb = _workspace(nbytes, U.device, workspace)
+    check("dr_assemble_update", lib.dr_assemble_update(
+        arr, len(layers), n, T, _ptr(lengths), _DTYPES[dtype], _ptr(w), w.shape[0], w.stride(0), gol, _ptr(U), offs,
+        _ptr(ws), wsb, _stream(stream)))
+    return U
+
+
 # ---------------------------------------------------------------------------
 # allocating conveniences (outputs created with torch on the inputs' device)
 # ---------------------------------------------------------------------------
@@ -259,3 +310,17 @@ def combine(G, w, goff=None, stream=None):
     u = torch.zeros(goff[-1], dtype=torch.float32, device=w.device)
     dr_combine(G, goff, w, u, stream=stream)
     return u
+
+
+def assemble_update(layers, w, n=None, lengths=None, group_of_layer=None, stream=None):
+    """Per-layer updates [d_out, d_in] (views of one flat fp32 buffer)."""
+    N, T = layers[0]["x"].shape[:2]
+    n = w.shape[-1] if n is None else n
+    sizes = [L["dy"].shape[2] * L["x"].shape[2] for L in layers]
+    offs, o = [], 0
+    for sz in sizes:
+        offs.append(o)
+        o += sz
+    U = torch.empty(o, dtype=torch.float32, device=w.device)
+    dr_assemble_update(layers, n, T, lengths, w, U, offs, group_of_layer=group_of_layer, stream=stream)
+    return [U[a:a + sz].view(L["dy"].shape[2], L["x"].shape[2]) for a, sz, L in zip(offs, sizes, layers)]

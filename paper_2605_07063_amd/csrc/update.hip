@@ -1,0 +1,621 @@
+// Assembly of the update in full parameter space (dr_assemble_update):
+//   U_l = sum_{i < n, w_i != 0} w_i sum_{t < len_i} dy_{i,t} x_{i,t}^T      (d_out x d_in)
+// the post-hoc step of Sec. 4.2 that turns the weights of the retained
+// examples into the layer updates (top-k weights 1/k on S give the subset
+// mean g_S; span or cone weights give u = G^T w of Eq. (proj)).
+//
+// Kernels
+//   update_plan_kernel   one workgroup per layer: the examples with w != 0
+//                        and len > 0 in ascending order, their clamped
+//                        lengths and weights (examples with w = 0 are never
+//                        read).
+//   update_bf16_kernel   one 256 (d_out) x 128 (d_in) tile per workgroup, 8
+//                        waves of 64 x 64.  Tokens go through a 3-stage LDS
+//                        ring in steps of 32, filled by buffer->LDS DMA in
+//                        their natural token-major layout; both MFMA operands
+//                        need 8 consecutive tokens per lane, which the gfx950
+//                        transposing LDS read (ds_read_b64_tr_b16) delivers
+//                        straight from that layout.  Each example accumulates
+//                        in fp32 (bf16 products are exact) and is added,
+//                        times its weight, to a second fp32 accumulator when
+//                        the weight changes (once for top-k weights).
+//   update_f32_kernel    the same for fp32 inputs: 64 x 64 tiles, 4 waves of
+//                        32 x 32, fp32 MFMA 16x16x4, staged by plain loads.
+//   update_reduce_kernel when there are fewer tiles than CUs the example
+//                        list of a tile is split over `split` workgroups;
+//                        their partial tiles are summed in split order.
+// Determinism: every sum runs in a fixed order (examples ascending, tokens
+// ascending, splits ascending); no atomics.
+
+#include "common.h"
+
+namespace dr {
+namespace {
+
+constexpr int kMaxUpdLayers = 16;
+constexpr int kMaxSplit = 32;
+
+// bf16 tile
+constexpr int kBO = 256, kBI = 128, kBK = 32;
+constexpr int kBThreads = 512;
+constexpr int kBDyBytes = kBK * kBO * 2;   // 16 KB: 32 token rows of 512 bytes
+constexpr int kBXBytes = kBK * kBI * 2;    // 8 KB: 32 token rows of 256 bytes
+constexpr int kBStage = kBDyBytes + kBXBytes;
+constexpr int kBStages = 3;
+
+// f32 tile
+constexpr int kFO = 64, kFI = 64, kFK = 16;
+constexpr int kFThreads = 256;
+constexpr int kFLd = 80;                   // LDS row stride (floats): the 4 rows of a b32 fragment read hit distinct banks
+
+struct UpdLayerArg {
+  const unsigned char* x;
+  const unsigned char* dy;
+  long long ldx, lddy;   // elements per token
+  long long exx, exdy;   // bytes per example (T * ld * element size)
+  int d_in, d_out;
+  int ti;                // tiles along d_in
+  int tile0;             // first tile of this layer within the launch
+  int list;              // example list of this layer
+  float* U;              // [d_out][d_in]
+};
+
+struct UpdArgs {
+  UpdLayerArg L[kMaxUpdLayers];
+  int num_layers;
+  int ntiles;            // tiles of the launch (all layers)
+  int split;             // workgroups per tile along the example list
+  int n;                 // list stride (>= 1)
+  int nw;                // weighted examples (may be 0)
+  const int* ex;         // [lists][n] selected examples, ascending
+  const int* exlen;      // [lists][n] their clamped lengths (> 0)
+  const float* exw;      // [lists][n] their weights (!= 0)
+  const int* cnt;        // [lists] list lengths
+  float* partial;        // [ntiles * split][tile elements] when split > 1
+};
+
+// ------------------------------------------------------------------ plan
+
+struct RowSel {
+  int r[kMaxUpdLayers];   // weight row (group) of each layer slot
+};
+
+__global__ __launch_bounds__(1024) void update_plan_kernel(const float* w, long long ldw, UpdArgs a,
+                                                           const int* len, int T, int list0, RowSel rs) {
+  __shared__ int wsum[16];
+  __shared__ int base_s;
+  const int j = blockIdx.x;                 // layer slot of the launch
+  const int list = list0 + j;
+  const float* wr = w + (long long)rs.r[j] * ldw;
+  int* ex = const_cast<int*>(a.ex) + (long long)list * a.n;
+  int* exlen = const_cast<int*>(a.exlen) + (long long)list * a.n;
+  float* exw = const_cast<float*>(a.exw) + (long long)list * a.n;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0) base_s = 0;
+  __syncthreads();
+  for (int b = 0; b < a.nw; b += 1024) {
+    const int i = b + tid;
+    int L = 0;
+    float wi = 0.f;
+    if (i < a.nw) {
+      wi = wr[i];
+      L = len ? len[i] : T;
+      L = L < 0 ? 0 : (L > T ? T : L);
+    }
+    const bool keep = i < a.nw && wi != 0.f && L > 0;
+    const unsigned long long m = __ballot(keep);
+    const int before = __popcll(m & ((1ull << lane) - 1ull));
+    if (lane == 0) wsum[wave] = __popcll(m);
+    __syncthreads();
+    int off = base_s;
+    for (int v = 0; v < wave; ++v) off += wsum[v];
+    if (keep) {
+      ex[off + before] = i;
+      exlen[off + before] = L;
+      exw[off + before] = wi;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int t = 0;
+      for (int v = 0; v < 16; ++v) t += wsum[v];
+      base_s += t;
+    }
+    __syncthreads();
+  }
+  if (tid == 0) const_cast<int*>(a.cnt)[list] = base_s;
+}
+
+// which layer / tile / split a workgroup runs.  Workgroup b runs on XCD
+// b % 8; each XCD takes a contiguous run of (tile, split) items, so the
+// workgroups sharing an L2 share d_out panels of one layer.
+__device__ __forceinline__ bool locate(const UpdArgs& a, int& layer, int& to, int& ti, int& s, int& item) {
+  const int items = a.ntiles * a.split;
+  const int per = (items + 7) >> 3;
+  const int k = blockIdx.x >> 3;
+  if (k >= per) return false;
+  item = (blockIdx.x & 7) * per + k;
+  if (item >= items) return false;
+  const int tile = item / a.split;
+  s = item - tile * a.split;
+  layer = 0;
+  while (layer + 1 < a.num_layers && a.L[layer + 1].tile0 <= tile) ++layer;
+  const int t = tile - a.L[layer].tile0;
+  to = t / a.L[layer].ti;
+  ti = t - to * a.L[layer].ti;
+  return true;
+}
+
+// ------------------------------------------------------------------ bf16
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s lds_v4s;
+
+// gfx950 transposing LDS read: within each 16-lane group, source lane
+// 4q + r addresses 4 consecutive 16-bit columns c..c+3 of row q; lane j of
+// the group receives column c_0 + j of the four rows (its four values are
+// rows 0..3 in order).
+__device__ __forceinline__ v4s lds_read_tr16(const unsigned char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p));
+}
+
+// swizzle of the 32-byte slots of a token row: rows that one transposing
+// read touches (q = r & 3 and bit 3 of r) land in distinct bank groups
+__device__ __forceinline__ int slot_xor(int r) { return (r & 3) | (((r >> 3) & 1) << 2); }
+
+__global__ __launch_bounds__(kBThreads) void update_bf16_kernel(UpdArgs a) {
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[kBStages * kBStage];
+  int layer, to, ti, s, item;
+  if (!locate(a, layer, to, ti, s, item)) return;
+  const UpdLayerArg& Lr = a.L[layer];
+  const int d_in = Lr.d_in, d_out = Lr.d_out;
+  const int o0 = to * kBO, i0 = ti * kBI;
+  const int cnt = a.cnt[Lr.list];
+  const int e_lo = (int)((long long)s * cnt / a.split), e_hi = (int)((long long)(s + 1) * cnt / a.split);
+  const int* ex = a.ex + (long long)Lr.list * a.n;
+  const int* exlen = a.exlen + (long long)Lr.list * a.n;
+  const float* exw = a.exw + (long long)Lr.list * a.n;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // DMA roles: dy rows 2w, 2w + 1 and 2w + 16, 2w + 17 (two 1 KB wave
+  // loads), x rows 4w .. 4w + 3 (one).  Lane l fills 16 bytes: physical
+  // slot u / 2, half u % 2 of its row.
+  int rdy[2], rx;
+  unsigned cdy[2], cx;   // byte column inside a token row, or kOobOffset
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int j = w + 8 * h;
+    const int r = 2 * j + (lane >> 5), u = lane & 31;
+    const int col = 16 * ((u >> 1) ^ slot_xor(r)) + 8 * (u & 1);
+    rdy[h] = r;
+    cdy[h] = o0 + col < d_out ? (unsigned)((o0 + col) * 2) : kOobOffset;
+  }
+  {
+    const int r = 4 * w + (lane >> 4), u = lane & 15;
+    const int col = 16 * ((u >> 1) ^ slot_xor(r)) + 8 * (u & 1);
+    rx = r;
+    cx = i0 + col < d_in ? (unsigned)((i0 + col) * 2) : kOobOffset;
+  }
+  const unsigned rowb_dy = (unsigned)(Lr.lddy * 2), rowb_x = (unsigned)(Lr.ldx * 2);
+
+  int ie = e_lo, it = 0, ilen = ie < e_hi ? exlen[ie] : 0;
+  auto issue = [&](int st) {
+    unsigned char* sb = lds + st * kBStage;
+    __amdgpu_buffer_rsrc_t rdys, rxs;
+    unsigned o_dy[2], o_x;
+    if (ie < e_hi) {
+      const long long e = ex[ie];
+      rdys = make_rsrc(Lr.dy + e * Lr.exdy, kOobOffset);
+      rxs = make_rsrc(Lr.x + e * Lr.exx, kOobOffset);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int t = it + rdy[h];
+        o_dy[h] = (t < ilen && cdy[h] != kOobOffset) ? (unsigned)t * rowb_dy + cdy[h] : kOobOffset;
+      }
+      const int t = it + rx;
+      o_x = (t < ilen && cx != kOobOffset) ? (unsigned)t * rowb_x + cx : kOobOffset;
+      it += kBK;
+      if (it >= ilen) {
+        ++ie;
+        it = 0;
+        ilen = ie < e_hi ? exlen[ie] : 0;
+      }
+    } else {
+      rdys = make_rsrc(Lr.dy, kOobOffset);
+      rxs = make_rsrc(Lr.x, kOobOffset);
+      o_dy[0] = o_dy[1] = o_x = kOobOffset;
+    }
+    dma16<kAuxCached>(rdys, sb + w * 1024, o_dy[0]);
+    dma16<kAuxCached>(rdys, sb + (w + 8) * 1024, o_dy[1]);
+    dma16<kAuxCached>(rxs, sb + kBDyBytes + w * 1024, o_x);
+  };
+
+  // fragment reads: lane (g, q, r) of the transposing read addresses token
+  // row 8g + q (+4 for the second half) and 8-byte piece r of the 16-column
+  // block; the block's logical slot is XOR-ed with the row's swizzle.
+  const int g = lane >> 4, q = (lane >> 2) & 3, rr = lane & 3;
+  const int fx = q | ((g & 1) << 2);
+  const int wo = w >> 1, wi = w & 1;
+  unsigned offa[4], offb[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    offa[b] = (unsigned)((8 * g + q) * 512 + (((4 * wo + b) ^ fx) * 32) + rr * 8);
+    offb[b] = (unsigned)(kBDyBytes + (8 * g + q) * 256 + (((4 * wi + b) ^ fx) * 32) + rr * 8);
+  }
+
+  f32x4 acc[4][4], tot[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      tot[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+
+  int ce = e_lo, ct = 0, clen = ce < e_hi ? exlen[ce] : 0;
+  if (ce < e_hi) {
+    issue(0);
+    issue(1);
+    for (int step = 0; ce < e_hi; ++step) {
+      DR_WAIT_VM(3);
+      DR_LDS_SYNC();
+      issue((step + 2) % kBStages);
+      const unsigned char* sb = lds + (step % kBStages) * kBStage;
+      u32x4 fa[4], fb[4];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const v4s lo = lds_read_tr16(sb + offa[b]);
+        const v4s hi = lds_read_tr16(sb + offa[b] + 4 * 512);
+        fa[b] = u32x4{__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
+                      __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y};
+        const v4s lo2 = lds_read_tr16(sb + offb[b]);
+        const v4s hi2 = lds_read_tr16(sb + offb[b] + 4 * 256);
+        fb[b] = u32x4{__builtin_bit_cast(uint2, lo2).x, __builtin_bit_cast(uint2, lo2).y,
+                      __builtin_bit_cast(uint2, hi2).x, __builtin_bit_cast(uint2, hi2).y};
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mma_bf16(fa[i], fb[j], acc[i][j]);
+      ct += kBK;
+      if (ct >= clen) {
+        const float we = exw[ce];
+        ++ce;
+        ct = 0;
+        clen = ce < e_hi ? exlen[ce] : 0;
+        if (ce >= e_hi || exw[ce] != we) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+#pragma unroll
+              for (int r = 0; r < 4; ++r) tot[i][j][r] = fmaf(we, acc[i][j][r], tot[i][j][r]);
+              acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+        }
+      }
+    }
+    DR_WAIT_VM(0);
+  }
+
+  // C layout: register r of block (i, j) is row 4g + r, column lane % 16
+  const int lc = lane & 15;
+  if (a.split == 1) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int o = o0 + 64 * wo + 16 * i + 4 * g + r;
+        if (o >= d_out) continue;
+        float* urow = Lr.U + (long long)o * d_in;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int c = i0 + 64 * wi + 16 * j + lc;
+          if (c < d_in) urow[c] = tot[i][j][r];
+        }
+      }
+  } else {
+    float* P = a.partial + (long long)item * (kBO * kBI);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          P[(64 * wo + 16 * i + 4 * g + r) * kBI + 64 * wi + 16 * j + lc] = tot[i][j][r];
+  }
+}
+
+// ------------------------------------------------------------------ f32
+
+__global__ __launch_bounds__(kFThreads) void update_f32_kernel(UpdArgs a) {
+  __shared__ __attribute__((aligned(16))) float sdy[2][kFK][kFLd];
+  __shared__ __attribute__((aligned(16))) float sx[2][kFK][kFLd];
+  int layer, to, ti, s, item;
+  if (!locate(a, layer, to, ti, s, item)) return;
+  const UpdLayerArg& Lr = a.L[layer];
+  const int d_in = Lr.d_in, d_out = Lr.d_out;
+  const int o0 = to * kFO, i0 = ti * kFI;
+  const int cnt = a.cnt[Lr.list];
+  const int e_lo = (int)((long long)s * cnt / a.split), e_hi = (int)((long long)(s + 1) * cnt / a.split);
+  const int* ex = a.ex + (long long)Lr.list * a.n;
+  const int* exlen = a.exlen + (long long)Lr.list * a.n;
+  const float* exw = a.exw + (long long)Lr.list * a.n;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // staging: thread t loads token row t / 16 (of 16), columns 4 (t % 16) .. +3 of both operands
+  const int sr = tid >> 4, sc = 4 * (tid & 15);
+  const bool okdy = o0 + sc < d_out, okx = i0 + sc < d_in;
+  float4 vdy = make_float4(0.f, 0.f, 0.f, 0.f), vx = vdy;
+  int ie = e_lo, it = 0, ilen = ie < e_hi ? exlen[ie] : 0;
+  auto fetch = [&]() {
+    vdy = make_float4(0.f, 0.f, 0.f, 0.f);
+    vx = vdy;
+    if (ie < e_hi) {
+      const long long e = ex[ie];
+      const int t = it + sr;
+      if (t < ilen) {
+        if (okdy)
+          vdy = *reinterpret_cast<const float4*>(Lr.dy + e * Lr.exdy + ((long long)t * Lr.lddy + o0 + sc) * 4);
+        if (okx) vx = *reinterpret_cast<const float4*>(Lr.x + e * Lr.exx + ((long long)t * Lr.ldx + i0 + sc) * 4);
+      }
+      it += kFK;
+      if (it >= ilen) {
+        ++ie;
+        it = 0;
+        ilen = ie < e_hi ? exlen[ie] : 0;
+      }
+    }
+  };
+
+  const int wo = w >> 1, wi = w & 1;   // 32 x 32 quarter of the tile
+  const int lr = lane & 15, lk = lane >> 4;
+  f32x4 acc[2][2], tot[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      tot[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  int ce = e_lo, ct = 0, clen = ce < e_hi ? exlen[ce] : 0;
+  if (ce < e_hi) fetch();
+  for (int step = 0; ce < e_hi; ++step) {
+    const int b = step & 1;
+    *reinterpret_cast<float4*>(&sdy[b][sr][sc]) = vdy;
+    *reinterpret_cast<float4*>(&sx[b][sr][sc]) = vx;
+    __syncthreads();
+    fetch();   // next step's loads in flight during this step's products
+#pragma unroll
+    for (int kk = 0; kk < kFK / 4; ++kk) {
+      const int k = 4 * kk + lk;
+      float fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) fa[i] = sdy[b][k][32 * wo + 16 * i + lr];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) fb[j] = sx[b][k][32 * wi + 16 * j + lr];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = mma_f32(fa[i], fb[j], acc[i][j]);
+    }
+    ct += kFK;
+    if (ct >= clen) {
+      const float we = exw[ce];
+      ++ce;
+      ct = 0;
+      clen = ce < e_hi ? exlen[ce] : 0;
+      if (ce >= e_hi || exw[ce] != we) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) tot[i][j][r] = fmaf(we, acc[i][j][r], tot[i][j][r]);
+            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+      }
+    }
+  }
+
+  const int g = lane >> 4;
+  if (a.split == 1) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int o = o0 + 32 * wo + 16 * i + 4 * g + r;
+        if (o >= d_out) continue;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int c = i0 + 32 * wi + 16 * j + lr;
+          if (c < d_in) Lr.U[(long long)o * d_in + c] = tot[i][j][r];
+        }
+      }
+  } else {
+    float* P = a.partial + (long long)item * (kFO * kFI);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) P[(32 * wo + 16 * i + 4 * g + r) * kFI + 32 * wi + 16 * j + lr] = tot[i][j][r];
+  }
+}
+
+// U = sum over splits of the partial tiles, in split order
+__global__ __launch_bounds__(256) void update_reduce_kernel(UpdArgs a, int TO, int TI) {
+  const int tile = blockIdx.y;
+  int layer = 0;
+  while (layer + 1 < a.num_layers && a.L[layer + 1].tile0 <= tile) ++layer;
+  const UpdLayerArg& Lr = a.L[layer];
+  const int t = tile - Lr.tile0, to = t / Lr.ti, ti = t - to * Lr.ti;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= TO * TI) return;
+  const int o = to * TO + e / TI, c = ti * TI + e % TI;
+  if (o >= Lr.d_out || c >= Lr.d_in) return;
+  const float* P = a.partial + (long long)tile * a.split * (TO * TI) + e;
+  float v = 0.f;
+  for (int s = 0; s < a.split; ++s) v += P[(long long)s * (TO * TI)];
+  Lr.U[(long long)o * Lr.d_in + c] = v;
+}
+
+// ------------------------------------------------------------------ host
+
+struct UpdPlan {
+  int64_t tiles;     // all layers
+  int split;
+  size_t off_ex, off_len, off_w, off_cnt, off_partial, bytes;
+};
+
+int cu_count() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                              hipSuccess || cus < 1)
+    cus = 256;
+  return cus;
+}
+
+void tile_dims(dr_dtype dtype, int& TO, int& TI) {
+  TO = dtype == DR_BF16 ? kBO : kFO;
+  TI = dtype == DR_BF16 ? kBI : kFI;
+}
+
+UpdPlan update_plan(const dr_layer* layers, int num_layers, int64_t n, dr_dtype dtype) {
+  UpdPlan p;
+  int TO, TI;
+  tile_dims(dtype, TO, TI);
+  p.tiles = 0;
+  for (int l = 0; l < num_layers; ++l)
+    p.tiles += ((layers[l].d_out + TO - 1) / TO) * ((layers[l].d_in + TI - 1) / TI);
+  // resident workgroups: one bf16 workgroup (72 KB of LDS, 8 waves) or four
+  // f32 workgroups per CU
+  const int64_t slots = (int64_t)cu_count() * (dtype == DR_BF16 ? 1 : 4);
+  int64_t split = 1;
+  if (p.tiles < slots && n > 1) {
+    split = (slots + p.tiles - 1) / p.tiles;
+    if (split > kMaxSplit) split = kMaxSplit;
+    if (split > n) split = n;
+  }
+  p.split = (int)split;
+  const size_t nn = (size_t)(n > 0 ? n : 1) * num_layers;
+  size_t o = 0;
+  p.off_ex = o;      o = align_up(o + nn * 4, 256);
+  p.off_len = o;     o = align_up(o + nn * 4, 256);
+  p.off_w = o;       o = align_up(o + nn * 4, 256);
+  p.off_cnt = o;     o = align_up(o + (size_t)num_layers * 4, 256);
+  p.off_partial = o;
+  if (p.split > 1) o = align_up(o + (size_t)p.tiles * p.split * TO * TI * 4, 256);
+  p.bytes = o;
+  return p;
+}
+
+dr_status validate_update(const dr_layer* layers, int num_layers, int64_t n, int64_t T, dr_dtype dtype,
+                          const float* w, int P, int64_t ldw, const int32_t* group_of_layer, const float* U,
+                          const int64_t* u_offset) {
+  if (dtype != DR_BF16 && dtype != DR_F32) return DR_ERR_DTYPE;
+  if (!layers || num_layers < 1 || n < 0 || T < 0 || P < 1) return DR_ERR_ARG;
+  if (n > (1 << 24) || T > (1 << 24) || ldw < n) return DR_ERR_ARG;
+  if (n > 0 && !w) return DR_ERR_ARG;
+  if (!U || !u_offset) return DR_ERR_ARG;
+  const int64_t vec = dtype == DR_BF16 ? 8 : 4;
+  const int64_t es = dtype == DR_BF16 ? 2 : 4;
+  for (int l = 0; l < num_layers; ++l) {
+    const dr_layer& L = layers[l];
+    if (group_of_layer && (group_of_layer[l] < 0 || group_of_layer[l] >= P)) return DR_ERR_ARG;
+    if (u_offset[l] < 0) return DR_ERR_ARG;
+    if (L.d_in < 1 || L.d_out < 1 || L.d_in % vec || L.d_out % vec) return DR_ERR_ARG;
+    if (L.d_in > (1 << 28) || L.d_out > (1 << 28)) return DR_ERR_ARG;
+    if (L.ldx < L.d_in || L.lddy < L.d_out || L.ldx % vec || L.lddy % vec) return DR_ERR_ARG;
+    if (n > 0 && T > 0) {
+      if (!L.x || !L.dy || !aligned16(L.x) || !aligned16(L.dy)) return DR_ERR_ARG;
+      // token rows are addressed with 32-bit offsets inside one example
+      if (T * L.ldx * es >= (int64_t)kOobOffset - 64 || T * L.lddy * es >= (int64_t)kOobOffset - 64)
+        return DR_ERR_UNSUPPORTED;
+    }
+  }
+  return DR_OK;
+}
+
+}  // namespace
+}  // namespace dr
+
+extern "C" size_t dr_update_workspace_size(const dr_layer* layers, int num_layers, int64_t n, int64_t T,
+                                           dr_dtype dtype) {
+  (void)T;
+  if (!layers || num_layers < 1 || n < 0) return 0;
+  if (dtype != DR_BF16 && dtype != DR_F32) return 0;
+  for (int l = 0; l < num_layers; ++l)
+    if (layers[l].d_in < 1 || layers[l].d_out < 1) return 0;
+  return dr::update_plan(layers, num_layers, n, dtype).bytes;
+}
+
+extern "C" dr_status dr_assemble_update(const dr_layer* layers, int num_layers, int64_t n, int64_t T,
+                                        const int32_t* len, dr_dtype dtype, const float* w, int P, int64_t ldw,
+                                        const int32_t* group_of_layer, float* U, const int64_t* u_offset,
+                                        void* workspace, size_t ws_bytes, void* stream) {
+  using namespace dr;
+  dr_status st = validate_update(layers, num_layers, n, T, dtype, w, P, ldw, group_of_layer, U, u_offset);
+  if (st != DR_OK) return st;
+  const UpdPlan pl = update_plan(layers, num_layers, n, dtype);
+  if (!workspace || ws_bytes < pl.bytes) return DR_ERR_WORKSPACE;
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  int TO, TI;
+  tile_dims(dtype, TO, TI);
+  const int64_t es = dtype == DR_BF16 ? 2 : 4;
+  const int nlist = n > 0 ? (int)n : 1;
+  for (int first = 0; first < num_layers && st == DR_OK; first += kMaxUpdLayers) {
+    const int count = num_layers - first < kMaxUpdLayers ? num_layers - first : kMaxUpdLayers;
+    UpdArgs a = {};
+    int rows[kMaxUpdLayers];
+    int tiles = 0;
+    for (int j = 0; j < count; ++j) {
+      const dr_layer& L = layers[first + j];
+      UpdLayerArg& la = a.L[j];
+      la.x = static_cast<const unsigned char*>(L.x);
+      la.dy = static_cast<const unsigned char*>(L.dy);
+      la.ldx = L.ldx;
+      la.lddy = L.lddy;
+      la.exx = T * L.ldx * es;
+      la.exdy = T * L.lddy * es;
+      la.d_in = (int)L.d_in;
+      la.d_out = (int)L.d_out;
+      la.ti = (int)((L.d_in + TI - 1) / TI);
+      la.tile0 = tiles;
+      la.list = first + j;
+      la.U = U + u_offset[first + j];
+      tiles += (int)(((L.d_out + TO - 1) / TO) * la.ti);
+      rows[j] = group_of_layer ? group_of_layer[first + j] : 0;
+    }
+    a.num_layers = count;
+    a.ntiles = tiles;
+    a.split = pl.split;
+    a.n = nlist;
+    a.nw = (int)n;
+    a.ex = reinterpret_cast<const int*>(ws + pl.off_ex);
+    a.exlen = reinterpret_cast<const int*>(ws + pl.off_len);
+    a.exw = reinterpret_cast<const float*>(ws + pl.off_w);
+    a.cnt = reinterpret_cast<const int*>(ws + pl.off_cnt);
+    a.partial = reinterpret_cast<float*>(ws + pl.off_partial);
+    RowSel rs;
+    for (int j = 0; j < kMaxUpdLayers; ++j) rs.r[j] = j < count ? rows[j] : 0;
+    hipLaunchKernelGGL(update_plan_kernel, dim3(count), dim3(1024), 0, hs, w, (long long)ldw, a, len, (int)T, first,
+                       rs);
+    if ((st = launch_status()) != DR_OK) break;
+    const int items = tiles * pl.split;
+    const int grid = (items + 7) / 8 * 8;
+    if (dtype == DR_BF16)
+      hipLaunchKernelGGL(update_bf16_kernel, dim3(grid), dim3(kBThreads), 0, hs, a);
+    else
+      hipLaunchKernelGGL(update_f32_kernel, dim3(grid), dim3(kFThreads), 0, hs, a);
+    if ((st = launch_status()) != DR_OK) break;
+    if (pl.split > 1) {
+      hipLaunchKernelGGL(update_reduce_kernel, dim3((TO * TI + 255) / 256, tiles), dim3(256), 0, hs, a, TO, TI);
+      st = launch_status();
+    }
+  }
+  return st;
+}

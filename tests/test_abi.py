@@ -138,3 +138,44 @@ def test_solver_and_select_argument_errors(lib):
     need = lib.dr_combine_workspace_size(8, g, 1)
     assert need > 0
     assert lib.dr_combine(FAKE, 8, 64, E.DR_F32, g, 1, FAKE, FAKE, None, 0, None) == E.DR_ERR_WORKSPACE
+
+
+def update_call(lib, layers, n=4, T=8, dtype=_lib.DR_F32, w=FAKE, P=1, ldw=4, gol=None, U=FAKE, offs=None,
+                ws=None, wsb=0):
+    arr = (_lib.DrLayer * max(1, len(layers)))(*layers)
+    if offs is None:
+        offs = [0] * max(1, len(layers))
+    oa = (ctypes.c_int64 * len(offs))(*offs)
+    ga = None if gol is None else (ctypes.c_int32 * len(gol))(*gol)
+    return lib.dr_assemble_update(arr, len(layers), n, T, None, dtype, w, P, ldw, ga, U, oa, ws, wsb, None)
+
+
+def test_update_argument_errors(lib):
+    E = _lib
+    assert update_call(lib, []) == E.DR_ERR_ARG
+    assert update_call(lib, [layer()], dtype=5) == E.DR_ERR_DTYPE
+    assert update_call(lib, [layer()], n=-1) == E.DR_ERR_ARG
+    assert update_call(lib, [layer()], ldw=3) == E.DR_ERR_ARG                   # ldw < n
+    assert update_call(lib, [layer()], w=None) == E.DR_ERR_ARG
+    assert update_call(lib, [layer()], U=None) == E.DR_ERR_ARG
+    assert update_call(lib, [layer()], P=0) == E.DR_ERR_ARG
+    assert update_call(lib, [layer(), layer()], P=2, gol=[0, 2]) == E.DR_ERR_ARG   # group row out of range
+    assert update_call(lib, [layer()], offs=[-4]) == E.DR_ERR_ARG
+    assert update_call(lib, [layer(d_in=254, ldx=256)]) == E.DR_ERR_ARG
+    assert update_call(lib, [layer(d_in=12, ldx=12)], dtype=E.DR_BF16) == E.DR_ERR_ARG
+    assert update_call(lib, [layer(dy=FAKE + 8)]) == E.DR_ERR_ARG
+    # one example spanning 4 GiB of rows cannot be addressed with 32-bit offsets
+    big = layer(d_in=8192, ldx=8192, d_out=8192, lddy=8192)
+    assert update_call(lib, [big], T=1 << 18, dtype=E.DR_BF16) == E.DR_ERR_UNSUPPORTED
+    # the projector fields are ignored
+    assert update_call(lib, [layer(p_in=None, p_out=None, k_in=3, k_out=0)]) == E.DR_ERR_WORKSPACE
+
+
+def test_update_workspace_query(lib):
+    layers = [layer(d_in=2048, d_out=2048, ldx=2048, lddy=2048) for _ in range(8)]
+    arr = (_lib.DrLayer * 8)(*layers)
+    ws = lib.dr_update_workspace_size(arr, 8, 64, 512, _lib.DR_BF16)
+    assert ws > 0 and ws % 256 == 0
+    assert update_call(lib, layers, n=64, T=512, ldw=64, dtype=_lib.DR_BF16, ws=FAKE, wsb=ws - 1) == \
+        _lib.DR_ERR_WORKSPACE
+    assert lib.dr_update_workspace_size(arr, 8, -1, 512, _lib.DR_BF16) == 0
