@@ -5,26 +5,33 @@
 // mean g_S; span or cone weights give u = G^T w of Eq. (proj)).
 //
 // Kernels
-//   update_plan_kernel   one workgroup per layer: the examples with w != 0
-//                        and len > 0 in ascending order, their clamped
-//                        lengths and weights (examples with w = 0 are never
-//                        read).
-//   update_bf16_kernel   one 256 (d_out) x 128 (d_in) tile per workgroup, 8
-//                        waves of 64 x 64.  Tokens go through a 3-stage LDS
-//                        ring in steps of 32, filled by buffer->LDS DMA in
-//                        their natural token-major layout; both MFMA operands
-//                        need 8 consecutive tokens per lane, which the gfx950
-//                        transposing LDS read (ds_read_b64_tr_b16) delivers
-//                        straight from that layout.  Each example accumulates
-//                        in fp32 (bf16 products are exact) and is added,
-//                        times its weight, to a second fp32 accumulator when
-//                        the weight changes (once for top-k weights).
-//   update_f32_kernel    the same for fp32 inputs: 64 x 64 tiles, 4 waves of
-//                        32 x 32, fp32 MFMA 16x16x4, staged by plain loads.
+//   update_plan_kernel   one workgroup per example list (one list per
+//                        distinct weight row): the examples with w != 0 and
+//                        len > 0, their clamped lengths and weights.
+//   update_sort_kernel   orders each list by |w| ascending (index breaks
+//                        ties) by ranking every entry against all others.
+//   update_bf16_kernel   one 256 x 256 tile of U per workgroup, 8 waves of
+//                        128 (d_out) x 64 (d_in).  Tokens go through a
+//                        4-stage LDS ring in steps of 32, filled by
+//                        buffer->LDS DMA in their natural token-major
+//                        layout; both MFMA operands need 8 consecutive
+//                        tokens per lane, which the gfx950 transposing LDS
+//                        read (ds_read_b64_tr_b16) delivers straight from
+//                        that layout.  One fp32 accumulator holds
+//                        sum_e (w_e / w_cur) P_e: when the weight changes
+//                        from w_cur to w_next it is multiplied by
+//                        w_cur / w_next, and by the last weight at the end.
+//                        The |w|-ascending order keeps every factor within
+//                        [-1, 1] (no overflow whatever the weights), and a
+//                        run of equal weights (all of them for top-k)
+//                        costs no rescaling at all.
+//   update_f32_kernel    fp32 inputs: 64 x 64 tiles, 4 waves of 32 x 32,
+//                        fp32 MFMA 16x16x4, staged by plain loads; per
+//                        example sums added to a second accumulator.
 //   update_reduce_kernel when there are fewer tiles than CUs the example
 //                        list of a tile is split over `split` workgroups;
 //                        their partial tiles are summed in split order.
-// Determinism: every sum runs in a fixed order (examples ascending, tokens
+// Determinism: every sum runs in a fixed order (the sorted list, tokens
 // ascending, splits ascending); no atomics.
 
 #include "common.h"
@@ -36,12 +43,12 @@ constexpr int kMaxUpdLayers = 16;
 constexpr int kMaxSplit = 32;
 
 // bf16 tile
-constexpr int kBO = 256, kBI = 128, kBK = 32;
+constexpr int kBO = 256, kBI = 256, kBK = 32;
 constexpr int kBThreads = 512;
 constexpr int kBDyBytes = kBK * kBO * 2;   // 16 KB: 32 token rows of 512 bytes
-constexpr int kBXBytes = kBK * kBI * 2;    // 8 KB: 32 token rows of 256 bytes
+constexpr int kBXBytes = kBK * kBI * 2;    // 16 KB
 constexpr int kBStage = kBDyBytes + kBXBytes;
-constexpr int kBStages = 3;
+constexpr int kBStages = 4;
 
 // f32 tile
 constexpr int kFO = 64, kFI = 64, kFK = 16;
@@ -67,10 +74,13 @@ struct UpdArgs {
   int split;             // workgroups per tile along the example list
   int n;                 // list stride (>= 1)
   int nw;                // weighted examples (may be 0)
-  const int* ex;         // [lists][n] selected examples, ascending
+  const int* ex;         // [lists][n] selected examples, |w| ascending
   const int* exlen;      // [lists][n] their clamped lengths (> 0)
   const float* exw;      // [lists][n] their weights (!= 0)
   const int* cnt;        // [lists] list lengths
+  int* uex;              // [lists][n] the same lists before sorting
+  int* ulen;
+  float* uw;
   float* partial;        // [ntiles * split][tile elements] when split > 1
 };
 
@@ -87,9 +97,9 @@ __global__ __launch_bounds__(1024) void update_plan_kernel(const float* w, long 
   const int j = blockIdx.x;                 // layer slot of the launch
   const int list = list0 + j;
   const float* wr = w + (long long)rs.r[j] * ldw;
-  int* ex = const_cast<int*>(a.ex) + (long long)list * a.n;
-  int* exlen = const_cast<int*>(a.exlen) + (long long)list * a.n;
-  float* exw = const_cast<float*>(a.exw) + (long long)list * a.n;
+  int* ex = a.uex + (long long)list * a.n;
+  int* exlen = a.ulen + (long long)list * a.n;
+  float* exw = a.uw + (long long)list * a.n;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid == 0) base_s = 0;
   __syncthreads();
@@ -123,6 +133,34 @@ __global__ __launch_bounds__(1024) void update_plan_kernel(const float* w, long 
     __syncthreads();
   }
   if (tid == 0) const_cast<int*>(a.cnt)[list] = base_s;
+}
+
+// entry i of a list goes to position #{j : (|w_j|, ex_j) < (|w_i|, ex_i)}
+__global__ __launch_bounds__(256) void update_sort_kernel(UpdArgs a) {
+  __shared__ float kw[256];
+  __shared__ int ki[256];
+  const int list = blockIdx.y;
+  const int cnt = a.cnt[list];
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (blockIdx.x * 256 >= cnt) return;
+  const long long base = (long long)list * a.n;
+  const float wi = i < cnt ? fabsf(a.uw[base + i]) : 0.f;
+  const int xi = i < cnt ? a.uex[base + i] : 0;
+  int rank = 0;
+  for (int j0 = 0; j0 < cnt; j0 += 256) {
+    __syncthreads();
+    const int j = j0 + threadIdx.x;
+    kw[threadIdx.x] = j < cnt ? fabsf(a.uw[base + j]) : 0.f;
+    ki[threadIdx.x] = j < cnt ? a.uex[base + j] : 0;
+    __syncthreads();
+    const int m = cnt - j0 < 256 ? cnt - j0 : 256;
+    for (int q = 0; q < m; ++q) rank += (kw[q] < wi || (kw[q] == wi && ki[q] < xi)) ? 1 : 0;
+  }
+  if (i < cnt) {
+    const_cast<int*>(a.ex)[base + rank] = xi;
+    const_cast<int*>(a.exlen)[base + rank] = a.ulen[base + i];
+    const_cast<float*>(a.exw)[base + rank] = a.uw[base + i];
+  }
 }
 
 // which layer / tile / split a workgroup runs.  Workgroup b runs on XCD
@@ -178,24 +216,19 @@ __global__ __launch_bounds__(kBThreads) void update_bf16_kernel(UpdArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  // DMA roles: dy rows 2w, 2w + 1 and 2w + 16, 2w + 17 (two 1 KB wave
-  // loads), x rows 4w .. 4w + 3 (one).  Lane l fills 16 bytes: physical
-  // slot u / 2, half u % 2 of its row.
-  int rdy[2], rx;
-  unsigned cdy[2], cx;   // byte column inside a token row, or kOobOffset
+  // DMA roles: both tiles have 32 token rows of 512 bytes; wave w fills
+  // rows 2w, 2w + 1 and 2w + 16, 2w + 17 of each (1 KB per wave load).
+  // Lane l fills 16 bytes: physical slot u / 2, half u % 2 of its row.
+  int rrow[2];
+  unsigned cdy[2], cx[2];   // byte column inside a token row, or kOobOffset
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int j = w + 8 * h;
     const int r = 2 * j + (lane >> 5), u = lane & 31;
     const int col = 16 * ((u >> 1) ^ slot_xor(r)) + 8 * (u & 1);
-    rdy[h] = r;
+    rrow[h] = r;
     cdy[h] = o0 + col < d_out ? (unsigned)((o0 + col) * 2) : kOobOffset;
-  }
-  {
-    const int r = 4 * w + (lane >> 4), u = lane & 15;
-    const int col = 16 * ((u >> 1) ^ slot_xor(r)) + 8 * (u & 1);
-    rx = r;
-    cx = i0 + col < d_in ? (unsigned)((i0 + col) * 2) : kOobOffset;
+    cx[h] = i0 + col < d_in ? (unsigned)((i0 + col) * 2) : kOobOffset;
   }
   const unsigned rowb_dy = (unsigned)(Lr.lddy * 2), rowb_x = (unsigned)(Lr.ldx * 2);
 
@@ -203,18 +236,17 @@ __global__ __launch_bounds__(kBThreads) void update_bf16_kernel(UpdArgs a) {
   auto issue = [&](int st) {
     unsigned char* sb = lds + st * kBStage;
     __amdgpu_buffer_rsrc_t rdys, rxs;
-    unsigned o_dy[2], o_x;
+    unsigned o_dy[2], o_x[2];
     if (ie < e_hi) {
       const long long e = ex[ie];
       rdys = make_rsrc(Lr.dy + e * Lr.exdy, kOobOffset);
       rxs = make_rsrc(Lr.x + e * Lr.exx, kOobOffset);
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        const int t = it + rdy[h];
+        const int t = it + rrow[h];
         o_dy[h] = (t < ilen && cdy[h] != kOobOffset) ? (unsigned)t * rowb_dy + cdy[h] : kOobOffset;
+        o_x[h] = (t < ilen && cx[h] != kOobOffset) ? (unsigned)t * rowb_x + cx[h] : kOobOffset;
       }
-      const int t = it + rx;
-      o_x = (t < ilen && cx != kOobOffset) ? (unsigned)t * rowb_x + cx : kOobOffset;
       it += kBK;
       if (it >= ilen) {
         ++ie;
@@ -224,11 +256,12 @@ __global__ __launch_bounds__(kBThreads) void update_bf16_kernel(UpdArgs a) {
     } else {
       rdys = make_rsrc(Lr.dy, kOobOffset);
       rxs = make_rsrc(Lr.x, kOobOffset);
-      o_dy[0] = o_dy[1] = o_x = kOobOffset;
+      o_dy[0] = o_dy[1] = o_x[0] = o_x[1] = kOobOffset;
     }
     dma16<kAuxCached>(rdys, sb + w * 1024, o_dy[0]);
     dma16<kAuxCached>(rdys, sb + (w + 8) * 1024, o_dy[1]);
-    dma16<kAuxCached>(rxs, sb + kBDyBytes + w * 1024, o_x);
+    dma16<kAuxCached>(rxs, sb + kBDyBytes + w * 1024, o_x[0]);
+    dma16<kAuxCached>(rxs, sb + kBDyBytes + (w + 8) * 1024, o_x[1]);
   };
 
   // fragment reads: lane (g, q, r) of the transposing read addresses token
@@ -236,46 +269,47 @@ __global__ __launch_bounds__(kBThreads) void update_bf16_kernel(UpdArgs a) {
   // block; the block's logical slot is XOR-ed with the row's swizzle.
   const int g = lane >> 4, q = (lane >> 2) & 3, rr = lane & 3;
   const int fx = q | ((g & 1) << 2);
-  const int wo = w >> 1, wi = w & 1;
-  unsigned offa[4], offb[4];
+  const int wr = w >> 2, wc = w & 3;   // 128-row half (d_out), 64-column quarter (d_in)
+  const unsigned rbase = (unsigned)((8 * g + q) * 512 + rr * 8);
+  unsigned offa[8], offb[4];
 #pragma unroll
-  for (int b = 0; b < 4; ++b) {
-    offa[b] = (unsigned)((8 * g + q) * 512 + (((4 * wo + b) ^ fx) * 32) + rr * 8);
-    offb[b] = (unsigned)(kBDyBytes + (8 * g + q) * 256 + (((4 * wi + b) ^ fx) * 32) + rr * 8);
-  }
+  for (int b = 0; b < 8; ++b) offa[b] = rbase + (unsigned)(((8 * wr + b) ^ fx) * 32);
+#pragma unroll
+  for (int b = 0; b < 4; ++b) offb[b] = kBDyBytes + rbase + (unsigned)(((4 * wc + b) ^ fx) * 32);
 
-  f32x4 acc[4][4], tot[4][4];
+  f32x4 acc[8][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-      tot[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  float wlast = 0.f;
   int ce = e_lo, ct = 0, clen = ce < e_hi ? exlen[ce] : 0;
   if (ce < e_hi) {
-    issue(0);
-    issue(1);
+#pragma unroll
+    for (int st = 0; st < kBStages - 1; ++st) issue(st);
     for (int step = 0; ce < e_hi; ++step) {
-      DR_WAIT_VM(3);
+      DR_WAIT_VM(4 * (kBStages - 2));   // this step's four loads are done; later steps' may be in flight
       DR_LDS_SYNC();
-      issue((step + 2) % kBStages);
+      issue((step + kBStages - 1) % kBStages);
       const unsigned char* sb = lds + (step % kBStages) * kBStage;
-      u32x4 fa[4], fb[4];
+      u32x4 fa[8], fb[4];
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
+        const v4s lo = lds_read_tr16(sb + offb[b]);
+        const v4s hi = lds_read_tr16(sb + offb[b] + 4 * 512);
+        fb[b] = u32x4{__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
+                      __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y};
+      }
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
         const v4s lo = lds_read_tr16(sb + offa[b]);
         const v4s hi = lds_read_tr16(sb + offa[b] + 4 * 512);
         fa[b] = u32x4{__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
                       __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y};
-        const v4s lo2 = lds_read_tr16(sb + offb[b]);
-        const v4s hi2 = lds_read_tr16(sb + offb[b] + 4 * 256);
-        fb[b] = u32x4{__builtin_bit_cast(uint2, lo2).x, __builtin_bit_cast(uint2, lo2).y,
-                      __builtin_bit_cast(uint2, hi2).x, __builtin_bit_cast(uint2, hi2).y};
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 8; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = mma_bf16(fa[i], fb[j], acc[i][j]);
       ct += kBK;
@@ -284,15 +318,18 @@ __global__ __launch_bounds__(kBThreads) void update_bf16_kernel(UpdArgs a) {
         ++ce;
         ct = 0;
         clen = ce < e_hi ? exlen[ce] : 0;
-        if (ce >= e_hi || exw[ce] != we) {
+        wlast = we;
+        if (ce < e_hi) {
+          const float wn = exw[ce];
+          if (wn != we) {
+            const float f = we / wn;   // |f| <= 1 in the sorted order
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < 8; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+              for (int j = 0; j < 4; ++j)
 #pragma unroll
-              for (int r = 0; r < 4; ++r) tot[i][j][r] = fmaf(we, acc[i][j][r], tot[i][j][r]);
-              acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-            }
+                for (int r = 0; r < 4; ++r) acc[i][j][r] *= f;
+          }
         }
       }
     }
@@ -303,27 +340,27 @@ __global__ __launch_bounds__(kBThreads) void update_bf16_kernel(UpdArgs a) {
   const int lc = lane & 15;
   if (a.split == 1) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int o = o0 + 64 * wo + 16 * i + 4 * g + r;
+        const int o = o0 + 128 * wr + 16 * i + 4 * g + r;
         if (o >= d_out) continue;
         float* urow = Lr.U + (long long)o * d_in;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int c = i0 + 64 * wi + 16 * j + lc;
-          if (c < d_in) urow[c] = tot[i][j][r];
+          const int c = i0 + 64 * wc + 16 * j + lc;
+          if (c < d_in) urow[c] = wlast * acc[i][j][r];
         }
       }
   } else {
     float* P = a.partial + (long long)item * (kBO * kBI);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          P[(64 * wo + 16 * i + 4 * g + r) * kBI + 64 * wi + 16 * j + lc] = tot[i][j][r];
+          P[(128 * wr + 16 * i + 4 * g + r) * kBI + 64 * wc + 16 * j + lc] = wlast * acc[i][j][r];
   }
 }
 
@@ -467,7 +504,7 @@ __global__ __launch_bounds__(256) void update_reduce_kernel(UpdArgs a, int TO, i
 struct UpdPlan {
   int64_t tiles;     // all layers
   int split;
-  size_t off_ex, off_len, off_w, off_cnt, off_partial, bytes;
+  size_t off_ex, off_len, off_w, off_uex, off_ulen, off_uw, off_cnt, off_partial, bytes;
 };
 
 int cu_count() {
@@ -490,8 +527,8 @@ UpdPlan update_plan(const dr_layer* layers, int num_layers, int64_t n, dr_dtype 
   p.tiles = 0;
   for (int l = 0; l < num_layers; ++l)
     p.tiles += ((layers[l].d_out + TO - 1) / TO) * ((layers[l].d_in + TI - 1) / TI);
-  // resident workgroups: one bf16 workgroup (72 KB of LDS, 8 waves) or four
-  // f32 workgroups per CU
+  // resident workgroups: one bf16 workgroup (128 KB of LDS, 8 waves) or
+  // four f32 workgroups per CU
   const int64_t slots = (int64_t)cu_count() * (dtype == DR_BF16 ? 1 : 4);
   int64_t split = 1;
   if (p.tiles < slots && n > 1) {
@@ -505,6 +542,9 @@ UpdPlan update_plan(const dr_layer* layers, int num_layers, int64_t n, dr_dtype 
   p.off_ex = o;      o = align_up(o + nn * 4, 256);
   p.off_len = o;     o = align_up(o + nn * 4, 256);
   p.off_w = o;       o = align_up(o + nn * 4, 256);
+  p.off_uex = o;     o = align_up(o + nn * 4, 256);
+  p.off_ulen = o;    o = align_up(o + nn * 4, 256);
+  p.off_uw = o;      o = align_up(o + nn * 4, 256);
   p.off_cnt = o;     o = align_up(o + (size_t)num_layers * 4, 256);
   p.off_partial = o;
   if (p.split > 1) o = align_up(o + (size_t)p.tiles * p.split * TO * TI * 4, 256);
@@ -566,11 +606,45 @@ extern "C" dr_status dr_assemble_update(const dr_layer* layers, int num_layers, 
   int TO, TI;
   tile_dims(dtype, TO, TI);
   const int64_t es = dtype == DR_BF16 ? 2 : 4;
-  const int nlist = n > 0 ? (int)n : 1;
+  const int nstride = n > 0 ? (int)n : 1;
+  // one example list per distinct weight row, in order of first use
+  int* layer_list = new int[num_layers];
+  int* list_row = new int[num_layers];
+  int nlists = 0;
+  for (int l = 0; l < num_layers; ++l) {
+    const int row = group_of_layer ? group_of_layer[l] : 0;
+    int q = 0;
+    while (q < nlists && list_row[q] != row) ++q;
+    if (q == nlists) list_row[nlists++] = row;
+    layer_list[l] = q;
+  }
+  UpdArgs base = {};
+  base.split = pl.split;
+  base.n = nstride;
+  base.nw = (int)n;
+  base.ex = reinterpret_cast<const int*>(ws + pl.off_ex);
+  base.exlen = reinterpret_cast<const int*>(ws + pl.off_len);
+  base.exw = reinterpret_cast<const float*>(ws + pl.off_w);
+  base.uex = reinterpret_cast<int*>(ws + pl.off_uex);
+  base.ulen = reinterpret_cast<int*>(ws + pl.off_ulen);
+  base.uw = reinterpret_cast<float*>(ws + pl.off_uw);
+  base.cnt = reinterpret_cast<const int*>(ws + pl.off_cnt);
+  base.partial = reinterpret_cast<float*>(ws + pl.off_partial);
+  for (int first = 0; first < nlists && st == DR_OK; first += kMaxUpdLayers) {
+    const int count = nlists - first < kMaxUpdLayers ? nlists - first : kMaxUpdLayers;
+    RowSel rs;
+    for (int j = 0; j < kMaxUpdLayers; ++j) rs.r[j] = j < count ? list_row[first + j] : 0;
+    hipLaunchKernelGGL(update_plan_kernel, dim3(count), dim3(1024), 0, hs, w, (long long)ldw, base, len, (int)T,
+                       first, rs);
+    st = launch_status();
+  }
+  if (st == DR_OK && n > 0) {
+    hipLaunchKernelGGL(update_sort_kernel, dim3((unsigned)((n + 255) / 256), nlists), dim3(256), 0, hs, base);
+    st = launch_status();
+  }
   for (int first = 0; first < num_layers && st == DR_OK; first += kMaxUpdLayers) {
     const int count = num_layers - first < kMaxUpdLayers ? num_layers - first : kMaxUpdLayers;
-    UpdArgs a = {};
-    int rows[kMaxUpdLayers];
+    UpdArgs a = base;
     int tiles = 0;
     for (int j = 0; j < count; ++j) {
       const dr_layer& L = layers[first + j];
@@ -585,26 +659,12 @@ extern "C" dr_status dr_assemble_update(const dr_layer* layers, int num_layers, 
       la.d_out = (int)L.d_out;
       la.ti = (int)((L.d_in + TI - 1) / TI);
       la.tile0 = tiles;
-      la.list = first + j;
+      la.list = layer_list[first + j];
       la.U = U + u_offset[first + j];
       tiles += (int)(((L.d_out + TO - 1) / TO) * la.ti);
-      rows[j] = group_of_layer ? group_of_layer[first + j] : 0;
     }
     a.num_layers = count;
     a.ntiles = tiles;
-    a.split = pl.split;
-    a.n = nlist;
-    a.nw = (int)n;
-    a.ex = reinterpret_cast<const int*>(ws + pl.off_ex);
-    a.exlen = reinterpret_cast<const int*>(ws + pl.off_len);
-    a.exw = reinterpret_cast<const float*>(ws + pl.off_w);
-    a.cnt = reinterpret_cast<const int*>(ws + pl.off_cnt);
-    a.partial = reinterpret_cast<float*>(ws + pl.off_partial);
-    RowSel rs;
-    for (int j = 0; j < kMaxUpdLayers; ++j) rs.r[j] = j < count ? rows[j] : 0;
-    hipLaunchKernelGGL(update_plan_kernel, dim3(count), dim3(1024), 0, hs, w, (long long)ldw, a, len, (int)T, first,
-                       rs);
-    if ((st = launch_status()) != DR_OK) break;
     const int items = tiles * pl.split;
     const int grid = (items + 7) / 8 * 8;
     if (dtype == DR_BF16)
@@ -617,5 +677,7 @@ extern "C" dr_status dr_assemble_update(const dr_layer* layers, int num_layers, 
       st = launch_status();
     }
   }
+  delete[] layer_list;
+  delete[] list_row;
   return st;
 }

@@ -199,3 +199,27 @@ def test_llama_down_proj_full_size_sampled_entries():
     cols = [0, 7, 127, 128, 8191, 8192, 14000, 14335]
     _, errs = check([dict(x=x, dy=dy)], w, n, None, rows=rows, cols=cols)
     print(f"llama down_proj max rel err {errs.max():.2e}")
+
+
+def test_weights_spanning_sixty_orders_of_magnitude():
+    """The kernel rescales one accumulator by w_prev / w_next in |w| order:
+    weights from 1e-30 to 1e30 with both signs must neither overflow nor
+    lose the large terms."""
+    n, T = 24, 64
+    lens = torch.randint(1, T + 1, (n,), dtype=torch.int32, device=DEV)
+    layers = make_layers([(256, 256), (64, 200)], n, T, torch.bfloat16, lens, seed=12)
+    mags = torch.logspace(-30, 30, n, device=DEV)
+    signs = torch.tensor([1.0, -1.0] * (n // 2), device=DEV)
+    perm = torch.randperm(n, generator=torch.Generator().manual_seed(3)).to(DEV)
+    w = (mags * signs)[perm].contiguous()
+    w[5] = w[7]                                       # a tie in |w| and sign
+    _, errs = check(layers, w, n, lens)
+    print(f"wide-range weights max layer rel err {errs.max():.2e}")
+    # the largest weights dominate: the same update from the top 3 alone is close
+    top = torch.zeros_like(w)
+    big = torch.argsort(w.abs(), descending=True)[:3]
+    top[big] = w[big]
+    Ua = api.assemble_update(layers, w, n=n, lengths=lens)
+    Ub = api.assemble_update(layers, top, n=n, lengths=lens)
+    for a, b in zip(Ua, Ub):
+        assert rel(host64(a), host64(b)) <= 1e-5
