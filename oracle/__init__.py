@@ -20,6 +20,8 @@ written for a reader who checks it against the paper by eye:
 * ``cone``    -- Eq. (proj) onto the convex cone of the general-data
   gradients (non-negative least squares, exact active-set solver).
 * ``topk``    -- the top-k rule of Sec. 3.3.2 with lowest-index tie break.
+* ``select``  -- thresholding / negative filtering and greedy construction,
+  the other subset rules of Sec. 3.3.2.
 * ``update``  -- the weighted assembly of the update in parameter space
   (Sec. 4.2, post-hoc assembly from the retained pairs).
 * ``brute``   -- exhaustive enumeration for tiny inputs.
@@ -34,6 +36,7 @@ from .span import ridge_lambda, span_ref, span_residual2, combine_ref
 from .cone import nnls_active_set, cone_ref, cone_kkt_residual, cone_pg_replay
 from .topk import topk_ref
 from .update import update_ref
+from .select import threshold_ref, greedy_ref, subset_objective
 from . import brute
 
 __all__ = [
@@ -42,5 +45,5 @@ __all__ = [
     "gram_ref",
     "ridge_lambda", "span_ref", "span_residual2", "combine_ref",
     "nnls_active_set", "cone_ref", "cone_kkt_residual", "cone_pg_replay",
-    "topk_ref", "update_ref", "brute",
+    "topk_ref", "update_ref", "threshold_ref", "greedy_ref", "subset_objective", "brute",
 ]

@@ -493,3 +493,71 @@ def test_update_sketch_equals_weighted_sum_of_sketches_per_group():
         want = sum(w[g, i] * S[i] for i in rows)
         got = (L["p_out"] @ U[li] @ L["p_in"].T).reshape(-1)
         np.testing.assert_allclose(got, want, rtol=1e-11, atol=1e-11)
+
+
+# --------------------------------------------------------------------------
+# Thresholding and greedy selection oracles
+# --------------------------------------------------------------------------
+
+def test_selection_hand_fixture(golden_dir):
+    fx = _load(golden_dir, "select_hand.json")
+    s = np.array(fx["s"], dtype=float)
+    K = np.array(fx["K"], dtype=float)
+    for c in fx["threshold"]:
+        idx, w = oracle.threshold_ref(s, c["tau"], c["inclusive"])
+        assert idx.tolist() == c["idx"]
+        np.testing.assert_array_equal(w[idx], np.full(len(idx), 1.0 / max(1, len(idx))))
+    idx, order = oracle.greedy_ref(K, s, fx["greedy"]["k"])
+    assert order.tolist() == fx["greedy"]["order"]
+    assert oracle.topk_ref(s, fx["greedy"]["k"]).tolist() == fx["greedy"]["topk"]
+    for S, f in fx["objective"]:
+        assert oracle.subset_objective(K, s, S) == pytest.approx(f, rel=1e-15, abs=1e-15)
+
+
+def test_threshold_against_comparisons_and_errors():
+    rng = np.random.default_rng(4)
+    s = np.round(rng.standard_normal(40), 1)          # many exact ties and zeros
+    s[3] = 0.0
+    s[7] = -0.0
+    for tau, inc in [(0.0, True), (0.0, False), (0.3, False), (-0.5, True), (9.0, False)]:
+        idx, w = oracle.threshold_ref(s, tau, inc)
+        want = np.flatnonzero(s >= tau) if inc else np.flatnonzero(s > tau)
+        assert idx.tolist() == want.tolist()
+        assert w.sum() == pytest.approx(1.0 if len(want) else 0.0)
+    assert 3 in oracle.threshold_ref(s, 0.0, True)[0] and 7 in oracle.threshold_ref(s, 0.0, True)[0]
+    with pytest.raises(ValueError):
+        oracle.threshold_ref(np.array([1.0, np.nan]), 0.0)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_greedy_matches_topk_for_orthogonal_equal_norm_gradients(seed):
+    """K = cI: f(S) = c/|S| - (2/|S|) sum s, so every greedy step adds the
+    largest remaining score -- the top-k set, ties to the lowest index."""
+    rng = np.random.default_rng(seed)
+    n, k = 12, 5
+    s = np.round(rng.standard_normal(n), 1)
+    idx, _ = oracle.greedy_ref(2.5 * np.eye(n), s, k)
+    assert idx.tolist() == oracle.topk_ref(s, k).tolist()
+
+
+@pytest.mark.parametrize("seed", [3, 4])
+def test_greedy_steps_are_best_single_additions_by_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    n, k = 9, 5
+    Gm = rng.standard_normal((n, 6))
+    gstar = rng.standard_normal(6)
+    K, s = Gm @ Gm.T, Gm @ gstar
+    _, order = oracle.greedy_ref(K, s, k)
+    S = []
+    for c in order:
+        cands = [j for j in range(n) if j not in S]
+        vals = [oracle.subset_objective(K, s, S + [j]) for j in cands]
+        assert c == cands[int(np.argmin(vals))]
+        # the objective is the S-dependent part of the projection distance
+        g_S = Gm[S + [c]].mean(axis=0)
+        assert np.sum((g_S - gstar) ** 2) - gstar @ gstar == pytest.approx(min(vals), rel=1e-10, abs=1e-10)
+        S.append(c)
+    # k = 1 closed form: argmin K_cc - 2 s_c
+    assert oracle.greedy_ref(K, s, 1)[0].tolist() == [int(np.argmin(np.diag(K) - 2 * s))]
+    with pytest.raises(ValueError):
+        oracle.greedy_ref(K, np.where(np.arange(n) == 2, np.nan, s), 2)
