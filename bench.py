@@ -25,6 +25,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "sketched per-example grads/sec + projection steps/sec; % of MFMA/HBM peak"
 HBM_PEAK_GBS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
 
 
 def parse():
@@ -213,9 +214,70 @@ def main():
         },
     }
 
+    out["next_rows"] = time_next_rows(api, layers, lens, n, T, wt, wc, goff, dev, K=K, s=s)
+
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layers, lens, S, K, s, t2, n, m, k_top, lam, cfg, args.cpu_seconds, goff)
     print(json.dumps(out), flush=True)
+
+
+def _event_ms(fn, reps):
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def time_next_rows(api, layers, lens, n, T, wt, wc, goff, dev, K=None, s=None, reps=20):
+    """Stages after the path, timed on their own (not part of `value`): the
+    update assembly in parameter space for the step's top-k weights (the
+    paper's subset mean) and for its cone weights; the thresholding
+    (negative score filtering) and greedy subset rules on the step's K, s."""
+    import numpy as np
+    import torch
+    ul = [dict(x=L["x"], dy=L["dy"]) for L in layers]
+    sizes = [L["dy"].shape[2] * L["x"].shape[2] for L in layers]
+    offs = [int(v) for v in np.cumsum([0] + sizes[:-1])]
+    U = torch.empty(sum(sizes), device=dev)
+    P = wt.shape[0]
+    gol = None if P == 1 else list(range(len(layers)))
+    ws = torch.empty(max(1, api.dr_update_workspace_size(ul, n, T, torch.bfloat16)), dtype=torch.uint8, device=dev)
+    lh = lens[:n].cpu().numpy().astype(np.int64)
+    res = {}
+    for name, w in (("update_topk", wt), ("update_cone", wc)):
+        wh = w.cpu().numpy()
+        flops = 0.0
+        for li, L in enumerate(layers):
+            row = 0 if P == 1 else li
+            flops += 2.0 * float(lh[wh[row] != 0].sum()) * L["x"].shape[2] * L["dy"].shape[2]
+        ms = _event_ms(lambda: api.dr_assemble_update(ul, n, T, lens, w, U, offs, group_of_layer=gol,
+                                                       workspace=ws), reps)
+        tf = flops / (ms * 1e-3) / 1e12
+        res[name] = {"ms": ms, "examples": int((wh != 0).any(axis=0).sum()),
+                     "roofline": {"kernel": "dr_assemble_update (update_plan_kernel + update_sort_kernel + "
+                                            "update_bf16_kernel)",
+                                  "bound": "mfma", "achieved": tf, "peak": BF16_MFMA_PEAK_TFLOPS,
+                                  "unit": "TFLOP/s", "frac": tf / BF16_MFMA_PEAK_TFLOPS,
+                                  "algorithmic_flops": flops}}
+    if K is not None:
+        P, nn = s.shape
+        idx = torch.empty(P, nn, dtype=torch.int32, device=dev)
+        cnt = torch.empty(P, dtype=torch.int32, device=dev)
+        wq = torch.empty(P, nn, device=dev)
+        info = torch.empty(P, dtype=torch.int32, device=dev)
+        res["select_negative_filter_ms"] = _event_ms(
+            lambda: api.dr_select_threshold(s, 0.0, True, idx, cnt, wq, info), reps)
+        kk = nn // 2
+        gidx = torch.empty(P, kk, dtype=torch.int32, device=dev)
+        gws = torch.empty(max(1, api.dr_greedy_workspace_size(nn, P)), dtype=torch.uint8, device=dev)
+        res["select_greedy_ms"] = _event_ms(lambda: api.dr_select_greedy(K, s, kk, gidx, wq, info, workspace=gws), reps)
+    return res
 
 
 SKETCH_SOURCES = ["paper_2605_07063_amd/csrc/sketch.hip", "paper_2605_07063_amd/csrc/common.h"]

@@ -215,6 +215,42 @@ dr_status dr_select_topk(const float* s, int64_t n, int P, int64_t k, int32_t* i
                          int32_t* info, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * dr_select_threshold -- the thresholding rule of Sec. 3.3.2 (keep every
+ * example whose score exceeds a fixed threshold: a subset of variable
+ * size), per group.  inclusive = 0 keeps s[p][i] > tau; inclusive = 1 keeps
+ * s[p][i] >= tau, so (tau = 0, inclusive = 1) is the negative score
+ * filtering of the RL experiments of Sec. 5 (drop the negative scores).
+ *   s [P][n] fp32; tau finite (else DR_ERR_ARG); n <= 2^30.
+ *   idx   int32 [P][n] or NULL: the kept indices in ascending order, then -1.
+ *   count int32 [P] (required): |S_p|.
+ *   w     fp32 [P][n] or NULL: 1/|S_p| on the kept set, 0 elsewhere (u =
+ *         G^T w is the subset mean g_S; all zero when nothing is kept).
+ *   info  int32 [P]: 0, or DR_INFO_NONFINITE if s[p] holds a NaN (then
+ *         count = 0, idx = -1, w = 0).
+ * ------------------------------------------------------------------------- */
+dr_status dr_select_threshold(const float* s, int64_t n, int P, float tau, int inclusive, int32_t* idx,
+                              int32_t* count, float* w, int32_t* info, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * dr_select_greedy -- the greedy construction of Sec. 3.3.2, per group:
+ * starting from the empty set, k times add the example c whose addition
+ * minimises the full subset objective
+ *   f(S) = ||g_S||^2 - 2 <g_S, gbar> = (1/|S|^2) sum_{S x S} K - (2/|S|) sum_S s
+ * (alignment and redundancy, the latter ignored by top-k), ties to the
+ * lowest index.  f is evaluated in fp64 from the fp32 K and s.
+ *   K [P][n][n] fp32 symmetric, s [P][n]; 0 <= k <= n <= 16384 (larger n:
+ *   DR_ERR_UNSUPPORTED).
+ *   idx int32 [P][k]: the chosen set in ascending index order.
+ *   w   fp32 [P][n] or NULL: 1/k on the set, 0 elsewhere.
+ *   info int32 [P]: 0, or DR_INFO_NONFINITE if K_p or s_p holds a NaN
+ *   (then idx = -1, w = 0).
+ *   workspace: at least dr_greedy_workspace_size(n, P) bytes.
+ * ------------------------------------------------------------------------- */
+dr_status dr_select_greedy(const float* K, const float* s, int64_t n, int P, int64_t k, int32_t* idx, float* w,
+                           int32_t* info, void* workspace, size_t ws_bytes, void* stream);
+size_t dr_greedy_workspace_size(int64_t n, int P);
+
+/* ---------------------------------------------------------------------------
  * dr_combine -- the update direction in sketch space, u = G_p^T w_p per
  * group (the assembled update of Eq. (proj) for span and cone weights, or
  * the subset mean g_S for top-k weights).

@@ -71,18 +71,17 @@ def greedy_ref(K, s, k):
         raise ValueError("NaN input")
     chosen = []
     in_set = np.zeros(n, dtype=bool)
+    diag = np.diag(K).copy()
     A = 0.0
     B = 0.0
     r = np.zeros(n)
     for step in range(k):
-        t = step + 1
-        best, best_f = -1, None
-        for c in range(n):
-            if in_set[c]:
-                continue
-            f = (A + 2.0 * r[c] + K[c, c]) / (t * t) - 2.0 * (B + s[c]) / t
-            if best_f is None or f < best_f:
-                best, best_f = c, f
+        t = float(step + 1)
+        # f(S + c) for every candidate at once (the same operations, in the
+        # same order, as the formula above applied to each c)
+        f = (A + 2.0 * r + diag) / (t * t) - 2.0 * (B + s) / t
+        f[in_set] = np.inf
+        best = int(np.argmin(f))          # first minimum: lowest index on ties
         A = A + 2.0 * r[best] + K[best, best]
         B = B + s[best]
         r = r + K[best]

@@ -176,6 +176,43 @@ def dr_select_topk(s, k, idx, w, info, stream=None):
                                                _stream(stream)))
 
 
+def dr_select_threshold(s, tau, inclusive, idx, count, w, info, stream=None):
+    """Keep s_i > tau (or >= tau when inclusive) per group; idx ascending then -1."""
+    lib = _lib.load()
+    _dev(s, "s", torch.float32)
+    _contig(s, "s")
+    P, n = s.shape
+    for t, nm, dt in ((count, "count", torch.int32), (info, "info", torch.int32)):
+        _dev(t, nm, dt)
+    if idx is not None:
+        _dev(idx, "idx", torch.int32)
+    if w is not None:
+        _dev(w, "w", torch.float32)
+    check("dr_select_threshold", lib.dr_select_threshold(_ptr(s), n, P, float(tau), 1 if inclusive else 0, _ptr(idx),
+                                                         _ptr(count), _ptr(w), _ptr(info), _stream(stream)))
+
+
+def dr_greedy_workspace_size(n, P):
+    return _lib.load().dr_greedy_workspace_size(n, P)
+
+
+def dr_select_greedy(K, s, k, idx, w, info, workspace=None, stream=None):
+    """Greedy subset of size k on the full objective, per group (ascending idx)."""
+    lib = _lib.load()
+    _dev(K, "K", torch.float32)
+    _dev(s, "s", torch.float32)
+    _contig(K, "K")
+    _contig(s, "s")
+    P, n = s.shape
+    _dev(idx, "idx", torch.int32)
+    _dev(info, "info", torch.int32)
+    if w is not None:
+        _dev(w, "w", torch.float32)
+    ws, wsb = _workspace(lib.dr_greedy_workspace_size(n, P), s.device, workspace)
+    check("dr_select_greedy", lib.dr_select_greedy(_ptr(K), _ptr(s), n, P, k, _ptr(idx), _ptr(w), _ptr(info), _ptr(ws),
+                                                   wsb, _stream(stream)))
+
+
 def dr_combine_workspace_size(n, goff):
     return _lib.load().dr_combine_workspace_size(n, _goff_array(goff), len(goff) - 1)
 
@@ -324,3 +361,25 @@ def assemble_update(layers, w, n=None, lengths=None, group_of_layer=None, stream
     U = torch.empty(o, dtype=torch.float32, device=w.device)
     dr_assemble_update(layers, n, T, lengths, w, U, offs, group_of_layer=group_of_layer, stream=stream)
     return [U[a:a + sz].view(L["dy"].shape[2], L["x"].shape[2]) for a, sz, L in zip(offs, sizes, layers)]
+
+
+def select_threshold(s, tau=0.0, inclusive=True, stream=None):
+    """Kept indices [P, n] (ascending, then -1), counts [P], weights [P, n], info [P]."""
+    P, n = s.shape
+    dev = s.device
+    idx = torch.empty(P, n, dtype=torch.int32, device=dev)
+    count = torch.empty(P, dtype=torch.int32, device=dev)
+    w = torch.empty(P, n, dtype=torch.float32, device=dev)
+    info = torch.empty(P, dtype=torch.int32, device=dev)
+    dr_select_threshold(s, tau, inclusive, idx, count, w, info, stream=stream)
+    return idx, count, w, info
+
+
+def select_greedy(K, s, k, stream=None):
+    P, n = s.shape
+    dev = s.device
+    idx = torch.empty(P, k, dtype=torch.int32, device=dev)
+    w = torch.empty(P, n, dtype=torch.float32, device=dev)
+    info = torch.empty(P, dtype=torch.int32, device=dev)
+    dr_select_greedy(K, s, k, idx, w, info, stream=stream)
+    return idx, w, info

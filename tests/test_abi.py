@@ -179,3 +179,20 @@ def test_update_workspace_query(lib):
     assert update_call(lib, layers, n=64, T=512, ldw=64, dtype=_lib.DR_BF16, ws=FAKE, wsb=ws - 1) == \
         _lib.DR_ERR_WORKSPACE
     assert lib.dr_update_workspace_size(arr, 8, -1, 512, _lib.DR_BF16) == 0
+
+
+def test_threshold_and_greedy_argument_errors(lib):
+    E = _lib
+    cnt, info = FAKE, FAKE
+    assert lib.dr_select_threshold(FAKE, -1, 1, 0.0, 1, None, cnt, None, info, None) == E.DR_ERR_ARG
+    assert lib.dr_select_threshold(FAKE, 8, 1, float("nan"), 1, None, cnt, None, info, None) == E.DR_ERR_ARG
+    assert lib.dr_select_threshold(FAKE, 8, 1, 0.0, 1, None, None, None, info, None) == E.DR_ERR_ARG
+    assert lib.dr_select_threshold(None, 8, 1, 0.0, 1, None, cnt, None, info, None) == E.DR_ERR_ARG
+    assert lib.dr_select_threshold(FAKE, 8, 0, 0.0, 1, None, cnt, None, info, None) == E.DR_OK
+    ws = lib.dr_greedy_workspace_size(100, 2)
+    assert ws >= 2 * 100 * 4
+    assert lib.dr_select_greedy(FAKE, FAKE, 100, 2, 101, FAKE, None, info, FAKE, ws, None) == E.DR_ERR_ARG
+    assert lib.dr_select_greedy(FAKE, FAKE, 16385, 1, 5, FAKE, None, info, FAKE, 1 << 30, None) == \
+        E.DR_ERR_UNSUPPORTED
+    assert lib.dr_select_greedy(FAKE, FAKE, 100, 2, 5, FAKE, None, info, FAKE, ws - 1, None) == E.DR_ERR_WORKSPACE
+    assert lib.dr_select_greedy(FAKE, FAKE, 100, 2, 5, None, None, info, FAKE, ws, None) == E.DR_ERR_ARG
