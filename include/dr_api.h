@@ -65,6 +65,8 @@ typedef enum {
 
 typedef enum { DR_F32 = 0, DR_BF16 = 1 } dr_dtype;
 
+typedef enum { DR_SCORE_DIRECT = 0, DR_SCORE_GIP = 1, DR_SCORE_PIP = 2 } dr_score_method;
+
 typedef enum {
   DR_RIDGE_ABS = 0,       /* lam_eff = lambda */
   DR_RIDGE_REL_TRACE = 1  /* lam_eff = lambda * trace(K_p) / n */
@@ -304,6 +306,40 @@ dr_status dr_assemble_update(const dr_layer* layers, int num_layers, int64_t n, 
                              void* workspace, size_t ws_bytes, void* stream);
 size_t dr_update_workspace_size(const dr_layer* layers, int num_layers, int64_t n, int64_t T,
                                 dr_dtype dtype);
+
+/* ---------------------------------------------------------------------------
+ * dr_score_exact -- exact per-sample scores of every layer (Sec. 4.3),
+ *   s[l][i] = <gbar*_l, G_i^(l)>,   gbar*_l = (1/m) sum_j G*_j^(l),
+ * the alignment score of Sec. 3.3.2 restricted to one layer, without any
+ * sketch.  `method` picks the contraction order of Sec. 4.3:
+ *   DR_SCORE_DIRECT  form G_i (tile by tile, never stored) and take its
+ *                    inner product with gbar* ("Direct");
+ *   DR_SCORE_GIP     (1/m) sum_j <D_i D*_j^T, X_i X*_j^T>, two T x T token
+ *                    cross-correlations per pair ("Ghost Inner Product");
+ *   DR_SCORE_PIP     sum_t dy_{i,t}^T gbar* x_{i,t} ("Per-Token Inner
+ *                    Product").
+ * All three give the same scores up to rounding; their costs differ with T,
+ * m and the layer size (the crossover the section analyses).
+ * Arguments
+ *   layers   (host) num_layers descriptors (x, ldx, dy, lddy, d_in, d_out
+ *            used); rows 0..n-1 of x / dy are the general examples, rows
+ *            n..n+m-1 the targets.
+ *   n >= 0, m >= 1, T >= 0; len device int32 [n + m] or NULL (all T).
+ *   dtype    DR_BF16 (DR_F32: DR_ERR_UNSUPPORTED).
+ *   s        fp32 [num_layers][n] out (a group's score is the sum over its
+ *            layers).
+ *   workspace at least dr_score_workspace_size() bytes.
+ * Arithmetic: bf16 MFMA with fp32 accumulation, partial sums in fp64; PIP
+ * multiplies by gbar* as a bf16 hi + lo pair.  Layers are processed one at a
+ * time (the workspace holds one layer's gbar*).
+ * Requirements as for dr_assemble_update; one layer's gbar* rows and one
+ * example's rows must span less than 4 GiB (else DR_ERR_UNSUPPORTED).
+ * ------------------------------------------------------------------------- */
+dr_status dr_score_exact(const dr_layer* layers, int num_layers, int64_t n, int64_t m, int64_t T,
+                         const int32_t* len, dr_dtype dtype, dr_score_method method, float* s,
+                         void* workspace, size_t ws_bytes, void* stream);
+size_t dr_score_workspace_size(const dr_layer* layers, int num_layers, int64_t n, int64_t m, int64_t T,
+                               dr_dtype dtype, dr_score_method method);
 
 #ifdef __cplusplus
 }

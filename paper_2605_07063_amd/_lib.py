@@ -16,6 +16,7 @@ DR_ERR_NONFINITE, DR_ERR_WORKSPACE, DR_ERR_HIP, DR_ERR_UNSUPPORTED = 5, 6, 7, 8
 DR_INFO_NOT_CONVERGED, DR_INFO_NONFINITE = -2, -3
 DR_F32, DR_BF16 = 0, 1
 DR_RIDGE_ABS, DR_RIDGE_REL_TRACE = 0, 1
+DR_SCORE_DIRECT, DR_SCORE_GIP, DR_SCORE_PIP = 0, 1, 2
 
 c_i64, c_int, c_size, c_vp, c_float = ctypes.c_int64, ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_float
 
@@ -55,6 +56,9 @@ SIGNATURES = {
     "dr_greedy_workspace_size": (c_size, [c_i64, c_int]),
     "dr_assemble_update": (c_int, [ctypes.POINTER(DrLayer), c_int, c_i64, c_i64, c_vp, c_int, c_vp, c_int, c_i64,
                                    ctypes.POINTER(ctypes.c_int32), c_vp, ctypes.POINTER(c_i64), c_vp, c_size, c_vp]),
+    "dr_score_exact": (c_int, [ctypes.POINTER(DrLayer), c_int, c_i64, c_i64, c_i64, c_vp, c_int, c_int, c_vp, c_vp,
+                               c_size, c_vp]),
+    "dr_score_workspace_size": (c_size, [ctypes.POINTER(DrLayer), c_int, c_i64, c_i64, c_i64, c_int, c_int]),
     "dr_update_workspace_size": (c_size, [ctypes.POINTER(DrLayer), c_int, c_i64, c_i64, c_int]),
 }
 

@@ -285,6 +285,34 @@ def dr_assemble_update(layers, n, T, lengths, w, U, u_offset, group_of_layer=Non
     return U
 
 
+_SCORE_METHODS = {"direct": _lib.DR_SCORE_DIRECT, "gip": _lib.DR_SCORE_GIP, "pip": _lib.DR_SCORE_PIP}
+
+
+def dr_score_workspace_size(layers, n, m, T, method):
+    arr = make_update_layer_array(layers)
+    return _lib.load().dr_score_workspace_size(arr, len(layers), n, m, T, _lib.DR_BF16, _SCORE_METHODS[method])
+
+
+def dr_score_exact(layers, n, m, T, lengths, method, s, workspace=None, stream=None):
+    """s[l, i] = <gbar*_l, G_i^(l)> by the Direct, GIP or PIP contraction order."""
+    lib = _lib.load()
+    for L in layers:
+        for nm in ("x", "dy"):
+            _dev(L[nm], nm, torch.bfloat16)
+    _dev(s, "s", torch.float32)
+    _contig(s, "s")
+    if lengths is not None:
+        _dev(lengths, "lengths", torch.int32)
+        _contig(lengths, "lengths")
+    arr = make_update_layer_array(layers)
+    meth = _SCORE_METHODS[method]
+    nbytes = lib.dr_score_workspace_size(arr, len(layers), n, m, T, _lib.DR_BF16, meth)
+    ws, wsb = _workspace(nbytes, s.device, workspace)
+    check("dr_score_exact", lib.dr_score_exact(arr, len(layers), n, m, T, _ptr(lengths), _lib.DR_BF16, meth, _ptr(s),
+                                               _ptr(ws), wsb, _stream(stream)))
+    return s
+
+
 # ---------------------------------------------------------------------------
 # allocating conveniences (outputs created with torch on the inputs' device)
 # ---------------------------------------------------------------------------
@@ -383,3 +411,10 @@ def select_greedy(K, s, k, stream=None):
     info = torch.empty(P, dtype=torch.int32, device=dev)
     dr_select_greedy(K, s, k, idx, w, info, stream=stream)
     return idx, w, info
+
+
+def score_exact(layers, n, m, lengths=None, method="pip", stream=None):
+    """Per-layer exact scores [num_layers, n] of the first n rows against the mean of the next m."""
+    T = layers[0]["x"].shape[1]
+    s = torch.empty(len(layers), n, dtype=torch.float32, device=layers[0]["x"].device)
+    return dr_score_exact(layers, n, m, T, lengths, method, s, stream=stream)

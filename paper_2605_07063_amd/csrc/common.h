@@ -79,4 +79,10 @@ dr_status span_large(const float* K, const float* s, const float* t2, int64_t n,
                      float* w, float* lam_eff, float* resid2, int32_t* info, void* ws, size_t ws_bytes,
                      hipStream_t hs);
 
+// Direct scorer over the update-assembly kernel (update.hip): s[l][i] =
+// <gstar_l, G_i^(l)> for bf16 layers, gstar_l = gstar + g_off[l]
+size_t direct_workspace(const dr_layer* layers, int num_layers, int64_t n);
+dr_status direct_scores(const dr_layer* layers, int num_layers, int64_t n, int64_t T, const int32_t* len,
+                        const float* gstar, const int64_t* g_off, float* s, void* workspace, hipStream_t hs);
+
 }  // namespace dr

@@ -65,6 +65,8 @@ struct UpdLayerArg {
   int tile0;             // first tile of this layer within the launch
   int list;              // example list of this layer
   float* U;              // [d_out][d_in]
+  const float* gstar;    // score mode: the target-mean gradient [d_out][d_in]
+  double* part;          // score mode: partial scores [tiles of the layer][n]
 };
 
 struct UpdArgs {
@@ -200,6 +202,11 @@ __device__ __forceinline__ v4s lds_read_tr16(const unsigned char* p) {
 // read touches (q = r & 3 and bit 3 of r) land in distinct bank groups
 __device__ __forceinline__ int slot_xor(int r) { return (r & 3) | (((r >> 3) & 1) << 2); }
 
+// SCORE = false: the update.  SCORE = true (the Direct scorer of Sec. 4.3):
+// every example of the list gets weight 1; at the end of each example its
+// tile of G_i is dotted with the same tile of the target-mean gradient and
+// the accumulator cleared, so G_i is formed tile by tile and never stored.
+template <bool SCORE>
 __global__ __launch_bounds__(kBThreads) void update_bf16_kernel(UpdArgs a) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[kBStages * kBStage];
   int layer, to, ti, s, item;
@@ -314,27 +321,64 @@ __global__ __launch_bounds__(kBThreads) void update_bf16_kernel(UpdArgs a) {
         for (int j = 0; j < 4; ++j) acc[i][j] = mma_bf16(fa[i], fb[j], acc[i][j]);
       ct += kBK;
       if (ct >= clen) {
-        const float we = exw[ce];
-        ++ce;
-        ct = 0;
-        clen = ce < e_hi ? exlen[ce] : 0;
-        wlast = we;
-        if (ce < e_hi) {
-          const float wn = exw[ce];
-          if (wn != we) {
-            const float f = we / wn;   // |f| <= 1 in the sorted order
+        if constexpr (SCORE) {
+          __shared__ double red[kBThreads / 64];
+          const int lc = lane & 15;
+          float d = 0.f;
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
+          for (int i = 0; i < 8; ++i)
 #pragma unroll
-              for (int j = 0; j < 4; ++j)
+            for (int r = 0; r < 4; ++r) {
+              const int o = o0 + 128 * wr + 16 * i + 4 * g + r;
+              if (o >= d_out) continue;
+              const float* grow = Lr.gstar + (long long)o * d_in;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) acc[i][j][r] *= f;
+              for (int j = 0; j < 4; ++j) {
+                const int c = i0 + 64 * wc + 16 * j + lc;
+                if (c < d_in) d = fmaf(acc[i][j][r], grow[c], d);
+              }
+            }
+          double dd = (double)d;
+          for (int off = 32; off > 0; off >>= 1) dd += __shfl_xor(dd, off, 64);
+          if (lane == 0) red[w] = dd;
+          __syncthreads();
+          if (tid == 0) {
+            double t = 0.0;
+            for (int v = 0; v < kBThreads / 64; ++v) t += red[v];
+            Lr.part[(long long)(to * Lr.ti + ti) * a.nw + ex[ce]] = t;
+          }
+          __syncthreads();
+#pragma unroll
+          for (int i = 0; i < 8; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+          ++ce;
+          ct = 0;
+          clen = ce < e_hi ? exlen[ce] : 0;
+        } else {
+          const float we = exw[ce];
+          ++ce;
+          ct = 0;
+          clen = ce < e_hi ? exlen[ce] : 0;
+          wlast = we;
+          if (ce < e_hi) {
+            const float wn = exw[ce];
+            if (wn != we) {
+              const float f = we / wn;   // |f| <= 1 in the sorted order
+#pragma unroll
+              for (int i = 0; i < 8; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                  for (int r = 0; r < 4; ++r) acc[i][j][r] *= f;
+            }
           }
         }
       }
     }
     DR_WAIT_VM(0);
   }
+  if constexpr (SCORE) return;
 
   // C layout: register r of block (i, j) is row 4g + r, column lane % 16
   const int lc = lane & 15;
@@ -579,6 +623,116 @@ dr_status validate_update(const dr_layer* layers, int num_layers, int64_t n, int
   return DR_OK;
 }
 
+__global__ void fill_f32_kernel(float* p, long long n, float v) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// s[i] = sum over the layer's tiles of the partial scores (tile order), 0 for empty examples
+__global__ void direct_reduce_kernel(const double* part, int tiles, int n, const int* len, int T, float* s) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  int L = len ? len[i] : T;
+  L = L < 0 ? 0 : (L > T ? T : L);
+  double t = 0.0;
+  if (L > 0)
+    for (int q = 0; q < tiles; ++q) t += part[(long long)q * n + i];
+  s[i] = (float)t;
+}
+
+}  // namespace
+
+size_t direct_workspace(const dr_layer* layers, int num_layers, int64_t n) {
+  const UpdPlan pl = update_plan(layers, num_layers, n, DR_BF16);
+  size_t o = align_up(pl.bytes, 256);
+  o = align_up(o + (size_t)(n > 0 ? n : 1) * 4, 256);   // unit weights
+  for (int l = 0; l < num_layers; ++l) {
+    const int64_t tiles = ((layers[l].d_out + kBO - 1) / kBO) * ((layers[l].d_in + kBI - 1) / kBI);
+    o = align_up(o + (size_t)tiles * (size_t)(n > 0 ? n : 1) * 8, 256);
+  }
+  return o;
+}
+
+// Direct scores s[l][i] = <gstar_l, G_i^(l)> of the first n examples, for
+// bf16 layers whose target-mean gradients sit at gstar + g_off[l]
+dr_status direct_scores(const dr_layer* layers, int num_layers, int64_t n, int64_t T, const int32_t* len,
+                        const float* gstar, const int64_t* g_off, float* s, void* workspace, hipStream_t hs) {
+  const UpdPlan pl = update_plan(layers, num_layers, n, DR_BF16);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  size_t o = align_up(pl.bytes, 256);
+  float* ones = reinterpret_cast<float*>(ws + o);
+  o = align_up(o + (size_t)(n > 0 ? n : 1) * 4, 256);
+  double* part0 = reinterpret_cast<double*>(ws + o);
+  if (n == 0) return DR_OK;
+  hipLaunchKernelGGL(fill_f32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, hs, ones, (long long)n, 1.0f);
+  dr_status st = launch_status();
+  UpdArgs base = {};
+  base.split = pl.split;
+  base.n = (int)n;
+  base.nw = (int)n;
+  base.ex = reinterpret_cast<const int*>(ws + pl.off_ex);
+  base.exlen = reinterpret_cast<const int*>(ws + pl.off_len);
+  base.exw = reinterpret_cast<const float*>(ws + pl.off_w);
+  base.uex = reinterpret_cast<int*>(ws + pl.off_uex);
+  base.ulen = reinterpret_cast<int*>(ws + pl.off_ulen);
+  base.uw = reinterpret_cast<float*>(ws + pl.off_uw);
+  base.cnt = reinterpret_cast<const int*>(ws + pl.off_cnt);
+  base.partial = reinterpret_cast<float*>(ws + pl.off_partial);
+  RowSel rs = {};
+  if (st == DR_OK) {
+    hipLaunchKernelGGL(update_plan_kernel, dim3(1), dim3(1024), 0, hs, (const float*)ones, (long long)n, base, len,
+                       (int)T, 0, rs);
+    st = launch_status();
+  }
+  if (st == DR_OK) {
+    hipLaunchKernelGGL(update_sort_kernel, dim3((unsigned)((n + 255) / 256), 1), dim3(256), 0, hs, base);
+    st = launch_status();
+  }
+  double* part = part0;
+  for (int first = 0; first < num_layers && st == DR_OK; first += kMaxUpdLayers) {
+    const int count = num_layers - first < kMaxUpdLayers ? num_layers - first : kMaxUpdLayers;
+    UpdArgs a = base;
+    int tiles = 0;
+    double* parts[kMaxUpdLayers];
+    int ltiles[kMaxUpdLayers];
+    for (int j = 0; j < count; ++j) {
+      const dr_layer& L = layers[first + j];
+      UpdLayerArg& la = a.L[j];
+      la.x = static_cast<const unsigned char*>(L.x);
+      la.dy = static_cast<const unsigned char*>(L.dy);
+      la.ldx = L.ldx;
+      la.lddy = L.lddy;
+      la.exx = T * L.ldx * 2;
+      la.exdy = T * L.lddy * 2;
+      la.d_in = (int)L.d_in;
+      la.d_out = (int)L.d_out;
+      la.ti = (int)((L.d_in + kBI - 1) / kBI);
+      la.tile0 = tiles;
+      la.list = 0;
+      la.U = nullptr;
+      la.gstar = gstar + g_off[first + j];
+      la.part = part;
+      ltiles[j] = (int)(((L.d_out + kBO - 1) / kBO) * la.ti);
+      parts[j] = part;
+      part = reinterpret_cast<double*>(reinterpret_cast<unsigned char*>(part) +
+                                       align_up((size_t)ltiles[j] * (size_t)n * 8, 256));
+      tiles += ltiles[j];
+    }
+    a.num_layers = count;
+    a.ntiles = tiles;
+    const int items = tiles * pl.split;
+    hipLaunchKernelGGL(update_bf16_kernel<true>, dim3((items + 7) / 8 * 8), dim3(kBThreads), 0, hs, a);
+    if ((st = launch_status()) != DR_OK) break;
+    for (int j = 0; j < count && st == DR_OK; ++j) {
+      hipLaunchKernelGGL(direct_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, hs,
+                         (const double*)parts[j], ltiles[j], (int)n, len, (int)T, s + (long long)(first + j) * n);
+      st = launch_status();
+    }
+  }
+  return st;
+}
+
+namespace {
 }  // namespace
 }  // namespace dr
 
@@ -668,7 +822,7 @@ extern "C" dr_status dr_assemble_update(const dr_layer* layers, int num_layers, 
     const int items = tiles * pl.split;
     const int grid = (items + 7) / 8 * 8;
     if (dtype == DR_BF16)
-      hipLaunchKernelGGL(update_bf16_kernel, dim3(grid), dim3(kBThreads), 0, hs, a);
+      hipLaunchKernelGGL(update_bf16_kernel<false>, dim3(grid), dim3(kBThreads), 0, hs, a);
     else
       hipLaunchKernelGGL(update_f32_kernel, dim3(grid), dim3(kFThreads), 0, hs, a);
     if ((st = launch_status()) != DR_OK) break;

@@ -196,3 +196,21 @@ def test_threshold_and_greedy_argument_errors(lib):
         E.DR_ERR_UNSUPPORTED
     assert lib.dr_select_greedy(FAKE, FAKE, 100, 2, 5, FAKE, None, info, FAKE, ws - 1, None) == E.DR_ERR_WORKSPACE
     assert lib.dr_select_greedy(FAKE, FAKE, 100, 2, 5, None, None, info, FAKE, ws, None) == E.DR_ERR_ARG
+
+
+def test_score_argument_errors(lib):
+    E = _lib
+    arr = (_lib.DrLayer * 1)(layer(ldx=256, lddy=256))
+    call = lambda **kw: lib.dr_score_exact(arr, kw.get("nl", 1), kw.get("n", 4), kw.get("m", 2), kw.get("T", 8), None,
+                                           kw.get("dtype", E.DR_BF16), kw.get("method", E.DR_SCORE_PIP),
+                                           kw.get("s", FAKE), kw.get("ws", None), kw.get("wsb", 0), None)
+    assert call(m=0) == E.DR_ERR_ARG
+    assert call(method=7) == E.DR_ERR_ARG
+    assert call(dtype=E.DR_F32) == E.DR_ERR_UNSUPPORTED
+    assert call(dtype=9) == E.DR_ERR_DTYPE
+    assert call(s=None) == E.DR_ERR_ARG
+    assert call(nl=0) == E.DR_ERR_ARG
+    for meth in (E.DR_SCORE_DIRECT, E.DR_SCORE_GIP, E.DR_SCORE_PIP):
+        ws = lib.dr_score_workspace_size(arr, 1, 4, 2, 8, E.DR_BF16, meth)
+        assert ws > 0
+        assert call(method=meth, ws=FAKE, wsb=ws - 1) == E.DR_ERR_WORKSPACE
