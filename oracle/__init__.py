@@ -22,6 +22,8 @@ written for a reader who checks it against the paper by eye:
 * ``topk``    -- the top-k rule of Sec. 3.3.2 with lowest-index tie break.
 * ``select``  -- thresholding / negative filtering and greedy construction,
   the other subset rules of Sec. 3.3.2.
+* ``simplex`` -- soft weighting over the probability simplex (Sec. 6) and
+  the back-projection Pi^T of App. C.1.
 * ``update``  -- the weighted assembly of the update in parameter space
   (Sec. 4.2, post-hoc assembly from the retained pairs).
 * ``brute``   -- exhaustive enumeration for tiny inputs.
@@ -37,6 +39,7 @@ from .cone import nnls_active_set, cone_ref, cone_kkt_residual, cone_pg_replay
 from .topk import topk_ref
 from .update import update_ref
 from .select import threshold_ref, greedy_ref, subset_objective
+from .simplex import simplex_ref, simplex_residual, simplex_objective, backproject_ref
 from . import brute
 
 __all__ = [
@@ -45,5 +48,5 @@ __all__ = [
     "gram_ref",
     "ridge_lambda", "span_ref", "span_residual2", "combine_ref",
     "nnls_active_set", "cone_ref", "cone_kkt_residual", "cone_pg_replay",
-    "topk_ref", "update_ref", "threshold_ref", "greedy_ref", "subset_objective", "brute",
+    "topk_ref", "update_ref", "threshold_ref", "greedy_ref", "subset_objective", "simplex_ref", "simplex_residual", "simplex_objective", "backproject_ref", "brute",
 ]

@@ -561,3 +561,101 @@ def test_greedy_steps_are_best_single_additions_by_brute_force(seed):
     assert oracle.greedy_ref(K, s, 1)[0].tolist() == [int(np.argmin(np.diag(K) - 2 * s))]
     with pytest.raises(ValueError):
         oracle.greedy_ref(K, np.where(np.arange(n) == 2, np.nan, s), 2)
+
+
+# --------------------------------------------------------------------------
+# Simplex soft weighting and back-projection oracles
+# --------------------------------------------------------------------------
+
+def _simplex_by_enumeration(K, s):
+    """Best KKT point over every support (the QP restricted to a support is an
+    equality-constrained least-squares problem)."""
+    n = s.shape[0]
+    best, best_f = None, np.inf
+    for mask in range(1, 1 << n):
+        idx = [i for i in range(n) if mask >> i & 1]
+        k = len(idx)
+        A = np.zeros((k + 1, k + 1))
+        A[:k, :k] = 2 * K[np.ix_(idx, idx)]
+        A[:k, k] = 1
+        A[k, :k] = 1
+        try:
+            sol = np.linalg.solve(A, np.concatenate([2 * s[idx], [1.0]]))
+        except np.linalg.LinAlgError:
+            continue
+        if (sol[:k] < -1e-12).any():
+            continue
+        w = np.zeros(n)
+        w[idx] = np.maximum(sol[:k], 0)
+        w /= w.sum()
+        f = w @ K @ w - 2 * s @ w
+        if f < best_f - 1e-14:
+            best, best_f = w, f
+    return best
+
+
+def _sort_projection(v):
+    """Textbook Euclidean projection onto the simplex (sort, find the pivot)."""
+    u = np.sort(v)[::-1]
+    css = np.cumsum(u)
+    rho = max(j for j in range(len(v)) if u[j] - (css[j] - 1) / (j + 1) > 0)
+    theta = (css[rho] - 1) / (rho + 1)
+    return np.maximum(v - theta, 0)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 3])
+def test_simplex_matches_support_enumeration(seed):
+    rng = np.random.default_rng(seed)
+    n = 7
+    Gm = rng.standard_normal((n, 5 + seed))            # rank-deficient for seeds 0, 1
+    gs = rng.standard_normal(5 + seed) * (0.3 + seed)
+    K, s = Gm @ Gm.T + 1e-3 * np.eye(n), Gm @ gs
+    w = oracle.simplex_ref(K, s)
+    we = _simplex_by_enumeration(K, s)
+    assert w.min() >= 0 and w.sum() == pytest.approx(1.0, abs=1e-12)
+    assert oracle.simplex_objective(K, s, w) == pytest.approx(oracle.simplex_objective(K, s, we), abs=1e-10)
+    np.testing.assert_allclose(w, we, atol=1e-7)
+    assert oracle.simplex_residual(K, s, w) < 1e-10
+
+
+@pytest.mark.parametrize("seed", [4, 5])
+def test_simplex_scaled_identity_is_the_projection_of_the_scores(seed):
+    """K = cI: f = c||w||^2 - 2 s^T w = c ||w - s/c||^2 + const, so the
+    optimum is the Euclidean projection of s / c onto the simplex."""
+    rng = np.random.default_rng(seed)
+    s = rng.standard_normal(30)
+    w = oracle.simplex_ref(3.0 * np.eye(30), s)
+    np.testing.assert_allclose(w, _sort_projection(s / 3.0), atol=1e-12)
+
+
+def test_simplex_special_cases():
+    # one example: the only point of the simplex
+    np.testing.assert_allclose(oracle.simplex_ref(np.array([[2.0]]), np.array([-5.0])), [1.0], atol=1e-14)
+    # target inside the convex hull: zero residual distance
+    Gm = np.array([[1.0, 0.0], [0.0, 1.0], [-1.0, -1.0]])
+    gstar = np.array([0.2, 0.3])                        # = 0.5 g0 + 0.6 g1 ... inside the hull
+    K, s = Gm @ Gm.T, Gm @ gstar
+    w = oracle.simplex_ref(K, s)
+    assert np.sum((Gm.T @ w - gstar) ** 2) == pytest.approx(0.0, abs=1e-12)
+    # a dominant example: the vertex
+    s2 = np.array([10.0, 0.0, 0.0])
+    w2 = oracle.simplex_ref(np.eye(3), s2)
+    np.testing.assert_allclose(w2, [1.0, 0.0, 0.0], atol=1e-14)
+
+
+def test_backprojection_is_the_adjoint_of_the_factorised_sketch():
+    rng = np.random.default_rng(6)
+    layers = []
+    off = 0
+    for d_in, d_out, k_in, k_out in [(7, 5, 3, 2), (4, 6, 2, 3)]:
+        layers.append(dict(p_in=rng.standard_normal((k_in, d_in)), p_out=rng.standard_normal((k_out, d_out)),
+                           col_offset=off, d_in=d_in, d_out=d_out))
+        off += k_in * k_out
+    u = rng.standard_normal(off)
+    Us = oracle.backproject_ref(u, layers)
+    for L, U in zip(layers, Us):
+        G = rng.standard_normal((L["d_out"], L["d_in"]))
+        Pi = np.kron(L["p_out"], L["p_in"])            # row-major vec, sketch layout [k_out][k_in]
+        x = u[L["col_offset"]:L["col_offset"] + Pi.shape[0]]
+        assert np.sum(G * U) == pytest.approx((Pi @ G.reshape(-1)) @ x, rel=1e-12)
+        np.testing.assert_allclose(U.reshape(-1), Pi.T @ x, rtol=1e-12, atol=1e-12)
