@@ -65,17 +65,23 @@ def simplex_residual(K, s, w):
 
 
 def _solve_on_support(K, s, P):
+    """KKT system of the equality-constrained problem on the support P.  The
+    constraint row and column are scaled by c = max |2 K_PP| (the system
+    [2K_PP c1; c1^T 0][w; mu/c] = [2 s_P; c] has the same solution), so that
+    the least-squares solve treats both blocks on the same scale."""
     idx = np.flatnonzero(P)
     k = idx.size
+    KP = 2.0 * K[np.ix_(idx, idx)]
+    c = max(np.abs(KP).max(), 1e-300)
     A = np.zeros((k + 1, k + 1))
-    A[:k, :k] = 2.0 * K[np.ix_(idx, idx)]
-    A[:k, k] = 1.0
-    A[k, :k] = 1.0
-    b = np.concatenate([2.0 * s[idx], [1.0]])
+    A[:k, :k] = KP
+    A[:k, k] = c
+    A[k, :k] = c
+    b = np.concatenate([2.0 * s[idx], [c]])
     sol = np.linalg.lstsq(A, b, rcond=None)[0]
     z = np.zeros(K.shape[0])
     z[idx] = sol[:k]
-    return z, sol[k]
+    return z, sol[k] * c
 
 
 def simplex_ref(K, s, max_outer=None):

@@ -628,6 +628,20 @@ def test_simplex_scaled_identity_is_the_projection_of_the_scores(seed):
     np.testing.assert_allclose(w, _sort_projection(s / 3.0), atol=1e-12)
 
 
+@pytest.mark.parametrize("c", [1e-6, 1e4, 1e8, 1e12])
+def test_simplex_is_invariant_to_scaling_the_objective(c):
+    """argmin of c (w^T K w - 2 s^T w) over the simplex does not depend on c > 0
+    (sketch Gram matrices have entries of order 1e6 and more)."""
+    rng = np.random.default_rng(12)
+    Gm = rng.standard_normal((40, 300))
+    K, s = Gm @ Gm.T, Gm @ (0.05 * rng.standard_normal(300))
+    w1 = oracle.simplex_ref(K, s)
+    wc = oracle.simplex_ref(c * K, c * s)
+    assert wc.sum() == pytest.approx(1.0, abs=1e-12) and wc.min() >= 0
+    np.testing.assert_allclose(wc, w1, atol=1e-9)
+    assert oracle.simplex_residual(c * K, c * s, wc) < 1e-10
+
+
 def test_simplex_special_cases():
     # one example: the only point of the simplex
     np.testing.assert_allclose(oracle.simplex_ref(np.array([[2.0]]), np.array([-5.0])), [1.0], atol=1e-14)
