@@ -202,6 +202,40 @@ dr_status dr_project_cone(const float* K, const float* s, const float* t2, int64
 size_t dr_cone_workspace_size(int64_t n, int P);
 
 /* ---------------------------------------------------------------------------
+ * dr_project_simplex -- soft weighting (Sec. 6, "Designing New Feasible
+ * Sets"): Eq. (proj) onto U_soft = { G^T w : w in the probability simplex },
+ * i.e. w_p = argmin { w^T K_p w - 2 s_p^T w : w >= 0, sum_i w_i = 1 }.
+ * Accelerated projected gradient (FISTA, step 1/L with L = 2 max_i
+ * sum_j |K_ij|) from the best single vertex, each step projected exactly onto
+ * the simplex; fp64 iterates on the fp32 K.  Stops after max_iter steps or
+ * when the step residual max_i |w_i - y_i| (projected point minus the point
+ * the gradient was taken at) is <= tol (tol <= 0: exactly max_iter steps).
+ *   w [P][n] out (on the simplex); resid2 [P] out = t2 + w.K.w - 2 s.w;
+ *   iters [P] out; res [P] out (the last step residual); info [P] out
+ *   (DR_INFO_NOT_CONVERGED if tol > 0 was not reached, DR_INFO_NONFINITE on
+ *   NaN / inf input).  n = 0: nothing to project onto (resid2 = t2).
+ *   Supports n <= 256.
+ * ------------------------------------------------------------------------- */
+dr_status dr_project_simplex(const float* K, const float* s, const float* t2, int64_t n, int P, int max_iter,
+                             float tol, float* w, float* resid2, int32_t* iters, float* res, int32_t* info,
+                             void* stream);
+
+/* ---------------------------------------------------------------------------
+ * dr_back_project -- the transpose of the factorised compressor (App. C.1,
+ * "Backward projection"), layer by layer: U + u_offset[l] (row-major
+ * [d_out][d_in], fp32) = P_out^T X' P_in with X' the layer's block of the
+ * sketch-space vector u (columns col_offset .. + k_out*k_in, read as
+ * [k_out][k_in], the layout of dr_sketch_grads).  With u = dr_combine's
+ * sketch-space update this is the parameter-space update of the MeSO
+ * variant.  p_in / p_out have dtype `dtype`; x, dy are not used.
+ * Requirements: 1 <= k_in, k_out <= 64; workspace of at least
+ * dr_backproject_workspace_size() bytes (one layer's P_in product).
+ * ------------------------------------------------------------------------- */
+dr_status dr_back_project(const dr_layer* layers, int num_layers, dr_dtype dtype, const float* u, float* U,
+                          const int64_t* u_offset, void* workspace, size_t ws_bytes, void* stream);
+size_t dr_backproject_workspace_size(const dr_layer* layers, int num_layers);
+
+/* ---------------------------------------------------------------------------
  * dr_select_topk -- the top-k rule of Sec. 3.3.2 (Select-S in the one-pass
  * algorithms of Sec. 4.2), per group.
  *

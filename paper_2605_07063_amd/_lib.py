@@ -51,6 +51,11 @@ SIGNATURES = {
     "dr_combine": (c_int, [c_vp, c_i64, c_i64, c_int, ctypes.POINTER(c_i64), c_int, c_vp, c_vp, c_vp, c_size,
                            c_vp]),
     "dr_combine_workspace_size": (c_size, [c_i64, ctypes.POINTER(c_i64), c_int]),
+    "dr_project_simplex": (c_int, [c_vp, c_vp, c_vp, c_i64, c_int, c_int, c_float, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                   c_vp]),
+    "dr_back_project": (c_int, [ctypes.POINTER(DrLayer), c_int, c_int, c_vp, c_vp, ctypes.POINTER(c_i64), c_vp, c_size,
+                                c_vp]),
+    "dr_backproject_workspace_size": (c_size, [ctypes.POINTER(DrLayer), c_int]),
     "dr_select_threshold": (c_int, [c_vp, c_i64, c_int, c_float, c_int, c_vp, c_vp, c_vp, c_vp, c_vp]),
     "dr_select_greedy": (c_int, [c_vp, c_vp, c_i64, c_int, c_i64, c_vp, c_vp, c_vp, c_vp, c_size, c_vp]),
     "dr_greedy_workspace_size": (c_size, [c_i64, c_int]),

@@ -162,6 +162,42 @@ def dr_project_cone(K, s, t2, max_iter, kkt_tol, w, resid2, iters, kkt, info, st
                                                  0, _stream(stream)))
 
 
+def dr_project_simplex(K, s, t2, max_iter, tol, w, resid2, iters, res, info, stream=None):
+    """Soft weighting: w = argmin over the simplex of w^T K w - 2 s^T w, per group."""
+    lib = _lib.load()
+    P, n = s.shape
+    for t, nm in ((K, "K"), (s, "s"), (t2, "t2"), (w, "w"), (resid2, "resid2"), (res, "res")):
+        _dev(t, nm, torch.float32)
+        _contig(t, nm)
+    _dev(iters, "iters", torch.int32)
+    _dev(info, "info", torch.int32)
+    check("dr_project_simplex", lib.dr_project_simplex(_ptr(K), _ptr(s), _ptr(t2), n, P, int(max_iter), float(tol),
+                                                       _ptr(w), _ptr(resid2), _ptr(iters), _ptr(res), _ptr(info),
+                                                       _stream(stream)))
+
+
+def dr_back_project(layers, u, U, u_offset, workspace=None, stream=None):
+    """U[u_offset[l]:] (as [d_out][d_in]) = P_out^T X'_l P_in for every layer."""
+    lib = _lib.load()
+    dtype = layers[0]["p_in"].dtype
+    if dtype not in _DTYPES:
+        raise ValueError("p_in must be float32 or bfloat16")
+    for L in layers:
+        for nm in ("p_in", "p_out"):
+            _dev(L[nm], nm, dtype)
+            _contig(L[nm], nm)
+    _dev(u, "u", torch.float32)
+    _dev(U, "U", torch.float32)
+    arr = (DrLayer * len(layers))()
+    for i, L in enumerate(layers):
+        arr[i] = DrLayer(None, 0, None, 0, L["p_in"].data_ptr(), L["p_out"].data_ptr(), L["p_in"].shape[1],
+                         L["p_out"].shape[1], L["p_in"].shape[0], L["p_out"].shape[0], int(L["col_offset"]))
+    ws, wsb = _workspace(lib.dr_backproject_workspace_size(arr, len(layers)), U.device, workspace)
+    check("dr_back_project", lib.dr_back_project(arr, len(layers), _DTYPES[dtype], _ptr(u), _ptr(U),
+                                                 _goff_array(u_offset), _ptr(ws), wsb, _stream(stream)))
+    return U
+
+
 def dr_select_topk(s, k, idx, w, info, stream=None):
     """idx_p = the k largest s_p (ties -> lowest index), ascending; w_p = 1/k on idx_p."""
     lib = _lib.load()
@@ -418,3 +454,27 @@ def score_exact(layers, n, m, lengths=None, method="pip", stream=None):
     T = layers[0]["x"].shape[1]
     s = torch.empty(len(layers), n, dtype=torch.float32, device=layers[0]["x"].device)
     return dr_score_exact(layers, n, m, T, lengths, method, s, stream=stream)
+
+
+def project_simplex(K, s, t2, max_iter=2000, tol=1e-7, stream=None):
+    P, n = s.shape
+    dev = t2.device
+    w = torch.empty(P, n, dtype=torch.float32, device=dev)
+    resid2 = torch.empty(P, dtype=torch.float32, device=dev)
+    iters = torch.empty(P, dtype=torch.int32, device=dev)
+    res = torch.empty(P, dtype=torch.float32, device=dev)
+    info = torch.empty(P, dtype=torch.int32, device=dev)
+    dr_project_simplex(K, s, t2, max_iter, tol, w, resid2, iters, res, info, stream=stream)
+    return w, resid2, iters, res, info
+
+
+def back_project(layers, u, stream=None):
+    """Per-layer parameter-space blocks [d_out, d_in] of a sketch-space vector."""
+    sizes = [L["p_out"].shape[1] * L["p_in"].shape[1] for L in layers]
+    offs, o = [], 0
+    for sz in sizes:
+        offs.append(o)
+        o += sz
+    U = torch.empty(o, dtype=torch.float32, device=u.device)
+    dr_back_project(layers, u, U, offs, stream=stream)
+    return [U[a:a + sz].view(L["p_out"].shape[1], L["p_in"].shape[1]) for a, sz, L in zip(offs, sizes, layers)]

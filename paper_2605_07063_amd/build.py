@@ -17,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdr.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["api.cpp", "sketch.hip", "gram.hip", "solve.hip", "chol.hip", "select.hip", "combine.hip", "update.hip", "score.hip"]
+SOURCES = ["api.cpp", "sketch.hip", "gram.hip", "solve.hip", "chol.hip", "select.hip", "combine.hip", "update.hip", "score.hip", "backproj.hip"]
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

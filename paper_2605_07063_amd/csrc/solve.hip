@@ -27,6 +27,13 @@
 // which is exactly w~ <- max(0, w~ - (K~ w~ - s~)/Lhat) for w~ = w / r.
 // K stays in registers as the exact fp32 input (rows split over a
 // power-of-two group of lanes within one wave); w and all sums are fp64.
+//
+// simplex_pg_kernel (n <= 256, dr_project_simplex): soft weighting over the
+// probability simplex, min_{w in simplex} w^T K w - 2 s^T w, by accelerated
+// projected gradient (FISTA) with step 1/L, L = 2 max_i sum_j |K_ij|, and
+// the exact Euclidean projection onto the simplex (Michelot's iteration:
+// theta = (sum_{v_i > theta} v_i - 1) / #{v_i > theta} until the set stops
+// shrinking, a handful of block reductions).  Same K layout as the cone.
 
 #include "common.h"
 
@@ -864,6 +871,218 @@ __global__ __launch_bounds__(NM * 4) void span_cols_kernel(const float* K, const
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// Soft weighting over the simplex.
+
+template <int MAXC>
+__global__ __launch_bounds__(kConeThreads) void simplex_pg_kernel(const float* K, const float* s, const float* t2, int n,
+                                                                  int max_iter, float tol, float* w, float* resid2,
+                                                                  int* iters, float* res_out, int* info) {
+  __shared__ double ybuf[kConeMaxN];       // the point the gradient is taken at
+  __shared__ double wprev[kConeMaxN];
+  __shared__ double vbuf[kConeMaxN];       // y - grad / L, projected next
+  __shared__ double scratch[kConeThreads / 64 + 1];
+  __shared__ double red_d[kConeThreads / 64];
+  __shared__ int red_i[kConeThreads / 64];
+  __shared__ int flag;
+  const int p = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float* Kp = K + (long long)p * n * n;
+  const float* sp = s + (long long)p * n;
+  int npad = 1;
+  while (npad < n) npad <<= 1;
+  int tpr = kConeThreads / npad;
+  if (tpr > 64) tpr = 64;
+  const int row = tid / tpr, part = tid % tpr;
+  const bool has_row = row < n;
+
+  if (tid == 0) flag = 0;
+  __syncthreads();
+  int bad = 0;
+  for (int e = tid; e < n * n; e += kConeThreads)
+    if (!isfinite(Kp[e])) bad = 1;
+  for (int i = tid; i < n; i += kConeThreads)
+    if (!isfinite(sp[i])) bad = 1;
+  if (bad) flag = 1;
+  __syncthreads();
+  if (flag) {
+    for (int i = tid; i < n; i += kConeThreads) w[(long long)p * n + i] = 0.f;
+    if (tid == 0) {
+      resid2[p] = t2[p];
+      iters[p] = 0;
+      res_out[p] = 0.f;
+      info[p] = DR_INFO_NONFINITE;
+    }
+    return;
+  }
+
+  // block-wide (sum, count) of v_i over v_i > theta: one Michelot pass
+  auto pass = [&](double theta, double& sum, int& cnt) {
+    double ls = 0.0;
+    int lc = 0;
+    for (int i = tid; i < n; i += kConeThreads)
+      if (vbuf[i] > theta) {
+        ls += vbuf[i];
+        ++lc;
+      }
+    for (int off = 32; off > 0; off >>= 1) {
+      ls += __shfl_xor(ls, off, 64);
+      lc += __shfl_xor(lc, off, 64);
+    }
+    if (lane == 0) {
+      red_d[wave] = ls;
+      red_i[wave] = lc;
+    }
+    __syncthreads();
+    sum = 0.0;
+    cnt = 0;
+    for (int q = 0; q < kConeThreads / 64; ++q) {
+      sum += red_d[q];
+      cnt += red_i[q];
+    }
+    __syncthreads();
+  };
+
+  constexpr int KREG = MAXC > 0 ? MAXC : 1;
+  float kr[KREG];
+  double lrow = 0.0;
+  if constexpr (MAXC > 0) {
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+      const int j = part + c * tpr;
+      kr[c] = (has_row && j < n) ? Kp[(long long)row * n + j] : 0.f;
+      lrow += fabs((double)kr[c]);
+    }
+  } else {
+    kr[0] = 0.f;
+    if (has_row)
+      for (int j = part; j < n; j += tpr) lrow += fabs((double)Kp[(long long)row * n + j]);
+  }
+  for (int off = tpr / 2; off > 0; off >>= 1) lrow += __shfl_xor(lrow, off, 64);
+  double lmax = has_row ? lrow : 0.0;
+  for (int off = 32; off > 0; off >>= 1) lmax = fmax(lmax, __shfl_xor(lmax, off, 64));
+  if (lane == 0) scratch[wave] = lmax;
+  // start: the best single vertex, argmin_i K_ii - 2 s_i (lowest index on ties)
+  double fbest = 0.0;
+  int ibest = -1;
+  for (int i = tid; i < n; i += kConeThreads) {
+    const double f = (double)Kp[(long long)i * n + i] - 2.0 * (double)sp[i];
+    if (ibest < 0 || f < fbest) {
+      fbest = f;
+      ibest = i;
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    const double fo = __shfl_xor(fbest, off, 64);
+    const int io = __shfl_xor(ibest, off, 64);
+    if (io >= 0 && (ibest < 0 || fo < fbest || (fo == fbest && io < ibest))) {
+      fbest = fo;
+      ibest = io;
+    }
+  }
+  if (lane == 0) {
+    red_d[wave] = fbest;
+    red_i[wave] = ibest;
+  }
+  __syncthreads();
+  double L = 0.0;
+  for (int q = 0; q < kConeThreads / 64; ++q) L = fmax(L, scratch[q]);
+  L *= 2.0;
+  int i0 = -1;
+  double f0 = 0.0;
+  for (int q = 0; q < kConeThreads / 64; ++q) {
+    const int io = red_i[q];
+    if (io >= 0 && (i0 < 0 || red_d[q] < f0 || (red_d[q] == f0 && io < i0))) {
+      f0 = red_d[q];
+      i0 = io;
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < n; i += kConeThreads) {
+    ybuf[i] = i == i0 ? 1.0 : 0.0;
+    wprev[i] = ybuf[i];
+  }
+  __syncthreads();
+  const double si = has_row ? (double)sp[row] : 0.0;
+
+  int it = 0;
+  double res = 0.0, tk = 1.0;
+  while (L > 0.0 && it < max_iter) {
+    // v = y - 2 (K y - s) / L
+    double acc = 0.0;
+    if constexpr (MAXC > 0) {
+#pragma unroll
+      for (int c = 0; c < MAXC; ++c) {
+        const int j = part + c * tpr;
+        if (j < n) acc += (double)kr[c] * ybuf[j];
+      }
+    } else {
+      if (has_row)
+        for (int j = part; j < n; j += tpr) acc += (double)Kp[(long long)row * n + j] * ybuf[j];
+    }
+    for (int off = tpr / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    if (has_row && part == 0) vbuf[row] = ybuf[row] - 2.0 * (acc - si) / L;
+    __syncthreads();
+    // theta with sum_i max(v_i - theta, 0) = 1
+    double sum;
+    int cnt, prev = n + 1;
+    double theta = -1.0e308;
+    while (true) {
+      pass(theta, sum, cnt);
+      if (cnt == prev || cnt == 0) break;
+      prev = cnt;
+      theta = (sum - 1.0) / (double)cnt;
+    }
+    // w = max(v - theta, 0); residual = max |w - y|; momentum step
+    const double tn = 0.5 * (1.0 + sqrt(1.0 + 4.0 * tk * tk));
+    const double beta = (tk - 1.0) / tn;
+    double r = 0.0;
+    for (int i = tid; i < n; i += kConeThreads) {
+      const double wi = fmax(vbuf[i] - theta, 0.0);
+      r = fmax(r, fabs(wi - ybuf[i]));
+      const double yn = wi + beta * (wi - wprev[i]);
+      wprev[i] = wi;
+      ybuf[i] = yn;
+    }
+    for (int off = 32; off > 0; off >>= 1) r = fmax(r, __shfl_xor(r, off, 64));
+    if (lane == 0) scratch[wave] = r;
+    __syncthreads();
+    res = 0.0;
+    for (int q = 0; q < kConeThreads / 64; ++q) res = fmax(res, scratch[q]);
+    __syncthreads();
+    tk = tn;
+    ++it;
+    if (tol > 0.f && res <= (double)tol) break;
+  }
+
+  // w = the last projected point; resid2 = t2 + w.K.w - 2 s.w
+  double acc = 0.0;
+  if constexpr (MAXC > 0) {
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+      const int j = part + c * tpr;
+      if (j < n) acc += (double)kr[c] * wprev[j];
+    }
+  } else {
+    if (has_row)
+      for (int j = part; j < n; j += tpr) acc += (double)Kp[(long long)row * n + j] * wprev[j];
+  }
+  for (int off = tpr / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+  double contrib = 0.0;
+  if (has_row && part == 0) {
+    const double wi = wprev[row];
+    contrib = wi * acc - 2.0 * si * wi;
+    w[(long long)p * n + row] = (float)wi;
+  }
+  const double q = block_sum<kConeThreads>(contrib, scratch);
+  if (tid == 0) {
+    resid2[p] = (float)((double)t2[p] + q);
+    iters[p] = it;
+    res_out[p] = (float)res;
+    info[p] = (tol > 0.f && res > (double)tol) ? DR_INFO_NOT_CONVERGED : 0;
+  }
+}
+
 __global__ void empty_group_kernel(const float* t2, int P, float* lam_eff, float* resid2, int32_t* iters, float* kkt,
                                    int32_t* info) {
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
@@ -967,5 +1186,37 @@ extern "C" dr_status dr_project_cone(const float* K, const float* s, const float
   else
     hipLaunchKernelGGL(cone_pg_kernel<0>, dim3(P), dim3(kConeThreads), 0, hs, K, s, t2, (int)n, max_iter, kkt_tol, w,
                        resid2, iters, kkt, info);
+  return launch_status();
+}
+
+extern "C" dr_status dr_project_simplex(const float* K, const float* s, const float* t2, int64_t n, int P, int max_iter,
+                                        float tol, float* w, float* resid2, int32_t* iters, float* res, int32_t* info,
+                                        void* stream) {
+  using namespace dr;
+  if (n < 0 || P < 0 || max_iter < 0 || !(tol == tol)) return DR_ERR_ARG;
+  if (P == 0) return DR_OK;
+  if (!t2 || !resid2 || !iters || !res || !info) return DR_ERR_ARG;
+  if (n > 0 && (!K || !s || !w)) return DR_ERR_ARG;
+  if (n > kConeMaxN) return DR_ERR_UNSUPPORTED;
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  if (n == 0) {   // the simplex of zero examples is empty: nothing to project onto
+    hipLaunchKernelGGL(empty_group_kernel, dim3((P + 255) / 256), dim3(256), 0, hs, t2, P, (float*)nullptr, resid2,
+                       iters, res, info);
+    return launch_status();
+  }
+  int npad = 1;
+  while (npad < n) npad <<= 1;
+  int tpr = kConeThreads / npad;
+  if (tpr > 64) tpr = 64;
+  const int cols = (npad + tpr - 1) / tpr;
+  if (cols <= 4)
+    hipLaunchKernelGGL(simplex_pg_kernel<4>, dim3(P), dim3(kConeThreads), 0, hs, K, s, t2, (int)n, max_iter, tol, w,
+                       resid2, iters, res, info);
+  else if (cols <= 16)
+    hipLaunchKernelGGL(simplex_pg_kernel<16>, dim3(P), dim3(kConeThreads), 0, hs, K, s, t2, (int)n, max_iter, tol, w,
+                       resid2, iters, res, info);
+  else
+    hipLaunchKernelGGL(simplex_pg_kernel<0>, dim3(P), dim3(kConeThreads), 0, hs, K, s, t2, (int)n, max_iter, tol, w,
+                       resid2, iters, res, info);
   return launch_status();
 }

@@ -214,3 +214,26 @@ def test_score_argument_errors(lib):
         ws = lib.dr_score_workspace_size(arr, 1, 4, 2, 8, E.DR_BF16, meth)
         assert ws > 0
         assert call(method=meth, ws=FAKE, wsb=ws - 1) == E.DR_ERR_WORKSPACE
+
+
+def test_simplex_and_backprojection_argument_errors(lib):
+    E = _lib
+    args = lambda **kw: (kw.get("K", FAKE), FAKE, FAKE, kw.get("n", 8), kw.get("P", 1), kw.get("it", 10),
+                         kw.get("tol", 0.0), FAKE, FAKE, FAKE, kw.get("res", FAKE), FAKE, None)
+    assert lib.dr_project_simplex(*args(n=-1)) == E.DR_ERR_ARG
+    assert lib.dr_project_simplex(*args(it=-1)) == E.DR_ERR_ARG
+    assert lib.dr_project_simplex(*args(tol=float("nan"))) == E.DR_ERR_ARG
+    assert lib.dr_project_simplex(*args(res=None)) == E.DR_ERR_ARG
+    assert lib.dr_project_simplex(*args(K=None)) == E.DR_ERR_ARG
+    assert lib.dr_project_simplex(*args(n=257)) == E.DR_ERR_UNSUPPORTED
+    assert lib.dr_project_simplex(*args(P=0)) == E.DR_OK
+    L = [layer(k_in=16, k_out=16)]
+    arr = (_lib.DrLayer * 1)(*L)
+    offs = (ctypes.c_int64 * 1)(0)
+    ws = lib.dr_backproject_workspace_size(arr, 1)
+    assert ws >= 16 * 256 * 4
+    assert lib.dr_back_project(arr, 1, 9, FAKE, FAKE, offs, FAKE, ws, None) == E.DR_ERR_DTYPE
+    assert lib.dr_back_project(arr, 1, E.DR_F32, None, FAKE, offs, FAKE, ws, None) == E.DR_ERR_ARG
+    assert lib.dr_back_project(arr, 1, E.DR_F32, FAKE, FAKE, offs, FAKE, ws - 1, None) == E.DR_ERR_WORKSPACE
+    big = (_lib.DrLayer * 1)(layer(k_in=128))
+    assert lib.dr_back_project(big, 1, E.DR_F32, FAKE, FAKE, offs, FAKE, 1 << 30, None) == E.DR_ERR_ARG
