@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--groups", choices=["global", "layer"], default="global",
                     help="one group over all sketch columns (default), or one group per layer (P = 8)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle's sketch sample")
+    ap.add_argument("--no-next-rows", action="store_true",
+                    help="skip the separately timed widening rows (update, scorers, selection rules, simplex, "
+                         "back-projection)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run three 1 GiB device-to-device copies first (known bytes, to scale HBM counters)")
     ap.add_argument("--summarize-profiles", nargs=3, metavar=("KT_DIR", "FETCH_DIR", "WRITE_DIR"),
@@ -214,7 +217,8 @@ def main():
         },
     }
 
-    out["next_rows"] = time_next_rows(api, layers, lens, n, T, wt, wc, goff, dev, K=K, s=s)
+    if not args.no_next_rows:
+        out["next_rows"] = time_next_rows(api, layers, lens, n, T, wt, wc, goff, dev, K=K, s=s)
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layers, lens, S, K, s, t2, n, m, k_top, lam, cfg, args.cpu_seconds, goff)
@@ -222,10 +226,14 @@ def main():
 
 
 def _event_ms(fn, reps):
+    """GPU milliseconds per call of fn: a spin kernel keeps the stream busy
+    while the host enqueues every call, so the two events bracket the calls'
+    GPU execution and not the host's launch rate."""
     import torch
     fn()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(100_000_000)
     e0.record()
     for _ in range(reps):
         fn()
@@ -277,6 +285,48 @@ def time_next_rows(api, layers, lens, n, T, wt, wc, goff, dev, K=None, s=None, r
         gidx = torch.empty(P, kk, dtype=torch.int32, device=dev)
         gws = torch.empty(max(1, api.dr_greedy_workspace_size(nn, P)), dtype=torch.uint8, device=dev)
         res["select_greedy_ms"] = _event_ms(lambda: api.dr_select_greedy(K, s, kk, gidx, wq, info, workspace=gws), reps)
+    # exact per-layer scores of the 64 general rows against the 8 targets, by
+    # the three contraction orders; algorithmic flops: the leading terms
+    # (2 tokens d_in d_out for Direct / PIP, 4 sum_i sum_j len_i len_j (d_in
+    # + d_out) / 2 for GIP's two cross-correlations)
+    m = lens.shape[0] - n
+    la = lens.cpu().numpy().astype(np.int64)
+    sc = torch.empty(len(layers), n, device=dev)
+    lead = {"direct": 0.0, "pip": 0.0, "gip": 0.0}
+    for L in layers:
+        di, do = L["x"].shape[2], L["dy"].shape[2]
+        lead["direct"] += 2.0 * float(la.sum()) * di * do
+        lead["pip"] += 2.0 * float(la.sum()) * di * do
+        lead["gip"] += 2.0 * float(la[:n].sum()) * float(la[n:].sum()) * (di + do)
+    scores = {}
+    for meth in ("direct", "gip", "pip"):
+        sws = torch.empty(max(1, api.dr_score_workspace_size(ul, n, m, T, meth)), dtype=torch.uint8, device=dev)
+        ms = _event_ms(lambda: api.dr_score_exact(ul, n, m, T, lens, meth, sc, workspace=sws), max(3, reps // 4))
+        scores[meth] = {"ms": ms, "algorithmic_tflops": lead[meth] / (ms * 1e-3) / 1e12}
+    res["score_exact"] = scores
+    if K is not None:
+        # soft weighting over the simplex on the step's K, s (to a step residual of 1e-7)
+        P, nn = s.shape
+        t2 = torch.zeros(P, device=dev)
+        wsx = torch.empty(P, nn, device=dev)
+        r2 = torch.empty(P, device=dev)
+        its = torch.empty(P, dtype=torch.int32, device=dev)
+        rs = torch.empty(P, device=dev)
+        inf = torch.empty(P, dtype=torch.int32, device=dev)
+        res["simplex_ms"] = _event_ms(lambda: api.dr_project_simplex(K, s, t2, 5000, 1e-7, wsx, r2, its, rs, inf), reps)
+        res["simplex_steps"] = its.cpu().tolist()
+        # back-projection of a sketch-space vector to the 8 layers: writes
+        # 8 x 2048 x 2048 fp32 (the HBM-bound part)
+        u = torch.empty(int(layers[-1]["col_offset"]) + layers[-1]["p_in"].shape[0] * layers[-1]["p_out"].shape[0],
+                        device=dev)
+        bws = torch.empty(max(1, api.dr_backproject_workspace_size(layers)), dtype=torch.uint8, device=dev)
+        u.normal_()
+        ms = _event_ms(lambda: api.dr_back_project(layers, u, U, offs, workspace=bws), reps)
+        wbytes = 4.0 * sum(sizes)
+        res["back_project"] = {"ms": ms, "roofline": {"bound": "hbm", "achieved": wbytes / (ms * 1e-3) / 1e9,
+                                                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                                      "frac": wbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                                                      "algorithmic_bytes": wbytes}}
     return res
 
 
@@ -285,7 +335,7 @@ SKETCH_KERNELS = ("sketch_plan_kernel", "sketch_packed_kernel", "sketch_packed_r
 KT_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_kt -o small -- "
           "python -u bench.py --steps 50 --warmup 10 --no-cpu-baseline")
 PMC_CMD = ("rocprofv3 --pmc {c} --output-format csv -d gpurun_out/prof_{d} -o small -- "
-           "python -u bench.py --steps 5 --warmup 2 --no-cpu-baseline --copy-calibration")
+           "python -u bench.py --steps 5 --warmup 2 --no-cpu-baseline --no-next-rows --copy-calibration")
 SUM_CMD = "python bench.py --summarize-profiles gpurun_out/prof_kt gpurun_out/prof_fetch gpurun_out/prof_write"
 
 
@@ -346,7 +396,9 @@ def summarize_profiles(kt_dir, fetch_dir, write_dir):
     kt = ["# Kernel trace: small-block workload, bench step", "",
           "Command (repository root on the GPU box, `TMPDIR=/tmp`), summarised by", "",
           "```", KT_CMD, SUM_CMD, "```", "",
-          "60 calls per kernel of the step = 10 warmup + 50 timed steps. Durations in microseconds.", "",
+          "60 calls per kernel of the step = 10 warmup + 50 timed steps. The widening-row kernels (update "
+          "assembly, exact scorers, subset rules, simplex, back-projection) run after the step in their own "
+          "timed loops, with their own call counts. Durations in microseconds.", "",
           "| Kernel | Calls | Avg (us) | Min | Max | Share |", "|---|---|---|---|---|---|"] + rows + [
           "", f"The sketch call (`dr_sketch_grads`) = {' + '.join(SKETCH_KERNELS)} = **{sk_avg:.1f} us** per call "
           "(average kernel durations; bench.py's HIP-event time of the same call also spans the launch gaps)."]

@@ -228,7 +228,8 @@ dr_status dr_project_simplex(const float* K, const float* s, const float* t2, in
  * [k_out][k_in], the layout of dr_sketch_grads).  With u = dr_combine's
  * sketch-space update this is the parameter-space update of the MeSO
  * variant.  p_in / p_out have dtype `dtype`; x, dy are not used.
- * Requirements: 1 <= k_in, k_out <= 64; workspace of at least
+ * Requirements: 1 <= k_in, k_out <= 64; d_in a multiple of 4; U + u_offset[l]
+ * 16-byte aligned; workspace of at least
  * dr_backproject_workspace_size() bytes (one layer's P_in product).
  * ------------------------------------------------------------------------- */
 dr_status dr_back_project(const dr_layer* layers, int num_layers, dr_dtype dtype, const float* u, float* U,

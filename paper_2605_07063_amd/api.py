@@ -176,6 +176,18 @@ def dr_project_simplex(K, s, t2, max_iter, tol, w, resid2, iters, res, info, str
                                                        _stream(stream)))
 
 
+def _projector_layer_array(layers):
+    arr = (DrLayer * len(layers))()
+    for i, L in enumerate(layers):
+        arr[i] = DrLayer(None, 0, None, 0, L["p_in"].data_ptr(), L["p_out"].data_ptr(), L["p_in"].shape[1],
+                         L["p_out"].shape[1], L["p_in"].shape[0], L["p_out"].shape[0], int(L["col_offset"]))
+    return arr
+
+
+def dr_backproject_workspace_size(layers):
+    return _lib.load().dr_backproject_workspace_size(_projector_layer_array(layers), len(layers))
+
+
 def dr_back_project(layers, u, U, u_offset, workspace=None, stream=None):
     """U[u_offset[l]:] (as [d_out][d_in]) = P_out^T X'_l P_in for every layer."""
     lib = _lib.load()
@@ -188,10 +200,7 @@ def dr_back_project(layers, u, U, u_offset, workspace=None, stream=None):
             _contig(L[nm], nm)
     _dev(u, "u", torch.float32)
     _dev(U, "U", torch.float32)
-    arr = (DrLayer * len(layers))()
-    for i, L in enumerate(layers):
-        arr[i] = DrLayer(None, 0, None, 0, L["p_in"].data_ptr(), L["p_out"].data_ptr(), L["p_in"].shape[1],
-                         L["p_out"].shape[1], L["p_in"].shape[0], L["p_out"].shape[0], int(L["col_offset"]))
+    arr = _projector_layer_array(layers)
     ws, wsb = _workspace(lib.dr_backproject_workspace_size(arr, len(layers)), U.device, workspace)
     check("dr_back_project", lib.dr_back_project(arr, len(layers), _DTYPES[dtype], _ptr(u), _ptr(U),
                                                  _goff_array(u_offset), _ptr(ws), wsb, _stream(stream)))

@@ -8,9 +8,9 @@
 // MeSO variant of the layer-wise algorithm.
 //
 //   bp_left_kernel   T = X' P_in   [k_out][d_in] fp32 (small, workspace)
-//   bp_right_kernel  U = P_out^T T, one 16 (d_out) x 256 (d_in) tile per
-//                    workgroup: each thread owns one column and 16 rows, so a
-//                    value of T read from L2 feeds 16 FMAs; the P_out columns
+//   bp_right_kernel  U = P_out^T T, one 64 (d_out) x 256 (d_in) tile per
+//                    workgroup: each thread owns 16 rows x 4 columns, so a
+//                    float4 of T read from L2 feeds 64 FMAs; the P_out columns
 //                    of the tile sit in LDS.  The d_out x d_in fp32 write is
 //                    the HBM bound.
 
@@ -19,8 +19,8 @@
 namespace dr {
 namespace {
 
-constexpr int kBpRows = 16;
-constexpr int kBpCols = 256;
+constexpr int kBpRows = 16;    // rows per wave (4 waves: 64 rows per tile)
+constexpr int kBpCols = 256;   // columns per tile (4 per lane)
 constexpr int kBpMaxK = 64;
 
 template <typename TP>
@@ -39,30 +39,49 @@ __global__ __launch_bounds__(256) void bp_left_kernel(const float* x, const TP* 
   T[(long long)a * d_in + c] = acc;
 }
 
-// U[o][c] = sum_a P_out[a][o] T[a][c]
+// U[o][c] = sum_a P_out[a][o] T[a][c] for a 64 (d_out) x 256 (d_in) tile:
+// wave v owns rows 16 v .. 16 v + 15, lane l columns 4 l .. 4 l + 3; the
+// tile's P_out columns sit in LDS (every lane of a wave reads the same four
+// 16-byte words per a: broadcasts), T comes from L2 as float4.
 template <typename TP>
 __global__ __launch_bounds__(256) void bp_right_kernel(const TP* p_out, const float* T, int k_out, int d_out, int d_in,
                                                        float* U) {
-  __shared__ float po[kBpMaxK][kBpRows];
-  const int o0 = blockIdx.y * kBpRows;
-  const int c = blockIdx.x * kBpCols + threadIdx.x;
-  for (int e = threadIdx.x; e < k_out * kBpRows; e += 256) {
-    const int a = e / kBpRows, r = e % kBpRows;
+  __shared__ __attribute__((aligned(16))) float po[kBpMaxK][kBpRows * 4];
+  const int o0 = blockIdx.y * (kBpRows * 4);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int v = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c = blockIdx.x * kBpCols + 4 * lane;
+  for (int e = tid; e < k_out * kBpRows * 4; e += 256) {
+    const int a = e / (kBpRows * 4), r = e % (kBpRows * 4);
     po[a][r] = o0 + r < d_out ? ld(p_out, (long long)a * d_out + o0 + r) : 0.f;
   }
   __syncthreads();
   if (c >= d_in) return;
-  float acc[kBpRows];
+  float4 acc[kBpRows];
 #pragma unroll
-  for (int r = 0; r < kBpRows; ++r) acc[r] = 0.f;
+  for (int r = 0; r < kBpRows; ++r) acc[r] = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int a = 0; a < k_out; ++a) {
-    const float t = T[(long long)a * d_in + c];
+    const float4 t = *reinterpret_cast<const float4*>(T + (long long)a * d_in + c);
+    const float4* pr = reinterpret_cast<const float4*>(&po[a][kBpRows * v]);
 #pragma unroll
-    for (int r = 0; r < kBpRows; ++r) acc[r] = fmaf(po[a][r], t, acc[r]);
+    for (int q = 0; q < kBpRows / 4; ++q) {
+      const float4 pq = pr[q];
+      const float pv[4] = {pq.x, pq.y, pq.z, pq.w};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        float4& A = acc[4 * q + u];
+        A.x = fmaf(pv[u], t.x, A.x);
+        A.y = fmaf(pv[u], t.y, A.y);
+        A.z = fmaf(pv[u], t.z, A.z);
+        A.w = fmaf(pv[u], t.w, A.w);
+      }
+    }
   }
 #pragma unroll
-  for (int r = 0; r < kBpRows; ++r)
-    if (o0 + r < d_out) U[(long long)(o0 + r) * d_in + c] = acc[r];
+  for (int r = 0; r < kBpRows; ++r) {
+    const int o = o0 + kBpRows * v + r;
+    if (o < d_out) *reinterpret_cast<float4*>(U + (long long)o * d_in + c) = acc[r];
+  }
 }
 
 }  // namespace
@@ -88,7 +107,8 @@ extern "C" dr_status dr_back_project(const dr_layer* layers, int num_layers, dr_
     if (L.k_in < 1 || L.k_out < 1 || L.k_in > kBpMaxK || L.k_out > kBpMaxK) return DR_ERR_ARG;
     if (L.d_in < 1 || L.d_out < 1 || L.d_in > (1 << 28) || L.d_out > (1 << 28)) return DR_ERR_ARG;
     if (!L.p_in || !L.p_out || L.col_offset < 0 || u_offset[l] < 0) return DR_ERR_ARG;
-    if ((L.d_out + kBpRows - 1) / kBpRows > 65535) return DR_ERR_UNSUPPORTED;   // grid rows
+    if ((L.d_out + 4 * kBpRows - 1) / (4 * kBpRows) > 65535) return DR_ERR_UNSUPPORTED;   // grid rows
+    if (L.d_in % 4 || !aligned16(U + u_offset[l])) return DR_ERR_ARG;   // float4 columns and stores
   }
   if (!workspace || ws_bytes < dr_backproject_workspace_size(layers, num_layers)) return DR_ERR_WORKSPACE;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
@@ -98,7 +118,7 @@ extern "C" dr_status dr_back_project(const dr_layer* layers, int num_layers, dr_
     const int k_in = (int)L.k_in, k_out = (int)L.k_out, d_in = (int)L.d_in, d_out = (int)L.d_out;
     const float* x = u + L.col_offset;
     float* Ul = U + u_offset[l];
-    const dim3 gl((d_in + 255) / 256, k_out), gr((d_in + kBpCols - 1) / kBpCols, (d_out + kBpRows - 1) / kBpRows);
+    const dim3 gl((d_in + 255) / 256, k_out), gr((d_in + kBpCols - 1) / kBpCols, (d_out + 4 * kBpRows - 1) / (4 * kBpRows));
     if (dtype == DR_BF16) {
       hipLaunchKernelGGL(bp_left_kernel<__bf16>, gl, dim3(256), 0, hs, x, static_cast<const __bf16*>(L.p_in), k_in,
                          d_in, T);
