@@ -7,6 +7,8 @@
 // sketch-space update u~ = G~^T w it gives the parameter-space update of the
 // MeSO variant of the layer-wise algorithm.
 //
+// Up to 16 layers go in one launch (blockIdx.z = layer), so that the small
+// per-layer grids fill the chip together.
 //   bp_left_kernel   T = X' P_in   [k_out][d_in] fp32 (small, workspace)
 //   bp_right_kernel  U = P_out^T T, one 64 (d_out) x 256 (d_in) tile per
 //                    workgroup: each thread owns 16 rows x 4 columns, so a
@@ -19,6 +21,7 @@
 namespace dr {
 namespace {
 
+constexpr int kBpLayers = 16;  // layers per launch (blockIdx.z)
 constexpr int kBpRows = 16;    // rows per wave (4 waves: 64 rows per tile)
 constexpr int kBpCols = 256;   // columns per tile (4 per lane)
 constexpr int kBpMaxK = 64;
@@ -28,14 +31,35 @@ __device__ __forceinline__ float ld(const TP* p, long long i) {
   return (float)p[i];
 }
 
+struct BpArgs {
+  const void* p_in[kBpLayers];
+  const void* p_out[kBpLayers];
+  const float* x[kBpLayers];   // the layer's block of the sketch-space vector
+  float* T[kBpLayers];         // [k_out][d_in] workspace
+  float* U[kBpLayers];         // [d_out][d_in] output
+  int k_in[kBpLayers], k_out[kBpLayers], d_in[kBpLayers], d_out[kBpLayers];
+};
+
 // T[a][c] = sum_b X'[a][b] P_in[b][c]
 template <typename TP>
-__global__ __launch_bounds__(256) void bp_left_kernel(const float* x, const TP* p_in, int k_in, int d_in, float* T) {
+__global__ __launch_bounds__(256) void bp_left_kernel(BpArgs g) {
+  const int l = blockIdx.z;
   const int a = blockIdx.y;
   const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= d_in) return;
+  const int k_in = g.k_in[l], d_in = g.d_in[l];
+  if (a >= g.k_out[l] || c >= d_in) return;
+  const float* x = g.x[l];
+  const TP* p_in = static_cast<const TP*>(g.p_in[l]);
+  float* T = g.T[l];
   float acc = 0.f;
-  for (int b = 0; b < k_in; ++b) acc = fmaf(x[a * k_in + b], ld(p_in, (long long)b * d_in + c), acc);
+  for (int b0 = 0; b0 < k_in; b0 += 16) {   // 16 loads in flight before the FMAs
+    float pv[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) pv[u] = b0 + u < k_in ? ld(p_in, (long long)(b0 + u) * d_in + c) : 0.f;
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      if (b0 + u < k_in) acc = fmaf(x[a * k_in + b0 + u], pv[u], acc);
+  }
   T[(long long)a * d_in + c] = acc;
 }
 
@@ -44,10 +68,15 @@ __global__ __launch_bounds__(256) void bp_left_kernel(const float* x, const TP* 
 // tile's P_out columns sit in LDS (every lane of a wave reads the same four
 // 16-byte words per a: broadcasts), T comes from L2 as float4.
 template <typename TP>
-__global__ __launch_bounds__(256) void bp_right_kernel(const TP* p_out, const float* T, int k_out, int d_out, int d_in,
-                                                       float* U) {
+__global__ __launch_bounds__(256) void bp_right_kernel(BpArgs g) {
   __shared__ __attribute__((aligned(16))) float po[kBpMaxK][kBpRows * 4];
+  const int l = blockIdx.z;
+  const int k_out = g.k_out[l], d_out = g.d_out[l], d_in = g.d_in[l];
+  const TP* p_out = static_cast<const TP*>(g.p_out[l]);
+  const float* T = g.T[l];
+  float* U = g.U[l];
   const int o0 = blockIdx.y * (kBpRows * 4);
+  if (o0 >= d_out || blockIdx.x * kBpCols >= d_in) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int v = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = blockIdx.x * kBpCols + 4 * lane;
@@ -60,20 +89,29 @@ __global__ __launch_bounds__(256) void bp_right_kernel(const TP* p_out, const fl
   float4 acc[kBpRows];
 #pragma unroll
   for (int r = 0; r < kBpRows; ++r) acc[r] = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int a = 0; a < k_out; ++a) {
-    const float4 t = *reinterpret_cast<const float4*>(T + (long long)a * d_in + c);
-    const float4* pr = reinterpret_cast<const float4*>(&po[a][kBpRows * v]);
+  for (int a0 = 0; a0 < k_out; a0 += 8) {   // eight rows of T in flight before the FMAs
+    float4 tv[8];
 #pragma unroll
-    for (int q = 0; q < kBpRows / 4; ++q) {
-      const float4 pq = pr[q];
-      const float pv[4] = {pq.x, pq.y, pq.z, pq.w};
+    for (int e = 0; e < 8; ++e)
+      tv[e] = a0 + e < k_out ? *reinterpret_cast<const float4*>(T + (long long)(a0 + e) * d_in + c)
+                             : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        float4& A = acc[4 * q + u];
-        A.x = fmaf(pv[u], t.x, A.x);
-        A.y = fmaf(pv[u], t.y, A.y);
-        A.z = fmaf(pv[u], t.z, A.z);
-        A.w = fmaf(pv[u], t.w, A.w);
+    for (int e = 0; e < 8; ++e) {
+      if (a0 + e >= k_out) break;
+      const float4 t = tv[e];
+      const float4* pr = reinterpret_cast<const float4*>(&po[a0 + e][kBpRows * v]);
+#pragma unroll
+      for (int q = 0; q < kBpRows / 4; ++q) {
+        const float4 pq = pr[q];
+        const float pv[4] = {pq.x, pq.y, pq.z, pq.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          float4& A = acc[4 * q + u];
+          A.x = fmaf(pv[u], t.x, A.x);
+          A.y = fmaf(pv[u], t.y, A.y);
+          A.z = fmaf(pv[u], t.z, A.z);
+          A.w = fmaf(pv[u], t.w, A.w);
+        }
       }
     }
   }
@@ -89,12 +127,16 @@ __global__ __launch_bounds__(256) void bp_right_kernel(const TP* p_out, const fl
 
 extern "C" size_t dr_backproject_workspace_size(const dr_layer* layers, int num_layers) {
   if (!layers || num_layers < 1) return 0;
-  int64_t mx = 1;
-  for (int l = 0; l < num_layers; ++l) {
-    const int64_t t = layers[l].k_out * layers[l].d_in;
-    mx = t > mx ? t : mx;
+  // one launch holds up to 16 layers: room for the largest such run of T blocks
+  size_t best = 256;
+  for (int f = 0; f < num_layers; f += dr::kBpLayers) {
+    size_t o = 0;
+    for (int l = f; l < num_layers && l < f + dr::kBpLayers; ++l)
+      o = dr::align_up(o + (size_t)(layers[l].k_out > 0 ? layers[l].k_out : 0) *
+                               (size_t)(layers[l].d_in > 0 ? layers[l].d_in : 0) * 4, 256);
+    best = o > best ? o : best;
   }
-  return dr::align_up((size_t)mx * 4, 256);
+  return best;
 }
 
 extern "C" dr_status dr_back_project(const dr_layer* layers, int num_layers, dr_dtype dtype, const float* u, float* U,
@@ -112,23 +154,35 @@ extern "C" dr_status dr_back_project(const dr_layer* layers, int num_layers, dr_
   }
   if (!workspace || ws_bytes < dr_backproject_workspace_size(layers, num_layers)) return DR_ERR_WORKSPACE;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
-  float* T = static_cast<float*>(workspace);
-  for (int l = 0; l < num_layers; ++l) {
-    const dr_layer& L = layers[l];
-    const int k_in = (int)L.k_in, k_out = (int)L.k_out, d_in = (int)L.d_in, d_out = (int)L.d_out;
-    const float* x = u + L.col_offset;
-    float* Ul = U + u_offset[l];
-    const dim3 gl((d_in + 255) / 256, k_out), gr((d_in + kBpCols - 1) / kBpCols, (d_out + 4 * kBpRows - 1) / (4 * kBpRows));
+  for (int f = 0; f < num_layers; f += kBpLayers) {
+    const int count = num_layers - f < kBpLayers ? num_layers - f : kBpLayers;
+    BpArgs g = {};
+    int kmax = 1, dimax = 1, domax = 1;
+    size_t o = 0;
+    for (int j = 0; j < count; ++j) {
+      const dr_layer& L = layers[f + j];
+      g.p_in[j] = L.p_in;
+      g.p_out[j] = L.p_out;
+      g.x[j] = u + L.col_offset;
+      g.T[j] = reinterpret_cast<float*>(static_cast<unsigned char*>(workspace) + o);
+      o = align_up(o + (size_t)L.k_out * (size_t)L.d_in * 4, 256);
+      g.U[j] = U + u_offset[f + j];
+      g.k_in[j] = (int)L.k_in;
+      g.k_out[j] = (int)L.k_out;
+      g.d_in[j] = (int)L.d_in;
+      g.d_out[j] = (int)L.d_out;
+      kmax = g.k_out[j] > kmax ? g.k_out[j] : kmax;
+      dimax = g.d_in[j] > dimax ? g.d_in[j] : dimax;
+      domax = g.d_out[j] > domax ? g.d_out[j] : domax;
+    }
+    const dim3 gl((dimax + 255) / 256, kmax, count);
+    const dim3 gr((dimax + kBpCols - 1) / kBpCols, (domax + 4 * kBpRows - 1) / (4 * kBpRows), count);
     if (dtype == DR_BF16) {
-      hipLaunchKernelGGL(bp_left_kernel<__bf16>, gl, dim3(256), 0, hs, x, static_cast<const __bf16*>(L.p_in), k_in,
-                         d_in, T);
-      hipLaunchKernelGGL(bp_right_kernel<__bf16>, gr, dim3(256), 0, hs, static_cast<const __bf16*>(L.p_out),
-                         (const float*)T, k_out, d_out, d_in, Ul);
+      hipLaunchKernelGGL(bp_left_kernel<__bf16>, gl, dim3(256), 0, hs, g);
+      hipLaunchKernelGGL(bp_right_kernel<__bf16>, gr, dim3(256), 0, hs, g);
     } else {
-      hipLaunchKernelGGL(bp_left_kernel<float>, gl, dim3(256), 0, hs, x, static_cast<const float*>(L.p_in), k_in,
-                         d_in, T);
-      hipLaunchKernelGGL(bp_right_kernel<float>, gr, dim3(256), 0, hs, static_cast<const float*>(L.p_out),
-                         (const float*)T, k_out, d_out, d_in, Ul);
+      hipLaunchKernelGGL(bp_left_kernel<float>, gl, dim3(256), 0, hs, g);
+      hipLaunchKernelGGL(bp_right_kernel<float>, gr, dim3(256), 0, hs, g);
     }
     const dr_status st = launch_status();
     if (st != DR_OK) return st;
