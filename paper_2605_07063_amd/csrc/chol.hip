@@ -20,6 +20,11 @@
 //                    inverse, 64 rows per workgroup.
 //   lg_syrk_kernel   A22 -= L21 L21^T on 128x128 lower-triangle tiles, fp32
 //                    MFMA, the panel slices streamed through LDS in chunks.
+// Look-ahead: each trailing update runs as two launches, the first tile
+// column (the next panel) and then the rest; between them a second stream
+// (created for the call, default priority, ordered by events) factors the
+// next diagonal block and solves the next panel, so those latency-bound
+// steps run under the bulk of the trailing update.
 // Solve: L y = r and L^T dx = y block by block (one launch per block and
 // direction; every workgroup applies the block's inverse, then updates its
 // share of the remaining right-hand side), x += dx; three solves (the
@@ -388,11 +393,23 @@ __device__ __forceinline__ void tile_pair(int q, int& I, int& J) {
 constexpr int SY_CH = 32;                 // panel columns per chunk
 constexpr int SY_PANEL = NB * SY_CH * 4;  // bytes of one tile row's chunk (16 KiB)
 
-__global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL, int n, int k, const LgCtl* ctl) {
+// part: 0 = every lower-triangle tile, 1 = the first tile column only
+// (J = 0, which holds the next panel), 2 = every tile with J >= 1
+__global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL, int n, int k, int part,
+                                                         const LgCtl* ctl) {
   if (ctl->skip) return;
   __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * 2 * SY_PANEL];
   int I, J;
-  tile_pair(blockIdx.x, I, J);
+  if (part == 1) {
+    I = blockIdx.x;
+    J = 0;
+  } else {
+    tile_pair(blockIdx.x, I, J);
+    if (part == 2) {
+      ++I;
+      ++J;
+    }
+  }
   const int k1 = k + NB;
   const int ri = k1 + NB * I, rj = k1 + NB * J;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -634,6 +651,11 @@ __global__ __launch_bounds__(1024) void lg_final_kernel(const float* s, const fl
 
 size_t span_large_workspace(int64_t n) { return lg_layout(n).total; }
 
+static dr_status span_large_groups(const float* K, const float* s, const float* t2, int n, int P, float lambda,
+                                   int mode, float* w, float* lam_eff, float* resid2, int32_t* info,
+                                   const LgLayout& lay, unsigned char* base, hipStream_t hs, hipStream_t aux,
+                                   hipEvent_t ev_col, hipEvent_t ev_next);
+
 dr_status span_large(const float* K, const float* s, const float* t2, int64_t n64, int P, float lambda, int mode,
                      float* w, float* lam_eff, float* resid2, int32_t* info, void* ws, size_t ws_bytes,
                      hipStream_t hs) {
@@ -642,6 +664,28 @@ dr_status span_large(const float* K, const float* s, const float* t2, int64_t n6
   if (!aligned16(ws)) return DR_ERR_ARG;
   const int n = (int)n64;
   unsigned char* base = static_cast<unsigned char*>(ws);
+  // the look-ahead stream (default priority) and its two events live for this call only
+  hipStream_t aux = nullptr;
+  hipEvent_t ev_col = nullptr, ev_next = nullptr;
+  if (hipStreamCreateWithFlags(&aux, hipStreamNonBlocking) != hipSuccess) return DR_ERR_HIP;
+  if (hipEventCreateWithFlags(&ev_col, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&ev_next, hipEventDisableTiming) != hipSuccess) {
+    if (ev_col) (void)hipEventDestroy(ev_col);
+    (void)hipStreamDestroy(aux);
+    return DR_ERR_HIP;
+  }
+  const dr_status st_all = span_large_groups(K, s, t2, n, P, lambda, mode, w, lam_eff, resid2, info, lay, base, hs,
+                                             aux, ev_col, ev_next);
+  (void)hipEventDestroy(ev_col);
+  (void)hipEventDestroy(ev_next);
+  (void)hipStreamDestroy(aux);
+  return st_all;
+}
+
+static dr_status span_large_groups(const float* K, const float* s, const float* t2, int n, int P, float lambda,
+                                   int mode, float* w, float* lam_eff, float* resid2, int32_t* info,
+                                   const LgLayout& lay, unsigned char* base, hipStream_t hs, hipStream_t aux,
+                                   hipEvent_t ev_col, hipEvent_t ev_next) {
   float* L = reinterpret_cast<float*>(base + lay.off_L);
   float* inv = reinterpret_cast<float*>(base + lay.off_inv);
   float* invT = reinterpret_cast<float*>(base + lay.off_invT);
@@ -663,18 +707,34 @@ dr_status span_large(const float* K, const float* s, const float* t2, int64_t n6
     hipLaunchKernelGGL(lg_prep_kernel, dim3(pb), dim3(256), 0, hs, Kp, nn, vec, ctl);
     hipLaunchKernelGGL(lg_setup_kernel, dim3(1), dim3(1024), 0, hs, Kp, sp, n, lambda, mode, ctl, lam_eff + p);
     hipLaunchKernelGGL(lg_copy_kernel, dim3(n, (n + 1023) / 1024), dim3(256), 0, hs, Kp, n, L, ldL, ctl);
-    for (int b = 0; b < nblk; ++b) {
+    // Right-looking blocked factorisation with a one-panel look-ahead: the
+    // trailing update of panel b first refreshes the next panel's column of
+    // tiles, then, while it updates the rest, the aux stream factors the
+    // next diagonal block and solves the next panel (they touch only that
+    // column, which the rest of the update does not).
+    auto factor_panel = [&](int b, hipStream_t st) {
       const int k = NB * b;
       const int kb = n - k < NB ? n - k : NB;
       float* ib = inv + (long long)b * NB * NB;
       float* ibT = invT + (long long)b * NB * NB;
-      hipLaunchKernelGGL(lg_potrf_kernel, dim3(1), dim3(1024), 0, hs, L, ldL, k, kb, ib, ibT, ctl);
+      hipLaunchKernelGGL(lg_potrf_kernel, dim3(1), dim3(1024), 0, st, L, ldL, k, kb, ib, ibT, ctl);
       const int rest = n - k - NB;
-      if (rest > 0) {
-        hipLaunchKernelGGL(lg_trsm_kernel, dim3((rest + 63) / 64), dim3(256), 0, hs, L, ldL, n, k, ib, ctl);
-        const int T = (rest + NB - 1) / NB;
-        hipLaunchKernelGGL(lg_syrk_kernel, dim3(T * (T + 1) / 2), dim3(256), 0, hs, L, ldL, n, k, ctl);
-      }
+      if (rest > 0)
+        hipLaunchKernelGGL(lg_trsm_kernel, dim3((rest + 63) / 64), dim3(256), 0, st, L, ldL, n, k, ib, ctl);
+    };
+    factor_panel(0, hs);
+    for (int b = 0; b < nblk; ++b) {
+      const int k = NB * b;
+      const int rest = n - k - NB;
+      if (rest <= 0) break;
+      const int T = (rest + NB - 1) / NB;
+      hipLaunchKernelGGL(lg_syrk_kernel, dim3(T), dim3(256), 0, hs, L, ldL, n, k, 1, ctl);
+      if (hipEventRecord(ev_col, hs) != hipSuccess || hipStreamWaitEvent(aux, ev_col, 0) != hipSuccess)
+        return DR_ERR_HIP;
+      factor_panel(b + 1, aux);
+      if (hipEventRecord(ev_next, aux) != hipSuccess) return DR_ERR_HIP;
+      if (T > 1) hipLaunchKernelGGL(lg_syrk_kernel, dim3(T * (T - 1) / 2), dim3(256), 0, hs, L, ldL, n, k, 2, ctl);
+      if (hipStreamWaitEvent(hs, ev_next, 0) != hipSuccess) return DR_ERR_HIP;
     }
     for (int it = 0; it <= kRefine; ++it) {
       if (it > 0)
