@@ -294,7 +294,7 @@ size_t dr_greedy_workspace_size(int64_t n, int P);
  *   G [n][ldG] (DR_F32 or DR_BF16), w fp32 [P][n], u fp32 [goff[P]]
  *   (columns outside [goff[0], goff[P]) untouched).  fp64 accumulation.
  *   workspace: at least dr_combine_workspace_size() bytes (row-chunk
- *   partials in fp64).
+ *   partials in fp64; none for n <= 256, which runs in one pass).
  * ------------------------------------------------------------------------- */
 dr_status dr_combine(const void* G, int64_t n, int64_t ldG, dr_dtype dtype, const int64_t* goff,
                      int P, const float* w, float* u, void* workspace, size_t ws_bytes,

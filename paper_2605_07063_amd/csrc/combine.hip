@@ -3,10 +3,14 @@
 // or the subset mean g_S of the top-k rule when w = 1/k on the subset
 // (Sec. 3.3.2).
 //
-// combine_partial_kernel: one thread per column, a chunk of rows per
-// workgroup, fp64 accumulation in row order (rows are coalesced across the
-// workgroup's threads).  combine_reduce_kernel sums the row-chunk partials
-// in chunk order.  Deterministic.
+// n <= 256 (the per-step batches): combine_small_kernel, one pass.  A
+// workgroup takes 64 columns; its four waves take the rows i = q mod 4
+// (q = wave), fp64 accumulation in row order, and the four partial sums
+// are added in a fixed order through LDS.
+// Larger n: combine_partial_kernel, one thread per column, a chunk of rows
+// per workgroup, fp64 accumulation in row order (rows are coalesced across
+// the workgroup's threads); combine_reduce_kernel sums the row-chunk
+// partials in chunk order.  Deterministic.
 
 #include "common.h"
 
@@ -16,6 +20,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kMaxGroups = 128;
 constexpr int kTargetWGs = 2048;
+constexpr int kSmallN = 256;
 
 struct CombineArgs {
   const unsigned char* G;
@@ -50,6 +55,44 @@ __global__ __launch_bounds__(kThreads) void combine_partial_kernel(CombineArgs a
   a.partial[(long long)ch * (a.goff[a.P] - a.col_base) + (c - a.col_base)] = acc;
 }
 
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void combine_small_kernel(CombineArgs a, float* u) {
+  __shared__ double part[4][64];
+  const int p = blockIdx.y;
+  const int cl = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const long long c = a.goff[p] + (long long)blockIdx.x * 64 + cl;
+  const bool ok = c < a.goff[p + 1];
+  const float* wp = a.w + (long long)p * a.n;
+  double acc = 0.0;
+  if (ok) {
+    int i = q;
+    for (; i + 12 < a.n; i += 16) {   // four rows in flight
+      float g[4];
+#pragma unroll
+      for (int u4 = 0; u4 < 4; ++u4) {
+        const long long e = (long long)(i + 4 * u4) * a.ldG + c;
+        if constexpr (BF16)
+          g[u4] = __uint_as_float((unsigned)reinterpret_cast<const unsigned short*>(a.G)[e] << 16);
+        else
+          g[u4] = reinterpret_cast<const float*>(a.G)[e];
+      }
+#pragma unroll
+      for (int u4 = 0; u4 < 4; ++u4) acc += (double)wp[i + 4 * u4] * (double)g[u4];
+    }
+    for (; i < a.n; i += 4) {
+      float g;
+      if constexpr (BF16)
+        g = __uint_as_float((unsigned)reinterpret_cast<const unsigned short*>(a.G)[(long long)i * a.ldG + c] << 16);
+      else
+        g = reinterpret_cast<const float*>(a.G)[(long long)i * a.ldG + c];
+      acc += (double)wp[i] * (double)g;
+    }
+  }
+  part[q][cl] = acc;
+  __syncthreads();
+  if (q == 0 && ok) u[c] = (float)((part[0][cl] + part[1][cl]) + (part[2][cl] + part[3][cl]));
+}
+
 __global__ __launch_bounds__(kThreads) void combine_reduce_kernel(CombineArgs a, float* u) {
   const long long width = a.goff[a.P] - a.col_base;
   const long long c = (long long)blockIdx.x * kThreads + threadIdx.x;
@@ -63,7 +106,7 @@ __global__ __launch_bounds__(kThreads) void combine_reduce_kernel(CombineArgs a,
 }  // namespace dr
 
 extern "C" size_t dr_combine_workspace_size(int64_t n, const int64_t* goff, int P) {
-  if (!goff || P < 1 || n < 0) return 0;
+  if (!goff || P < 1 || n < 0 || n <= dr::kSmallN) return 0;
   const int64_t width = goff[P] - goff[0];
   int64_t maxw = 0;
   for (int p = 0; p < P; ++p) maxw = goff[p + 1] - goff[p] > maxw ? goff[p + 1] - goff[p] : maxw;
@@ -114,6 +157,16 @@ extern "C" dr_status dr_combine(const void* G, int64_t n, int64_t ldG, dr_dtype 
     a.partial = static_cast<double*>(workspace);
     a.col_base = goff[p0];
     if (a.goff[gp] == a.col_base) continue;
+    if (n <= kSmallN) {
+      dim3 grid((unsigned)((maxw + 63) / 64), (unsigned)gp);
+      if (dtype == DR_BF16)
+        hipLaunchKernelGGL(combine_small_kernel<true>, grid, dim3(kThreads), 0, hs, a, u);
+      else
+        hipLaunchKernelGGL(combine_small_kernel<false>, grid, dim3(kThreads), 0, hs, a, u);
+      dr_status st = launch_status();
+      if (st != DR_OK) return st;
+      continue;
+    }
     if (n > 0) {
       dim3 grid((unsigned)colblocks, (unsigned)nch, (unsigned)gp);
       if (dtype == DR_BF16)

@@ -28,6 +28,18 @@
 //                        scheduled in 4x8-tile chunks, one per XCD at a time.
 //   gram_mirror_kernel : fills the upper triangle from the lower one
 //                        (64x64 tiles through LDS), so K is exactly symmetric.
+// Small fp32 problems (n + 1 <= 128 rows: the per-step batches):
+//   gram_small_kernel  : one workgroup per 128-column chunk of a group forms
+//                        the chunk of gbar from the target rows (fp64 sum /
+//                        m, as target_mean_kernel) and stages the n + 1
+//                        augmented rows in LDS (row stride 132 floats: the
+//                        16 rows x 4 columns of an fp32 MFMA operand fall on
+//                        distinct banks); the four waves take the lower
+//                        16x16 blocks of the augmented Gram round-robin
+//                        (fp32 16x16x4 MFMA) and write chunk partials.
+//   gram_small_reduce_kernel : sums the chunk partials (one wave per element,
+//                        a fixed order) into K (both triangles), s (row n)
+//                        and t2 (element n, n).
 // No atomics: results are deterministic.
 
 #include "common.h"
@@ -169,6 +181,122 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_kernel(GramArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r)
         out[(wr * 32 + i * 16 + lg * 4 + r) * kTile + wc * 32 + j * 16 + lr] = acc[i][j][r];
+}
+
+
+// ---------------------------------------------------------------- small fp32
+
+constexpr int kSmCK = 128;           // columns per workgroup
+constexpr int kSmLd = kSmCK + 4;     // LDS row stride (floats)
+constexpr int kSmMaxRows = 128;      // n + 1 <= 128
+
+__global__ __launch_bounds__(kThreads) void gram_small_kernel(GramArgs a, const float* Gt, long long ldGt, int m,
+                                                              int NRP, int nchunks) {
+  __shared__ __attribute__((aligned(16))) float R[kSmMaxRows * kSmLd];
+  const int chunk = blockIdx.x, p = blockIdx.y;
+  const long long g0 = a.goff[p], g1 = a.goff[p + 1];
+  const long long c0 = g0 + (long long)chunk * kSmCK;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nb = NRP / 16;
+  float* out = a.partial + ((long long)p * nchunks + chunk) * NRP * NRP;
+  if (c0 >= g1) return;   // (uniform) past the group: the reduction skips this chunk
+  const int width = (int)(g1 - c0 < kSmCK ? g1 - c0 : kSmCK);   // a multiple of 4
+  // general rows 0 .. n-1 (float4 loads, eight in flight per thread before
+  // any store), zero columns past the group
+  const int c4 = tid & (kSmCK / 4 - 1), r0 = tid / (kSmCK / 4);   // 8 rows per pass
+  const bool cok = 4 * c4 < width;
+  for (int rb = 0; rb < a.n; rb += 64) {
+    float4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int r = rb + r0 + 8 * u;
+      v[u] = (r < a.n && cok) ? *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(a.G) +
+                                                                 (long long)r * a.ldG + c0 + 4 * c4)
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int r = rb + r0 + 8 * u;
+      if (r < a.n) *reinterpret_cast<float4*>(&R[r * kSmLd + 4 * c4]) = v[u];
+    }
+  }
+  // row n: the target mean of this chunk (fp64 sum over the m rows in order,
+  // eight loads in flight); rows n + 1 .. NRP - 1: zeros
+  if (tid < kSmCK) {
+    float gv = 0.f;
+    if (tid < width) {
+      double acc = 0.0;
+      for (int j0 = 0; j0 < m; j0 += 8) {
+        float t[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) t[u] = j0 + u < m ? Gt[(long long)(j0 + u) * ldGt + c0 + tid] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (j0 + u < m) acc += (double)t[u];
+      }
+      gv = (float)(acc / (double)m);
+    }
+    R[a.n * kSmLd + tid] = gv;
+  }
+  for (int e = tid; e < (NRP - a.n - 1) * kSmCK; e += kThreads)
+    R[(a.n + 1 + e / kSmCK) * kSmLd + e % kSmCK] = 0.f;
+  __syncthreads();
+  // lower blocks (I, J <= I) round-robin over the waves
+  const int lr = lane & 15, lk = lane >> 4, lg = lane >> 4;
+  const int nblocks = nb * (nb + 1) / 2;
+  for (int q = wave; q < nblocks; q += kThreads / 64) {
+    int I = 0;
+    while ((I + 1) * (I + 2) / 2 <= q) ++I;
+    const int J = q - I * (I + 1) / 2;
+    const float* ra = &R[(16 * I + lr) * kSmLd + lk];
+    const float* rb = &R[(16 * J + lr) * kSmLd + lk];
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+    for (int k = 0; k < kSmCK; k += 4) acc = mma_f32(ra[k], rb[k], acc);
+    // C layout: register r is row 4 lg + r of the block, column lane % 16
+#pragma unroll
+    for (int r = 0; r < 4; ++r) out[(16 * I + 4 * lg + r) * NRP + 16 * J + lr] = acc[r];
+  }
+}
+
+// K (both triangles), s and t2 from the chunk partials: one wave per element
+// of the lower triangle, lane l sums chunks l, l + 64, ... in order, then a
+// fixed xor tree across the lanes
+__global__ __launch_bounds__(kThreads) void gram_small_reduce_kernel(GramArgs a, int NRP, int nchunks, float* K,
+                                                                     float* s, float* t2, long long pbase) {
+  const int p = blockIdx.y;
+  const int nr = a.n + 1;
+  const int e = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);   // lower-triangle element
+  const int lane = threadIdx.x & 63;
+  if (e >= nr * (nr + 1) / 2) return;
+  int r = 0;
+  while ((r + 1) * (r + 2) / 2 <= e) ++r;
+  const int c = e - r * (r + 1) / 2;
+  const long long width = a.goff[p + 1] - a.goff[p];
+  const int nvalid = (int)((width + kSmCK - 1) / kSmCK);
+  const float* src = a.partial + (long long)p * nchunks * NRP * NRP + r * NRP + c;
+  float acc = 0.f;
+  for (int ch0 = 0; ch0 < nvalid; ch0 += 256) {
+    float v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int ch = ch0 + lane + 64 * u;
+      v[u] = ch < nvalid ? src[(long long)ch * NRP * NRP] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc += v[u];
+  }
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+  if (lane != 0) return;
+  if (r < a.n) {
+    float* Kp = K + (pbase + p) * (long long)a.n * a.n;
+    Kp[(long long)r * a.n + c] = acc;
+    Kp[(long long)c * a.n + r] = acc;
+  } else if (c < a.n) {
+    s[(pbase + p) * (long long)a.n + c] = acc;
+  } else {
+    t2[pbase + p] = acc;
+  }
 }
 
 // ---------------------------------------------------------------- large n
@@ -426,7 +554,11 @@ struct GramPlan {
   int64_t rows;
   int NT, pairs, CK, maxchunks;
   size_t gbar_bytes, partial_bytes;
+  bool small;       // gram_small_kernel path
+  int NRP;          // its padded row count
 };
+
+bool gram_use_small(int64_t n, dr_dtype dtype) { return dtype == DR_F32 && n >= 1 && n + 1 <= kSmMaxRows; }
 
 // Chunk length: a multiple of 256 columns, shrunk until a launch has about
 // kTargetWGs workgroups; identical for every launch of a call.
@@ -448,6 +580,13 @@ GramPlan gram_plan(int64_t n, const int64_t* goff, int P, dr_dtype dtype) {
   g.partial_bytes = (size_t)gp * g.pairs * g.maxchunks * kTile * kTile * sizeof(float);
   if (rows == 0 || gram_use_big(n, P, dtype)) g.partial_bytes = 0;
   g.rows = rows;
+  g.small = gram_use_small(n, dtype);
+  g.NRP = (int)((n + 1 + 15) / 16 * 16);
+  if (g.small) {
+    g.maxchunks = (int)((maxw + kSmCK - 1) / kSmCK);
+    if (g.maxchunks < 1) g.maxchunks = 1;
+    g.partial_bytes = (size_t)gp * g.maxchunks * g.NRP * g.NRP * sizeof(float);
+  }
   return g;
 }
 
@@ -495,7 +634,7 @@ extern "C" dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* 
   float* partial = reinterpret_cast<float*>(static_cast<unsigned char*>(workspace) + g.gbar_bytes);
 
   const long long c_lo = goff[0], c_hi = goff[P];
-  if (c_hi > c_lo) {
+  if (c_hi > c_lo && !g.small) {   // the small path forms gbar inside its chunks
     const int blocks = (int)((c_hi - c_lo + kThreads - 1) / kThreads);
     if (bf)
       hipLaunchKernelGGL(target_mean_kernel<true>, dim3(blocks), dim3(kThreads), 0, hs,
@@ -537,6 +676,14 @@ extern "C" dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* 
       const int T64 = (int)((n + 63) / 64);
       hipLaunchKernelGGL(gram_mirror_kernel, dim3(T64 * (T64 + 1) / 2, gp), dim3(kThreads), 0, hs,
                          K + (long long)p0 * n * n, (int)n);
+      if ((st = launch_status()) != DR_OK) return st;
+    } else if (g.small) {
+      hipLaunchKernelGGL(gram_small_kernel, dim3(g.maxchunks, gp), dim3(kThreads), 0, hs, a,
+                         static_cast<const float*>(Gt), (long long)ldGt, (int)m, g.NRP, g.maxchunks);
+      if ((st = launch_status()) != DR_OK) return st;
+      const int nr = (int)n + 1;
+      hipLaunchKernelGGL(gram_small_reduce_kernel, dim3((nr * (nr + 1) / 2 + kThreads / 64 - 1) / (kThreads / 64), gp),
+                         dim3(kThreads), 0, hs, a, g.NRP, g.maxchunks, K, s, t2, (long long)p0);
       if ((st = launch_status()) != DR_OK) return st;
     } else if (g.rows > 0) {
       dim3 grid(g.maxchunks, g.pairs, gp);

@@ -135,9 +135,10 @@ def test_solver_and_select_argument_errors(lib):
     g = goff(0, 64)
     assert lib.dr_combine(FAKE, 8, 64, 9, g, 1, FAKE, FAKE, None, 0, None) == E.DR_ERR_DTYPE
     assert lib.dr_combine(FAKE, 8, 32, E.DR_F32, g, 1, FAKE, FAKE, None, 0, None) == E.DR_ERR_ARG
-    need = lib.dr_combine_workspace_size(8, g, 1)
+    assert lib.dr_combine_workspace_size(8, g, 1) == 0          # n <= 256: one pass, no partials
+    need = lib.dr_combine_workspace_size(1000, g, 1)
     assert need > 0
-    assert lib.dr_combine(FAKE, 8, 64, E.DR_F32, g, 1, FAKE, FAKE, None, 0, None) == E.DR_ERR_WORKSPACE
+    assert lib.dr_combine(FAKE, 1000, 64, E.DR_F32, g, 1, FAKE, FAKE, None, 0, None) == E.DR_ERR_WORKSPACE
 
 
 def update_call(lib, layers, n=4, T=8, dtype=_lib.DR_F32, w=FAKE, P=1, ldw=4, gol=None, U=FAKE, offs=None,

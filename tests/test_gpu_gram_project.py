@@ -29,6 +29,8 @@ def rand(shape, seed, dtype=torch.float32, scale=1.0):
     (130, 2048 + 512, [0, 512, 512, 2560], torch.float32),   # three groups, one empty
     (200, 3000 // 8 * 8, None, torch.bfloat16),
     (1, 64, None, torch.float32),
+    (64, 2048 + 512 + 68, [0, 512, 512, 2628], torch.float32),   # one-pass small path: groups, one empty, ragged chunk
+    (127, 8192, None, torch.float32),                 # largest n of the one-pass path
 ])
 def test_gram_matches_oracle(n, kappa, goff, dtype):
     G = rand((n, kappa), 10 + n, dtype)
@@ -423,9 +425,10 @@ def test_topk_ties_signed_zero_infinities_and_nan(golden_dir):
 
 # --------------------------------------------------------------------------- combine
 
-@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-def test_combine_groups(dtype):
-    n, kappa = 300, 4096
+@pytest.mark.parametrize("dtype,n", [(torch.float32, 300), (torch.bfloat16, 300), (torch.float32, 64),
+                                     (torch.bfloat16, 64), (torch.float32, 1), (torch.float32, 13)])
+def test_combine_groups(dtype, n):
+    kappa = 4096
     G = rand((n, kappa), 500, dtype)
     goff = [0, 1024, 1024, 4096]
     w = rand((3, n), 501)
