@@ -12,7 +12,9 @@
 //                        ties) by ranking every entry against all others.
 //   update_bf16_kernel   one 256 x 256 tile of U per workgroup, 8 waves of
 //                        128 (d_out) x 64 (d_in).  Tokens go through a
-//                        4-stage LDS ring in steps of 32, filled by
+//                        2-stage LDS ring in steps of 64 (64 KB a stage:
+//                        the next step loads during the 64 MFMAs of this
+//                        one, fewer and longer steps than 4 x 32), filled by
 //                        buffer->LDS DMA in their natural token-major
 //                        layout; both MFMA operands need 8 consecutive
 //                        tokens per lane, which the gfx950 transposing LDS
@@ -43,12 +45,14 @@ constexpr int kMaxUpdLayers = 16;
 constexpr int kMaxSplit = 32;
 
 // bf16 tile
-constexpr int kBO = 256, kBI = 256, kBK = 32;
+constexpr int kBO = 256, kBI = 256, kBK = 64;
 constexpr int kBThreads = 512;
-constexpr int kBDyBytes = kBK * kBO * 2;   // 16 KB: 32 token rows of 512 bytes
-constexpr int kBXBytes = kBK * kBI * 2;    // 16 KB
+constexpr int kBDyBytes = kBK * kBO * 2;   // kBK token rows of 512 bytes
+constexpr int kBXBytes = kBK * kBI * 2;
+constexpr int kBNH = kBK / 16;             // 1 KB DMA blocks per operand per wave and step
+constexpr int kBKK = kBK / 32;             // MFMA reduction slices per step
 constexpr int kBStage = kBDyBytes + kBXBytes;
-constexpr int kBStages = 4;
+constexpr int kBStages = 2;
 
 // f32 tile
 constexpr int kFO = 64, kFI = 64, kFK = 16;
@@ -223,13 +227,13 @@ __global__ __launch_bounds__(kBThreads) void update_bf16_kernel(UpdArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  // DMA roles: both tiles have 32 token rows of 512 bytes; wave w fills
-  // rows 2w, 2w + 1 and 2w + 16, 2w + 17 of each (1 KB per wave load).
+  // DMA roles: both tiles have kBK token rows of 512 bytes; wave w fills
+  // rows 2j, 2j + 1 for j = w, w + 8, ... of each (1 KB per wave load).
   // Lane l fills 16 bytes: physical slot u / 2, half u % 2 of its row.
-  int rrow[2];
-  unsigned cdy[2], cx[2];   // byte column inside a token row, or kOobOffset
+  int rrow[kBNH];
+  unsigned cdy[kBNH], cx[kBNH];   // byte column inside a token row, or kOobOffset
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
+  for (int h = 0; h < kBNH; ++h) {
     const int j = w + 8 * h;
     const int r = 2 * j + (lane >> 5), u = lane & 31;
     const int col = 16 * ((u >> 1) ^ slot_xor(r)) + 8 * (u & 1);
@@ -243,13 +247,13 @@ __global__ __launch_bounds__(kBThreads) void update_bf16_kernel(UpdArgs a) {
   auto issue = [&](int st) {
     unsigned char* sb = lds + st * kBStage;
     __amdgpu_buffer_rsrc_t rdys, rxs;
-    unsigned o_dy[2], o_x[2];
+    unsigned o_dy[kBNH], o_x[kBNH];
     if (ie < e_hi) {
       const long long e = ex[ie];
       rdys = make_rsrc(Lr.dy + e * Lr.exdy, kOobOffset);
       rxs = make_rsrc(Lr.x + e * Lr.exx, kOobOffset);
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
+      for (int h = 0; h < kBNH; ++h) {
         const int t = it + rrow[h];
         o_dy[h] = (t < ilen && cdy[h] != kOobOffset) ? (unsigned)t * rowb_dy + cdy[h] : kOobOffset;
         o_x[h] = (t < ilen && cx[h] != kOobOffset) ? (unsigned)t * rowb_x + cx[h] : kOobOffset;
@@ -263,12 +267,13 @@ __global__ __launch_bounds__(kBThreads) void update_bf16_kernel(UpdArgs a) {
     } else {
       rdys = make_rsrc(Lr.dy, kOobOffset);
       rxs = make_rsrc(Lr.x, kOobOffset);
-      o_dy[0] = o_dy[1] = o_x[0] = o_x[1] = kOobOffset;
+#pragma unroll
+      for (int h = 0; h < kBNH; ++h) o_dy[h] = o_x[h] = kOobOffset;
     }
-    dma16<kAuxCached>(rdys, sb + w * 1024, o_dy[0]);
-    dma16<kAuxCached>(rdys, sb + (w + 8) * 1024, o_dy[1]);
-    dma16<kAuxCached>(rxs, sb + kBDyBytes + w * 1024, o_x[0]);
-    dma16<kAuxCached>(rxs, sb + kBDyBytes + (w + 8) * 1024, o_x[1]);
+#pragma unroll
+    for (int h = 0; h < kBNH; ++h) dma16<kAuxCached>(rdys, sb + (w + 8 * h) * 1024, o_dy[h]);
+#pragma unroll
+    for (int h = 0; h < kBNH; ++h) dma16<kAuxCached>(rxs, sb + kBDyBytes + (w + 8 * h) * 1024, o_x[h]);
   };
 
   // fragment reads: lane (g, q, r) of the transposing read addresses token
@@ -296,29 +301,33 @@ __global__ __launch_bounds__(kBThreads) void update_bf16_kernel(UpdArgs a) {
 #pragma unroll
     for (int st = 0; st < kBStages - 1; ++st) issue(st);
     for (int step = 0; ce < e_hi; ++step) {
-      DR_WAIT_VM(4 * (kBStages - 2));   // this step's four loads are done; later steps' may be in flight
+      DR_WAIT_VM(2 * kBNH * (kBStages - 2));   // this step's loads are done; later steps' may be in flight
       DR_LDS_SYNC();
       issue((step + kBStages - 1) % kBStages);
-      const unsigned char* sb = lds + (step % kBStages) * kBStage;
-      u32x4 fa[8], fb[4];
+      const unsigned char* sb0 = lds + (step % kBStages) * kBStage;
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const v4s lo = lds_read_tr16(sb + offb[b]);
-        const v4s hi = lds_read_tr16(sb + offb[b] + 4 * 512);
-        fb[b] = u32x4{__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
-                      __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y};
+      for (int kk = 0; kk < kBKK; ++kk) {
+        const unsigned char* sb = sb0 + kk * 32 * 512;   // token rows 32 kk .. 32 kk + 31
+        u32x4 fa[8], fb[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const v4s lo = lds_read_tr16(sb + offb[b]);
+          const v4s hi = lds_read_tr16(sb + offb[b] + 4 * 512);
+          fb[b] = u32x4{__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
+                        __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y};
+        }
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+          const v4s lo = lds_read_tr16(sb + offa[b]);
+          const v4s hi = lds_read_tr16(sb + offa[b] + 4 * 512);
+          fa[b] = u32x4{__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
+                        __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y};
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[i][j] = mma_bf16(fa[i], fb[j], acc[i][j]);
       }
-#pragma unroll
-      for (int b = 0; b < 8; ++b) {
-        const v4s lo = lds_read_tr16(sb + offa[b]);
-        const v4s hi = lds_read_tr16(sb + offa[b] + 4 * 512);
-        fa[b] = u32x4{__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
-                      __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y};
-      }
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mma_bf16(fa[i], fb[j], acc[i][j]);
       ct += kBK;
       if (ct >= clen) {
         if constexpr (SCORE) {
