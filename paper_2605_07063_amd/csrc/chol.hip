@@ -13,18 +13,23 @@
 //   ctl   status shared by the kernels of one group (skip / info / lam_eff)
 //
 // Per 128-column panel k:
-//   lg_potrf_kernel  one workgroup factors the diagonal block in registers
-//                    (rows over lanes, 16-column slices over 16 waves, one
-//                    barrier per pivot), then inverts it row by row.
+//   lg_potrf_kernel  one workgroup factors and inverts the diagonal block
+//                    in 16-column steps: one wave factors and inverts each
+//                    16x16 diagonal sub-block in registers (v_readlane
+//                    broadcasts, no barrier per pivot); the sub-panel solve,
+//                    the trailing update and the off-diagonal blocks of the
+//                    inverse are fp32 MFMA products in LDS.
 //   lg_trsm_kernel   L21 = A21 L11^-T as an fp32 MFMA product with the
 //                    inverse, 64 rows per workgroup.
 //   lg_syrk_kernel   A22 -= L21 L21^T on 128x128 lower-triangle tiles, fp32
 //                    MFMA, the panel slices streamed through LDS in chunks.
-// Look-ahead: each trailing update runs as two launches, the first tile
-// column (the next panel) and then the rest; between them a second stream
-// (created for the call, default priority, ordered by events) factors the
-// next diagonal block and solves the next panel, so those latency-bound
-// steps run under the bulk of the trailing update.
+// Panels go in pairs: the trailing matrix takes one rank-256 update per
+// pair, as two launches, the next pair's two tile columns and then the
+// rest; between them a second stream (created for the call, default
+// priority, ordered by events) factors the next pair (diagonal block, panel
+// solve, the rank-128 update of the pair's second column, its diagonal
+// block and panel), so those latency-bound steps run under the bulk of the
+// trailing update.
 // Solve: L y = r and L^T dx = y block by block (one launch per block and
 // direction; every workgroup applies the block's inverse, then updates its
 // share of the remaining right-hand side), x += dx; three solves (the
@@ -190,137 +195,250 @@ __global__ __launch_bounds__(256) void lg_copy_kernel(const float* K, int n, flo
 
 // ---------------------------------------------------------------- panel
 
+__device__ __forceinline__ void tile_pair(int q, int& I, int& J) {
+  int i = (int)((sqrtf(8.f * q + 1.f) - 1.f) * 0.5f);
+  while ((i + 1) * (i + 2) / 2 <= q) ++i;
+  while (i * (i + 1) / 2 > q) --i;
+  I = i;
+  J = q - i * (i + 1) / 2;
+}
+
+__device__ __forceinline__ float readlane_f(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
 // Factor and invert the kb x kb diagonal block at (k, k) (kb <= 128; the
-// block is padded to 128 with the identity).  Wave w owns rows
-// 64 (w & 1) .. +64 (one per lane) and columns 16 (w >> 1) .. +16.
-__global__ __launch_bounds__(1024) void lg_potrf_kernel(float* L, long long ldL, int k, int kb, float* inv,
-                                                        float* invT, LgCtl* ctl) {
+// block is padded to 128 with the identity), blocked by PB-column steps:
+//   one wave factors the PB x PB diagonal sub-block D and inverts it in
+//   registers (lane r holds row r; the pivot row and column reach the
+//   other lanes by v_readlane, so no barrier inside);
+//   the sub-panel below becomes A D^-T and the trailing sub-matrix takes
+//   its rank-PB update, both as fp32 MFMA products over the four waves;
+// then the off-diagonal PB-blocks of the inverse follow by block distance
+// from the diagonal, X_ij = -X_ii sum_{m=j}^{i-1} L_im X_mj.
+constexpr int LDA = NB + 4;   // LDS row stride (floats) of the block and of its inverse
+
+template <int PB>
+__device__ void potrf_base(float* As, float* Xs, int c0, int lane, int& bad) {
+  const int r = lane % PB;
+  float a[PB];
+  const float* src = As + (c0 + r) * LDA + c0;
+#pragma unroll
+  for (int m = 0; m < PB; ++m) a[m] = m <= r ? src[m] : 0.f;
+  float dv[PB];
+#pragma unroll
+  for (int j = 0; j < PB; ++j) {
+    float d = readlane_f(a[j], j);
+    if (!(d > 0.f)) {
+      if (bad == 0) bad = c0 + j + 1;
+      d = 1.f;
+    }
+    const float rs = rsqrt_nr(d);
+    dv[j] = rs;
+    const float l = r > j ? a[j] * rs : (r == j ? d * rs : 0.f);
+    a[j] = l;
+    const float f = r > j ? l : 0.f;
+#pragma unroll
+    for (int c = j + 1; c < PB; ++c) a[c] = fmaf(-f, readlane_f(a[j], c), a[c]);
+  }
+  // inverse, lane r = column r: x_i = (delta_ir - sum_{m<i} L_im x_m) / L_ii
+  float x[PB];
+#pragma unroll
+  for (int i = 0; i < PB; ++i) {
+    float acc = i == r ? 1.f : 0.f;
+#pragma unroll
+    for (int m = 0; m < i; ++m) acc = fmaf(-readlane_f(a[m], i), x[m], acc);
+    x[i] = acc * dv[i];
+  }
+  if (lane < PB) {
+    float* dst = As + (c0 + r) * LDA + c0;
+#pragma unroll
+    for (int m = 0; m < PB; ++m) dst[m] = m <= r ? a[m] : 0.f;
+#pragma unroll
+    for (int i = 0; i < PB; ++i) Xs[(c0 + i) * LDA + c0 + r] = x[i];
+  }
+}
+
+// C[row][col] += sum_{m < len} A[ra + row][ca + m] B[rb + col][cb + m] on one
+// 16x16 tile (both operands read along their rows, a float4 per lane)
+__device__ __forceinline__ f32x4 tile_nt(const float* A, int ra, int ca, const float* B, int rb, int cb, int len,
+                                         int lr, int lq, f32x4 acc) {
+  for (int m = 0; m < len; m += 16) {
+    const float4 av = *reinterpret_cast<const float4*>(&A[(ra + lr) * LDA + ca + m + 4 * lq]);
+    const float4 bv = *reinterpret_cast<const float4*>(&B[(rb + lr) * LDA + cb + m + 4 * lq]);
+    acc = mma_f32(av.x, bv.x, acc);
+    acc = mma_f32(av.y, bv.y, acc);
+    acc = mma_f32(av.z, bv.z, acc);
+    acc = mma_f32(av.w, bv.w, acc);
+  }
+  return acc;
+}
+
+// C[row][col] += sum_{m < len} A[ra + row][ca + m] B[rb + m][cb + col]
+__device__ __forceinline__ f32x4 tile_nn(const float* A, int ra, int ca, const float* B, int rb, int cb, int len,
+                                         int lr, int lq, f32x4 acc) {
+  for (int m = 0; m < len; m += 16) {
+    const float4 av = *reinterpret_cast<const float4*>(&A[(ra + lr) * LDA + ca + m + 4 * lq]);
+    const float* bp = &B[(rb + m + 4 * lq) * LDA + cb + lr];
+    acc = mma_f32(av.x, bp[0], acc);
+    acc = mma_f32(av.y, bp[LDA], acc);
+    acc = mma_f32(av.z, bp[2 * LDA], acc);
+    acc = mma_f32(av.w, bp[3 * LDA], acc);
+  }
+  return acc;
+}
+
+template <int PB>
+__global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, int k, int kb, float* inv,
+                                                       float* invT, LgCtl* ctl) {
   if (ctl->skip) return;
-  __shared__ __attribute__((aligned(16))) float colb[2][NB];
-  __shared__ __attribute__((aligned(16))) float rowb[2][NB];
-  __shared__ float Ls[NB][NB + 1];
-  __shared__ float dinv[NB];      // 1 / L_jj
+  constexpr int NS = NB / PB;            // sub-blocks
+  constexpr int TPB = PB / 16;           // 16-wide tiles per sub-block edge
+  constexpr int MAXP = (NB - PB) / 16 * TPB;   // tiles of the largest sub-panel
+  constexpr int MAXX = (NS - 1) * TPB * TPB;   // tiles of the largest inverse diagonal
+  constexpr int UP = (MAXP + 3) / 4, UX = (MAXX + 3) / 4;
+  __shared__ __attribute__((aligned(16))) float lds_f[2 * NB * LDA];
+  float* As = lds_f;              // [NB][LDA] the block, then its factor
+  float* Xs = lds_f + NB * LDA;   // [NB][LDA] the inverse
+  __shared__ int bad_s;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int cs = w >> 1;          // column slice
-  const int rlast = 64 * (w & 1) + 63;   // last row of this wave
-  const int i = 64 * (w & 1) + lane;
-  const int c0 = 16 * cs;
-  const bool live = i < kb;
-  float a[16];
-  if (live) {
-    // only chunks that start on or left of the diagonal (they end inside the row)
-    const float4* src = reinterpret_cast<const float4*>(L + (long long)(k + i) * ldL + k + c0);
+  const int lr = lane & 15, lq = lane >> 4;
+
+  {
+    // all 16 row chunks of a thread in flight before the LDS writes
+    float4 v[NB * NB / 4 / 256];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float4 v = c0 + 4 * q <= i ? src[q] : make_float4(0.f, 0.f, 0.f, 0.f);
-      a[4 * q] = v.x;
-      a[4 * q + 1] = v.y;
-      a[4 * q + 2] = v.z;
-      a[4 * q + 3] = v.w;
+    for (int u = 0; u < NB * NB / 4 / 256; ++u) {
+      const int e = tid + 256 * u, i = e / (NB / 4), c = 4 * (e % (NB / 4));
+      v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      // only chunks that start on or left of the diagonal (they end inside the row)
+      if (i < kb && c <= i) v[u] = *reinterpret_cast<const float4*>(L + (long long)(k + i) * ldL + k + c);
     }
 #pragma unroll
-    for (int c = 0; c < 16; ++c)
-      if (c0 + c > i) a[c] = 0.f;
-  } else {
-#pragma unroll
-    for (int c = 0; c < 16; ++c) a[c] = (c0 + c == i) ? 1.f : 0.f;
+    for (int u = 0; u < NB * NB / 4 / 256; ++u) {
+      const int e = tid + 256 * u, i = e / (NB / 4), c = 4 * (e % (NB / 4));
+      float4 a = v[u];
+      if (i < kb) {
+        if (c + 1 > i) a.y = 0.f;
+        if (c + 2 > i) a.z = 0.f;
+        if (c + 3 > i) a.w = 0.f;
+      } else {
+        a.x = c == i ? 1.f : 0.f;
+        a.y = c + 1 == i ? 1.f : 0.f;
+        a.z = c + 2 == i ? 1.f : 0.f;
+        a.w = c + 3 == i ? 1.f : 0.f;
+      }
+      *reinterpret_cast<float4*>(&As[i * LDA + c]) = a;
+      *reinterpret_cast<float4*>(&Xs[i * LDA + c]) = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
   }
-  if (cs == 0) colb[0][i] = a[0];
   __syncthreads();
 
   int bad = 0;
-  for (int jb = 0; jb < NB / 16; ++jb) {
+  for (int sb = 0; sb < NS; ++sb) {
+    const int c0 = PB * sb, r0 = c0 + PB;
+    if (w == 0) potrf_base<PB>(As, Xs, c0, lane, bad);
+    __syncthreads();
+    // sub-panel: L[i][c0 + c] = sum_m A[i][c0 + m] X_D[c][m], rows i >= r0
+    const int np = (NB - r0) / 16 * TPB;
+    f32x4 acc[UP];
 #pragma unroll
-    for (int jc = 0; jc < 16; ++jc) {
-      const int j = 16 * jb + jc;
-      const float* cb = colb[jc & 1];
-      float d = cb[j];
-      if (!(d > 0.f)) {
-        if (bad == 0) bad = j + 1;
-        d = 1.f;
-      }
-      const float r = rsqrt_nr(d);
-      if (tid == 0) dinv[j] = r;
-      const float lij = i > j ? cb[i] * r : 0.f;
-      const float f = lij * r;
-      if (cs == jb) {
-        a[jc] = i > j ? lij : (i == j ? d * r : 0.f);
-#pragma unroll
-        for (int c = jc + 1; c < 16; ++c) a[c] = fmaf(-f, cb[c0 + c], a[c]);
-        if (jc + 1 < 16) colb[(jc + 1) & 1][i] = a[jc + 1];
-      } else if (cs > jb) {
-        if (rlast > j) {   // rows at or above the pivot have f = 0
-#pragma unroll
-          for (int c = 0; c < 16; c += 4) {
-            const float4 v = *reinterpret_cast<const float4*>(&cb[c0 + c]);
-            a[c] = fmaf(-f, v.x, a[c]);
-            a[c + 1] = fmaf(-f, v.y, a[c + 1]);
-            a[c + 2] = fmaf(-f, v.z, a[c + 2]);
-            a[c + 3] = fmaf(-f, v.w, a[c + 3]);
-          }
-        }
-        if (jc == 15 && cs == jb + 1) colb[0][i] = a[0];
-      }
-      __syncthreads();
+    for (int u = 0; u < UP; ++u) {
+      const int t = w + 4 * u;
+      acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (t < np) acc[u] = tile_nt(As, r0 + 16 * (t / TPB), c0, Xs, c0 + 16 * (t % TPB), c0, PB, lr, lq, acc[u]);
     }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < UP; ++u) {
+      const int t = w + 4 * u;
+      if (t < np) {
+        const int i0 = r0 + 16 * (t / TPB), cc = c0 + 16 * (t % TPB);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) As[(i0 + 4 * lq + j) * LDA + cc + lr] = acc[u][j];
+      }
+    }
+    __syncthreads();
+    // trailing: A[i][j] -= sum_m L[i][c0 + m] L[j][c0 + m], lower 16x16 tiles
+    const int T = (NB - r0) / 16, nt = T * (T + 1) / 2;
+    for (int t = w; t < nt; t += 4) {
+      int I, J;
+      tile_pair(t, I, J);
+      const f32x4 p = tile_nt(As, r0 + 16 * I, c0, As, r0 + 16 * J, c0, PB, lr, lq, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+      for (int j = 0; j < 4; ++j) As[(r0 + 16 * I + 4 * lq + j) * LDA + r0 + 16 * J + lr] -= p[j];
+    }
+    __syncthreads();
   }
-  if (bad) {
+  if (w == 0 && lane == 0) bad_s = bad;
+  __syncthreads();
+  if (bad_s) {
     // padded pivots are exactly 1: a failure is always inside the block
     if (tid == 0) {
-      ctl->info = k + bad;
+      ctl->info = k + bad_s;
       ctl->skip = 1;
     }
     return;
   }
-#pragma unroll
-  for (int c = 0; c < 16; ++c) Ls[i][c0 + c] = a[c];
-  if (live) {
-    float4* dst = reinterpret_cast<float4*>(L + (long long)(k + i) * ldL + k + c0);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (c0 + 4 * q <= i) dst[q] = make_float4(a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]);
-    }
+  for (int e = tid; e < NB * (NB / 4); e += 256) {
+    const int i = e / (NB / 4), c = 4 * (e % (NB / 4));
+    if (i < kb && c <= i)
+      *reinterpret_cast<float4*>(L + (long long)(k + i) * ldL + k + c) = *reinterpret_cast<const float4*>(&As[i * LDA + c]);
   }
-  __syncthreads();
 
-  // X = L^-1 row by row: X_j = (e_j - sum_{m<j} L_jm X_m) / L_jj, applied
-  // right-looking (once row j is final every later row subtracts L_ij X_j)
-  float xr[16];
+  // off-diagonal blocks of the inverse, distance d = i - j from the diagonal
+  for (int d = 1; d < NS; ++d) {
+    const int nx = (NS - d) * TPB * TPB;
+    f32x4 acc[UX];
 #pragma unroll
-  for (int c = 0; c < 16; ++c) xr[c] = (c0 + c == i) ? 1.f : 0.f;
-  for (int jb = 0; jb < NB / 16; ++jb) {
+    for (int u = 0; u < UX; ++u) {
+      const int t = w + 4 * u;
+      acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (t < nx) {
+        const int jb = t / (TPB * TPB), q = t % (TPB * TPB), ib = jb + d;
+        const int i0 = PB * ib + 16 * (q / TPB), j0 = PB * jb + 16 * (q % TPB);
+        // T = sum_{m=j}^{i-1} L_im X_mj
+        acc[u] = tile_nn(As, i0, PB * jb, Xs, PB * jb, j0, PB * d, lr, lq, acc[u]);
 #pragma unroll
-    for (int jc = 0; jc < 16; ++jc) {
-      const int j = 16 * jb + jc;
-      if (i == j) {
-        const float dj = dinv[j];
-#pragma unroll
-        for (int c = 0; c < 16; ++c) xr[c] *= dj;
-#pragma unroll
-        for (int c = 0; c < 16; c += 4)
-          *reinterpret_cast<float4*>(&rowb[j & 1][c0 + c]) = make_float4(xr[c], xr[c + 1], xr[c + 2], xr[c + 3]);
-      }
-      __syncthreads();
-      if (rlast > j && i > j) {
-        const float lij = Ls[i][j];
-#pragma unroll
-        for (int c = 0; c < 16; c += 4) {
-          const float4 v = *reinterpret_cast<const float4*>(&rowb[j & 1][c0 + c]);
-          xr[c] = fmaf(-lij, v.x, xr[c]);
-          xr[c + 1] = fmaf(-lij, v.y, xr[c + 1]);
-          xr[c + 2] = fmaf(-lij, v.z, xr[c + 2]);
-          xr[c + 3] = fmaf(-lij, v.w, xr[c + 3]);
-        }
+        for (int j = 0; j < 4; ++j) Xs[(i0 + 4 * lq + j) * LDA + j0 + lr] = acc[u][j];
       }
     }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < UX; ++u) {
+      const int t = w + 4 * u;
+      acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (t < nx) {
+        const int jb = t / (TPB * TPB), q = t % (TPB * TPB), ib = jb + d;
+        const int i0 = PB * ib + 16 * (q / TPB), j0 = PB * jb + 16 * (q % TPB);
+        acc[u] = tile_nn(Xs, i0, PB * ib, Xs, PB * ib, j0, PB, lr, lq, acc[u]);   // X_ii T
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < UX; ++u) {
+      const int t = w + 4 * u;
+      if (t < nx) {
+        const int jb = t / (TPB * TPB), q = t % (TPB * TPB), ib = jb + d;
+        const int i0 = PB * ib + 16 * (q / TPB), j0 = PB * jb + 16 * (q % TPB);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) Xs[(i0 + 4 * lq + j) * LDA + j0 + lr] = -acc[u][j];
+      }
+    }
+    __syncthreads();
   }
-  float4* drow = reinterpret_cast<float4*>(inv + (long long)i * NB + c0);
-#pragma unroll
-  for (int q = 0; q < 4; ++q) drow[q] = make_float4(xr[4 * q], xr[4 * q + 1], xr[4 * q + 2], xr[4 * q + 3]);
-#pragma unroll
-  for (int c = 0; c < 16; ++c) invT[(long long)(c0 + c) * NB + i] = xr[c];
+  for (int e = tid; e < NB * (NB / 4); e += 256) {
+    const int i = e / (NB / 4), c = 4 * (e % (NB / 4));
+    *reinterpret_cast<float4*>(inv + (long long)i * NB + c) = *reinterpret_cast<const float4*>(&Xs[i * LDA + c]);
+  }
+#pragma unroll 8
+  for (int e = tid; e < NB * NB; e += 256) {   // invT[c][i] = X[i][c], consecutive lanes along i
+    const int c = e / NB, i = e % NB;
+    invT[(long long)c * NB + i] = Xs[i * LDA + c];
+  }
 }
+constexpr int kPotrfPB = 16;
 
 // L21 = A21 L11^-T: rows k+128+64b .. +64, X[r][c] = sum_m A[r][m] Inv[c][m].
 // 16x16x4 fp32 MFMA; each lane reads a float4 along the reduction of both
@@ -333,16 +451,32 @@ __global__ __launch_bounds__(256) void lg_trsm_kernel(float* L, long long ldL, i
   __shared__ __attribute__((aligned(16))) float Bs[NB][LDP];
   const int tid = threadIdx.x;
   const int r0 = k + NB + 64 * blockIdx.x;
-  for (int t = tid; t < 64 * (NB / 4); t += 256) {
-    const int rr = t / (NB / 4), cq = t % (NB / 4);
-    const int row = r0 + rr;
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (row < n) v = *reinterpret_cast<const float4*>(L + (long long)row * ldL + k + 4 * cq);
-    *reinterpret_cast<float4*>(&As[rr][4 * cq]) = v;
-  }
-  for (int t = tid; t < NB * (NB / 4); t += 256) {
-    const int rr = t / (NB / 4), cq = t % (NB / 4);
-    *reinterpret_cast<float4*>(&Bs[rr][4 * cq]) = *reinterpret_cast<const float4*>(inv + (long long)rr * NB + 4 * cq);
+  {
+    // every load of the thread in flight before the LDS writes
+    constexpr int UA = 64 * (NB / 4) / 256, UB = NB * (NB / 4) / 256;
+    float4 va[UA], vb[UB];
+#pragma unroll
+    for (int u = 0; u < UA; ++u) {
+      const int t = tid + 256 * u, rr = t / (NB / 4), cq = t % (NB / 4);
+      const int row = r0 + rr;
+      va[u] = row < n ? *reinterpret_cast<const float4*>(L + (long long)row * ldL + k + 4 * cq)
+                      : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+      const int t = tid + 256 * u, rr = t / (NB / 4), cq = t % (NB / 4);
+      vb[u] = *reinterpret_cast<const float4*>(inv + (long long)rr * NB + 4 * cq);
+    }
+#pragma unroll
+    for (int u = 0; u < UA; ++u) {
+      const int t = tid + 256 * u;
+      *reinterpret_cast<float4*>(&As[t / (NB / 4)][4 * (t % (NB / 4))]) = va[u];
+    }
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+      const int t = tid + 256 * u;
+      *reinterpret_cast<float4*>(&Bs[t / (NB / 4)][4 * (t % (NB / 4))]) = vb[u];
+    }
   }
   __syncthreads();
   const int w = tid >> 6, lane = tid & 63, lr = lane & 15, lq = lane >> 4;
@@ -371,17 +505,10 @@ __global__ __launch_bounds__(256) void lg_trsm_kernel(float* L, long long ldL, i
   }
 }
 
-__device__ __forceinline__ void tile_pair(int q, int& I, int& J) {
-  int i = (int)((sqrtf(8.f * q + 1.f) - 1.f) * 0.5f);
-  while ((i + 1) * (i + 2) / 2 <= q) ++i;
-  while (i * (i + 1) / 2 > q) --i;
-  I = i;
-  J = q - i * (i + 1) / 2;
-}
 
 // A22 -= L21 L21^T on the lower-triangle 128x128 tiles of the trailing
-// matrix (rows and columns from k1 = k + 128).  The 128-column panel slices
-// of both tile rows stream through LDS in four 32-column chunks (buffer ->
+// matrix (rows and columns from k1 = k + W).  The W-column panel slices
+// of both tile rows stream through LDS in 32-column chunks (buffer ->
 // LDS DMA, double buffered, 32 KiB per chunk, so two workgroups share a
 // CU), in the conflict-free operand layout of the bf16 kernels (a 32-float
 // row is 8 segments of 4 floats).  The tile of A22 is read into registers
@@ -393,24 +520,28 @@ __device__ __forceinline__ void tile_pair(int q, int& I, int& J) {
 constexpr int SY_CH = 32;                 // panel columns per chunk
 constexpr int SY_PANEL = NB * SY_CH * 4;  // bytes of one tile row's chunk (16 KiB)
 
-// part: 0 = every lower-triangle tile, 1 = the first tile column only
-// (J = 0, which holds the next panel), 2 = every tile with J >= 1
-__global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL, int n, int k, int part,
+// W: panel width (the update has rank W: 128 for one panel, 256 for two).
+// head = true: the tiles of the first h (1 or 2) tile columns, column by
+// column (they hold the next panels); head = false: every tile with
+// I >= J >= h.
+template <int W>
+__global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL, int n, int k, int h, int head,
                                                          const LgCtl* ctl) {
   if (ctl->skip) return;
   __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * 2 * SY_PANEL];
+  constexpr int NCH = W / SY_CH;
+  const int k1 = k + W;
   int I, J;
-  if (part == 1) {
-    I = blockIdx.x;
-    J = 0;
+  if (head) {
+    const int T = (n - k1 + NB - 1) / NB;
+    const int q = blockIdx.x;
+    I = q < T ? q : q - T + 1;
+    J = q < T ? 0 : 1;
   } else {
     tile_pair(blockIdx.x, I, J);
-    if (part == 2) {
-      ++I;
-      ++J;
-    }
+    I += h;
+    J += h;
   }
-  const int k1 = k + NB;
   const int ri = k1 + NB * I, rj = k1 + NB * J;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -462,11 +593,11 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
     for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
   issue(0, 0);
 #pragma unroll
-  for (int ch = 0; ch < NB / SY_CH; ++ch) {
+  for (int ch = 0; ch < NCH; ++ch) {
     DR_WAIT_VM(0);
     DR_LDS_SYNC();
-    if (ch + 1 < NB / SY_CH) issue(ch + 1, (ch + 1) & 1);
-    if (ch == NB / SY_CH - 2 && active) load_c();
+    if (ch + 1 < NCH) issue(ch + 1, (ch + 1) & 1);
+    if (ch == NCH - 2 && active) load_c();
     if (active) {
       const unsigned char* sa = lds + (ch & 1) * 2 * SY_PANEL;
       const unsigned char* sbp = sa + SY_PANEL;
@@ -707,34 +838,47 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
     hipLaunchKernelGGL(lg_prep_kernel, dim3(pb), dim3(256), 0, hs, Kp, nn, vec, ctl);
     hipLaunchKernelGGL(lg_setup_kernel, dim3(1), dim3(1024), 0, hs, Kp, sp, n, lambda, mode, ctl, lam_eff + p);
     hipLaunchKernelGGL(lg_copy_kernel, dim3(n, (n + 1023) / 1024), dim3(256), 0, hs, Kp, n, L, ldL, ctl);
-    // Right-looking blocked factorisation with a one-panel look-ahead: the
-    // trailing update of panel b first refreshes the next panel's column of
-    // tiles, then, while it updates the rest, the aux stream factors the
-    // next diagonal block and solves the next panel (they touch only that
-    // column, which the rest of the update does not).
+    // Right-looking blocked factorisation by pairs of panels, with
+    // look-ahead.  The trailing matrix takes one rank-256 update per pair
+    // (half the passes over it of rank-128 updates).  For the pair (b, b+1)
+    // the aux stream factors panel b, applies it to panel b+1's column
+    // (rank 128), and factors panel b+1, while the main stream still runs
+    // the previous pair's update of the columns right of b+1; then the main
+    // stream updates the next pair's two columns (head) and, while the aux
+    // stream factors that pair, the rest.
     auto factor_panel = [&](int b, hipStream_t st) {
       const int k = NB * b;
       const int kb = n - k < NB ? n - k : NB;
       float* ib = inv + (long long)b * NB * NB;
       float* ibT = invT + (long long)b * NB * NB;
-      hipLaunchKernelGGL(lg_potrf_kernel, dim3(1), dim3(1024), 0, st, L, ldL, k, kb, ib, ibT, ctl);
+      hipLaunchKernelGGL(lg_potrf_kernel<kPotrfPB>, dim3(1), dim3(256), 0, st, L, ldL, k, kb, ib, ibT, ctl);
       const int rest = n - k - NB;
       if (rest > 0)
         hipLaunchKernelGGL(lg_trsm_kernel, dim3((rest + 63) / 64), dim3(256), 0, st, L, ldL, n, k, ib, ctl);
     };
-    factor_panel(0, hs);
-    for (int b = 0; b < nblk; ++b) {
+    if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;   // after the set-up kernels
+    for (int b = 0; b < nblk; b += 2) {
       const int k = NB * b;
-      const int rest = n - k - NB;
-      if (rest <= 0) break;
-      const int T = (rest + NB - 1) / NB;
-      hipLaunchKernelGGL(lg_syrk_kernel, dim3(T), dim3(256), 0, hs, L, ldL, n, k, 1, ctl);
-      if (hipEventRecord(ev_col, hs) != hipSuccess || hipStreamWaitEvent(aux, ev_col, 0) != hipSuccess)
+      if (hipStreamWaitEvent(aux, ev_col, 0) != hipSuccess) return DR_ERR_HIP;
+      factor_panel(b, aux);
+      const bool pair = b + 1 < nblk;
+      if (pair) {
+        const int T1 = (n - k - NB + NB - 1) / NB;
+        hipLaunchKernelGGL(lg_syrk_kernel<NB>, dim3(T1), dim3(256), 0, aux, L, ldL, n, k, 1, 1, ctl);
+        factor_panel(b + 1, aux);
+      }
+      if (hipEventRecord(ev_next, aux) != hipSuccess || hipStreamWaitEvent(hs, ev_next, 0) != hipSuccess)
         return DR_ERR_HIP;
-      factor_panel(b + 1, aux);
-      if (hipEventRecord(ev_next, aux) != hipSuccess) return DR_ERR_HIP;
-      if (T > 1) hipLaunchKernelGGL(lg_syrk_kernel, dim3(T * (T - 1) / 2), dim3(256), 0, hs, L, ldL, n, k, 2, ctl);
-      if (hipStreamWaitEvent(hs, ev_next, 0) != hipSuccess) return DR_ERR_HIP;
+      const int rest = n - k - 2 * NB;
+      if (!pair || rest <= 0) break;
+      const int T = (rest + NB - 1) / NB;
+      const int h = T < 2 ? T : 2;
+      const int nhead = h * T - h * (h - 1) / 2;
+      const int nrest = (T - h) * (T - h + 1) / 2;
+      hipLaunchKernelGGL(lg_syrk_kernel<2 * NB>, dim3(nhead), dim3(256), 0, hs, L, ldL, n, k, h, 1, ctl);
+      if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;
+      if (nrest > 0)
+        hipLaunchKernelGGL(lg_syrk_kernel<2 * NB>, dim3(nrest), dim3(256), 0, hs, L, ldL, n, k, h, 0, ctl);
     }
     for (int it = 0; it <= kRefine; ++it) {
       if (it > 0)
