@@ -6,9 +6,11 @@
 //
 // Workspace (one group at a time; groups run one after another):
 //   L     fp32 [n][ldL]   the factor (lower triangle; the rest is never read)
-//   inv   fp32 [nblk][128][128] and its transpose: the inverse of every
-//         128x128 diagonal block of L (used by the panel solve and by the
-//         two triangular solves)
+//   inv   fp32 [nblk][128][128]: the inverse of every 128x128 diagonal
+//         block of L (used by the panel solve)
+//   sinv  fp32 [nsb][1024][1024]: the inverse of every 1024x1024 diagonal
+//         super-block of L, lower blocks only (used by the two triangular
+//         solves; 64 MiB at n = 16384)
 //   x, dx, r, z  fp64 [npad] solution, correction, residual, work
 //   ctl   status shared by the kernels of one group (skip / info / lam_eff)
 //
@@ -30,11 +32,14 @@
 // solve, the rank-128 update of the pair's second column, its diagonal
 // block and panel), so those latency-bound steps run under the bulk of the
 // trailing update.
-// Solve: L y = r and L^T dx = y block by block (one launch per block and
-// direction; every workgroup applies the block's inverse, then updates its
-// share of the remaining right-hand side), x += dx; three solves (the
-// first and kRefine refinement steps), each refinement preceded by
-// r = s - (K + lam_eff I) x in fp64 read straight from K.
+// Solve: the super-block inverses are built block by block from the
+// 128x128 ones (lg_sinv_kernel, one launch per distance from the
+// diagonal); then L y = r and L^T dx = y go super-block by super-block,
+// two wide launches each (the super-block's share of the solution as a
+// product with its inverse, then its update of the rest of the right-hand
+// side), x += dx; three solves (the first and kRefine refinement steps),
+// each refinement preceded by r = s - (K + lam_eff I) x in fp64 read
+// straight from K.
 // Every kernel first reads ctl->skip: once a group's result is decided (a
 // non-finite input, an empty span, a non-positive pivot) the remaining
 // launches of that group return at once.
@@ -45,6 +50,8 @@ namespace dr {
 namespace {
 
 constexpr int NB = 128;        // panel width
+constexpr int SB = 8;          // 128-blocks per super-block of the triangular solves
+constexpr int SBN = SB * NB;   // rows of a super-block (leading dimension of its inverse)
 constexpr int LDP = NB + 4;    // LDS row stride (floats) of staged slices: b128 reads are conflict-free
 constexpr int kRefine = 2;
 constexpr int kPrepBlocks = 2048;
@@ -58,7 +65,7 @@ struct LgCtl {
 
 struct LgLayout {
   long long n, ldL, nblk, npad;
-  size_t off_L, off_inv, off_invT, off_x, off_dx, off_r, off_z, off_ctl, total;
+  size_t off_L, off_inv, off_sinv, off_x, off_dx, off_r, off_z, off_ctl, total;
 };
 
 LgLayout lg_layout(long long n) {
@@ -70,7 +77,7 @@ LgLayout lg_layout(long long n) {
   size_t o = 0;
   l.off_L = o;    o = align_up(o + (size_t)n * l.ldL * 4, 256);
   l.off_inv = o;  o = align_up(o + (size_t)l.nblk * NB * NB * 4, 256);
-  l.off_invT = o; o = align_up(o + (size_t)l.nblk * NB * NB * 4, 256);
+  l.off_sinv = o; o = align_up(o + (size_t)((l.nblk + SB - 1) / SB) * SBN * SBN * 4, 256);
   l.off_x = o;    o = align_up(o + (size_t)l.npad * 8, 256);
   l.off_dx = o;   o = align_up(o + (size_t)l.npad * 8, 256);
   l.off_r = o;    o = align_up(o + (size_t)l.npad * 8, 256);
@@ -290,7 +297,7 @@ __device__ __forceinline__ f32x4 tile_nn(const float* A, int ra, int ca, const f
 
 template <int PB>
 __global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, int k, int kb, float* inv,
-                                                       float* invT, LgCtl* ctl) {
+                                                       LgCtl* ctl) {
   if (ctl->skip) return;
   constexpr int NS = NB / PB;            // sub-blocks
   constexpr int TPB = PB / 16;           // 16-wide tiles per sub-block edge
@@ -431,11 +438,6 @@ __global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, 
   for (int e = tid; e < NB * (NB / 4); e += 256) {
     const int i = e / (NB / 4), c = 4 * (e % (NB / 4));
     *reinterpret_cast<float4*>(inv + (long long)i * NB + c) = *reinterpret_cast<const float4*>(&Xs[i * LDA + c]);
-  }
-#pragma unroll 8
-  for (int e = tid; e < NB * NB; e += 256) {   // invT[c][i] = X[i][c], consecutive lanes along i
-    const int c = e / NB, i = e % NB;
-    invT[(long long)c * NB + i] = Xs[i * LDA + c];
   }
 }
 constexpr int kPotrfPB = 16;
@@ -633,98 +635,175 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
 
 // ---------------------------------------------------------------- solves
 
-// y_c = sum_m M[m][c] v_m for a 128x128 block M staged in LDS (row-major,
-// thread pairs split m); every thread of the workgroup takes part, the
-// result lands in out[] (LDS).  M is lower- or upper-triangular with zeros
-// elsewhere, so the sum runs over all m.
-__device__ __forceinline__ void block_matvec_T(const float* Ms, const double* v, double* part, double* out) {
-  const int tid = threadIdx.x;
-  const int c = tid & (NB - 1), h = tid >> 7;
-  double a0 = 0.0, a1 = 0.0;
-#pragma unroll 8
-  for (int m = 64 * h; m < 64 * h + 64; m += 2) {
-    a0 += (double)Ms[m * NB + c] * v[m];
-    a1 += (double)Ms[(m + 1) * NB + c] * v[m + 1];
-  }
-  if (h == 1) part[c] = a0 + a1;
-  __syncthreads();
-  if (h == 0) out[c] = (a0 + a1) + part[c];
-  __syncthreads();
-}
+// Triangular solves by super-blocks of SB diagonal blocks (1024 rows).
+// After the factorisation, the inverse of every 1024 x 1024 diagonal
+// super-block of L is formed (lower triangle, from the 128 x 128 block
+// inverses); a solve then takes two wide launches per super-block: the
+// super-block's part of the solution as one product with its inverse, and
+// its contribution to the rest of the right-hand side.
 
-// stage a 128x128 fp32 block (row stride ld floats) into LDS: 16 float4 per thread, all in flight
-__device__ __forceinline__ void stage_block(float* dst, const float* src, long long ld, int rows_valid) {
-  const int tid = threadIdx.x;
-  float4 v[16];
-#pragma unroll
-  for (int u = 0; u < 16; ++u) {
-    const int e = tid + 256 * u;   // float4 index: row e / 32, column 4 (e % 32)
-    const int r = e >> 5, c4 = e & 31;
-    v[u] = r < rows_valid ? *reinterpret_cast<const float4*>(src + (long long)r * ld + 4 * c4)
-                          : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
-#pragma unroll
-  for (int u = 0; u < 16; ++u) reinterpret_cast<float4*>(dst)[tid + 256 * u] = v[u];
-}
-
-// Forward step for block b of L y = r: y_b = Inv_b r_b (every workgroup
-// forms it from the staged inverse; workgroup 0 stores it in y), then
-// r_i -= L[i, block b] . y_b for this workgroup's 128 rows of the trailing
-// part (32 lanes per row; the row loads are issued first).
-__global__ __launch_bounds__(256) void lg_fwd_kernel(const float* L, long long ldL, int n, int b, const float* invT,
-                                                     double* r, double* y, const LgCtl* ctl) {
+// Block (i, j) = (j + d, j) of the inverse X of super-block S, d >= 1:
+//   X_ij = -X_ii sum_{m=j}^{i-1} L_im X_mj
+// (d = 0 copies the 128 x 128 block inverses onto the diagonal).  One
+// workgroup per block; the 128 x 128 operands are staged in LDS and wave w
+// computes rows 32 w .. 32 w + 31 with fp32 MFMA.
+__global__ __launch_bounds__(256) void lg_sinv_kernel(const float* L, long long ldL, int n, int nblk,
+                                                      const float* inv, float* sinv, int d, const LgCtl* ctl) {
   if (ctl->skip) return;
-  __shared__ __attribute__((aligned(16))) float Ms[NB * NB];
-  __shared__ double rb[NB], yb[NB], part[NB];
+  const int S = blockIdx.y, jj = blockIdx.x, ii = jj + d;
+  const int bj = SB * S + jj, bi = bj + d;
+  if (ii >= SB || bi >= nblk) return;
+  float* X = sinv + (long long)S * SBN * SBN;   // [SBN][SBN]
   const int tid = threadIdx.x;
-  const int o = NB * b;
-  const int g = tid >> 5, l32 = tid & 31;   // 8 rows at a time, 32 lanes each
-  const int base = o + NB + NB * blockIdx.x;
-  float4 v[NB / 8];
-#pragma unroll
-  for (int t = 0; t < NB / 8; ++t) {
-    const int row = base + g + 8 * t;
-    v[t] = row < n ? *reinterpret_cast<const float4*>(L + (long long)row * ldL + o + 4 * l32)
-                   : make_float4(0.f, 0.f, 0.f, 0.f);
+  if (d == 0) {
+    for (int e = tid; e < NB * NB / 4; e += 256) {
+      const int r = e / (NB / 4), c = 4 * (e % (NB / 4));
+      *reinterpret_cast<float4*>(X + (long long)(NB * ii + r) * SBN + NB * ii + c) =
+          *reinterpret_cast<const float4*>(inv + (long long)bi * NB * NB + r * NB + c);
+    }
+    return;
   }
-  stage_block(Ms, invT, NB, NB);   // invT[m][c] = Inv_b[c][m]
-  if (tid < NB) rb[tid] = r[o + tid];
-  __syncthreads();
-  block_matvec_T(Ms, rb, part, yb);
-  if (blockIdx.x == 0 && tid < NB) y[o + tid] = yb[tid];
-  const double y0 = yb[4 * l32], y1 = yb[4 * l32 + 1], y2 = yb[4 * l32 + 2], y3 = yb[4 * l32 + 3];
+  __shared__ __attribute__((aligned(16))) float As[NB * LDA];
+  __shared__ __attribute__((aligned(16))) float Bs[NB * LDA];
+  const int lane = tid & 63, w = tid >> 6, lr = lane & 15, lq = lane >> 4;
+  // stage a 128 x 128 block (row stride ld, rows >= rows_valid read as 0)
+  auto stage = [&](float* dst, const float* src, long long ld, int rows_valid) {
+    float4 v[16];
 #pragma unroll
-  for (int t = 0; t < NB / 8; ++t) {
-    const int row = base + g + 8 * t;
-    double acc = (double)v[t].x * y0 + (double)v[t].y * y1 + (double)v[t].z * y2 + (double)v[t].w * y3;
-    for (int off = 16; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 32);
-    if (l32 == 0 && row < n) r[row] -= acc;
+    for (int u = 0; u < 16; ++u) {
+      const int e = tid + 256 * u, r = e / (NB / 4), c = 4 * (e % (NB / 4));
+      v[u] = r < rows_valid ? *reinterpret_cast<const float4*>(src + (long long)r * ld + c)
+                            : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int e = tid + 256 * u, r = e / (NB / 4), c = 4 * (e % (NB / 4));
+      *reinterpret_cast<float4*>(&dst[r * LDA + c]) = v[u];
+    }
+  };
+  f32x4 acc[2][8];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[a][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int rows_i = n - NB * bi < NB ? n - NB * bi : NB;   // rows of L that exist in block row bi
+  for (int m = bj; m < bi; ++m) {
+    stage(As, L + (long long)NB * bi * ldL + NB * m, ldL, rows_i);                       // L_im
+    stage(Bs, X + (long long)(NB * (m - SB * S)) * SBN + NB * jj, SBN, NB);            // X_mj
+    __syncthreads();
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) acc[a][c] = tile_nn(As, 32 * w + 16 * a, 0, Bs, 0, 16 * c, NB, lr, lq, acc[a][c]);
+    __syncthreads();
+  }
+  // T into Bs, X_ii into As, then X_ij = -X_ii T
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) Bs[(32 * w + 16 * a + 4 * lq + q) * LDA + 16 * c + lr] = acc[a][c][q];
+  stage(As, X + (long long)(NB * ii) * SBN + NB * ii, SBN, NB);
+  __syncthreads();
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const f32x4 p = tile_nn(As, 32 * w + 16 * a, 0, Bs, 0, 16 * c, NB, lr, lq, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        X[(long long)(NB * ii + 32 * w + 16 * a + 4 * lq + q) * SBN + NB * jj + 16 * c + lr] = -p[q];
+    }
+}
+
+// out[i] = (or -=) sum_c M[i][c] v_c for rows i < rows, columns c < width
+// (<= SBN); lower != 0 limits row i to the 128-blocks on or left of its own
+// (a lower-triangular block matrix whose upper blocks are never read).  32
+// rows per workgroup, 8 per wave, all their loads in flight; lane l takes
+// columns 4 l + 256 t.
+__global__ __launch_bounds__(256) void lg_rowdot_kernel(const float* M, long long ldM, int rows, int width, int lower,
+                                                        const double* v, double* out, int sub, const LgCtl* ctl) {
+  if (ctl->skip) return;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int row0 = 32 * blockIdx.x + 8 * w;
+  double vv[SB / 2][4];
+#pragma unroll
+  for (int t = 0; t < SB / 2; ++t) {
+    const int c = 4 * lane + 256 * t;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) vv[t][q] = c < width ? v[c + q] : 0.0;
+  }
+  float4 mv[8][SB / 2];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const int row = row0 + u;
+    const int lim = lower ? min(width, NB * (row / NB + 1)) : width;
+#pragma unroll
+    for (int t = 0; t < SB / 2; ++t) {
+      const int c = 4 * lane + 256 * t;
+      mv[u][t] = (row < rows && c < lim) ? *reinterpret_cast<const float4*>(M + (long long)row * ldM + c)
+                                         : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    double acc = 0.0;
+#pragma unroll
+    for (int t = 0; t < SB / 2; ++t)
+      acc += (double)mv[u][t].x * vv[t][0] + (double)mv[u][t].y * vv[t][1] + (double)mv[u][t].z * vv[t][2] +
+             (double)mv[u][t].w * vv[t][3];
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    const int row = row0 + u;
+    if (lane == 0 && row < rows) out[row] = sub ? out[row] - acc : acc;
   }
 }
 
-// Backward step for block b of L^T x = y: x_b = Inv_b^T y_b (every
-// workgroup forms it; workgroup 0 stores it), then y_m -= sum_{i in block b}
-// L[i][m] x_i for this workgroup's 128 columns m < 128 b, with the 128x128
-// block of L staged in LDS.
-__global__ __launch_bounds__(256) void lg_bwd_kernel(const float* L, long long ldL, int n, int b, const float* inv,
-                                                     double* y, double* x, const LgCtl* ctl) {
+// out[c] = (or -=) sum_i M[i][c] v_i for columns c < 64 * gridDim.x and rows
+// i < rows (<= SBN); lower != 0 starts at the 128-block row of the column's
+// own block (a lower-triangular block matrix).  64 columns per workgroup:
+// lane l of wave w reads a float4 of columns 4 (l % 16) in row stream
+// 4 w + l / 16, streams take every 16th row (a wave load covers 4 rows x
+// 256 bytes); the 16 stream sums of a column are added in a fixed order.
+__global__ __launch_bounds__(256) void lg_coldot_kernel(const float* M, long long ldM, int rows, int lower,
+                                                        const double* v, double* out, int sub, const LgCtl* ctl) {
   if (ctl->skip) return;
-  __shared__ __attribute__((aligned(16))) float Ms[NB * NB];
-  __shared__ double zb[NB], xb[NB], part[NB], sums[NB];
-  const int tid = threadIdx.x;
-  const int o = NB * b;
-  const int rows = n - o < NB ? n - o : NB;
-  stage_block(Ms, inv, NB, NB);    // inv[m][c] = Inv_b[m][c]: x_c = sum_m inv[m][c] y_m
-  if (tid < NB) zb[tid] = y[o + tid];
+  __shared__ double vs[SBN], part[16][64];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  for (int i = tid; i < rows; i += 256) vs[i] = v[i];
   __syncthreads();
-  block_matvec_T(Ms, zb, part, xb);
-  if (blockIdx.x == 0 && tid < NB) x[o + tid] = xb[tid];
-  const int m0 = NB * blockIdx.x;
-  if (m0 >= o) return;   // (uniform) block 0 has no columns to the left
-  stage_block(Ms, L + (long long)o * ldL + m0, ldL, rows);   // rows o .. o + rows, columns m0 .. m0 + 128
+  const int m0 = 64 * blockIdx.x, c4 = lane & 15, st = 4 * w + (lane >> 4);
+  const int i_start = lower ? NB * (m0 / NB) : 0;
+  const float* col = M + m0 + 4 * c4;
+  double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+  for (int i0 = i_start + st; i0 < rows; i0 += 16 * 8) {
+    float4 mv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + 16 * u;
+      mv[u] = i < rows ? *reinterpret_cast<const float4*>(col + (long long)i * ldM) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + 16 * u;
+      const double vi = i < rows ? vs[i] : 0.0;
+      a0 += (double)mv[u].x * vi;
+      a1 += (double)mv[u].y * vi;
+      a2 += (double)mv[u].z * vi;
+      a3 += (double)mv[u].w * vi;
+    }
+  }
+  part[st][4 * c4] = a0;
+  part[st][4 * c4 + 1] = a1;
+  part[st][4 * c4 + 2] = a2;
+  part[st][4 * c4 + 3] = a3;
   __syncthreads();
-  block_matvec_T(Ms, xb, part, sums);   // sums_c = sum_i L[o + i][m0 + c] x_i
-  if (tid < NB) y[m0 + tid] -= sums[tid];
+  if (tid < 64) {
+    double t = 0.0;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) t += part[q][tid];
+    out[m0 + tid] = sub ? out[m0 + tid] - t : t;
+  }
 }
 
 __global__ void lg_axpy_kernel(double* x, const double* dx, int npad, const LgCtl* ctl) {
@@ -819,7 +898,7 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
                                    hipEvent_t ev_col, hipEvent_t ev_next) {
   float* L = reinterpret_cast<float*>(base + lay.off_L);
   float* inv = reinterpret_cast<float*>(base + lay.off_inv);
-  float* invT = reinterpret_cast<float*>(base + lay.off_invT);
+  float* sinv = reinterpret_cast<float*>(base + lay.off_sinv);
   double* x = reinterpret_cast<double*>(base + lay.off_x);
   double* dx = reinterpret_cast<double*>(base + lay.off_dx);
   double* r = reinterpret_cast<double*>(base + lay.off_r);
@@ -850,8 +929,7 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       const int k = NB * b;
       const int kb = n - k < NB ? n - k : NB;
       float* ib = inv + (long long)b * NB * NB;
-      float* ibT = invT + (long long)b * NB * NB;
-      hipLaunchKernelGGL(lg_potrf_kernel<kPotrfPB>, dim3(1), dim3(256), 0, st, L, ldL, k, kb, ib, ibT, ctl);
+      hipLaunchKernelGGL(lg_potrf_kernel<kPotrfPB>, dim3(1), dim3(256), 0, st, L, ldL, k, kb, ib, ctl);
       const int rest = n - k - NB;
       if (rest > 0)
         hipLaunchKernelGGL(lg_trsm_kernel, dim3((rest + 63) / 64), dim3(256), 0, st, L, ldL, n, k, ib, ctl);
@@ -880,21 +958,34 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       if (nrest > 0)
         hipLaunchKernelGGL(lg_syrk_kernel<2 * NB>, dim3(nrest), dim3(256), 0, hs, L, ldL, n, k, h, 0, ctl);
     }
+    const int nsb = (nblk + SB - 1) / SB;
+    for (int d = 0; d < SB; ++d)
+      hipLaunchKernelGGL(lg_sinv_kernel, dim3(SB - d, nsb), dim3(256), 0, hs, L, ldL, n, nblk, inv, sinv, d, ctl);
     for (int it = 0; it <= kRefine; ++it) {
       if (it > 0)
         hipLaunchKernelGGL(lg_resid_kernel, dim3((n + 3) / 4), dim3(256), 0, hs, Kp, n, sp, x, r, (double*)nullptr,
                            ctl);
-      // L z = r (r is consumed), then L^T dx = z (z is consumed)
-      for (int b = 0; b < nblk; ++b) {
-        const int rest = n - NB * (b + 1);
-        const int g = rest > 0 ? (rest + NB - 1) / NB : 1;
-        hipLaunchKernelGGL(lg_fwd_kernel, dim3(g), dim3(256), 0, hs, L, ldL, n, b, invT + (long long)b * NB * NB, r,
-                           z, ctl);
+      // L z = r (r is consumed), then L^T dx = z (z is consumed), by super-blocks
+      for (int S = 0; S < nsb; ++S) {
+        const int o0 = SBN * S, nb = nblk - SB * S < SB ? nblk - SB * S : SB, width = NB * nb;
+        const float* Xs = sinv + (long long)S * SBN * SBN;
+        hipLaunchKernelGGL(lg_rowdot_kernel, dim3((width + 31) / 32), dim3(256), 0, hs, Xs, (long long)SBN, width,
+                           width, 1, r + o0, z + o0, 0, ctl);
+        const int below = n - o0 - width;
+        if (below > 0)
+          hipLaunchKernelGGL(lg_rowdot_kernel, dim3((below + 31) / 32), dim3(256), 0, hs,
+                             L + (long long)(o0 + width) * ldL + o0, ldL, below, width, 0, z + o0, r + o0 + width, 1,
+                             ctl);
       }
-      for (int b = nblk - 1; b >= 0; --b) {
-        const int g = b > 0 ? b : 1;
-        hipLaunchKernelGGL(lg_bwd_kernel, dim3(g), dim3(256), 0, hs, L, ldL, n, b, inv + (long long)b * NB * NB, z,
-                           dx, ctl);
+      for (int S = nsb - 1; S >= 0; --S) {
+        const int o0 = SBN * S, nb = nblk - SB * S < SB ? nblk - SB * S : SB, width = NB * nb;
+        const float* Xs = sinv + (long long)S * SBN * SBN;
+        hipLaunchKernelGGL(lg_coldot_kernel, dim3(width / 64), dim3(256), 0, hs, Xs, (long long)SBN, width, 1, z + o0,
+                           dx + o0, 0, ctl);
+        const int rows = n - o0 < width ? n - o0 : width;
+        if (o0 > 0)
+          hipLaunchKernelGGL(lg_coldot_kernel, dim3(o0 / 64), dim3(256), 0, hs, L + (long long)o0 * ldL, ldL, rows, 0,
+                             dx + o0, z, 1, ctl);
       }
       hipLaunchKernelGGL(lg_axpy_kernel, dim3((npad + 255) / 256), dim3(256), 0, hs, x, dx, npad, ctl);
     }
