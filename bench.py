@@ -37,11 +37,17 @@ def parse():
     ap.add_argument("--groups", choices=["global", "layer"], default="global",
                     help="one group over all sketch columns (default), or one group per layer (P = 8)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle's sketch sample")
+    ap.add_argument("--no-gram-dominated", action="store_true",
+                    help="skip the Gram-dominated stage timings (16384 x 8192 Gram, span, top-1024)")
+    ap.add_argument("--gram-dominated-only", action="store_true",
+                    help="time only the Gram-dominated stages and print their JSON object (for profiling)")
     ap.add_argument("--no-next-rows", action="store_true",
                     help="skip the separately timed widening rows (update, scorers, selection rules, simplex, "
                          "back-projection)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run three 1 GiB device-to-device copies first (known bytes, to scale HBM counters)")
+    ap.add_argument("--summarize-gram-profile", metavar="KT_DIR",
+                    help="write the Gram-dominated kernel-trace summary under profiles/ from rocprofv3 csv output")
     ap.add_argument("--summarize-profiles", nargs=3, metavar=("KT_DIR", "FETCH_DIR", "WRITE_DIR"),
                     help="write the profiles/ summaries from the csv output of a rocprofv3 kernel-trace run "
                          "and the FETCH_SIZE / WRITE_SIZE counter runs of this script (no GPU needed)")
@@ -52,6 +58,9 @@ def main():
     args = parse()
     if args.summarize_profiles:
         summarize_profiles(*args.summarize_profiles)
+        return
+    if args.summarize_gram_profile:
+        summarize_gram_profile(args.summarize_gram_profile)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
@@ -66,6 +75,9 @@ def main():
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.gram_dominated_only:
+        print(json.dumps(time_gram_dominated(api, _lib, workloads, dev)), flush=True)
+        return
     cfg = workloads.CONFIGS["small"]
     n, m, T = cfg["n"], cfg["m"], cfg["T"]
     N = n + m
@@ -219,6 +231,8 @@ def main():
 
     if not args.no_next_rows:
         out["next_rows"] = time_next_rows(api, layers, lens, n, T, wt, wc, goff, dev, K=K, s=s)
+    if not args.no_gram_dominated:
+        out["gram_dominated"] = time_gram_dominated(api, _lib, workloads, dev)
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layers, lens, S, K, s, t2, n, m, k_top, lam, cfg, args.cpu_seconds, goff)
@@ -330,13 +344,65 @@ def time_next_rows(api, layers, lens, n, T, wt, wc, goff, dev, K=None, s=None, r
     return res
 
 
+def time_gram_dominated(api, _lib, workloads, dev, reps=3):
+    """The Gram-dominated workload's projection step, stage by stage: the
+    16384 x 16384 Gram of 16384 bf16 rows of dimension 8192 (+ 32 target
+    rows: scores and the target's squared norm), the ridge span at n = 16384
+    (blocked Cholesky + refinement) and top-1024.  The Gram is the one stage
+    of the path whose algorithmic work can reach the bf16 MFMA roofline:
+    n (n + 1) / 2 entries of K and n scores, kappa MACs (2 FLOP) each."""
+    import torch
+    cfg = workloads.CONFIGS["gram"]
+    rows = workloads.gram_rows(cfg, dev)
+    n, kappa = cfg["n"], rows.shape[1]
+    G, Gt = rows[:n], rows[n:]
+    K = torch.empty(1, n, n, device=dev)
+    s = torch.empty(1, n, device=dev)
+    t2 = torch.empty(1, device=dev)
+    gws = torch.empty(max(1, api.dr_gram_workspace_size(n, Gt.shape[0], [0, kappa], torch.bfloat16)),
+                      dtype=torch.uint8, device=dev)
+    w = torch.empty(1, n, device=dev)
+    le = torch.empty(1, device=dev)
+    r2 = torch.empty(1, device=dev)
+    info = torch.empty(1, dtype=torch.int32, device=dev)
+    sws = torch.empty(api.dr_span_workspace_size(n, 1), dtype=torch.uint8, device=dev)
+    k = cfg["topk"]
+    idx = torch.empty(1, k, dtype=torch.int32, device=dev)
+    wt = torch.empty(1, n, device=dev)
+    it = torch.empty(1, dtype=torch.int32, device=dev)
+    gram_ms = _event_ms(lambda: api.dr_gram(G, Gt, [0, kappa], K, s, t2, workspace=gws), reps)
+    span_ms = _event_ms(lambda: api.dr_project_span(K, s, t2, cfg["lam"], _lib.DR_RIDGE_REL_TRACE, w, le, r2, info,
+                                                     workspace=sws), reps)
+    topk_ms = _event_ms(lambda: api.dr_select_topk(s, k, idx, wt, it), 10 * reps)
+    if int(info[0]) != 0 or int(it[0]) != 0:
+        raise RuntimeError("Gram-dominated projection reported a non-zero info code")
+    flops = float(n) * (n + 1) * kappa + 2.0 * n * kappa   # lower triangle of K, then the scores
+    tf = flops / (gram_ms * 1e-3) / 1e12
+    del K, sws, rows
+    torch.cuda.empty_cache()
+    return {
+        "workload": "Gram-dominated: 16384 general + 32 target pre-sketched bf16 rows of dimension 8192 "
+                    "(N(0,1) plus a rank-32 component of scale 3), ridge span lambda = 1e-2 relative, top-1024",
+        "gram_ms": gram_ms, "span_ms": span_ms, "topk_ms": topk_ms,
+        "projection_steps_per_s": 1e3 / (gram_ms + span_ms + topk_ms),
+        "gram_roofline": {"kernel": "dr_gram (gram_big_kernel + gram_mirror_kernel + target mean + scores)",
+                          "bound": "mfma", "achieved": tf, "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                          "frac": tf / BF16_MFMA_PEAK_TFLOPS, "algorithmic_flops": flops},
+        "span_fp32_factor_tflops": (n ** 3 / 3.0) / (span_ms * 1e-3) / 1e12,
+    }
+
+
 SKETCH_SOURCES = ["paper_2605_07063_amd/csrc/sketch.hip", "paper_2605_07063_amd/csrc/common.h"]
 SKETCH_KERNELS = ("sketch_plan_kernel", "sketch_packed_kernel", "sketch_packed_reduce_kernel")
 KT_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_kt -o small -- "
           "python -u bench.py --steps 50 --warmup 10 --no-cpu-baseline")
 PMC_CMD = ("rocprofv3 --pmc {c} --output-format csv -d gpurun_out/prof_{d} -o small -- "
-           "python -u bench.py --steps 5 --warmup 2 --no-cpu-baseline --no-next-rows --copy-calibration")
+           "python -u bench.py --steps 5 --warmup 2 --no-cpu-baseline --no-next-rows --no-gram-dominated "
+           "--copy-calibration")
 SUM_CMD = "python bench.py --summarize-profiles gpurun_out/prof_kt gpurun_out/prof_fetch gpurun_out/prof_write"
+GD_KT_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_gd -o gd -- "
+             "python -u bench.py --gram-dominated-only")
+GD_SUM_CMD = "python bench.py --summarize-gram-profile gpurun_out/prof_gd"
 
 
 def sketch_sources_sha():
@@ -370,6 +436,48 @@ def _short_name(name):
     return n.split("(")[0].strip()
 
 
+def _kernel_rows(stats_csv):
+    """Markdown rows (name, calls, avg / min / max us, share) of a rocprofv3
+    kernel_stats.csv, and the average duration of each kernel."""
+    import csv
+    stats = list(csv.DictReader(open(stats_csv)))
+    tot = sum(float(r["TotalDurationNs"]) for r in stats)
+    rows, avg = [], {}
+    for r in stats:
+        nm = _short_name(r["Name"])
+        if nm.startswith("Cijk_"):
+            nm = "hipBLASLt GEMM " + nm[:24] + "..."
+        ours = not r["Name"].startswith(("void at::", "at::", "__amd", "Cijk_"))
+        avg[nm] = avg.get(nm, 0.0) + float(r["AverageNs"]) / 1e3
+        rows.append(f"| `{nm}`{'' if ours else ' (input generation, untimed)'} | {int(r['Calls'])} | "
+                    f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+                    f"{float(r['MaxNs']) / 1e3:.2f} | {100 * float(r['TotalDurationNs']) / tot:.1f}% |")
+    return rows, avg
+
+
+def summarize_gram_profile(kt_dir):
+    """profiles/gram_dominated_kernel_trace.md from the rocprofv3 kernel
+    trace of `bench.py --gram-dominated-only`."""
+    import glob
+    f = sorted(glob.glob(os.path.join(kt_dir, "**", "*_kernel_stats.csv"), recursive=True))
+    if not f:
+        raise SystemExit(f"no kernel_stats.csv under {kt_dir}")
+    rows, avg = _kernel_rows(f[0])
+    gram = sum(v for k, v in avg.items() if k.startswith(("gram_big_kernel", "gram_mirror_kernel", "score_kernel",
+                                                           "target_mean_kernel")))
+    kt = ["# Kernel trace: Gram-dominated workload (Gram, span, top-1024)", "",
+          "Command (repository root on the GPU box, `TMPDIR=/tmp`), summarised by", "",
+          "```", GD_KT_CMD, GD_SUM_CMD, "```", "",
+          "`bench.py --gram-dominated-only` times each stage once untimed and 3 times timed (top-k 30 times): "
+          "4 `dr_gram` calls (16416 x 8192 bf16 rows) and 4 `dr_project_span` calls at n = 16384. "
+          "Durations in microseconds. The span's kernels run on two streams (the diagonal-block chain "
+          "overlaps the trailing updates), so their durations add up to more than the call's wall time.", "",
+          "| Kernel | Calls | Avg (us) | Min | Max | Share |", "|---|---|---|---|---|---|"] + rows + [
+          "", f"One `dr_gram` call = gram_big_kernel + gram_mirror_kernel + target_mean_kernel + score_kernel = "
+          f"**{gram:.1f} us** (average kernel durations)."]
+    open(os.path.join(ROOT, "profiles", "gram_dominated_kernel_trace.md"), "w").write("\n".join(kt) + "\n")
+
+
 def summarize_profiles(kt_dir, fetch_dir, write_dir):
     """profiles/ summaries (kernel trace, HBM traffic, the traffic record
     bench.py reads) from rocprofv3 csv output of this script's commands."""
@@ -382,17 +490,8 @@ def summarize_profiles(kt_dir, fetch_dir, write_dir):
             raise SystemExit(f"no {pattern} under {d}")
         return f[0]
 
-    stats = list(csv.DictReader(open(one("*_kernel_stats.csv", kt_dir))))
-    tot = sum(float(r["TotalDurationNs"]) for r in stats)
-    rows, sk_avg = [], 0.0
-    for r in stats:
-        nm = _short_name(r["Name"])
-        ours = not r["Name"].startswith(("void at::", "at::", "__amd"))
-        if nm.startswith(SKETCH_KERNELS):
-            sk_avg += float(r["AverageNs"]) / 1e3
-        rows.append(f"| `{nm}`{'' if ours else ' (input generation, untimed)'} | {int(r['Calls'])} | "
-                    f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
-                    f"{float(r['MaxNs']) / 1e3:.2f} | {100 * float(r['TotalDurationNs']) / tot:.1f}% |")
+    rows, avg = _kernel_rows(one("*_kernel_stats.csv", kt_dir))
+    sk_avg = sum(v for k, v in avg.items() if k.startswith(SKETCH_KERNELS))
     kt = ["# Kernel trace: small-block workload, bench step", "",
           "Command (repository root on the GPU box, `TMPDIR=/tmp`), summarised by", "",
           "```", KT_CMD, SUM_CMD, "```", "",
