@@ -385,7 +385,7 @@ def time_gram_dominated(api, _lib, workloads, dev, reps=3):
                     "(N(0,1) plus a rank-32 component of scale 3), ridge span lambda = 1e-2 relative, top-1024",
         "gram_ms": gram_ms, "span_ms": span_ms, "topk_ms": topk_ms,
         "projection_steps_per_s": 1e3 / (gram_ms + span_ms + topk_ms),
-        "gram_roofline": {"kernel": "dr_gram (gram_big_kernel + gram_mirror_kernel + target mean + scores)",
+        "gram_roofline": {"kernel": "dr_gram (gram_big_kernel + target mean + scores)",
                           "bound": "mfma", "achieved": tf, "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                           "frac": tf / BF16_MFMA_PEAK_TFLOPS, "algorithmic_flops": flops},
         "span_fp32_factor_tflops": (n ** 3 / 3.0) / (span_ms * 1e-3) / 1e12,
@@ -463,8 +463,7 @@ def summarize_gram_profile(kt_dir):
     if not f:
         raise SystemExit(f"no kernel_stats.csv under {kt_dir}")
     rows, avg = _kernel_rows(f[0])
-    gram = sum(v for k, v in avg.items() if k.startswith(("gram_big_kernel", "gram_mirror_kernel", "score_kernel",
-                                                           "target_mean_kernel")))
+    gram = sum(v for k, v in avg.items() if k.startswith(("gram_big_kernel", "score_kernel", "target_mean_kernel")))
     kt = ["# Kernel trace: Gram-dominated workload (Gram, span, top-1024)", "",
           "Command (repository root on the GPU box, `TMPDIR=/tmp`), summarised by", "",
           "```", GD_KT_CMD, GD_SUM_CMD, "```", "",
@@ -473,7 +472,7 @@ def summarize_gram_profile(kt_dir):
           "Durations in microseconds. The span's kernels run on two streams (the diagonal-block chain "
           "overlaps the trailing updates), so their durations add up to more than the call's wall time.", "",
           "| Kernel | Calls | Avg (us) | Min | Max | Share |", "|---|---|---|---|---|---|"] + rows + [
-          "", f"One `dr_gram` call = gram_big_kernel + gram_mirror_kernel + target_mean_kernel + score_kernel = "
+          "", f"One `dr_gram` call = gram_big_kernel + target_mean_kernel + score_kernel = "
           f"**{gram:.1f} us** (average kernel durations)."]
     open(os.path.join(ROOT, "profiles", "gram_dominated_kernel_trace.md"), "w").write("\n".join(kt) + "\n")
 

@@ -26,8 +26,9 @@
 //                        eight waves each hold a 128x64 fp32 accumulator
 //                        (bf16 16x16x32 MFMA); lower-triangle tiles only,
 //                        scheduled in 4x8-tile chunks, one per XCD at a time.
-//   gram_mirror_kernel : fills the upper triangle from the lower one
-//                        (64x64 tiles through LDS), so K is exactly symmetric.
+//                        Each tile is also stored transposed into the upper
+//                        triangle (through LDS, whole rows of K), so K is
+//                        exactly symmetric without a second pass.
 // Small fp32 problems (n + 1 <= 128 rows: the per-step batches):
 //   gram_small_kernel  : one workgroup per 128-column chunk of a group forms
 //                        the chunk of gbar from the target rows (fp64 sum /
@@ -307,16 +308,20 @@ constexpr int kBPanel = kBT * kBK * 2;     // bytes of one operand panel per ste
 constexpr int kBStage = 2 * kBPanel;       // A and B panels
 constexpr int kBigMinTiles = 512;
 
+constexpr int kBTLd = 132;   // row stride (floats) of the transposed half tile staged in LDS
+constexpr int kBLds = 2 * kBStage > kBT * kBTLd * 4 ? 2 * kBStage : kBT * kBTLd * 4;
+
 struct BigArgs {
   const unsigned char* G;
   long long ldG;   // elements
   int n, T, pairs;
+  int vec4;        // K rows start 16-byte aligned (n % 4 == 0, K aligned): float4 stores of the transposed tile
   long long goff[kMaxGroups + 1];
   float* K;        // [P][n][n] of this launch's groups
 };
 
 __global__ __launch_bounds__(512) void gram_big_kernel(BigArgs a) {
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * kBStage];
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[kBLds];
   const int p = blockIdx.y;
   // Workgroup i runs on XCD i % 8, and an XCD's 32 CUs take its workgroups
   // in order.  The lower-triangle tiles are grouped in chunks of 4 tile rows
@@ -422,25 +427,35 @@ __global__ __launch_bounds__(512) void gram_big_kernel(BigArgs a) {
         const int col = rowB0 + wc * 64 + 16 * j + lr;
         if (row < a.n && col < a.n && (!diag || col <= row)) Kp[(long long)row * a.n + col] = acc[i][j][r];
       }
-}
-
-// K[c][r] = K[r][c] for c > r: lower 64x64 tiles through LDS
-__global__ __launch_bounds__(kThreads) void gram_mirror_kernel(float* K, int n) {
-  __shared__ float tile[64][65];
-  int I, J;
-  pair_to_tiles(blockIdx.x, I, J);
-  float* Kp = K + (long long)blockIdx.y * n * n;
-  const int r0 = I * 64, c0 = J * 64;
-  for (int e = threadIdx.x; e < 64 * 64; e += kThreads) {
-    const int rr = e >> 6, cc = e & 63;
-    const int r = r0 + rr, c = c0 + cc;
-    tile[rr][cc] = (r < n && c <= r) ? Kp[(long long)r * n + c] : 0.f;
-  }
-  __syncthreads();
-  for (int e = threadIdx.x; e < 64 * 64; e += kThreads) {
-    const int rr = e >> 6, cc = e & 63;
-    const int orow = c0 + rr, ocol = r0 + cc;   // the mirror of (ocol, orow)
-    if (orow < n && ocol < n && ocol > orow) Kp[(long long)orow * n + ocol] = tile[cc][rr];
+  // the same values into the upper triangle, K[col][row] = C[row][col]
+  // (strictly below the diagonal for a diagonal tile): each 128-row half of
+  // the tile is staged transposed in LDS, then stored as whole rows of K
+  __syncthreads();   // every wave is past the k-loop's last LDS read
+  float* Tt = reinterpret_cast<float*>(lds);   // [256 columns][kBTLd]: Tt[c][r] = C[128 h + r][c]
+  for (int h = 0; h < 2; ++h) {
+    if (wr == h) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<f32x4*>(&Tt[(wc * 64 + 16 * j + lr) * kBTLd + 16 * i + 4 * lg]) = acc[i][j];
+    }
+    __syncthreads();
+    for (int e = tid; e < kBT * 32; e += 512) {   // 32 float4 per transposed row
+      const int c = e >> 5, r4 = 4 * (e & 31);
+      const int grow = rowB0 + c, gcol = rowA0 + 128 * h + r4;
+      if (grow >= a.n) continue;
+      const f32x4 v = *reinterpret_cast<const f32x4*>(&Tt[c * kBTLd + r4]);
+      float* dst = Kp + (long long)grow * a.n + gcol;
+      if (a.vec4 && gcol + 3 < a.n && (!diag || 128 * h + r4 > c)) {
+        *reinterpret_cast<f32x4*>(dst) = v;
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (gcol + q < a.n && (!diag || 128 * h + r4 + q > c)) dst[q] = v[q];
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -671,11 +686,8 @@ extern "C" dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* 
       b.K = K + (long long)p0 * n * n;
       int chunks = 0;
       for (int band = 0; 4 * band < b.T; ++band) chunks += ((4 * band + 4 < b.T ? 4 * band + 4 : b.T) + 7) / 8;
+      b.vec4 = (n % 4 == 0) && aligned16(K);
       hipLaunchKernelGGL(gram_big_kernel, dim3((chunks + 7) / 8 * 256, gp), dim3(512), 0, hs, b);
-      if ((st = launch_status()) != DR_OK) return st;
-      const int T64 = (int)((n + 63) / 64);
-      hipLaunchKernelGGL(gram_mirror_kernel, dim3(T64 * (T64 + 1) / 2, gp), dim3(kThreads), 0, hs,
-                         K + (long long)p0 * n * n, (int)n);
       if ((st = launch_status()) != DR_OK) return st;
     } else if (g.small) {
       hipLaunchKernelGGL(gram_small_kernel, dim3(g.maxchunks, gp), dim3(kThreads), 0, hs, a,

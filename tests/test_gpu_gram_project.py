@@ -80,16 +80,18 @@ def test_gram_dominated_full_size_sampled():
     assert torch.equal(K[0, :64, 8000:8064], K[0, 8000:8064, :64].T)
 
 
-def test_gram_large_tiles_ragged_groups():
-    """The 256x256-tile path: ragged n (8200 rows), a ragged group width (1000
-    columns), an empty group and a full-width one; sampled rows of each K_p
-    against the oracle, every K_p exactly symmetric."""
-    n, goff = 8200, [0, 1000, 1000, 2600]
+@pytest.mark.parametrize("n", [8200, 8195])
+def test_gram_large_tiles_ragged_groups(n):
+    """The 256x256-tile path: ragged n (8200 rows; 8195, whose K rows are not
+    16-byte aligned), a ragged group width (1000 columns), an empty group and
+    a full-width one; sampled rows of each K_p against the oracle, every K_p
+    exactly symmetric."""
+    goff = [0, 1000, 1000, 2600]
     G = rand((n, 2600), 77, torch.bfloat16)
     Gt = rand((3, 2600), 78, torch.bfloat16)
     K, s, t2 = api.gram(G, Gt, goff)
     torch.cuda.synchronize()
-    pick = [0, 255, 256, 4100, 8191, 8199]
+    pick = [0, 255, 256, 4100, 8191, n - 1]
     Gh, Gth = host64(G), host64(Gt)
     for p in range(3):
         c0, c1 = goff[p], goff[p + 1]
