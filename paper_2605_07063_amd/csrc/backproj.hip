@@ -9,12 +9,15 @@
 //
 // Up to 16 layers go in one launch (blockIdx.z = layer), so that the small
 // per-layer grids fill the chip together.
-//   bp_left_kernel   T = X' P_in   [k_out][d_in] fp32 (small, workspace)
+//   bp_left_kernel   T = X' P_in   [k_out][d_in] fp32 (small, workspace),
+//                    one 64-column slice of T per workgroup, fp32 MFMA
+//                    (16x16x4) with both operands staged in LDS
 //   bp_right_kernel  U = P_out^T T, one 64 (d_out) x 256 (d_in) tile per
 //                    workgroup: each thread owns 16 rows x 4 columns, so a
 //                    float4 of T read from L2 feeds 64 FMAs; the P_out columns
 //                    of the tile sit in LDS.  The d_out x d_in fp32 write is
-//                    the HBM bound.
+//                    the HBM bound.  (fp32 MFMA has the same peak as fp32
+//                    FMA on this chip; staged or not, it measured slower here.)
 
 #include "common.h"
 
@@ -22,9 +25,11 @@ namespace dr {
 namespace {
 
 constexpr int kBpLayers = 16;  // layers per launch (blockIdx.z)
-constexpr int kBpRows = 16;    // rows per wave (4 waves: 64 rows per tile)
-constexpr int kBpCols = 256;   // columns per tile (4 per lane)
+constexpr int kBpTile = 64;    // columns of T per workgroup of bp_left_kernel
+constexpr int kBpRows = 16;    // bp_right_kernel: rows per wave (4 waves: 64 rows per tile)
+constexpr int kBpCols = 256;   // bp_right_kernel: columns per tile (4 per lane)
 constexpr int kBpMaxK = 64;
+constexpr int kBpLd = 132;     // LDS row stride (floats)
 
 template <typename TP>
 __device__ __forceinline__ float ld(const TP* p, long long i) {
@@ -40,27 +45,63 @@ struct BpArgs {
   int k_in[kBpLayers], k_out[kBpLayers], d_in[kBpLayers], d_out[kBpLayers];
 };
 
-// T[a][c] = sum_b X'[a][b] P_in[b][c]
+// T[a][c] = sum_b X'[a][b] P_in[b][c] for c in this workgroup's 64 columns;
+// a < k_out <= 64 (4 row tiles), 4 column tiles: wave w takes column tile w
+// of every row tile.  Rows and columns past k_in / k_out /
+// d_in are zero in LDS.
 template <typename TP>
 __global__ __launch_bounds__(256) void bp_left_kernel(BpArgs g) {
+  __shared__ __attribute__((aligned(16))) float xs[kBpMaxK * 68];   // X'[a][b], stride 68
+  __shared__ __attribute__((aligned(16))) float ps[kBpMaxK * kBpLd];   // P_in[b][c - c0]
   const int l = blockIdx.z;
-  const int a = blockIdx.y;
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  const int k_in = g.k_in[l], d_in = g.d_in[l];
-  if (a >= g.k_out[l] || c >= d_in) return;
+  const int k_in = g.k_in[l], k_out = g.k_out[l], d_in = g.d_in[l];
+  const int c0 = blockIdx.x * kBpTile;
+  if (c0 >= d_in) return;
   const float* x = g.x[l];
   const TP* p_in = static_cast<const TP*>(g.p_in[l]);
-  float* T = g.T[l];
-  float acc = 0.f;
-  for (int b0 = 0; b0 < k_in; b0 += 16) {   // 16 loads in flight before the FMAs
-    float pv[16];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, lr = lane & 15, lq = lane >> 4;
+  {
+    // every load of the thread in flight before the LDS writes
+    float xv[kBpMaxK * kBpMaxK / 256], pv[kBpMaxK * kBpTile / 256];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) pv[u] = b0 + u < k_in ? ld(p_in, (long long)(b0 + u) * d_in + c) : 0.f;
+    for (int u = 0; u < kBpMaxK * kBpMaxK / 256; ++u) {
+      const int e = tid + 256 * u, a = e >> 6, b = e & 63;
+      xv[u] = (a < k_out && b < k_in) ? x[a * k_in + b] : 0.f;
+    }
 #pragma unroll
-    for (int u = 0; u < 16; ++u)
-      if (b0 + u < k_in) acc = fmaf(x[a * k_in + b0 + u], pv[u], acc);
+    for (int u = 0; u < kBpMaxK * kBpTile / 256; ++u) {
+      const int e = tid + 256 * u, b = e / kBpTile, c = e % kBpTile;
+      pv[u] = (b < k_in && c0 + c < d_in) ? ld(p_in, (long long)b * d_in + c0 + c) : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kBpMaxK * kBpMaxK / 256; ++u) {
+      const int e = tid + 256 * u;
+      xs[(e >> 6) * 68 + (e & 63)] = xv[u];
+    }
+#pragma unroll
+    for (int u = 0; u < kBpMaxK * kBpTile / 256; ++u) {
+      const int e = tid + 256 * u;
+      ps[(e / kBpTile) * kBpLd + e % kBpTile] = pv[u];
+    }
   }
-  T[(long long)a * d_in + c] = acc;
+  __syncthreads();
+  f32x4 acc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int kq = (k_in + 3) & ~3;
+  for (int b0 = 0; b0 < kq; b0 += 4) {
+    const float bv = ps[(b0 + lq) * kBpLd + 16 * w + lr];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] = mma_f32(xs[(16 * i + lr) * 68 + b0 + lq], bv, acc[i]);
+  }
+  float* T = g.T[l];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int a = 16 * i + 4 * lq + q, c = c0 + 16 * w + lr;
+      if (a < k_out && c < d_in) T[(long long)a * d_in + c] = acc[i][q];
+    }
 }
 
 // U[o][c] = sum_a P_out[a][o] T[a][c] for a 64 (d_out) x 256 (d_in) tile:
@@ -157,7 +198,7 @@ extern "C" dr_status dr_back_project(const dr_layer* layers, int num_layers, dr_
   for (int f = 0; f < num_layers; f += kBpLayers) {
     const int count = num_layers - f < kBpLayers ? num_layers - f : kBpLayers;
     BpArgs g = {};
-    int kmax = 1, dimax = 1, domax = 1;
+    int dimax = 1, domax = 1;
     size_t o = 0;
     for (int j = 0; j < count; ++j) {
       const dr_layer& L = layers[f + j];
@@ -171,11 +212,10 @@ extern "C" dr_status dr_back_project(const dr_layer* layers, int num_layers, dr_
       g.k_out[j] = (int)L.k_out;
       g.d_in[j] = (int)L.d_in;
       g.d_out[j] = (int)L.d_out;
-      kmax = g.k_out[j] > kmax ? g.k_out[j] : kmax;
       dimax = g.d_in[j] > dimax ? g.d_in[j] : dimax;
       domax = g.d_out[j] > domax ? g.d_out[j] : domax;
     }
-    const dim3 gl((dimax + 255) / 256, kmax, count);
+    const dim3 gl((dimax + kBpTile - 1) / kBpTile, 1, count);
     const dim3 gr((dimax + kBpCols - 1) / kBpCols, (domax + 4 * kBpRows - 1) / (4 * kBpRows), count);
     if (dtype == DR_BF16) {
       hipLaunchKernelGGL(bp_left_kernel<__bf16>, gl, dim3(256), 0, hs, g);
