@@ -394,15 +394,15 @@ def time_gram_dominated(api, _lib, workloads, dev, reps=3):
 
 SKETCH_SOURCES = ["paper_2605_07063_amd/csrc/sketch.hip", "paper_2605_07063_amd/csrc/common.h"]
 SKETCH_KERNELS = ("sketch_plan_kernel", "sketch_packed_kernel", "sketch_packed_reduce_kernel")
-KT_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_kt -o small -- "
+KT_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d prof_out/kt -o small -- "
           "python -u bench.py --steps 50 --warmup 10 --no-cpu-baseline")
-PMC_CMD = ("rocprofv3 --pmc {c} --output-format csv -d gpurun_out/prof_{d} -o small -- "
+PMC_CMD = ("rocprofv3 --pmc {c} --output-format csv -d prof_out/{d} -o small -- "
            "python -u bench.py --steps 5 --warmup 2 --no-cpu-baseline --no-next-rows --no-gram-dominated "
            "--copy-calibration")
-SUM_CMD = "python bench.py --summarize-profiles gpurun_out/prof_kt gpurun_out/prof_fetch gpurun_out/prof_write"
-GD_KT_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_gd -o gd -- "
+SUM_CMD = "python bench.py --summarize-profiles prof_out/kt prof_out/fetch prof_out/write"
+GD_KT_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d prof_out/gd -o gd -- "
              "python -u bench.py --gram-dominated-only")
-GD_SUM_CMD = "python bench.py --summarize-gram-profile gpurun_out/prof_gd"
+GD_SUM_CMD = "python bench.py --summarize-gram-profile prof_out/gd"
 
 
 def sketch_sources_sha():
@@ -465,7 +465,7 @@ def summarize_gram_profile(kt_dir):
     rows, avg = _kernel_rows(f[0])
     gram = sum(v for k, v in avg.items() if k.startswith(("gram_big_kernel", "score_kernel", "target_mean_kernel")))
     kt = ["# Kernel trace: Gram-dominated workload (Gram, span, top-1024)", "",
-          "Command (repository root on the GPU box, `TMPDIR=/tmp`), summarised by", "",
+          "Command (run from the repository root with `TMPDIR=/tmp`), summarised by", "",
           "```", GD_KT_CMD, GD_SUM_CMD, "```", "",
           "`bench.py --gram-dominated-only` times each stage once untimed and 3 times timed (top-k 30 times): "
           "4 `dr_gram` calls (16416 x 8192 bf16 rows) and 4 `dr_project_span` calls at n = 16384. "
@@ -492,7 +492,7 @@ def summarize_profiles(kt_dir, fetch_dir, write_dir):
     rows, avg = _kernel_rows(one("*_kernel_stats.csv", kt_dir))
     sk_avg = sum(v for k, v in avg.items() if k.startswith(SKETCH_KERNELS))
     kt = ["# Kernel trace: small-block workload, bench step", "",
-          "Command (repository root on the GPU box, `TMPDIR=/tmp`), summarised by", "",
+          "Command (run from the repository root with `TMPDIR=/tmp`), summarised by", "",
           "```", KT_CMD, SUM_CMD, "```", "",
           "60 calls per kernel of the step = 10 warmup + 50 timed steps. The widening-row kernels (update "
           "assembly, exact scorers, subset rules, simplex, back-projection) run after the step in their own "
@@ -530,7 +530,8 @@ def summarize_profiles(kt_dir, fetch_dir, write_dir):
         if k.startswith(SKETCH_KERNELS):
             sk_bytes += (fa * ffac + wa * wfac) * 1024
     tr = ["# HBM traffic: small-block workload, bench step", "",
-          "Two counter passes, each in its own run (`TMPDIR=/tmp`), summarised by the last command:", "", "```",
+          "Two counter passes, each in its own run (from the repository root, `TMPDIR=/tmp`), summarised by the "
+          "last command:", "", "```",
           PMC_CMD.format(c="FETCH_SIZE", d="fetch"), PMC_CMD.format(c="WRITE_SIZE", d="write"), SUM_CMD, "```", "",
           "Calibration: `--copy-calibration` makes three 1 GiB device-to-device copies (1,048,576 KiB read and "
           "written).",
