@@ -495,8 +495,9 @@ def summarize_profiles(kt_dir, fetch_dir, write_dir):
           "Command (run from the repository root with `TMPDIR=/tmp`), summarised by", "",
           "```", KT_CMD, SUM_CMD, "```", "",
           "60 calls per kernel of the step = 10 warmup + 50 timed steps. The widening-row kernels (update "
-          "assembly, exact scorers, subset rules, simplex, back-projection) run after the step in their own "
-          "timed loops, with their own call counts. Durations in microseconds.", "",
+          "assembly, exact scorers, subset rules, simplex, back-projection) and the Gram-dominated stages "
+          "(gram_big_kernel, the blocked span's lg_* kernels, top-1024) run after the step in their own timed "
+          "loops, with their own call counts. Durations in microseconds.", "",
           "| Kernel | Calls | Avg (us) | Min | Max | Share |", "|---|---|---|---|---|---|"] + rows + [
           "", f"The sketch call (`dr_sketch_grads`) = {' + '.join(SKETCH_KERNELS)} = **{sk_avg:.1f} us** per call "
           "(average kernel durations; bench.py's HIP-event time of the same call also spans the launch gaps)."]
