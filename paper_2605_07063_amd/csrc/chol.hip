@@ -526,21 +526,26 @@ constexpr int SY_PANEL = NB * SY_CH * 4;  // bytes of one tile row's chunk (16 K
 // head = true: the tiles of the first h (1 or 2) tile columns, column by
 // column (they hold the next panels); head = false: every tile with
 // I >= J >= h.
+// A workgroup takes tiles blockIdx.x, blockIdx.x + gridDim.x, ... < ntiles:
+// a grid smaller than the chip leaves CUs free for the factorisation chain
+// running on the other stream.
 template <int W>
 __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL, int n, int k, int h, int head,
-                                                         const LgCtl* ctl) {
+                                                         int ntiles, const LgCtl* ctl) {
   if (ctl->skip) return;
   __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * 2 * SY_PANEL];
   constexpr int NCH = W / SY_CH;
   const int k1 = k + W;
+  for (int qt = blockIdx.x; qt < ntiles; qt += gridDim.x) {
+  __syncthreads();   // (uniform) the previous tile is done with the LDS ring
   int I, J;
   if (head) {
     const int T = (n - k1 + NB - 1) / NB;
-    const int q = blockIdx.x;
+    const int q = qt;
     I = q < T ? q : q - T + 1;
     J = q < T ? 0 : 1;
   } else {
-    tile_pair(blockIdx.x, I, J);
+    tile_pair(qt, I, J);
     I += h;
     J += h;
   }
@@ -620,17 +625,20 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
       }
     }
   }
-  if (!active) return;
+  if (active) {
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb)
+    for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb)
+      for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int row = ri + 64 * wr + 16 * rb + 4 * lg + q;
-        const int col = rj + 64 * wc + 16 * cb + lr;
-        if (row < n && col < n && (!diag || col <= row)) L[(long long)row * ldL + col] = c[rb][cb][q] - acc[rb][cb][q];
-      }
+        for (int q = 0; q < 4; ++q) {
+          const int row = ri + 64 * wr + 16 * rb + 4 * lg + q;
+          const int col = rj + 64 * wc + 16 * cb + lr;
+          if (row < n && col < n && (!diag || col <= row))
+            L[(long long)row * ldL + col] = c[rb][cb][q] - acc[rb][cb][q];
+        }
+  }
+  }   // tiles of this workgroup
 }
 
 // ---------------------------------------------------------------- solves
@@ -896,6 +904,14 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
                                    int mode, float* w, float* lam_eff, float* resid2, int32_t* info,
                                    const LgLayout& lay, unsigned char* base, hipStream_t hs, hipStream_t aux,
                                    hipEvent_t ev_col, hipEvent_t ev_next) {
+  // the bulk trailing update runs on at most two workgroups per CU of all but
+  // one CU in 32 (one per XCD on a 256-CU part), so that the diagonal-block
+  // chain of the next pair finds free CUs instead of queueing behind it
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                              hipSuccess || cus < 32)
+    cus = 256;
+  const int rest_slots = 2 * (cus - cus / 32);
   float* L = reinterpret_cast<float*>(base + lay.off_L);
   float* inv = reinterpret_cast<float*>(base + lay.off_inv);
   float* sinv = reinterpret_cast<float*>(base + lay.off_sinv);
@@ -942,7 +958,7 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       const bool pair = b + 1 < nblk;
       if (pair) {
         const int T1 = (n - k - NB + NB - 1) / NB;
-        hipLaunchKernelGGL(lg_syrk_kernel<NB>, dim3(T1), dim3(256), 0, aux, L, ldL, n, k, 1, 1, ctl);
+        hipLaunchKernelGGL(lg_syrk_kernel<NB>, dim3(T1), dim3(256), 0, aux, L, ldL, n, k, 1, 1, T1, ctl);
         factor_panel(b + 1, aux);
       }
       if (hipEventRecord(ev_next, aux) != hipSuccess || hipStreamWaitEvent(hs, ev_next, 0) != hipSuccess)
@@ -953,10 +969,12 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       const int h = T < 2 ? T : 2;
       const int nhead = h * T - h * (h - 1) / 2;
       const int nrest = (T - h) * (T - h + 1) / 2;
-      hipLaunchKernelGGL(lg_syrk_kernel<2 * NB>, dim3(nhead), dim3(256), 0, hs, L, ldL, n, k, h, 1, ctl);
+      hipLaunchKernelGGL(lg_syrk_kernel<2 * NB>, dim3(nhead), dim3(256), 0, hs, L, ldL, n, k, h, 1, nhead, ctl);
       if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;
-      if (nrest > 0)
-        hipLaunchKernelGGL(lg_syrk_kernel<2 * NB>, dim3(nrest), dim3(256), 0, hs, L, ldL, n, k, h, 0, ctl);
+      if (nrest > 0) {
+        const int grid = nrest < rest_slots ? nrest : rest_slots;
+        hipLaunchKernelGGL(lg_syrk_kernel<2 * NB>, dim3(grid), dim3(256), 0, hs, L, ldL, n, k, h, 0, nrest, ctl);
+      }
     }
     const int nsb = (nblk + SB - 1) / SB;
     for (int d = 0; d < SB; ++d)
