@@ -34,6 +34,8 @@
 // the exact Euclidean projection onto the simplex (Michelot's iteration:
 // theta = (sum_{v_i > theta} v_i - 1) / #{v_i > theta} until the set stops
 // shrinking, a handful of block reductions).  Same K layout as the cone.
+// simplex_wave_kernel (n <= 64): the same iteration on one wave, every
+// reduction a wave reduction (no block barrier per step).
 
 #include "common.h"
 
@@ -1083,6 +1085,111 @@ __global__ __launch_bounds__(kConeThreads) void simplex_pg_kernel(const float* K
   }
 }
 
+// simplex_pg_kernel for n <= 64 on one wave: lane i keeps row i of K in
+// registers and its own y_i, v_i, w_i; y is published through LDS for the
+// product and every block reduction of the block version (Michelot's
+// passes, the residual, the start vertex) is a wave reduction, so a step
+// has no block barrier.  Same iteration as simplex_pg_kernel.
+__global__ __launch_bounds__(kWaveN) void simplex_wave_kernel(const float* K, const float* s, const float* t2, int n,
+                                                              int max_iter, float tol, float* w, float* resid2,
+                                                              int* iters, float* res_out, int* info) {
+  __shared__ __attribute__((aligned(16))) double yb[kWaveN];
+  const int p = blockIdx.x, i = threadIdx.x;
+  const float* Kp = K + (long long)p * n * n;
+  const float* sp = s + (long long)p * n;
+  const bool own = i < n;
+  float kr[kWaveN];
+  bool bad = own && !isfinite(sp[i]);
+  double lrow = 0.0;
+#pragma unroll
+  for (int j = 0; j < kWaveN; ++j) {
+    kr[j] = (own && j < n) ? Kp[(long long)i * n + j] : 0.f;
+    bad |= !isfinite(kr[j]);
+    lrow += fabs((double)kr[j]);
+  }
+  if (__any(bad)) {
+    if (own) w[(long long)p * n + i] = 0.f;
+    if (i == 0) {
+      resid2[p] = t2[p];
+      iters[p] = 0;
+      res_out[p] = 0.f;
+      info[p] = DR_INFO_NONFINITE;
+    }
+    return;
+  }
+  const double L = 2.0 * wave_max(own ? lrow : 0.0);
+  const double si = own ? (double)sp[i] : 0.0;
+  // start: the best single vertex, argmin_i K_ii - 2 s_i (lowest index on ties)
+  double fbest = own ? (double)Kp[(long long)i * n + i] - 2.0 * si : 0.0;
+  int ibest = own ? i : -1;
+  for (int off = 32; off > 0; off >>= 1) {
+    const double fo = __shfl_xor(fbest, off, 64);
+    const int io = __shfl_xor(ibest, off, 64);
+    if (io >= 0 && (ibest < 0 || fo < fbest || (fo == fbest && io < ibest))) {
+      fbest = fo;
+      ibest = io;
+    }
+  }
+  double y = i == ibest ? 1.0 : 0.0, wp = y;
+  auto product = [&](double x) {   // (K x)_i with x_j held by lane j
+    yb[i] = x;
+    __syncthreads();   // (one wave) the LDS writes are visible
+    double a0 = 0.0, a1 = 0.0;
+#pragma unroll
+    for (int j = 0; j < kWaveN; j += 2) {
+      const f64x2 v = *reinterpret_cast<const f64x2*>(&yb[j]);
+      a0 += (double)kr[j] * v.x;
+      a1 += (double)kr[j + 1] * v.y;
+    }
+    __syncthreads();   // every lane has read yb before the next write
+    return a0 + a1;
+  };
+
+  int it = 0;
+  double res = 0.0, tk = 1.0;
+  while (L > 0.0 && it < max_iter) {
+    // v = y - 2 (K y - s) / L
+    const double acc = product(own ? y : 0.0);
+    const double v = own ? y - 2.0 * (acc - si) / L : 0.0;
+    // theta with sum_i max(v_i - theta, 0) = 1
+    int prev = n + 1;
+    double theta = -1.0e308;
+    while (true) {
+      const bool in = own && v > theta;
+      double sum = in ? v : 0.0;
+      int cnt = in ? 1 : 0;
+      for (int off = 32; off > 0; off >>= 1) {
+        sum += __shfl_xor(sum, off, 64);
+        cnt += __shfl_xor(cnt, off, 64);
+      }
+      if (cnt == prev || cnt == 0) break;
+      prev = cnt;
+      theta = (sum - 1.0) / (double)cnt;
+    }
+    // w = max(v - theta, 0); residual = max |w - y|; momentum step
+    const double tn = 0.5 * (1.0 + sqrt(1.0 + 4.0 * tk * tk));
+    const double beta = (tk - 1.0) / tn;
+    const double wi = own ? fmax(v - theta, 0.0) : 0.0;
+    res = wave_max(own ? fabs(wi - y) : 0.0);
+    y = wi + beta * (wi - wp);
+    wp = wi;
+    tk = tn;
+    ++it;
+    if (tol > 0.f && res <= (double)tol) break;
+  }
+
+  // w = the last projected point; resid2 = t2 + w.K.w - 2 s.w
+  const double acc = product(own ? wp : 0.0);
+  const double q = wave_sum(own ? wp * acc - 2.0 * si * wp : 0.0);
+  if (own) w[(long long)p * n + i] = (float)wp;
+  if (i == 0) {
+    resid2[p] = (float)((double)t2[p] + q);
+    iters[p] = it;
+    res_out[p] = (float)res;
+    info[p] = (tol > 0.f && res > (double)tol) ? DR_INFO_NOT_CONVERGED : 0;
+  }
+}
+
 __global__ void empty_group_kernel(const float* t2, int P, float* lam_eff, float* resid2, int32_t* iters, float* kkt,
                                    int32_t* info) {
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
@@ -1201,6 +1308,11 @@ extern "C" dr_status dr_project_simplex(const float* K, const float* s, const fl
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   if (n == 0) {   // the simplex of zero examples is empty: nothing to project onto
     hipLaunchKernelGGL(empty_group_kernel, dim3((P + 255) / 256), dim3(256), 0, hs, t2, P, (float*)nullptr, resid2,
+                       iters, res, info);
+    return launch_status();
+  }
+  if (n <= kWaveN) {
+    hipLaunchKernelGGL(simplex_wave_kernel, dim3(P), dim3(kWaveN), 0, hs, K, s, t2, (int)n, max_iter, tol, w, resid2,
                        iters, res, info);
     return launch_status();
   }
