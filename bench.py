@@ -506,7 +506,8 @@ def summarize_profiles(kt_dir, fetch_dir, write_dir):
     kt = ["# Kernel trace: small-block workload, bench step", "",
           "Command (run from the repository root with `TMPDIR=/tmp`), summarised by", "",
           "```", KT_CMD, SUM_CMD, "```", "",
-          "60 calls per kernel of the step = 10 warmup + 50 timed steps. The widening-row kernels (update "
+          "110 calls per kernel of the step = 10 warmup + 50 timed steps + 50 steps of the per-stage "
+          "breakdown. The widening-row kernels (update "
           "assembly, exact scorers, subset rules, simplex, back-projection) and the Gram-dominated stages "
           "(gram_big_kernel, the blocked span's lg_* kernels, top-1024) run after the step in their own timed "
           "loops, with their own call counts. Durations in microseconds.", "",
