@@ -193,7 +193,8 @@ size_t dr_span_workspace_size(int64_t n, int P);
  *   w [P][n] out; resid2 [P] out (as for the span); iters [P] out (steps
  *   taken); kkt [P] out (rho of the returned w); info [P] out
  *   (DR_INFO_NOT_CONVERGED if kkt_tol > 0 and rho > kkt_tol at the end).
- * Coordinates with K_ii = 0 get w_i = 0.  Supports n <= 1024.
+ * Coordinates with K_ii = 0 get w_i = 0.  Supports n <= 256 (larger n:
+ * DR_ERR_UNSUPPORTED); the whole problem runs in one workgroup per group.
  * ------------------------------------------------------------------------- */
 dr_status dr_project_cone(const float* K, const float* s, const float* t2, int64_t n, int P,
                           int max_iter, float kkt_tol, float* w, float* resid2, int32_t* iters,
