@@ -107,9 +107,11 @@ const char* dr_status_string(dr_status s);
  * read, so padding may hold any bits (NaN included).
  *
  * Arithmetic: DR_BF16 inputs are contracted on bf16 MFMA with fp32
- * accumulation; the second (token) contraction runs in fp32.  DR_F32
- * inputs use fp32 MFMA throughout.  Nothing below fp32 is rounded after
- * the inputs.
+ * accumulation; the second (token) contraction splits each fp32 stage-1
+ * value into bf16 hi + lo parts and sums Dh Yh + Dh Yl + Dl Yh on bf16
+ * MFMA with fp32 accumulation (about 3 * 2^-16 relative error per
+ * product, far inside the bf16 inputs' own rounding).  DR_F32 inputs use
+ * fp32 MFMA throughout.
  *
  * Arguments
  *   layers      (host) array of num_layers descriptors, 1 <= num_layers.
