@@ -315,8 +315,12 @@ size_t dr_combine_workspace_size(int64_t n, const int64_t* goff, int P);
  * Eq. (proj) in parameter space.  Examples with weight 0 and padded tokens
  * t >= len[i] are never read (they may hold any bits, NaN included).
  *
- * Arithmetic: DR_BF16 inputs on bf16 MFMA with fp32 accumulation, each
- * example's sum scaled by its weight in fp32; DR_F32 inputs on fp32 MFMA.
+ * Arithmetic: DR_BF16 inputs on bf16 MFMA with fp32 accumulation.  The
+ * weighted examples of a layer are taken in |w|-ascending order into one
+ * fp32 accumulator holding sum_e (w_e / w_cur) G_e, multiplied by
+ * w_cur / w_next when the weight changes and by the last weight at the end
+ * (every factor lies in [-1, 1]; equal weights cost nothing).  DR_F32
+ * inputs on fp32 MFMA.
  *
  * Arguments
  *   layers      (host) num_layers descriptors; x, ldx, dy, lddy, d_in, d_out
