@@ -233,7 +233,10 @@ dr_status dr_project_simplex(const float* K, const float* s, const float* t2, in
  * variant.  p_in / p_out have dtype `dtype`; x, dy are not used.
  * Requirements: 1 <= k_in, k_out <= 64; d_in a multiple of 4; U + u_offset[l]
  * 16-byte aligned; workspace of at least
- * dr_backproject_workspace_size() bytes (one layer's P_in product).
+ * dr_backproject_workspace_size() bytes (X' P_in of up to 16 layers, as
+ * fp32 or as three bf16 planes).  bf16 projectors with d_in, d_out
+ * multiples of 8 run P_out^T on bf16 MFMA over the three planes (exact to
+ * fp32 rounding); otherwise fp32 FMA.
  * ------------------------------------------------------------------------- */
 dr_status dr_back_project(const dr_layer* layers, int num_layers, dr_dtype dtype, const float* u, float* U,
                           const int64_t* u_offset, void* workspace, size_t ws_bytes, void* stream);

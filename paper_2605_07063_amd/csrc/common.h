@@ -63,6 +63,21 @@ __device__ __forceinline__ u32x4 swz_read(const unsigned char* blk, int r, int s
 // the segment that lane l loads when its wave fills half block h (0 or 1)
 __device__ __forceinline__ int swz_seg_of_lane(int l, int h) { return (l & 7) ^ (4 * h + (l >> 4)); }
 
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s lds_v4s;
+
+// gfx950 transposing LDS read: within each 16-lane group, source lane
+// 4q + r addresses 4 consecutive 16-bit columns c..c+3 of row q; lane j of
+// the group receives column c_0 + j of the four rows (its four values are
+// rows 0..3 in order).
+__device__ __forceinline__ v4s lds_read_tr16(const unsigned char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p));
+}
+
+// swizzle of the 32-byte slots of a token row: rows that one transposing
+// read touches (q = r & 3 and bit 3 of r) land in distinct bank groups
+__device__ __forceinline__ int slot_xor(int r) { return (r & 3) | (((r >> 3) & 1) << 2); }
+
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 inline dr_status launch_status() {

@@ -191,20 +191,6 @@ __device__ __forceinline__ bool locate(const UpdArgs& a, int& layer, int& to, in
 
 // ------------------------------------------------------------------ bf16
 
-typedef short v4s __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) v4s lds_v4s;
-
-// gfx950 transposing LDS read: within each 16-lane group, source lane
-// 4q + r addresses 4 consecutive 16-bit columns c..c+3 of row q; lane j of
-// the group receives column c_0 + j of the four rows (its four values are
-// rows 0..3 in order).
-__device__ __forceinline__ v4s lds_read_tr16(const unsigned char* p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p));
-}
-
-// swizzle of the 32-byte slots of a token row: rows that one transposing
-// read touches (q = r & 3 and bit 3 of r) land in distinct bank groups
-__device__ __forceinline__ int slot_xor(int r) { return (r & 3) | (((r >> 3) & 1) << 2); }
 
 // SCORE = false: the update.  SCORE = true (the Direct scorer of Sec. 4.3):
 // every example of the list gets weight 1; at the end of each example its

@@ -101,11 +101,16 @@ def test_simplex_on_the_small_block_gram():
         check(K, s, t2, max_iter=50000, tol=1e-9)
 
 
-@pytest.mark.parametrize("dtype,tol", [(torch.float32, 1e-5), (torch.bfloat16, 1e-5)])
-def test_back_projection_matches_oracle(dtype, tol):
+@pytest.mark.parametrize("dtype,tol,specs", [
+    (torch.float32, 1e-5, [(200, 136, 64, 64), (128, 264, 16, 32), (72, 64, 32, 16)]),
+    # bf16, every dimension a multiple of 8: the bf16-MFMA path (T as three bf16 planes)
+    (torch.bfloat16, 1e-5, [(200, 136, 64, 64), (128, 264, 16, 32), (72, 64, 32, 16)]),
+    # bf16 with d_in = 100 (not a multiple of 8): the fp32 path for the whole launch
+    (torch.bfloat16, 1e-5, [(100, 60, 8, 12), (136, 40, 64, 33)]),
+])
+def test_back_projection_matches_oracle(dtype, tol, specs):
     g = torch.Generator(device=DEV)
     g.manual_seed(5)
-    specs = [(200, 136, 64, 64), (128, 264, 16, 32), (72, 64, 32, 16)]
     layers, off = [], 0
     for d_in, d_out, k_in, k_out in specs:
         layers.append(dict(p_in=(torch.randn(k_in, d_in, generator=g, device=DEV) / k_in ** 0.5).to(dtype),
