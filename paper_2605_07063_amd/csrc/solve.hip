@@ -6,10 +6,13 @@
 // t2 - 2 s.w + w.K.w without touching G.
 //
 // span_small_kernel (n <= 256): the lower triangle of K + lam_eff I is held
-// packed in LDS (fp32, at most 129 KiB) and factored right-looking by the
-// whole workgroup; forward / back substitution run on fp64 vectors; two
-// steps of iterative refinement recompute s - (K + lam_eff I) w in fp64
-// from the fp32 K read from global memory, which brings the solution to
+// in LDS as 16 x 16 fp32 tiles (at most 136 KiB) and factored right-looking
+// in 16-column steps by the whole workgroup (a one-wave register factor of
+// the diagonal tile, then fp32 MFMA tile products); forward / back substitution
+// run on fp64 vectors held in the registers of one wave (column-oriented,
+// one lane broadcast per step, no block barrier); two steps of iterative
+// refinement recompute s - (K + lam_eff I) w in fp64 from the fp32 K read
+// from global memory (one wave per row), which brings the solution to
 // fp64-level accuracy whenever cond(K + lam_eff I) * 2^-24 < 1.
 //
 // n <= 64 (the tiny, small-block and long-context workloads) is latency
@@ -67,27 +70,109 @@ __device__ double block_sum(double v, double* scratch) {
   return r;
 }
 
+constexpr int kWaveN = 64;
+
+__device__ __forceinline__ double wave_sum(double v) {
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+__device__ __forceinline__ double wave_max(double v) {
+  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
+  return v;
+}
+// value of lane src (src uniform) as a scalar broadcast
+__device__ __forceinline__ double readlane_d(double v, int src) {
+  const int lo = __builtin_amdgcn_readlane(__double2loint(v), src);
+  const int hi = __builtin_amdgcn_readlane(__double2hiint(v), src);
+  return __hiloint2double(hi, lo);
+}
+
+// The lower triangle of the (padded) matrix as 16 x 16 tiles: tile (I, J),
+// J <= I, starts at float (I (I + 1) / 2 + J) * 256, and row r of a tile is
+// stored at row position rperm(r), so that the rows 4q + j (q = 0..3) that
+// one MFMA result register covers fall in four different LDS bank groups
+// while a tile row stays 16 contiguous floats.
+constexpr int kSpanTiles = kSpanMaxN / 16;
+__device__ __forceinline__ int rperm(int r) { return 4 * (r & 3) + (r >> 2); }
+__device__ __forceinline__ int tile_at(int I, int J) { return (I * (I + 1) / 2 + J) * 256; }
+// offset of column i inside the tile row that holds it
+__device__ __forceinline__ int col_off(int i) { return (i >> 4) * 256 + (i & 15); }
+// start of row k of the matrix (tile column 0)
+__device__ __forceinline__ int row_at(int k) { return tile_at(k >> 4, 0) + rperm(k & 15) * 16; }
+
+__device__ __forceinline__ float readlane_f(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+// 1 / sqrt(d), d > 0 normal: hardware estimate plus one Newton step
+__device__ __forceinline__ float rsqrt_nr(float d) {
+  const float r = __builtin_amdgcn_rsqf(d);
+  return r * fmaf(-0.5f * d * r, r, 1.5f);
+}
+// q -> (I, J) with q = I (I + 1) / 2 + J, 0 <= J <= I
+__device__ __forceinline__ void tri_pair(int q, int& I, int& J) {
+  int i = (int)((sqrtf(8.f * q + 1.f) - 1.f) * 0.5f);
+  while ((i + 1) * (i + 2) / 2 <= q) ++i;
+  while (i * (i + 1) / 2 > q) --i;
+  I = i;
+  J = q - i * (i + 1) / 2;
+}
+
 __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K, const float* s, const float* t2,
                                                                   int n, float lambda, int mode, float* w,
                                                                   float* lam_eff_out, float* resid2, int* info) {
-  __shared__ float Lp[kSpanMaxN * (kSpanMaxN + 1) / 2];
-  __shared__ double x[kSpanMaxN], y[kSpanMaxN], r[kSpanMaxN];
+  __shared__ __attribute__((aligned(16))) float Lt[kSpanTiles * (kSpanTiles + 1) / 2 * 256];
+  __shared__ __attribute__((aligned(16))) float Xs[256];
+  __shared__ double x[kSpanMaxN], y[kSpanMaxN], dinv[kSpanMaxN];
   __shared__ double scratch[kSpanThreads / 64 + 1];
   __shared__ int flag;
   const int p = blockIdx.x, tid = threadIdx.x;
+  const int wid = tid >> 6, lane = tid & 63;
+  const int lr = lane & 15, lq = lane >> 4;
+  constexpr int NW = kSpanThreads / 64;
   const float* Kp = K + (long long)p * n * n;
   const float* sp = s + (long long)p * n;
+  const int nt = (n + 15) >> 4;
 
-  // non-finite inputs and the trace
-  double tr = 0.0;
-  int bad = 0;
-  for (int i = tid; i < n; i += kSpanThreads) {
-    tr += (double)Kp[(long long)i * n + i];
-    if (!isfinite(sp[i])) bad = 1;
-  }
-  for (int e = tid; e < n * n; e += kSpanThreads)
-    if (!isfinite(Kp[e])) bad = 1;
+  // K into the tiles (lower triangle, padded to a multiple of 16 with the
+  // identity), the finiteness of every entry of K (tile (I, J) and its
+  // mirror (J, I)) and of s, and the trace; loads with clamped addresses and
+  // masked values, two tiles' worth in flight per lane
   if (tid == 0) flag = 0;
+  double tr = 0.0;
+  bool bad = false;
+  for (int i = tid; i < n; i += kSpanThreads) bad |= !isfinite(sp[i]);
+  for (int q0 = wid; q0 < nt * (nt + 1) / 2; q0 += 2 * NW) {
+    float v[2][4], vm[2][4];
+    int I[2], J[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int q = min(q0 + h * NW, nt * (nt + 1) / 2 - 1);
+      tri_pair(q, I[h], J[h]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int e = lane + 64 * u, rr = e >> 4, c = e & 15;
+        const int i = min(16 * I[h] + rr, n - 1), j = min(16 * J[h] + c, n - 1);
+        v[h][u] = Kp[(long long)i * n + j];
+        const int im = min(16 * J[h] + rr, n - 1), jm = min(16 * I[h] + c, n - 1);
+        vm[h][u] = Kp[(long long)im * n + jm];
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (q0 + h * NW >= nt * (nt + 1) / 2) break;
+      float* T = Lt + (q0 + h * NW) * 256;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int e = lane + 64 * u, rr = e >> 4, c = e & 15;
+        const int i = 16 * I[h] + rr, j = 16 * J[h] + c;
+        const bool in = i < n && j < n;
+        const bool inm = 16 * J[h] + rr < n && 16 * I[h] + c < n;
+        bad |= (in && !isfinite(v[h][u])) || (inm && !isfinite(vm[h][u]));
+        if (in && i == j) tr += (double)v[h][u];
+        T[rperm(rr) * 16 + c] = in ? v[h][u] : (i == j ? 1.f : 0.f);
+      }
+    }
+  }
   __syncthreads();
   if (bad) flag = 1;
   tr = block_sum<kSpanThreads>(tr, scratch);
@@ -104,42 +189,115 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
     }
     return;
   }
-
-  for (int e = tid; e < n * (n + 1) / 2; e += kSpanThreads) {
-    int i = (int)((sqrtf(8.f * e + 1.f) - 1.f) * 0.5f);
-    while (tri(i + 1, 0) <= e) ++i;
-    while (tri(i, 0) > e) --i;
-    const int j = e - tri(i, 0);
-    float v = Kp[(long long)i * n + j];
-    if (i == j) v += lam;
-    Lp[e] = v;
-  }
+  for (int i = tid; i < n; i += kSpanThreads) Lt[row_at(i) + col_off(i)] += lam;
   if (tid == 0) flag = 0;
   __syncthreads();
 
-  // right-looking Cholesky, column by column
-  for (int j = 0; j < n; ++j) {
-    if (tid == 0) {
-      const float d = Lp[tri(j, j)];
-      if (!(d > 0.f))
-        flag = j + 1;
-      else
-        Lp[tri(j, j)] = sqrtf(d);
+  // right-looking blocked Cholesky, 16 columns per step, three barriers per
+  // step: wave 0 factors the diagonal tile D and inverts it in registers
+  // (lane r holds row r; the pivot and the column reach the other lanes by
+  // v_readlane); every wave then takes panel tiles L_IJ = A_IJ D^-T and
+  // trailing tiles A_IK -= L_IJ L_KJ^T, each one 16x16x16 fp32 MFMA product.
+  for (int J = 0; J < nt; ++J) {
+    if (wid == 0) {
+      float* D = Lt + tile_at(J, J) + rperm(lr) * 16;
+      float a[16];
+#pragma unroll
+      for (int m = 0; m < 16; m += 4) {
+        const float4 t = *reinterpret_cast<const float4*>(D + m);
+        a[m] = t.x;
+        a[m + 1] = t.y;
+        a[m + 2] = t.z;
+        a[m + 3] = t.w;
+      }
+#pragma unroll
+      for (int m = 0; m < 16; ++m) a[m] = m <= lr ? a[m] : 0.f;
+      float dv[16], dg[16];
+      int bad_j = 0;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        float d = readlane_f(a[j], j);
+        if (bad_j == 0 && !(d > 0.f)) bad_j = 16 * J + j + 1;
+        d = d > 0.f ? d : 1.f;
+        const float rs = rsqrt_nr(d);
+        dv[j] = rs;
+        dg[j] = d * rs;
+        const float l = lr > j ? a[j] * rs : (lr == j ? dg[j] : 0.f);
+        a[j] = l;
+        const float f = lr > j ? l : 0.f;
+#pragma unroll
+        for (int c = j + 1; c < 16; ++c) a[c] = fmaf(-f, readlane_f(a[j], c), a[c]);
+      }
+      // row r of X = D^-1 from X D = I, columns right to left
+      float xr[16];
+#pragma unroll
+      for (int c = 15; c >= 0; --c) {
+        float acc = c == lr ? 1.f : 0.f;
+#pragma unroll
+        for (int m = c + 1; m < 16; ++m) acc = fmaf(-xr[m], readlane_f(a[c], m), acc);
+        xr[c] = acc * dv[c];
+      }
+      float mine = 1.f;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) mine = lr == j ? dg[j] : mine;
+      if (lane < 16) {
+#pragma unroll
+        for (int m = 0; m < 16; m += 4) {
+          *reinterpret_cast<float4*>(D + m) =
+              make_float4(m <= lr ? a[m] : 0.f, m + 1 <= lr ? a[m + 1] : 0.f, m + 2 <= lr ? a[m + 2] : 0.f,
+                          m + 3 <= lr ? a[m + 3] : 0.f);
+          *reinterpret_cast<float4*>(&Xs[lr * 16 + m]) = make_float4(xr[m], xr[m + 1], xr[m + 2], xr[m + 3]);
+        }
+        dinv[16 * J + lr] = 1.0 / (double)mine;
+      }
+      if (lane == 0 && bad_j) flag = bad_j;
     }
     __syncthreads();
     if (flag) break;
-    const float ljj = Lp[tri(j, j)];
-    for (int i = j + 1 + tid; i < n; i += kSpanThreads) Lp[tri(i, j)] /= ljj;
+    for (int I = J + 1 + wid; I < nt; I += NW) {
+      float* A = Lt + tile_at(I, J);
+      const float4 av = *reinterpret_cast<const float4*>(&A[rperm(lr) * 16 + 4 * lq]);
+      const float4 bv = *reinterpret_cast<const float4*>(&Xs[lr * 16 + 4 * lq]);
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      acc = mma_f32(av.x, bv.x, acc);
+      acc = mma_f32(av.y, bv.y, acc);
+      acc = mma_f32(av.z, bv.z, acc);
+      acc = mma_f32(av.w, bv.w, acc);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) A[rperm(4 * lq + j) * 16 + lr] = acc[j];
+    }
     __syncthreads();
-    const int m = n - 1 - j;
-    const int cnt = m * (m + 1) / 2;
-    for (int e = tid; e < cnt; e += kSpanThreads) {
-      int rr = (int)((sqrtf(8.f * e + 1.f) - 1.f) * 0.5f);
-      while (tri(rr + 1, 0) <= e) ++rr;
-      while (tri(rr, 0) > e) --rr;
-      const int cc = e - tri(rr, 0);
-      const int i = j + 1 + rr, k = j + 1 + cc;
-      Lp[tri(i, k)] -= Lp[tri(i, j)] * Lp[tri(k, j)];
+    // trailing tiles, two per wave at a time (distinct tiles, so the loads
+    // of both are issued before either result is written)
+    const int rest = nt - 1 - J, nrest = rest * (rest + 1) / 2;
+    for (int q0 = wid; q0 < nrest; q0 += 2 * NW) {
+      float4 av[2], bv[2];
+      int C[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        int I, Kt;
+        tri_pair(min(q0 + h * NW, nrest - 1), I, Kt);
+        I += J + 1;
+        Kt += J + 1;
+        av[h] = *reinterpret_cast<const float4*>(&Lt[tile_at(I, J) + rperm(lr) * 16 + 4 * lq]);
+        bv[h] = *reinterpret_cast<const float4*>(&Lt[tile_at(Kt, J) + rperm(lr) * 16 + 4 * lq]);
+        C[h] = tile_at(I, Kt);
+      }
+      f32x4 acc[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        acc[h] = f32x4{0.f, 0.f, 0.f, 0.f};
+        acc[h] = mma_f32(av[h].x, bv[h].x, acc[h]);
+        acc[h] = mma_f32(av[h].y, bv[h].y, acc[h]);
+        acc[h] = mma_f32(av[h].z, bv[h].z, acc[h]);
+        acc[h] = mma_f32(av[h].w, bv[h].w, acc[h]);
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        if (q0 + h * NW >= nrest) break;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) Lt[C[h] + rperm(4 * lq + j) * 16 + lr] -= acc[h][j];
+      }
     }
     __syncthreads();
   }
@@ -153,43 +311,129 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
     return;
   }
 
-  // solve (L L^T) z = rhs in place (rhs in y on entry, z in y on exit)
+  // solve (L L^T) z = rhs in place (rhs in y on entry, z in y on exit) on
+  // wave 0 alone, column-oriented: lane l keeps rows l, l + 64, ... of the
+  // right-hand side in registers; at step i the finished entry is broadcast
+  // from its lane (v_readlane) and every lane subtracts its rows' multiple of
+  // column i of L (forward) or row i of L (backward).  The L entries of step
+  // i + 1 are loaded during step i, so one step costs a readlane, a multiply
+  // and an FMA on the critical path.
   auto chol_solve = [&]() {
-    for (int j = 0; j < n; ++j) {
-      if (tid == 0) y[j] /= (double)Lp[tri(j, j)];
-      __syncthreads();
-      const double yj = y[j];
-      for (int i = j + 1 + tid; i < n; i += kSpanThreads) y[i] -= (double)Lp[tri(i, j)] * yj;
-      __syncthreads();
+    if (wid == 0) {
+      constexpr int R = kSpanMaxN / 64;
+      double v[R];
+      int rb[R], co[R];
+      bool kin[R];
+#pragma unroll
+      for (int m = 0; m < R; ++m) {
+        const int k = lane + 64 * m;
+        kin[m] = k < n;
+        v[m] = kin[m] ? y[k] : 0.0;
+        rb[m] = row_at(k);
+        co[m] = col_off(k);
+      }
+#pragma unroll
+      for (int mb = 0; mb < R; ++mb) {
+        if (64 * mb >= n) break;
+        const int ie = min(64, n - 64 * mb);
+        float lc[R];
+        int ci = col_off(64 * mb);
+#pragma unroll
+        for (int m = mb; m < R; ++m) lc[m] = Lt[rb[m] + ci];
+        double dc = dinv[64 * mb];
+        for (int ii = 0; ii < ie; ++ii) {
+          const int i = 64 * mb + ii;
+          const int in = min(i + 1, n - 1);
+          ci = col_off(in);
+          float ln[R];
+#pragma unroll
+          for (int m = mb; m < R; ++m) ln[m] = Lt[rb[m] + ci];
+          const double dn = dinv[in];
+          const double zi = readlane_d(v[mb], ii) * dc;
+          v[mb] = lane == ii ? zi : v[mb];
+#pragma unroll
+          for (int m = mb; m < R; ++m) {
+            const float l = (kin[m] && (m > mb || lane > ii)) ? lc[m] : 0.f;
+            v[m] = fma(-(double)l, zi, v[m]);
+            lc[m] = ln[m];
+          }
+          dc = dn;
+        }
+      }
+#pragma unroll
+      for (int mb = R - 1; mb >= 0; --mb) {
+        if (64 * mb >= n) continue;
+        const int ie = min(64, n - 64 * mb);
+        float lc[R];
+        int ri = row_at(64 * mb + ie - 1);
+#pragma unroll
+        for (int m = 0; m <= mb; ++m) lc[m] = Lt[ri + co[m]];
+        double dc = dinv[64 * mb + ie - 1];
+        for (int ii = ie - 1; ii >= 0; --ii) {
+          const int i = 64 * mb + ii;
+          const int in = max(i - 1, 0);
+          ri = row_at(in);
+          float ln[R];
+#pragma unroll
+          for (int m = 0; m <= mb; ++m) ln[m] = Lt[ri + co[m]];
+          const double dn = dinv[in];
+          const double zi = readlane_d(v[mb], ii) * dc;
+          v[mb] = lane == ii ? zi : v[mb];
+#pragma unroll
+          for (int m = 0; m <= mb; ++m) {
+            const float l = (m < mb || lane < ii) ? lc[m] : 0.f;
+            v[m] = fma(-(double)l, zi, v[m]);
+            lc[m] = ln[m];
+          }
+          dc = dn;
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < R; ++m)
+        if (kin[m]) y[lane + 64 * m] = v[m];
     }
-    for (int j = n - 1; j >= 0; --j) {
-      if (tid == 0) y[j] /= (double)Lp[tri(j, j)];
-      __syncthreads();
-      const double yj = y[j];
-      for (int i = tid; i < j; i += kSpanThreads) y[i] -= (double)Lp[tri(j, i)] * yj;
-      __syncthreads();
+    __syncthreads();
+  };
+
+  // (K x)_i in fp64 from the fp32 K for every row: one wave per row, the
+  // lanes across the row (coalesced), all of a wave's rows loaded before
+  // the fixed-order wave reductions; f(i, (K x)_i) on lane 0
+  auto kx_rows = [&](auto&& f) {
+    constexpr int RB = 8, C4 = kSpanMaxN / 64;
+    double xv[C4];
+#pragma unroll
+    for (int c = 0; c < C4; ++c) xv[c] = lane + 64 * c < n ? x[lane + 64 * c] : 0.0;
+    for (int t0 = 0; wid + NW * t0 < n; t0 += RB) {
+      float kv[RB][C4];
+#pragma unroll
+      for (int t = 0; t < RB; ++t) {
+        const int i = min(wid + NW * (t0 + t), n - 1);
+#pragma unroll
+        for (int c = 0; c < C4; ++c) kv[t][c] = Kp[(long long)i * n + min(lane + 64 * c, n - 1)];
+      }
+#pragma unroll
+      for (int t = 0; t < RB; ++t) {
+        const int i = wid + NW * (t0 + t);
+        if (i >= n) break;
+        double acc = 0.0;
+#pragma unroll
+        for (int c = 0; c < C4; ++c) acc += (double)kv[t][c] * xv[c];
+        acc = wave_sum(acc);
+        if (lane == 0) f(i, acc);
+      }
     }
   };
 
-  for (int i = tid; i < n; i += kSpanThreads) {
-    y[i] = (double)sp[i];
-    x[i] = 0.0;
-  }
+  for (int i = tid; i < n; i += kSpanThreads) y[i] = (double)sp[i];
   __syncthreads();
   chol_solve();
   for (int i = tid; i < n; i += kSpanThreads) x[i] = y[i];
   __syncthreads();
 
-  // iterative refinement with fp64 residuals of the fp32 K
+  // two steps of iterative refinement: y = s - (K + lam I) x in fp64 from
+  // the fp32 K, solve, x += y
   for (int it = 0; it < 2; ++it) {
-    for (int i = tid; i < n; i += kSpanThreads) {
-      const float* Ki = Kp + (long long)i * n;
-      double acc = (double)sp[i] - (double)lam * x[i];
-      for (int j = 0; j < n; ++j) acc -= (double)Ki[j] * x[j];
-      r[i] = acc;
-    }
-    __syncthreads();
-    for (int i = tid; i < n; i += kSpanThreads) y[i] = r[i];
+    kx_rows([&](int i, double kx) { y[i] = (double)sp[i] - (double)lam * x[i] - kx; });
     __syncthreads();
     chol_solve();
     for (int i = tid; i < n; i += kSpanThreads) x[i] += y[i];
@@ -198,12 +442,7 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
 
   // resid2 = t2 - 2 s.x + x.K.x
   double part = 0.0;
-  for (int i = tid; i < n; i += kSpanThreads) {
-    const float* Ki = Kp + (long long)i * n;
-    double kx = 0.0;
-    for (int j = 0; j < n; ++j) kx += (double)Ki[j] * x[j];
-    part += x[i] * kx - 2.0 * (double)sp[i] * x[i];
-  }
+  kx_rows([&](int i, double kx) { part += x[i] * kx - 2.0 * (double)sp[i] * x[i]; });
   const double q = block_sum<kSpanThreads>(part, scratch);
   for (int i = tid; i < n; i += kSpanThreads) w[(long long)p * n + i] = (float)x[i];
   if (tid == 0) {
@@ -350,16 +589,6 @@ __global__ __launch_bounds__(kConeThreads) void cone_pg_kernel(const float* K, c
 // Single-wave solvers for n <= 64 (one 64-lane wave per group, lane i owns
 // row i, everything in fp64 on the exact fp32 inputs; no block barriers).
 
-constexpr int kWaveN = 64;
-
-__device__ __forceinline__ double wave_sum(double v) {
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
-}
-__device__ __forceinline__ double wave_max(double v) {
-  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
-  return v;
-}
 
 typedef __attribute__((ext_vector_type(2))) double f64x2;
 
@@ -374,13 +603,6 @@ __device__ __forceinline__ double quad_sum(double v) {
   o = __hiloint2double(__builtin_amdgcn_mov_dpp(hi, 0x4E, 0xF, 0xF, false),
                        __builtin_amdgcn_mov_dpp(lo, 0x4E, 0xF, 0xF, false));
   return v + o;
-}
-
-// value of lane src (src uniform) as a scalar broadcast
-__device__ __forceinline__ double readlane_d(double v, int src) {
-  const int lo = __builtin_amdgcn_readlane(__double2loint(v), src);
-  const int hi = __builtin_amdgcn_readlane(__double2hiint(v), src);
-  return __hiloint2double(hi, lo);
 }
 
 // Cholesky of K + lam I in fp64: lane i keeps row i of the factor in
