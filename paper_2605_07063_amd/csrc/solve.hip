@@ -9,8 +9,9 @@
 // in LDS as 16 x 16 fp32 tiles (at most 136 KiB) and factored right-looking
 // in 16-column steps by the whole workgroup (a one-wave register factor of
 // the diagonal tile, then fp32 MFMA tile products); forward / back substitution
-// run on fp64 vectors held in the registers of one wave (column-oriented,
-// one lane broadcast per step, no block barrier); two steps of iterative
+// run in fp32 on vectors held in the registers of one wave, 16 rows at a time
+// through the stored inverses of the diagonal tiles (v_readlane broadcasts,
+// no block barrier); two steps of iterative
 // refinement recompute s - (K + lam_eff I) w in fp64 from the fp32 K read
 // from global memory (one wave per row), which brings the solution to
 // fp64-level accuracy whenever cond(K + lam_eff I) * 2^-24 < 1.
@@ -80,6 +81,25 @@ __device__ __forceinline__ double wave_max(double v) {
   for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
   return v;
 }
+// fixed-order wave sum by DPP moves (no LDS round trips); the total is
+// exact in lane 63 only: pairs, quads (quad_perm), halves of a row
+// (row_half_mirror), rows (row_mirror), then row_bcast15 / row_bcast31
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_d(double v) {
+  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), CTRL, ROWS, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, ROWS, 0xF, false);
+  return __hiloint2double(hi, lo);
+}
+__device__ __forceinline__ double wave_sum_l63(double v) {
+  v += dpp_d<0xB1, 0xF>(v);    // quad_perm [1, 0, 3, 2]
+  v += dpp_d<0x4E, 0xF>(v);    // quad_perm [2, 3, 0, 1]
+  v += dpp_d<0x141, 0xF>(v);   // row_half_mirror
+  v += dpp_d<0x140, 0xF>(v);   // row_mirror
+  v += dpp_d<0x142, 0xA>(v);   // row_bcast15 into rows 1 and 3
+  v += dpp_d<0x143, 0xC>(v);   // row_bcast31 into rows 2 and 3
+  return v;
+}
+
 // value of lane src (src uniform) as a scalar broadcast
 __device__ __forceinline__ double readlane_d(double v, int src) {
   const int lo = __builtin_amdgcn_readlane(__double2loint(v), src);
@@ -121,8 +141,8 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
                                                                   int n, float lambda, int mode, float* w,
                                                                   float* lam_eff_out, float* resid2, int* info) {
   __shared__ __attribute__((aligned(16))) float Lt[kSpanTiles * (kSpanTiles + 1) / 2 * 256];
-  __shared__ __attribute__((aligned(16))) float Xs[256];
-  __shared__ double x[kSpanMaxN], y[kSpanMaxN], dinv[kSpanMaxN];
+  __shared__ __attribute__((aligned(16))) float Xt[kSpanTiles * 256];   // inverses of the diagonal tiles
+  __shared__ double x[kSpanMaxN], y[kSpanMaxN];
   __shared__ double scratch[kSpanThreads / 64 + 1];
   __shared__ int flag;
   const int p = blockIdx.x, tid = threadIdx.x;
@@ -136,16 +156,17 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
   // K into the tiles (lower triangle, padded to a multiple of 16 with the
   // identity), the finiteness of every entry of K (tile (I, J) and its
   // mirror (J, I)) and of s, and the trace; loads with clamped addresses and
-  // masked values, two tiles' worth in flight per lane
+  // masked values, four tiles' worth in flight per lane
   if (tid == 0) flag = 0;
   double tr = 0.0;
   bool bad = false;
   for (int i = tid; i < n; i += kSpanThreads) bad |= !isfinite(sp[i]);
-  for (int q0 = wid; q0 < nt * (nt + 1) / 2; q0 += 2 * NW) {
-    float v[2][4], vm[2][4];
-    int I[2], J[2];
+  constexpr int LB = 4;
+  for (int q0 = wid; q0 < nt * (nt + 1) / 2; q0 += LB * NW) {
+    float v[LB][4], vm[LB][4];
+    int I[LB], J[LB];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < LB; ++h) {
       const int q = min(q0 + h * NW, nt * (nt + 1) / 2 - 1);
       tri_pair(q, I[h], J[h]);
 #pragma unroll
@@ -158,7 +179,7 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
       }
     }
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < LB; ++h) {
       if (q0 + h * NW >= nt * (nt + 1) / 2) break;
       float* T = Lt + (q0 + h * NW) * 256;
 #pragma unroll
@@ -193,71 +214,93 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
   if (tid == 0) flag = 0;
   __syncthreads();
 
-  // right-looking blocked Cholesky, 16 columns per step, three barriers per
-  // step: wave 0 factors the diagonal tile D and inverts it in registers
-  // (lane r holds row r; the pivot and the column reach the other lanes by
-  // v_readlane); every wave then takes panel tiles L_IJ = A_IJ D^-T and
-  // trailing tiles A_IK -= L_IJ L_KJ^T, each one 16x16x16 fp32 MFMA product.
-  for (int J = 0; J < nt; ++J) {
-    if (wid == 0) {
-      float* D = Lt + tile_at(J, J) + rperm(lr) * 16;
-      float a[16];
+  // right-looking blocked Cholesky, 16 columns per step.  The diagonal tile
+  // D_J is factored and inverted in registers by wave 0 alone (lane r holds
+  // row r; the pivot and the column reach the other lanes by v_readlane),
+  // one step ahead: while waves 1.. take the trailing tiles of step J, wave 0
+  // updates tile (J+1, J+1) first and factors it.  Per step, two barriers:
+  // panel tiles L_IJ = A_IJ D_J^-T, then trailing tiles A_IK -= L_IJ L_KJ^T,
+  // each one 16x16x16 fp32 MFMA product.
+  auto factor_diag = [&](int J) {
+    float* D = Lt + tile_at(J, J) + rperm(lr) * 16;
+    float a[16];
+#pragma unroll
+    for (int m = 0; m < 16; m += 4) {
+      const float4 t = *reinterpret_cast<const float4*>(D + m);
+      a[m] = t.x;
+      a[m + 1] = t.y;
+      a[m + 2] = t.z;
+      a[m + 3] = t.w;
+    }
+    // per-lane predicates as 0 / 1 floats (products instead of selects
+    // keep them out of SGPR pairs); K is finite here, so the entries above
+    // the diagonal can be cleared by a product
+    auto gt = [&](int j) { return (float)((unsigned)(j - lr) >> 31); };   // 1 if lr > j
+    auto eq = [&](int j) { return gt(j - 1) - gt(j); };                  // 1 if lr == j
+#pragma unroll
+    for (int m = 0; m < 16; ++m) a[m] *= gt(m - 1);
+    float dv[16], dg[16];
+    int bad_j = 0;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      float d = readlane_f(a[j], j);
+      if (bad_j == 0 && !(d > 0.f)) bad_j = 16 * J + j + 1;
+      d = d > 0.f ? d : 1.f;
+      const float rs = rsqrt_nr(d);
+      dv[j] = rs;
+      dg[j] = d * rs;
+      const float f = gt(j) * (a[j] * rs);   // L[r][j] below the diagonal, 0 on and above it
+      a[j] = f;
+#pragma unroll
+      for (int c = j + 1; c < 16; ++c) a[c] = fmaf(-f, readlane_f(a[j], c), a[c]);
+    }
+    // row r of X = D^-1 from X D = I, columns right to left (X is lower
+    // triangular: the entries right of the diagonal come out exactly 0)
+    float xr[16];
+#pragma unroll
+    for (int c = 15; c >= 0; --c) {
+      float acc = eq(c);
+#pragma unroll
+      for (int m = c + 1; m < 16; ++m) acc = fmaf(-xr[m], readlane_f(a[c], m), acc);
+      xr[c] = acc * dv[c];
+    }
+    float mine = 0.f;   // this row's diagonal entry of L
+#pragma unroll
+    for (int j = 0; j < 16; ++j) mine = fmaf(eq(j), dg[j], mine);
+    if (lane < 16) {
 #pragma unroll
       for (int m = 0; m < 16; m += 4) {
-        const float4 t = *reinterpret_cast<const float4*>(D + m);
-        a[m] = t.x;
-        a[m + 1] = t.y;
-        a[m + 2] = t.z;
-        a[m + 3] = t.w;
+        float4 t;
+        t.x = fmaf(a[m], gt(m), eq(m) * mine);
+        t.y = fmaf(a[m + 1], gt(m + 1), eq(m + 1) * mine);
+        t.z = fmaf(a[m + 2], gt(m + 2), eq(m + 2) * mine);
+        t.w = fmaf(a[m + 3], gt(m + 3), eq(m + 3) * mine);
+        *reinterpret_cast<float4*>(D + m) = t;
+        *reinterpret_cast<float4*>(&Xt[J * 256 + lr * 16 + m]) = make_float4(xr[m], xr[m + 1], xr[m + 2], xr[m + 3]);
       }
-#pragma unroll
-      for (int m = 0; m < 16; ++m) a[m] = m <= lr ? a[m] : 0.f;
-      float dv[16], dg[16];
-      int bad_j = 0;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        float d = readlane_f(a[j], j);
-        if (bad_j == 0 && !(d > 0.f)) bad_j = 16 * J + j + 1;
-        d = d > 0.f ? d : 1.f;
-        const float rs = rsqrt_nr(d);
-        dv[j] = rs;
-        dg[j] = d * rs;
-        const float l = lr > j ? a[j] * rs : (lr == j ? dg[j] : 0.f);
-        a[j] = l;
-        const float f = lr > j ? l : 0.f;
-#pragma unroll
-        for (int c = j + 1; c < 16; ++c) a[c] = fmaf(-f, readlane_f(a[j], c), a[c]);
-      }
-      // row r of X = D^-1 from X D = I, columns right to left
-      float xr[16];
-#pragma unroll
-      for (int c = 15; c >= 0; --c) {
-        float acc = c == lr ? 1.f : 0.f;
-#pragma unroll
-        for (int m = c + 1; m < 16; ++m) acc = fmaf(-xr[m], readlane_f(a[c], m), acc);
-        xr[c] = acc * dv[c];
-      }
-      float mine = 1.f;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) mine = lr == j ? dg[j] : mine;
-      if (lane < 16) {
-#pragma unroll
-        for (int m = 0; m < 16; m += 4) {
-          *reinterpret_cast<float4*>(D + m) =
-              make_float4(m <= lr ? a[m] : 0.f, m + 1 <= lr ? a[m + 1] : 0.f, m + 2 <= lr ? a[m + 2] : 0.f,
-                          m + 3 <= lr ? a[m + 3] : 0.f);
-          *reinterpret_cast<float4*>(&Xs[lr * 16 + m]) = make_float4(xr[m], xr[m + 1], xr[m + 2], xr[m + 3]);
-        }
-        dinv[16 * J + lr] = 1.0 / (double)mine;
-      }
-      if (lane == 0 && bad_j) flag = bad_j;
     }
-    __syncthreads();
+    if (lane == 0 && bad_j) flag = bad_j;
+  };
+  auto trail_tile = [&](int J, int I, int Kt) {
+    const float4 av = *reinterpret_cast<const float4*>(&Lt[tile_at(I, J) + rperm(lr) * 16 + 4 * lq]);
+    const float4 bv = *reinterpret_cast<const float4*>(&Lt[tile_at(Kt, J) + rperm(lr) * 16 + 4 * lq]);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    acc = mma_f32(av.x, bv.x, acc);
+    acc = mma_f32(av.y, bv.y, acc);
+    acc = mma_f32(av.z, bv.z, acc);
+    acc = mma_f32(av.w, bv.w, acc);
+    float* C = Lt + tile_at(I, Kt);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) C[rperm(4 * lq + j) * 16 + lr] -= acc[j];
+  };
+  if (wid == 0) factor_diag(0);
+  __syncthreads();
+  for (int J = 0; J < nt; ++J) {
     if (flag) break;
     for (int I = J + 1 + wid; I < nt; I += NW) {
       float* A = Lt + tile_at(I, J);
       const float4 av = *reinterpret_cast<const float4*>(&A[rperm(lr) * 16 + 4 * lq]);
-      const float4 bv = *reinterpret_cast<const float4*>(&Xs[lr * 16 + 4 * lq]);
+      const float4 bv = *reinterpret_cast<const float4*>(&Xt[J * 256 + lr * 16 + 4 * lq]);
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
       acc = mma_f32(av.x, bv.x, acc);
       acc = mma_f32(av.y, bv.y, acc);
@@ -267,36 +310,44 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
       for (int j = 0; j < 4; ++j) A[rperm(4 * lq + j) * 16 + lr] = acc[j];
     }
     __syncthreads();
-    // trailing tiles, two per wave at a time (distinct tiles, so the loads
-    // of both are issued before either result is written)
     const int rest = nt - 1 - J, nrest = rest * (rest + 1) / 2;
-    for (int q0 = wid; q0 < nrest; q0 += 2 * NW) {
-      float4 av[2], bv[2];
-      int C[2];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        int I, Kt;
-        tri_pair(min(q0 + h * NW, nrest - 1), I, Kt);
-        I += J + 1;
-        Kt += J + 1;
-        av[h] = *reinterpret_cast<const float4*>(&Lt[tile_at(I, J) + rperm(lr) * 16 + 4 * lq]);
-        bv[h] = *reinterpret_cast<const float4*>(&Lt[tile_at(Kt, J) + rperm(lr) * 16 + 4 * lq]);
-        C[h] = tile_at(I, Kt);
+    if (wid == 0) {
+      if (rest > 0) {   // tile (J+1, J+1) is trailing tile 0
+        trail_tile(J, J + 1, J + 1);
+        factor_diag(J + 1);
       }
-      f32x4 acc[2];
+    } else {
+      // the other trailing tiles over waves 1.., two per wave at a time
+      // (distinct tiles, so the loads of both are issued before either
+      // result is written)
+      for (int q0 = wid; q0 < nrest; q0 += 2 * (NW - 1)) {
+        float4 av[2], bv[2];
+        int C[2];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        acc[h] = f32x4{0.f, 0.f, 0.f, 0.f};
-        acc[h] = mma_f32(av[h].x, bv[h].x, acc[h]);
-        acc[h] = mma_f32(av[h].y, bv[h].y, acc[h]);
-        acc[h] = mma_f32(av[h].z, bv[h].z, acc[h]);
-        acc[h] = mma_f32(av[h].w, bv[h].w, acc[h]);
-      }
+        for (int h = 0; h < 2; ++h) {
+          int I, Kt;
+          tri_pair(min(q0 + h * (NW - 1), nrest - 1), I, Kt);
+          I += J + 1;
+          Kt += J + 1;
+          av[h] = *reinterpret_cast<const float4*>(&Lt[tile_at(I, J) + rperm(lr) * 16 + 4 * lq]);
+          bv[h] = *reinterpret_cast<const float4*>(&Lt[tile_at(Kt, J) + rperm(lr) * 16 + 4 * lq]);
+          C[h] = tile_at(I, Kt);
+        }
+        f32x4 acc[2];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        if (q0 + h * NW >= nrest) break;
+        for (int h = 0; h < 2; ++h) {
+          acc[h] = f32x4{0.f, 0.f, 0.f, 0.f};
+          acc[h] = mma_f32(av[h].x, bv[h].x, acc[h]);
+          acc[h] = mma_f32(av[h].y, bv[h].y, acc[h]);
+          acc[h] = mma_f32(av[h].z, bv[h].z, acc[h]);
+          acc[h] = mma_f32(av[h].w, bv[h].w, acc[h]);
+        }
 #pragma unroll
-        for (int j = 0; j < 4; ++j) Lt[C[h] + rperm(4 * lq + j) * 16 + lr] -= acc[h][j];
+        for (int h = 0; h < 2; ++h) {
+          if (q0 + h * (NW - 1) >= nrest) break;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) Lt[C[h] + rperm(4 * lq + j) * 16 + lr] -= acc[h][j];
+        }
       }
     }
     __syncthreads();
@@ -312,92 +363,101 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
   }
 
   // solve (L L^T) z = rhs in place (rhs in y on entry, z in y on exit) on
-  // wave 0 alone, column-oriented: lane l keeps rows l, l + 64, ... of the
-  // right-hand side in registers; at step i the finished entry is broadcast
-  // from its lane (v_readlane) and every lane subtracts its rows' multiple of
-  // column i of L (forward) or row i of L (backward).  The L entries of step
-  // i + 1 are loaded during step i, so one step costs a readlane, a multiply
-  // and an FMA on the critical path.
+  // wave 0 alone, in fp32 (the factor's precision; the refinement recovers
+  // the rest), by 16-row blocks: lane l keeps rows l, l + 64, ... of the
+  // right-hand side in registers.  Block J takes its 16 entries from their
+  // lanes by v_readlane, applies the stored inverse of the diagonal tile
+  // (X_J forward, X_J^T backward) on the 16 lanes that own the block, and
+  // broadcasts the result the same way; every lane then subtracts its rows'
+  // share of block column J of L (forward: rows below the block) or block
+  // row J (backward: rows above it).  Rows past n hold values that are never
+  // broadcast or stored (the identity padding keeps those of the last block
+  // at exactly 0).
   auto chol_solve = [&]() {
     if (wid == 0) {
       constexpr int R = kSpanMaxN / 64;
-      double v[R];
-      int rb[R], co[R];
-      bool kin[R];
+      const int kb = lane >> 4, kc = lane & 15;   // lane's 16-row group and row within it
+      float v[R];
 #pragma unroll
-      for (int m = 0; m < R; ++m) {
-        const int k = lane + 64 * m;
-        kin[m] = k < n;
-        v[m] = kin[m] ? y[k] : 0.0;
-        rb[m] = row_at(k);
-        co[m] = col_off(k);
-      }
+      for (int m = 0; m < R; ++m) v[m] = lane + 64 * m < n ? (float)y[lane + 64 * m] : 0.f;
 #pragma unroll
       for (int mb = 0; mb < R; ++mb) {
-        if (64 * mb >= n) break;
-        const int ie = min(64, n - 64 * mb);
-        float lc[R];
-        int ci = col_off(64 * mb);
+#pragma unroll 1
+        for (int jj = 0; jj < 4; ++jj) {
+          const int J = 4 * mb + jj;
+          if (J >= nt) break;
+          float xrow[16];   // row kc of X_J
 #pragma unroll
-        for (int m = mb; m < R; ++m) lc[m] = Lt[rb[m] + ci];
-        double dc = dinv[64 * mb];
-        for (int ii = 0; ii < ie; ++ii) {
-          const int i = 64 * mb + ii;
-          const int in = min(i + 1, n - 1);
-          ci = col_off(in);
-          float ln[R];
+          for (int c = 0; c < 16; c += 4) {
+            const float4 t4 = *reinterpret_cast<const float4*>(&Xt[J * 256 + kc * 16 + c]);
+            xrow[c] = t4.x;
+            xrow[c + 1] = t4.y;
+            xrow[c + 2] = t4.z;
+            xrow[c + 3] = t4.w;
+          }
+          float acc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int m = mb; m < R; ++m) ln[m] = Lt[rb[m] + ci];
-          const double dn = dinv[in];
-          const double zi = readlane_d(v[mb], ii) * dc;
-          v[mb] = lane == ii ? zi : v[mb];
+          for (int c = 0; c < 16; ++c) acc[c & 3] = fmaf(xrow[c], readlane_f(v[mb], 16 * jj + c), acc[c & 3]);
+          v[mb] = kb == jj ? (acc[0] + acc[1]) + (acc[2] + acc[3]) : v[mb];
+          float yb[16];
+#pragma unroll
+          for (int c = 0; c < 16; ++c) yb[c] = readlane_f(v[mb], 16 * jj + c);
 #pragma unroll
           for (int m = mb; m < R; ++m) {
-            const float l = (kin[m] && (m > mb || lane > ii)) ? lc[m] : 0.f;
-            v[m] = fma(-(double)l, zi, v[m]);
-            lc[m] = ln[m];
+            const int k = lane + 64 * m;
+            if (64 * m + 63 < 16 * J + 16) continue;   // no row of this register lies below the block
+            const float* Lr = Lt + row_at(k) + J * 256;   // row k of tile (k / 16, J)
+            float d[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c = 0; c < 16; c += 4) {
+              const float4 l4 = *reinterpret_cast<const float4*>(Lr + c);
+              d[0] = fmaf(l4.x, yb[c], d[0]);
+              d[1] = fmaf(l4.y, yb[c + 1], d[1]);
+              d[2] = fmaf(l4.z, yb[c + 2], d[2]);
+              d[3] = fmaf(l4.w, yb[c + 3], d[3]);
+            }
+            v[m] = (k >> 4) > J ? v[m] - ((d[0] + d[1]) + (d[2] + d[3])) : v[m];
           }
-          dc = dn;
         }
       }
 #pragma unroll
       for (int mb = R - 1; mb >= 0; --mb) {
-        if (64 * mb >= n) continue;
-        const int ie = min(64, n - 64 * mb);
-        float lc[R];
-        int ri = row_at(64 * mb + ie - 1);
+#pragma unroll 1
+        for (int jj = 3; jj >= 0; --jj) {
+          const int J = 4 * mb + jj;
+          if (J >= nt) continue;
+          float xcol[16];   // column kc of X_J
 #pragma unroll
-        for (int m = 0; m <= mb; ++m) lc[m] = Lt[ri + co[m]];
-        double dc = dinv[64 * mb + ie - 1];
-        for (int ii = ie - 1; ii >= 0; --ii) {
-          const int i = 64 * mb + ii;
-          const int in = max(i - 1, 0);
-          ri = row_at(in);
-          float ln[R];
+          for (int c = 0; c < 16; ++c) xcol[c] = Xt[J * 256 + c * 16 + kc];
+          float acc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int m = 0; m <= mb; ++m) ln[m] = Lt[ri + co[m]];
-          const double dn = dinv[in];
-          const double zi = readlane_d(v[mb], ii) * dc;
-          v[mb] = lane == ii ? zi : v[mb];
+          for (int c = 0; c < 16; ++c) acc[c & 3] = fmaf(xcol[c], readlane_f(v[mb], 16 * jj + c), acc[c & 3]);
+          v[mb] = kb == jj ? (acc[0] + acc[1]) + (acc[2] + acc[3]) : v[mb];
+          float zb[16];
+#pragma unroll
+          for (int c = 0; c < 16; ++c) zb[c] = readlane_f(v[mb], 16 * jj + c);
 #pragma unroll
           for (int m = 0; m <= mb; ++m) {
-            const float l = (m < mb || lane < ii) ? lc[m] : 0.f;
-            v[m] = fma(-(double)l, zi, v[m]);
-            lc[m] = ln[m];
+            const int k = lane + 64 * m;
+            if (64 * m >= 16 * J) continue;   // no row of this register lies above the block
+            const float* Lc = Lt + tile_at(J, min(k >> 4, J)) + (k & 15);   // column k of block row J
+            float d[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c = 0; c < 16; ++c) d[c & 3] = fmaf(Lc[rperm(c) * 16], zb[c], d[c & 3]);
+            v[m] = (k >> 4) < J ? v[m] - ((d[0] + d[1]) + (d[2] + d[3])) : v[m];
           }
-          dc = dn;
         }
       }
 #pragma unroll
       for (int m = 0; m < R; ++m)
-        if (kin[m]) y[lane + 64 * m] = v[m];
+        if (lane + 64 * m < n) y[lane + 64 * m] = (double)v[m];
     }
     __syncthreads();
   };
 
   // (K x)_i in fp64 from the fp32 K for every row: one wave per row, the
   // lanes across the row (coalesced), all of a wave's rows loaded before
-  // the fixed-order wave reductions; f(i, (K x)_i) on lane 0
+  // the fixed-order wave reductions; f(i, (K x)_i) on lane 63
   auto kx_rows = [&](auto&& f) {
     constexpr int RB = 8, C4 = kSpanMaxN / 64;
     double xv[C4];
@@ -418,8 +478,8 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
         double acc = 0.0;
 #pragma unroll
         for (int c = 0; c < C4; ++c) acc += (double)kv[t][c] * xv[c];
-        acc = wave_sum(acc);
-        if (lane == 0) f(i, acc);
+        acc = wave_sum_l63(acc);
+        if (lane == 63) f(i, acc);
       }
     }
   };
