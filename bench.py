@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle's sketch sample")
     ap.add_argument("--no-gram-dominated", action="store_true",
                     help="skip the Gram-dominated stage timings (16384 x 8192 Gram, span, top-1024)")
+    ap.add_argument("--no-scale-configs", action="store_true",
+                    help="skip the Llama-shaped block and long-context sketch timings")
     ap.add_argument("--gram-dominated-only", action="store_true",
                     help="time only the Gram-dominated stages and print their JSON object (for profiling)")
     ap.add_argument("--no-next-rows", action="store_true",
@@ -245,6 +247,8 @@ def main():
         out["next_rows"] = time_next_rows(api, layers, lens, n, T, wt, wc, goff, dev, K=K, s=s)
     if not args.no_gram_dominated:
         out["gram_dominated"] = time_gram_dominated(api, _lib, workloads, dev)
+    if not args.no_scale_configs:
+        out.update(time_scale_configs(api, _lib, workloads, dev))
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layers, lens, S, K, s, t2, n, m, k_top, lam, cfg, args.cpu_seconds, goff)
@@ -404,13 +408,121 @@ def time_gram_dominated(api, _lib, workloads, dev, reps=3):
     }
 
 
+def _sketch_bytes(layers, lens, N, ktot):
+    """Algorithmic bytes of one sketch call: the valid tokens' x and dy rows,
+    the projectors and the fp32 sketch output."""
+    tok = int(lens.sum())
+    b = sum(tok * (L["x"].shape[2] + L["dy"].shape[2]) * L["x"].element_size()
+            + (L["p_in"].numel() + L["p_out"].numel()) * L["p_in"].element_size() for L in layers)
+    return b + N * ktot * 4
+
+
+def time_scale_configs(api, _lib, workloads, dev, reps=3):
+    """The two largest workloads, timed on their own (not part of `value`):
+    * llama_block: one full Llama-3-8B-shaped block (q, k, v, o, gate, up,
+      down; 256 + 16 examples x 1024 tokens, bf16, 32 x 32 sketches) -- the
+      whole step streams 32 such blocks (46 GB each, 1.46 TB in all, more
+      than the HBM holds), so the step's sketch time is 32 block calls; the
+      Gram, span (lambda = 0) and top-64 run on a [272, 229376] fp32 sketch
+      matrix of random N(0, 1) entries (their cost does not depend on the
+      values);
+    * long_context: the whole long-context workload (16 layers 4096 x 4096,
+      32 + 4 examples x 4096 tokens, Student-t(3) activations, 30% of the
+      examples padded), sketch, Gram and the cone to a KKT residual of 1e-6."""
+    import torch
+    res = {}
+    # Llama-shaped block
+    cfg = workloads.CONFIGS["llama"]
+    n, m, T = cfg["n"], cfg["m"], cfg["T"]
+    N = n + m
+    layers, lens, kb = workloads.sketch_inputs(cfg, dev, layers=range(7))
+    Sb = torch.empty(N, kb, device=dev)
+    ws = torch.empty(max(1, api.dr_sketch_workspace_size(layers, N, T, torch.bfloat16)), dtype=torch.uint8, device=dev)
+    ms = _event_ms(lambda: api.dr_sketch_grads(layers, N, T, lens, Sb, workspace=ws), reps)
+    by = _sketch_bytes(layers, lens, N, kb)
+    del layers, Sb, ws
+    torch.cuda.empty_cache()
+    ktot = 32 * kb
+    S = torch.randn(N, ktot, device=dev)
+    G, Gt = S[:n], S[n:]
+    K = torch.empty(1, n, n, device=dev)
+    sc = torch.empty(1, n, device=dev)
+    t2 = torch.empty(1, device=dev)
+    gws = torch.empty(max(1, api.dr_gram_workspace_size(n, m, [0, ktot], torch.float32)), dtype=torch.uint8, device=dev)
+    gram_ms = _event_ms(lambda: api.dr_gram(G, Gt, [0, ktot], K, sc, t2, workspace=gws), reps)
+    w = torch.empty(1, n, device=dev)
+    le = torch.empty(1, device=dev)
+    r2 = torch.empty(1, device=dev)
+    info = torch.empty(1, dtype=torch.int32, device=dev)
+    span_ms = _event_ms(lambda: api.dr_project_span(K, sc, t2, 0.0, _lib.DR_RIDGE_ABS, w, le, r2, info), 10 * reps)
+    idx = torch.empty(1, cfg["topk"], dtype=torch.int32, device=dev)
+    wt = torch.empty(1, n, device=dev)
+    it = torch.empty(1, dtype=torch.int32, device=dev)
+    topk_ms = _event_ms(lambda: api.dr_select_topk(sc, cfg["topk"], idx, wt, it), 10 * reps)
+    if int(info[0]) != 0 or int(it[0]) != 0:
+        raise RuntimeError("Llama-shaped projection reported a non-zero info code")
+    step_sketch_ms = 32 * ms
+    res["llama_block"] = {
+        "workload": "Llama-3-8B-shaped: one block of 7 maps (q 4096->4096, k/v 4096->1024, o 4096->4096, "
+                    "gate/up 4096->14336, down 14336->4096), 256 + 16 examples x 1024 tokens, bf16 N(0, 0.02^2), "
+                    "32x32 sketches; the step is 32 such blocks",
+        "block_sketch_ms": ms,
+        "sketch_roofline": {"bound": "hbm", "achieved": by / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                            "frac": by / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": by},
+        "step_sketch_ms": step_sketch_ms,
+        "sketched_grads_per_s": N / (step_sketch_ms * 1e-3),
+        "gram_ms": gram_ms, "span_ms": span_ms, "topk_ms": topk_ms,
+        "projection_steps_per_s": 1e3 / (gram_ms + span_ms + topk_ms),
+    }
+    del S, G, Gt, K, gws
+    torch.cuda.empty_cache()
+    # long context
+    cfg = workloads.CONFIGS["long"]
+    n, m, T = cfg["n"], cfg["m"], cfg["T"]
+    N = n + m
+    layers, lens, ktot = workloads.sketch_inputs(cfg, dev)
+    S = torch.empty(N, ktot, device=dev)
+    ws = torch.empty(max(1, api.dr_sketch_workspace_size(layers, N, T, torch.bfloat16)), dtype=torch.uint8, device=dev)
+    ms = _event_ms(lambda: api.dr_sketch_grads(layers, N, T, lens, S, workspace=ws), reps)
+    by = _sketch_bytes(layers, lens, N, ktot)
+    G, Gt = S[:n], S[n:]
+    K = torch.empty(1, n, n, device=dev)
+    sc = torch.empty(1, n, device=dev)
+    t2 = torch.empty(1, device=dev)
+    gws = torch.empty(max(1, api.dr_gram_workspace_size(n, m, [0, ktot], torch.float32)), dtype=torch.uint8, device=dev)
+    gram_ms = _event_ms(lambda: api.dr_gram(G, Gt, [0, ktot], K, sc, t2, workspace=gws), reps)
+    w = torch.empty(1, n, device=dev)
+    r2 = torch.empty(1, device=dev)
+    its = torch.empty(1, dtype=torch.int32, device=dev)
+    kkt = torch.empty(1, device=dev)
+    info = torch.empty(1, dtype=torch.int32, device=dev)
+    cone_ms = _event_ms(lambda: api.dr_project_cone(K, sc, t2, 10000, cfg["kkt_tol"], w, r2, its, kkt, info),
+                        10 * reps)
+    if int(info[0]) != 0:
+        raise RuntimeError("long-context cone reported a non-zero info code")
+    res["long_context"] = {
+        "workload": "long-context: 16 layers 4096x4096, 32 + 4 examples x 4096 tokens, bf16 Student-t(3) "
+                    "activations at unit variance, 30% of the examples padded to random lengths >= 256, 64x64 "
+                    "sketches, cone to KKT 1e-6",
+        "sketch_ms": ms, "valid_tokens": int(lens.sum()),
+        "sketch_roofline": {"bound": "hbm", "achieved": by / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                            "frac": by / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": by},
+        "sketched_grads_per_s": N / (ms * 1e-3),
+        "gram_ms": gram_ms, "cone_ms": cone_ms, "cone_steps": int(its[0]), "cone_kkt": float(kkt[0]),
+        "projection_steps_per_s": 1e3 / (gram_ms + cone_ms),
+    }
+    del layers, S, G, Gt, K, ws, gws
+    torch.cuda.empty_cache()
+    return res
+
+
 SKETCH_SOURCES = ["paper_2605_07063_amd/csrc/sketch.hip", "paper_2605_07063_amd/csrc/common.h"]
 SKETCH_KERNELS = ("sketch_plan_kernel", "sketch_packed_kernel", "sketch_packed_reduce_kernel")
 KT_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d prof_out/kt -o small -- "
-          "python -u bench.py --steps 50 --warmup 10 --no-cpu-baseline")
+          "python -u bench.py --steps 50 --warmup 10 --no-cpu-baseline --no-scale-configs")
 PMC_CMD = ("rocprofv3 --pmc {c} --output-format csv -d prof_out/{d} -o small -- "
            "python -u bench.py --steps 5 --warmup 2 --no-cpu-baseline --no-next-rows --no-gram-dominated "
-           "--copy-calibration")
+           "--no-scale-configs --copy-calibration")
 SUM_CMD = "python bench.py --summarize-profiles prof_out/kt prof_out/fetch prof_out/write"
 GD_KT_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d prof_out/gd -o gd -- "
              "python -u bench.py --gram-dominated-only")
