@@ -16,13 +16,16 @@
 //
 // Per 128-column panel k:
 //   lg_potrf_kernel  one workgroup factors and inverts the diagonal block
-//                    in 16-column steps: one wave factors and inverts each
-//                    16x16 diagonal sub-block in registers (v_readlane
-//                    broadcasts, no barrier per pivot); the sub-panel solve,
-//                    the trailing update and the off-diagonal blocks of the
-//                    inverse are fp32 MFMA products in LDS.
+//                    in 16-column steps on packed 16x16 LDS tiles: one wave
+//                    factors and inverts each 16x16 diagonal tile in
+//                    registers (v_readlane broadcasts, no barrier per
+//                    pivot), one step ahead of the others; the panel solve,
+//                    the trailing update and the off-diagonal tiles of the
+//                    inverse are fp32 MFMA products.
 //   lg_trsm_kernel   L21 = A21 L11^-T as an fp32 MFMA product with the
 //                    inverse, 64 rows per workgroup.
+// Both keep their LDS under 96 KiB, so either fits on a CU beside one
+// trailing-update workgroup while the update runs.
 //   lg_syrk_kernel   A22 -= L21 L21^T on 128x128 lower-triangle tiles, fp32
 //                    MFMA, the panel slices streamed through LDS in chunks.
 // Panels go in pairs: the trailing matrix takes one rank-256 update per
@@ -214,57 +217,7 @@ __device__ __forceinline__ float readlane_f(float v, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
 }
 
-// Factor and invert the kb x kb diagonal block at (k, k) (kb <= 128; the
-// block is padded to 128 with the identity), blocked by PB-column steps:
-//   one wave factors the PB x PB diagonal sub-block D and inverts it in
-//   registers (lane r holds row r; the pivot row and column reach the
-//   other lanes by v_readlane, so no barrier inside);
-//   the sub-panel below becomes A D^-T and the trailing sub-matrix takes
-//   its rank-PB update, both as fp32 MFMA products over the four waves;
-// then the off-diagonal PB-blocks of the inverse follow by block distance
-// from the diagonal, X_ij = -X_ii sum_{m=j}^{i-1} L_im X_mj.
-constexpr int LDA = NB + 4;   // LDS row stride (floats) of the block and of its inverse
-
-template <int PB>
-__device__ void potrf_base(float* As, float* Xs, int c0, int lane, int& bad) {
-  const int r = lane % PB;
-  float a[PB];
-  const float* src = As + (c0 + r) * LDA + c0;
-#pragma unroll
-  for (int m = 0; m < PB; ++m) a[m] = m <= r ? src[m] : 0.f;
-  float dv[PB];
-#pragma unroll
-  for (int j = 0; j < PB; ++j) {
-    float d = readlane_f(a[j], j);
-    if (!(d > 0.f)) {
-      if (bad == 0) bad = c0 + j + 1;
-      d = 1.f;
-    }
-    const float rs = rsqrt_nr(d);
-    dv[j] = rs;
-    const float l = r > j ? a[j] * rs : (r == j ? d * rs : 0.f);
-    a[j] = l;
-    const float f = r > j ? l : 0.f;
-#pragma unroll
-    for (int c = j + 1; c < PB; ++c) a[c] = fmaf(-f, readlane_f(a[j], c), a[c]);
-  }
-  // inverse, lane r = column r: x_i = (delta_ir - sum_{m<i} L_im x_m) / L_ii
-  float x[PB];
-#pragma unroll
-  for (int i = 0; i < PB; ++i) {
-    float acc = i == r ? 1.f : 0.f;
-#pragma unroll
-    for (int m = 0; m < i; ++m) acc = fmaf(-readlane_f(a[m], i), x[m], acc);
-    x[i] = acc * dv[i];
-  }
-  if (lane < PB) {
-    float* dst = As + (c0 + r) * LDA + c0;
-#pragma unroll
-    for (int m = 0; m < PB; ++m) dst[m] = m <= r ? a[m] : 0.f;
-#pragma unroll
-    for (int i = 0; i < PB; ++i) Xs[(c0 + i) * LDA + c0 + r] = x[i];
-  }
-}
+constexpr int LDA = NB + 4;   // LDS row stride (floats) of staged 128-wide blocks
 
 // C[row][col] += sum_{m < len} A[ra + row][ca + m] B[rb + col][cb + m] on one
 // 16x16 tile (both operands read along their rows, a float4 per lane)
@@ -295,91 +248,187 @@ __device__ __forceinline__ f32x4 tile_nn(const float* A, int ra, int ca, const f
   return acc;
 }
 
+// Factor and invert the kb x kb diagonal block at (k, k) (kb <= 128; the
+// block is padded to 128 with the identity) in one workgroup, in LDS as
+// packed lower-triangle 16x16 tiles (72 KiB in all, so the workgroup fits
+// on a CU beside a trailing-update workgroup):
+//   the diagonal tile D_J is factored and inverted in registers by wave 0
+//   (lane r holds row r; the pivot and the column reach the other lanes by
+//   v_readlane), one step ahead: while waves 1..3 take the trailing tiles
+//   of step J, wave 0 updates tile (J+1, J+1) first and factors it;
+//   panel tiles L_IJ = A_IJ D_J^-T and trailing tiles A_IK -= L_IJ L_KJ^T
+//   are 16x16x16 fp32 MFMA products (two barriers per step);
+// then the off-diagonal tiles of the inverse follow by distance from the
+// diagonal, X_IJ = -X_II sum_{m=J}^{I-1} L_Im X_mJ (one barrier per
+// distance).  Row r of every tile is stored at row position prm(r), so the
+// rows 4q + j (q = 0..3) that one MFMA result register covers fall in four
+// different LDS bank groups.
+__device__ __forceinline__ int prm(int r) { return 4 * (r & 3) + (r >> 2); }
+__device__ __forceinline__ int ptile(int I, int J) { return (I * (I + 1) / 2 + J) * 256; }   // J <= I
+__device__ __forceinline__ int otile(int I, int J) { return (I * (I - 1) / 2 + J) * 256; }   // J < I
+
 template <int PB>
 __global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, int k, int kb, float* inv,
                                                        LgCtl* ctl) {
+  static_assert(PB == 16, "16x16 tiles");
   if (ctl->skip) return;
-  constexpr int NS = NB / PB;            // sub-blocks
-  constexpr int TPB = PB / 16;           // 16-wide tiles per sub-block edge
-  constexpr int MAXP = (NB - PB) / 16 * TPB;   // tiles of the largest sub-panel
-  constexpr int MAXX = (NS - 1) * TPB * TPB;   // tiles of the largest inverse diagonal
-  constexpr int UP = (MAXP + 3) / 4, UX = (MAXX + 3) / 4;
-  __shared__ __attribute__((aligned(16))) float lds_f[2 * NB * LDA];
-  float* As = lds_f;              // [NB][LDA] the block, then its factor
-  float* Xs = lds_f + NB * LDA;   // [NB][LDA] the inverse
+  constexpr int NT = NB / 16;
+  __shared__ __attribute__((aligned(16))) float Lt[NT * (NT + 1) / 2 * 256];   // the block, then its factor
+  __shared__ __attribute__((aligned(16))) float Xd[NT * 256];                  // inverses of the diagonal tiles
+  __shared__ __attribute__((aligned(16))) float Xo[NT * (NT - 1) / 2 * 256];   // off-diagonal tiles of the inverse
   __shared__ int bad_s;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lq = lane >> 4;
 
+  // the block into the tiles: rows past kb are identity rows; a float4
+  // chunk is read only if it starts on or left of the diagonal (it then
+  // ends inside the row), and entries right of the diagonal are cleared
   {
-    // all 16 row chunks of a thread in flight before the LDS writes
-    float4 v[NB * NB / 4 / 256];
+    constexpr int NQ = NT * (NT + 1) / 2, UQ = (NQ + 3) / 4;
+    const int r = lane >> 2, c4 = 4 * (lane & 3);
+    float4 v[UQ];
 #pragma unroll
-    for (int u = 0; u < NB * NB / 4 / 256; ++u) {
-      const int e = tid + 256 * u, i = e / (NB / 4), c = 4 * (e % (NB / 4));
+    for (int u = 0; u < UQ; ++u) {
+      const int q = w + 4 * u;
       v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-      // only chunks that start on or left of the diagonal (they end inside the row)
-      if (i < kb && c <= i) v[u] = *reinterpret_cast<const float4*>(L + (long long)(k + i) * ldL + k + c);
+      if (q < NQ) {
+        int I, J;
+        tile_pair(q, I, J);
+        const int i = 16 * I + r, j = 16 * J + c4;
+        if (i < kb && j <= i) v[u] = *reinterpret_cast<const float4*>(L + (long long)(k + i) * ldL + k + j);
+      }
     }
 #pragma unroll
-    for (int u = 0; u < NB * NB / 4 / 256; ++u) {
-      const int e = tid + 256 * u, i = e / (NB / 4), c = 4 * (e % (NB / 4));
-      float4 a = v[u];
-      if (i < kb) {
-        if (c + 1 > i) a.y = 0.f;
-        if (c + 2 > i) a.z = 0.f;
-        if (c + 3 > i) a.w = 0.f;
-      } else {
-        a.x = c == i ? 1.f : 0.f;
-        a.y = c + 1 == i ? 1.f : 0.f;
-        a.z = c + 2 == i ? 1.f : 0.f;
-        a.w = c + 3 == i ? 1.f : 0.f;
+    for (int u = 0; u < UQ; ++u) {
+      const int q = w + 4 * u;
+      if (q < NQ) {
+        int I, J;
+        tile_pair(q, I, J);
+        const int i = 16 * I + r, j = 16 * J + c4;
+        float4 a = v[u];
+        if (i < kb) {
+          if (j + 1 > i) a.y = 0.f;
+          if (j + 2 > i) a.z = 0.f;
+          if (j + 3 > i) a.w = 0.f;
+        } else {
+          a.x = j == i ? 1.f : 0.f;
+          a.y = j + 1 == i ? 1.f : 0.f;
+          a.z = j + 2 == i ? 1.f : 0.f;
+          a.w = j + 3 == i ? 1.f : 0.f;
+        }
+        *reinterpret_cast<float4*>(&Lt[q * 256 + prm(r) * 16 + c4]) = a;
       }
-      *reinterpret_cast<float4*>(&As[i * LDA + c]) = a;
-      *reinterpret_cast<float4*>(&Xs[i * LDA + c]) = make_float4(0.f, 0.f, 0.f, 0.f);
     }
   }
+  if (tid == 0) bad_s = 0;
   __syncthreads();
 
-  int bad = 0;
-  for (int sb = 0; sb < NS; ++sb) {
-    const int c0 = PB * sb, r0 = c0 + PB;
-    if (w == 0) potrf_base<PB>(As, Xs, c0, lane, bad);
-    __syncthreads();
-    // sub-panel: L[i][c0 + c] = sum_m A[i][c0 + m] X_D[c][m], rows i >= r0
-    const int np = (NB - r0) / 16 * TPB;
-    f32x4 acc[UP];
+  // wave 0: factor and invert diagonal tile J (block-relative pivot on failure)
+  auto factor_diag = [&](int J) {
+    float* D = Lt + ptile(J, J) + prm(lr) * 16;
+    float a[16];
 #pragma unroll
-    for (int u = 0; u < UP; ++u) {
-      const int t = w + 4 * u;
-      acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (t < np) acc[u] = tile_nt(As, r0 + 16 * (t / TPB), c0, Xs, c0 + 16 * (t % TPB), c0, PB, lr, lq, acc[u]);
+    for (int m = 0; m < 16; m += 4) {
+      const float4 t = *reinterpret_cast<const float4*>(D + m);
+      a[m] = t.x;
+      a[m + 1] = t.y;
+      a[m + 2] = t.z;
+      a[m + 3] = t.w;
     }
-    __syncthreads();
+    // per-lane predicates as 0 / 1 floats (products instead of selects keep
+    // them out of SGPR pairs); the tile is finite (non-finite inputs stop
+    // the group before any factor), so products can clear entries
+    auto gt = [&](int j) { return (float)((unsigned)(j - lr) >> 31); };   // 1 if lr > j
+    auto eq = [&](int j) { return gt(j - 1) - gt(j); };                  // 1 if lr == j
 #pragma unroll
-    for (int u = 0; u < UP; ++u) {
-      const int t = w + 4 * u;
-      if (t < np) {
-        const int i0 = r0 + 16 * (t / TPB), cc = c0 + 16 * (t % TPB);
+    for (int m = 0; m < 16; ++m) a[m] *= gt(m - 1);
+    float dv[16], dg[16];
+    int bad_j = 0;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) As[(i0 + 4 * lq + j) * LDA + cc + lr] = acc[u][j];
+    for (int j = 0; j < 16; ++j) {
+      float d = readlane_f(a[j], j);
+      if (bad_j == 0 && !(d > 0.f)) bad_j = 16 * J + j + 1;   // uniform: d came from one lane
+      d = d > 0.f ? d : 1.f;
+      const float rs = rsqrt_nr(d);
+      dv[j] = rs;
+      dg[j] = d * rs;
+      const float f = gt(j) * (a[j] * rs);   // L[r][j] below the diagonal, 0 on and above it
+      a[j] = f;
+#pragma unroll
+      for (int c = j + 1; c < 16; ++c) a[c] = fmaf(-f, readlane_f(a[j], c), a[c]);
+    }
+    // row r of X = D^-1 from X D = I, columns right to left (X is lower
+    // triangular: the entries right of the diagonal come out exactly 0)
+    float xr[16];
+#pragma unroll
+    for (int c = 15; c >= 0; --c) {
+      float acc = eq(c);
+#pragma unroll
+      for (int m = c + 1; m < 16; ++m) acc = fmaf(-xr[m], readlane_f(a[c], m), acc);
+      xr[c] = acc * dv[c];
+    }
+    float mine = 0.f;   // this row's diagonal entry of L
+#pragma unroll
+    for (int j = 0; j < 16; ++j) mine = fmaf(eq(j), dg[j], mine);
+    if (lane < 16) {
+#pragma unroll
+      for (int m = 0; m < 16; m += 4) {
+        float4 t;
+        t.x = fmaf(a[m], gt(m), eq(m) * mine);
+        t.y = fmaf(a[m + 1], gt(m + 1), eq(m + 1) * mine);
+        t.z = fmaf(a[m + 2], gt(m + 2), eq(m + 2) * mine);
+        t.w = fmaf(a[m + 3], gt(m + 3), eq(m + 3) * mine);
+        *reinterpret_cast<float4*>(D + m) = t;
+        *reinterpret_cast<float4*>(&Xd[J * 256 + prm(lr) * 16 + m]) = make_float4(xr[m], xr[m + 1], xr[m + 2], xr[m + 3]);
       }
     }
-    __syncthreads();
-    // trailing: A[i][j] -= sum_m L[i][c0 + m] L[j][c0 + m], lower 16x16 tiles
-    const int T = (NB - r0) / 16, nt = T * (T + 1) / 2;
-    for (int t = w; t < nt; t += 4) {
-      int I, J;
-      tile_pair(t, I, J);
-      const f32x4 p = tile_nt(As, r0 + 16 * I, c0, As, r0 + 16 * J, c0, PB, lr, lq, f32x4{0.f, 0.f, 0.f, 0.f});
+    if (lane == 0 && bad_j && bad_s == 0) bad_s = bad_j;
+  };
+  // C = A B^T on one tile pair (both read along their rows)
+  auto nt16 = [&](const float* A, const float* B) {
+    const float4 av = *reinterpret_cast<const float4*>(A + prm(lr) * 16 + 4 * lq);
+    const float4 bv = *reinterpret_cast<const float4*>(B + prm(lr) * 16 + 4 * lq);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    acc = mma_f32(av.x, bv.x, acc);
+    acc = mma_f32(av.y, bv.y, acc);
+    acc = mma_f32(av.z, bv.z, acc);
+    acc = mma_f32(av.w, bv.w, acc);
+    return acc;
+  };
+
+  if (w == 0) factor_diag(0);
+  __syncthreads();
+  for (int J = 0; J < NT; ++J) {
+    if (bad_s) break;
+    for (int I = J + 1 + w; I < NT; I += 4) {
+      float* A = Lt + ptile(I, J);
+      const f32x4 acc = nt16(A, Xd + J * 256);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) As[(r0 + 16 * I + 4 * lq + j) * LDA + r0 + 16 * J + lr] -= p[j];
+      for (int j = 0; j < 4; ++j) A[prm(4 * lq + j) * 16 + lr] = acc[j];
+    }
+    __syncthreads();
+    const int rest = NT - 1 - J, nrest = rest * (rest + 1) / 2;
+    auto trail = [&](int q) {
+      int I, K2;
+      tile_pair(q, I, K2);
+      I += J + 1;
+      K2 += J + 1;
+      const f32x4 p = nt16(Lt + ptile(I, J), Lt + ptile(K2, J));
+      float* C = Lt + ptile(I, K2);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) C[prm(4 * lq + j) * 16 + lr] -= p[j];
+    };
+    if (w == 0) {
+      if (rest > 0) {   // tile (J+1, J+1) is trailing tile 0
+        trail(0);
+        factor_diag(J + 1);
+      }
+    } else {
+      for (int q = w; q < nrest; q += 3) trail(q);
     }
     __syncthreads();
   }
-  if (w == 0 && lane == 0) bad_s = bad;
-  __syncthreads();
   if (bad_s) {
     // padded pivots are exactly 1: a failure is always inside the block
     if (tid == 0) {
@@ -388,56 +437,56 @@ __global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, 
     }
     return;
   }
-  for (int e = tid; e < NB * (NB / 4); e += 256) {
-    const int i = e / (NB / 4), c = 4 * (e % (NB / 4));
-    if (i < kb && c <= i)
-      *reinterpret_cast<float4*>(L + (long long)(k + i) * ldL + k + c) = *reinterpret_cast<const float4*>(&As[i * LDA + c]);
+  // the factor back to L (the chunk rule of the load; entries right of the
+  // diagonal inside a chunk are never read)
+  {
+    constexpr int NQ = NT * (NT + 1) / 2;
+    const int r = lane >> 2, c4 = 4 * (lane & 3);
+    for (int q = w; q < NQ; q += 4) {
+      int I, J;
+      tile_pair(q, I, J);
+      const int i = 16 * I + r, j = 16 * J + c4;
+      if (i < kb && j <= i)
+        *reinterpret_cast<float4*>(L + (long long)(k + i) * ldL + k + j) =
+            *reinterpret_cast<const float4*>(&Lt[q * 256 + prm(r) * 16 + c4]);
+    }
   }
 
-  // off-diagonal blocks of the inverse, distance d = i - j from the diagonal
-  for (int d = 1; d < NS; ++d) {
-    const int nx = (NS - d) * TPB * TPB;
-    f32x4 acc[UX];
-#pragma unroll
-    for (int u = 0; u < UX; ++u) {
-      const int t = w + 4 * u;
-      acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (t < nx) {
-        const int jb = t / (TPB * TPB), q = t % (TPB * TPB), ib = jb + d;
-        const int i0 = PB * ib + 16 * (q / TPB), j0 = PB * jb + 16 * (q % TPB);
-        // T = sum_{m=j}^{i-1} L_im X_mj
-        acc[u] = tile_nn(As, i0, PB * jb, Xs, PB * jb, j0, PB * d, lr, lq, acc[u]);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) Xs[(i0 + 4 * lq + j) * LDA + j0 + lr] = acc[u][j];
+  // off-diagonal tiles of the inverse by distance d = I - J from the diagonal
+  for (int d = 1; d < NT; ++d) {
+    for (int J = w; J + d < NT; J += 4) {
+      const int I = J + d;
+      // T = sum_{m=J}^{I-1} L_Im X_mJ, X_mJ read as the MFMA B operand (k = row)
+      f32x4 t = {0.f, 0.f, 0.f, 0.f};
+      for (int m = J; m < I; ++m) {
+        const float4 av = *reinterpret_cast<const float4*>(Lt + ptile(I, m) + prm(lr) * 16 + 4 * lq);
+        const float* X = m == J ? Xd + J * 256 : Xo + otile(m, J);
+        t = mma_f32(av.x, X[prm(4 * lq + 0) * 16 + lr], t);
+        t = mma_f32(av.y, X[prm(4 * lq + 1) * 16 + lr], t);
+        t = mma_f32(av.z, X[prm(4 * lq + 2) * 16 + lr], t);
+        t = mma_f32(av.w, X[prm(4 * lq + 3) * 16 + lr], t);
       }
-    }
-    __syncthreads();
+      // X_IJ = -X_II T: T's result layout (row 4 lq + j, column lr in
+      // register j) is the B operand of reduction index 4 lq + j
+      const float4 xv = *reinterpret_cast<const float4*>(Xd + I * 256 + prm(lr) * 16 + 4 * lq);
+      f32x4 x = {0.f, 0.f, 0.f, 0.f};
+      x = mma_f32(xv.x, t[0], x);
+      x = mma_f32(xv.y, t[1], x);
+      x = mma_f32(xv.z, t[2], x);
+      x = mma_f32(xv.w, t[3], x);
 #pragma unroll
-    for (int u = 0; u < UX; ++u) {
-      const int t = w + 4 * u;
-      acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (t < nx) {
-        const int jb = t / (TPB * TPB), q = t % (TPB * TPB), ib = jb + d;
-        const int i0 = PB * ib + 16 * (q / TPB), j0 = PB * jb + 16 * (q % TPB);
-        acc[u] = tile_nn(Xs, i0, PB * ib, Xs, PB * ib, j0, PB, lr, lq, acc[u]);   // X_ii T
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < UX; ++u) {
-      const int t = w + 4 * u;
-      if (t < nx) {
-        const int jb = t / (TPB * TPB), q = t % (TPB * TPB), ib = jb + d;
-        const int i0 = PB * ib + 16 * (q / TPB), j0 = PB * jb + 16 * (q % TPB);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) Xs[(i0 + 4 * lq + j) * LDA + j0 + lr] = -acc[u][j];
-      }
+      for (int j = 0; j < 4; ++j) Xo[otile(I, J) + prm(4 * lq + j) * 16 + lr] = -x[j];
     }
     __syncthreads();
   }
+  // the whole 128 x 128 inverse (upper tiles zero), row-major
   for (int e = tid; e < NB * (NB / 4); e += 256) {
     const int i = e / (NB / 4), c = 4 * (e % (NB / 4));
-    *reinterpret_cast<float4*>(inv + (long long)i * NB + c) = *reinterpret_cast<const float4*>(&Xs[i * LDA + c]);
+    const int I = i >> 4, J = c >> 4, r = i & 15;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (J == I) v = *reinterpret_cast<const float4*>(&Xd[I * 256 + prm(r) * 16 + (c & 15)]);
+    else if (J < I) v = *reinterpret_cast<const float4*>(&Xo[otile(I, J) + prm(r) * 16 + (c & 15)]);
+    *reinterpret_cast<float4*>(inv + (long long)i * NB + c) = v;
   }
 }
 constexpr int kPotrfPB = 16;
@@ -449,30 +498,27 @@ constexpr int kPotrfPB = 16;
 __global__ __launch_bounds__(256) void lg_trsm_kernel(float* L, long long ldL, int n, int k, const float* inv,
                                                       const LgCtl* ctl) {
   if (ctl->skip) return;
-  __shared__ __attribute__((aligned(16))) float As[64][LDP];
+  // only the inverse goes through LDS (68 KiB, so the workgroup fits on a CU
+  // beside a trailing-update workgroup); each wave reads its 16 rows of A21
+  // straight into the MFMA operand layout
   __shared__ __attribute__((aligned(16))) float Bs[NB][LDP];
   const int tid = threadIdx.x;
   const int r0 = k + NB + 64 * blockIdx.x;
+  const int w = tid >> 6, lane = tid & 63, lr = lane & 15, lq = lane >> 4;
+  float4 av[NB / 16];
   {
-    // every load of the thread in flight before the LDS writes
-    constexpr int UA = 64 * (NB / 4) / 256, UB = NB * (NB / 4) / 256;
-    float4 va[UA], vb[UB];
+    const int row = r0 + 16 * w + lr;
 #pragma unroll
-    for (int u = 0; u < UA; ++u) {
-      const int t = tid + 256 * u, rr = t / (NB / 4), cq = t % (NB / 4);
-      const int row = r0 + rr;
-      va[u] = row < n ? *reinterpret_cast<const float4*>(L + (long long)row * ldL + k + 4 * cq)
-                      : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
+    for (int kk = 0; kk < NB / 16; ++kk)
+      av[kk] = row < n ? *reinterpret_cast<const float4*>(L + (long long)row * ldL + k + 16 * kk + 4 * lq)
+                       : make_float4(0.f, 0.f, 0.f, 0.f);
+    // every load of the thread in flight before the LDS writes
+    constexpr int UB = NB * (NB / 4) / 256;
+    float4 vb[UB];
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
       const int t = tid + 256 * u, rr = t / (NB / 4), cq = t % (NB / 4);
       vb[u] = *reinterpret_cast<const float4*>(inv + (long long)rr * NB + 4 * cq);
-    }
-#pragma unroll
-    for (int u = 0; u < UA; ++u) {
-      const int t = tid + 256 * u;
-      *reinterpret_cast<float4*>(&As[t / (NB / 4)][4 * (t % (NB / 4))]) = va[u];
     }
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
@@ -481,20 +527,18 @@ __global__ __launch_bounds__(256) void lg_trsm_kernel(float* L, long long ldL, i
     }
   }
   __syncthreads();
-  const int w = tid >> 6, lane = tid & 63, lr = lane & 15, lq = lane >> 4;
   f32x4 acc[8];
 #pragma unroll
   for (int cb = 0; cb < 8; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 2
+#pragma unroll
   for (int kk = 0; kk < NB / 16; ++kk) {
-    const float4 av = *reinterpret_cast<const float4*>(&As[16 * w + lr][16 * kk + 4 * lq]);
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) {
       const float4 bv = *reinterpret_cast<const float4*>(&Bs[16 * cb + lr][16 * kk + 4 * lq]);
-      acc[cb] = mma_f32(av.x, bv.x, acc[cb]);
-      acc[cb] = mma_f32(av.y, bv.y, acc[cb]);
-      acc[cb] = mma_f32(av.z, bv.z, acc[cb]);
-      acc[cb] = mma_f32(av.w, bv.w, acc[cb]);
+      acc[cb] = mma_f32(av[kk].x, bv.x, acc[cb]);
+      acc[cb] = mma_f32(av[kk].y, bv.y, acc[cb]);
+      acc[cb] = mma_f32(av[kk].z, bv.z, acc[cb]);
+      acc[cb] = mma_f32(av[kk].w, bv.w, acc[cb]);
     }
   }
 #pragma unroll
@@ -904,14 +948,16 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
                                    int mode, float* w, float* lam_eff, float* resid2, int32_t* info,
                                    const LgLayout& lay, unsigned char* base, hipStream_t hs, hipStream_t aux,
                                    hipEvent_t ev_col, hipEvent_t ev_next) {
-  // the bulk trailing update runs on at most two workgroups per CU of all but
-  // one CU in 32 (one per XCD on a 256-CU part), so that the diagonal-block
-  // chain of the next pair finds free CUs instead of queueing behind it
+  // the bulk trailing update runs persistent on 7/8 of the two-per-CU
+  // workgroup slots: one CU in four keeps room (LDS and waves) for one more
+  // workgroup, where the diagonal-block chain of the next pair (factor,
+  // panel solve, rank-128 update, each under 96 KiB of LDS) runs beside the
+  // update instead of queueing behind it
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
                                               hipSuccess || cus < 32)
     cus = 256;
-  const int rest_slots = 2 * (cus - cus / 32);
+  const int rest_slots = 2 * cus - cus / 4;
   float* L = reinterpret_cast<float*>(base + lay.off_L);
   float* inv = reinterpret_cast<float*>(base + lay.off_inv);
   float* sinv = reinterpret_cast<float*>(base + lay.off_sinv);

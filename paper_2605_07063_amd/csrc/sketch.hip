@@ -41,6 +41,7 @@ constexpr int kTokWave = 32;                  // tokens per wave per tile
 constexpr int kTokTile = kWaves * kTokWave;   // tokens per workgroup tile
 constexpr int kMaxLayersPerLaunch = 16;
 constexpr int kTargetUnits = 2048;            // aim for >= 8 units per CU
+constexpr int kXcds = 8;                      // accelerator dies; workgroups are dealt to them round robin
 
 struct LayerArg {
   const unsigned char* x;
@@ -371,6 +372,7 @@ struct PackArgs {
   int num_layers;
   int N, T;
   int WL, KS;           // workgroups per layer, tiles per workgroup (upper bound)
+  int xcd;              // 1: number workgroups XCD by XCD (all layers of the launch alike)
   int max_tiles;        // WL * KS: tile slots per layer
   const int* cum;       // [N + 2]: exclusive prefix of the clamped lengths, then R
   const int* tile_ex;   // [max_tiles] example holding the first position of each tile, -1 if empty
@@ -473,8 +475,17 @@ __global__ __launch_bounds__(kThreads, 2) void sketch_packed_kernel(PackArgs a) 
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4, hr = lane >> 3;
-  const int li = blockIdx.x / a.WL;
-  const int wg = blockIdx.x - li * a.WL;
+  // XCD-aware numbering (layers of one shape): workgroups are dealt to the
+  // 8 XCDs round robin, so the (layer, range) index v gives each XCD a
+  // contiguous run of ranges and a layer's projector chunks stay in few
+  // XCDs' L2 (one when the launch holds a multiple of 8 layers).  With layers
+  // of different sizes the runs would leave some XCDs idle, so the plain
+  // order is kept.
+  const int G8 = a.xcd ? (int)gridDim.x / kXcds : 0;
+  const int b = blockIdx.x;
+  const int v = b < G8 * kXcds ? (b % kXcds) * G8 + b / kXcds : b;
+  const int li = v / a.WL;
+  const int wg = v - li * a.WL;
   const int total = a.cum[a.N];
   const int R = a.cum[a.N + 1];
   const int r_lo = wg * R;
@@ -1016,6 +1027,9 @@ extern "C" dr_status dr_sketch_grads(const dr_layer* layers, int num_layers, int
       pa.L[j] = la;
     }
     a.num_layers = pa.num_layers = l.count;
+    pa.xcd = 1;
+    for (int j = 1; j < l.count; ++j)
+      if (pa.L[j].d_in != pa.L[0].d_in || pa.L[j].d_out != pa.L[0].d_out) pa.xcd = 0;
     a.N = pa.N = (int)N;
     a.T = pa.T = (int)T;
     a.chunk_tokens = l.chunk;
