@@ -9,8 +9,11 @@
 //   inv   fp32 [nblk][128][128]: the inverse of every 128x128 diagonal
 //         block of L (used by the panel solve)
 //   sinv  fp32 [nsb][1024][1024]: the inverse of every 1024x1024 diagonal
-//         super-block of L, lower blocks only (used by the two triangular
-//         solves; 64 MiB at n = 16384)
+//         super-block of L, lower blocks only (used by the L solve; 64 MiB
+//         at n = 16384)
+//   sinvt fp32 [nsb][1024][1024]: the same inverses transposed, upper
+//         blocks only (used by the L^T solve, so that both solves apply
+//         their super-block inverse row by row)
 //   x, dx, r, z  fp64 [npad] solution, correction, residual, work
 //   ctl   status shared by the kernels of one group (skip / info / lam_eff)
 //
@@ -68,7 +71,7 @@ struct LgCtl {
 
 struct LgLayout {
   long long n, ldL, nblk, npad;
-  size_t off_L, off_inv, off_sinv, off_x, off_dx, off_r, off_z, off_ctl, total;
+  size_t off_L, off_inv, off_sinv, off_sinvt, off_x, off_dx, off_r, off_z, off_ctl, total;
 };
 
 LgLayout lg_layout(long long n) {
@@ -81,6 +84,7 @@ LgLayout lg_layout(long long n) {
   l.off_L = o;    o = align_up(o + (size_t)n * l.ldL * 4, 256);
   l.off_inv = o;  o = align_up(o + (size_t)l.nblk * NB * NB * 4, 256);
   l.off_sinv = o; o = align_up(o + (size_t)((l.nblk + SB - 1) / SB) * SBN * SBN * 4, 256);
+  l.off_sinvt = o; o = align_up(o + (size_t)((l.nblk + SB - 1) / SB) * SBN * SBN * 4, 256);
   l.off_x = o;    o = align_up(o + (size_t)l.npad * 8, 256);
   l.off_dx = o;   o = align_up(o + (size_t)l.npad * 8, 256);
   l.off_r = o;    o = align_up(o + (size_t)l.npad * 8, 256);
@@ -700,18 +704,24 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
 // workgroup per block; the 128 x 128 operands are staged in LDS and wave w
 // computes rows 32 w .. 32 w + 31 with fp32 MFMA.
 __global__ __launch_bounds__(256) void lg_sinv_kernel(const float* L, long long ldL, int n, int nblk,
-                                                      const float* inv, float* sinv, int d, const LgCtl* ctl) {
+                                                      const float* inv, float* sinv, float* sinvt, int d,
+                                                      const LgCtl* ctl) {
   if (ctl->skip) return;
   const int S = blockIdx.y, jj = blockIdx.x, ii = jj + d;
   const int bj = SB * S + jj, bi = bj + d;
   if (ii >= SB || bi >= nblk) return;
-  float* X = sinv + (long long)S * SBN * SBN;   // [SBN][SBN]
+  float* X = sinv + (long long)S * SBN * SBN;     // [SBN][SBN]
+  float* XT = sinvt + (long long)S * SBN * SBN;   // [SBN][SBN], X transposed
   const int tid = threadIdx.x;
   if (d == 0) {
+    const float* ib = inv + (long long)bi * NB * NB;
     for (int e = tid; e < NB * NB / 4; e += 256) {
       const int r = e / (NB / 4), c = 4 * (e % (NB / 4));
       *reinterpret_cast<float4*>(X + (long long)(NB * ii + r) * SBN + NB * ii + c) =
-          *reinterpret_cast<const float4*>(inv + (long long)bi * NB * NB + r * NB + c);
+          *reinterpret_cast<const float4*>(ib + r * NB + c);
+      // row r of the transpose = column r of the block
+      *reinterpret_cast<float4*>(XT + (long long)(NB * ii + r) * SBN + NB * ii + c) =
+          make_float4(ib[c * NB + r], ib[(c + 1) * NB + r], ib[(c + 2) * NB + r], ib[(c + 3) * NB + r]);
     }
     return;
   }
@@ -758,91 +768,112 @@ __global__ __launch_bounds__(256) void lg_sinv_kernel(const float* L, long long 
       for (int q = 0; q < 4; ++q) Bs[(32 * w + 16 * a + 4 * lq + q) * LDA + 16 * c + lr] = acc[a][c][q];
   stage(As, X + (long long)(NB * ii) * SBN + NB * ii, SBN, NB);
   __syncthreads();
+  f32x4 xo[2][8];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const f32x4 p = tile_nn(As, 32 * w + 16 * a, 0, Bs, 0, 16 * c, NB, lr, lq, f32x4{0.f, 0.f, 0.f, 0.f});
+    for (int c = 0; c < 8; ++c) xo[a][c] = tile_nn(As, 32 * w + 16 * a, 0, Bs, 0, 16 * c, NB, lr, lq, f32x4{0.f, 0.f, 0.f, 0.f});
+  __syncthreads();   // every wave is done reading As and Bs
+  // X_ij = -X_ii T through LDS, then out row by row and, transposed, into
+  // block (jj, ii) of XT (coalesced both ways)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        X[(long long)(NB * ii + 32 * w + 16 * a + 4 * lq + q) * SBN + NB * jj + 16 * c + lr] = -p[q];
-    }
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) Bs[(32 * w + 16 * a + 4 * lq + q) * LDA + 16 * c + lr] = -xo[a][c][q];
+  __syncthreads();
+  for (int e = tid; e < NB * NB / 4; e += 256) {
+    const int r = e / (NB / 4), c = 4 * (e % (NB / 4));
+    *reinterpret_cast<float4*>(X + (long long)(NB * ii + r) * SBN + NB * jj + c) =
+        *reinterpret_cast<const float4*>(&Bs[r * LDA + c]);
+    *reinterpret_cast<float4*>(XT + (long long)(NB * jj + r) * SBN + NB * ii + c) =
+        make_float4(Bs[c * LDA + r], Bs[(c + 1) * LDA + r], Bs[(c + 2) * LDA + r], Bs[(c + 3) * LDA + r]);
+  }
 }
 
 // out[i] = (or -=) sum_c M[i][c] v_c for rows i < rows, columns c < width
-// (<= SBN); lower != 0 limits row i to the 128-blocks on or left of its own
-// (a lower-triangular block matrix whose upper blocks are never read).  32
-// rows per workgroup, 8 per wave, all their loads in flight; lane l takes
-// columns 4 l + 256 t.
-__global__ __launch_bounds__(256) void lg_rowdot_kernel(const float* M, long long ldM, int rows, int width, int lower,
+// (<= SBN); mode 1 limits row i to the 128-blocks on or left of its own (a
+// lower-triangular block matrix), mode 2 to those on or right of it (an
+// upper one); the other blocks are never read.  RW rows per wave, 4 waves
+// per workgroup, all their loads in flight; lane l takes columns
+// 4 l + 256 t; each row's sum is a fixed-order DPP reduction.
+template <int RW>
+__global__ __launch_bounds__(256) void lg_rowdot_kernel(const float* M, long long ldM, int rows, int width, int mode,
                                                         const double* v, double* out, int sub, const LgCtl* ctl) {
   if (ctl->skip) return;
+  constexpr int CT = SBN / 256;   // float4 columns per lane
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int row0 = 32 * blockIdx.x + 8 * w;
-  double vv[SB / 2][4];
+  const int row0 = 4 * RW * blockIdx.x + RW * w;
+  float4 mv[RW][CT];
 #pragma unroll
-  for (int t = 0; t < SB / 2; ++t) {
+  for (int u = 0; u < RW; ++u) {
+    const int row = row0 + u;
+    const int lo = mode == 2 ? NB * (row / NB) : 0;
+    const int hi = mode == 1 ? min(width, NB * (row / NB + 1)) : width;
+#pragma unroll
+    for (int t = 0; t < CT; ++t) {
+      const int c = 4 * lane + 256 * t;
+      mv[u][t] = (row < rows && c >= lo && c < hi) ? *reinterpret_cast<const float4*>(M + (long long)row * ldM + c)
+                                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  }
+  double vv[CT][4];
+#pragma unroll
+  for (int t = 0; t < CT; ++t) {
     const int c = 4 * lane + 256 * t;
 #pragma unroll
     for (int q = 0; q < 4; ++q) vv[t][q] = c < width ? v[c + q] : 0.0;
   }
-  float4 mv[8][SB / 2];
 #pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const int row = row0 + u;
-    const int lim = lower ? min(width, NB * (row / NB + 1)) : width;
-#pragma unroll
-    for (int t = 0; t < SB / 2; ++t) {
-      const int c = 4 * lane + 256 * t;
-      mv[u][t] = (row < rows && c < lim) ? *reinterpret_cast<const float4*>(M + (long long)row * ldM + c)
-                                         : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-  }
-#pragma unroll
-  for (int u = 0; u < 8; ++u) {
+  for (int u = 0; u < RW; ++u) {
     double acc = 0.0;
 #pragma unroll
-    for (int t = 0; t < SB / 2; ++t)
+    for (int t = 0; t < CT; ++t)
       acc += (double)mv[u][t].x * vv[t][0] + (double)mv[u][t].y * vv[t][1] + (double)mv[u][t].z * vv[t][2] +
              (double)mv[u][t].w * vv[t][3];
-    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    acc = wave_sum_l63(acc);
     const int row = row0 + u;
-    if (lane == 0 && row < rows) out[row] = sub ? out[row] - acc : acc;
+    if (lane == 63 && row < rows) out[row] = sub ? out[row] - acc : acc;
   }
 }
 
-// out[c] = (or -=) sum_i M[i][c] v_i for columns c < 64 * gridDim.x and rows
-// i < rows (<= SBN); lower != 0 starts at the 128-block row of the column's
-// own block (a lower-triangular block matrix).  64 columns per workgroup:
-// lane l of wave w reads a float4 of columns 4 (l % 16) in row stream
-// 4 w + l / 16, streams take every 16th row (a wave load covers 4 rows x
-// 256 bytes); the 16 stream sums of a column are added in a fixed order.
-__global__ __launch_bounds__(256) void lg_coldot_kernel(const float* M, long long ldM, int rows, int lower,
-                                                        const double* v, double* out, int sub, const LgCtl* ctl) {
+// out[c] -= sum_i M[i][c] v_i for columns c < 64 * gridDim.x and rows
+// i < rows (<= SBN).  64 columns per workgroup of 1024 threads: lane l of
+// wave w reads a float4 of columns 4 (l % 16) in row stream 4 w + l / 16;
+// the 64 streams take every 64th row, so all 1024 rows of a super-block are
+// in flight at once (a wave load covers 4 rows x 256 bytes); the stream sums
+// of a column are added in a fixed order.
+constexpr int kColThreads = 1024;
+__global__ __launch_bounds__(kColThreads) void lg_coldot_kernel(const float* M, long long ldM, int rows,
+                                                                const double* v, double* out, const LgCtl* ctl) {
   if (ctl->skip) return;
-  __shared__ double vs[SBN], part[16][64];
+  constexpr int NS = kColThreads / 16, CU = SBN / NS;   // row streams, rows of a stream
+  __shared__ double vs[SBN], part[NS][64];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  for (int i = tid; i < rows; i += 256) vs[i] = v[i];
-  __syncthreads();
+  for (int i = tid; i < rows; i += kColThreads) vs[i] = v[i];
   const int m0 = 64 * blockIdx.x, c4 = lane & 15, st = 4 * w + (lane >> 4);
-  const int i_start = lower ? NB * (m0 / NB) : 0;
   const float* col = M + m0 + 4 * c4;
+  __syncthreads();   // vs
+  // the stream's rows in two rounds of CH loads in flight (registers)
+  constexpr int CH = CU / 2;
   double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
-  for (int i0 = i_start + st; i0 < rows; i0 += 16 * 8) {
-    float4 mv[8];
+#pragma unroll 1
+  for (int h = 0; h < 2; ++h) {
+    float4 mv[CH];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int i = i0 + 16 * u;
+    for (int u = 0; u < CH; ++u) {
+      const int i = st + NS * (h * CH + u);
       mv[u] = i < rows ? *reinterpret_cast<const float4*>(col + (long long)i * ldM) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int i = i0 + 16 * u;
+    for (int u = 0; u < CH; ++u) {
+      const int i = st + NS * (h * CH + u);
       const double vi = i < rows ? vs[i] : 0.0;
-      a0 += (double)mv[u].x * vi;
-      a1 += (double)mv[u].y * vi;
-      a2 += (double)mv[u].z * vi;
-      a3 += (double)mv[u].w * vi;
+      a0 = fma((double)mv[u].x, vi, a0);
+      a1 = fma((double)mv[u].y, vi, a1);
+      a2 = fma((double)mv[u].z, vi, a2);
+      a3 = fma((double)mv[u].w, vi, a3);
     }
   }
   part[st][4 * c4] = a0;
@@ -852,9 +883,8 @@ __global__ __launch_bounds__(256) void lg_coldot_kernel(const float* M, long lon
   __syncthreads();
   if (tid < 64) {
     double t = 0.0;
-#pragma unroll
-    for (int q = 0; q < 16; ++q) t += part[q][tid];
-    out[m0 + tid] = sub ? out[m0 + tid] - t : t;
+    for (int q = 0; q < NS; ++q) t += part[q][tid];
+    out[m0 + tid] -= t;
   }
 }
 
@@ -961,6 +991,7 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
   float* L = reinterpret_cast<float*>(base + lay.off_L);
   float* inv = reinterpret_cast<float*>(base + lay.off_inv);
   float* sinv = reinterpret_cast<float*>(base + lay.off_sinv);
+  float* sinvt = reinterpret_cast<float*>(base + lay.off_sinvt);
   double* x = reinterpret_cast<double*>(base + lay.off_x);
   double* dx = reinterpret_cast<double*>(base + lay.off_dx);
   double* r = reinterpret_cast<double*>(base + lay.off_r);
@@ -1024,7 +1055,8 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
     }
     const int nsb = (nblk + SB - 1) / SB;
     for (int d = 0; d < SB; ++d)
-      hipLaunchKernelGGL(lg_sinv_kernel, dim3(SB - d, nsb), dim3(256), 0, hs, L, ldL, n, nblk, inv, sinv, d, ctl);
+      hipLaunchKernelGGL(lg_sinv_kernel, dim3(SB - d, nsb), dim3(256), 0, hs, L, ldL, n, nblk, inv, sinv, sinvt, d,
+                         ctl);
     for (int it = 0; it <= kRefine; ++it) {
       if (it > 0)
         hipLaunchKernelGGL(lg_resid_kernel, dim3((n + 3) / 4), dim3(256), 0, hs, Kp, n, sp, x, r, (double*)nullptr,
@@ -1033,23 +1065,23 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       for (int S = 0; S < nsb; ++S) {
         const int o0 = SBN * S, nb = nblk - SB * S < SB ? nblk - SB * S : SB, width = NB * nb;
         const float* Xs = sinv + (long long)S * SBN * SBN;
-        hipLaunchKernelGGL(lg_rowdot_kernel, dim3((width + 31) / 32), dim3(256), 0, hs, Xs, (long long)SBN, width,
+        hipLaunchKernelGGL(lg_rowdot_kernel<1>, dim3((width + 3) / 4), dim3(256), 0, hs, Xs, (long long)SBN, width,
                            width, 1, r + o0, z + o0, 0, ctl);
         const int below = n - o0 - width;
         if (below > 0)
-          hipLaunchKernelGGL(lg_rowdot_kernel, dim3((below + 31) / 32), dim3(256), 0, hs,
+          hipLaunchKernelGGL(lg_rowdot_kernel<4>, dim3((below + 15) / 16), dim3(256), 0, hs,
                              L + (long long)(o0 + width) * ldL + o0, ldL, below, width, 0, z + o0, r + o0 + width, 1,
                              ctl);
       }
       for (int S = nsb - 1; S >= 0; --S) {
         const int o0 = SBN * S, nb = nblk - SB * S < SB ? nblk - SB * S : SB, width = NB * nb;
-        const float* Xs = sinv + (long long)S * SBN * SBN;
-        hipLaunchKernelGGL(lg_coldot_kernel, dim3(width / 64), dim3(256), 0, hs, Xs, (long long)SBN, width, 1, z + o0,
-                           dx + o0, 0, ctl);
+        const float* XTs = sinvt + (long long)S * SBN * SBN;
+        hipLaunchKernelGGL(lg_rowdot_kernel<1>, dim3((width + 3) / 4), dim3(256), 0, hs, XTs, (long long)SBN, width,
+                           width, 2, z + o0, dx + o0, 0, ctl);
         const int rows = n - o0 < width ? n - o0 : width;
         if (o0 > 0)
-          hipLaunchKernelGGL(lg_coldot_kernel, dim3(o0 / 64), dim3(256), 0, hs, L + (long long)o0 * ldL, ldL, rows, 0,
-                             dx + o0, z, 1, ctl);
+          hipLaunchKernelGGL(lg_coldot_kernel, dim3(o0 / 64), dim3(kColThreads), 0, hs, L + (long long)o0 * ldL, ldL,
+                             rows, dx + o0, z, ctl);
       }
       hipLaunchKernelGGL(lg_axpy_kernel, dim3((npad + 255) / 256), dim3(256), 0, hs, x, dx, npad, ctl);
     }

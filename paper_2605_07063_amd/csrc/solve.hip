@@ -81,25 +81,6 @@ __device__ __forceinline__ double wave_max(double v) {
   for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
   return v;
 }
-// fixed-order wave sum by DPP moves (no LDS round trips); the total is
-// exact in lane 63 only: pairs, quads (quad_perm), halves of a row
-// (row_half_mirror), rows (row_mirror), then row_bcast15 / row_bcast31
-template <int CTRL, int ROWS>
-__device__ __forceinline__ double dpp_d(double v) {
-  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), CTRL, ROWS, 0xF, false);
-  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, ROWS, 0xF, false);
-  return __hiloint2double(hi, lo);
-}
-__device__ __forceinline__ double wave_sum_l63(double v) {
-  v += dpp_d<0xB1, 0xF>(v);    // quad_perm [1, 0, 3, 2]
-  v += dpp_d<0x4E, 0xF>(v);    // quad_perm [2, 3, 0, 1]
-  v += dpp_d<0x141, 0xF>(v);   // row_half_mirror
-  v += dpp_d<0x140, 0xF>(v);   // row_mirror
-  v += dpp_d<0x142, 0xA>(v);   // row_bcast15 into rows 1 and 3
-  v += dpp_d<0x143, 0xC>(v);   // row_bcast31 into rows 2 and 3
-  return v;
-}
-
 // value of lane src (src uniform) as a scalar broadcast
 __device__ __forceinline__ double readlane_d(double v, int src) {
   const int lo = __builtin_amdgcn_readlane(__double2loint(v), src);
