@@ -583,110 +583,130 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
   if (ctl->skip) return;
   __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * 2 * SY_PANEL];
   constexpr int NCH = W / SY_CH;
+  static_assert(NCH % 2 == 0, "the next tile's first chunk goes to stage 0");
   const int k1 = k + W;
-  for (int qt = blockIdx.x; qt < ntiles; qt += gridDim.x) {
-  __syncthreads();   // (uniform) the previous tile is done with the LDS ring
-  int I, J;
-  if (head) {
-    const int T = (n - k1 + NB - 1) / NB;
-    const int q = qt;
-    I = q < T ? q : q - T + 1;
-    J = q < T ? 0 : 1;
-  } else {
-    tile_pair(qt, I, J);
-    I += h;
-    J += h;
-  }
-  const int ri = k1 + NB * I, rj = k1 + NB * J;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wr = w & 1, wc = w >> 1;
-  const bool diag = I == J;
-  const bool active = !(diag && wc > wr);
   const int lr = lane & 15, lg = lane >> 4;
-  // this lane's C entries (rows 4 lg + q of each 16-row block, column lr),
-  // loaded during the last two chunks
-  f32x4 c[4][4];
-  auto load_c = [&]() {
-#pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int row = ri + 64 * wr + 16 * rb + 4 * lg + q;
-          const int col = rj + 64 * wc + 16 * cb + lr;
-          c[rb][cb][q] = (row < n && col < n) ? L[(long long)row * ldL + col] : 0.f;
-        }
+  // a tile's coordinates and this lane's DMA row offsets
+  struct Tile {
+    int ri, rj;
+    bool diag;
+    unsigned offi[4], offj[4];
   };
-  // DMA of one chunk: wave w fills half blocks w, w + 4, w + 8, w + 12 of each panel
-  const __amdgpu_buffer_rsrc_t rsi = make_rsrc(L + (long long)ri * ldL, kOobOffset);
-  const __amdgpu_buffer_rsrc_t rsj = make_rsrc(L + (long long)rj * ldL, kOobOffset);
-  unsigned offi[4], offj[4];
   int segs[4];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int hb = w + 4 * u;
-    const int r = 8 * hb + (lane >> 3);
-    segs[u] = swz_seg_of_lane(lane, hb & 1);
-    offi[u] = ri + r < n ? (unsigned)((long long)r * ldL * 4) : kOobOffset;
-    offj[u] = rj + r < n ? (unsigned)((long long)r * ldL * 4) : kOobOffset;
-  }
-  auto issue = [&](int ch, int st) {
+  for (int u = 0; u < 4; ++u) segs[u] = swz_seg_of_lane(lane, (w + 4 * u) & 1);
+  auto tile_of = [&](int qt) {
+    int I, J;
+    if (head) {
+      const int T = (n - k1 + NB - 1) / NB;
+      I = qt < T ? qt : qt - T + 1;
+      J = qt < T ? 0 : 1;
+    } else {
+      tile_pair(qt, I, J);
+      I += h;
+      J += h;
+    }
+    Tile t;
+    t.ri = k1 + NB * I;
+    t.rj = k1 + NB * J;
+    t.diag = I == J;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = 8 * (w + 4 * u) + (lane >> 3);
+      t.offi[u] = t.ri + r < n ? (unsigned)((long long)r * ldL * 4) : kOobOffset;
+      t.offj[u] = t.rj + r < n ? (unsigned)((long long)r * ldL * 4) : kOobOffset;
+    }
+    return t;
+  };
+  // DMA of one chunk: wave w fills half blocks w, w + 4, w + 8, w + 12 of each panel
+  auto issue = [&](const Tile& t, int ch, int st) {
+    const __amdgpu_buffer_rsrc_t rsi = make_rsrc(L + (long long)t.ri * ldL, kOobOffset);
+    const __amdgpu_buffer_rsrc_t rsj = make_rsrc(L + (long long)t.rj * ldL, kOobOffset);
     unsigned char* sb = lds + st * 2 * SY_PANEL;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const unsigned cofs = (unsigned)((k + SY_CH * ch + 4 * segs[u]) * 4);
-      dma16<kAuxCached>(rsi, sb + (w + 4 * u) * 1024, offi[u] == kOobOffset ? kOobOffset : offi[u] + cofs);
-      dma16<kAuxCached>(rsj, sb + SY_PANEL + (w + 4 * u) * 1024, offj[u] == kOobOffset ? kOobOffset : offj[u] + cofs);
+      dma16<kAuxCached>(rsi, sb + (w + 4 * u) * 1024, t.offi[u] == kOobOffset ? kOobOffset : t.offi[u] + cofs);
+      dma16<kAuxCached>(rsj, sb + SY_PANEL + (w + 4 * u) * 1024,
+                        t.offj[u] == kOobOffset ? kOobOffset : t.offj[u] + cofs);
     }
   };
-  f32x4 acc[4][4];
+  int qt = blockIdx.x;
+  if (qt >= ntiles) return;
+  Tile cur = tile_of(qt);
+  issue(cur, 0, 0);
+  for (; qt < ntiles; qt += gridDim.x) {
+    const int qn = qt + gridDim.x;
+    const Tile nxt = tile_of(qn < ntiles ? qn : qt);
+    const bool active = !(cur.diag && wc > wr);
+    // this lane's C entries (rows 4 lg + q of each 16-row block, column lr),
+    // loaded under the first chunk's products
+    f32x4 c[4][4];
+    f32x4 acc[4][4];
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb)
+    for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  issue(0, 0);
+      for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int ch = 0; ch < NCH; ++ch) {
-    DR_WAIT_VM(0);
-    DR_LDS_SYNC();
-    if (ch + 1 < NCH) issue(ch + 1, (ch + 1) & 1);
-    if (ch == NCH - 2 && active) load_c();
-    if (active) {
-      const unsigned char* sa = lds + (ch & 1) * 2 * SY_PANEL;
-      const unsigned char* sbp = sa + SY_PANEL;
-#pragma unroll
-      for (int sub = 0; sub < 2; ++sub) {
-        const int seg = 4 * sub + lg;
-        f32x4 fa[4], fb[4];
-#pragma unroll
-        for (int rb = 0; rb < 4; ++rb) fa[rb] = __builtin_bit_cast(f32x4, swz_read(sa + (4 * wr + rb) * 2048, lr, seg));
-#pragma unroll
-        for (int cb = 0; cb < 4; ++cb) fb[cb] = __builtin_bit_cast(f32x4, swz_read(sbp + (4 * wc + cb) * 2048, lr, seg));
+    for (int ch = 0; ch < NCH; ++ch) {
+      DR_WAIT_VM(0);
+      DR_LDS_SYNC();
+      // the last chunk brings in the next tile's first one (stage 0 was
+      // last read by chunk NCH - 2, before this barrier)
+      if (ch + 1 < NCH)
+        issue(cur, ch + 1, (ch + 1) & 1);
+      else if (qn < ntiles)
+        issue(nxt, 0, 0);
+      if (ch == 0 && active) {
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
           for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-            for (int t = 0; t < 4; ++t) acc[rb][cb] = mma_f32(fa[rb][t], fb[cb][t], acc[rb][cb]);
+            for (int q = 0; q < 4; ++q) {
+              const int row = cur.ri + 64 * wr + 16 * rb + 4 * lg + q;
+              const int col = cur.rj + 64 * wc + 16 * cb + lr;
+              c[rb][cb][q] = (row < n && col < n) ? L[(long long)row * ldL + col] : 0.f;
+            }
+      }
+      if (active) {
+        const unsigned char* sa = lds + (ch & 1) * 2 * SY_PANEL;
+        const unsigned char* sbp = sa + SY_PANEL;
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub) {
+          const int seg = 4 * sub + lg;
+          f32x4 fa[4], fb[4];
+#pragma unroll
+          for (int rb = 0; rb < 4; ++rb) fa[rb] = __builtin_bit_cast(f32x4, swz_read(sa + (4 * wr + rb) * 2048, lr, seg));
+#pragma unroll
+          for (int cb = 0; cb < 4; ++cb) fb[cb] = __builtin_bit_cast(f32x4, swz_read(sbp + (4 * wc + cb) * 2048, lr, seg));
+#pragma unroll
+          for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+              for (int t = 0; t < 4; ++t) acc[rb][cb] = mma_f32(fa[rb][t], fb[cb][t], acc[rb][cb]);
+        }
       }
     }
+    if (active) {
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int row = cur.ri + 64 * wr + 16 * rb + 4 * lg + q;
+            const int col = cur.rj + 64 * wc + 16 * cb + lr;
+            if (row < n && col < n && (!cur.diag || col <= row))
+              L[(long long)row * ldL + col] = c[rb][cb][q] - acc[rb][cb][q];
+          }
+    }
+    cur = nxt;
   }
-  if (active) {
-#pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int row = ri + 64 * wr + 16 * rb + 4 * lg + q;
-          const int col = rj + 64 * wc + 16 * cb + lr;
-          if (row < n && col < n && (!diag || col <= row))
-            L[(long long)row * ldL + col] = c[rb][cb][q] - acc[rb][cb][q];
-        }
-  }
-  }   // tiles of this workgroup
 }
 
 // ---------------------------------------------------------------- solves
@@ -694,9 +714,10 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
 // Triangular solves by super-blocks of SB diagonal blocks (1024 rows).
 // After the factorisation, the inverse of every 1024 x 1024 diagonal
 // super-block of L is formed (lower triangle, from the 128 x 128 block
-// inverses); a solve then takes two wide launches per super-block: the
-// super-block's part of the solution as one product with its inverse, and
-// its contribution to the rest of the right-hand side.
+// inverses), and its transpose; a solve then takes two wide launches per
+// super-block: the super-block's part of the solution as one product with
+// its inverse (or the transpose, for L^T), and its contribution to the rest
+// of the right-hand side.
 
 // Block (i, j) = (j + d, j) of the inverse X of super-block S, d >= 1:
 //   X_ij = -X_ii sum_{m=j}^{i-1} L_im X_mj
