@@ -128,6 +128,9 @@ def spd_problem(n, kappa, seed, target_in_span=False):
     (32, 1024, 0.0, RIDGE_ABS),
     (48, 2048, 1e-2, RIDGE_REL_TRACE),
     (63, 4096, 0.0, RIDGE_ABS),
+    (65, 4096, 0.0, RIDGE_ABS),             # 16x16-tile path: one row in the last tile
+    (129, 8192, 1e-2, RIDGE_REL_TRACE),
+    (255, 16384, 0.0, RIDGE_ABS),
 ])
 def test_span_matches_oracle_and_normal_equations(n, kappa, lam, mode):
     G, gbar, K, s, t2 = spd_problem(n, kappa, 100 + n)
@@ -187,7 +190,7 @@ def test_span_special_cases():
     assert torch.all(info == 0) and torch.equal(resid2.cpu(), torch.tensor([1.0, 2.0]))
 
 
-@pytest.mark.parametrize("n", [12, 20, 32, 40, 64, 100])
+@pytest.mark.parametrize("n", [12, 20, 32, 40, 64, 100, 150, 256])
 def test_span_bad_pivot_and_batched_groups(n):
     # group 0: K = diag(1, ..., -1 at j = n - 3, ..., 1) -> info = n - 2 (1-based), w = 0, resid2 = t2;
     # groups 1, 2: random SPD problems of the same n, each against the oracle
@@ -209,6 +212,24 @@ def test_span_bad_pivot_and_batched_groups(n):
         assert rel(host64(w[g]), w_ref) <= TOL_SOLVE
         r2_ref = oracle.span_residual2(host64(K[g]), host64(s[g]), float(t2[g]), w_ref)
         assert abs(float(resid2[g]) - r2_ref) <= 1e-5 * float(t2[g])
+
+
+def test_span_tiles_first_pivot_and_upper_nan():
+    # 64 < n <= 256 (16x16 LDS tiles): a non-positive pivot in the first tile
+    # (factored before the look-ahead starts) and one at the last column
+    for n, j in ((150, 5), (150, 149), (200, 16)):
+        d = torch.ones(n, device=DEV)
+        d[j] = 0.0
+        w, _, resid2, info = api.project_span(torch.diag(d)[None].contiguous(), torch.ones(1, n, device=DEV),
+                                              torch.full((1,), 2.0, device=DEV), 0.0, RIDGE_ABS)
+        torch.cuda.synchronize()
+        assert int(info[0]) == j + 1 and torch.all(w == 0) and float(resid2[0]) == 2.0
+    # a NaN strictly above the diagonal (never factored) is still reported
+    _, _, K, s, t2 = spd_problem(200, 2048, 901)
+    K[0, 3, 170] = float("nan")
+    w, _, _, info = api.project_span(K, s, t2, 0.0, RIDGE_ABS)
+    torch.cuda.synchronize()
+    assert int(info[0]) == -3 and torch.all(w == 0)
 
 
 # ------------------------------------------------------------ span, n > 256 (blocked)
