@@ -258,8 +258,10 @@ def test_span_blocked_matches_oracle(n, kappa, lam, mode):
 
 def test_span_blocked_special_cases():
     n = 400
-    # a non-positive pivot in the second panel and one in the last row
-    for j in (200, n - 1):
+    # non-positive pivots: in the first diagonal tile of the first block, at
+    # the end of the first tile of the second block, inside a later tile of
+    # it (factored one step ahead), and in the last row (a 16-row block)
+    for j in (5, 143, 200, n - 1):
         d = torch.ones(n, device=DEV)
         d[j] = -1.0
         w, _, r2, info = api.project_span(torch.diag(d)[None].contiguous(), torch.ones(1, n, device=DEV),
