@@ -373,6 +373,7 @@ struct PackArgs {
   int N, T;
   int WL, KS;           // workgroups per layer, tiles per workgroup (upper bound)
   int xcd;              // 1: number workgroups XCD by XCD (all layers of the launch alike)
+  int out_vec4;         // 1: S rows and every layer's column offset are 16-byte aligned
   int max_tiles;        // WL * KS: tile slots per layer
   const int* cum;       // [N + 2]: exclusive prefix of the clamped lengths, then R
   const int* tile_ex;   // [max_tiles] example holding the first position of each tile, -1 if empty
@@ -717,12 +718,29 @@ __global__ __launch_bounds__(kThreads, 2) void sketch_packed_kernel(PackArgs a) 
     const bool inside = ce >= p0 && ce1 <= pend;
     float* out = inside ? a.S + (long long)e * a.ldS + L.col_offset
                         : a.partial + (((long long)li * a.max_tiles + tile) * 2 + (e == e0 ? 0 : 1)) * SW;
-    for (int k = tid; k < SW; k += kThreads) {
-      const float v = (red[k] + red[2 * SW + k]) + (red[SW + k] + red[3 * SW + k]);
-      const int l = k & 63, oiq = k >> 6;           // (o * TI + i) * 4 + q
-      const int q = oiq & 3, oi = oiq >> 2;
-      const int o = oi / TI, i = oi - o * TI;
-      out[(o * 16 + (l >> 4) * 4 + q) * KIN + i * 16 + (l & 15)] = v;
+    if (!inside || a.out_vec4) {
+      // four consecutive lanes' entries are four consecutive columns of one
+      // output row: float4 reads of the four regions and one float4 store
+      for (int k = 4 * tid; k < SW; k += 4 * kThreads) {
+        const float4 r0 = *reinterpret_cast<const float4*>(&red[k]);
+        const float4 r1 = *reinterpret_cast<const float4*>(&red[SW + k]);
+        const float4 r2 = *reinterpret_cast<const float4*>(&red[2 * SW + k]);
+        const float4 r3 = *reinterpret_cast<const float4*>(&red[3 * SW + k]);
+        const float4 v = make_float4((r0.x + r2.x) + (r1.x + r3.x), (r0.y + r2.y) + (r1.y + r3.y),
+                                     (r0.z + r2.z) + (r1.z + r3.z), (r0.w + r2.w) + (r1.w + r3.w));
+        const int l = k & 63, oiq = k >> 6;           // (o * TI + i) * 4 + q
+        const int q = oiq & 3, oi = oiq >> 2;
+        const int o = oi / TI, i = oi - o * TI;
+        *reinterpret_cast<float4*>(&out[(o * 16 + (l >> 4) * 4 + q) * KIN + i * 16 + (l & 15)]) = v;
+      }
+    } else {
+      for (int k = tid; k < SW; k += kThreads) {
+        const float v = (red[k] + red[2 * SW + k]) + (red[SW + k] + red[3 * SW + k]);
+        const int l = k & 63, oiq = k >> 6;           // (o * TI + i) * 4 + q
+        const int q = oiq & 3, oi = oiq >> 2;
+        const int o = oi / TI, i = oi - o * TI;
+        out[(o * 16 + (l >> 4) * 4 + q) * KIN + i * 16 + (l & 15)] = v;
+      }
     }
     DR_LDS_SYNC();
   }
@@ -1030,6 +1048,9 @@ extern "C" dr_status dr_sketch_grads(const dr_layer* layers, int num_layers, int
     pa.xcd = 1;
     for (int j = 1; j < l.count; ++j)
       if (pa.L[j].d_in != pa.L[0].d_in || pa.L[j].d_out != pa.L[0].d_out) pa.xcd = 0;
+    pa.out_vec4 = aligned16(S) && ldS % 4 == 0;
+    for (int j = 0; j < l.count; ++j)
+      if (pa.L[j].col_offset % 4 != 0) pa.out_vec4 = 0;
     a.N = pa.N = (int)N;
     a.T = pa.T = (int)T;
     a.chunk_tokens = l.chunk;
