@@ -176,3 +176,21 @@ def test_lengths_on_tile_boundaries():
     lens = torch.tensor([128, 128, 256, 0, 64, 64, 384, 1, 127], dtype=torch.int32, device=DEV)
     layers = custom_layers([(128, 64, 64, 32)], N, T, torch.bfloat16, lens, nan_padding=True, seed=13)
     run_case(layers, lens, N, T, TOL_SKETCH_BF16)
+
+
+def test_unaligned_output_layout_matches_aligned():
+    # column offsets and a row stride that are not multiples of 4 floats take
+    # the scalar store path of the packed kernel: the same sums, bit for bit
+    N, T = 9, 300
+    lens = torch.tensor([0, 1, 130, 255, 256, 257, 299, 300, 77], dtype=torch.int32, device=DEV)
+    specs = [(256, 128, 64, 64), (128, 256, 16, 32)]
+    for dtype in (torch.bfloat16, torch.float32):
+        layers = custom_layers(specs, N, T, dtype, lens, nan_padding=True, seed=5)
+        S_ref = api.sketch(layers, lens)
+        shifted = [dict(L, col_offset=int(L["col_offset"]) + 3) for L in layers]
+        tot = int(S_ref.shape[1])
+        S = torch.full((N, tot + 5), float("nan"), device=DEV)
+        api.dr_sketch_grads(shifted, N, T, lens, S)
+        torch.cuda.synchronize()
+        assert torch.equal(S[:, 3:3 + tot], S_ref)
+        assert torch.isnan(S[:, :3]).all() and torch.isnan(S[:, 3 + tot:]).all()
