@@ -1070,7 +1070,10 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       hipLaunchKernelGGL(lg_syrk_kernel<2 * NB>, dim3(nhead), dim3(256), 0, hs, L, ldL, n, k, h, 1, nhead, ctl);
       if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;
       if (nrest > 0) {
-        const int grid = nrest < rest_slots ? nrest : rest_slots;
+        // many rounds of tiles: the chain has slack, 15/16 of the slots;
+        // under two rounds: the chain is the longer path, 3/4 of them
+        const int slots = nrest >= 8 * cus ? 2 * cus - cus / 8 : (nrest < 4 * cus ? 2 * cus - cus / 2 : rest_slots);
+        const int grid = nrest < slots ? nrest : slots;
         hipLaunchKernelGGL(lg_syrk_kernel<2 * NB>, dim3(grid), dim3(256), 0, hs, L, ldL, n, k, h, 0, nrest, ctl);
       }
     }
