@@ -35,7 +35,7 @@
 //                        m, as target_mean_kernel) and stages the n + 1
 //                        augmented rows in LDS (row stride 132 floats: the
 //                        16 rows x 4 columns of an fp32 MFMA operand fall on
-//                        distinct banks); the four waves take the lower
+//                        distinct banks); the eight waves take the lower
 //                        16x16 blocks of the augmented Gram round-robin
 //                        (fp32 16x16x4 MFMA) and write chunk partials.
 //   gram_small_reduce_kernel : sums the chunk partials (one wave per element,
@@ -190,8 +190,9 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_kernel(GramArgs a) {
 constexpr int kSmCK = 128;           // columns per workgroup
 constexpr int kSmLd = kSmCK + 4;     // LDS row stride (floats)
 constexpr int kSmMaxRows = 128;      // n + 1 <= 128
+constexpr int kSmThreads = 512;      // eight waves share the lower blocks
 
-__global__ __launch_bounds__(kThreads) void gram_small_kernel(GramArgs a, const float* Gt, long long ldGt, int m,
+__global__ __launch_bounds__(kSmThreads) void gram_small_kernel(GramArgs a, const float* Gt, long long ldGt, int m,
                                                               int NRP, int nchunks) {
   __shared__ __attribute__((aligned(16))) float R[kSmMaxRows * kSmLd];
   const int chunk = blockIdx.x, p = blockIdx.y;
@@ -204,20 +205,21 @@ __global__ __launch_bounds__(kThreads) void gram_small_kernel(GramArgs a, const 
   const int width = (int)(g1 - c0 < kSmCK ? g1 - c0 : kSmCK);   // a multiple of 4
   // general rows 0 .. n-1 (float4 loads, eight in flight per thread before
   // any store), zero columns past the group
-  const int c4 = tid & (kSmCK / 4 - 1), r0 = tid / (kSmCK / 4);   // 8 rows per pass
+  constexpr int RPP = kSmThreads / (kSmCK / 4);                    // rows per pass
+  const int c4 = tid & (kSmCK / 4 - 1), r0 = tid / (kSmCK / 4);
   const bool cok = 4 * c4 < width;
-  for (int rb = 0; rb < a.n; rb += 64) {
+  for (int rb = 0; rb < a.n; rb += 8 * RPP) {
     float4 v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int r = rb + r0 + 8 * u;
+      const int r = rb + r0 + RPP * u;
       v[u] = (r < a.n && cok) ? *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(a.G) +
                                                                  (long long)r * a.ldG + c0 + 4 * c4)
                               : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int r = rb + r0 + 8 * u;
+      const int r = rb + r0 + RPP * u;
       if (r < a.n) *reinterpret_cast<float4*>(&R[r * kSmLd + 4 * c4]) = v[u];
     }
   }
@@ -239,13 +241,13 @@ __global__ __launch_bounds__(kThreads) void gram_small_kernel(GramArgs a, const 
     }
     R[a.n * kSmLd + tid] = gv;
   }
-  for (int e = tid; e < (NRP - a.n - 1) * kSmCK; e += kThreads)
+  for (int e = tid; e < (NRP - a.n - 1) * kSmCK; e += kSmThreads)
     R[(a.n + 1 + e / kSmCK) * kSmLd + e % kSmCK] = 0.f;
   __syncthreads();
   // lower blocks (I, J <= I) round-robin over the waves
   const int lr = lane & 15, lk = lane >> 4, lg = lane >> 4;
   const int nblocks = nb * (nb + 1) / 2;
-  for (int q = wave; q < nblocks; q += kThreads / 64) {
+  for (int q = wave; q < nblocks; q += kSmThreads / 64) {
     int I = 0;
     while ((I + 1) * (I + 2) / 2 <= q) ++I;
     const int J = q - I * (I + 1) / 2;
@@ -690,7 +692,7 @@ extern "C" dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* 
       hipLaunchKernelGGL(gram_big_kernel, dim3((chunks + 7) / 8 * 256, gp), dim3(512), 0, hs, b);
       if ((st = launch_status()) != DR_OK) return st;
     } else if (g.small) {
-      hipLaunchKernelGGL(gram_small_kernel, dim3(g.maxchunks, gp), dim3(kThreads), 0, hs, a,
+      hipLaunchKernelGGL(gram_small_kernel, dim3(g.maxchunks, gp), dim3(kSmThreads), 0, hs, a,
                          static_cast<const float*>(Gt), (long long)ldGt, (int)m, g.NRP, g.maxchunks);
       if ((st = launch_status()) != DR_OK) return st;
       const int nr = (int)n + 1;
