@@ -264,7 +264,7 @@ __global__ __launch_bounds__(kSmThreads) void gram_small_kernel(GramArgs a, cons
 
 // K (both triangles), s and t2 from the chunk partials: one wave per element
 // of the lower triangle, lane l sums chunks l, l + 64, ... in order, then a
-// fixed xor tree across the lanes
+// fixed-order DPP reduction across the lanes (total in lane 63)
 __global__ __launch_bounds__(kThreads) void gram_small_reduce_kernel(GramArgs a, int NRP, int nchunks, float* K,
                                                                      float* s, float* t2, long long pbase) {
   const int p = blockIdx.y;
@@ -289,8 +289,8 @@ __global__ __launch_bounds__(kThreads) void gram_small_reduce_kernel(GramArgs a,
 #pragma unroll
     for (int u = 0; u < 4; ++u) acc += v[u];
   }
-  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
-  if (lane != 0) return;
+  acc = wave_sum_l63f(acc);
+  if (lane != 63) return;
   if (r < a.n) {
     float* Kp = K + (pbase + p) * (long long)a.n * a.n;
     Kp[(long long)r * a.n + c] = acc;
