@@ -11,7 +11,10 @@
  *   row-major; a leading dimension is counted in elements.
  * - The caller owns every buffer, including the workspace whose size the
  *   matching *_workspace_size query returns.  The library allocates no
- *   device memory and keeps no state between calls.
+ *   device memory and keeps no data between calls.  The one runtime object
+ *   it keeps: dr_project_span with n > 256 runs its look-ahead on one
+ *   auxiliary stream (default priority) and two events per device, created
+ *   by the first such call on that device and kept until the process ends.
  * - `stream` is a hipStream_t (NULL = the default stream).  Calls only
  *   enqueue work.  The returned dr_status covers argument validation and
  *   launch errors; every argument is validated before the first HIP call,
@@ -100,7 +103,7 @@ const char* dr_status_string(dr_status s);
  *   S[i][col_offset_l + a*k_in + b] =
  *       sum_{t < len[i]} (P_out dy_{i,t})[a] * (P_in x_{i,t})[b],
  * i.e. P_out G_i P_in^T with G_i = sum_t dy_{i,t} x_{i,t}^T the per-sample
- * weight gradient (Sec. 4.1 "Backward pass"; compressed as in App. C.1,
+ * weight gradient (Sec. 4.1 "Backward pass"; compressed as in App. C.3,
  * "Factorized Projection" forward form and "Per-Sample Gradient
  * Compression", with the second-stage projector taken as the identity).
  * G_i is never formed.  Tokens t >= len[i] are padding: they are never
@@ -173,8 +176,12 @@ size_t dr_gram_workspace_size(int64_t n, int64_t m, const int64_t* goff, int P, 
  * Empty feasible set: n = 0 is a valid no-op beyond lam_eff = resid2 = t2,
  * info = 0; a group with trace(K) = 0 under REL_TRACE returns w = 0.
  * A factor pivot that is not positive sets info = its 1-based index and
- * w = 0.  Arithmetic: fp32 Cholesky factor, iterative refinement with
- * fp64 residuals of the fp32 K.
+ * w = 0.  Arithmetic: n <= 64 entirely in fp64 on the exact fp32 K; n > 64
+ * an fp32 Cholesky factor and two steps of iterative refinement with fp64
+ * residuals of the fp32 K.  When those two steps do not bring w to about
+ * 1e-6 relative accuracy (their corrections do not shrink fast enough,
+ * which happens when cond(K + lam_eff I) * 2^-24 is not small), info =
+ * DR_INFO_NOT_CONVERGED and w holds the last iterate.
  * ------------------------------------------------------------------------- */
 dr_status dr_project_span(const float* K, const float* s, const float* t2, int64_t n, int P,
                           float lambda, dr_ridge_mode mode, float* w, float* lam_eff,
@@ -224,7 +231,7 @@ dr_status dr_project_simplex(const float* K, const float* s, const float* t2, in
                              void* stream);
 
 /* ---------------------------------------------------------------------------
- * dr_back_project -- the transpose of the factorised compressor (App. C.1,
+ * dr_back_project -- the transpose of the factorised compressor (App. C.3,
  * "Backward projection"), layer by layer: U + u_offset[l] (row-major
  * [d_out][d_in], fp32) = P_out^T X' P_in with X' the layer's block of the
  * sketch-space vector u (columns col_offset .. + k_out*k_in, read as

@@ -9,7 +9,7 @@ written for a reader who checks it against the paper by eye:
 
 * ``sketch``  -- explicit per-example linear-layer gradients (sum of outer
   products over valid tokens, Sec. 4.1 "Backward pass"), compressed by the
-  factorised projector of App. C.1 ("Factorized Projection", "Per-Sample
+  factorised projector of App. C.3 ("Factorized Projection", "Per-Sample
   Gradient Compression").
 * ``scores``  -- the three exact scorers of Sec. 4.3 (Direct, Ghost Inner
   Product, Per-Token Inner Product); used to pin the sketch oracle.
@@ -23,7 +23,7 @@ written for a reader who checks it against the paper by eye:
 * ``select``  -- thresholding / negative filtering and greedy construction,
   the other subset rules of Sec. 3.3.2.
 * ``simplex`` -- soft weighting over the probability simplex (Sec. 6) and
-  the back-projection Pi^T of App. C.1.
+  the back-projection Pi^T of App. C.3.
 * ``update``  -- the weighted assembly of the update in parameter space
   (Sec. 4.2, post-hoc assembly from the retained pairs).
 * ``brute``   -- exhaustive enumeration for tiny inputs.

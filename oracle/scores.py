@@ -13,7 +13,7 @@ of the contractions:
   T x T cross-correlations per (train, target) pair.
 * Per-Token Inner Product (PIP): sum_tau dL/de_{i,tau}^T  G_star_hat  a_{i,tau}.
 Compressed scoring replaces the two gradients by their sketches and takes
-the inner product in sketch space (Sec. 4.3.4).
+the inner product in sketch space (Sec. 4.3.3).
 
 Rows are token-major here ([T, d]); the paper stores tokens as columns, which
 only transposes the T x T products.  Padding rows (tau >= len) are dropped.

@@ -21,7 +21,7 @@ Definitions followed
   fixed-point residual of a projected-gradient step,
       rho = max_i |w_i - proj(w - grad / L)_i|,  L = 2 max_i sum_j |K_ij|,
   zero exactly at the optimum.
-* Back-projection (App. C.1, "Backward projection"): for a sketch-space
+* Back-projection (App. C.3, "Backward projection"): for a sketch-space
   vector x~ and a layer with first-stage projectors P_in, P_out (second
   stage the identity), Pi^T x~ reshaped to d_out x d_in is
       P_out^T X' P_in,   X' = x~ reshaped to [k_out][k_in] (row-major, the

@@ -5,13 +5,13 @@ Test infrastructure only (see the package header).
 Definitions followed
 --------------------
 * Per-sample weight gradient of a linear layer (Sec. 4.1, "Backward pass";
-  App. C.1 "Per-Sample Gradient Compression"):
+  App. C.3 "Per-Sample Gradient Compression"):
       G_i = sum over tokens tau of  dL/de_{i,tau}  (outer)  a_{i,tau},
   a d_out x d_in matrix.  Only the valid tokens tau < len_i enter the sum:
   padded positions are loss-masked and contribute nothing (they are sliced
   away, never multiplied by zero, so NaN padding cannot leak).
 * Factorised projector Pi = P_final (P_in kron P_out) applied to an
-  outer-product sum (App. C.1 "Forward projection"): each token contributes
+  outer-product sum (App. C.3 "Forward projection"): each token contributes
   the small outer product (P_out b)(P_in a)^T.  With P_final = I this is
       S_i = P_out G_i P_in^T   (kappa_out x kappa_in),
   stored row-major, i.e. element (a, b) at position a*kappa_in + b.

@@ -24,6 +24,32 @@ def _stream(stream):
     return ctypes.c_void_p(int(stream))
 
 
+def _side_stream(stream, device):
+    """The launch stream as a torch stream when it is not the current stream
+    of `device` (None otherwise)."""
+    if stream is None:
+        return None
+    if isinstance(stream, torch.cuda.Stream):
+        ts = stream
+    else:
+        ts = torch.cuda.ExternalStream(int(stream), device=device)
+    if ts.cuda_stream == torch.cuda.current_stream(device).cuda_stream:
+        return None
+    return ts
+
+
+def _keep(stream, *tensors):
+    """Tensors allocated here on the current stream but used by work enqueued
+    on another stream: tell the caching allocator, so that their memory is
+    not handed out again before that stream's work has finished."""
+    for t in tensors:
+        if t is None:
+            continue
+        ts = _side_stream(stream, t.device)
+        if ts is not None:
+            t.record_stream(ts)
+
+
 def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
@@ -40,11 +66,12 @@ def _contig(t, name):
         raise ValueError(f"{name} must be contiguous")
 
 
-def _workspace(nbytes, device, workspace):
+def _workspace(nbytes, device, workspace, stream=None):
     if nbytes == 0:
         return None, 0
     if workspace is None:
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        _keep(stream, workspace)
     if workspace.numel() * workspace.element_size() < nbytes:
         raise ValueError("workspace too small")
     return workspace, workspace.numel() * workspace.element_size()
@@ -97,7 +124,7 @@ def dr_sketch_grads(layers, N, T, lengths, S, workspace=None, stream=None):
         _contig(lengths, "lengths")
     arr = make_layer_array(layers)
     nbytes = lib.dr_sketch_workspace_size(arr, len(layers), N, T, _DTYPES[dtype])
-    ws, wsb = _workspace(nbytes, S.device, workspace)
+    ws, wsb = _workspace(nbytes, S.device, workspace, stream)
     check("dr_sketch_grads", lib.dr_sketch_grads(arr, len(layers), N, T, _ptr(lengths), _DTYPES[dtype], _ptr(S),
                                                  S.stride(0), _ptr(ws), wsb, _stream(stream)))
     return S
@@ -121,7 +148,7 @@ def dr_gram(G, Gt, goff, K, s, t2, workspace=None, stream=None):
     P = len(goff) - 1
     ga = _goff_array(goff)
     nbytes = lib.dr_gram_workspace_size(n, m, ga, P, _DTYPES[dtype])
-    ws, wsb = _workspace(nbytes, Gt.device, workspace)
+    ws, wsb = _workspace(nbytes, Gt.device, workspace, stream)
     check("dr_gram", lib.dr_gram(_ptr(G), n, G.stride(0) if n > 0 else 0, _ptr(Gt), m, Gt.stride(0),
                                  _DTYPES[dtype], ga, P, _ptr(K), _ptr(s), _ptr(t2), _ptr(ws), wsb,
                                  _stream(stream)))
@@ -141,7 +168,7 @@ def dr_project_span(K, s, t2, lam, mode, w, lam_eff, resid2, info, workspace=Non
         _contig(t, nm)
     _dev(info, "info", torch.int32)
     nbytes = lib.dr_span_workspace_size(n, P)
-    ws, wsb = _workspace(nbytes, t2.device, workspace)
+    ws, wsb = _workspace(nbytes, t2.device, workspace, stream)
     check("dr_project_span", lib.dr_project_span(_ptr(K), _ptr(s), _ptr(t2), n, P, float(lam), int(mode), _ptr(w),
                                                  _ptr(lam_eff), _ptr(resid2), _ptr(info), _ptr(ws), wsb,
                                                  _stream(stream)))
@@ -201,7 +228,7 @@ def dr_back_project(layers, u, U, u_offset, workspace=None, stream=None):
     _dev(u, "u", torch.float32)
     _dev(U, "U", torch.float32)
     arr = _projector_layer_array(layers)
-    ws, wsb = _workspace(lib.dr_backproject_workspace_size(arr, len(layers)), U.device, workspace)
+    ws, wsb = _workspace(lib.dr_backproject_workspace_size(arr, len(layers)), U.device, workspace, stream)
     check("dr_back_project", lib.dr_back_project(arr, len(layers), _DTYPES[dtype], _ptr(u), _ptr(U),
                                                  _goff_array(u_offset), _ptr(ws), wsb, _stream(stream)))
     return U
@@ -253,7 +280,7 @@ def dr_select_greedy(K, s, k, idx, w, info, workspace=None, stream=None):
     _dev(info, "info", torch.int32)
     if w is not None:
         _dev(w, "w", torch.float32)
-    ws, wsb = _workspace(lib.dr_greedy_workspace_size(n, P), s.device, workspace)
+    ws, wsb = _workspace(lib.dr_greedy_workspace_size(n, P), s.device, workspace, stream)
     check("dr_select_greedy", lib.dr_select_greedy(_ptr(K), _ptr(s), n, P, k, _ptr(idx), _ptr(w), _ptr(info), _ptr(ws),
                                                    wsb, _stream(stream)))
 
@@ -274,7 +301,7 @@ def dr_combine(G, goff, w, u, workspace=None, stream=None):
     P = len(goff) - 1
     ga = _goff_array(goff)
     nbytes = lib.dr_combine_workspace_size(n, ga, P)
-    ws, wsb = _workspace(nbytes, u.device, workspace)
+    ws, wsb = _workspace(nbytes, u.device, workspace, stream)
     check("dr_combine", lib.dr_combine(_ptr(G), n, G.stride(0) if n > 0 else 0, _DTYPES[dtype], ga, P, _ptr(w),
                                        _ptr(u), _ptr(ws), wsb, _stream(stream)))
 
@@ -323,7 +350,7 @@ def dr_assemble_update(layers, n, T, lengths, w, U, u_offset, group_of_layer=Non
     if group_of_layer is not None:
         gol = (ctypes.c_int32 * len(layers))(*[int(v) for v in group_of_layer])
     nbytes = lib.dr_update_workspace_size(arr, len(layers), n, T, _DTYPES[dtype])
-    ws, wsb = _workspace(nbytes, U.device, workspace)
+    ws, wsb = _workspace(nbytes, U.device, workspace, stream)
     check("dr_assemble_update", lib.dr_assemble_update(
         arr, len(layers), n, T, _ptr(lengths), _DTYPES[dtype], _ptr(w), w.shape[0], w.stride(0), gol, _ptr(U), offs,
         _ptr(ws), wsb, _stream(stream)))
@@ -352,7 +379,7 @@ def dr_score_exact(layers, n, m, T, lengths, method, s, workspace=None, stream=N
     arr = make_update_layer_array(layers)
     meth = _SCORE_METHODS[method]
     nbytes = lib.dr_score_workspace_size(arr, len(layers), n, m, T, _lib.DR_BF16, meth)
-    ws, wsb = _workspace(nbytes, s.device, workspace)
+    ws, wsb = _workspace(nbytes, s.device, workspace, stream)
     check("dr_score_exact", lib.dr_score_exact(arr, len(layers), n, m, T, _ptr(lengths), _lib.DR_BF16, meth, _ptr(s),
                                                _ptr(ws), wsb, _stream(stream)))
     return s
@@ -366,6 +393,7 @@ def sketch(layers, lengths=None, stream=None):
     N, T = layers[0]["x"].shape[:2]
     kt = max(int(L["col_offset"]) + L["p_in"].shape[0] * L["p_out"].shape[0] for L in layers)
     S = torch.empty(N, kt, dtype=torch.float32, device=layers[0]["x"].device)
+    _keep(stream, S)
     return dr_sketch_grads(layers, N, T, lengths, S, stream=stream)
 
 
@@ -377,6 +405,7 @@ def gram(G, Gt, goff=None, stream=None):
     K = torch.empty(P, n, n, dtype=torch.float32, device=dev)
     s = torch.empty(P, n, dtype=torch.float32, device=dev)
     t2 = torch.empty(P, dtype=torch.float32, device=dev)
+    _keep(stream, K, s, t2)
     dr_gram(G, Gt, goff, K, s, t2, stream=stream)
     return K, s, t2
 
@@ -388,6 +417,7 @@ def project_span(K, s, t2, lam, mode=_lib.DR_RIDGE_REL_TRACE, stream=None):
     lam_eff = torch.empty(P, dtype=torch.float32, device=dev)
     resid2 = torch.empty(P, dtype=torch.float32, device=dev)
     info = torch.empty(P, dtype=torch.int32, device=dev)
+    _keep(stream, w, lam_eff, resid2, info)
     dr_project_span(K, s, t2, lam, mode, w, lam_eff, resid2, info, stream=stream)
     return w, lam_eff, resid2, info
 
@@ -400,6 +430,7 @@ def project_cone(K, s, t2, max_iter, kkt_tol=0.0, stream=None):
     iters = torch.empty(P, dtype=torch.int32, device=dev)
     kkt = torch.empty(P, dtype=torch.float32, device=dev)
     info = torch.empty(P, dtype=torch.int32, device=dev)
+    _keep(stream, w, resid2, iters, kkt, info)
     dr_project_cone(K, s, t2, max_iter, kkt_tol, w, resid2, iters, kkt, info, stream=stream)
     return w, resid2, iters, kkt, info
 
@@ -410,6 +441,7 @@ def select_topk(s, k, with_weights=True, stream=None):
     idx = torch.empty(P, k, dtype=torch.int32, device=dev)
     w = torch.empty(P, n, dtype=torch.float32, device=dev) if with_weights else None
     info = torch.empty(P, dtype=torch.int32, device=dev)
+    _keep(stream, idx, w, info)
     dr_select_topk(s, k, idx, w, info, stream=stream)
     return idx, w, info
 
@@ -418,6 +450,11 @@ def combine(G, w, goff=None, stream=None):
     if goff is None:
         goff = [0, G.shape[1]]
     u = torch.zeros(goff[-1], dtype=torch.float32, device=w.device)
+    _keep(stream, u)
+    ts = _side_stream(stream, u.device)
+    if ts is not None:
+        # the zero fill runs on the current stream: order the combine after it
+        ts.wait_stream(torch.cuda.current_stream(u.device))
     dr_combine(G, goff, w, u, stream=stream)
     return u
 
@@ -432,6 +469,7 @@ def assemble_update(layers, w, n=None, lengths=None, group_of_layer=None, stream
         offs.append(o)
         o += sz
     U = torch.empty(o, dtype=torch.float32, device=w.device)
+    _keep(stream, U)
     dr_assemble_update(layers, n, T, lengths, w, U, offs, group_of_layer=group_of_layer, stream=stream)
     return [U[a:a + sz].view(L["dy"].shape[2], L["x"].shape[2]) for a, sz, L in zip(offs, sizes, layers)]
 
@@ -444,6 +482,7 @@ def select_threshold(s, tau=0.0, inclusive=True, stream=None):
     count = torch.empty(P, dtype=torch.int32, device=dev)
     w = torch.empty(P, n, dtype=torch.float32, device=dev)
     info = torch.empty(P, dtype=torch.int32, device=dev)
+    _keep(stream, idx, count, w, info)
     dr_select_threshold(s, tau, inclusive, idx, count, w, info, stream=stream)
     return idx, count, w, info
 
@@ -454,6 +493,7 @@ def select_greedy(K, s, k, stream=None):
     idx = torch.empty(P, k, dtype=torch.int32, device=dev)
     w = torch.empty(P, n, dtype=torch.float32, device=dev)
     info = torch.empty(P, dtype=torch.int32, device=dev)
+    _keep(stream, idx, w, info)
     dr_select_greedy(K, s, k, idx, w, info, stream=stream)
     return idx, w, info
 
@@ -462,6 +502,7 @@ def score_exact(layers, n, m, lengths=None, method="pip", stream=None):
     """Per-layer exact scores [num_layers, n] of the first n rows against the mean of the next m."""
     T = layers[0]["x"].shape[1]
     s = torch.empty(len(layers), n, dtype=torch.float32, device=layers[0]["x"].device)
+    _keep(stream, s)
     return dr_score_exact(layers, n, m, T, lengths, method, s, stream=stream)
 
 
@@ -473,6 +514,7 @@ def project_simplex(K, s, t2, max_iter=2000, tol=1e-7, stream=None):
     iters = torch.empty(P, dtype=torch.int32, device=dev)
     res = torch.empty(P, dtype=torch.float32, device=dev)
     info = torch.empty(P, dtype=torch.int32, device=dev)
+    _keep(stream, w, resid2, iters, res, info)
     dr_project_simplex(K, s, t2, max_iter, tol, w, resid2, iters, res, info, stream=stream)
     return w, resid2, iters, res, info
 
@@ -485,5 +527,6 @@ def back_project(layers, u, stream=None):
         offs.append(o)
         o += sz
     U = torch.empty(o, dtype=torch.float32, device=u.device)
+    _keep(stream, U)
     dr_back_project(layers, u, U, offs, stream=stream)
     return [U[a:a + sz].view(L["p_out"].shape[1], L["p_in"].shape[1]) for a, sz, L in zip(offs, sizes, layers)]

@@ -3,7 +3,7 @@
 // P_out (second stage the identity), the transpose of the factorised
 // compressor maps the layer's block x~ of a sketch-space vector to
 //   U_l = P_out^T X' P_in,  X' = x~ as [k_out][k_in]     (d_out x d_in)
-// (App. C.1, "Backward projection"), never forming Pi^T.  Applied to the
+// (App. C.3, "Backward projection"), never forming Pi^T.  Applied to the
 // sketch-space update u~ = G~^T w it gives the parameter-space update of the
 // MeSO variant of the layer-wise algorithm.
 //

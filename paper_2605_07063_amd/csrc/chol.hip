@@ -50,6 +50,8 @@
 // non-finite input, an empty span, a non-positive pivot) the remaining
 // launches of that group return at once.
 
+#include <mutex>
+
 #include "common.h"
 
 namespace dr {
@@ -67,6 +69,7 @@ struct LgCtl {
   int nonfinite;   // some entry of K or s is not finite
   int info;        // reported info (1-based pivot, or DR_INFO_NONFINITE)
   float lam;       // lam_eff
+  double dxn[kRefine + 1];   // max |dx| of each solve (the first solve's dx is x itself)
 };
 
 struct LgLayout {
@@ -124,6 +127,7 @@ __global__ void lg_init_kernel(LgCtl* ctl, const float* s, int n, int npad, doub
     ctl->nonfinite = 0;
     ctl->info = 0;
     ctl->lam = 0.f;
+    for (int k = 0; k <= kRefine; ++k) ctl->dxn[k] = 0.0;
   }
   if (i < npad) {
     x[i] = 0.0;
@@ -909,10 +913,23 @@ __global__ __launch_bounds__(kColThreads) void lg_coldot_kernel(const float* M, 
   }
 }
 
-__global__ void lg_axpy_kernel(double* x, const double* dx, int npad, const LgCtl* ctl) {
+// x += dx, and the solve's max |dx| into ctl->dxn[it] (one workgroup)
+__global__ __launch_bounds__(1024) void lg_axpy_kernel(double* x, const double* dx, int npad, int it, LgCtl* ctl) {
+  __shared__ double sh[16];
   if (ctl->skip) return;
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < npad) x[i] += dx[i];
+  double m = 0.0;
+  for (int i = threadIdx.x; i < npad; i += 1024) {
+    x[i] += dx[i];
+    m = fmax(m, fabs(dx[i]));
+  }
+  for (int off = 32; off > 0; off >>= 1) m = fmax(m, __shfl_xor(m, off, 64));
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double r = 0.0;
+    for (int q = 0; q < 16; ++q) r = fmax(r, sh[q]);
+    ctl->dxn[it] = r;
+  }
 }
 
 // r = s - (K + lam I) x and kx = K x in fp64, one wave per row of K
@@ -943,20 +960,27 @@ __global__ __launch_bounds__(1024) void lg_final_kernel(const float* s, const fl
                                                         const double* kx, const LgCtl* ctl, float* w, float* resid2,
                                                         int* info) {
   __shared__ double sh[16];
+  __shared__ double shm[16];
   const bool skip = ctl->skip != 0;
-  double q = 0.0;
+  double q = 0.0, xm = 0.0;
   for (int i = threadIdx.x; i < n; i += 1024) {
     if (skip) {
       w[i] = 0.f;
     } else {
       w[i] = (float)x[i];
       q += x[i] * kx[i] - 2.0 * (double)s[i] * x[i];
+      xm = fmax(xm, fabs(x[i]));
     }
   }
-  q = block_sum_d<1024>(q, sh);
+  for (int off = 32; off > 0; off >>= 1) xm = fmax(xm, __shfl_xor(xm, off, 64));
+  if ((threadIdx.x & 63) == 0) shm[threadIdx.x >> 6] = xm;
+  q = block_sum_d<1024>(q, sh);   // its barriers also publish shm
   if (threadIdx.x == 0) {
+    double X = 0.0;
+    for (int k = 0; k < 16; ++k) X = fmax(X, shm[k]);
+    const bool converged = refine_converged(ctl->dxn[kRefine - 1], ctl->dxn[kRefine], X);
     resid2[0] = skip ? t2[0] : (float)((double)t2[0] + q);
-    info[0] = skip ? ctl->info : 0;
+    info[0] = skip ? ctl->info : (converged ? 0 : DR_INFO_NOT_CONVERGED);
   }
 }
 
@@ -969,6 +993,23 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
                                    const LgLayout& lay, unsigned char* base, hipStream_t hs, hipStream_t aux,
                                    hipEvent_t ev_col, hipEvent_t ev_next);
 
+// The look-ahead stream (default priority) and its two events: one set per
+// device, created by the first blocked solve on that device and kept until
+// the process ends, so a call creates and destroys nothing.  A call holds
+// its device's lock while it enqueues, so that the records of ev_col /
+// ev_next and the waits on them pair up when several host threads call at
+// once (their work then shares the look-ahead stream in call order).
+namespace {
+constexpr int kMaxDevices = 64;
+struct AuxSet {
+  std::mutex mu;
+  bool ready = false;
+  hipStream_t aux = nullptr;
+  hipEvent_t ev_col = nullptr, ev_next = nullptr;
+};
+AuxSet g_aux[kMaxDevices];
+}  // namespace
+
 dr_status span_large(const float* K, const float* s, const float* t2, int64_t n64, int P, float lambda, int mode,
                      float* w, float* lam_eff, float* resid2, int32_t* info, void* ws, size_t ws_bytes,
                      hipStream_t hs) {
@@ -977,22 +1018,24 @@ dr_status span_large(const float* K, const float* s, const float* t2, int64_t n6
   if (!aligned16(ws)) return DR_ERR_ARG;
   const int n = (int)n64;
   unsigned char* base = static_cast<unsigned char*>(ws);
-  // the look-ahead stream (default priority) and its two events live for this call only
-  hipStream_t aux = nullptr;
-  hipEvent_t ev_col = nullptr, ev_next = nullptr;
-  if (hipStreamCreateWithFlags(&aux, hipStreamNonBlocking) != hipSuccess) return DR_ERR_HIP;
-  if (hipEventCreateWithFlags(&ev_col, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&ev_next, hipEventDisableTiming) != hipSuccess) {
-    if (ev_col) (void)hipEventDestroy(ev_col);
-    (void)hipStreamDestroy(aux);
-    return DR_ERR_HIP;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return DR_ERR_HIP;
+  AuxSet& a = g_aux[dev];
+  std::lock_guard<std::mutex> lock(a.mu);
+  if (!a.ready) {
+    if (hipStreamCreateWithFlags(&a.aux, hipStreamNonBlocking) != hipSuccess) return DR_ERR_HIP;
+    if (hipEventCreateWithFlags(&a.ev_col, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&a.ev_next, hipEventDisableTiming) != hipSuccess) {
+      if (a.ev_col) (void)hipEventDestroy(a.ev_col);
+      (void)hipStreamDestroy(a.aux);
+      a.aux = nullptr;
+      a.ev_col = nullptr;
+      return DR_ERR_HIP;
+    }
+    a.ready = true;
   }
-  const dr_status st_all = span_large_groups(K, s, t2, n, P, lambda, mode, w, lam_eff, resid2, info, lay, base, hs,
-                                             aux, ev_col, ev_next);
-  (void)hipEventDestroy(ev_col);
-  (void)hipEventDestroy(ev_next);
-  (void)hipStreamDestroy(aux);
-  return st_all;
+  return span_large_groups(K, s, t2, n, P, lambda, mode, w, lam_eff, resid2, info, lay, base, hs, a.aux, a.ev_col,
+                           a.ev_next);
 }
 
 static dr_status span_large_groups(const float* K, const float* s, const float* t2, int n, int P, float lambda,
@@ -1107,7 +1150,7 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
           hipLaunchKernelGGL(lg_coldot_kernel, dim3(o0 / 64), dim3(kColThreads), 0, hs, L + (long long)o0 * ldL, ldL,
                              rows, dx + o0, z, ctl);
       }
-      hipLaunchKernelGGL(lg_axpy_kernel, dim3((npad + 255) / 256), dim3(256), 0, hs, x, dx, npad, ctl);
+      hipLaunchKernelGGL(lg_axpy_kernel, dim3(1), dim3(1024), 0, hs, x, dx, npad, it, ctl);
     }
     hipLaunchKernelGGL(lg_resid_kernel, dim3((n + 3) / 4), dim3(256), 0, hs, Kp, n, sp, x, r, z, ctl);
     hipLaunchKernelGGL(lg_final_kernel, dim3(1), dim3(1024), 0, hs, sp, t2 + p, n, x, z, ctl, w + (long long)p * n,

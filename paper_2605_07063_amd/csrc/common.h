@@ -112,6 +112,19 @@ __device__ __forceinline__ float wave_sum_l63f(float v) {
   return v;
 }
 
+// Mixed-precision iterative refinement (fp32 factor, fp64 residuals) of a
+// span solve: a = max|dx| of the next-to-last correction, b = max|dx| of
+// the last one, X = max|x| after it.  The corrections shrink geometrically
+// with rate about b / a, so b * b / a estimates the error left in x.  The
+// solve counts as converged when the last correction is negligible, or
+// when the corrections contract and that estimate is below 1e-6 of |x|
+// (ten times under the 1e-5 relative accuracy the span solve promises).
+__device__ __forceinline__ bool refine_converged(double a, double b, double X) {
+  if (!(b <= 1e300) || !(X <= 1e300)) return false;   // NaN or inf
+  if (b <= 1e-9 * X) return true;
+  return b <= 0.5 * a && b * b <= 1e-6 * X * a;
+}
+
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 inline dr_status launch_status() {

@@ -2,7 +2,7 @@
 //
 // For example i and layer l the sketch is P_out G_i P_in^T with
 // G_i = sum_{t < len_i} dy_{i,t} x_{i,t}^T (per-sample weight gradient,
-// Sec. 4.1; factorised compression of App. C.1 with the identity as
+// Sec. 4.1; factorised compression of App. C.3 with the identity as
 // second-stage projector).  G_i is never formed: per token tile
 //   stage 1:  Y = X P_in^T  [tokens x k_in],  D = dY P_out^T  [tokens x k_out]
 //             (bf16 or fp32 MFMA, fp32 accumulate, contraction over d)

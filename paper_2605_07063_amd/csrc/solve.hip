@@ -71,6 +71,25 @@ __device__ double block_sum(double v, double* scratch) {
   return r;
 }
 
+// block-wide maximum of |v| over NT threads
+template <int NT>
+__device__ double block_absmax(double v, double* scratch) {
+  const int tid = threadIdx.x;
+  v = fabs(v);
+  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_down(v, off, 64));
+  if ((tid & 63) == 0) scratch[tid >> 6] = v;
+  __syncthreads();
+  if (tid == 0) {
+    double r = 0.0;
+    for (int w = 0; w < NT / 64; ++w) r = fmax(r, scratch[w]);
+    scratch[NT / 64] = r;
+  }
+  __syncthreads();
+  const double r = scratch[NT / 64];
+  __syncthreads();
+  return r;
+}
+
 constexpr int kWaveN = 64;
 
 __device__ __forceinline__ double wave_sum(double v) {
@@ -472,14 +491,23 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
   __syncthreads();
 
   // two steps of iterative refinement: y = s - (K + lam I) x in fp64 from
-  // the fp32 K, solve, x += y
+  // the fp32 K, solve, x += y; the sizes of the two corrections decide
+  // whether the refinement converged
+  double dxmax[2];
   for (int it = 0; it < 2; ++it) {
     kx_rows([&](int i, double kx) { y[i] = (double)sp[i] - (double)lam * x[i] - kx; });
     __syncthreads();
     chol_solve();
-    for (int i = tid; i < n; i += kSpanThreads) x[i] += y[i];
-    __syncthreads();
+    double dm = 0.0;
+    for (int i = tid; i < n; i += kSpanThreads) {
+      x[i] += y[i];
+      dm = fmax(dm, fabs(y[i]));
+    }
+    dxmax[it] = block_absmax<kSpanThreads>(dm, scratch);
   }
+  double xm = 0.0;
+  for (int i = tid; i < n; i += kSpanThreads) xm = fmax(xm, fabs(x[i]));
+  const bool converged = refine_converged(dxmax[0], dxmax[1], block_absmax<kSpanThreads>(xm, scratch));
 
   // resid2 = t2 - 2 s.x + x.K.x
   double part = 0.0;
@@ -489,7 +517,7 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
   if (tid == 0) {
     lam_eff_out[p] = lam;
     resid2[p] = (float)((double)t2[p] + q);
-    info[p] = 0;
+    info[p] = converged ? 0 : DR_INFO_NOT_CONVERGED;
   }
 }
 

@@ -151,6 +151,45 @@ def sketch_inputs(cfg, device, layers=None, nan_padding=False, **over):
     return out, lens, off
 
 
+def llama_step_inputs(cfg, device, buffers=2, blocks=None):
+    """The whole Llama-shaped step: 32 blocks x 7 maps, 224 sketch column
+    blocks of 32 x 32 (229376 columns in all).
+
+    One block's retained pairs are 45.6 GB of bf16 (272 examples x 1024
+    tokens over the seven maps), and the step's 32 blocks (1.46 TB) do not
+    fit in HBM at once, so `buffers` blocks of activations are drawn and
+    kept resident: block b reads the activations of block b % buffers.  Its
+    projectors are its own (seeded by the map index 7 b + j) and it writes
+    its own column range.  Every sketch call still streams a whole block
+    from HBM (far above the last-level cache), so the reuse changes the
+    values, not the traffic.  Returns (blocks: list of 7-layer lists with
+    col_offset set, lens, k_tot)."""
+    nb = len(cfg["layers"]) // len(LLAMA_BLOCK)
+    blocks = list(range(nb)) if blocks is None else list(blocks)
+    lens = lengths(cfg, device)
+    kk = cfg["k_in"] * cfg["k_out"]
+    acts = {}
+    out = []
+    for b in blocks:
+        src = b % buffers
+        if src not in acts:
+            acts[src] = []
+            for j in range(len(LLAMA_BLOCK)):
+                L = layer_inputs(cfg, 7 * src + j, device, lens=lens)
+                acts[src].append((L["x"], L["dy"]))
+        blk = []
+        for j in range(len(LLAMA_BLOCK)):
+            l = 7 * b + j
+            di, do = cfg["layers"][l]
+            x, dy = acts[src][j]
+            blk.append(dict(x=x, dy=dy,
+                            p_in=projector(cfg["k_in"], di, cfg["dtype"], device, cfg["cid"], S_PIN, l),
+                            p_out=projector(cfg["k_out"], do, cfg["dtype"], device, cfg["cid"], S_POUT, l),
+                            col_offset=l * kk))
+        out.append(blk)
+    return out, lens, len(cfg["layers"]) * kk
+
+
 def gram_rows(cfg, device, rows=None, dim=None):
     """Pre-sketched rows Z + scale * C B (rank-r shared component), bf16."""
     cid = cfg["cid"]

@@ -84,7 +84,7 @@ def test_sum_of_per_example_gradients_is_the_batch_weight_gradient():
 
 
 def test_factorised_sketch_equals_explicit_kronecker_projector():
-    """Pi = P_in kron P_out acting on vec(G) (App. C.1) equals P_out G P_in^T
+    """Pi = P_in kron P_out acting on vec(G) (App. C.3) equals P_out G P_in^T
     stored [k_out][k_in]: with row-major vec, kron(P_out, P_in) vec(G)."""
     rng = np.random.default_rng(3)
     d_in, d_out, k_in, k_out, T = 9, 7, 3, 4, 5
@@ -305,6 +305,15 @@ def test_cone_hand_fixture(golden_dir):
     for c in fx["cases"]:
         w, _ = oracle.cone_ref(fx["K"], c["s"])
         np.testing.assert_allclose(w, c["w"], rtol=1e-14, atol=1e-14)
+
+
+def test_cone_kkt_residual_hand_fixture_away_from_the_optimum(golden_dir):
+    """rho at non-optimal points, hand-computed: a wrong power of D in the
+    scaling, a flipped gradient sign or a dropped scaling all change it."""
+    fx = _load(golden_dir, "cone_kkt_hand.json")
+    for c in fx["cases"]:
+        rho = oracle.cone_kkt_residual(c["K"], c["s"], c["w"])
+        assert math.isclose(rho, c["rho"], rel_tol=1e-14), (c, rho)
 
 
 @pytest.mark.parametrize("seed", range(6))
