@@ -114,27 +114,37 @@ def _host_cores():
 
 
 def measured_peaks(dev):
-    """Peaks measured on this GPU with library kernels: a 4 GiB
-    device-to-device copy (bytes read + written per second) and 8192^3
-    dense products in bf16 and fp32 (torch.matmul -> hipBLASLt)."""
+    """Ceilings measured on this GPU by the probe library (libdrprobe.so):
+    a plain streaming read of 8 GiB (every byte once), and MFMA issue
+    loops on register operands in bf16 (16x16x32) and fp32 (16x16x4), the
+    instruction shapes the library's kernels use."""
+    import ctypes
     import torch
+    from paper_2605_07063_amd import build as _build
+    lib = ctypes.CDLL(_build.PROBE_LIB)
+    lib.dr_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+    lib.dr_probe_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+    cur = lambda: ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     res = {}
-    nb = 4 << 30
-    src = torch.empty(nb, dtype=torch.uint8, device=dev)
-    dst = torch.empty_like(src)
-    ms = _event_ms(lambda: dst.copy_(src), 10)
-    res["hbm_copy_GBs"] = 2.0 * nb / (ms * 1e-3) / 1e9
-    del src, dst
-    for name, dt in (("bf16_gemm_TFLOPs", torch.bfloat16), ("fp32_gemm_TFLOPs", torch.float32)):
-        a = torch.randn(8192, 8192, device=dev).to(dt)
-        b = torch.randn(8192, 8192, device=dev).to(dt)
-        c = torch.empty(8192, 8192, device=dev, dtype=dt)
-        ms = _event_ms(lambda: torch.matmul(a, b, out=c), 10)
-        res[name] = 2.0 * 8192 ** 3 / (ms * 1e-3) / 1e12
-        del a, b, c
+    nb = 8 << 30
+    buf = torch.empty(nb, dtype=torch.uint8, device=dev)
+    buf.fill_(1)
+    best = 0.0
+    for blocks in (2048, 4096, 8192):
+        sink = torch.empty(blocks, device=dev)
+        ms = _event_ms(lambda: lib.dr_probe_read(buf.data_ptr(), nb, sink.data_ptr(), blocks, cur()), 5)
+        best = max(best, nb / (ms * 1e-3) / 1e9)
+    res["hbm_read_GBs"] = best
+    del buf
+    blocks, iters = 2048, 512
+    sink = torch.empty(blocks * 256, device=dev)
+    for name, bf, flop in (("bf16_mfma_TFLOPs", 1, 16384.0), ("fp32_mfma_TFLOPs", 0, 2048.0)):
+        ms = _event_ms(lambda: lib.dr_probe_mfma(bf, iters, sink.data_ptr(), blocks, cur()), 5)
+        res[name] = blocks * 4 * 8 * iters * flop / (ms * 1e-3) / 1e12
     torch.cuda.empty_cache()
-    res["how"] = ("4 GiB torch copy_ (read + write bytes / time); 8192^3 torch.matmul in bf16 and fp32, "
-                  "10 calls each after one untimed")
+    res["how"] = ("probe library: streaming read of 8 GiB (best of 2048 / 4096 / 8192 workgroups of 256 threads, "
+                  "16-byte loads, four in flight per lane); MFMA loops of 8 independent accumulators per wave, "
+                  "2048 workgroups of 4 waves, 512 iterations; 5 timed calls each after one untimed")
     return res
 
 
@@ -250,7 +260,7 @@ def run_llama(args, api, _lib, workloads, dev, peaks):
         "roofline": _roofline(
             "dr_sketch_grads, one block of 7 maps (sketch_plan_kernel + sketch_packed_kernel + "
             "sketch_packed_reduce_kernel)", "hbm", by, avg_blk, HBM_PEAK_GBS, "GB/s",
-            measured_peak=peaks.get("hbm_copy_GBs") if peaks else None, traffic=traffic,
+            measured_peak=peaks.get("hbm_read_GBs") if peaks else None, traffic=traffic,
             algorithmic_bytes=by, avg_launch_ms=avg_blk, timed_calls=int(blk_ms.size)),
         "gram_roofline": _roofline("dr_gram (fp32 rows: gram_tile_kernel + reduce + target mean + scores)", "hbm",
                                    N * ktot * 4.0, stage["gram"], HBM_PEAK_GBS, "GB/s",
@@ -480,7 +490,7 @@ def run_small(args, api, _lib, workloads, dev, peaks, with_cpu, with_next):
         "valid_tokens": int(lens.sum()),
         "roofline": _roofline("dr_sketch_grads (sketch_plan_kernel + sketch_packed_kernel + "
                               "sketch_packed_reduce_kernel)", "hbm", by, stage_ms["sketch"], HBM_PEAK_GBS, "GB/s",
-                              measured_peak=peaks.get("hbm_copy_GBs") if peaks else None,
+                              measured_peak=peaks.get("hbm_read_GBs") if peaks else None,
                               traffic=measured_traffic("small_block"), algorithmic_bytes=by,
                               avg_launch_ms=stage_ms["sketch"], timed_calls=steps),
     }
@@ -588,11 +598,11 @@ def run_gram_dominated(api, _lib, workloads, dev, peaks, with_cpu, reps=3):
         "projection_steps_per_s": 1e3 / (gram_ms + span_ms + topk_ms),
         "gram_roofline": _roofline("dr_gram (gram_big_kernel + target mean + scores)", "mfma", flops, gram_ms,
                                    BF16_MFMA_PEAK_TFLOPS, "TFLOP/s",
-                                   measured_peak=peaks.get("bf16_gemm_TFLOPs") if peaks else None,
+                                   measured_peak=peaks.get("bf16_mfma_TFLOPs") if peaks else None,
                                    algorithmic_flops=flops),
         "span_roofline": _roofline("dr_project_span at n = 16384 (blocked Cholesky + 2 refinement steps), n^3/3 "
                                    "factor flops", "mfma", n ** 3 / 3.0, span_ms, F32_MFMA_PEAK_TFLOPS, "TFLOP/s",
-                                   measured_peak=peaks.get("fp32_gemm_TFLOPs") if peaks else None,
+                                   measured_peak=peaks.get("fp32_mfma_TFLOPs") if peaks else None,
                                    algorithmic_flops=n ** 3 / 3.0),
         "lam_eff": float(le[0]),
     }
@@ -664,7 +674,7 @@ def run_long(api, _lib, workloads, dev, peaks, with_cpu, reps=3):
         "sketch_ms": ms, "valid_tokens": int(lens.sum()), "step_ms": step_ms,
         "sketched_grads_per_s": N / (step_ms * 1e-3),
         "roofline": _roofline("dr_sketch_grads, 16 layers", "hbm", by, ms, HBM_PEAK_GBS, "GB/s",
-                              measured_peak=peaks.get("hbm_copy_GBs") if peaks else None, algorithmic_bytes=by),
+                              measured_peak=peaks.get("hbm_read_GBs") if peaks else None, algorithmic_bytes=by),
         "gram_ms": gram_ms, "cone_ms": cone_ms, "cone_steps": int(its[0]), "cone_kkt": float(kkt[0]),
         "projection_steps_per_s": 1e3 / (gram_ms + cone_ms),
     }
@@ -904,24 +914,34 @@ SKETCH_KERNELS = ("sketch_plan_kernel", "sketch_packed_kernel", "sketch_packed_r
 
 # the commands behind each committed summary (run from the repository root
 # with TMPDIR=/tmp; rocprofv3 writes csv files under prof_out/)
-PROFILE_CMDS = {
+_SEL = "--kernel-include-regex 'dr::|copyBuffer'"
+MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES "
+                 "GRBM_GUI_ACTIVE")
+TRACE_CMDS = {
     "llama_step": "rocprofv3 --kernel-trace --stats --output-format csv -d prof_out/llama_kt -o run -- "
                   "python -u bench.py --only llama --steps 5 --warmup 2 --no-cpu-baseline",
     "small_block": "rocprofv3 --kernel-trace --stats --output-format csv -d prof_out/small_kt -o run -- "
                    "python -u bench.py --only small --no-cpu-baseline",
     "gram_dominated": "rocprofv3 --kernel-trace --stats --output-format csv -d prof_out/gram_kt -o run -- "
                       "python -u bench.py --only gram --no-cpu-baseline",
-    "llama_block": "rocprofv3 --pmc {c} --output-format csv -d prof_out/llama_{d} -o run -- "
-                   "python -u bench.py --only llama --steps 1 --warmup 0 --no-cpu-baseline --copy-calibration",
-    "small_block_traffic": "rocprofv3 --pmc {c} --output-format csv -d prof_out/small_{d} -o run -- "
-                           "python -u bench.py --only small --steps 1 --warmup 1 --no-cpu-baseline --no-next-rows "
-                           "--copy-calibration",
-    "gram_dominated_traffic": "rocprofv3 --pmc {c} --output-format csv -d prof_out/gram_{d} -o run -- "
-                              "python -u bench.py --only gram --no-cpu-baseline --copy-calibration",
 }
-TRACE_CMD = {"llama_step": "llama_step", "small_block": "small_block", "gram_dominated": "gram_dominated"}
-TRAFFIC_CMD = {"llama_block": "llama_block", "small_block": "small_block_traffic",
-               "gram_dominated": "gram_dominated_traffic"}
+TRAFFIC_CMDS = {
+    "llama_block": f"rocprofv3 --pmc {{c}} {_SEL} --output-format csv -d prof_out/llama_{{d}} -o run -- "
+                   "python -u bench.py --only llama --steps 1 --warmup 0 --no-cpu-baseline --copy-calibration",
+    "small_block": f"rocprofv3 --pmc {{c}} {_SEL} --output-format csv -d prof_out/small_{{d}} -o run -- "
+                   "python -u bench.py --only small --steps 1 --warmup 1 --no-cpu-baseline --no-next-rows "
+                   "--copy-calibration",
+    "gram_dominated": f"rocprofv3 --pmc {{c}} {_SEL} --output-format csv -d prof_out/gram_{{d}} -o run -- "
+                      "python -u bench.py --only gram --no-cpu-baseline --copy-calibration",
+}
+COUNTER_CMDS = {
+    "llama_block": f"rocprofv3 --pmc {MFMA_COUNTERS} {_SEL} --output-format csv -d prof_out/llama_mfma -o run -- "
+                   "python -u bench.py --only llama --steps 1 --warmup 0 --no-cpu-baseline",
+    "small_block": f"rocprofv3 --pmc {MFMA_COUNTERS} {_SEL} --output-format csv -d prof_out/small_mfma -o run -- "
+                   "python -u bench.py --only small --steps 1 --warmup 1 --no-cpu-baseline",
+    "gram_dominated": f"rocprofv3 --pmc {MFMA_COUNTERS} {_SEL} --output-format csv -d prof_out/gram_mfma -o run -- "
+                      "python -u bench.py --only gram --no-cpu-baseline",
+}
 
 
 def sketch_sources_sha():
@@ -985,7 +1005,7 @@ def _kernel_rows(stats_csv):
 def summarize_trace(name, kt_dir):
     rows, avg = _kernel_rows(_find("*_kernel_stats.csv", kt_dir))
     sk = sum(v for k, v in avg.items() if k.startswith(SKETCH_KERNELS))
-    cmd = PROFILE_CMDS[TRACE_CMD[name]]
+    cmd = TRACE_CMDS[name]
     lines = [f"# Kernel trace: {name.replace('_', ' ')}", "",
              "Command (from the repository root, `TMPDIR=/tmp`), then "
              f"`python bench.py --summarize-trace {name} {cmd.split(' -d ')[1].split()[0]}`:", "",
@@ -1030,7 +1050,7 @@ def summarize_traffic(name, fetch_dir, write_dir):
                      f"{wa * wfac * 1024 / 1e6:,.1f} MB |")
         if k.startswith(SKETCH_KERNELS):
             sk_bytes += b
-    cmd = PROFILE_CMDS[TRAFFIC_CMD[name]]
+    cmd = TRAFFIC_CMDS[name]
     tr = [f"# HBM traffic: {name.replace('_', ' ')}", "",
           "Two counter passes, each in its own run (from the repository root, `TMPDIR=/tmp`), summarised by "
           f"`python bench.py --summarize-traffic {name} <fetch dir> <write dir>`:", "", "```",
@@ -1054,28 +1074,59 @@ def summarize_traffic(name, fetch_dir, write_dir):
     print(f"{name}: sketch call {sk_bytes / 1e9:.4f} GB")
 
 
+XCDS, SIMDS = 8, 1024          # MI355X: 8 XCDs, 256 CUs x 4 SIMDs
+MFMA_FLOP_PER_CLK = {"SQ_INSTS_VALU_MFMA_MOPS_BF16": 1024.0, "SQ_INSTS_VALU_MFMA_MOPS_F32": 64.0}   # per SIMD
+
+
 def summarize_counters(name, pmc_dir):
-    """Per-kernel averages of every counter in a rocprofv3 --pmc run, and
-    the MFMA rate they imply: SQ_INSTS_VALU_MFMA_MOPS_* counts MFMA work in
-    units of 512 flops; with SQ_BUSY_CYCLES (per shader engine, 32 of them)
-    and the 2.4 GHz clock that is executed TFLOP/s while the kernel runs."""
+    """Per-kernel averages of the MFMA counters of a rocprofv3 --pmc run and
+    what they imply:
+    - clock = GRBM_GUI_ACTIVE / 8 XCDs / the dispatch's duration (its start
+      and end stamps; counter runs serialise the dispatches);
+    - executed TFLOP/s = SQ_INSTS_VALU_MFMA_MOPS_* x 512 flops / duration;
+    - MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE / 8);
+    - executed / dense peak at that clock (bf16 1024 and fp32 64 flops per
+      SIMD per clock: 2.5 PFLOP/s and 157.3 TFLOP/s at 2.4 GHz)."""
     import csv
     import glob
-    per = {}
+    per, dur = {}, {}
     for f in sorted(glob.glob(os.path.join(pmc_dir, "**", "*_counter_collection.csv"), recursive=True)):
         for r in csv.DictReader(open(f)):
             k = _short_name(r["Kernel_Name"])
             if k.startswith(("at::", "void at::", "Cijk_")) or "rocclr" in k:
                 continue
             per.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
-    names = sorted({c for v in per.values() for c in v})
-    lines = [f"# Counters: {name.replace('_', ' ')}", "", "Per-kernel average per dispatch.", "",
-             "| Kernel | dispatches | " + " | ".join(names) + " |", "|---|---|" + "---|" * len(names)]
+            dur.setdefault(k, {})[r["Dispatch_Id"]] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    avg = lambda v: sum(v) / len(v)
+    cmd = COUNTER_CMDS[name]
+    lines = [f"# MFMA counters: {name.replace('_', ' ')}", "",
+             "Command (from the repository root, `TMPDIR=/tmp`), then "
+             f"`python bench.py --summarize-counters {name} {cmd.split(' -d ')[1].split()[0]}`:", "",
+             "```", cmd, "```", "",
+             "Per-kernel averages per dispatch (counter runs serialise the dispatches). Clock = GRBM_GUI_ACTIVE / 8 "
+             "XCDs / duration. Executed = SQ_INSTS_VALU_MFMA_MOPS_BF16 and _F32 x 512 flops / duration. MFMA busy "
+             "= SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE / 8). Of peak at clock = executed / "
+             "(1024 SIMDs x 1024 bf16 or 64 fp32 flops per clock x clock). The clock is meaningful for dispatches of "
+             "about 100 us and longer only: GRBM_GUI_ACTIVE also counts the dispatch's start-up and drain.", "",
+             "| Kernel | dispatches | avg duration (us) | clock (GHz) | MOPS_BF16 | MOPS_F32 | executed TFLOP/s | "
+             "MFMA busy | of peak at clock |", "|---|---|---|---|---|---|---|---|---|"]
     for k, cs in per.items():
-        nd = max(len(v) for v in cs.values())
-        lines.append(f"| `{k}` | {nd} | " + " | ".join(f"{sum(cs[c]) / len(cs[c]):,.4g}" if c in cs else "-"
-                                                       for c in names) + " |")
+        nd = len(dur[k])
+        d_s = avg(list(dur[k].values())) * 1e-9
+        g = avg(cs.get("GRBM_GUI_ACTIVE", [0.0])) / XCDS
+        clk = g / d_s / 1e9 if d_s > 0 else 0.0
+        mb = avg(cs.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", [0.0]))
+        mf = avg(cs.get("SQ_INSTS_VALU_MFMA_MOPS_F32", [0.0]))
+        tf = (mb + mf) * 512 / d_s / 1e12 if d_s > 0 else 0.0
+        busy = avg(cs.get("SQ_VALU_MFMA_BUSY_CYCLES", [0.0])) / (SIMDS * g) if g > 0 else 0.0
+        # peak at this clock for the kernel's dominant MFMA type
+        kind = "SQ_INSTS_VALU_MFMA_MOPS_BF16" if mb >= mf else "SQ_INSTS_VALU_MFMA_MOPS_F32"
+        pk = SIMDS * MFMA_FLOP_PER_CLK[kind] * clk * 1e9 / 1e12
+        of = tf / pk if (mb + mf) > 0 and pk > 0 else 0.0
+        lines.append(f"| `{k}` | {nd} | {d_s * 1e6:,.1f} | {clk:.2f} | {mb:,.4g} | {mf:,.4g} | {tf:,.1f} | "
+                     f"{busy:.3f} | {of:.3f} |")
     open(os.path.join(ROOT, "profiles", f"{name}_counters.md"), "w").write("\n".join(lines) + "\n")
+    print(f"{name}: {len(per)} kernels")
 
 
 if __name__ == "__main__":

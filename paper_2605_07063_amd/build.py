@@ -15,9 +15,14 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdr.so")
+PROBE_LIB = os.path.join(PKG, "libdrprobe.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["api.cpp", "sketch.hip", "gram.hip", "solve.hip", "chol.hip", "select.hip", "combine.hip", "update.hip", "score.hip", "backproj.hip"]
+SOURCES = ["api.cpp", "sketch.hip", "gram.hip", "solve.hip", "chol.hip", "select.hip", "combine.hip", "update.hip",
+           "score.hip", "backproj.hip"]
+# measurement probes of the benchmark (HBM stream and MFMA issue ceilings),
+# a library of their own
+PROBE_SOURCES = ["probe.hip"]
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -40,20 +45,27 @@ def _compile(src):
     return out
 
 
-def build(verbose=False):
-    """Compile every source for gfx950 and link libdr.so next to this file."""
-    os.makedirs(BUILD_DIR, exist_ok=True)
-    workers = min(len(SOURCES), os.cpu_count() or 1, 8)
-    with concurrent.futures.ThreadPoolExecutor(workers) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, out):
+    tmp = out + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
+
+
+def build(verbose=False):
+    """Compile every source for gfx950 and link libdr.so (and the probe
+    library libdrprobe.so) next to this file."""
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    srcs = SOURCES + PROBE_SOURCES
+    workers = min(len(srcs), os.cpu_count() or 1, 8)
+    with concurrent.futures.ThreadPoolExecutor(workers) as ex:
+        objs = list(ex.map(_compile, srcs))
+    _link(objs[:len(SOURCES)], LIB)
+    _link(objs[len(SOURCES):], PROBE_LIB)
     if verbose:
-        print(f"built {LIB}")
+        print(f"built {LIB} and {PROBE_LIB}")
     return LIB
 
 

@@ -39,7 +39,7 @@ def test_every_declared_symbol_is_exported_and_bound(lib):
 def test_version_and_status_strings(lib):
     assert lib.dr_abi_version() == 1
     for code in range(9):
-        assert lib.dr_status_string(code)
+        assert lib.dr_status_string(code) != b"unknown status"
     assert lib.dr_status_string(0) == b"ok"
 
 
@@ -238,3 +238,23 @@ def test_simplex_and_backprojection_argument_errors(lib):
     assert lib.dr_back_project(arr, 1, E.DR_F32, FAKE, FAKE, offs, FAKE, ws - 1, None) == E.DR_ERR_WORKSPACE
     big = (_lib.DrLayer * 1)(layer(k_in=128))
     assert lib.dr_back_project(big, 1, E.DR_F32, FAKE, FAKE, offs, FAKE, 1 << 30, None) == E.DR_ERR_ARG
+
+
+def test_probe_library_exports_its_header():
+    """The measurement probes' library exports what dr_probe.h declares and
+    rejects invalid arguments before any HIP call."""
+    from paper_2605_07063_amd import build
+    if not os.path.exists(build.PROBE_LIB):
+        build.build()
+    plib = ctypes.CDLL(build.PROBE_LIB)
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "dr_probe.h")).read(), flags=re.S)
+    names = re.findall(r"^\s*int\s+(dr_probe_\w+)\s*\(", text, flags=re.M)
+    assert sorted(names) == ["dr_probe_mfma", "dr_probe_read"]
+    for nm in names:
+        assert hasattr(plib, nm)
+    plib.dr_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+    plib.dr_probe_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+    assert plib.dr_probe_read(FAKE, 24, FAKE, 16, None) == 1        # not a multiple of 16 bytes
+    assert plib.dr_probe_read(FAKE, 4096, FAKE, 0, None) == 1
+    assert plib.dr_probe_mfma(1, 0, FAKE, 16, None) == 1
+    assert plib.dr_probe_mfma(1, 16, None, 16, None) == 1

@@ -296,6 +296,40 @@ def test_span_blocked_special_cases():
     assert rel(host64(w[1]), w_ref) <= TOL_SOLVE
 
 
+@pytest.mark.parametrize("n", [128, 320])
+def test_span_refinement_flag_tracks_accuracy_over_a_conditioning_sweep(n):
+    """n = 128 (one-workgroup tiles) and n = 320 (blocked): K = Q diag(l) Q^T
+    with l from 1 down to 1 / cond, cond = 1e2 .. 1e7, rounded to fp32.  A
+    result reported converged (info = 0) must be within 1e-5 of the fp64
+    solution of the same fp32 system; the ill-conditioned end of the sweep
+    must be reported (DR_INFO_NOT_CONVERGED, or a non-positive pivot), not
+    returned silently."""
+    rng = np.random.default_rng(31 + n)
+    Q, _ = np.linalg.qr(rng.standard_normal((n, n)))
+    out = []
+    for cond in (1e2, 1e3, 1e4, 1e5, 1e6, 1e7):
+        lam = np.geomspace(1.0, 1.0 / cond, n)
+        K32 = ((Q * lam) @ Q.T).astype(np.float32)
+        K32 = ((K32 + K32.T) / 2).astype(np.float32)
+        s32 = (K32.astype(np.float64) @ rng.standard_normal(n)).astype(np.float32)
+        K = torch.from_numpy(K32)[None].to(DEV)
+        s = torch.from_numpy(s32)[None].to(DEV)
+        t2 = torch.ones(1, device=DEV)
+        w, le, r2, info = api.project_span(K, s, t2, 0.0, RIDGE_ABS)
+        torch.cuda.synchronize()
+        w_ref = np.linalg.solve(K32.astype(np.float64), s32.astype(np.float64))
+        err = rel(host64(w[0]), w_ref)
+        inf = int(info[0])
+        out.append((cond, inf, err))
+        print(f"n={n} cond {cond:.0e}: info {inf}, rel err {err:.2e}", flush=True)
+        if inf == 0:
+            assert err <= TOL_SOLVE, (cond, err)
+        else:
+            assert inf == -2 or inf > 0, (cond, inf)
+    assert out[0][1] == 0 and out[1][1] == 0
+    assert out[-1][1] != 0
+
+
 def test_span_gram_dominated_full_size():
     """n = 16384 from the 16384 x 8192 bf16 rows with a rank-32 spike, relative ridge 1e-2:
     parity with the fp64 LAPACK oracle and the ridge normal equations G (gbar - G^T w) = lam w."""
