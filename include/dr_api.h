@@ -60,7 +60,8 @@ typedef enum {
   DR_ERR_NONFINITE = 5,     /* reserved for callers that map info == -3 */
   DR_ERR_WORKSPACE = 6,     /* workspace pointer NULL or smaller than the query */
   DR_ERR_HIP = 7,           /* a HIP launch failed */
-  DR_ERR_UNSUPPORTED = 8    /* valid but not implemented (e.g. projection size) */
+  DR_ERR_UNSUPPORTED = 8,   /* valid but not implemented (e.g. projection size) */
+  DR_ERR_TOO_LARGE = 9      /* needs more scratch than a no-allocation entry point holds */
 } dr_status;
 
 #define DR_INFO_NOT_CONVERGED (-2)
@@ -162,6 +163,28 @@ dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* Gt, int64_t
                   dr_dtype dtype, const int64_t* goff, int P, float* K, float* s, float* t2,
                   void* workspace, size_t ws_bytes, void* stream);
 size_t dr_gram_workspace_size(int64_t n, int64_t m, const int64_t* goff, int P, dr_dtype dtype);
+
+/* ---------------------------------------------------------------------------
+ * dr_gram_noalloc -- dr_gram for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same computation, arguments and results as dr_gram, minus
+ * the workspace.  Its workspace is a fixed array of DR_GRAM_NOALLOC_MAX_BYTES
+ * in the library's device code, one per GPU, held until the process ends.
+ * The call allocates nothing (no hipMalloc / hipFree, no allocating library
+ * routine); its first call on a device looks up that device's array.
+ *   Returns DR_ERR_TOO_LARGE, before any HIP call, when
+ *   dr_gram_workspace_size(n, m, goff, P, dtype) > DR_GRAM_NOALLOC_MAX_BYTES
+ *   (every workload shape here needs at most half of it: 32 MB for 256
+ *   rows over 229376 fp32 columns).
+ * All calls on one GPU share its array (and it keeps the last call's
+ * contents; nothing in it needs to start at zero): calls that overlap on one
+ * GPU -- on different streams, or from different host threads without
+ * ordering -- race.  Order them on one stream, or synchronise.
+ * ------------------------------------------------------------------------- */
+#define DR_GRAM_NOALLOC_MAX_BYTES ((size_t)64 << 20)
+dr_status dr_gram_noalloc(const void* G, int64_t n, int64_t ldG, const void* Gt, int64_t m, int64_t ldGt,
+                          dr_dtype dtype, const int64_t* goff, int P, float* K, float* s, float* t2,
+                          void* stream);
 
 /* ---------------------------------------------------------------------------
  * dr_project_span -- Eq. (proj) onto the span of the general gradients,

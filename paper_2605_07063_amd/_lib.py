@@ -12,7 +12,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libdr.so")
 
 DR_OK, DR_ERR_ARG, DR_ERR_DTYPE, DR_ERR_NOT_SPD, DR_ERR_NOT_CONVERGED = 0, 1, 2, 3, 4
-DR_ERR_NONFINITE, DR_ERR_WORKSPACE, DR_ERR_HIP, DR_ERR_UNSUPPORTED = 5, 6, 7, 8
+DR_ERR_NONFINITE, DR_ERR_WORKSPACE, DR_ERR_HIP, DR_ERR_UNSUPPORTED, DR_ERR_TOO_LARGE = 5, 6, 7, 8, 9
+DR_GRAM_NOALLOC_MAX_BYTES = 64 << 20
 DR_INFO_NOT_CONVERGED, DR_INFO_NONFINITE = -2, -3
 DR_F32, DR_BF16 = 0, 1
 DR_RIDGE_ABS, DR_RIDGE_REL_TRACE = 0, 1
@@ -41,6 +42,8 @@ SIGNATURES = {
     "dr_gram": (c_int, [c_vp, c_i64, c_i64, c_vp, c_i64, c_i64, c_int, ctypes.POINTER(c_i64), c_int,
                         c_vp, c_vp, c_vp, c_vp, c_size, c_vp]),
     "dr_gram_workspace_size": (c_size, [c_i64, c_i64, ctypes.POINTER(c_i64), c_int, c_int]),
+    "dr_gram_noalloc": (c_int, [c_vp, c_i64, c_i64, c_vp, c_i64, c_i64, c_int, ctypes.POINTER(c_i64), c_int,
+                                c_vp, c_vp, c_vp, c_vp]),
     "dr_project_span": (c_int, [c_vp, c_vp, c_vp, c_i64, c_int, c_float, c_int, c_vp, c_vp, c_vp, c_vp,
                                 c_vp, c_size, c_vp]),
     "dr_span_workspace_size": (c_size, [c_i64, c_int]),

@@ -154,6 +154,23 @@ def dr_gram(G, Gt, goff, K, s, t2, workspace=None, stream=None):
                                  _stream(stream)))
 
 
+def dr_gram_noalloc(G, Gt, goff, K, s, t2, stream=None):
+    """dr_gram with the library's fixed per-device scratch instead of a workspace."""
+    lib = _lib.load()
+    dtype = Gt.dtype
+    _dev(Gt, "Gt", dtype)
+    n, m = G.shape[0], Gt.shape[0]
+    if n > 0:
+        _dev(G, "G", dtype)
+    for t, nm in ((K, "K"), (s, "s"), (t2, "t2")):
+        _dev(t, nm, torch.float32)
+        _contig(t, nm)
+    ga = _goff_array(goff)
+    check("dr_gram_noalloc", lib.dr_gram_noalloc(_ptr(G), n, G.stride(0) if n > 0 else 0, _ptr(Gt), m, Gt.stride(0),
+                                                 _DTYPES[dtype], ga, len(goff) - 1, _ptr(K), _ptr(s), _ptr(t2),
+                                                 _stream(stream)))
+
+
 def dr_span_workspace_size(n, P):
     return _lib.load().dr_span_workspace_size(n, P)
 

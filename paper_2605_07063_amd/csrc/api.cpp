@@ -14,6 +14,7 @@ extern "C" const char* dr_status_string(dr_status s) {
     case DR_ERR_WORKSPACE: return "workspace missing or too small";
     case DR_ERR_HIP: return "HIP launch error";
     case DR_ERR_UNSUPPORTED: return "unsupported size";
+    case DR_ERR_TOO_LARGE: return "problem needs more scratch than the no-allocation entry point holds";
   }
   return "unknown status";
 }

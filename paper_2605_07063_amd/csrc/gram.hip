@@ -43,6 +43,8 @@
 //                        and t2 (element n, n).
 // No atomics: results are deterministic.
 
+#include <mutex>
+
 #include "common.h"
 
 namespace dr {
@@ -635,17 +637,26 @@ extern "C" size_t dr_gram_workspace_size(int64_t n, int64_t m, const int64_t* go
   return g.gbar_bytes + g.partial_bytes;
 }
 
-extern "C" dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* Gt, int64_t m, int64_t ldGt,
-                             dr_dtype dtype, const int64_t* goff, int P, float* K, float* s, float* t2,
-                             void* workspace, size_t ws_bytes, void* stream) {
-  using namespace dr;
+namespace dr {
+namespace {
+
+// host checks of a call (before any HIP call), then the plan
+dr_status gram_check(const void* G, int64_t n, int64_t ldG, const void* Gt, int64_t m, int64_t ldGt, dr_dtype dtype,
+                     const int64_t* goff, int P, float* K, float* s, float* t2, GramPlan* plan) {
   dr_status st = gram_validate(G, n, ldG, Gt, m, ldGt, dtype, goff, P, K, s, t2);
   if (st != DR_OK) return st;
   // the large-n kernel addresses a 256-row panel with 32-bit buffer offsets
   if (gram_use_big(n, P, dtype) && (uint64_t)ldG * 2 * (kBT + 1) >= (uint64_t)kOobOffset) return DR_ERR_UNSUPPORTED;
-  GramPlan g = gram_plan(n, goff, P, dtype);
-  if (!workspace || ws_bytes < g.gbar_bytes + g.partial_bytes) return DR_ERR_WORKSPACE;
-  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  *plan = gram_plan(n, goff, P, dtype);
+  return DR_OK;
+}
+
+// enqueue the Gram on hs with the workspace at `workspace` (every byte of
+// it that a kernel reads is written earlier in the same call)
+dr_status gram_run(const GramPlan& g, const void* G, int64_t n, int64_t ldG, const void* Gt, int64_t m, int64_t ldGt,
+                   dr_dtype dtype, const int64_t* goff, int P, float* K, float* s, float* t2, void* workspace,
+                   hipStream_t hs) {
+  dr_status st = DR_OK;
   const bool bf = dtype == DR_BF16;
   float* gbar = static_cast<float*>(workspace);
   float* partial = reinterpret_cast<float*>(static_cast<unsigned char*>(workspace) + g.gbar_bytes);
@@ -717,4 +728,55 @@ extern "C" dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* 
     }
   }
   return DR_OK;
+}
+
+}  // namespace
+}  // namespace dr
+
+extern "C" dr_status dr_gram(const void* G, int64_t n, int64_t ldG, const void* Gt, int64_t m, int64_t ldGt,
+                             dr_dtype dtype, const int64_t* goff, int P, float* K, float* s, float* t2,
+                             void* workspace, size_t ws_bytes, void* stream) {
+  dr::GramPlan g;
+  const dr_status st = dr::gram_check(G, n, ldG, Gt, m, ldGt, dtype, goff, P, K, s, t2, &g);
+  if (st != DR_OK) return st;
+  if (!workspace || ws_bytes < g.gbar_bytes + g.partial_bytes) return DR_ERR_WORKSPACE;
+  return dr::gram_run(g, G, n, ldG, Gt, m, ldGt, dtype, goff, P, K, s, t2, workspace,
+                      reinterpret_cast<hipStream_t>(stream));
+}
+
+// ---------------------------------------------------------------------------
+// dr_gram_noalloc: the same Gram with its workspace in a fixed device array.
+// In host code `scratch` names a host-side stand-in, not device memory: its
+// device address is looked up once per device (hipGetSymbolAddress, with
+// that device current) and only that address is ever handed to a kernel.
+// Each device holds its own copy of the array until the process ends.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[DR_GRAM_NOALLOC_MAX_BYTES];
+
+namespace {
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevices];   // device address of `scratch` per device, null until looked up
+}  // namespace
+
+extern "C" dr_status dr_gram_noalloc(const void* G, int64_t n, int64_t ldG, const void* Gt, int64_t m, int64_t ldGt,
+                                     dr_dtype dtype, const int64_t* goff, int P, float* K, float* s, float* t2,
+                                     void* stream) {
+  dr::GramPlan g;
+  const dr_status st = dr::gram_check(G, n, ldG, Gt, m, ldGt, dtype, goff, P, K, s, t2, &g);
+  if (st != DR_OK) return st;
+  if (g.gbar_bytes + g.partial_bytes > (size_t)DR_GRAM_NOALLOC_MAX_BYTES) return DR_ERR_TOO_LARGE;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices) return DR_ERR_HIP;
+  void* ptr = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+      void* p = nullptr;
+      if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return DR_ERR_HIP;
+      g_scratch_ptr[dev] = p;
+    }
+    ptr = g_scratch_ptr[dev];
+  }
+  return dr::gram_run(g, G, n, ldG, Gt, m, ldGt, dtype, goff, P, K, s, t2, ptr, reinterpret_cast<hipStream_t>(stream));
 }

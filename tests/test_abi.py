@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported_and_bound(lib):
 
 def test_version_and_status_strings(lib):
     assert lib.dr_abi_version() == 1
-    for code in range(9):
+    for code in range(10):
         assert lib.dr_status_string(code) != b"unknown status"
     assert lib.dr_status_string(0) == b"ok"
 
@@ -107,6 +107,26 @@ def test_gram_argument_errors(lib):
     assert call(ws=None) == E.DR_ERR_WORKSPACE
     assert call(wsb=16) == E.DR_ERR_WORKSPACE
     assert lib.dr_gram_workspace_size(64, 8, goff(0, 32768), 1, E.DR_F32) > 0
+
+
+def test_gram_noalloc_argument_errors_and_scratch_limit(lib):
+    """The no-allocation Gram validates like dr_gram, and refuses a problem
+    whose workspace exceeds its fixed scratch, all before any HIP call."""
+    E = _lib
+    g = goff(0, 64)
+    call = lambda **kw: lib.dr_gram_noalloc(FAKE, kw.get("n", 8), kw.get("ldG", 64), FAKE, 2, kw.get("ldGt", 64),
+                                            kw.get("dtype", E.DR_F32), kw.get("goff", g), kw.get("P", 1), FAKE, FAKE,
+                                            FAKE, None)
+    assert call(P=0) == E.DR_ERR_ARG
+    assert call(ldG=32) == E.DR_ERR_ARG
+    assert call(dtype=3) == E.DR_ERR_DTYPE
+    n, cols = 8000, 1 << 20
+    need = lib.dr_gram_workspace_size(n, 2, goff(0, cols), 1, E.DR_F32)
+    assert need > E.DR_GRAM_NOALLOC_MAX_BYTES
+    assert call(n=n, ldG=cols, ldGt=cols, goff=goff(0, cols)) == E.DR_ERR_TOO_LARGE
+    assert lib.dr_status_string(E.DR_ERR_TOO_LARGE).startswith(b"problem needs more scratch")
+    hdr = open(HEADER).read()
+    assert re.search(r"#define DR_GRAM_NOALLOC_MAX_BYTES \(\(size_t\)64 << 20\)", hdr)
 
 
 def test_solver_and_select_argument_errors(lib):
