@@ -74,7 +74,7 @@ struct LgCtl {
 
 struct LgLayout {
   long long n, ldL, nblk, npad;
-  size_t off_L, off_inv, off_sinv, off_sinvt, off_x, off_dx, off_r, off_z, off_ctl, total;
+  size_t off_L, off_inv, off_sinv, off_sinvt, off_pl, off_x, off_dx, off_r, off_z, off_ctl, total;
 };
 
 LgLayout lg_layout(long long n) {
@@ -88,6 +88,7 @@ LgLayout lg_layout(long long n) {
   l.off_inv = o;  o = align_up(o + (size_t)l.nblk * NB * NB * 4, 256);
   l.off_sinv = o; o = align_up(o + (size_t)((l.nblk + SB - 1) / SB) * SBN * SBN * 4, 256);
   l.off_sinvt = o; o = align_up(o + (size_t)((l.nblk + SB - 1) / SB) * SBN * SBN * 4, 256);
+  l.off_pl = o;   o = align_up(o + (size_t)3 * n * 2 * NB * 2, 256);   // three bf16 planes of a panel pair
   l.off_x = o;    o = align_up(o + (size_t)l.npad * 8, 256);
   l.off_dx = o;   o = align_up(o + (size_t)l.npad * 8, 256);
   l.off_r = o;    o = align_up(o + (size_t)l.npad * 8, 256);
@@ -713,6 +714,191 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
   }
 }
 
+// ------------------------------------------- bulk update on bf16 MFMA
+//
+// The bulk of the rank-256 trailing update, A22 -= L21 L21^T, with the fp32
+// products taken on bf16 MFMA (16 times the fp32 MFMA rate):
+//   lg_split_kernel  writes the panel pair's rows below it (L21, 256
+//                    columns) as three bf16 planes, x = x1 + x2 + x3 with
+//                    x1 = bf16(x), x2 = bf16(x - x1), x3 = bf16(x - x1 - x2)
+//                    (round to nearest even; each difference is exact in
+//                    fp32), so x1 + x2 + x3 holds x to about 2^-24.
+//   lg_syrk6_kernel  C -= sum over the six plane pairs (a, b) with
+//                    a + b <= 2 (0-based: 00, 01, 10, 02, 11, 20) of
+//                    P_a P_b^T: every product of bf16 values is exact in
+//                    fp32 and the accumulation is fp32, and the dropped
+//                    pairs (12, 21, 22) weigh 2^-24 and less, so each
+//                    element's error is about 3 * 2^-24 of |x||y|: fp32
+//                    products, at a sixth of the bf16 MFMA rate (2.6 times
+//                    the fp32 MFMA rate).  The six products are run as one
+//                    bf16 contraction over 6 x 256 = 1536 virtual columns,
+//                    64 per step: step s reads plane a of the tile's row
+//                    panel and plane b of its column panel, columns
+//                    64 (s mod 4) ..., for the pair s / 4.
+// The tile machinery is that of the large-n Gram kernel: 256 x 256 tiles
+// of the trailing matrix right of the pair's two head tile columns (tiles
+// I >= J >= 1 in units of 256 from the trailing matrix's first row), eight
+// waves of 128 x 64 fp32 accumulators, a two-stage buffer -> LDS DMA ring
+// of 64-column steps in the conflict-free operand layout.  At the end the
+// tile goes through LDS in two 128-row halves (row-major, 260-float rows:
+// the accumulator writes of a wave fall on distinct banks) and each thread
+// updates 16 float4 of C: read, subtract, write (on a diagonal tile only
+// entries on or below the diagonal).
+
+constexpr int S6_T = 256;                      // tile edge
+constexpr int S6_K = 64;                       // virtual columns per step
+constexpr int S6_PANEL = S6_T * S6_K * 2;      // bytes of one operand panel per step (32 KiB)
+constexpr int S6_STAGE = 2 * S6_PANEL;
+constexpr int S6_LDC = S6_T + 4;               // row stride (floats) of the half tile staged in LDS
+constexpr int S6_LDS = 2 * S6_STAGE > 128 * S6_LDC * 4 ? 2 * S6_STAGE : 128 * S6_LDC * 4;
+constexpr int S6_STEPS = 6 * (2 * NB) / S6_K;   // 24
+#ifndef DR_S6_MIN_ROUNDS
+#define DR_S6_MIN_ROUNDS 1
+#endif
+constexpr int kS6MinRounds = DR_S6_MIN_ROUNDS;   // rounds of tiles below which the fp32 kernel takes the bulk
+
+__device__ __forceinline__ unsigned bf16_rne_bits(float x) {
+  const unsigned u = __float_as_uint(x);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+// rows k1 .. n-1, columns k .. k+255 of L -> planes [3][n][256] bf16 (row r of
+// a plane is row k1 + r); one thread per 8 columns of a row
+__global__ __launch_bounds__(256) void lg_split_kernel(const float* L, long long ldL, int n, int k, int k1,
+                                                       unsigned short* pl, const LgCtl* ctl) {
+  if (ctl->skip) return;
+  const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
+  const int r = (int)(t >> 5), c = (int)(t & 31) * 8;
+  if (k1 + r >= n) return;
+  const float* src = L + (long long)(k1 + r) * ldL + k + c;
+  const float4 v0 = *reinterpret_cast<const float4*>(src);
+  const float4 v1 = *reinterpret_cast<const float4*>(src + 4);
+  const float x[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+  unsigned p0[4], p1[4], p2[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    unsigned h[2], m[2], l[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const float v = x[2 * q + e];
+      h[e] = bf16_rne_bits(v);
+      const float r1 = v - __uint_as_float(h[e] << 16);
+      m[e] = bf16_rne_bits(r1);
+      const float r2 = r1 - __uint_as_float(m[e] << 16);
+      l[e] = bf16_rne_bits(r2);
+    }
+    p0[q] = h[0] | (h[1] << 16);
+    p1[q] = m[0] | (m[1] << 16);
+    p2[q] = l[0] | (l[1] << 16);
+  }
+  const long long plane = (long long)n * 2 * NB;
+  unsigned short* d = pl + (long long)r * 2 * NB + c;
+  *reinterpret_cast<u32x4*>(d) = u32x4{p0[0], p0[1], p0[2], p0[3]};
+  *reinterpret_cast<u32x4*>(d + plane) = u32x4{p1[0], p1[1], p1[2], p1[3]};
+  *reinterpret_cast<u32x4*>(d + 2 * plane) = u32x4{p2[0], p2[1], p2[2], p2[3]};
+}
+
+__global__ __launch_bounds__(512) void lg_syrk6_kernel(const unsigned char* pl, float* L, long long ldL, int n, int k1,
+                                                       int ntiles, const LgCtl* ctl) {
+  if (ctl->skip) return;
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[S6_LDS];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = w >> 2, wc = w & 3;   // 128-row half, 64-column quarter of the tile
+  const int lr = lane & 15, lg = lane >> 4;
+  const int rows = n - k1;             // rows of the planes
+  const long long planeB = (long long)n * 2 * NB * 2;
+  int segs[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) segs[u] = swz_seg_of_lane(lane, (w + 8 * u) & 1);
+  for (int qt = blockIdx.x; qt < ntiles; qt += gridDim.x) {
+    int I, J;
+    tile_pair(qt, I, J);
+    const int rowA0 = S6_T * (I + 1), rowB0 = S6_T * (J + 1);   // plane rows (trailing rows from k1)
+    const bool diag = I == J;
+    unsigned offA[4], offB[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = 8 * (w + 8 * u) + (lane >> 3);
+      offA[u] = rowA0 + r < rows ? (unsigned)(r * 2 * NB * 2) : kOobOffset;
+      offB[u] = rowB0 + r < rows ? (unsigned)(r * 2 * NB * 2) : kOobOffset;
+    }
+    auto issue = [&](int s, int st) {
+      const int t = s >> 2, c0 = S6_K * (s & 3);
+      const int pa = t == 2 || t == 4 ? 1 : (t == 5 ? 2 : 0);   // plane pairs 00 01 10 02 11 20
+      const int pb = t == 1 || t == 4 ? 1 : (t == 3 ? 2 : 0);
+      const __amdgpu_buffer_rsrc_t ra = make_rsrc(pl + pa * planeB + (long long)rowA0 * 2 * NB * 2, kOobOffset);
+      const __amdgpu_buffer_rsrc_t rb = make_rsrc(pl + pb * planeB + (long long)rowB0 * 2 * NB * 2, kOobOffset);
+      unsigned char* sb = lds + st * S6_STAGE;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const unsigned cb = (unsigned)((c0 + segs[u] * 8) * 2);
+        dma16<kAuxCached>(ra, sb + (w + 8 * u) * 1024, offA[u] == kOobOffset ? kOobOffset : offA[u] + cb);
+        dma16<kAuxCached>(rb, sb + S6_PANEL + (w + 8 * u) * 1024, offB[u] == kOobOffset ? kOobOffset : offB[u] + cb);
+      }
+    };
+    f32x4 acc[8][4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    __syncthreads();   // the previous tile's last reads of the staging area are done
+    issue(0, 0);
+    for (int s = 0; s < S6_STEPS; ++s) {
+      DR_WAIT_VM(0);
+      DR_LDS_SYNC();
+      if (s + 1 < S6_STEPS) issue(s + 1, (s + 1) & 1);
+      const unsigned char* sa = lds + (s & 1) * S6_STAGE;
+      const unsigned char* sbp = sa + S6_PANEL;
+      u32x4 fa[2][8], fb[2][4];
+#pragma unroll
+      for (int kh = 0; kh < 2; ++kh) {
+        const int seg = 4 * kh + lg;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) fa[kh][i] = swz_read(sa + (wr * 8 + i) * 2048, lr, seg);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) fb[kh][j] = swz_read(sbp + (wc * 4 + j) * 2048, lr, seg);
+      }
+#pragma unroll
+      for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int i = 0; i < 8; ++i) acc[i][j] = mma_bf16(fa[kh][i], fb[kh][j], acc[i][j]);
+    }
+    // C -= acc through LDS, one 128-row half at a time
+    float* St = reinterpret_cast<float*>(lds);   // [128][S6_LDC]
+    for (int h = 0; h < 2; ++h) {
+      __syncthreads();   // the ring's (or the previous half's) last LDS reads are done
+      if (wr == h) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) St[(16 * i + 4 * lg + q) * S6_LDC + wc * 64 + 16 * j + lr] = acc[i][j][q];
+      }
+      __syncthreads();
+#pragma unroll 4
+      for (int e = tid; e < 128 * (S6_T / 4); e += 512) {
+        const int rr = e >> 6, c4 = 4 * (e & 63);
+        const int grow = k1 + rowA0 + 128 * h + rr, gcol = k1 + rowB0 + c4;
+        if (grow >= n) continue;
+        const f32x4 a = *reinterpret_cast<const f32x4*>(&St[rr * S6_LDC + c4]);
+        float* dst = L + (long long)grow * ldL + gcol;
+        if (gcol + 3 < n && (!diag || 128 * h + rr >= c4 + 3)) {
+          f32x4 c = *reinterpret_cast<const f32x4*>(dst);
+          *reinterpret_cast<f32x4*>(dst) = c - a;
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (gcol + q < n && (!diag || 128 * h + rr >= c4 + q)) dst[q] -= a[q];
+        }
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- solves
 
 // Triangular solves by super-blocks of SB diagonal blocks (1024 rows).
@@ -1061,6 +1247,7 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
   double* r = reinterpret_cast<double*>(base + lay.off_r);
   double* z = reinterpret_cast<double*>(base + lay.off_z);
   LgCtl* ctl = reinterpret_cast<LgCtl*>(base + lay.off_ctl);
+  unsigned short* pl = reinterpret_cast<unsigned short*>(base + lay.off_pl);
   const long long ldL = lay.ldL;
   const int nblk = (int)lay.nblk, npad = (int)lay.npad;
   const long long nn = (long long)n * n;
@@ -1112,7 +1299,17 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       const int nrest = (T - h) * (T - h + 1) / 2;
       hipLaunchKernelGGL(lg_syrk_kernel<2 * NB>, dim3(nhead), dim3(256), 0, hs, L, ldL, n, k, h, 1, nhead, ctl);
       if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;
-      if (nrest > 0) {
+      // the bulk on bf16 MFMA (split planes) while it has enough 256 x 256
+      // tiles for the 7/8 of the CUs it runs on (one workgroup each)
+      const int T2 = (rest + S6_T - 1) / S6_T;
+      const int n6 = T2 * (T2 - 1) / 2;
+      const int slots6 = cus - cus / 8;
+      if (n6 >= kS6MinRounds * slots6) {
+        const int k1 = k + 2 * NB;
+        hipLaunchKernelGGL(lg_split_kernel, dim3((rest * 32 + 255) / 256), dim3(256), 0, hs, L, ldL, n, k, k1, pl, ctl);
+        hipLaunchKernelGGL(lg_syrk6_kernel, dim3(n6 < slots6 ? n6 : slots6), dim3(512), 0, hs,
+                           reinterpret_cast<const unsigned char*>(pl), L, ldL, n, k1, n6, ctl);
+      } else if (nrest > 0) {
         // many rounds of tiles: the chain has slack, 15/16 of the slots;
         // under two rounds: the chain is the longer path, 3/4 of them
         const int slots = nrest >= 8 * cus ? 2 * cus - cus / 8 : (nrest < 4 * cus ? 2 * cus - cus / 2 : rest_slots);
