@@ -1029,8 +1029,21 @@ extern "C" dr_status dr_sketch_grads(const dr_layer* layers, int num_layers, int
     const Launch& l = lv[q];
     SketchArgs a = {};
     PackArgs pa = {};
+    // layers with the most bytes per token first: the launch's last
+    // workgroups then stream the smallest tiles, which shortens its tail
+    // (outputs go to each layer's own column range, so the order is free)
+    int ord[kMaxLayersPerLaunch];
     for (int j = 0; j < l.count; ++j) {
-      const dr_layer& L = layers[l.first + j];
+      int p = j;
+      const int64_t wj = layers[l.first + j].d_in + layers[l.first + j].d_out;
+      while (p > 0 && layers[l.first + ord[p - 1]].d_in + layers[l.first + ord[p - 1]].d_out < wj) {
+        ord[p] = ord[p - 1];
+        --p;
+      }
+      ord[p] = j;
+    }
+    for (int j = 0; j < l.count; ++j) {
+      const dr_layer& L = layers[l.first + ord[j]];
       LayerArg la;
       la.x = static_cast<const unsigned char*>(L.x);
       la.dy = static_cast<const unsigned char*>(L.dy);
