@@ -820,7 +820,7 @@ def main():
         summarize_counters(*args.summarize_counters)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+        print("bench.py runs on exactly one GPU: the library has no multi-GPU path "
               "(the per-GPU share is the single-GPU workload; see the design notes on sharding)",
               file=sys.stderr)
         sys.exit(2)
