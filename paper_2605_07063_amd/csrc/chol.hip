@@ -866,10 +866,28 @@ __global__ __launch_bounds__(512) void lg_syrk6_kernel(const unsigned char* pl, 
 #pragma unroll
           for (int i = 0; i < 8; ++i) acc[i][j] = mma_bf16(fa[kh][i], fb[kh][j], acc[i][j]);
     }
-    // C -= acc through LDS, one 128-row half at a time
+    // C -= acc through LDS, one 128-row half at a time.  Wave w updates
+    // rows w + 8 u (u < RMW) of the half, lane l the four columns from 4 l;
+    // all RMW float4 of C are requested before the half is staged, so their
+    // latency passes under the staging.  Rows past n are skipped (a
+    // wave-uniform test); a column start past n loads column 0 instead
+    // (k1 and the tile origin are multiples of 4 and the row stride is n
+    // rounded up to 4, so a float4 that starts below n lies in its row) and
+    // stores nothing; on a diagonal tile only entries on or below the
+    // diagonal are written.
     float* St = reinterpret_cast<float*>(lds);   // [128][S6_LDC]
+    constexpr int RMW = 128 / 8;
+    const int c4 = 4 * lane, gcol = k1 + rowB0 + c4;
+    const int gcl = gcol < n ? gcol : 0;
+    const bool colfull = gcol + 3 < n;
     for (int h = 0; h < 2; ++h) {
       __syncthreads();   // the ring's (or the previous half's) last LDS reads are done
+      const int row0 = k1 + rowA0 + 128 * h + w;   // wave-uniform
+      float* Lr = L + (long long)row0 * ldL;
+      f32x4 cv[RMW];
+#pragma unroll
+      for (int u = 0; u < RMW; ++u)
+        cv[u] = row0 + 8 * u < n ? *reinterpret_cast<const f32x4*>(Lr + 8 * u * ldL + gcl) : f32x4{0.f, 0.f, 0.f, 0.f};
       if (wr == h) {
 #pragma unroll
         for (int i = 0; i < 8; ++i)
@@ -879,20 +897,18 @@ __global__ __launch_bounds__(512) void lg_syrk6_kernel(const unsigned char* pl, 
             for (int q = 0; q < 4; ++q) St[(16 * i + 4 * lg + q) * S6_LDC + wc * 64 + 16 * j + lr] = acc[i][j][q];
       }
       __syncthreads();
-#pragma unroll 4
-      for (int e = tid; e < 128 * (S6_T / 4); e += 512) {
-        const int rr = e >> 6, c4 = 4 * (e & 63);
-        const int grow = k1 + rowA0 + 128 * h + rr, gcol = k1 + rowB0 + c4;
-        if (grow >= n) continue;
-        const f32x4 a = *reinterpret_cast<const f32x4*>(&St[rr * S6_LDC + c4]);
-        float* dst = L + (long long)grow * ldL + gcol;
-        if (gcol + 3 < n && (!diag || 128 * h + rr >= c4 + 3)) {
-          f32x4 c = *reinterpret_cast<const f32x4*>(dst);
-          *reinterpret_cast<f32x4*>(dst) = c - a;
+#pragma unroll
+      for (int u = 0; u < RMW; ++u) {
+        if (row0 + 8 * u >= n) continue;
+        const int rr = w + 8 * u;
+        const f32x4 v = cv[u] - *reinterpret_cast<const f32x4*>(&St[rr * S6_LDC + c4]);
+        float* dst = Lr + 8 * u * ldL + gcol;
+        if (colfull && (!diag || 128 * h + rr >= c4 + 3)) {
+          *reinterpret_cast<f32x4*>(dst) = v;
         } else {
 #pragma unroll
           for (int q = 0; q < 4; ++q)
-            if (gcol + q < n && (!diag || 128 * h + rr >= c4 + q)) dst[q] -= a[q];
+            if (gcol + q < n && (!diag || 128 * h + rr >= c4 + q)) dst[q] = v[q];
         }
       }
     }

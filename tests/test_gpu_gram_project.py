@@ -241,6 +241,7 @@ def test_span_tiles_first_pivot_and_upper_nan():
     (2085, 8192, 0.5, RIDGE_ABS),           # ragged last panel, several trailing tiles
     (6144, 8192, 1e-3, RIDGE_REL_TRACE),    # the first panel pairs' bulk updates on split bf16 planes
     (7000, 8192, 0.0, RIDGE_ABS),           # ... with a partial last 256-row tile, no ridge
+    (6998, 8192, 1e-3, RIDGE_ABS),          # ... with n not a multiple of 4: partial float4 column tails
 ])
 def test_span_blocked_matches_oracle(n, kappa, lam, mode):
     G, gbar, K, s, t2 = spd_problem(n, kappa, 900 + n)
