@@ -200,11 +200,13 @@ dr_status dr_gram_noalloc(const void* G, int64_t n, int64_t ldG, const void* Gt,
  * info = 0; a group with trace(K) = 0 under REL_TRACE returns w = 0.
  * A factor pivot that is not positive sets info = its 1-based index and
  * w = 0.  Arithmetic: n <= 64 entirely in fp64 on the exact fp32 K; n > 64
- * an fp32 Cholesky factor and two steps of iterative refinement with fp64
- * residuals of the fp32 K.  When those two steps do not bring w to about
- * 1e-6 relative accuracy (their corrections do not shrink fast enough,
- * which happens when cond(K + lam_eff I) * 2^-24 is not small), info =
- * DR_INFO_NOT_CONVERGED and w holds the last iterate.
+ * an fp32 Cholesky factor and at most two steps of iterative refinement
+ * with fp64 residuals of the fp32 K.  Refinement stops once the last two
+ * corrections (the first solution counting as the first) estimate the
+ * error left at about 1e-6 relative or less, so a well-conditioned group
+ * takes one step.  When two steps do not get there (the corrections do not
+ * shrink fast enough, which happens when cond(K + lam_eff I) * 2^-24 is not
+ * small), info = DR_INFO_NOT_CONVERGED and w holds the last iterate.
  * ------------------------------------------------------------------------- */
 dr_status dr_project_span(const float* K, const float* s, const float* t2, int64_t n, int P,
                           float lambda, dr_ridge_mode mode, float* w, float* lam_eff,

@@ -69,6 +69,7 @@ struct LgCtl {
   int nonfinite;   // some entry of K or s is not finite
   int info;        // reported info (1-based pivot, or DR_INFO_NONFINITE)
   float lam;       // lam_eff
+  int done;        // refinement converged before its last step; its remaining kernels return at once
   double dxn[kRefine + 1];   // max |dx| of each solve (the first solve's dx is x itself)
 };
 
@@ -128,6 +129,7 @@ __global__ void lg_init_kernel(LgCtl* ctl, const float* s, int n, int npad, doub
     ctl->nonfinite = 0;
     ctl->info = 0;
     ctl->lam = 0.f;
+    ctl->done = 0;
     for (int k = 0; k <= kRefine; ++k) ctl->dxn[k] = 0.0;
   }
   if (i < npad) {
@@ -1028,7 +1030,7 @@ __global__ __launch_bounds__(256) void lg_sinv_kernel(const float* L, long long 
 template <int RW>
 __global__ __launch_bounds__(256) void lg_rowdot_kernel(const float* M, long long ldM, int rows, int width, int mode,
                                                         const double* v, double* out, int sub, const LgCtl* ctl) {
-  if (ctl->skip) return;
+  if (ctl->skip || ctl->done) return;
   constexpr int CT = SBN / 256;   // float4 columns per lane
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int row0 = 4 * RW * blockIdx.x + RW * w;
@@ -1074,7 +1076,7 @@ __global__ __launch_bounds__(256) void lg_rowdot_kernel(const float* M, long lon
 constexpr int kColThreads = 1024;
 __global__ __launch_bounds__(kColThreads) void lg_coldot_kernel(const float* M, long long ldM, int rows,
                                                                 const double* v, double* out, const LgCtl* ctl) {
-  if (ctl->skip) return;
+  if (ctl->skip || ctl->done) return;
   constexpr int NS = kColThreads / 16, CU = SBN / NS;   // row streams, rows of a stream
   __shared__ double vs[SBN], part[NS][64];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -1115,29 +1117,45 @@ __global__ __launch_bounds__(kColThreads) void lg_coldot_kernel(const float* M, 
   }
 }
 
-// x += dx, and the solve's max |dx| into ctl->dxn[it] (one workgroup)
+// x += dx, and the solve's max |dx| into ctl->dxn[it] (one workgroup).
+// After the first refinement step (it = 1) the corrections so far are the
+// first solution x0 and dx1: if they already pass the convergence test
+// (the geometric estimate |dx1|^2 / |x0| of the error left), the second
+// step's kernels return at once.
 __global__ __launch_bounds__(1024) void lg_axpy_kernel(double* x, const double* dx, int npad, int it, LgCtl* ctl) {
-  __shared__ double sh[16];
-  if (ctl->skip) return;
-  double m = 0.0;
+  __shared__ double sh[16], shx[16];
+  if (ctl->skip || ctl->done) return;
+  double m = 0.0, mx = 0.0;
   for (int i = threadIdx.x; i < npad; i += 1024) {
-    x[i] += dx[i];
+    const double xi = x[i] + dx[i];
+    x[i] = xi;
     m = fmax(m, fabs(dx[i]));
+    mx = fmax(mx, fabs(xi));
   }
-  for (int off = 32; off > 0; off >>= 1) m = fmax(m, __shfl_xor(m, off, 64));
-  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = m;
+  for (int off = 32; off > 0; off >>= 1) {
+    m = fmax(m, __shfl_xor(m, off, 64));
+    mx = fmax(mx, __shfl_xor(mx, off, 64));
+  }
+  if ((threadIdx.x & 63) == 0) {
+    sh[threadIdx.x >> 6] = m;
+    shx[threadIdx.x >> 6] = mx;
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
-    double r = 0.0;
-    for (int q = 0; q < 16; ++q) r = fmax(r, sh[q]);
+    double r = 0.0, X = 0.0;
+    for (int q = 0; q < 16; ++q) {
+      r = fmax(r, sh[q]);
+      X = fmax(X, shx[q]);
+    }
     ctl->dxn[it] = r;
+    if (it >= 1 && it < kRefine && refine_converged(ctl->dxn[it - 1], r, X)) ctl->done = 1;
   }
 }
 
 // r = s - (K + lam I) x and kx = K x in fp64, one wave per row of K
 __global__ __launch_bounds__(256) void lg_resid_kernel(const float* K, int n, const float* s, const double* x,
                                                        double* r, double* kx, const LgCtl* ctl) {
-  if (ctl->skip) return;
+  if (ctl->skip || (!kx && ctl->done)) return;   // the final pass (kx != nullptr) always runs
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= n) return;
   const float* kr = K + (long long)row * n;
@@ -1180,7 +1198,7 @@ __global__ __launch_bounds__(1024) void lg_final_kernel(const float* s, const fl
   if (threadIdx.x == 0) {
     double X = 0.0;
     for (int k = 0; k < 16; ++k) X = fmax(X, shm[k]);
-    const bool converged = refine_converged(ctl->dxn[kRefine - 1], ctl->dxn[kRefine], X);
+    const bool converged = ctl->done || refine_converged(ctl->dxn[kRefine - 1], ctl->dxn[kRefine], X);
     resid2[0] = skip ? t2[0] : (float)((double)t2[0] + q);
     info[0] = skip ? ctl->info : (converged ? 0 : DR_INFO_NOT_CONVERGED);
   }

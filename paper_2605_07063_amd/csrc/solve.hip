@@ -487,27 +487,33 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
   for (int i = tid; i < n; i += kSpanThreads) y[i] = (double)sp[i];
   __syncthreads();
   chol_solve();
-  for (int i = tid; i < n; i += kSpanThreads) x[i] = y[i];
-  __syncthreads();
+  double x0m = 0.0;
+  for (int i = tid; i < n; i += kSpanThreads) {
+    x[i] = y[i];
+    x0m = fmax(x0m, fabs(y[i]));
+  }
+  // (block_absmax's barriers also publish x)
+  double dprev = block_absmax<kSpanThreads>(x0m, scratch);
 
-  // two steps of iterative refinement: y = s - (K + lam I) x in fp64 from
-  // the fp32 K, solve, x += y; the sizes of the two corrections decide
-  // whether the refinement converged
-  double dxmax[2];
-  for (int it = 0; it < 2; ++it) {
+  // at most two steps of iterative refinement: y = s - (K + lam I) x in
+  // fp64 from the fp32 K, solve, x += y; the sizes of the last two
+  // corrections (the first solution counts as the first) decide whether
+  // the refinement converged, and it stops as soon as they do
+  bool converged = false;
+  for (int it = 0; it < 2 && !converged; ++it) {
     kx_rows([&](int i, double kx) { y[i] = (double)sp[i] - (double)lam * x[i] - kx; });
     __syncthreads();
     chol_solve();
-    double dm = 0.0;
+    double dm = 0.0, xm = 0.0;
     for (int i = tid; i < n; i += kSpanThreads) {
       x[i] += y[i];
       dm = fmax(dm, fabs(y[i]));
+      xm = fmax(xm, fabs(x[i]));
     }
-    dxmax[it] = block_absmax<kSpanThreads>(dm, scratch);
+    const double dcur = block_absmax<kSpanThreads>(dm, scratch);
+    converged = refine_converged(dprev, dcur, block_absmax<kSpanThreads>(xm, scratch));
+    dprev = dcur;
   }
-  double xm = 0.0;
-  for (int i = tid; i < n; i += kSpanThreads) xm = fmax(xm, fabs(x[i]));
-  const bool converged = refine_converged(dxmax[0], dxmax[1], block_absmax<kSpanThreads>(xm, scratch));
 
   // resid2 = t2 - 2 s.x + x.K.x
   double part = 0.0;
