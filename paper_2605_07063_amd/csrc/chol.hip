@@ -101,11 +101,6 @@ LgLayout lg_layout(long long n) {
 
 __device__ __forceinline__ bool finite_f(float v) { return (__float_as_uint(v) & 0x7f800000u) != 0x7f800000u; }
 
-// 1 / sqrt(d), d > 0 normal: hardware estimate plus one Newton step
-__device__ __forceinline__ float rsqrt_nr(float d) {
-  const float r = __builtin_amdgcn_rsqf(d);
-  return r * fmaf(-0.5f * d * r, r, 1.5f);
-}
 
 template <int NT>
 __device__ double block_sum_d(double v, double* sh) {
@@ -224,10 +219,6 @@ __device__ __forceinline__ void tile_pair(int q, int& I, int& J) {
   J = q - i * (i + 1) / 2;
 }
 
-__device__ __forceinline__ float readlane_f(float v, int l) {
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
-}
-
 constexpr int LDA = NB + 4;   // LDS row stride (floats) of staged 128-wide blocks
 
 // C[row][col] += sum_{m < len} A[ra + row][ca + m] B[rb + col][cb + m] on one
@@ -264,14 +255,14 @@ __device__ __forceinline__ f32x4 tile_nn(const float* A, int ra, int ca, const f
 // packed lower-triangle 16x16 tiles (72 KiB in all, so the workgroup fits
 // on a CU beside a trailing-update workgroup):
 //   the diagonal tile D_J is factored and inverted in registers by wave 0
-//   (lane r holds row r; the pivot and the column reach the other lanes by
-//   v_readlane), one step ahead: while waves 1..3 take the trailing tiles
-//   of step J, wave 0 updates tile (J+1, J+1) first and factors it;
+//   (tile16_chol_inv), one step ahead: while waves 1..3 take the trailing
+//   tiles of step J, wave 0 updates tile (J+1, J+1) first and factors it;
 //   panel tiles L_IJ = A_IJ D_J^-T and trailing tiles A_IK -= L_IJ L_KJ^T
 //   are 16x16x16 fp32 MFMA products (two barriers per step);
-// then the off-diagonal tiles of the inverse follow by distance from the
-// diagonal, X_IJ = -X_II sum_{m=J}^{I-1} L_Im X_mJ (one barrier per
-// distance).  Row r of every tile is stored at row position prm(r), so the
+//   row J of the inverse, X_Jm = -X_JJ sum_{i=m}^{J-1} L_Ji X_im (m < J),
+//   needs only rows < J of it, the final tiles L_Ji and D_J^-1, so waves
+//   1..3 form it in step J after their trailing tiles, while wave 0
+//   factors tile J+1.  Row r of every tile is stored at row position prm(r), so the
 // rows 4q + j (q = 0..3) that one MFMA result register covers fall in four
 // different LDS bank groups.
 __device__ __forceinline__ int prm(int r) { return 4 * (r & 3) + (r >> 2); }
@@ -336,9 +327,9 @@ __global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, 
   __syncthreads();
 
   // wave 0: factor and invert diagonal tile J (block-relative pivot on failure)
-  auto factor_diag = [&](int J) {
+  auto factor_diag = [&](int J) __attribute__((always_inline)) {
     float* D = Lt + ptile(J, J) + prm(lr) * 16;
-    float a[16];
+    float a[16], xr[16];
 #pragma unroll
     for (int m = 0; m < 16; m += 4) {
       const float4 t = *reinterpret_cast<const float4*>(D + m);
@@ -347,54 +338,15 @@ __global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, 
       a[m + 2] = t.z;
       a[m + 3] = t.w;
     }
-    // per-lane predicates as 0 / 1 floats (products instead of selects keep
-    // them out of SGPR pairs); the tile is finite (non-finite inputs stop
-    // the group before any factor), so products can clear entries
-    auto gt = [&](int j) { return (float)((unsigned)(j - lr) >> 31); };   // 1 if lr > j
-    auto eq = [&](int j) { return gt(j - 1) - gt(j); };                  // 1 if lr == j
-#pragma unroll
-    for (int m = 0; m < 16; ++m) a[m] *= gt(m - 1);
-    float dv[16], dg[16];
-    int bad_j = 0;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      float d = readlane_f(a[j], j);
-      if (bad_j == 0 && !(d > 0.f)) bad_j = 16 * J + j + 1;   // uniform: d came from one lane
-      d = d > 0.f ? d : 1.f;
-      const float rs = rsqrt_nr(d);
-      dv[j] = rs;
-      dg[j] = d * rs;
-      const float f = gt(j) * (a[j] * rs);   // L[r][j] below the diagonal, 0 on and above it
-      a[j] = f;
-#pragma unroll
-      for (int c = j + 1; c < 16; ++c) a[c] = fmaf(-f, readlane_f(a[j], c), a[c]);
-    }
-    // row r of X = D^-1 from X D = I, columns right to left (X is lower
-    // triangular: the entries right of the diagonal come out exactly 0)
-    float xr[16];
-#pragma unroll
-    for (int c = 15; c >= 0; --c) {
-      float acc = eq(c);
-#pragma unroll
-      for (int m = c + 1; m < 16; ++m) acc = fmaf(-xr[m], readlane_f(a[c], m), acc);
-      xr[c] = acc * dv[c];
-    }
-    float mine = 0.f;   // this row's diagonal entry of L
-#pragma unroll
-    for (int j = 0; j < 16; ++j) mine = fmaf(eq(j), dg[j], mine);
+    const int bad_j = tile16_chol_inv(a, xr, lr);
     if (lane < 16) {
 #pragma unroll
       for (int m = 0; m < 16; m += 4) {
-        float4 t;
-        t.x = fmaf(a[m], gt(m), eq(m) * mine);
-        t.y = fmaf(a[m + 1], gt(m + 1), eq(m + 1) * mine);
-        t.z = fmaf(a[m + 2], gt(m + 2), eq(m + 2) * mine);
-        t.w = fmaf(a[m + 3], gt(m + 3), eq(m + 3) * mine);
-        *reinterpret_cast<float4*>(D + m) = t;
+        *reinterpret_cast<float4*>(D + m) = make_float4(a[m], a[m + 1], a[m + 2], a[m + 3]);
         *reinterpret_cast<float4*>(&Xd[J * 256 + prm(lr) * 16 + m]) = make_float4(xr[m], xr[m + 1], xr[m + 2], xr[m + 3]);
       }
     }
-    if (lane == 0 && bad_j && bad_s == 0) bad_s = bad_j;
+    if (lane == 0 && bad_j && bad_s == 0) bad_s = 16 * J + bad_j;
   };
   // C = A B^T on one tile pair (both read along their rows)
   auto nt16 = [&](const float* A, const float* B) {
@@ -406,6 +358,30 @@ __global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, 
     acc = mma_f32(av.z, bv.z, acc);
     acc = mma_f32(av.w, bv.w, acc);
     return acc;
+  };
+
+  // tile (I, J), J < I, of the inverse
+  auto inv_tile = [&](int I, int J) {
+    // T = sum_{m=J}^{I-1} L_Im X_mJ, X_mJ read as the MFMA B operand (k = row)
+    f32x4 t = {0.f, 0.f, 0.f, 0.f};
+    for (int m = J; m < I; ++m) {
+      const float4 av = *reinterpret_cast<const float4*>(Lt + ptile(I, m) + prm(lr) * 16 + 4 * lq);
+      const float* X = m == J ? Xd + J * 256 : Xo + otile(m, J);
+      t = mma_f32(av.x, X[prm(4 * lq + 0) * 16 + lr], t);
+      t = mma_f32(av.y, X[prm(4 * lq + 1) * 16 + lr], t);
+      t = mma_f32(av.z, X[prm(4 * lq + 2) * 16 + lr], t);
+      t = mma_f32(av.w, X[prm(4 * lq + 3) * 16 + lr], t);
+    }
+    // X_IJ = -X_II T: T's result layout (row 4 lq + j, column lr in
+    // register j) is the B operand of reduction index 4 lq + j
+    const float4 xv = *reinterpret_cast<const float4*>(Xd + I * 256 + prm(lr) * 16 + 4 * lq);
+    f32x4 x = {0.f, 0.f, 0.f, 0.f};
+    x = mma_f32(xv.x, t[0], x);
+    x = mma_f32(xv.y, t[1], x);
+    x = mma_f32(xv.z, t[2], x);
+    x = mma_f32(xv.w, t[3], x);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) Xo[otile(I, J) + prm(4 * lq + j) * 16 + lr] = -x[j];
   };
 
   if (w == 0) factor_diag(0);
@@ -437,6 +413,7 @@ __global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, 
       }
     } else {
       for (int q = w; q < nrest; q += 3) trail(q);
+      for (int m = w - 1; m < J; m += 3) inv_tile(J, m);
     }
     __syncthreads();
   }
@@ -463,33 +440,6 @@ __global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, 
     }
   }
 
-  // off-diagonal tiles of the inverse by distance d = I - J from the diagonal
-  for (int d = 1; d < NT; ++d) {
-    for (int J = w; J + d < NT; J += 4) {
-      const int I = J + d;
-      // T = sum_{m=J}^{I-1} L_Im X_mJ, X_mJ read as the MFMA B operand (k = row)
-      f32x4 t = {0.f, 0.f, 0.f, 0.f};
-      for (int m = J; m < I; ++m) {
-        const float4 av = *reinterpret_cast<const float4*>(Lt + ptile(I, m) + prm(lr) * 16 + 4 * lq);
-        const float* X = m == J ? Xd + J * 256 : Xo + otile(m, J);
-        t = mma_f32(av.x, X[prm(4 * lq + 0) * 16 + lr], t);
-        t = mma_f32(av.y, X[prm(4 * lq + 1) * 16 + lr], t);
-        t = mma_f32(av.z, X[prm(4 * lq + 2) * 16 + lr], t);
-        t = mma_f32(av.w, X[prm(4 * lq + 3) * 16 + lr], t);
-      }
-      // X_IJ = -X_II T: T's result layout (row 4 lq + j, column lr in
-      // register j) is the B operand of reduction index 4 lq + j
-      const float4 xv = *reinterpret_cast<const float4*>(Xd + I * 256 + prm(lr) * 16 + 4 * lq);
-      f32x4 x = {0.f, 0.f, 0.f, 0.f};
-      x = mma_f32(xv.x, t[0], x);
-      x = mma_f32(xv.y, t[1], x);
-      x = mma_f32(xv.z, t[2], x);
-      x = mma_f32(xv.w, t[3], x);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) Xo[otile(I, J) + prm(4 * lq + j) * 16 + lr] = -x[j];
-    }
-    __syncthreads();
-  }
   // the whole 128 x 128 inverse (upper tiles zero), row-major
   for (int e = tid; e < NB * (NB / 4); e += 256) {
     const int i = e / (NB / 4), c = 4 * (e % (NB / 4));

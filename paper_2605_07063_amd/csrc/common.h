@@ -125,6 +125,75 @@ __device__ __forceinline__ bool refine_converged(double a, double b, double X) {
   return b <= 0.5 * a && b * b <= 1e-6 * X * a;
 }
 
+// ---- one-wave Cholesky factor and inverse of a 16 x 16 tile (the diagonal
+// tiles of the blocked factorisations).  Lane l holds row r = l % 16 of the
+// tile in a[0..15] (lanes 16.. repeat rows 0..15; entries right of the
+// diagonal are ignored).  On return a is row r of L (zeros right of the
+// diagonal) and x row r of L^-1.  Column j: the pivot d = a_j[j] reaches
+// every lane by v_readlane; L[r][j] = a_r[j] / sqrt(d); the later columns
+// take a_r[c] -= L[r][j] L[c][j].  Lane j + 1 forms its next pivot from its
+// own L[j+1][j] (the value the broadcast would bring it), so the chain from
+// one pivot to the next is a readlane, a reciprocal square root (the
+// hardware estimate, 1 ulp: the factor is refined in fp64 by its users), a
+// product and an fma.  The inverse is a forward elimination of [D | I] run
+// alongside: y starts as row r of I, and at step j rows below j take
+// -(L[r][j] / L[j][j]) times row j (its columns <= j, the only ones it has
+// yet), so row r of L^-1 is y / L[r][r] at the end; these products fill the
+// latency of the pivot chain.  Returns the 1-based index of the first pivot
+// that is not positive, else 0 (the tile's values are then meaningless).
+__device__ __forceinline__ int tile16_chol_inv(float (&a)[16], float (&x)[16], int r) {
+  auto bcast = [](float v, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); };
+  // per-lane predicates as 0 / 1 floats (products instead of selects keep
+  // them out of SGPR pairs); a valid tile is finite, so products can clear
+  // entries
+  auto gt = [r](int j) { return (float)((unsigned)(j - r) >> 31); };   // 1 if r > j
+  auto eq = [&](int j) { return gt(j - 1) - gt(j); };                 // 1 if r == j
+  float y[16], dv[16], dg[16];
+#pragma unroll
+  for (int m = 0; m < 16; ++m) {
+    a[m] *= gt(m - 1);
+    y[m] = eq(m);
+  }
+  int bad = 0;
+  float p = a[0];   // lane j: a_j[j] after the columns before j
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const float d = bcast(p, j);
+    if (bad == 0 && !(d > 0.f)) bad = j + 1;   // uniform: d came from one lane
+    const float rs = __builtin_amdgcn_rsqf(d);
+    dv[j] = rs;
+    dg[j] = d * rs;
+    const float u = a[j] * rs;
+    if (j + 1 < 16) p = fmaf(-u, u, a[j + 1]);
+    const float f = gt(j) * u;   // L[r][j] below the diagonal, 0 on and above it
+    a[j] = f;
+    const float g = f * rs;
+    // the broadcasts first, into separate registers, then the products (a
+    // product right after the readlane that feeds it waits out a hazard)
+    float sa[16], sy[16];
+#pragma unroll
+    for (int c = j + 1; c < 16; ++c) sa[c] = bcast(f, c);
+#pragma unroll
+    for (int c = 0; c <= j; ++c) sy[c] = bcast(y[c], j);
+#pragma unroll
+    for (int c = j + 1; c < 16; ++c) a[c] = fmaf(-f, sa[c], a[c]);
+#pragma unroll
+    for (int c = 0; c <= j; ++c) y[c] = fmaf(-g, sy[c], y[c]);
+  }
+  float ld = 0.f, li = 0.f;   // L[r][r] and 1 / L[r][r]
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    ld = fmaf(eq(j), dg[j], ld);
+    li = fmaf(eq(j), dv[j], li);
+  }
+#pragma unroll
+  for (int m = 0; m < 16; ++m) {
+    a[m] = fmaf(a[m], gt(m), eq(m) * ld);
+    x[m] = y[m] * li;
+  }
+  return bad;
+}
+
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 inline dr_status launch_status() {

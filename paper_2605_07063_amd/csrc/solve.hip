@@ -123,11 +123,6 @@ __device__ __forceinline__ int row_at(int k) { return tile_at(k >> 4, 0) + rperm
 __device__ __forceinline__ float readlane_f(float v, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
 }
-// 1 / sqrt(d), d > 0 normal: hardware estimate plus one Newton step
-__device__ __forceinline__ float rsqrt_nr(float d) {
-  const float r = __builtin_amdgcn_rsqf(d);
-  return r * fmaf(-0.5f * d * r, r, 1.5f);
-}
 // q -> (I, J) with q = I (I + 1) / 2 + J, 0 <= J <= I
 __device__ __forceinline__ void tri_pair(int q, int& I, int& J) {
   int i = (int)((sqrtf(8.f * q + 1.f) - 1.f) * 0.5f);
@@ -221,9 +216,9 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
   // updates tile (J+1, J+1) first and factors it.  Per step, two barriers:
   // panel tiles L_IJ = A_IJ D_J^-T, then trailing tiles A_IK -= L_IJ L_KJ^T,
   // each one 16x16x16 fp32 MFMA product.
-  auto factor_diag = [&](int J) {
+  auto factor_diag = [&](int J) __attribute__((always_inline)) {
     float* D = Lt + tile_at(J, J) + rperm(lr) * 16;
-    float a[16];
+    float a[16], xr[16];
 #pragma unroll
     for (int m = 0; m < 16; m += 4) {
       const float4 t = *reinterpret_cast<const float4*>(D + m);
@@ -232,54 +227,15 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
       a[m + 2] = t.z;
       a[m + 3] = t.w;
     }
-    // per-lane predicates as 0 / 1 floats (products instead of selects
-    // keep them out of SGPR pairs); K is finite here, so the entries above
-    // the diagonal can be cleared by a product
-    auto gt = [&](int j) { return (float)((unsigned)(j - lr) >> 31); };   // 1 if lr > j
-    auto eq = [&](int j) { return gt(j - 1) - gt(j); };                  // 1 if lr == j
-#pragma unroll
-    for (int m = 0; m < 16; ++m) a[m] *= gt(m - 1);
-    float dv[16], dg[16];
-    int bad_j = 0;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      float d = readlane_f(a[j], j);
-      if (bad_j == 0 && !(d > 0.f)) bad_j = 16 * J + j + 1;
-      d = d > 0.f ? d : 1.f;
-      const float rs = rsqrt_nr(d);
-      dv[j] = rs;
-      dg[j] = d * rs;
-      const float f = gt(j) * (a[j] * rs);   // L[r][j] below the diagonal, 0 on and above it
-      a[j] = f;
-#pragma unroll
-      for (int c = j + 1; c < 16; ++c) a[c] = fmaf(-f, readlane_f(a[j], c), a[c]);
-    }
-    // row r of X = D^-1 from X D = I, columns right to left (X is lower
-    // triangular: the entries right of the diagonal come out exactly 0)
-    float xr[16];
-#pragma unroll
-    for (int c = 15; c >= 0; --c) {
-      float acc = eq(c);
-#pragma unroll
-      for (int m = c + 1; m < 16; ++m) acc = fmaf(-xr[m], readlane_f(a[c], m), acc);
-      xr[c] = acc * dv[c];
-    }
-    float mine = 0.f;   // this row's diagonal entry of L
-#pragma unroll
-    for (int j = 0; j < 16; ++j) mine = fmaf(eq(j), dg[j], mine);
+    const int bad_j = tile16_chol_inv(a, xr, lr);
     if (lane < 16) {
 #pragma unroll
       for (int m = 0; m < 16; m += 4) {
-        float4 t;
-        t.x = fmaf(a[m], gt(m), eq(m) * mine);
-        t.y = fmaf(a[m + 1], gt(m + 1), eq(m + 1) * mine);
-        t.z = fmaf(a[m + 2], gt(m + 2), eq(m + 2) * mine);
-        t.w = fmaf(a[m + 3], gt(m + 3), eq(m + 3) * mine);
-        *reinterpret_cast<float4*>(D + m) = t;
+        *reinterpret_cast<float4*>(D + m) = make_float4(a[m], a[m + 1], a[m + 2], a[m + 3]);
         *reinterpret_cast<float4*>(&Xt[J * 256 + lr * 16 + m]) = make_float4(xr[m], xr[m + 1], xr[m + 2], xr[m + 3]);
       }
     }
-    if (lane == 0 && bad_j) flag = bad_j;
+    if (lane == 0 && bad_j) flag = 16 * J + bad_j;
   };
   auto trail_tile = [&](int J, int I, int Kt) {
     const float4 av = *reinterpret_cast<const float4*>(&Lt[tile_at(I, J) + rperm(lr) * 16 + 4 * lq]);
