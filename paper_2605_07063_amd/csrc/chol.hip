@@ -62,7 +62,6 @@ constexpr int SB = 8;          // 128-blocks per super-block of the triangular s
 constexpr int SBN = SB * NB;   // rows of a super-block (leading dimension of its inverse)
 constexpr int LDP = NB + 4;    // LDS row stride (floats) of staged slices: b128 reads are conflict-free
 constexpr int kRefine = 2;
-constexpr int kPrepBlocks = 2048;
 
 struct LgCtl {
   int skip;        // the group's result is decided; later kernels return at once
@@ -136,28 +135,8 @@ __global__ void lg_init_kernel(LgCtl* ctl, const float* s, int n, int npad, doub
 }
 
 // non-finite check over all n*n entries of K (float4 when 16-byte aligned)
-__global__ __launch_bounds__(256) void lg_prep_kernel(const float* K, long long nn, int vec, LgCtl* ctl) {
-  __shared__ int any;
-  if (threadIdx.x == 0) any = 0;
-  __syncthreads();
-  bool bad = false;
-  const long long stride = (long long)gridDim.x * blockDim.x;
-  long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (vec) {
-    const float4* K4 = reinterpret_cast<const float4*>(K);
-    for (long long q = t; q < nn / 4; q += stride) {
-      const float4 v = K4[q];
-      bad |= !(finite_f(v.x) && finite_f(v.y) && finite_f(v.z) && finite_f(v.w));
-    }
-  } else {
-    for (long long q = t; q < nn; q += stride) bad |= !finite_f(K[q]);
-  }
-  if (bad) any = 1;
-  __syncthreads();
-  if (threadIdx.x == 0 && any) atomicOr(&ctl->nonfinite, 1);
-}
-
-// trace, lam_eff and the early outcomes (non-finite input, empty span)
+// trace, lam_eff and the early outcomes of s (non-finite entries) and of
+// the trace (empty span); non-finite entries of K are found by lg_load_kernel
 __global__ __launch_bounds__(1024) void lg_setup_kernel(const float* K, const float* s, int n, float lambda, int mode,
                                                         LgCtl* ctl, float* lam_eff_out) {
   __shared__ double sh[16];
@@ -173,7 +152,7 @@ __global__ __launch_bounds__(1024) void lg_setup_kernel(const float* K, const fl
   if (bad) sbad = 1;
   tr = block_sum_d<1024>(tr, sh);   // contains a barrier: sbad is visible after it
   if (threadIdx.x == 0) {
-    const bool nonfinite = ctl->nonfinite != 0 || sbad != 0;
+    const bool nonfinite = sbad != 0;
     const float lam = mode == DR_RIDGE_REL_TRACE ? (float)((double)lambda * tr / (double)n) : lambda;
     ctl->lam = lam;
     if (nonfinite) {
@@ -187,26 +166,54 @@ __global__ __launch_bounds__(1024) void lg_setup_kernel(const float* K, const fl
   }
 }
 
-// L = lower triangle of K + lam_eff I (row i, 4 columns per thread)
-__global__ __launch_bounds__(256) void lg_copy_kernel(const float* K, int n, float* L, long long ldL,
-                                                      const LgCtl* ctl) {
-  if (ctl->skip) return;
-  const int i = blockIdx.x;
-  const int c = (blockIdx.y * 256 + threadIdx.x) * 4;
-  if (c > i) return;
+// L = lower triangle of K + lam_eff I, and the finiteness scan of all of K
+// in the same pass (the upper triangle is read only for the scan): row i,
+// 4096 columns per workgroup, a float4 per thread and step (scalar loads
+// when n is not a multiple of 4 or K is not 16-byte aligned).  L is written
+// only when the group is still open; a non-finite entry closes it with
+// DR_INFO_NONFINITE, over the empty-span outcome of a zero trace.
+constexpr int kLoadCols = 4096;
+__global__ __launch_bounds__(256) void lg_load_kernel(const float* K, int n, int vec, float* L, long long ldL,
+                                                      LgCtl* ctl, float* lam_eff_out) {
+  __shared__ int any;
+  const int i = blockIdx.x, tid = threadIdx.x;
+  if (tid == 0) any = 0;
+  const bool write = ctl->skip == 0;
   const float lam = ctl->lam;
   const float* kr = K + (long long)i * n;
-  float4 v;
-  v.x = kr[c];
-  v.y = c + 1 < n ? kr[c + 1] : 0.f;
-  v.z = c + 2 < n ? kr[c + 2] : 0.f;
-  v.w = c + 3 < n ? kr[c + 3] : 0.f;
-  if (c == i) v.x += lam;
-  if (c + 1 == i) v.y += lam;
-  if (c + 2 == i) v.z += lam;
-  if (c + 3 == i) v.w += lam;
-  // columns past the diagonal (and past n, up to ldL) are never read
-  *reinterpret_cast<float4*>(L + (long long)i * ldL + c) = v;
+  __syncthreads();
+  bool bad = false;
+#pragma unroll
+  for (int u = 0; u < kLoadCols / 1024; ++u) {
+    const int c = blockIdx.y * kLoadCols + 1024 * u + 4 * tid;
+    if (c >= n) break;
+    float4 v;
+    if (vec) {
+      v = *reinterpret_cast<const float4*>(kr + c);
+    } else {
+      v.x = kr[c];
+      v.y = c + 1 < n ? kr[c + 1] : 0.f;
+      v.z = c + 2 < n ? kr[c + 2] : 0.f;
+      v.w = c + 3 < n ? kr[c + 3] : 0.f;
+    }
+    bad |= !(finite_f(v.x) && finite_f(v.y) && finite_f(v.z) && finite_f(v.w));
+    if (write && c <= i) {
+      if (c == i) v.x += lam;
+      if (c + 1 == i) v.y += lam;
+      if (c + 2 == i) v.z += lam;
+      if (c + 3 == i) v.w += lam;
+      // columns past the diagonal (and past n, up to ldL) are never read
+      *reinterpret_cast<float4*>(L + (long long)i * ldL + c) = v;
+    }
+  }
+  if (bad) any = 1;
+  __syncthreads();
+  if (tid == 0 && any) {   // every workgroup that finds one stores the same outcome
+    ctl->nonfinite = 1;
+    ctl->skip = 1;
+    ctl->info = DR_INFO_NONFINITE;
+    *lam_eff_out = 0.f;
+  }
 }
 
 // ---------------------------------------------------------------- panel
@@ -1126,6 +1133,45 @@ __global__ __launch_bounds__(256) void lg_resid_kernel(const float* K, int n, co
   }
 }
 
+// The same with four rows per wave (n a multiple of 4, K 16-byte aligned):
+// each load of x (fp64) serves four rows of K, where one row per wave
+// fetched x from L2 once per row, twice the bytes of K itself.  Lane l takes
+// columns 4 l + 256 t as a float4 of each row; rows past n reread row n - 1
+// and their sums are dropped.
+__global__ __launch_bounds__(256) void lg_resid4_kernel(const float* K, int n, const float* s, const double* x,
+                                                        double* r, double* kx, const LgCtl* ctl) {
+  if (ctl->skip || (!kx && ctl->done)) return;   // the final pass (kx != nullptr) always runs
+  const int lane = threadIdx.x & 63;
+  const int row0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * 4;
+  if (row0 >= n) return;
+  const float* kr[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) kr[u] = K + (long long)min(row0 + u, n - 1) * n;
+  double acc[4][2] = {{0.0, 0.0}, {0.0, 0.0}, {0.0, 0.0}, {0.0, 0.0}};
+#pragma unroll 2
+  for (int j = 4 * lane; j < n; j += 256) {
+    const double2 x01 = *reinterpret_cast<const double2*>(x + j);
+    const double2 x23 = *reinterpret_cast<const double2*>(x + j + 2);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float4 kv = *reinterpret_cast<const float4*>(kr[u] + j);
+      acc[u][0] = fma((double)kv.x, x01.x, acc[u][0]);
+      acc[u][1] = fma((double)kv.y, x01.y, acc[u][1]);
+      acc[u][0] = fma((double)kv.z, x23.x, acc[u][0]);
+      acc[u][1] = fma((double)kv.w, x23.y, acc[u][1]);
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const double t = wave_sum_l63(acc[u][0] + acc[u][1]);
+    const int row = row0 + u;
+    if (lane == 63 && row < n) {
+      r[row] = (double)s[row] - t - (double)ctl->lam * x[row];
+      if (kx) kx[row] = t;
+    }
+  }
+}
+
 __global__ __launch_bounds__(1024) void lg_final_kernel(const float* s, const float* t2, int n, const double* x,
                                                         const double* kx, const LgCtl* ctl, float* w, float* resid2,
                                                         int* info) {
@@ -1239,12 +1285,10 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
     const float* Kp = K + (long long)p * nn;
     const float* sp = s + (long long)p * n;
     hipLaunchKernelGGL(lg_init_kernel, dim3((npad + 255) / 256), dim3(256), 0, hs, ctl, sp, n, npad, x, dx, r, z);
-    const int vec = aligned16(Kp) && (nn % 4 == 0);
-    long long want = (nn / (vec ? 4 : 1) + 255) / 256;
-    const int pb = (int)(want < kPrepBlocks ? want : kPrepBlocks);
-    hipLaunchKernelGGL(lg_prep_kernel, dim3(pb), dim3(256), 0, hs, Kp, nn, vec, ctl);
+    const int vec = aligned16(Kp) && n % 4 == 0;
     hipLaunchKernelGGL(lg_setup_kernel, dim3(1), dim3(1024), 0, hs, Kp, sp, n, lambda, mode, ctl, lam_eff + p);
-    hipLaunchKernelGGL(lg_copy_kernel, dim3(n, (n + 1023) / 1024), dim3(256), 0, hs, Kp, n, L, ldL, ctl);
+    hipLaunchKernelGGL(lg_load_kernel, dim3(n, (n + kLoadCols - 1) / kLoadCols), dim3(256), 0, hs, Kp, n, vec, L, ldL,
+                       ctl, lam_eff + p);
     // Right-looking blocked factorisation by pairs of panels, with
     // look-ahead.  The trailing matrix takes one rank-256 update per pair
     // (half the passes over it of rank-128 updates).  For the pair (b, b+1)
@@ -1301,14 +1345,21 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
         hipLaunchKernelGGL(lg_syrk_kernel<2 * NB>, dim3(grid), dim3(256), 0, hs, L, ldL, n, k, h, 0, nrest, ctl);
       }
     }
+    // r = s - (K + lam I) x, and K x into kx when kx != nullptr
+    const bool rows4 = n % 4 == 0 && aligned16(Kp);
+    auto resid = [&](double* kx) {
+      if (rows4)
+        hipLaunchKernelGGL(lg_resid4_kernel, dim3((n + 15) / 16), dim3(256), 0, hs, Kp, n, sp, x, r, kx, ctl);
+      else
+        hipLaunchKernelGGL(lg_resid_kernel, dim3((n + 3) / 4), dim3(256), 0, hs, Kp, n, sp, x, r, kx, ctl);
+    };
     const int nsb = (nblk + SB - 1) / SB;
     for (int d = 0; d < SB; ++d)
       hipLaunchKernelGGL(lg_sinv_kernel, dim3(SB - d, nsb), dim3(256), 0, hs, L, ldL, n, nblk, inv, sinv, sinvt, d,
                          ctl);
     for (int it = 0; it <= kRefine; ++it) {
       if (it > 0)
-        hipLaunchKernelGGL(lg_resid_kernel, dim3((n + 3) / 4), dim3(256), 0, hs, Kp, n, sp, x, r, (double*)nullptr,
-                           ctl);
+        resid(nullptr);
       // L z = r (r is consumed), then L^T dx = z (z is consumed), by super-blocks
       for (int S = 0; S < nsb; ++S) {
         const int o0 = SBN * S, nb = nblk - SB * S < SB ? nblk - SB * S : SB, width = NB * nb;
@@ -1333,7 +1384,7 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       }
       hipLaunchKernelGGL(lg_axpy_kernel, dim3(1), dim3(1024), 0, hs, x, dx, npad, it, ctl);
     }
-    hipLaunchKernelGGL(lg_resid_kernel, dim3((n + 3) / 4), dim3(256), 0, hs, Kp, n, sp, x, r, z, ctl);
+    resid(z);
     hipLaunchKernelGGL(lg_final_kernel, dim3(1), dim3(1024), 0, hs, sp, t2 + p, n, x, z, ctl, w + (long long)p * n,
                        resid2 + p, info + p);
     const dr_status st = launch_status();
