@@ -127,25 +127,61 @@ __device__ __forceinline__ bool refine_converged(double a, double b, double X) {
 
 // ---- one-wave Cholesky factor and inverse of a 16 x 16 tile (the diagonal
 // tiles of the blocked factorisations).  Lane l holds row r = l % 16 of the
-// tile in a[0..15] (lanes 16.. repeat rows 0..15; entries right of the
-// diagonal are ignored).  On return a is row r of L (zeros right of the
-// diagonal) and x row r of L^-1.  Column j: the pivot d = a_j[j] reaches
-// every lane by v_readlane; L[r][j] = a_r[j] / sqrt(d); the later columns
-// take a_r[c] -= L[r][j] L[c][j].  Lane j + 1 forms its next pivot from its
-// own L[j+1][j] (the value the broadcast would bring it), so the chain from
-// one pivot to the next is a readlane, a reciprocal square root (the
+// tile in a[0..15]; each 16-lane row of the wave holds the whole tile
+// (entries right of the diagonal are ignored).  On return a is row r of L
+// (zeros right of the diagonal) and x row r of L^-1.  Column j: the pivot
+// d = a_j[j]; L[r][j] = a_r[j] / sqrt(d); the later columns take
+// a_r[c] -= L[r][j] L[c][j].  Values cross lanes only inside a 16-lane row,
+// by the DPP row_newbcast source modifier (lane n of the row to every lane
+// of it), fused into the fma that uses them: one instruction per update and
+// no trip through a scalar register.  Lane j + 1 forms its next pivot from
+// its own L[j+1][j] (the value the broadcast would bring it), so the chain
+// from one pivot to the next is a broadcast, a reciprocal square root (the
 // hardware estimate, 1 ulp: the factor is refined in fp64 by its users), a
 // product and an fma.  The inverse is a forward elimination of [D | I] run
 // alongside: y starts as row r of I, and at step j rows below j take
 // -(L[r][j] / L[j][j]) times row j (its columns <= j, the only ones it has
-// yet), so row r of L^-1 is y / L[r][r] at the end; these products fill the
-// latency of the pivot chain.  Returns the 1-based index of the first pivot
-// that is not positive, else 0 (the tile's values are then meaningless).
+// yet), so row r of L^-1 is y / L[r][r] at the end; these updates fill the
+// latency of the pivot chain.  A DPP source must not have been written by
+// the two instructions before it: the first update of a column carries two
+// wait states after the write of L[.][j]; an inverse update reads y[c],
+// last written by the inverse updates of the previous column, at least
+// fourteen of these (ordered) instructions back.  All 64 lanes must be
+// active.  Returns the 1-based index of the first pivot that is not
+// positive, else 0 (the tile's values are then meaningless).
+template <int N>
+__device__ __forceinline__ float row_bcast16(float v) {   // lane N of this lane's 16-lane row
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x150 + N, 0xF, 0xF, false));
+}
+// acc += (src of lane N of this lane's 16-lane row) * mul, one instruction;
+// NOP: two wait states first (a VALU write of src must be that far back)
+template <int N, bool NOP>
+__device__ __forceinline__ void fmac_row(float& acc, float src, float mul) {
+  if (NOP)
+    asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf"
+                 : "+v"(acc) : "v"(src), "v"(mul), "n"(N));
+  else
+    asm volatile("v_fmac_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf"
+                 : "+v"(acc) : "v"(src), "v"(mul), "n"(N));
+}
+#define DR_ROW_CASES(F) F(0) F(1) F(2) F(3) F(4) F(5) F(6) F(7) F(8) F(9) F(10) F(11) F(12) F(13) F(14) F(15)
+__device__ __forceinline__ float row_bcast(float v, int n) {   // n a constant after unrolling
+  switch (n) {
+#define DR_CASE(K) case K: return row_bcast16<K>(v);
+    DR_ROW_CASES(DR_CASE)
+#undef DR_CASE
+  }
+  return v;
+}
+template <bool NOP>
+__device__ __forceinline__ void fmac_rown(float& acc, float src, float mul, int n) {
+  switch (n) {
+#define DR_CASE(K) case K: fmac_row<K, NOP>(acc, src, mul); break;
+    DR_ROW_CASES(DR_CASE)
+#undef DR_CASE
+  }
+}
 __device__ __forceinline__ int tile16_chol_inv(float (&a)[16], float (&x)[16], int r) {
-  auto bcast = [](float v, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); };
-  // per-lane predicates as 0 / 1 floats (products instead of selects keep
-  // them out of SGPR pairs); a valid tile is finite, so products can clear
-  // entries
   auto gt = [r](int j) { return (float)((unsigned)(j - r) >> 31); };   // 1 if r > j
   auto eq = [&](int j) { return gt(j - 1) - gt(j); };                 // 1 if r == j
   float y[16], dv[16], dg[16];
@@ -155,32 +191,28 @@ __device__ __forceinline__ int tile16_chol_inv(float (&a)[16], float (&x)[16], i
     y[m] = eq(m);
   }
   int bad = 0;
-  float p = a[0];   // lane j: a_j[j] after the columns before j
+  float p = a[0];
 #pragma unroll
   for (int j = 0; j < 16; ++j) {
-    const float d = bcast(p, j);
-    if (bad == 0 && !(d > 0.f)) bad = j + 1;   // uniform: d came from one lane
+    const float d = row_bcast(p, j);
+    if (bad == 0 && !(d > 0.f)) bad = j + 1;
     const float rs = __builtin_amdgcn_rsqf(d);
     dv[j] = rs;
     dg[j] = d * rs;
     const float u = a[j] * rs;
     if (j + 1 < 16) p = fmaf(-u, u, a[j + 1]);
-    const float f = gt(j) * u;   // L[r][j] below the diagonal, 0 on and above it
+    const float f = gt(j) * u;
     a[j] = f;
-    const float g = f * rs;
-    // the broadcasts first, into separate registers, then the products (a
-    // product right after the readlane that feeds it waits out a hazard)
-    float sa[16], sy[16];
+    const float nf = -f, ng = -(f * rs);
 #pragma unroll
-    for (int c = j + 1; c < 16; ++c) sa[c] = bcast(f, c);
+    for (int c = j + 1; c < 16; ++c) {
+      if (c == j + 1) fmac_rown<true>(a[c], f, nf, c);
+      else fmac_rown<false>(a[c], f, nf, c);
+    }
 #pragma unroll
-    for (int c = 0; c <= j; ++c) sy[c] = bcast(y[c], j);
-#pragma unroll
-    for (int c = j + 1; c < 16; ++c) a[c] = fmaf(-f, sa[c], a[c]);
-#pragma unroll
-    for (int c = 0; c <= j; ++c) y[c] = fmaf(-g, sy[c], y[c]);
+    for (int c = 0; c <= j; ++c) fmac_rown<false>(y[c], y[c], ng, j);
   }
-  float ld = 0.f, li = 0.f;   // L[r][r] and 1 / L[r][r]
+  float ld = 0.f, li = 0.f;
 #pragma unroll
   for (int j = 0; j < 16; ++j) {
     ld = fmaf(eq(j), dg[j], ld);
@@ -191,7 +223,7 @@ __device__ __forceinline__ int tile16_chol_inv(float (&a)[16], float (&x)[16], i
     a[m] = fmaf(a[m], gt(m), eq(m) * ld);
     x[m] = y[m] * li;
   }
-  return bad;
+  return __builtin_amdgcn_readfirstlane(bad);
 }
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
