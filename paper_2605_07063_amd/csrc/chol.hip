@@ -884,38 +884,60 @@ __global__ __launch_bounds__(512) void lg_syrk6_kernel(const unsigned char* pl, 
 // its inverse (or the transpose, for L^T), and its contribution to the rest
 // of the right-hand side.
 
-// Block (i, j) = (j + d, j) of the inverse X of super-block S, d >= 1:
-//   X_ij = -X_ii sum_{m=j}^{i-1} L_im X_mj
-// (d = 0 copies the 128 x 128 block inverses onto the diagonal).  One
-// workgroup per block; the 128 x 128 operands are staged in LDS and wave w
-// computes rows 32 w .. 32 w + 31 with fp32 MFMA.
+// Block row ii of the inverse X of super-block S: block (ii, jj), jj < ii,
+//   X_ij = -X_ii sum_{m=j}^{i-1} L_im X_mj,
+// needs only the factor's block row ii (final once block ii is factored),
+// the rows of X above it and X_ii, the inverse of the 128 x 128 diagonal
+// block (read where the block factor left it); jj = ii copies X_ii onto the
+// diagonal.  Each block is split over SV_CQ workgroups by column quarters
+// (the chain of products of a block is the latency that counts); the
+// 128 x 128 L_im and the quarter of X_mj are staged in LDS and wave w
+// computes rows 32 w .. 32 w + 31 of the quarter with fp32 MFMA.  The block
+// also goes, transposed, into block (jj, ii) of the transpose.
+constexpr int SV_CQ = 4, SV_CW = NB / SV_CQ, SV_LDB = SV_CW + 4;
+
+// C[row][col] += sum_{m < len} A[ra + row][ca + m] B[rb + m][cb + col], B
+// with row stride SV_LDB
+__device__ __forceinline__ f32x4 tile_nn_q(const float* A, int ra, const float* B, int cb, int lr, int lq, f32x4 acc) {
+  for (int m = 0; m < NB; m += 16) {
+    const float4 av = *reinterpret_cast<const float4*>(&A[(ra + lr) * LDA + m + 4 * lq]);
+    const float* bp = &B[(m + 4 * lq) * SV_LDB + cb + lr];
+    acc = mma_f32(av.x, bp[0], acc);
+    acc = mma_f32(av.y, bp[SV_LDB], acc);
+    acc = mma_f32(av.z, bp[2 * SV_LDB], acc);
+    acc = mma_f32(av.w, bp[3 * SV_LDB], acc);
+  }
+  return acc;
+}
+
 __global__ __launch_bounds__(256) void lg_sinv_kernel(const float* L, long long ldL, int n, int nblk,
-                                                      const float* inv, float* sinv, float* sinvt, int d,
+                                                      const float* inv, float* sinv, float* sinvt, int S, int ii,
                                                       const LgCtl* ctl) {
   if (ctl->skip) return;
-  const int S = blockIdx.y, jj = blockIdx.x, ii = jj + d;
+  const int jj = blockIdx.x / SV_CQ, cq = blockIdx.x % SV_CQ, d = ii - jj;
   const int bj = SB * S + jj, bi = bj + d;
-  if (ii >= SB || bi >= nblk) return;
+  if (d < 0 || bi >= nblk) return;
   float* X = sinv + (long long)S * SBN * SBN;     // [SBN][SBN]
   float* XT = sinvt + (long long)S * SBN * SBN;   // [SBN][SBN], X transposed
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, c0 = SV_CW * cq;
   if (d == 0) {
     const float* ib = inv + (long long)bi * NB * NB;
-    for (int e = tid; e < NB * NB / 4; e += 256) {
-      const int r = e / (NB / 4), c = 4 * (e % (NB / 4));
+    for (int e = tid; e < NB * SV_CW / 4; e += 256) {
+      // columns c0.. of all rows of X_ii, and rows c0.. of its transpose
+      const int r = e / (SV_CW / 4), c = c0 + 4 * (e % (SV_CW / 4));
       *reinterpret_cast<float4*>(X + (long long)(NB * ii + r) * SBN + NB * ii + c) =
           *reinterpret_cast<const float4*>(ib + r * NB + c);
-      // row r of the transpose = column r of the block
-      *reinterpret_cast<float4*>(XT + (long long)(NB * ii + r) * SBN + NB * ii + c) =
-          make_float4(ib[c * NB + r], ib[(c + 1) * NB + r], ib[(c + 2) * NB + r], ib[(c + 3) * NB + r]);
+      const int t = c0 + e / (NB / 4), cc = 4 * (e % (NB / 4));
+      *reinterpret_cast<float4*>(XT + (long long)(NB * ii + t) * SBN + NB * ii + cc) =
+          make_float4(ib[cc * NB + t], ib[(cc + 1) * NB + t], ib[(cc + 2) * NB + t], ib[(cc + 3) * NB + t]);
     }
     return;
   }
   __shared__ __attribute__((aligned(16))) float As[NB * LDA];
-  __shared__ __attribute__((aligned(16))) float Bs[NB * LDA];
+  __shared__ __attribute__((aligned(16))) float Bs[NB * SV_LDB];
   const int lane = tid & 63, w = tid >> 6, lr = lane & 15, lq = lane >> 4;
-  // stage a 128 x 128 block (row stride ld, rows >= rows_valid read as 0)
-  auto stage = [&](float* dst, const float* src, long long ld, int rows_valid) {
+  // stage a 128 x 128 block into As (row stride ld, rows >= rows_valid read as 0)
+  auto stage_a = [&](const float* src, long long ld, int rows_valid) {
     float4 v[16];
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
@@ -926,55 +948,72 @@ __global__ __launch_bounds__(256) void lg_sinv_kernel(const float* L, long long 
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
       const int e = tid + 256 * u, r = e / (NB / 4), c = 4 * (e % (NB / 4));
-      *reinterpret_cast<float4*>(&dst[r * LDA + c]) = v[u];
+      *reinterpret_cast<float4*>(&As[r * LDA + c]) = v[u];
     }
   };
-  f32x4 acc[2][8];
+  // columns c0 .. c0 + SV_CW of a 128-row block of X into Bs
+  auto stage_b = [&](const float* src) {
+    float4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = tid + 256 * u, r = e / (SV_CW / 4), c = 4 * (e % (SV_CW / 4));
+      v[u] = *reinterpret_cast<const float4*>(src + (long long)r * SBN + c0 + c);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = tid + 256 * u, r = e / (SV_CW / 4), c = 4 * (e % (SV_CW / 4));
+      *reinterpret_cast<float4*>(&Bs[r * SV_LDB + c]) = v[u];
+    }
+  };
+  constexpr int CT = SV_CW / 16;   // 16-column tiles of the quarter
+  f32x4 acc[2][CT];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int c = 0; c < 8; ++c) acc[a][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < CT; ++c) acc[a][c] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int rows_i = n - NB * bi < NB ? n - NB * bi : NB;   // rows of L that exist in block row bi
   for (int m = bj; m < bi; ++m) {
-    stage(As, L + (long long)NB * bi * ldL + NB * m, ldL, rows_i);                       // L_im
-    stage(Bs, X + (long long)(NB * (m - SB * S)) * SBN + NB * jj, SBN, NB);            // X_mj
+    stage_a(L + (long long)NB * bi * ldL + NB * m, ldL, rows_i);        // L_im
+    stage_b(X + (long long)(NB * (m - SB * S)) * SBN + NB * jj);        // X_mj, the quarter
     __syncthreads();
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int c = 0; c < 8; ++c) acc[a][c] = tile_nn(As, 32 * w + 16 * a, 0, Bs, 0, 16 * c, NB, lr, lq, acc[a][c]);
+      for (int c = 0; c < CT; ++c) acc[a][c] = tile_nn_q(As, 32 * w + 16 * a, Bs, 16 * c, lr, lq, acc[a][c]);
     __syncthreads();
   }
   // T into Bs, X_ii into As, then X_ij = -X_ii T
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int c = 0; c < 8; ++c)
+    for (int c = 0; c < CT; ++c)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) Bs[(32 * w + 16 * a + 4 * lq + q) * LDA + 16 * c + lr] = acc[a][c][q];
-  stage(As, X + (long long)(NB * ii) * SBN + NB * ii, SBN, NB);
+      for (int q = 0; q < 4; ++q) Bs[(32 * w + 16 * a + 4 * lq + q) * SV_LDB + 16 * c + lr] = acc[a][c][q];
+  stage_a(inv + (long long)bi * NB * NB, NB, NB);
   __syncthreads();
-  f32x4 xo[2][8];
+  f32x4 xo[2][CT];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int c = 0; c < 8; ++c) xo[a][c] = tile_nn(As, 32 * w + 16 * a, 0, Bs, 0, 16 * c, NB, lr, lq, f32x4{0.f, 0.f, 0.f, 0.f});
+    for (int c = 0; c < CT; ++c) xo[a][c] = tile_nn_q(As, 32 * w + 16 * a, Bs, 16 * c, lr, lq, f32x4{0.f, 0.f, 0.f, 0.f});
   __syncthreads();   // every wave is done reading As and Bs
-  // X_ij = -X_ii T through LDS, then out row by row and, transposed, into
-  // block (jj, ii) of XT (coalesced both ways)
+  // the quarter of X_ij = -X_ii T through LDS, then out row by row and,
+  // transposed, into rows c0.. of block (jj, ii) of XT (coalesced both ways)
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int c = 0; c < 8; ++c)
+    for (int c = 0; c < CT; ++c)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) Bs[(32 * w + 16 * a + 4 * lq + q) * LDA + 16 * c + lr] = -xo[a][c][q];
+      for (int q = 0; q < 4; ++q) Bs[(32 * w + 16 * a + 4 * lq + q) * SV_LDB + 16 * c + lr] = -xo[a][c][q];
   __syncthreads();
-  for (int e = tid; e < NB * NB / 4; e += 256) {
-    const int r = e / (NB / 4), c = 4 * (e % (NB / 4));
-    *reinterpret_cast<float4*>(X + (long long)(NB * ii + r) * SBN + NB * jj + c) =
-        *reinterpret_cast<const float4*>(&Bs[r * LDA + c]);
-    *reinterpret_cast<float4*>(XT + (long long)(NB * jj + r) * SBN + NB * ii + c) =
-        make_float4(Bs[c * LDA + r], Bs[(c + 1) * LDA + r], Bs[(c + 2) * LDA + r], Bs[(c + 3) * LDA + r]);
+  for (int e = tid; e < NB * SV_CW / 4; e += 256) {
+    const int r = e / (SV_CW / 4), c = 4 * (e % (SV_CW / 4));
+    *reinterpret_cast<float4*>(X + (long long)(NB * ii + r) * SBN + NB * jj + c0 + c) =
+        *reinterpret_cast<const float4*>(&Bs[r * SV_LDB + c]);
+    const int t = e / (NB / 4), cc = 4 * (e % (NB / 4));
+    *reinterpret_cast<float4*>(XT + (long long)(NB * jj + c0 + t) * SBN + NB * ii + cc) =
+        make_float4(Bs[cc * SV_LDB + t], Bs[(cc + 1) * SV_LDB + t], Bs[(cc + 2) * SV_LDB + t],
+                    Bs[(cc + 3) * SV_LDB + t]);
   }
 }
 
@@ -1204,10 +1243,17 @@ __global__ __launch_bounds__(1024) void lg_final_kernel(const float* s, const fl
 
 size_t span_large_workspace(int64_t n) { return lg_layout(n).total; }
 
+// the blocked solver's own streams and events (default priority), besides
+// the caller's stream: aux runs the diagonal-block chain one pair ahead;
+// sol forms the inverses of the diagonal super-blocks and the first forward
+// solve while the factorisation is still running
+struct LgStreams {
+  hipStream_t aux = nullptr, sol = nullptr;
+  hipEvent_t ev_col = nullptr, ev_next = nullptr, ev_blk = nullptr, ev_sol = nullptr;
+};
 static dr_status span_large_groups(const float* K, const float* s, const float* t2, int n, int P, float lambda,
                                    int mode, float* w, float* lam_eff, float* resid2, int32_t* info,
-                                   const LgLayout& lay, unsigned char* base, hipStream_t hs, hipStream_t aux,
-                                   hipEvent_t ev_col, hipEvent_t ev_next);
+                                   const LgLayout& lay, unsigned char* base, hipStream_t hs, const LgStreams& st);
 
 // The look-ahead stream (default priority) and its two events: one set per
 // device, created by the first blocked solve on that device and kept until
@@ -1220,10 +1266,19 @@ constexpr int kMaxDevices = 64;
 struct AuxSet {
   std::mutex mu;
   bool ready = false;
-  hipStream_t aux = nullptr;
-  hipEvent_t ev_col = nullptr, ev_next = nullptr;
+  LgStreams st;
 };
 AuxSet g_aux[kMaxDevices];
+
+void destroy_streams(LgStreams& st) {
+  if (st.ev_col) (void)hipEventDestroy(st.ev_col);
+  if (st.ev_next) (void)hipEventDestroy(st.ev_next);
+  if (st.ev_blk) (void)hipEventDestroy(st.ev_blk);
+  if (st.ev_sol) (void)hipEventDestroy(st.ev_sol);
+  if (st.aux) (void)hipStreamDestroy(st.aux);
+  if (st.sol) (void)hipStreamDestroy(st.sol);
+  st = LgStreams{};
+}
 }  // namespace
 
 dr_status span_large(const float* K, const float* s, const float* t2, int64_t n64, int P, float lambda, int mode,
@@ -1239,25 +1294,26 @@ dr_status span_large(const float* K, const float* s, const float* t2, int64_t n6
   AuxSet& a = g_aux[dev];
   std::lock_guard<std::mutex> lock(a.mu);
   if (!a.ready) {
-    if (hipStreamCreateWithFlags(&a.aux, hipStreamNonBlocking) != hipSuccess) return DR_ERR_HIP;
-    if (hipEventCreateWithFlags(&a.ev_col, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&a.ev_next, hipEventDisableTiming) != hipSuccess) {
-      if (a.ev_col) (void)hipEventDestroy(a.ev_col);
-      (void)hipStreamDestroy(a.aux);
-      a.aux = nullptr;
-      a.ev_col = nullptr;
+    LgStreams& st = a.st;
+    if (hipStreamCreateWithFlags(&st.aux, hipStreamNonBlocking) != hipSuccess ||
+        hipStreamCreateWithFlags(&st.sol, hipStreamNonBlocking) != hipSuccess ||
+        hipEventCreateWithFlags(&st.ev_col, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&st.ev_next, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&st.ev_blk, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&st.ev_sol, hipEventDisableTiming) != hipSuccess) {
+      destroy_streams(st);
       return DR_ERR_HIP;
     }
     a.ready = true;
   }
-  return span_large_groups(K, s, t2, n, P, lambda, mode, w, lam_eff, resid2, info, lay, base, hs, a.aux, a.ev_col,
-                           a.ev_next);
+  return span_large_groups(K, s, t2, n, P, lambda, mode, w, lam_eff, resid2, info, lay, base, hs, a.st);
 }
 
 static dr_status span_large_groups(const float* K, const float* s, const float* t2, int n, int P, float lambda,
                                    int mode, float* w, float* lam_eff, float* resid2, int32_t* info,
-                                   const LgLayout& lay, unsigned char* base, hipStream_t hs, hipStream_t aux,
-                                   hipEvent_t ev_col, hipEvent_t ev_next) {
+                                   const LgLayout& lay, unsigned char* base, hipStream_t hs, const LgStreams& st) {
+  hipStream_t aux = st.aux, sol = st.sol;
+  hipEvent_t ev_col = st.ev_col, ev_next = st.ev_next, ev_blk = st.ev_blk, ev_sol = st.ev_sol;
   // the bulk trailing update runs persistent on 7/8 of the two-per-CU
   // workgroup slots: one CU in four keeps room (LDS and waves) for one more
   // workgroup, where the diagonal-block chain of the next pair (factor,
@@ -1297,20 +1353,60 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
     // the previous pair's update of the columns right of b+1; then the main
     // stream updates the next pair's two columns (head) and, while the aux
     // stream factors that pair, the rest.
-    auto factor_panel = [&](int b, hipStream_t st) {
+    auto factor_panel = [&](int b, hipStream_t strm) {
       const int k = NB * b;
       const int kb = n - k < NB ? n - k : NB;
       float* ib = inv + (long long)b * NB * NB;
-      hipLaunchKernelGGL(lg_potrf_kernel<kPotrfPB>, dim3(1), dim3(256), 0, st, L, ldL, k, kb, ib, ctl);
+      hipLaunchKernelGGL(lg_potrf_kernel<kPotrfPB>, dim3(1), dim3(256), 0, strm, L, ldL, k, kb, ib, ctl);
       const int rest = n - k - NB;
       if (rest > 0)
-        hipLaunchKernelGGL(lg_trsm_kernel, dim3((rest + 63) / 64), dim3(256), 0, st, L, ldL, n, k, ib, ctl);
+        hipLaunchKernelGGL(lg_trsm_kernel, dim3((rest + 63) / 64), dim3(256), 0, strm, L, ldL, n, k, ib, ctl);
     };
+    // Triangular solves by super-blocks of SB diagonal blocks (lg_sinv_kernel
+    // forms the inverses).  L z = r for super-block S (r is consumed): its
+    // share of z as one product with the inverse, then its update of the
+    // right-hand side below it.
+    const int nsb = (nblk + SB - 1) / SB;
+    auto fwd_step = [&](int S, hipStream_t strm) {
+      const int o0 = SBN * S, nb = nblk - SB * S < SB ? nblk - SB * S : SB, width = NB * nb;
+      const float* Xs = sinv + (long long)S * SBN * SBN;
+      hipLaunchKernelGGL(lg_rowdot_kernel<1>, dim3((width + 3) / 4), dim3(256), 0, strm, Xs, (long long)SBN, width,
+                         width, 1, r + o0, z + o0, 0, ctl);
+      const int below = n - o0 - width;
+      if (below > 0)
+        hipLaunchKernelGGL(lg_rowdot_kernel<4>, dim3((below + 15) / 16), dim3(256), 0, strm,
+                           L + (long long)(o0 + width) * ldL + o0, ldL, below, width, 0, z + o0, r + o0 + width, 1,
+                           ctl);
+    };
+    // Block bb of the factor is final (factored, and its column below
+    // solved): on the sol stream, row bb % SB of its super-block's inverse,
+    // and the first solve's forward step of the super-block once its last
+    // row is in.  So the inverses and the first forward solve run beside the
+    // factorisation, and only the last block's row and forward step follow
+    // it.  While the bulk updates run on bf16 MFMA the GPU is full and work
+    // beside them only slows them down; from the first pair whose bulk does
+    // not (the last pairs leave most CUs idle), the blocks factored so far
+    // are queued at once, then each block as soon as it is final.
+    auto after_block = [&](int bb) {
+      const int S = bb / SB, ii = bb % SB;
+      hipLaunchKernelGGL(lg_sinv_kernel, dim3((ii + 1) * SV_CQ), dim3(256), 0, sol, L, ldL, n, nblk, inv, sinv, sinvt,
+                         S, ii, ctl);
+      if (ii == SB - 1 || bb == nblk - 1) fwd_step(S, sol);
+    };
+    const int slots6 = cus - cus / 8;
+    int queued = 0;      // blocks whose inverse rows are queued on sol
+    bool late = false;   // the bulk updates have left bf16 MFMA
     if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;   // after the set-up kernels
     for (int b = 0; b < nblk; b += 2) {
       const int k = NB * b;
       if (hipStreamWaitEvent(aux, ev_col, 0) != hipSuccess) return DR_ERR_HIP;
       factor_panel(b, aux);
+      if (late) {
+        if (hipEventRecord(ev_blk, aux) != hipSuccess || hipStreamWaitEvent(sol, ev_blk, 0) != hipSuccess)
+          return DR_ERR_HIP;
+        after_block(b);
+        queued = b + 1;
+      }
       const bool pair = b + 1 < nblk;
       if (pair) {
         const int T1 = (n - k - NB + NB - 1) / NB;
@@ -1320,6 +1416,20 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       if (hipEventRecord(ev_next, aux) != hipSuccess || hipStreamWaitEvent(hs, ev_next, 0) != hipSuccess)
         return DR_ERR_HIP;
       const int rest = n - k - 2 * NB;
+      // the bulk on bf16 MFMA (split planes) while it has enough 256 x 256
+      // tiles for the 7/8 of the CUs it runs on (one workgroup each)
+      const int T2 = rest > 0 ? (rest + S6_T - 1) / S6_T : 0;
+      const int n6 = T2 * (T2 - 1) / 2;
+      const bool bulk6 = pair && rest > 0 && n6 >= kS6MinRounds * slots6;
+      late = late || !bulk6;
+      if (late) {
+        const int done_to = pair ? b + 2 : b + 1;
+        if (queued < done_to) {
+          if (hipStreamWaitEvent(sol, ev_next, 0) != hipSuccess) return DR_ERR_HIP;
+          for (int bb = queued; bb < done_to; ++bb) after_block(bb);
+          queued = done_to;
+        }
+      }
       if (!pair || rest <= 0) break;
       const int T = (rest + NB - 1) / NB;
       const int h = T < 2 ? T : 2;
@@ -1327,12 +1437,7 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       const int nrest = (T - h) * (T - h + 1) / 2;
       hipLaunchKernelGGL(lg_syrk_kernel<2 * NB>, dim3(nhead), dim3(256), 0, hs, L, ldL, n, k, h, 1, nhead, ctl);
       if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;
-      // the bulk on bf16 MFMA (split planes) while it has enough 256 x 256
-      // tiles for the 7/8 of the CUs it runs on (one workgroup each)
-      const int T2 = (rest + S6_T - 1) / S6_T;
-      const int n6 = T2 * (T2 - 1) / 2;
-      const int slots6 = cus - cus / 8;
-      if (n6 >= kS6MinRounds * slots6) {
+      if (bulk6) {
         const int k1 = k + 2 * NB;
         hipLaunchKernelGGL(lg_split_kernel, dim3((rest * 32 + 255) / 256), dim3(256), 0, hs, L, ldL, n, k, k1, pl, ctl);
         hipLaunchKernelGGL(lg_syrk6_kernel, dim3(n6 < slots6 ? n6 : slots6), dim3(512), 0, hs,
@@ -1353,24 +1458,15 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       else
         hipLaunchKernelGGL(lg_resid_kernel, dim3((n + 3) / 4), dim3(256), 0, hs, Kp, n, sp, x, r, kx, ctl);
     };
-    const int nsb = (nblk + SB - 1) / SB;
-    for (int d = 0; d < SB; ++d)
-      hipLaunchKernelGGL(lg_sinv_kernel, dim3(SB - d, nsb), dim3(256), 0, hs, L, ldL, n, nblk, inv, sinv, sinvt, d,
-                         ctl);
+    // the inverses and the first forward solve are in
+    if (hipEventRecord(ev_sol, sol) != hipSuccess || hipStreamWaitEvent(hs, ev_sol, 0) != hipSuccess)
+      return DR_ERR_HIP;
     for (int it = 0; it <= kRefine; ++it) {
-      if (it > 0)
+      // L z = r (r is consumed; the first solve's was done beside the
+      // factorisation), then L^T dx = z (z is consumed), by super-blocks
+      if (it > 0) {
         resid(nullptr);
-      // L z = r (r is consumed), then L^T dx = z (z is consumed), by super-blocks
-      for (int S = 0; S < nsb; ++S) {
-        const int o0 = SBN * S, nb = nblk - SB * S < SB ? nblk - SB * S : SB, width = NB * nb;
-        const float* Xs = sinv + (long long)S * SBN * SBN;
-        hipLaunchKernelGGL(lg_rowdot_kernel<1>, dim3((width + 3) / 4), dim3(256), 0, hs, Xs, (long long)SBN, width,
-                           width, 1, r + o0, z + o0, 0, ctl);
-        const int below = n - o0 - width;
-        if (below > 0)
-          hipLaunchKernelGGL(lg_rowdot_kernel<4>, dim3((below + 15) / 16), dim3(256), 0, hs,
-                             L + (long long)(o0 + width) * ldL + o0, ldL, below, width, 0, z + o0, r + o0 + width, 1,
-                             ctl);
+        for (int S = 0; S < nsb; ++S) fwd_step(S, hs);
       }
       for (int S = nsb - 1; S >= 0; --S) {
         const int o0 = SBN * S, nb = nblk - SB * S < SB ? nblk - SB * S : SB, width = NB * nb;
@@ -1387,8 +1483,8 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
     resid(z);
     hipLaunchKernelGGL(lg_final_kernel, dim3(1), dim3(1024), 0, hs, sp, t2 + p, n, x, z, ctl, w + (long long)p * n,
                        resid2 + p, info + p);
-    const dr_status st = launch_status();
-    if (st != DR_OK) return st;
+    const dr_status rc = launch_status();
+    if (rc != DR_OK) return rc;
   }
   return DR_OK;
 }
