@@ -51,6 +51,7 @@
 // launches of that group return at once.
 
 #include <mutex>
+#include <type_traits>
 
 #include "common.h"
 
@@ -532,20 +533,26 @@ __global__ __launch_bounds__(256) void lg_trsm_kernel(float* L, long long ldL, i
 // same set for both operands).  On a diagonal tile the strictly upper
 // sub-tile is skipped and only entries on or below the diagonal are written.
 constexpr int SY_CH = 32;                 // panel columns per chunk
-constexpr int SY_PANEL = NB * SY_CH * 4;  // bytes of one tile row's chunk (16 KiB)
 
 // W: panel width (the update has rank W: 128 for one panel, 256 for two).
-// head = true: the tiles of the first h (1 or 2) tile columns, column by
-// column (they hold the next panels); head = false: every tile with
-// I >= J >= h.
+// TS: tile edge, 128 (waves of 64 x 64) or 64 (waves of 32 x 32: a quarter
+// of the products per workgroup, for launches with fewer 128-tiles than
+// CUs, where the products of one tile are the latency).
+// head = true: the tiles of the first h panels' columns (h NB / TS tile
+// columns, column by column: they hold the next panels); head = false:
+// every tile with I >= J >= h NB / TS.
 // A workgroup takes tiles blockIdx.x, blockIdx.x + gridDim.x, ... < ntiles:
 // a grid smaller than the chip leaves CUs free for the factorisation chain
 // running on the other stream.
-template <int W>
+template <int W, int TS>
 __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL, int n, int k, int h, int head,
                                                          int ntiles, const LgCtl* ctl) {
+  static_assert(TS == 128 || TS == 64, "tile edge");
+  constexpr int PANEL = TS * SY_CH * 4;   // bytes of one tile row's chunk
+  constexpr int RB = TS / 32;             // 16-row blocks per wave
+  constexpr int HB = TS / 32;             // DMA half blocks (8 rows) per wave and panel
   if (ctl->skip) return;
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * 2 * SY_PANEL];
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * 2 * PANEL];
   constexpr int NCH = W / SY_CH;
   static_assert(NCH % 2 == 0, "the next tile's first chunk goes to stage 0");
   const int k1 = k + W;
@@ -557,44 +564,49 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
   struct Tile {
     int ri, rj;
     bool diag;
-    unsigned offi[4], offj[4];
+    unsigned offi[HB], offj[HB];
   };
-  int segs[4];
+  int segs[HB];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) segs[u] = swz_seg_of_lane(lane, (w + 4 * u) & 1);
+  for (int u = 0; u < HB; ++u) segs[u] = swz_seg_of_lane(lane, (w + 4 * u) & 1);
+  const int hc = h * (NB / TS);   // tile columns of the head
   auto tile_of = [&](int qt) {
     int I, J;
     if (head) {
-      const int T = (n - k1 + NB - 1) / NB;
-      I = qt < T ? qt : qt - T + 1;
-      J = qt < T ? 0 : 1;
+      const int T = (n - k1 + TS - 1) / TS;
+      J = 0;
+      while (qt >= T - J) {
+        qt -= T - J;
+        ++J;
+      }
+      I = J + qt;
     } else {
       tile_pair(qt, I, J);
-      I += h;
-      J += h;
+      I += hc;
+      J += hc;
     }
     Tile t;
-    t.ri = k1 + NB * I;
-    t.rj = k1 + NB * J;
+    t.ri = k1 + TS * I;
+    t.rj = k1 + TS * J;
     t.diag = I == J;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < HB; ++u) {
       const int r = 8 * (w + 4 * u) + (lane >> 3);
       t.offi[u] = t.ri + r < n ? (unsigned)((long long)r * ldL * 4) : kOobOffset;
       t.offj[u] = t.rj + r < n ? (unsigned)((long long)r * ldL * 4) : kOobOffset;
     }
     return t;
   };
-  // DMA of one chunk: wave w fills half blocks w, w + 4, w + 8, w + 12 of each panel
+  // DMA of one chunk: wave w fills half blocks w, w + 4, ... of each panel
   auto issue = [&](const Tile& t, int ch, int st) {
     const __amdgpu_buffer_rsrc_t rsi = make_rsrc(L + (long long)t.ri * ldL, kOobOffset);
     const __amdgpu_buffer_rsrc_t rsj = make_rsrc(L + (long long)t.rj * ldL, kOobOffset);
-    unsigned char* sb = lds + st * 2 * SY_PANEL;
+    unsigned char* sb = lds + st * 2 * PANEL;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < HB; ++u) {
       const unsigned cofs = (unsigned)((k + SY_CH * ch + 4 * segs[u]) * 4);
       dma16<kAuxCached>(rsi, sb + (w + 4 * u) * 1024, t.offi[u] == kOobOffset ? kOobOffset : t.offi[u] + cofs);
-      dma16<kAuxCached>(rsj, sb + SY_PANEL + (w + 4 * u) * 1024,
+      dma16<kAuxCached>(rsj, sb + PANEL + (w + 4 * u) * 1024,
                         t.offj[u] == kOobOffset ? kOobOffset : t.offj[u] + cofs);
     }
   };
@@ -608,12 +620,12 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
     const bool active = !(cur.diag && wc > wr);
     // this lane's C entries (rows 4 lg + q of each 16-row block, column lr),
     // loaded under the first chunk's products
-    f32x4 c[4][4];
-    f32x4 acc[4][4];
+    f32x4 c[RB][RB];
+    f32x4 acc[RB][RB];
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
+    for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int cb = 0; cb < RB; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch) {
       DR_WAIT_VM(0);
@@ -626,31 +638,31 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
         issue(nxt, 0, 0);
       if (ch == 0 && active) {
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb)
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-          for (int cb = 0; cb < 4; ++cb)
+          for (int cb = 0; cb < RB; ++cb)
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-              const int row = cur.ri + 64 * wr + 16 * rb + 4 * lg + q;
-              const int col = cur.rj + 64 * wc + 16 * cb + lr;
+              const int row = cur.ri + (TS / 2) * wr + 16 * rb + 4 * lg + q;
+              const int col = cur.rj + (TS / 2) * wc + 16 * cb + lr;
               c[rb][cb][q] = (row < n && col < n) ? L[(long long)row * ldL + col] : 0.f;
             }
       }
       if (active) {
-        const unsigned char* sa = lds + (ch & 1) * 2 * SY_PANEL;
-        const unsigned char* sbp = sa + SY_PANEL;
+        const unsigned char* sa = lds + (ch & 1) * 2 * PANEL;
+        const unsigned char* sbp = sa + PANEL;
 #pragma unroll
         for (int sub = 0; sub < 2; ++sub) {
           const int seg = 4 * sub + lg;
-          f32x4 fa[4], fb[4];
+          f32x4 fa[RB], fb[RB];
 #pragma unroll
-          for (int rb = 0; rb < 4; ++rb) fa[rb] = __builtin_bit_cast(f32x4, swz_read(sa + (4 * wr + rb) * 2048, lr, seg));
+          for (int rb = 0; rb < RB; ++rb) fa[rb] = __builtin_bit_cast(f32x4, swz_read(sa + (RB * wr + rb) * 2048, lr, seg));
 #pragma unroll
-          for (int cb = 0; cb < 4; ++cb) fb[cb] = __builtin_bit_cast(f32x4, swz_read(sbp + (4 * wc + cb) * 2048, lr, seg));
+          for (int cb = 0; cb < RB; ++cb) fb[cb] = __builtin_bit_cast(f32x4, swz_read(sbp + (RB * wc + cb) * 2048, lr, seg));
 #pragma unroll
-          for (int rb = 0; rb < 4; ++rb)
+          for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-            for (int cb = 0; cb < 4; ++cb)
+            for (int cb = 0; cb < RB; ++cb)
 #pragma unroll
               for (int t = 0; t < 4; ++t) acc[rb][cb] = mma_f32(fa[rb][t], fb[cb][t], acc[rb][cb]);
         }
@@ -658,13 +670,13 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
     }
     if (active) {
 #pragma unroll
-      for (int rb = 0; rb < 4; ++rb)
+      for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int cb = 0; cb < 4; ++cb)
+        for (int cb = 0; cb < RB; ++cb)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int row = cur.ri + 64 * wr + 16 * rb + 4 * lg + q;
-            const int col = cur.rj + 64 * wc + 16 * cb + lr;
+            const int row = cur.ri + (TS / 2) * wr + 16 * rb + 4 * lg + q;
+            const int col = cur.rj + (TS / 2) * wc + 16 * cb + lr;
             if (row < n && col < n && (!cur.diag || col <= row))
               L[(long long)row * ldL + col] = c[rb][cb][q] - acc[rb][cb][q];
           }
@@ -1353,6 +1365,22 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
     // the previous pair's update of the columns right of b+1; then the main
     // stream updates the next pair's two columns (head) and, while the aux
     // stream factors that pair, the rest.
+    // the head update of rank W (the first h panels' columns right of
+    // k + W), on 64-tiles when 128-tiles would not give every CU one
+    auto head_update = [&](auto wtag, int k, int h, hipStream_t strm) {
+      constexpr int W = decltype(wtag)::value;
+      const int rows = n - k - W;
+      const int T = (rows + NB - 1) / NB;
+      const int n128 = h * T - h * (h - 1) / 2;
+      if (n128 >= cus) {
+        hipLaunchKernelGGL((lg_syrk_kernel<W, 128>), dim3(n128), dim3(256), 0, strm, L, ldL, n, k, h, 1, n128, ctl);
+      } else {
+        const int T64 = (rows + 63) / 64;
+        int n64 = 0;
+        for (int J = 0; J < 2 * h; ++J) n64 += T64 - J > 0 ? T64 - J : 0;
+        hipLaunchKernelGGL((lg_syrk_kernel<W, 64>), dim3(n64), dim3(256), 0, strm, L, ldL, n, k, h, 1, n64, ctl);
+      }
+    };
     auto factor_panel = [&](int b, hipStream_t strm) {
       const int k = NB * b;
       const int kb = n - k < NB ? n - k : NB;
@@ -1409,8 +1437,7 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       }
       const bool pair = b + 1 < nblk;
       if (pair) {
-        const int T1 = (n - k - NB + NB - 1) / NB;
-        hipLaunchKernelGGL(lg_syrk_kernel<NB>, dim3(T1), dim3(256), 0, aux, L, ldL, n, k, 1, 1, T1, ctl);
+        head_update(std::integral_constant<int, NB>{}, k, 1, aux);
         factor_panel(b + 1, aux);
       }
       if (hipEventRecord(ev_next, aux) != hipSuccess || hipStreamWaitEvent(hs, ev_next, 0) != hipSuccess)
@@ -1433,9 +1460,8 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       if (!pair || rest <= 0) break;
       const int T = (rest + NB - 1) / NB;
       const int h = T < 2 ? T : 2;
-      const int nhead = h * T - h * (h - 1) / 2;
       const int nrest = (T - h) * (T - h + 1) / 2;
-      hipLaunchKernelGGL(lg_syrk_kernel<2 * NB>, dim3(nhead), dim3(256), 0, hs, L, ldL, n, k, h, 1, nhead, ctl);
+      head_update(std::integral_constant<int, 2 * NB>{}, k, h, hs);
       if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;
       if (bulk6) {
         const int k1 = k + 2 * NB;
@@ -1447,7 +1473,7 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
         // under two rounds: the chain is the longer path, 3/4 of them
         const int slots = nrest >= 8 * cus ? 2 * cus - cus / 8 : (nrest < 4 * cus ? 2 * cus - cus / 2 : rest_slots);
         const int grid = nrest < slots ? nrest : slots;
-        hipLaunchKernelGGL(lg_syrk_kernel<2 * NB>, dim3(grid), dim3(256), 0, hs, L, ldL, n, k, h, 0, nrest, ctl);
+        hipLaunchKernelGGL((lg_syrk_kernel<2 * NB, 128>), dim3(grid), dim3(256), 0, hs, L, ldL, n, k, h, 0, nrest, ctl);
       }
     }
     // r = s - (K + lam I) x, and K x into kx when kx != nullptr
