@@ -89,7 +89,7 @@ LgLayout lg_layout(long long n) {
   l.off_inv = o;  o = align_up(o + (size_t)l.nblk * NB * NB * 4, 256);
   l.off_sinv = o; o = align_up(o + (size_t)((l.nblk + SB - 1) / SB) * SBN * SBN * 4, 256);
   l.off_sinvt = o; o = align_up(o + (size_t)((l.nblk + SB - 1) / SB) * SBN * SBN * 4, 256);
-  l.off_pl = o;   o = align_up(o + (size_t)3 * n * 2 * NB * 2, 256);   // three bf16 planes of a panel pair
+  l.off_pl = o;   o = align_up(o + (size_t)3 * n * 4 * NB * 2, 256);   // three bf16 planes of four panels
   l.off_x = o;    o = align_up(o + (size_t)l.npad * 8, 256);
   l.off_dx = o;   o = align_up(o + (size_t)l.npad * 8, 256);
   l.off_r = o;    o = align_up(o + (size_t)l.npad * 8, 256);
@@ -722,7 +722,6 @@ constexpr int S6_PANEL = S6_T * S6_K * 2;      // bytes of one operand panel per
 constexpr int S6_STAGE = 2 * S6_PANEL;
 constexpr int S6_LDC = S6_T + 4;               // row stride (floats) of the half tile staged in LDS
 constexpr int S6_LDS = 2 * S6_STAGE > 128 * S6_LDC * 4 ? 2 * S6_STAGE : 128 * S6_LDC * 4;
-constexpr int S6_STEPS = 6 * (2 * NB) / S6_K;   // 24
 #ifndef DR_S6_MIN_ROUNDS
 #define DR_S6_MIN_ROUNDS 1
 #endif
@@ -733,13 +732,14 @@ __device__ __forceinline__ unsigned bf16_rne_bits(float x) {
   return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
 
-// rows k1 .. n-1, columns k .. k+255 of L -> planes [3][n][256] bf16 (row r of
+// rows k1 .. n-1, columns k .. k+W-1 of L -> planes [3][n][W] bf16 (row r of
 // a plane is row k1 + r); one thread per 8 columns of a row
+template <int W>
 __global__ __launch_bounds__(256) void lg_split_kernel(const float* L, long long ldL, int n, int k, int k1,
                                                        unsigned short* pl, const LgCtl* ctl) {
   if (ctl->skip) return;
   const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
-  const int r = (int)(t >> 5), c = (int)(t & 31) * 8;
+  const int r = (int)(t / (W / 8)), c = (int)(t % (W / 8)) * 8;
   if (k1 + r >= n) return;
   const float* src = L + (long long)(k1 + r) * ldL + k + c;
   const float4 v0 = *reinterpret_cast<const float4*>(src);
@@ -762,15 +762,21 @@ __global__ __launch_bounds__(256) void lg_split_kernel(const float* L, long long
     p1[q] = m[0] | (m[1] << 16);
     p2[q] = l[0] | (l[1] << 16);
   }
-  const long long plane = (long long)n * 2 * NB;
-  unsigned short* d = pl + (long long)r * 2 * NB + c;
+  const long long plane = (long long)n * W;
+  unsigned short* d = pl + (long long)r * W + c;
   *reinterpret_cast<u32x4*>(d) = u32x4{p0[0], p0[1], p0[2], p0[3]};
   *reinterpret_cast<u32x4*>(d + plane) = u32x4{p1[0], p1[1], p1[2], p1[3]};
   *reinterpret_cast<u32x4*>(d + 2 * plane) = u32x4{p2[0], p2[1], p2[2], p2[3]};
 }
 
+// W: the width of the panels (the rank of the update): 256 (a pair) or 512
+// (four panels); skip: the tile columns left to the head update (the next
+// step's panels)
+template <int W>
 __global__ __launch_bounds__(512) void lg_syrk6_kernel(const unsigned char* pl, float* L, long long ldL, int n, int k1,
-                                                       int ntiles, const LgCtl* ctl) {
+                                                       int skip, int ntiles, const LgCtl* ctl) {
+  constexpr int SPP = W / S6_K;         // steps per plane pair
+  constexpr int S6_STEPS = 6 * SPP;     // 24 or 48
   if (ctl->skip) return;
   __shared__ __attribute__((aligned(1024))) unsigned char lds[S6_LDS];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -778,28 +784,28 @@ __global__ __launch_bounds__(512) void lg_syrk6_kernel(const unsigned char* pl, 
   const int wr = w >> 2, wc = w & 3;   // 128-row half, 64-column quarter of the tile
   const int lr = lane & 15, lg = lane >> 4;
   const int rows = n - k1;             // rows of the planes
-  const long long planeB = (long long)n * 2 * NB * 2;
+  const long long planeB = (long long)n * W * 2;
   int segs[4];
 #pragma unroll
   for (int u = 0; u < 4; ++u) segs[u] = swz_seg_of_lane(lane, (w + 8 * u) & 1);
   for (int qt = blockIdx.x; qt < ntiles; qt += gridDim.x) {
     int I, J;
     tile_pair(qt, I, J);
-    const int rowA0 = S6_T * (I + 1), rowB0 = S6_T * (J + 1);   // plane rows (trailing rows from k1)
+    const int rowA0 = S6_T * (I + skip), rowB0 = S6_T * (J + skip);   // plane rows (trailing rows from k1)
     const bool diag = I == J;
     unsigned offA[4], offB[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int r = 8 * (w + 8 * u) + (lane >> 3);
-      offA[u] = rowA0 + r < rows ? (unsigned)(r * 2 * NB * 2) : kOobOffset;
-      offB[u] = rowB0 + r < rows ? (unsigned)(r * 2 * NB * 2) : kOobOffset;
+      offA[u] = rowA0 + r < rows ? (unsigned)(r * W * 2) : kOobOffset;
+      offB[u] = rowB0 + r < rows ? (unsigned)(r * W * 2) : kOobOffset;
     }
     auto issue = [&](int s, int st) {
-      const int t = s >> 2, c0 = S6_K * (s & 3);
+      const int t = s / SPP, c0 = S6_K * (s % SPP);
       const int pa = t == 2 || t == 4 ? 1 : (t == 5 ? 2 : 0);   // plane pairs 00 01 10 02 11 20
       const int pb = t == 1 || t == 4 ? 1 : (t == 3 ? 2 : 0);
-      const __amdgpu_buffer_rsrc_t ra = make_rsrc(pl + pa * planeB + (long long)rowA0 * 2 * NB * 2, kOobOffset);
-      const __amdgpu_buffer_rsrc_t rb = make_rsrc(pl + pb * planeB + (long long)rowB0 * 2 * NB * 2, kOobOffset);
+      const __amdgpu_buffer_rsrc_t ra = make_rsrc(pl + pa * planeB + (long long)rowA0 * W * 2, kOobOffset);
+      const __amdgpu_buffer_rsrc_t rb = make_rsrc(pl + pb * planeB + (long long)rowB0 * W * 2, kOobOffset);
       unsigned char* sb = lds + st * S6_STAGE;
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -1357,17 +1363,19 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
     hipLaunchKernelGGL(lg_setup_kernel, dim3(1), dim3(1024), 0, hs, Kp, sp, n, lambda, mode, ctl, lam_eff + p);
     hipLaunchKernelGGL(lg_load_kernel, dim3(n, (n + kLoadCols - 1) / kLoadCols), dim3(256), 0, hs, Kp, n, vec, L, ldL,
                        ctl, lam_eff + p);
-    // Right-looking blocked factorisation by pairs of panels, with
-    // look-ahead.  The trailing matrix takes one rank-256 update per pair
-    // (half the passes over it of rank-128 updates).  For the pair (b, b+1)
-    // the aux stream factors panel b, applies it to panel b+1's column
-    // (rank 128), and factors panel b+1, while the main stream still runs
-    // the previous pair's update of the columns right of b+1; then the main
-    // stream updates the next pair's two columns (head) and, while the aux
-    // stream factors that pair, the rest.
+    // Right-looking blocked factorisation by steps of four or two panels,
+    // with look-ahead.  The trailing matrix takes one rank-512 update per
+    // step of four panels while that update fills the CUs on bf16 MFMA
+    // (a quarter of the passes over it of rank-128 updates), then one
+    // rank-256 update per pair.  For the step of panels b .. b + m - 1 the
+    // aux stream factors panel b, applies it to the step's other panel
+    // columns (rank 128), factors panel b + 1, and so on, while the main
+    // stream still runs the previous step's update of the columns right of
+    // it; then the main stream updates the next step's panel columns (head)
+    // and, while the aux stream factors that step, the rest (bulk).
     // the head update of rank W (the first h panels' columns right of
     // k + W), on 64-tiles when 128-tiles would not give every CU one
-    auto head_update = [&](auto wtag, int k, int h, hipStream_t strm) {
+    auto head_update_w = [&](auto wtag, int k, int h, hipStream_t strm) {
       constexpr int W = decltype(wtag)::value;
       const int rows = n - k - W;
       const int T = (rows + NB - 1) / NB;
@@ -1380,6 +1388,14 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
         for (int J = 0; J < 2 * h; ++J) n64 += T64 - J > 0 ? T64 - J : 0;
         hipLaunchKernelGGL((lg_syrk_kernel<W, 64>), dim3(n64), dim3(256), 0, strm, L, ldL, n, k, h, 1, n64, ctl);
       }
+    };
+    auto head_update = [&](int W, int k, int h, hipStream_t strm) {
+      if (W == NB)
+        head_update_w(std::integral_constant<int, NB>{}, k, h, strm);
+      else if (W == 2 * NB)
+        head_update_w(std::integral_constant<int, 2 * NB>{}, k, h, strm);
+      else
+        head_update_w(std::integral_constant<int, 4 * NB>{}, k, h, strm);
     };
     auto factor_panel = [&](int b, hipStream_t strm) {
       const int k = NB * b;
@@ -1422,59 +1438,87 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       if (ii == SB - 1 || bb == nblk - 1) fwd_step(S, sol);
     };
     const int slots6 = cus - cus / 8;
+    // panels in the step starting at block b: four while the rank-512 bulk
+    // after them has a round of 256 x 256 tiles for the CUs it runs on
+    auto width_at = [&](int b) -> int {
+      if (b >= nblk) return 0;
+      const int restq = n - NB * b - 4 * NB;
+      if (b + 4 <= nblk && restq > 0) {
+        const int T2 = (restq + S6_T - 1) / S6_T;
+        if (T2 > 2 && (T2 - 2) * (T2 - 1) / 2 >= kS6MinRounds * slots6) return 4;
+      }
+      return b + 1 < nblk ? 2 : 1;
+    };
     int queued = 0;      // blocks whose inverse rows are queued on sol
     bool late = false;   // the bulk updates have left bf16 MFMA
     if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;   // after the set-up kernels
-    for (int b = 0; b < nblk; b += 2) {
-      const int k = NB * b;
+    int b = 0, m = width_at(0);
+    while (b < nblk) {
+      const int k = NB * b, W = NB * m;
       if (hipStreamWaitEvent(aux, ev_col, 0) != hipSuccess) return DR_ERR_HIP;
-      factor_panel(b, aux);
-      if (late) {
-        if (hipEventRecord(ev_blk, aux) != hipSuccess || hipStreamWaitEvent(sol, ev_blk, 0) != hipSuccess)
-          return DR_ERR_HIP;
-        after_block(b);
-        queued = b + 1;
-      }
-      const bool pair = b + 1 < nblk;
-      if (pair) {
-        head_update(std::integral_constant<int, NB>{}, k, 1, aux);
-        factor_panel(b + 1, aux);
+      for (int i = 0; i < m; ++i) {
+        factor_panel(b + i, aux);
+        if (late) {
+          if (hipEventRecord(ev_blk, aux) != hipSuccess || hipStreamWaitEvent(sol, ev_blk, 0) != hipSuccess)
+            return DR_ERR_HIP;
+          after_block(b + i);
+          queued = b + i + 1;
+        }
+        if (i + 1 < m) head_update(NB, k + NB * i, m - 1 - i, aux);
       }
       if (hipEventRecord(ev_next, aux) != hipSuccess || hipStreamWaitEvent(hs, ev_next, 0) != hipSuccess)
         return DR_ERR_HIP;
-      const int rest = n - k - 2 * NB;
+      const int b2 = b + m, m2 = width_at(b2);
+      const int rest = n - k - W;
       // the bulk on bf16 MFMA (split planes) while it has enough 256 x 256
-      // tiles for the 7/8 of the CUs it runs on (one workgroup each)
+      // tiles for the 7/8 of the CUs it runs on (one workgroup each); the
+      // head takes the next step's m2 panel columns, skip tile columns
+      const int skip = NB * m2 / S6_T;
       const int T2 = rest > 0 ? (rest + S6_T - 1) / S6_T : 0;
-      const int n6 = T2 * (T2 - 1) / 2;
-      const bool bulk6 = pair && rest > 0 && n6 >= kS6MinRounds * slots6;
+      const int n6 = T2 > skip ? (T2 - skip) * (T2 - skip + 1) / 2 : 0;
+      const bool bulk6 = m >= 2 && m2 >= 2 && rest > 0 && n6 >= kS6MinRounds * slots6;
       late = late || !bulk6;
-      if (late) {
-        const int done_to = pair ? b + 2 : b + 1;
-        if (queued < done_to) {
-          if (hipStreamWaitEvent(sol, ev_next, 0) != hipSuccess) return DR_ERR_HIP;
-          for (int bb = queued; bb < done_to; ++bb) after_block(bb);
-          queued = done_to;
+      if (late && queued < b2) {
+        if (hipStreamWaitEvent(sol, ev_next, 0) != hipSuccess) return DR_ERR_HIP;
+        for (int bb = queued; bb < b2; ++bb) after_block(bb);
+        queued = b2;
+      }
+      if (m2 == 0 || rest <= 0) break;
+      head_update(W, k, m2, hs);
+      if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;
+      const int k1 = k + W;
+      if (bulk6) {
+        if (W == 4 * NB) {
+          hipLaunchKernelGGL(lg_split_kernel<4 * NB>, dim3((rest * 64 + 255) / 256), dim3(256), 0, hs, L, ldL, n, k, k1,
+                             pl, ctl);
+          hipLaunchKernelGGL(lg_syrk6_kernel<4 * NB>, dim3(n6 < slots6 ? n6 : slots6), dim3(512), 0, hs,
+                             reinterpret_cast<const unsigned char*>(pl), L, ldL, n, k1, skip, n6, ctl);
+        } else {
+          hipLaunchKernelGGL(lg_split_kernel<2 * NB>, dim3((rest * 32 + 255) / 256), dim3(256), 0, hs, L, ldL, n, k, k1,
+                             pl, ctl);
+          hipLaunchKernelGGL(lg_syrk6_kernel<2 * NB>, dim3(n6 < slots6 ? n6 : slots6), dim3(512), 0, hs,
+                             reinterpret_cast<const unsigned char*>(pl), L, ldL, n, k1, skip, n6, ctl);
+        }
+      } else {
+        const int T = (rest + NB - 1) / NB;
+        const int nrest = T > m2 ? (T - m2) * (T - m2 + 1) / 2 : 0;
+        if (nrest > 0) {
+          // many rounds of tiles: the chain has slack, 15/16 of the slots;
+          // under two rounds: the chain is the longer path, 3/4 of them
+          const int slots =
+              nrest >= 8 * cus ? 2 * cus - cus / 8 : (nrest < 4 * cus ? 2 * cus - cus / 2 : rest_slots);
+          const int grid = nrest < slots ? nrest : slots;
+          // (a step of one panel is the last: it has no bulk)
+          if (W == 4 * NB)
+            hipLaunchKernelGGL((lg_syrk_kernel<4 * NB, 128>), dim3(grid), dim3(256), 0, hs, L, ldL, n, k, m2, 0, nrest,
+                               ctl);
+          else
+            hipLaunchKernelGGL((lg_syrk_kernel<2 * NB, 128>), dim3(grid), dim3(256), 0, hs, L, ldL, n, k, m2, 0, nrest,
+                               ctl);
         }
       }
-      if (!pair || rest <= 0) break;
-      const int T = (rest + NB - 1) / NB;
-      const int h = T < 2 ? T : 2;
-      const int nrest = (T - h) * (T - h + 1) / 2;
-      head_update(std::integral_constant<int, 2 * NB>{}, k, h, hs);
-      if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;
-      if (bulk6) {
-        const int k1 = k + 2 * NB;
-        hipLaunchKernelGGL(lg_split_kernel, dim3((rest * 32 + 255) / 256), dim3(256), 0, hs, L, ldL, n, k, k1, pl, ctl);
-        hipLaunchKernelGGL(lg_syrk6_kernel, dim3(n6 < slots6 ? n6 : slots6), dim3(512), 0, hs,
-                           reinterpret_cast<const unsigned char*>(pl), L, ldL, n, k1, n6, ctl);
-      } else if (nrest > 0) {
-        // many rounds of tiles: the chain has slack, 15/16 of the slots;
-        // under two rounds: the chain is the longer path, 3/4 of them
-        const int slots = nrest >= 8 * cus ? 2 * cus - cus / 8 : (nrest < 4 * cus ? 2 * cus - cus / 2 : rest_slots);
-        const int grid = nrest < slots ? nrest : slots;
-        hipLaunchKernelGGL((lg_syrk_kernel<2 * NB, 128>), dim3(grid), dim3(256), 0, hs, L, ldL, n, k, h, 0, nrest, ctl);
-      }
+      b = b2;
+      m = m2;
     }
     // r = s - (K + lam I) x, and K x into kx when kx != nullptr
     const bool rows4 = n % 4 == 0 && aligned16(Kp);
