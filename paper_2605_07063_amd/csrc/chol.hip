@@ -21,31 +21,31 @@
 //   lg_potrf_kernel  one workgroup factors and inverts the diagonal block
 //                    in 16-column steps on packed 16x16 LDS tiles: one wave
 //                    factors and inverts each 16x16 diagonal tile in
-//                    registers (v_readlane broadcasts, no barrier per
-//                    pivot), one step ahead of the others; the panel solve,
-//                    the trailing update and the off-diagonal tiles of the
-//                    inverse are fp32 MFMA products.
+//                    registers (tile16_chol_inv), one step ahead of the
+//                    others; the panel solve, the trailing update and the
+//                    tiles of the inverse are fp32 MFMA products.
 //   lg_trsm_kernel   L21 = A21 L11^-T as an fp32 MFMA product with the
 //                    inverse, 64 rows per workgroup.
 // Both keep their LDS under 96 KiB, so either fits on a CU beside one
 // trailing-update workgroup while the update runs.
-//   lg_syrk_kernel   A22 -= L21 L21^T on 128x128 lower-triangle tiles, fp32
-//                    MFMA, the panel slices streamed through LDS in chunks.
-// Panels go in pairs: the trailing matrix takes one rank-256 update per
-// pair, as two launches, the next pair's two tile columns and then the
-// rest; between them a second stream (created for the call, default
-// priority, ordered by events) factors the next pair (diagonal block, panel
-// solve, the rank-128 update of the pair's second column, its diagonal
-// block and panel), so those latency-bound steps run under the bulk of the
-// trailing update.
-// Solve: the super-block inverses are built block by block from the
-// 128x128 ones (lg_sinv_kernel, one launch per distance from the
-// diagonal); then L y = r and L^T dx = y go super-block by super-block,
-// two wide launches each (the super-block's share of the solution as a
-// product with its inverse, then its update of the rest of the right-hand
-// side), x += dx; three solves (the first and kRefine refinement steps),
-// each refinement preceded by r = s - (K + lam_eff I) x in fp64 read
-// straight from K.
+// Trailing updates: steps of four panels (rank 512) while the bulk of the
+// update fills the CUs on bf16 MFMA, then pairs (rank 256).  Per step, two
+// launches on the caller's stream: the head (lg_syrk_kernel, fp32 MFMA on
+// 128x128 or 64x64 tiles: the next step's panel columns) and the bulk
+// (lg_split_kernel + lg_syrk6_kernel on bf16 planes, or lg_syrk_kernel);
+// meanwhile a second stream factors the next step's panels in turn (block
+// factor, panel solve, rank-128 update of the step's other panel columns),
+// so those latency-bound steps run under the bulk.
+// Solve: the inverses of the 1024x1024 diagonal super-blocks are built a
+// block row at a time from the 128x128 ones (lg_sinv_kernel) on a third
+// stream as the factorisation finalises each block, with the first
+// solve's forward sweep; then L y = r and L^T dx = y go super-block by
+// super-block, two wide launches each (the super-block's share of the
+// solution as a product with its inverse, then its update of the rest of
+// the right-hand side), x += dx; the first solve and up to kRefine
+// refinement steps, each preceded by r = s - (K + lam_eff I) x in fp64
+// read straight from K, until the corrections pass the convergence test.
+// The extra streams and their events are created once per device and kept.
 // Every kernel first reads ctl->skip: once a group's result is decided (a
 // non-finite input, an empty span, a non-positive pivot) the remaining
 // launches of that group return at once.
@@ -689,8 +689,8 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
 //
 // The bulk of the rank-256 trailing update, A22 -= L21 L21^T, with the fp32
 // products taken on bf16 MFMA (16 times the fp32 MFMA rate):
-//   lg_split_kernel  writes the panel pair's rows below it (L21, 256
-//                    columns) as three bf16 planes, x = x1 + x2 + x3 with
+//   lg_split_kernel  writes the step's panel rows below it (L21, W = 512 or
+//                    256 columns) as three bf16 planes, x = x1 + x2 + x3 with
 //                    x1 = bf16(x), x2 = bf16(x - x1), x3 = bf16(x - x1 - x2)
 //                    (round to nearest even; each difference is exact in
 //                    fp32), so x1 + x2 + x3 holds x to about 2^-24.
@@ -702,19 +702,20 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
 //                    element's error is about 3 * 2^-24 of |x||y|: fp32
 //                    products, at a sixth of the bf16 MFMA rate (2.6 times
 //                    the fp32 MFMA rate).  The six products are run as one
-//                    bf16 contraction over 6 x 256 = 1536 virtual columns,
-//                    64 per step: step s reads plane a of the tile's row
-//                    panel and plane b of its column panel, columns
-//                    64 (s mod 4) ..., for the pair s / 4.
+//                    bf16 contraction over 6 W virtual columns, 64 per
+//                    step: step s reads plane a of the tile's row panel and
+//                    plane b of its column panel, columns 64 (s mod W/64)
+//                    ..., for the pair s / (W/64).
 // The tile machinery is that of the large-n Gram kernel: 256 x 256 tiles
-// of the trailing matrix right of the pair's two head tile columns (tiles
-// I >= J >= 1 in units of 256 from the trailing matrix's first row), eight
+// of the trailing matrix right of the head's tile columns (tiles
+// I >= J >= skip in units of 256 from the trailing matrix's first row), eight
 // waves of 128 x 64 fp32 accumulators, a two-stage buffer -> LDS DMA ring
 // of 64-column steps in the conflict-free operand layout.  At the end the
 // tile goes through LDS in two 128-row halves (row-major, 260-float rows:
 // the accumulator writes of a wave fall on distinct banks) and each thread
-// updates 16 float4 of C: read, subtract, write (on a diagonal tile only
-// entries on or below the diagonal).
+// updates 16 float4 of C: read (requested before the half is staged),
+// subtract, write (on a diagonal tile only entries on or below the
+// diagonal).
 
 constexpr int S6_T = 256;                      // tile edge
 constexpr int S6_K = 64;                       // virtual columns per step
