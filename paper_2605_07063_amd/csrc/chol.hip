@@ -1268,18 +1268,18 @@ size_t span_large_workspace(int64_t n) { return lg_layout(n).total; }
 // solve while the factorisation is still running
 struct LgStreams {
   hipStream_t aux = nullptr, sol = nullptr;
-  hipEvent_t ev_col = nullptr, ev_next = nullptr, ev_blk = nullptr, ev_sol = nullptr;
+  hipEvent_t ev_col = nullptr, ev_next = nullptr, ev_blk = nullptr, ev_bulk = nullptr, ev_sol = nullptr;
 };
 static dr_status span_large_groups(const float* K, const float* s, const float* t2, int n, int P, float lambda,
                                    int mode, float* w, float* lam_eff, float* resid2, int32_t* info,
                                    const LgLayout& lay, unsigned char* base, hipStream_t hs, const LgStreams& st);
 
-// The look-ahead stream (default priority) and its two events: one set per
-// device, created by the first blocked solve on that device and kept until
-// the process ends, so a call creates and destroys nothing.  A call holds
-// its device's lock while it enqueues, so that the records of ev_col /
-// ev_next and the waits on them pair up when several host threads call at
-// once (their work then shares the look-ahead stream in call order).
+// The solver's two extra streams (default priority) and their events: one
+// set per device, created by the first blocked solve on that device and
+// kept until the process ends, so a call creates and destroys nothing.  A
+// call holds its device's lock while it enqueues, so that the records of
+// the events and the waits on them pair up when several host threads call
+// at once (their work then shares the extra streams in call order).
 namespace {
 constexpr int kMaxDevices = 64;
 struct AuxSet {
@@ -1293,6 +1293,7 @@ void destroy_streams(LgStreams& st) {
   if (st.ev_col) (void)hipEventDestroy(st.ev_col);
   if (st.ev_next) (void)hipEventDestroy(st.ev_next);
   if (st.ev_blk) (void)hipEventDestroy(st.ev_blk);
+  if (st.ev_bulk) (void)hipEventDestroy(st.ev_bulk);
   if (st.ev_sol) (void)hipEventDestroy(st.ev_sol);
   if (st.aux) (void)hipStreamDestroy(st.aux);
   if (st.sol) (void)hipStreamDestroy(st.sol);
@@ -1319,6 +1320,7 @@ dr_status span_large(const float* K, const float* s, const float* t2, int64_t n6
         hipEventCreateWithFlags(&st.ev_col, hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&st.ev_next, hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&st.ev_blk, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&st.ev_bulk, hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&st.ev_sol, hipEventDisableTiming) != hipSuccess) {
       destroy_streams(st);
       return DR_ERR_HIP;
@@ -1332,7 +1334,7 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
                                    int mode, float* w, float* lam_eff, float* resid2, int32_t* info,
                                    const LgLayout& lay, unsigned char* base, hipStream_t hs, const LgStreams& st) {
   hipStream_t aux = st.aux, sol = st.sol;
-  hipEvent_t ev_col = st.ev_col, ev_next = st.ev_next, ev_blk = st.ev_blk, ev_sol = st.ev_sol;
+  hipEvent_t ev_col = st.ev_col, ev_next = st.ev_next, ev_blk = st.ev_blk, ev_bulk = st.ev_bulk, ev_sol = st.ev_sol;
   // the bulk trailing update runs persistent on 7/8 of the two-per-CU
   // workgroup slots: one CU in four keeps room (LDS and waves) for one more
   // workgroup, where the diagonal-block chain of the next pair (factor,
@@ -1370,10 +1372,11 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
     // (a quarter of the passes over it of rank-128 updates), then one
     // rank-256 update per pair.  For the step of panels b .. b + m - 1 the
     // aux stream factors panel b, applies it to the step's other panel
-    // columns (rank 128), factors panel b + 1, and so on, while the main
-    // stream still runs the previous step's update of the columns right of
-    // it; then the main stream updates the next step's panel columns (head)
-    // and, while the aux stream factors that step, the rest (bulk).
+    // columns (rank 128), factors panel b + 1, and so on, then updates the
+    // next step's panel columns with the step's panels (head) and goes on
+    // to factor them; the main stream meanwhile updates the rest (bulk).
+    // The head and the bulk touch disjoint tiles and run side by side; the
+    // head follows the previous step's bulk, whose columns include its own.
     // the head update of rank W (the first h panels' columns right of
     // k + W), on 64-tiles when 128-tiles would not give every CU one
     auto head_update_w = [&](auto wtag, int k, int h, hipStream_t strm) {
@@ -1453,10 +1456,11 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
     int queued = 0;      // blocks whose inverse rows are queued on sol
     bool late = false;   // the bulk updates have left bf16 MFMA
     if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;   // after the set-up kernels
+    if (hipStreamWaitEvent(aux, ev_col, 0) != hipSuccess) return DR_ERR_HIP;
+    if (hipEventRecord(ev_bulk, hs) != hipSuccess) return DR_ERR_HIP;   // no bulk yet
     int b = 0, m = width_at(0);
     while (b < nblk) {
       const int k = NB * b, W = NB * m;
-      if (hipStreamWaitEvent(aux, ev_col, 0) != hipSuccess) return DR_ERR_HIP;
       for (int i = 0; i < m; ++i) {
         factor_panel(b + i, aux);
         if (late) {
@@ -1485,8 +1489,8 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
         queued = b2;
       }
       if (m2 == 0 || rest <= 0) break;
-      head_update(W, k, m2, hs);
-      if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;
+      if (hipStreamWaitEvent(aux, ev_bulk, 0) != hipSuccess) return DR_ERR_HIP;
+      head_update(W, k, m2, aux);
       const int k1 = k + W;
       if (bulk6) {
         if (W == 4 * NB) {
@@ -1518,6 +1522,7 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
                                ctl);
         }
       }
+      if (hipEventRecord(ev_bulk, hs) != hipSuccess) return DR_ERR_HIP;
       b = b2;
       m = m2;
     }
