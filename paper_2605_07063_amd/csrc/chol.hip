@@ -262,25 +262,31 @@ __device__ __forceinline__ f32x4 tile_nn(const float* A, int ra, int ca, const f
 // block is padded to 128 with the identity) in one workgroup, in LDS as
 // packed lower-triangle 16x16 tiles (72 KiB in all, so the workgroup fits
 // on a CU beside a trailing-update workgroup):
-//   the diagonal tile D_J is factored and inverted in registers by wave 0
-//   (tile16_chol_inv), one step ahead: while waves 1..3 take the trailing
-//   tiles of step J, wave 0 updates tile (J+1, J+1) first and factors it;
+//   eight waves; the diagonal tile D_J is factored and inverted in
+//   registers by wave 0 (tile16_chol_inv), one step ahead: while six
+//   waves take the trailing tiles of step J, wave 0 updates tile
+//   (J+1, J+1) first and factors it (wave 4, which shares wave 0's SIMD,
+//   stays out of that phase); tile (0, 0) is loaded and factored by wave 0
+//   while the others load the rest of the block;
 //   panel tiles L_IJ = A_IJ D_J^-T and trailing tiles A_IK -= L_IJ L_KJ^T
 //   are 16x16x16 fp32 MFMA products (two barriers per step);
 //   row J of the inverse, X_Jm = -X_JJ sum_{i=m}^{J-1} L_Ji X_im (m < J),
-//   needs only rows < J of it, the final tiles L_Ji and D_J^-1, so waves
-//   1..3 form it in step J after their trailing tiles, while wave 0
-//   factors tile J+1.  Row r of every tile is stored at row position prm(r), so the
-// rows 4q + j (q = 0..3) that one MFMA result register covers fall in four
+//   needs only rows < J of it, the final tiles L_Ji and D_J^-1, so the six
+//   waves form it in step J after their trailing tiles, while wave 0
+//   factors tile J+1.
+// Row r of every tile is stored at row position prm(r), so the rows
+// 4q + j (q = 0..3) that one MFMA result register covers fall in four
 // different LDS bank groups.
 __device__ __forceinline__ int prm(int r) { return 4 * (r & 3) + (r >> 2); }
 __device__ __forceinline__ int ptile(int I, int J) { return (I * (I + 1) / 2 + J) * 256; }   // J <= I
 __device__ __forceinline__ int otile(int I, int J) { return (I * (I - 1) / 2 + J) * 256; }   // J < I
 
+constexpr int kPotrfWaves = 8;   // wave 0 factors the diagonal tiles, the others the rest
 template <int PB>
-__global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, int k, int kb, float* inv,
-                                                       LgCtl* ctl) {
+__global__ __launch_bounds__(64 * kPotrfWaves) void lg_potrf_kernel(float* L, long long ldL, int k, int kb,
+                                                                    float* inv, LgCtl* ctl) {
   static_assert(PB == 16, "16x16 tiles");
+  constexpr int NW = kPotrfWaves;
   if (ctl->skip) return;
   constexpr int NT = NB / 16;
   __shared__ __attribute__((aligned(16))) float Lt[NT * (NT + 1) / 2 * 256];   // the block, then its factor
@@ -293,46 +299,51 @@ __global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, 
 
   // the block into the tiles: rows past kb are identity rows; a float4
   // chunk is read only if it starts on or left of the diagonal (it then
-  // ends inside the row), and entries right of the diagonal are cleared
-  {
-    constexpr int NQ = NT * (NT + 1) / 2, UQ = (NQ + 3) / 4;
-    const int r = lane >> 2, c4 = 4 * (lane & 3);
+  // ends inside the row), and entries right of the diagonal are cleared.
+  // Wave 0 loads tile (0, 0) alone and factors it (below) while the other
+  // waves load the rest.
+  const int lrow = lane >> 2, lc4 = 4 * (lane & 3);
+  auto load_tile = [&](int q) {
+    int I, J;
+    tile_pair(q, I, J);
+    const int i = 16 * I + lrow, j = 16 * J + lc4;
+    return (i < kb && j <= i) ? *reinterpret_cast<const float4*>(L + (long long)(k + i) * ldL + k + j)
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
+  };
+  auto store_tile = [&](int q, float4 a) {
+    int I, J;
+    tile_pair(q, I, J);
+    const int i = 16 * I + lrow, j = 16 * J + lc4;
+    if (i < kb) {
+      if (j + 1 > i) a.y = 0.f;
+      if (j + 2 > i) a.z = 0.f;
+      if (j + 3 > i) a.w = 0.f;
+    } else {
+      a.x = j == i ? 1.f : 0.f;
+      a.y = j + 1 == i ? 1.f : 0.f;
+      a.z = j + 2 == i ? 1.f : 0.f;
+      a.w = j + 3 == i ? 1.f : 0.f;
+    }
+    *reinterpret_cast<float4*>(&Lt[q * 256 + prm(lrow) * 16 + lc4]) = a;
+  };
+  constexpr int NQ = NT * (NT + 1) / 2;
+  if (w == 0) {
+    if (tid == 0) bad_s = 0;
+    store_tile(0, load_tile(0));
+  } else {
+    constexpr int UQ = (NQ - 1 + NW - 2) / (NW - 1);
     float4 v[UQ];
 #pragma unroll
     for (int u = 0; u < UQ; ++u) {
-      const int q = w + 4 * u;
-      v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (q < NQ) {
-        int I, J;
-        tile_pair(q, I, J);
-        const int i = 16 * I + r, j = 16 * J + c4;
-        if (i < kb && j <= i) v[u] = *reinterpret_cast<const float4*>(L + (long long)(k + i) * ldL + k + j);
-      }
+      const int q = w + (NW - 1) * u;   // 1 .. NQ - 1
+      v[u] = q < NQ ? load_tile(q) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 #pragma unroll
     for (int u = 0; u < UQ; ++u) {
-      const int q = w + 4 * u;
-      if (q < NQ) {
-        int I, J;
-        tile_pair(q, I, J);
-        const int i = 16 * I + r, j = 16 * J + c4;
-        float4 a = v[u];
-        if (i < kb) {
-          if (j + 1 > i) a.y = 0.f;
-          if (j + 2 > i) a.z = 0.f;
-          if (j + 3 > i) a.w = 0.f;
-        } else {
-          a.x = j == i ? 1.f : 0.f;
-          a.y = j + 1 == i ? 1.f : 0.f;
-          a.z = j + 2 == i ? 1.f : 0.f;
-          a.w = j + 3 == i ? 1.f : 0.f;
-        }
-        *reinterpret_cast<float4*>(&Lt[q * 256 + prm(r) * 16 + c4]) = a;
-      }
+      const int q = w + (NW - 1) * u;
+      if (q < NQ) store_tile(q, v[u]);
     }
   }
-  if (tid == 0) bad_s = 0;
-  __syncthreads();
 
   // wave 0: factor and invert diagonal tile J (block-relative pivot on failure)
   auto factor_diag = [&](int J) __attribute__((always_inline)) {
@@ -396,7 +407,7 @@ __global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, 
   __syncthreads();
   for (int J = 0; J < NT; ++J) {
     if (bad_s) break;
-    for (int I = J + 1 + w; I < NT; I += 4) {
+    for (int I = J + 1 + w; I < NT; I += NW) {
       float* A = Lt + ptile(I, J);
       const f32x4 acc = nt16(A, Xd + J * 256);
 #pragma unroll
@@ -420,8 +431,12 @@ __global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, 
         factor_diag(J + 1);
       }
     } else {
-      for (int q = w; q < nrest; q += 3) trail(q);
-      for (int m = w - 1; m < J; m += 3) inv_tile(J, m);
+      // waves 1..3 and 5..7: wave 4 shares wave 0's SIMD and stays idle
+      if (w != 4) {
+        const int v = w < 4 ? w - 1 : w - 2;   // 0 .. 5
+        for (int q = 1 + v; q < nrest; q += NW - 2) trail(q);
+        for (int m = v; m < J; m += NW - 2) inv_tile(J, m);
+      }
     }
     __syncthreads();
   }
@@ -438,7 +453,7 @@ __global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, 
   {
     constexpr int NQ = NT * (NT + 1) / 2;
     const int r = lane >> 2, c4 = 4 * (lane & 3);
-    for (int q = w; q < NQ; q += 4) {
+    for (int q = w; q < NQ; q += NW) {
       int I, J;
       tile_pair(q, I, J);
       const int i = 16 * I + r, j = 16 * J + c4;
@@ -449,7 +464,7 @@ __global__ __launch_bounds__(256) void lg_potrf_kernel(float* L, long long ldL, 
   }
 
   // the whole 128 x 128 inverse (upper tiles zero), row-major
-  for (int e = tid; e < NB * (NB / 4); e += 256) {
+  for (int e = tid; e < NB * (NB / 4); e += 64 * NW) {
     const int i = e / (NB / 4), c = 4 * (e % (NB / 4));
     const int I = i >> 4, J = c >> 4, r = i & 15;
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -1405,7 +1420,7 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       const int k = NB * b;
       const int kb = n - k < NB ? n - k : NB;
       float* ib = inv + (long long)b * NB * NB;
-      hipLaunchKernelGGL(lg_potrf_kernel<kPotrfPB>, dim3(1), dim3(256), 0, strm, L, ldL, k, kb, ib, ctl);
+      hipLaunchKernelGGL(lg_potrf_kernel<kPotrfPB>, dim3(1), dim3(64 * kPotrfWaves), 0, strm, L, ldL, k, kb, ib, ctl);
       const int rest = n - k - NB;
       if (rest > 0)
         hipLaunchKernelGGL(lg_trsm_kernel, dim3((rest + 63) / 64), dim3(256), 0, strm, L, ldL, n, k, ib, ctl);
