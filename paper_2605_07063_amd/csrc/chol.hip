@@ -379,11 +379,11 @@ __global__ __launch_bounds__(64 * kPotrfWaves) void lg_potrf_kernel(float* L, lo
     return acc;
   };
 
-  // tile (I, J), J < I, of the inverse
-  auto inv_tile = [&](int I, int J) {
-    // T = sum_{m=J}^{I-1} L_Im X_mJ, X_mJ read as the MFMA B operand (k = row)
-    f32x4 t = {0.f, 0.f, 0.f, 0.f};
-    for (int m = J; m < I; ++m) {
+  // tile (I, J), J < I, of the inverse: T = sum_{m=J}^{I-1} L_Im X_mJ
+  // (inv_sum over a range of m, X_mJ read as the MFMA B operand, k = row),
+  // then X_IJ = -X_II T (inv_store)
+  auto inv_sum = [&](int I, int J, int m0, int m1, f32x4 t) {
+    for (int m = m0; m < m1; ++m) {
       const float4 av = *reinterpret_cast<const float4*>(Lt + ptile(I, m) + prm(lr) * 16 + 4 * lq);
       const float* X = m == J ? Xd + J * 256 : Xo + otile(m, J);
       t = mma_f32(av.x, X[prm(4 * lq + 0) * 16 + lr], t);
@@ -391,6 +391,9 @@ __global__ __launch_bounds__(64 * kPotrfWaves) void lg_potrf_kernel(float* L, lo
       t = mma_f32(av.z, X[prm(4 * lq + 2) * 16 + lr], t);
       t = mma_f32(av.w, X[prm(4 * lq + 3) * 16 + lr], t);
     }
+    return t;
+  };
+  auto inv_store = [&](int I, int J, f32x4 t) {
     // X_IJ = -X_II T: T's result layout (row 4 lq + j, column lr in
     // register j) is the B operand of reduction index 4 lq + j
     const float4 xv = *reinterpret_cast<const float4*>(Xd + I * 256 + prm(lr) * 16 + 4 * lq);
@@ -402,6 +405,31 @@ __global__ __launch_bounds__(64 * kPotrfWaves) void lg_potrf_kernel(float* L, lo
 #pragma unroll
     for (int j = 0; j < 4; ++j) Xo[otile(I, J) + prm(4 * lq + j) * 16 + lr] = -x[j];
   };
+  auto inv_tile = [&](int I, int J) { inv_store(I, J, inv_sum(I, J, J, I, f32x4{0.f, 0.f, 0.f, 0.f})); };
+  // results out while the steps run: column J of the factor (tiles (I, J),
+  // the chunk rule of the load: entries right of the diagonal inside a
+  // chunk are never read) and block row I of the inverse (zero right of
+  // its diagonal tile), one wave each
+  auto write_lcol = [&](int J) {
+    const int r = lane >> 2, c4 = 4 * (lane & 3);
+    for (int I = J; I < NT; ++I) {
+      const int i = 16 * I + r, j = 16 * J + c4;
+      if (i < kb && j <= i)
+        *reinterpret_cast<float4*>(L + (long long)(k + i) * ldL + k + j) =
+            *reinterpret_cast<const float4*>(&Lt[ptile(I, J) + prm(r) * 16 + c4]);
+    }
+  };
+  auto write_inv_row = [&](int I, int t0, int nt) {
+    for (int e = t0; e < 16 * (NB / 4); e += nt) {
+      const int r = e / (NB / 4), c = 4 * (e % (NB / 4)), J = c >> 4;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (J == I) v = *reinterpret_cast<const float4*>(&Xd[I * 256 + prm(r) * 16 + (c & 15)]);
+      else if (J < I) v = *reinterpret_cast<const float4*>(&Xo[otile(I, J) + prm(r) * 16 + (c & 15)]);
+      *reinterpret_cast<float4*>(inv + (long long)(16 * I + r) * NB + c) = v;
+    }
+  };
+  static_assert(NT == NW, "one partial sum of the last inverse row per inverse wave");
+  f32x4 tlast = {0.f, 0.f, 0.f, 0.f};   // wave v: row NT - 1, column v, over m < NT - 2
 
   if (w == 0) factor_diag(0);
   __syncthreads();
@@ -430,12 +458,22 @@ __global__ __launch_bounds__(64 * kPotrfWaves) void lg_potrf_kernel(float* L, lo
         trail(0);
         factor_diag(J + 1);
       }
+    } else if (w == 4) {
+      // wave 4 shares wave 0's SIMD: it only writes out what is final
+      write_lcol(J);
+      if (J > 0) write_inv_row(J - 1, lane, 64);
     } else {
-      // waves 1..3 and 5..7: wave 4 shares wave 0's SIMD and stays idle
-      if (w != 4) {
-        const int v = w < 4 ? w - 1 : w - 2;   // 0 .. 5
-        for (int q = 1 + v; q < nrest; q += NW - 2) trail(q);
+      // waves 1..3 and 5..7: the other trailing tiles, then row J of the
+      // inverse; in step NT - 2 also the sums of row NT - 1 that need
+      // only rows < NT - 2, so that step NT - 1 adds one term to each
+      const int v = w < 4 ? w - 1 : w - 2;   // 0 .. 5
+      for (int q = 1 + v; q < nrest; q += NW - 2) trail(q);
+      if (J == NT - 1) {
+        for (int m = v; m < J; m += NW - 2)
+          inv_store(J, m, m < NT - 2 ? inv_sum(J, m, NT - 2, NT - 1, tlast) : inv_sum(J, m, m, J, f32x4{0.f, 0.f, 0.f, 0.f}));
+      } else {
         for (int m = v; m < J; m += NW - 2) inv_tile(J, m);
+        if (J == NT - 2) tlast = inv_sum(NT - 1, v, v, NT - 2, tlast);
       }
     }
     __syncthreads();
@@ -448,30 +486,9 @@ __global__ __launch_bounds__(64 * kPotrfWaves) void lg_potrf_kernel(float* L, lo
     }
     return;
   }
-  // the factor back to L (the chunk rule of the load; entries right of the
-  // diagonal inside a chunk are never read)
-  {
-    constexpr int NQ = NT * (NT + 1) / 2;
-    const int r = lane >> 2, c4 = 4 * (lane & 3);
-    for (int q = w; q < NQ; q += NW) {
-      int I, J;
-      tile_pair(q, I, J);
-      const int i = 16 * I + r, j = 16 * J + c4;
-      if (i < kb && j <= i)
-        *reinterpret_cast<float4*>(L + (long long)(k + i) * ldL + k + j) =
-            *reinterpret_cast<const float4*>(&Lt[q * 256 + prm(r) * 16 + c4]);
-    }
-  }
-
-  // the whole 128 x 128 inverse (upper tiles zero), row-major
-  for (int e = tid; e < NB * (NB / 4); e += 64 * NW) {
-    const int i = e / (NB / 4), c = 4 * (e % (NB / 4));
-    const int I = i >> 4, J = c >> 4, r = i & 15;
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (J == I) v = *reinterpret_cast<const float4*>(&Xd[I * 256 + prm(r) * 16 + (c & 15)]);
-    else if (J < I) v = *reinterpret_cast<const float4*>(&Xo[otile(I, J) + prm(r) * 16 + (c & 15)]);
-    *reinterpret_cast<float4*>(inv + (long long)i * NB + c) = v;
-  }
+  // the factor's columns and the inverse's rows above the last went out
+  // during the steps
+  write_inv_row(NT - 1, tid, 64 * NW);
 }
 constexpr int kPotrfPB = 16;
 
