@@ -158,6 +158,7 @@ __global__ __launch_bounds__(1024) void lg_setup_kernel(const float* K, const fl
     ctl->lam = lam;
     if (nonfinite) {
       ctl->skip = 1;
+      ctl->nonfinite = 1;
       ctl->info = DR_INFO_NONFINITE;
       *lam_eff_out = 0.f;
     } else {
@@ -168,14 +169,15 @@ __global__ __launch_bounds__(1024) void lg_setup_kernel(const float* K, const fl
 }
 
 // L = lower triangle of K + lam_eff I, and the finiteness scan of all of K
-// in the same pass (the upper triangle is read only for the scan): row i,
-// 4096 columns per workgroup, a float4 per thread and step (scalar loads
-// when n is not a multiple of 4 or K is not 16-byte aligned).  L is written
+// in the same pass (the upper triangle is read only for the scan), columns
+// c0 .. c1 - 1 (c0 a multiple of 4): row i, 4096 columns per workgroup, a
+// float4 per thread and step (scalar loads when n is not a multiple of 4
+// or K is not 16-byte aligned).  L is written
 // only when the group is still open; a non-finite entry closes it with
 // DR_INFO_NONFINITE, over the empty-span outcome of a zero trace.
 constexpr int kLoadCols = 4096;
-__global__ __launch_bounds__(256) void lg_load_kernel(const float* K, int n, int vec, float* L, long long ldL,
-                                                      LgCtl* ctl, float* lam_eff_out) {
+__global__ __launch_bounds__(256) void lg_load_kernel(const float* K, int n, int vec, int c0, int c1, float* L,
+                                                      long long ldL, LgCtl* ctl, float* lam_eff_out) {
   __shared__ int any;
   const int i = blockIdx.x, tid = threadIdx.x;
   if (tid == 0) any = 0;
@@ -186,8 +188,8 @@ __global__ __launch_bounds__(256) void lg_load_kernel(const float* K, int n, int
   bool bad = false;
 #pragma unroll
   for (int u = 0; u < kLoadCols / 1024; ++u) {
-    const int c = blockIdx.y * kLoadCols + 1024 * u + 4 * tid;
-    if (c >= n) break;
+    const int c = c0 + blockIdx.y * kLoadCols + 1024 * u + 4 * tid;
+    if (c >= c1) break;
     float4 v;
     if (vec) {
       v = *reinterpret_cast<const float4*>(kr + c);
@@ -1286,7 +1288,9 @@ __global__ __launch_bounds__(1024) void lg_final_kernel(const float* s, const fl
     for (int k = 0; k < 16; ++k) X = fmax(X, shm[k]);
     const bool converged = ctl->done || refine_converged(ctl->dxn[kRefine - 1], ctl->dxn[kRefine], X);
     resid2[0] = skip ? t2[0] : (float)((double)t2[0] + q);
-    info[0] = skip ? ctl->info : (converged ? 0 : DR_INFO_NOT_CONVERGED);
+    // a non-finite input outranks a pivot failure (the factorisation of the
+    // first panels starts before the whole of K is scanned)
+    info[0] = skip ? (ctl->nonfinite ? DR_INFO_NONFINITE : ctl->info) : (converged ? 0 : DR_INFO_NOT_CONVERGED);
   }
 }
 
@@ -1396,8 +1400,7 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
     hipLaunchKernelGGL(lg_init_kernel, dim3((npad + 255) / 256), dim3(256), 0, hs, ctl, sp, n, npad, x, dx, r, z);
     const int vec = aligned16(Kp) && n % 4 == 0;
     hipLaunchKernelGGL(lg_setup_kernel, dim3(1), dim3(1024), 0, hs, Kp, sp, n, lambda, mode, ctl, lam_eff + p);
-    hipLaunchKernelGGL(lg_load_kernel, dim3(n, (n + kLoadCols - 1) / kLoadCols), dim3(256), 0, hs, Kp, n, vec, L, ldL,
-                       ctl, lam_eff + p);
+
     // Right-looking blocked factorisation by steps of four or two panels,
     // with look-ahead.  The trailing matrix takes one rank-512 update per
     // step of four panels while that update fills the CUs on bf16 MFMA
@@ -1487,10 +1490,19 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
     };
     int queued = 0;      // blocks whose inverse rows are queued on sol
     bool late = false;   // the bulk updates have left bf16 MFMA
-    if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;   // after the set-up kernels
-    if (hipStreamWaitEvent(aux, ev_col, 0) != hipSuccess) return DR_ERR_HIP;
-    if (hipEventRecord(ev_bulk, hs) != hipSuccess) return DR_ERR_HIP;   // no bulk yet
+    // K into L in two parts: the first step's panel columns, which its
+    // chain needs, then the rest, which the first head and bulk need
     int b = 0, m = width_at(0);
+    auto load = [&](int c0, int c1) {
+      if (c1 > c0)
+        hipLaunchKernelGGL(lg_load_kernel, dim3(n, (c1 - c0 + kLoadCols - 1) / kLoadCols), dim3(256), 0, hs, Kp, n, vec,
+                           c0, c1, L, ldL, ctl, lam_eff + p);
+    };
+    load(0, NB * m < n ? NB * m : n);
+    if (hipEventRecord(ev_col, hs) != hipSuccess) return DR_ERR_HIP;
+    if (hipStreamWaitEvent(aux, ev_col, 0) != hipSuccess) return DR_ERR_HIP;
+    load(NB * m, n);
+    if (hipEventRecord(ev_bulk, hs) != hipSuccess) return DR_ERR_HIP;   // no bulk yet
     while (b < nblk) {
       const int k = NB * b, W = NB * m;
       for (int i = 0; i < m; ++i) {

@@ -278,6 +278,19 @@ def test_span_blocked_special_cases():
     w, le, r2, info = api.project_span(Kn, s, t2, 1e-3, RIDGE_REL_TRACE)
     torch.cuda.synchronize()
     assert int(info[0]) == -3 and torch.all(w == 0) and float(le[0]) == 0.0
+    # a non-finite entry outranks a non-positive pivot, wherever each lies
+    # (the first panels are factored while the rest of K is still scanned):
+    # a pivot failure in the first block with a NaN in a late column, below
+    # and above the diagonal
+    for (i, j) in ((390, 350), (300, 399)):
+        d = torch.ones(n, device=DEV)
+        d[2] = -1.0
+        Kb = torch.diag(d)[None].contiguous()
+        Kb[0, i, j] = float("nan")
+        w, le, r2, info = api.project_span(Kb, torch.ones(1, n, device=DEV), torch.full((1,), 5.0, device=DEV), 0.0,
+                                           RIDGE_ABS)
+        torch.cuda.synchronize()
+        assert int(info[0]) == -3 and torch.all(w == 0) and float(le[0]) == 0.0 and float(r2[0]) == 5.0
     # relative ridge with K = 0: empty span
     w, le, r2, info = api.project_span(torch.zeros(1, n, n, device=DEV), torch.zeros(1, n, device=DEV),
                                        torch.full((1,), 3.0, device=DEV), 1e-2, RIDGE_REL_TRACE)
