@@ -942,7 +942,8 @@ __global__ __launch_bounds__(512) void lg_syrk6_kernel(const unsigned char* pl, 
 // needs only the factor's block row ii (final once block ii is factored),
 // the rows of X above it and X_ii, the inverse of the 128 x 128 diagonal
 // block (read where the block factor left it); jj = ii copies X_ii onto the
-// diagonal.  Each block is split over SV_CQ workgroups by column quarters
+// diagonal; the same row of several super-blocks in one launch (grid y).
+// Each block is split over SV_CQ workgroups by column quarters
 // (the chain of products of a block is the latency that counts); the
 // 128 x 128 L_im and the quarter of X_mj are staged in LDS and wave w
 // computes rows 32 w .. 32 w + 31 of the quarter with fp32 MFMA.  The block
@@ -964,9 +965,10 @@ __device__ __forceinline__ f32x4 tile_nn_q(const float* A, int ra, const float* 
 }
 
 __global__ __launch_bounds__(256) void lg_sinv_kernel(const float* L, long long ldL, int n, int nblk,
-                                                      const float* inv, float* sinv, float* sinvt, int S, int ii,
+                                                      const float* inv, float* sinv, float* sinvt, int S0, int ii,
                                                       const LgCtl* ctl) {
   if (ctl->skip) return;
+  const int S = S0 + blockIdx.y;   // row ii of super-blocks S0, S0 + 1, ...
   const int jj = blockIdx.x / SV_CQ, cq = blockIdx.x % SV_CQ, d = ii - jj;
   const int bj = SB * S + jj, bi = bj + d;
   if (d < 0 || bi >= nblk) return;
@@ -1529,8 +1531,18 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
       late = late || !bulk6;
       if (late && queued < b2) {
         if (hipStreamWaitEvent(sol, ev_next, 0) != hipSuccess) return DR_ERR_HIP;
-        for (int bb = queued; bb < b2; ++bb) after_block(bb);
-        queued = b2;
+        // whole super-blocks of the backlog: each row of all of them in one
+        // launch, then their forward steps; the rest block by block
+        while (queued < b2 && queued % SB != 0) after_block(queued++);
+        const int S_lo = queued / SB, S_hi = b2 / SB;
+        if (S_hi > S_lo) {
+          for (int ii = 0; ii < SB; ++ii)
+            hipLaunchKernelGGL(lg_sinv_kernel, dim3((ii + 1) * SV_CQ, S_hi - S_lo), dim3(256), 0, sol, L, ldL, n, nblk,
+                               inv, sinv, sinvt, S_lo, ii, ctl);
+          for (int S = S_lo; S < S_hi; ++S) fwd_step(S, sol);
+          queued = SB * S_hi;
+        }
+        while (queued < b2) after_block(queued++);
       }
       if (m2 == 0 || rest <= 0) break;
       if (hipStreamWaitEvent(aux, ev_bulk, 0) != hipSuccess) return DR_ERR_HIP;
