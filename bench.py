@@ -76,15 +76,24 @@ def parse():
 # timing helpers
 # ---------------------------------------------------------------------------
 
-def _event_ms(fn, reps):
-    """GPU milliseconds per call of fn: a spin kernel keeps the stream busy
-    while the host enqueues every call, so the two events bracket the calls'
-    GPU execution and not the host's launch rate."""
+def _event_ms(fn, reps, warm=0):
+    """GPU milliseconds per call of fn.  By default a spin kernel keeps the
+    stream busy while the host enqueues every call, so the two events bracket
+    the calls' GPU execution and not the host's launch rate.  With warm > 0
+    (calls of a millisecond and longer, whose launch rate never starves the
+    GPU) warm untimed calls run right before the timed ones instead: the
+    clock settles at its loaded level before the first event, as it is in a
+    sequence of projection steps, where it takes several milliseconds to
+    climb back after the GPU has idled (the spin kernel occupies one CU)."""
     import torch
     fn()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda._sleep(100_000_000)
+    if warm > 0:
+        for _ in range(warm):
+            fn()
+    else:
+        torch.cuda._sleep(100_000_000)
     e0.record()
     for _ in range(reps):
         fn()
@@ -558,7 +567,7 @@ def cpu_baseline_small(layers, lens, S, K, s, t2, n, m, k_top, lam, budget_s, go
     }
 
 
-def run_gram_dominated(api, _lib, workloads, dev, peaks, with_cpu, reps=3):
+def run_gram_dominated(api, _lib, workloads, dev, peaks, with_cpu, reps=10, warm=5):
     """The Gram-dominated projection step, stage by stage: the 16384 x 16384
     Gram of 16384 bf16 rows of dimension 8192 (+ 32 target rows: scores and
     the target's squared norm), the ridge span at n = 16384 (blocked
@@ -584,9 +593,9 @@ def run_gram_dominated(api, _lib, workloads, dev, peaks, with_cpu, reps=3):
     idx = torch.empty(1, k, dtype=torch.int32, device=dev)
     wt = torch.empty(1, n, device=dev)
     it = torch.empty(1, dtype=torch.int32, device=dev)
-    gram_ms = _event_ms(lambda: api.dr_gram(G, Gt, [0, kappa], K, s, t2, workspace=gws), reps)
+    gram_ms = _event_ms(lambda: api.dr_gram(G, Gt, [0, kappa], K, s, t2, workspace=gws), reps, warm)
     span_ms = _event_ms(lambda: api.dr_project_span(K, s, t2, cfg["lam"], _lib.DR_RIDGE_REL_TRACE, w, le, r2, info,
-                                                     workspace=sws), reps)
+                                                     workspace=sws), reps, warm)
     topk_ms = _event_ms(lambda: api.dr_select_topk(s, k, idx, wt, it), 10 * reps)
     if int(info[0]) != 0 or int(it[0]) != 0:
         raise RuntimeError(f"Gram-dominated projection reported info {int(info[0])} / {int(it[0])}")
