@@ -312,20 +312,57 @@ constexpr int kBPanel = kBT * kBK * 2;     // bytes of one operand panel per ste
 constexpr int kBStage = 2 * kBPanel;       // A and B panels
 constexpr int kBigMinTiles = 512;
 
-constexpr int kBTLd = 132;   // row stride (floats) of the transposed half tile staged in LDS
-constexpr int kBLds = 2 * kBStage > kBT * kBTLd * 4 ? 2 * kBStage : kBT * kBTLd * 4;
-
 struct BigArgs {
   const unsigned char* G;
   long long ldG;   // elements
   int n, T, pairs;
-  int vec4;        // K rows start 16-byte aligned (n % 4 == 0, K aligned): float4 stores of the transposed tile
+  int vec4;        // K rows start 16-byte aligned (n % 4 == 0, K aligned): float4 stores
   long long goff[kMaxGroups + 1];
   float* K;        // [P][n][n] of this launch's groups
 };
 
-__global__ __launch_bounds__(512) void gram_big_kernel(BigArgs a) {
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[kBLds];
+// One 16x16 block of C (lane l holds C[4 (l / 16) + r][l % 16] in element r)
+// into K at rows R.., columns C.. and, mirrored, at rows C.., columns R..,
+// for an off-diagonal tile inside K with 16-byte aligned rows: every element
+// goes out in non-temporal float4 stores.  The mirror is the accumulator as
+// it stands (four consecutive rows of one column are four consecutive
+// columns of the transposed row); the block itself after a 4 x 4 transpose
+// inside each quad of lanes (two rounds of DPP quad permutations).
+__device__ __forceinline__ void big_store_block_fast(float* Kp, int n, int R, int C, f32x4 v, int lane) {
+  const int lr = lane & 15, lg = lane >> 4, c = lane & 3, m = lr >> 2;
+  __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(Kp + (long long)(C + lr) * n + R + 4 * lg));
+  float x0 = v[0], x1 = v[1], x2 = v[2], x3 = v[3];
+  {  // exchange across bit 0 of the quad lane
+    const float s01 = (c & 1) ? x0 : x1, s23 = (c & 1) ? x2 : x3;
+    const float r01 = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s01), 0xB1, 0xF, 0xF, false));
+    const float r23 = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s23), 0xB1, 0xF, 0xF, false));
+    if (c & 1) { x0 = r01; x2 = r23; } else { x1 = r01; x3 = r23; }
+  }
+  {  // exchange across bit 1
+    const float s02 = (c & 2) ? x0 : x2, s13 = (c & 2) ? x1 : x3;
+    const float r02 = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s02), 0x4E, 0xF, 0xF, false));
+    const float r13 = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s13), 0x4E, 0xF, 0xF, false));
+    if (c & 2) { x0 = r02; x1 = r13; } else { x2 = r02; x3 = r13; }
+  }
+  __builtin_nontemporal_store(f32x4{x0, x1, x2, x3}, reinterpret_cast<f32x4*>(Kp + (long long)(R + 4 * lg + c) * n + C + 4 * m));
+}
+
+// the same block element by element: rows and columns past n are skipped,
+// and in a diagonal tile only the lower triangle (with its mirror above)
+__device__ __forceinline__ void big_store_block_masked(float* Kp, int n, bool diag, int R, int C, f32x4 v, int lane) {
+  const int lr = lane & 15, lg = lane >> 4;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int row = R + 4 * lg + r, col = C + lr;
+    if (row < n && col < n) {
+      if (!diag || col <= row) Kp[(long long)row * n + col] = v[r];
+      if (!diag || col < row) Kp[(long long)col * n + row] = v[r];
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gram_big_kernel(BigArgs a) {
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * kBStage];
   const int p = blockIdx.y;
   // Workgroup i runs on XCD i % 8, and an XCD's 32 CUs take its workgroups
   // in order.  The lower-triangle tiles are grouped in chunks of 4 tile rows
@@ -352,114 +389,116 @@ __global__ __launch_bounds__(512) void gram_big_kernel(BigArgs a) {
   const int nk = (int)((g1 - g0 + kBK - 1) / kBK);
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wr = w >> 2, wc = w & 3;   // 128-row half, 64-column quarter of the tile
+  const int wr = w >> 1, wc = w & 1;   // 128-row half of A, 128-row half of B
+  const int lr = lane & 15, lg = lane >> 4;
   const int rowA0 = I * kBT, rowB0 = J * kBT;
   const int rowsA = a.n - rowA0 < kBT ? a.n - rowA0 : kBT;
   const int rowsB = a.n - rowB0 < kBT ? a.n - rowB0 : kBT;
   const bool diag = I == J;
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(a.G + (long long)rowA0 * a.ldG * 2, kOobOffset);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.G + (long long)rowB0 * a.ldG * 2, kOobOffset);
-  // this lane's 4 rows of each panel (half blocks w, w + 8, w + 16, w + 24) and its segment
-  unsigned offA[4], offB[4];
-  int segs[4];
+  // this lane's 8 rows of each panel (half blocks w, w + 4, ..., w + 28) and its segment
+  unsigned offA[8], offB[8];
+  int segs[8];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int hb = w + 8 * u;             // half block: rows 8 hb .. 8 hb + 7
+  for (int u = 0; u < 8; ++u) {
+    const int hb = w + 4 * u;             // half block: rows 8 hb .. 8 hb + 7
     const int r = 8 * hb + (lane >> 3);
     segs[u] = swz_seg_of_lane(lane, hb & 1);
     offA[u] = r < rowsA ? (unsigned)((long long)r * a.ldG * 2) : kOobOffset;
     offB[u] = r < rowsB ? (unsigned)((long long)r * a.ldG * 2) : kOobOffset;
   }
-  // straight-line issue (no branches around the loads keeps the accumulators
-  // in place): a diagonal tile loads its panel twice, and the step after the
-  // last one loads zeros (every column is past the group) into the free stage
-  auto issue = [&](int t, int st) {
+  // DMA q (0..15) of step t into stage st: q even A, q odd B, half block
+  // w + 4 (q / 2); steps past the group load zeros (no memory access)
+  auto dma1 = [&](int t, int st, int q) {
     unsigned char* sb = lds + st * kBStage;
-    const long long cbase = g0 + (long long)t * kBK;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const long long col = cbase + segs[u] * 8;
-      const bool cok = col < g1;
-      const unsigned ca = (offA[u] == kOobOffset || !cok) ? kOobOffset : offA[u] + (unsigned)(col * 2);
+    const int u = q >> 1;
+    const long long col = g0 + (long long)t * kBK + segs[u] * 8;
+    const bool cok = col < g1;
+    if (q & 1) {
       const unsigned cb = (offB[u] == kOobOffset || !cok) ? kOobOffset : offB[u] + (unsigned)(col * 2);
-      dma16<kAuxCached>(ra, sb + (w + 8 * u) * 1024, ca);
-      dma16<kAuxCached>(rb, sb + kBPanel + (w + 8 * u) * 1024, cb);
+      dma16<kAuxCached>(rb, sb + kBPanel + (w + 4 * u) * 1024, cb);
+    } else {
+      const unsigned ca = (offA[u] == kOobOffset || !cok) ? kOobOffset : offA[u] + (unsigned)(col * 2);
+      dma16<kAuxCached>(ra, sb + (w + 4 * u) * 1024, ca);
     }
   };
-
-  f32x4 acc[8][4];
+  // fragment read q (0..15) of 32-column half kh: q even A block q / 2, odd B block
+  auto rd1 = [&](u32x4* fa, u32x4* fb, const unsigned char* sa, int kh, int q) {
+    const int seg = 4 * kh + lg;
+    if (q & 1) fb[q >> 1] = swz_read(sa + kBPanel + (wc * 8 + (q >> 1)) * 2048, lr, seg);
+    else fa[q >> 1] = swz_read(sa + (wr * 8 + (q >> 1)) * 2048, lr, seg);
+  };
+  // The 128 x 128 accumulator (256 registers) sits in the AGPRs: each product
+  // is an in-place asm MFMA on its accumulator, so the register allocator
+  // keeps every accumulator where it is (the compiler's own MFMA form moves
+  // them between register files at this size).  Volatile asm also keeps the
+  // written order: each fragment read and DMA issue sits between MFMAs.
+  f32x4 acc[8][8];
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const int lr = lane & 15, lg = lane >> 4;
-  issue(0, 0);
+    for (int j = 0; j < 8; ++j) {
+      acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      // the zeros are in place before the prologue below: the compiler does
+      // not see the MFMAs inside the asm, so it would not space a register
+      // write and the product that reads it apart
+      asm volatile("" : "+a"(acc[i][j]));
+    }
+  auto mma = [&](int i, int j, const u32x4* fa, const u32x4* fb) {
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc[i][j]) : "v"(fa[i]), "v"(fb[j]));
+  };
+  u32x4 fa0[8], fb0[8], fa1[8], fb1[8];
+#pragma unroll
+  for (int q = 0; q < 16; ++q) dma1(0, 0, q);
+  DR_WAIT_VM(0);
+  DR_LDS_SYNC();
+#pragma unroll
+  for (int q = 0; q < 16; ++q) dma1(1, 1, q);
+#pragma unroll
+  for (int q = 0; q < 16; ++q) rd1(fa0, fb0, lds, 0, q);
+  // Per 64-column step t (stage t & 1): the first half's products with the
+  // second half's fragment reads between them; one barrier (step t + 1
+  // landed everywhere, every wave done with stage t & 1); then the second
+  // half's products with the DMA of step t + 2 into stage t & 1 and the reads
+  // of step t + 1's first half between them.  Products accumulate in the
+  // same order as a plain loop over 32-column halves.
   for (int t = 0; t < nk; ++t) {
+    const unsigned char* sa = lds + (t & 1) * kBStage;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      rd1(fa1, fb1, sa, 1, q);
+#pragma unroll
+      for (int m = 4 * q; m < 4 * q + 4; ++m) mma(m & 7, m >> 3, fa0, fb0);
+    }
     DR_WAIT_VM(0);
     DR_LDS_SYNC();
-    issue(t + 1, (t + 1) & 1);
-    const unsigned char* sa = lds + (t & 1) * kBStage;
-    const unsigned char* sbp = sa + kBPanel;
-    // both 32-column halves' fragments are read up front, so the second
-    // half's reads are in flight during the first half's MFMAs
-    u32x4 fa[2][8], fb[2][4];
+    const unsigned char* sn = lds + ((t + 1) & 1) * kBStage;
 #pragma unroll
-    for (int kh = 0; kh < 2; ++kh) {
-      const int seg = 4 * kh + lg;
+    for (int q = 0; q < 16; ++q) {
+      dma1(t + 2, t & 1, q);
+      rd1(fa0, fb0, sn, 0, q);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) fa[kh][i] = swz_read(sa + (wr * 8 + i) * 2048, lr, seg);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) fb[kh][j] = swz_read(sbp + (wc * 4 + j) * 2048, lr, seg);
+      for (int m = 4 * q; m < 4 * q + 4; ++m) mma(m & 7, m >> 3, fa1, fb1);
     }
-#pragma unroll
-    for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc[i][j] = mma_bf16(fa[kh][i], fb[kh][j], acc[i][j]);
   }
+  // the last products' results are read below: wait states after an MFMA
+  // that the compiler does not see inside the asm
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
 
   float* Kp = a.K + (long long)p * a.n * a.n;
+  if (a.vec4 && !diag && rowA0 + kBT <= a.n) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 8; ++j)
+        big_store_block_fast(Kp, a.n, rowA0 + wr * 128 + 16 * i, rowB0 + wc * 128 + 16 * j, acc[i][j], lane);
+  } else {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rowA0 + wr * 128 + 16 * i + 4 * lg + r;
-        const int col = rowB0 + wc * 64 + 16 * j + lr;
-        if (row < a.n && col < a.n && (!diag || col <= row)) Kp[(long long)row * a.n + col] = acc[i][j][r];
-      }
-  // the same values into the upper triangle, K[col][row] = C[row][col]
-  // (strictly below the diagonal for a diagonal tile): each 128-row half of
-  // the tile is staged transposed in LDS, then stored as whole rows of K
-  __syncthreads();   // every wave is past the k-loop's last LDS read
-  float* Tt = reinterpret_cast<float*>(lds);   // [256 columns][kBTLd]: Tt[c][r] = C[128 h + r][c]
-  for (int h = 0; h < 2; ++h) {
-    if (wr == h) {
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          *reinterpret_cast<f32x4*>(&Tt[(wc * 64 + 16 * j + lr) * kBTLd + 16 * i + 4 * lg]) = acc[i][j];
-    }
-    __syncthreads();
-    for (int e = tid; e < kBT * 32; e += 512) {   // 32 float4 per transposed row
-      const int c = e >> 5, r4 = 4 * (e & 31);
-      const int grow = rowB0 + c, gcol = rowA0 + 128 * h + r4;
-      if (grow >= a.n) continue;
-      const f32x4 v = *reinterpret_cast<const f32x4*>(&Tt[c * kBTLd + r4]);
-      float* dst = Kp + (long long)grow * a.n + gcol;
-      if (a.vec4 && gcol + 3 < a.n && (!diag || 128 * h + r4 > c)) {
-        *reinterpret_cast<f32x4*>(dst) = v;
-      } else {
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (gcol + q < a.n && (!diag || 128 * h + r4 + q > c)) dst[q] = v[q];
-      }
-    }
-    __syncthreads();
+      for (int j = 0; j < 8; ++j)
+        big_store_block_masked(Kp, a.n, diag, rowA0 + wr * 128 + 16 * i, rowB0 + wc * 128 + 16 * j, acc[i][j], lane);
   }
 }
 
@@ -700,7 +739,7 @@ dr_status gram_run(const GramPlan& g, const void* G, int64_t n, int64_t ldG, con
       int chunks = 0;
       for (int band = 0; 4 * band < b.T; ++band) chunks += ((4 * band + 4 < b.T ? 4 * band + 4 : b.T) + 7) / 8;
       b.vec4 = (n % 4 == 0) && aligned16(K);
-      hipLaunchKernelGGL(gram_big_kernel, dim3((chunks + 7) / 8 * 256, gp), dim3(512), 0, hs, b);
+      hipLaunchKernelGGL(gram_big_kernel, dim3((chunks + 7) / 8 * 256, gp), dim3(256), 0, hs, b);
       if ((st = launch_status()) != DR_OK) return st;
     } else if (g.small) {
       hipLaunchKernelGGL(gram_small_kernel, dim3(g.maxchunks, gp), dim3(kSmThreads), 0, hs, a,
