@@ -755,8 +755,6 @@ constexpr int S6_T = 256;                      // tile edge
 constexpr int S6_K = 64;                       // virtual columns per step
 constexpr int S6_PANEL = S6_T * S6_K * 2;      // bytes of one operand panel per step (32 KiB)
 constexpr int S6_STAGE = 2 * S6_PANEL;
-constexpr int S6_LDC = S6_T + 4;               // row stride (floats) of the half tile staged in LDS
-constexpr int S6_LDS = 2 * S6_STAGE > 128 * S6_LDC * 4 ? 2 * S6_STAGE : 128 * S6_LDC * 4;
 #ifndef DR_S6_MIN_ROUNDS
 #define DR_S6_MIN_ROUNDS 1
 #endif
@@ -806,124 +804,192 @@ __global__ __launch_bounds__(256) void lg_split_kernel(const float* L, long long
 
 // W: the width of the panels (the rank of the update): 256 (a pair) or 512
 // (four panels); skip: the tile columns left to the head update (the next
-// step's panels)
+// step's panels).  Four waves of 128 x 128 (one per SIMD) with the
+// accumulators pinned in AGPRs by in-place asm MFMAs; per 64-column step
+// the first half's products run with the second half's fragment reads
+// between them, then one barrier, then the second half's products with the
+// DMA of step s + 2 and the reads of step s + 1's first half between them.
+// At the end each 16 x 16 block goes through a 4 x 4 transpose inside each
+// quad of lanes (DPP), so lane 4 m + c holds four consecutive columns of one
+// row: C is read, reduced and written as float4 straight from registers.
 template <int W>
-__global__ __launch_bounds__(512) void lg_syrk6_kernel(const unsigned char* pl, float* L, long long ldL, int n, int k1,
-                                                       int skip, int ntiles, const LgCtl* ctl) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void lg_syrk6_kernel(const unsigned char* pl, float* L, long long ldL, int n, int k1, int skip, int ntiles,
+                     const LgCtl* ctl) {
   constexpr int SPP = W / S6_K;         // steps per plane pair
   constexpr int S6_STEPS = 6 * SPP;     // 24 or 48
   if (ctl->skip) return;
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[S6_LDS];
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * S6_STAGE];
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wr = w >> 2, wc = w & 3;   // 128-row half, 64-column quarter of the tile
-  const int lr = lane & 15, lg = lane >> 4;
+  const int wr = w >> 1, wc = w & 1;   // 128-row half of the tile's rows, of its columns
+  const int lr = lane & 15, lg = lane >> 4, qc = lane & 3, qm = lr >> 2;
   const int rows = n - k1;             // rows of the planes
   const long long planeB = (long long)n * W * 2;
-  int segs[4];
+  int segs[8];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) segs[u] = swz_seg_of_lane(lane, (w + 8 * u) & 1);
+  for (int u = 0; u < 8; ++u) segs[u] = swz_seg_of_lane(lane, (w + 4 * u) & 1);
   for (int qt = blockIdx.x; qt < ntiles; qt += gridDim.x) {
     int I, J;
     tile_pair(qt, I, J);
     const int rowA0 = S6_T * (I + skip), rowB0 = S6_T * (J + skip);   // plane rows (trailing rows from k1)
     const bool diag = I == J;
-    unsigned offA[4], offB[4];
+    unsigned offA[8], offB[8];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int r = 8 * (w + 8 * u) + (lane >> 3);
+    for (int u = 0; u < 8; ++u) {
+      const int r = 8 * (w + 4 * u) + (lane >> 3);
       offA[u] = rowA0 + r < rows ? (unsigned)(r * W * 2) : kOobOffset;
       offB[u] = rowB0 + r < rows ? (unsigned)(r * W * 2) : kOobOffset;
     }
-    auto issue = [&](int s, int st) {
+    // DMA q (0..15) of step s into stage st (q even: row panel, odd: column
+    // panel; half block w + 4 (q / 2)); steps past the last load zeros
+    auto dma1 = [&](int s, int st, int q) {
       const int t = s / SPP, c0 = S6_K * (s % SPP);
       const int pa = t == 2 || t == 4 ? 1 : (t == 5 ? 2 : 0);   // plane pairs 00 01 10 02 11 20
       const int pb = t == 1 || t == 4 ? 1 : (t == 3 ? 2 : 0);
-      const __amdgpu_buffer_rsrc_t ra = make_rsrc(pl + pa * planeB + (long long)rowA0 * W * 2, kOobOffset);
-      const __amdgpu_buffer_rsrc_t rb = make_rsrc(pl + pb * planeB + (long long)rowB0 * W * 2, kOobOffset);
+      const int u = q >> 1;
+      const unsigned cb = (unsigned)((c0 + segs[u] * 8) * 2);
       unsigned char* sb = lds + st * S6_STAGE;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const unsigned cb = (unsigned)((c0 + segs[u] * 8) * 2);
-        dma16<kAuxCached>(ra, sb + (w + 8 * u) * 1024, offA[u] == kOobOffset ? kOobOffset : offA[u] + cb);
-        dma16<kAuxCached>(rb, sb + S6_PANEL + (w + 8 * u) * 1024, offB[u] == kOobOffset ? kOobOffset : offB[u] + cb);
+      if (q & 1) {
+        const __amdgpu_buffer_rsrc_t rb = make_rsrc(pl + pb * planeB + (long long)rowB0 * W * 2, kOobOffset);
+        dma16<kAuxCached>(rb, sb + S6_PANEL + (w + 4 * u) * 1024,
+                          offB[u] == kOobOffset || s >= S6_STEPS ? kOobOffset : offB[u] + cb);
+      } else {
+        const __amdgpu_buffer_rsrc_t ra = make_rsrc(pl + pa * planeB + (long long)rowA0 * W * 2, kOobOffset);
+        dma16<kAuxCached>(ra, sb + (w + 4 * u) * 1024,
+                          offA[u] == kOobOffset || s >= S6_STEPS ? kOobOffset : offA[u] + cb);
       }
     };
-    f32x4 acc[8][4];
+    auto rd1 = [&](u32x4* fa, u32x4* fb, const unsigned char* sa, int kh, int q) {
+      const int seg = 4 * kh + lg;
+      if (q & 1) fb[q >> 1] = swz_read(sa + S6_PANEL + (wc * 8 + (q >> 1)) * 2048, lr, seg);
+      else fa[q >> 1] = swz_read(sa + (wr * 8 + (q >> 1)) * 2048, lr, seg);
+    };
+    f32x4 acc[8][8];
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    __syncthreads();   // the previous tile's last reads of the staging area are done
-    issue(0, 0);
+      for (int j = 0; j < 8; ++j) {
+        acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        // the zeros are in place before the prologue: the compiler does not
+        // see the MFMAs inside the asm, so it would not space a register
+        // write and the product that reads it apart
+        asm volatile("" : "+a"(acc[i][j]));
+      }
+    auto mma = [&](int i, int j, const u32x4* fa, const u32x4* fb) {
+      asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc[i][j]) : "v"(fa[i]), "v"(fb[j]));
+    };
+    u32x4 fa0[8], fb0[8], fa1[8], fb1[8];
+    __syncthreads();   // every wave is done with the ring (previous tile)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) dma1(0, 0, q);
+    DR_WAIT_VM(0);
+    DR_LDS_SYNC();
+#pragma unroll
+    for (int q = 0; q < 16; ++q) dma1(1, 1, q);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) rd1(fa0, fb0, lds, 0, q);
     for (int s = 0; s < S6_STEPS; ++s) {
+      const unsigned char* sa = lds + (s & 1) * S6_STAGE;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        rd1(fa1, fb1, sa, 1, q);
+#pragma unroll
+        for (int m = 4 * q; m < 4 * q + 4; ++m) mma(m & 7, m >> 3, fa0, fb0);
+      }
       DR_WAIT_VM(0);
       DR_LDS_SYNC();
-      if (s + 1 < S6_STEPS) issue(s + 1, (s + 1) & 1);
-      const unsigned char* sa = lds + (s & 1) * S6_STAGE;
-      const unsigned char* sbp = sa + S6_PANEL;
-      u32x4 fa[2][8], fb[2][4];
+      const unsigned char* sn = lds + ((s + 1) & 1) * S6_STAGE;
 #pragma unroll
-      for (int kh = 0; kh < 2; ++kh) {
-        const int seg = 4 * kh + lg;
+      for (int q = 0; q < 16; ++q) {
+        dma1(s + 2, s & 1, q);
+        rd1(fa0, fb0, sn, 0, q);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) fa[kh][i] = swz_read(sa + (wr * 8 + i) * 2048, lr, seg);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) fb[kh][j] = swz_read(sbp + (wc * 4 + j) * 2048, lr, seg);
+        for (int m = 4 * q; m < 4 * q + 4; ++m) mma(m & 7, m >> 3, fa1, fb1);
       }
-#pragma unroll
-      for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int i = 0; i < 8; ++i) acc[i][j] = mma_bf16(fa[kh][i], fb[kh][j], acc[i][j]);
     }
-    // C -= acc through LDS, one 128-row half at a time.  Wave w updates
-    // rows w + 8 u (u < RMW) of the half, lane l the four columns from 4 l;
-    // all RMW float4 of C are requested before the half is staged, so their
-    // latency passes under the staging.  Rows past n are skipped (a
-    // wave-uniform test); a column start past n loads column 0 instead
-    // (k1 and the tile origin are multiples of 4 and the row stride is n
-    // rounded up to 4, so a float4 that starts below n lies in its row) and
-    // stores nothing; on a diagonal tile only entries on or below the
-    // diagonal are written.
-    float* St = reinterpret_cast<float*>(lds);   // [128][S6_LDC]
-    constexpr int RMW = 128 / 8;
-    const int c4 = 4 * lane, gcol = k1 + rowB0 + c4;
-    const int gcl = gcol < n ? gcol : 0;
-    const bool colfull = gcol + 3 < n;
-    for (int h = 0; h < 2; ++h) {
-      __syncthreads();   // the ring's (or the previous half's) last LDS reads are done
-      const int row0 = k1 + rowA0 + 128 * h + w;   // wave-uniform
-      float* Lr = L + (long long)row0 * ldL;
-      f32x4 cv[RMW];
+    // the last products' results are read below: wait states after an MFMA
+    // that the compiler does not see inside the asm
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+
+    // C -= acc.  Block (i, j) after the quad transpose: lane 4 m + c holds
+    // row 16 i + 4 (l / 16) + c, columns 16 j + 4 m .. + 3 of the wave's
+    // quarter.  Rows past n are skipped; a column start past n reads column 0
+    // instead (k1 and the tile origin are multiples of 4 and the row stride
+    // is n rounded up to 4, so a float4 that starts below n lies in its row)
+    // and writes nothing; on a diagonal tile only entries on or below the
+    // diagonal are written.  Two block rows at a time, software-pipelined:
+    // the next pair's sixteen float4 of C are requested before the current
+    // pair is reduced and written.
+    const int rq = k1 + rowA0 + wr * 128 + 4 * lg + qc;   // + 16 i
+    const int cq = k1 + rowB0 + wc * 128 + 4 * qm;        // + 16 j
+    const bool fast_tile_now = !diag && k1 + rowA0 + S6_T <= n && k1 + rowB0 + S6_T <= n;
+    auto load_c = [&](f32x4 (&cv)[2][8], int ib) {
 #pragma unroll
-      for (int u = 0; u < RMW; ++u)
-        cv[u] = row0 + 8 * u < n ? *reinterpret_cast<const f32x4*>(Lr + 8 * u * ldL + gcl) : f32x4{0.f, 0.f, 0.f, 0.f};
-      if (wr == h) {
+      for (int di = 0; di < 2; ++di)
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) St[(16 * i + 4 * lg + q) * S6_LDC + wc * 64 + 16 * j + lr] = acc[i][j][q];
-      }
-      __syncthreads();
-#pragma unroll
-      for (int u = 0; u < RMW; ++u) {
-        if (row0 + 8 * u >= n) continue;
-        const int rr = w + 8 * u;
-        const f32x4 v = cv[u] - *reinterpret_cast<const f32x4*>(&St[rr * S6_LDC + c4]);
-        float* dst = Lr + 8 * u * ldL + gcol;
-        if (colfull && (!diag || 128 * h + rr >= c4 + 3)) {
-          *reinterpret_cast<f32x4*>(dst) = v;
-        } else {
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-            if (gcol + q < n && (!diag || 128 * h + rr >= c4 + q)) dst[q] = v[q];
+        for (int j = 0; j < 8; ++j) {
+          const int row = rq + 16 * (ib + di), col = cq + 16 * j;
+          // (a row past n reads row n - 1 instead and writes nothing: the
+          // loads stay unconditional, so their waits stay counted)
+          cv[di][j] = *reinterpret_cast<const f32x4*>(L + (long long)(row < n ? row : n - 1) * ldL + (col < n ? col : 0));
         }
-      }
-    }
+    };
+    auto reduce_c = [&](const f32x4 (&cv)[2][8], int ib, auto fast_tile) {
+      constexpr bool fast = decltype(fast_tile)::value;
+#pragma unroll
+      for (int di = 0; di < 2; ++di)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const f32x4 v = acc[ib + di][j];
+          float x0 = v[0], x1 = v[1], x2 = v[2], x3 = v[3];
+          {  // exchange across bit 0 of the quad lane
+            const float s01 = (qc & 1) ? x0 : x1, s23 = (qc & 1) ? x2 : x3;
+            const float r01 = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s01), 0xB1, 0xF, 0xF, false));
+            const float r23 = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s23), 0xB1, 0xF, 0xF, false));
+            if (qc & 1) { x0 = r01; x2 = r23; } else { x1 = r01; x3 = r23; }
+          }
+          {  // exchange across bit 1
+            const float s02 = (qc & 2) ? x0 : x2, s13 = (qc & 2) ? x1 : x3;
+            const float r02 = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s02), 0x4E, 0xF, 0xF, false));
+            const float r13 = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s13), 0x4E, 0xF, 0xF, false));
+            if (qc & 2) { x0 = r02; x1 = r13; } else { x2 = r02; x3 = r13; }
+          }
+          const int row = rq + 16 * (ib + di), col = cq + 16 * j;
+          const f32x4 r = cv[di][j] - f32x4{x0, x1, x2, x3};
+          float* dst = L + (long long)row * ldL + col;
+          if (fast) {
+            *reinterpret_cast<f32x4*>(dst) = r;
+          } else if (row < n) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (col + e < n && (!diag || col + e <= row)) dst[e] = r[e];
+          }
+        }
+    };
+    // (the empty asm statements keep the compiler from regrouping the loads
+    // and stores of different pairs)
+    auto pipeline = [&](auto fast_tile) {
+      f32x4 cva[2][8], cvb[2][8];
+      load_c(cva, 0);
+      load_c(cvb, 2);
+      asm volatile("" ::: "memory");
+      reduce_c(cva, 0, fast_tile);
+      asm volatile("" ::: "memory");
+      load_c(cva, 4);
+      asm volatile("" ::: "memory");
+      reduce_c(cvb, 2, fast_tile);
+      asm volatile("" ::: "memory");
+      load_c(cvb, 6);
+      asm volatile("" ::: "memory");
+      reduce_c(cva, 4, fast_tile);
+      asm volatile("" ::: "memory");
+      reduce_c(cvb, 6, fast_tile);
+    };
+    if (fast_tile_now)
+      pipeline(std::true_type{});
+    else
+      pipeline(std::false_type{});
   }
 }
 
@@ -1552,12 +1618,12 @@ static dr_status span_large_groups(const float* K, const float* s, const float* 
         if (W == 4 * NB) {
           hipLaunchKernelGGL(lg_split_kernel<4 * NB>, dim3((rest * 64 + 255) / 256), dim3(256), 0, hs, L, ldL, n, k, k1,
                              pl, ctl);
-          hipLaunchKernelGGL(lg_syrk6_kernel<4 * NB>, dim3(n6 < slots6 ? n6 : slots6), dim3(512), 0, hs,
+          hipLaunchKernelGGL(lg_syrk6_kernel<4 * NB>, dim3(n6 < slots6 ? n6 : slots6), dim3(256), 0, hs,
                              reinterpret_cast<const unsigned char*>(pl), L, ldL, n, k1, skip, n6, ctl);
         } else {
           hipLaunchKernelGGL(lg_split_kernel<2 * NB>, dim3((rest * 32 + 255) / 256), dim3(256), 0, hs, L, ldL, n, k, k1,
                              pl, ctl);
-          hipLaunchKernelGGL(lg_syrk6_kernel<2 * NB>, dim3(n6 < slots6 ? n6 : slots6), dim3(512), 0, hs,
+          hipLaunchKernelGGL(lg_syrk6_kernel<2 * NB>, dim3(n6 < slots6 ? n6 : slots6), dim3(256), 0, hs,
                              reinterpret_cast<const unsigned char*>(pl), L, ldL, n, k1, skip, n6, ctl);
         }
       } else {
