@@ -742,14 +742,11 @@ __global__ __launch_bounds__(256, 2) void lg_syrk_kernel(float* L, long long ldL
 //                    ..., for the pair s / (W/64).
 // The tile machinery is that of the large-n Gram kernel: 256 x 256 tiles
 // of the trailing matrix right of the head's tile columns (tiles
-// I >= J >= skip in units of 256 from the trailing matrix's first row), eight
-// waves of 128 x 64 fp32 accumulators, a two-stage buffer -> LDS DMA ring
-// of 64-column steps in the conflict-free operand layout.  At the end the
-// tile goes through LDS in two 128-row halves (row-major, 260-float rows:
-// the accumulator writes of a wave fall on distinct banks) and each thread
-// updates 16 float4 of C: read (requested before the half is staged),
-// subtract, write (on a diagonal tile only entries on or below the
-// diagonal).
+// I >= J >= skip in units of 256 from the trailing matrix's first row), four
+// waves of 128 x 128 fp32 accumulators, a two-stage buffer -> LDS DMA ring
+// of 64-column steps in the conflict-free operand layout.  At the end C is
+// read, reduced and written as float4 straight from registers (on a
+// diagonal tile only entries on or below the diagonal).
 
 constexpr int S6_T = 256;                      // tile edge
 constexpr int S6_K = 64;                       // virtual columns per step

@@ -23,12 +23,13 @@
 //   gram_big_kernel    : one 256x256 tile of K_p per workgroup over all of
 //                        the group's columns (no split): 64-column steps
 //                        stream into a two-stage LDS ring by buffer->LDS DMA,
-//                        eight waves each hold a 128x64 fp32 accumulator
-//                        (bf16 16x16x32 MFMA); lower-triangle tiles only,
-//                        scheduled in 4x8-tile chunks, one per XCD at a time.
-//                        Each tile is also stored transposed into the upper
-//                        triangle (through LDS, whole rows of K), so K is
-//                        exactly symmetric without a second pass.
+//                        four waves (one per SIMD) each hold a 128x128 fp32
+//                        accumulator in AGPRs (bf16 16x16x32 MFMA); lower-
+//                        triangle tiles only, scheduled in 4x8-tile chunks,
+//                        one per XCD at a time.  Each tile goes out from
+//                        registers in non-temporal float4 stores, also
+//                        transposed into the upper triangle, so K is exactly
+//                        symmetric without a second pass.
 // Small fp32 problems (n + 1 <= 128 rows: the per-step batches):
 //   gram_small_kernel  : one workgroup per 128-column chunk of a group forms
 //                        the chunk of gbar from the target rows (fp64 sum /
