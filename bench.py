@@ -168,6 +168,13 @@ def _roofline(kernel, bound, work, ms, peak, unit, measured_peak=None, traffic=N
     return r
 
 
+def _gram_f32_flops(n, m, ktot):
+    """Algorithmic flops of dr_gram over ktot columns: the lower triangle of
+    K = G G^T with its diagonal, s = G gbar, t2 = |gbar|^2 and the target
+    mean of m rows."""
+    return (n * (n + 1) + 2 * n + 2 + m) * float(ktot)
+
+
 def _sketch_bytes(layers, lens, N, ktot):
     """Algorithmic bytes of one sketch call: the valid tokens' x and dy rows,
     the projectors and the fp32 sketch output (its column range)."""
@@ -271,9 +278,13 @@ def run_llama(args, api, _lib, workloads, dev, peaks):
             "sketch_packed_reduce_kernel)", "hbm", by, avg_blk, HBM_PEAK_GBS, "GB/s",
             measured_peak=peaks.get("hbm_read_GBs") if peaks else None, traffic=traffic,
             algorithmic_bytes=by, avg_launch_ms=avg_blk, timed_calls=int(blk_ms.size)),
-        "gram_roofline": _roofline("dr_gram (fp32 rows: gram_tile_kernel + reduce + target mean + scores)", "hbm",
-                                   N * ktot * 4.0, stage["gram"], HBM_PEAK_GBS, "GB/s",
-                                   algorithmic_bytes=N * ktot * 4.0),
+        # fp32 rows, (n(n+1) + 2n + 2 + m) kappa flops on 4 (n + m) kappa bytes:
+        # about 61 flops per byte, above the fp32 MFMA ridge (157.3 / 8), so
+        # the Gram is priced against the fp32 MFMA peak
+        "gram_roofline": _roofline("dr_gram (fp32 rows: gram_tile_kernel + reduce + target mean + scores)", "mfma",
+                                   _gram_f32_flops(n, m, ktot), stage["gram"], F32_MFMA_PEAK_TFLOPS, "TFLOP/s",
+                                   measured_peak=peaks.get("fp32_mfma_TFLOPs") if peaks else None,
+                                   algorithmic_flops=_gram_f32_flops(n, m, ktot), algorithmic_bytes=N * ktot * 4.0),
         "span_info": int(info[0]),
     }
     return res, dict(blocks=blocks, lens=lens, S=S, K=K, s=s, t2=t2, w=w, idx=idx, u=u, n=n, m=m, k_top=k_top,
@@ -317,8 +328,9 @@ def run_layerwise(api, _lib, st, dev):
         "nonzero_info_groups": bad,
         "span_roofline": _roofline("dr_project_span, 224 groups at n = 256 (span_small_kernel, one workgroup per "
                                    "group)", "hbm", kb, span_ms, HBM_PEAK_GBS, "GB/s", algorithmic_bytes=kb),
-        "gram_roofline": _roofline("dr_gram, 224 groups (fp32 rows)", "hbm", (st["n"] + st["m"]) * ktot * 4.0,
-                                   gram_ms, HBM_PEAK_GBS, "GB/s", algorithmic_bytes=(st["n"] + st["m"]) * ktot * 4.0),
+        "gram_roofline": _roofline("dr_gram, 224 groups (fp32 rows)", "mfma", _gram_f32_flops(n, m, ktot), gram_ms,
+                                   F32_MFMA_PEAK_TFLOPS, "TFLOP/s", algorithmic_flops=_gram_f32_flops(n, m, ktot),
+                                   algorithmic_bytes=(st["n"] + st["m"]) * ktot * 4.0),
     }
 
 

@@ -147,33 +147,41 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_kernel(GramArgs a) {
       const bool cok = c < c1;
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
-        va[b][v] = (okA[b] && cok) ? *reinterpret_cast<const u32x4*>(baseA[b] + c * E::ES)
-                                   : u32x4{0u, 0u, 0u, 0u};
-        vb[b][v] = (okB[b] && cok) ? *reinterpret_cast<const u32x4*>(baseB[b] + c * E::ES)
-                                   : u32x4{0u, 0u, 0u, 0u};
+        // unconditional loads (an entry outside the problem reads the first
+        // 16 bytes of the target mean instead, which every call has: G may
+        // be empty, and then null; the value is then zeroed), so that the
+        // compiler's waits count the loads in flight
+        const unsigned char* dummy = reinterpret_cast<const unsigned char*>(a.gbar);
+        const bool ea = okA[b] && cok, eb = okB[b] && cok;
+        const u32x4 xa = *reinterpret_cast<const u32x4*>(ea ? baseA[b] + c * E::ES : dummy);
+        const u32x4 xb = *reinterpret_cast<const u32x4*>(eb ? baseB[b] + c * E::ES : dummy);
+        va[b][v] = ea ? xa : u32x4{0u, 0u, 0u, 0u};
+        vb[b][v] = eb ? xb : u32x4{0u, 0u, 0u, 0u};
       }
     }
   };
 
-  u32x4 va[2][NV], vb[2][NV], na[2][NV], nb[2][NV];
-  load(c0, va, vb);
-  for (long long cs = c0; cs < c1; cs += STEP) {
-    const bool more = cs + STEP < c1;
-    if (more) load(cs + STEP, na, nb);
+  // DEPTH steps of loads in flight: the operands come from L2 straight
+  // into registers, so their latency is what the products wait for; loads
+  // past the chunk read zeros (no memory access), whose products add 0
+  constexpr int DEPTH = 3;
+  u32x4 ba[DEPTH][2][NV], bb[DEPTH][2][NV];
 #pragma unroll
-    for (int v = 0; v < NV; ++v)
+  for (int d = 0; d < DEPTH - 1; ++d) load(c0 + (long long)d * STEP, ba[d], bb[d]);
+  for (long long cs = c0; cs < c1; cs += DEPTH * STEP) {
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+    for (int d = 0; d < DEPTH; ++d) {
+      load(cs + (long long)(d + DEPTH - 1) * STEP, ba[(d + DEPTH - 1) % DEPTH], bb[(d + DEPTH - 1) % DEPTH]);
+      // the loads go out before this step's products (the scheduler would
+      // otherwise move them next to their uses)
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mma_v<BF16>(va[i][v], vb[j][v], acc[i][j]);
-    if (more) {
+      for (int v = 0; v < NV; ++v)
 #pragma unroll
-      for (int b = 0; b < 2; ++b)
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int v = 0; v < NV; ++v) {
-          va[b][v] = na[b][v];
-          vb[b][v] = nb[b][v];
-        }
+          for (int j = 0; j < 2; ++j) acc[i][j] = mma_v<BF16>(ba[d][i][v], bb[d][j][v], acc[i][j]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
