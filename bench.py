@@ -281,7 +281,7 @@ def run_llama(args, api, _lib, workloads, dev, peaks):
         # fp32 rows, (n(n+1) + 2n + 2 + m) kappa flops on 4 (n + m) kappa bytes:
         # about 61 flops per byte, above the fp32 MFMA ridge (157.3 / 8), so
         # the Gram is priced against the fp32 MFMA peak
-        "gram_roofline": _roofline("dr_gram (fp32 rows: gram_tile_kernel + reduce + target mean + scores)", "mfma",
+        "gram_roofline": _roofline("dr_gram (fp32 rows: gram_tile_lds_kernel + reduce + target mean)", "mfma",
                                    _gram_f32_flops(n, m, ktot), stage["gram"], F32_MFMA_PEAK_TFLOPS, "TFLOP/s",
                                    measured_peak=peaks.get("fp32_mfma_TFLOPs") if peaks else None,
                                    algorithmic_flops=_gram_f32_flops(n, m, ktot), algorithmic_bytes=N * ktot * 4.0),

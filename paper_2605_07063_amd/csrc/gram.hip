@@ -7,10 +7,13 @@
 //
 // Kernels
 //   target_mean_kernel : gbar in fp32 (fp64 sum over the m rows).
-//   gram_tile_kernel   : one 64x64 tile of K_p over one chunk of the group's
-//                        columns (lower-triangle tile pairs only), on MFMA
-//                        (bf16 16x16x32 or fp32 16x16x4, fp32 accumulate).
-//                        Operands stream from memory straight into registers.
+//   gram_tile_kernel   : bf16 rows: one 64x64 tile of K_p over one chunk of
+//                        the group's columns (lower-triangle tile pairs only),
+//                        bf16 16x16x32 MFMA, fp32 accumulate; operands stream
+//                        from memory straight into registers.
+//   gram_tile_lds_kernel : fp32 rows, the same tiles and chunks on fp32
+//                        16x16x4 MFMA, the workgroup's rows staged once per
+//                        step through a three-stage LDS ring.
 //   gram_reduce_kernel : sums the chunk partials of a tile in chunk order and
 //                        writes the lower triangle and its mirror, so K is
 //                        exactly symmetric.  For fp32 sketches the target
@@ -195,6 +198,121 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_kernel(GramArgs a) {
         out[(wr * 32 + i * 16 + lg * 4 + r) * kTile + wc * 32 + j * 16 + lr] = acc[i][j][r];
 }
 
+
+// fp32 rows, n + 1 > 128: the same 64x64 tile pairs and chunk partials as
+// gram_tile_kernel, with the operands staged through LDS: per step of 32
+// columns the workgroup's 64 + 64 rows (16 KB) are loaded once into
+// registers (each thread 4 segments of 16 bytes), written to a three-stage
+// LDS ring in the conflict-free operand layout, and read by the four waves
+// as fp32 MFMA fragments.  Loads run two steps ahead of their LDS writes,
+// and the LDS writes one step ahead of the products.
+constexpr int kLS = 32;                          // fp32 columns per step (128-byte rows)
+constexpr int kLNS = 3;                          // ring stages
+constexpr int kLStage = 2 * kTile * kLS * 4;     // 64 A rows + 64 B rows
+
+__global__ __launch_bounds__(kThreads, 2) void gram_tile_lds_kernel(GramArgs a) {
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[kLNS * kLStage];
+  const int chunk = blockIdx.x, q = blockIdx.y, p = blockIdx.z;
+  const long long g0 = a.goff[p], g1 = a.goff[p + 1];
+  const long long c0 = g0 + (long long)chunk * a.CK;
+  if (c0 >= g1) return;
+  const long long c1 = c0 + a.CK < g1 ? c0 + a.CK : g1;
+  const int nsteps = (int)((c1 - c0 + kLS - 1) / kLS);
+  int I, J;
+  pair_to_tiles(q, I, J);
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int wr = w >> 1, wc = w & 1;
+  // loader: segment e = tid + 256 u of a stage is row e / 8 (A rows 0..63,
+  // B rows 64..127), segment e % 8; row n of the augmented problem is the
+  // target mean.  An entry outside the problem reads the target mean's
+  // first 16 bytes instead (every call has them; G may be empty) and is
+  // zeroed, so the loads are unconditional and their waits counted.
+  const unsigned char* dummy = reinterpret_cast<const unsigned char*>(a.gbar);
+  const unsigned char* src[4];
+  bool rok[4];
+  int sseg[4];
+  unsigned loff[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int e = tid + kThreads * u, R = e >> 3, s = e & 7;
+    const int grow = R < kTile ? I * kTile + R : J * kTile + (R - kTile);
+    rok[u] = grow < a.rows;
+    src[u] = grow < a.n ? a.G + (long long)grow * a.ldG * 4 : dummy;   // row n: the target mean (by column)
+    sseg[u] = s;
+    loff[u] = (unsigned)(R * 128 + ((s ^ ((R >> 1) & 7)) * 16));
+  }
+  auto seg_ok = [&](int t, int u) { return rok[u] && c0 + (long long)t * kLS + sseg[u] * 4 < c1; };
+  // the zeroing happens at the LDS write, so nothing waits for the loads
+  // until then
+  auto gload = [&](int t, u32x4 (&v)[4]) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const long long c = c0 + (long long)t * kLS + sseg[u] * 4;
+      v[u] = *reinterpret_cast<const u32x4*>(seg_ok(t, u) ? src[u] + c * 4 : dummy);
+    }
+  };
+  auto lstore = [&](int t, const u32x4 (&v)[4]) {
+    unsigned char* sb = lds + (t % kLNS) * kLStage;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      *reinterpret_cast<u32x4*>(sb + loff[u]) = seg_ok(t, u) ? v[u] : u32x4{0u, 0u, 0u, 0u};
+  };
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](int t) {
+    const unsigned char* sb = lds + (t % kLNS) * kLStage;
+#pragma unroll
+    for (int kh = 0; kh < 2; ++kh) {
+      u32x4 fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) fa[i] = swz_read(sb + (wr * 32 + 16 * i) * 128, lr, 4 * kh + lg);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) fb[j] = swz_read(sb + (kTile + wc * 32 + 16 * j) * 128, lr, 4 * kh + lg);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = mma_v<false>(fa[i], fb[j], acc[i][j]);
+    }
+  };
+  u32x4 va[4], vb[4];
+  gload(0, va);
+  gload(1, vb);
+  lstore(0, va);
+  lstore(1, vb);
+  gload(2, va);
+  gload(3, vb);
+  __syncthreads();
+  // step t: products from stage t % 3; the data of step t + 2 (loaded two
+  // steps ago) into stage (t + 2) % 3, last read at step t - 1; the loads of
+  // step t + 4; one barrier
+  for (int t = 0; t < nsteps; t += 2) {
+    compute(t);
+    lstore(t + 2, va);
+    __builtin_amdgcn_sched_barrier(0);
+    gload(t + 4, va);
+    __builtin_amdgcn_sched_barrier(0);
+    DR_LDS_SYNC();
+    compute(t + 1);   // past the last step its stage holds zeros: the products add 0
+    lstore(t + 3, vb);
+    __builtin_amdgcn_sched_barrier(0);
+    gload(t + 5, vb);
+    __builtin_amdgcn_sched_barrier(0);
+    DR_LDS_SYNC();
+  }
+
+  float* out = a.partial + (((long long)p * a.pairs + q) * a.maxchunks + chunk) * (kTile * kTile);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        out[(wr * 32 + i * 16 + lg * 4 + r) * kTile + wc * 32 + j * 16 + lr] = acc[i][j][r];
+}
 
 // ---------------------------------------------------------------- small fp32
 
@@ -763,7 +881,7 @@ dr_status gram_run(const GramPlan& g, const void* G, int64_t n, int64_t ldG, con
       if (bf)
         hipLaunchKernelGGL(gram_tile_kernel<true>, grid, dim3(kThreads), 0, hs, a);
       else
-        hipLaunchKernelGGL(gram_tile_kernel<false>, grid, dim3(kThreads), 0, hs, a);
+        hipLaunchKernelGGL(gram_tile_lds_kernel, grid, dim3(kThreads), 0, hs, a);
       if ((st = launch_status()) != DR_OK) return st;
       hipLaunchKernelGGL(gram_reduce_kernel, dim3(g.pairs, gp, kTile * kTile / kThreads), dim3(kThreads), 0, hs, a,
                          K, s, t2, (long long)p0);
