@@ -31,6 +31,7 @@ def rand(shape, seed, dtype=torch.float32, scale=1.0):
     (1, 64, None, torch.float32),
     (64, 2048 + 512 + 68, [0, 512, 512, 2628], torch.float32),   # one-pass small path: groups, one empty, ragged chunk
     (127, 8192, None, torch.float32),                 # largest n of the one-pass path
+    (150, 1068, [0, 604, 1068], torch.float32),       # LDS-staged tiles: ragged 32-column steps in both groups
 ])
 def test_gram_matches_oracle(n, kappa, goff, dtype):
     G = rand((n, kappa), 10 + n, dtype)
