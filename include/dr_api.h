@@ -12,9 +12,10 @@
  * - The caller owns every buffer, including the workspace whose size the
  *   matching *_workspace_size query returns.  The library allocates no
  *   device memory and keeps no data between calls.  The one runtime object
- *   it keeps: dr_project_span with n > 256 runs its look-ahead on one
- *   auxiliary stream (default priority) and two events per device, created
- *   by the first such call on that device and kept until the process ends.
+ *   it keeps: dr_project_span with n > 256 runs its look-ahead on two
+ *   auxiliary streams (default priority) and five events per device,
+ *   created by the first such call on that device and kept until the
+ *   process ends.
  * - `stream` is a hipStream_t (NULL = the default stream).  Calls only
  *   enqueue work.  The returned dr_status covers argument validation and
  *   launch errors; every argument is validated before the first HIP call,
