@@ -48,6 +48,7 @@
 // No atomics: results are deterministic.
 
 #include <mutex>
+#include <type_traits>
 
 #include "common.h"
 
@@ -263,19 +264,23 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_lds_kernel(GramArgs a) 
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  auto compute = [&](int t) {
-    const unsigned char* sb = lds + (t % kLNS) * kLStage;
+  // products of the wave's first NA 16-row A blocks with its two B blocks
+  auto compute = [&](int t, auto na) {
+    constexpr int NA = decltype(na)::value;
+    if constexpr (NA > 0) {
+      const unsigned char* sb = lds + (t % kLNS) * kLStage;
 #pragma unroll
-    for (int kh = 0; kh < 2; ++kh) {
-      u32x4 fa[2], fb[2];
+      for (int kh = 0; kh < 2; ++kh) {
+        u32x4 fa[NA], fb[2];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) fa[i] = swz_read(sb + (wr * 32 + 16 * i) * 128, lr, 4 * kh + lg);
+        for (int i = 0; i < NA; ++i) fa[i] = swz_read(sb + (wr * 32 + 16 * i) * 128, lr, 4 * kh + lg);
 #pragma unroll
-      for (int j = 0; j < 2; ++j) fb[j] = swz_read(sb + (kTile + wc * 32 + 16 * j) * 128, lr, 4 * kh + lg);
+        for (int j = 0; j < 2; ++j) fb[j] = swz_read(sb + (kTile + wc * 32 + 16 * j) * 128, lr, 4 * kh + lg);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < NA; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mma_v<false>(fa[i], fb[j], acc[i][j]);
+          for (int j = 0; j < 2; ++j) acc[i][j] = mma_v<false>(fa[i], fb[j], acc[i][j]);
+      }
     }
   };
   u32x4 va[4], vb[4];
@@ -289,20 +294,34 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_lds_kernel(GramArgs a) 
   // step t: products from stage t % 3; the data of step t + 2 (loaded two
   // steps ago) into stage (t + 2) % 3, last read at step t - 1; the loads of
   // step t + 4; one barrier
-  for (int t = 0; t < nsteps; t += 2) {
-    compute(t);
-    lstore(t + 2, va);
-    __builtin_amdgcn_sched_barrier(0);
-    gload(t + 4, va);
-    __builtin_amdgcn_sched_barrier(0);
-    DR_LDS_SYNC();
-    compute(t + 1);   // past the last step its stage holds zeros: the products add 0
-    lstore(t + 3, vb);
-    __builtin_amdgcn_sched_barrier(0);
-    gload(t + 5, vb);
-    __builtin_amdgcn_sched_barrier(0);
-    DR_LDS_SYNC();
-  }
+  auto run = [&](auto na) {
+    for (int t = 0; t < nsteps; t += 2) {
+      compute(t, na);
+      lstore(t + 2, va);
+      __builtin_amdgcn_sched_barrier(0);
+      gload(t + 4, va);
+      __builtin_amdgcn_sched_barrier(0);
+      DR_LDS_SYNC();
+      compute(t + 1, na);   // past the last step its stage holds zeros: the products add 0
+      lstore(t + 3, vb);
+      __builtin_amdgcn_sched_barrier(0);
+      gload(t + 5, vb);
+      __builtin_amdgcn_sched_barrier(0);
+      DR_LDS_SYNC();
+    }
+  };
+  // A blocks wholly outside the problem take no products (I >= J, so these
+  // are the rows past n of the last tile row, which for n + 1 = 64 t + 1 holds
+  // the target mean alone); their accumulators stay zero.  The count is
+  // uniform over the wave, so each wave runs one variant of the loop.
+  const int arow = I * kTile + wr * 32;
+  const int na = (arow < a.rows) + (arow + 16 < a.rows);
+  if (na == 2)
+    run(std::integral_constant<int, 2>{});
+  else if (na == 1)
+    run(std::integral_constant<int, 1>{});
+  else
+    run(std::integral_constant<int, 0>{});
 
   float* out = a.partial + (((long long)p * a.pairs + q) * a.maxchunks + chunk) * (kTile * kTile);
 #pragma unroll
