@@ -264,22 +264,24 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_lds_kernel(GramArgs a) 
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // products of the wave's first NA 16-row A blocks with its two B blocks
-  auto compute = [&](int t, auto na) {
-    constexpr int NA = decltype(na)::value;
-    if constexpr (NA > 0) {
+  // products of the wave's 16 x 16 blocks (i, j) whose bit i * 2 + j is set
+  // in M (A block i against B block j)
+  auto compute = [&](int t, auto mask) {
+    constexpr int M = decltype(mask)::value;
+    constexpr bool ra0 = (M & 3) != 0, ra1 = (M & 12) != 0, rb0 = (M & 5) != 0, rb1 = (M & 10) != 0;
+    if constexpr (M != 0) {
       const unsigned char* sb = lds + (t % kLNS) * kLStage;
 #pragma unroll
       for (int kh = 0; kh < 2; ++kh) {
-        u32x4 fa[NA], fb[2];
-#pragma unroll
-        for (int i = 0; i < NA; ++i) fa[i] = swz_read(sb + (wr * 32 + 16 * i) * 128, lr, 4 * kh + lg);
-#pragma unroll
-        for (int j = 0; j < 2; ++j) fb[j] = swz_read(sb + (kTile + wc * 32 + 16 * j) * 128, lr, 4 * kh + lg);
-#pragma unroll
-        for (int i = 0; i < NA; ++i)
-#pragma unroll
-          for (int j = 0; j < 2; ++j) acc[i][j] = mma_v<false>(fa[i], fb[j], acc[i][j]);
+        u32x4 fa[2], fb[2];
+        if constexpr (ra0) fa[0] = swz_read(sb + (wr * 32) * 128, lr, 4 * kh + lg);
+        if constexpr (ra1) fa[1] = swz_read(sb + (wr * 32 + 16) * 128, lr, 4 * kh + lg);
+        if constexpr (rb0) fb[0] = swz_read(sb + (kTile + wc * 32) * 128, lr, 4 * kh + lg);
+        if constexpr (rb1) fb[1] = swz_read(sb + (kTile + wc * 32 + 16) * 128, lr, 4 * kh + lg);
+        if constexpr ((M & 1) != 0) acc[0][0] = mma_v<false>(fa[0], fb[0], acc[0][0]);
+        if constexpr ((M & 2) != 0) acc[0][1] = mma_v<false>(fa[0], fb[1], acc[0][1]);
+        if constexpr ((M & 4) != 0) acc[1][0] = mma_v<false>(fa[1], fb[0], acc[1][0]);
+        if constexpr ((M & 8) != 0) acc[1][1] = mma_v<false>(fa[1], fb[1], acc[1][1]);
       }
     }
   };
@@ -294,15 +296,15 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_lds_kernel(GramArgs a) 
   // step t: products from stage t % 3; the data of step t + 2 (loaded two
   // steps ago) into stage (t + 2) % 3, last read at step t - 1; the loads of
   // step t + 4; one barrier
-  auto run = [&](auto na) {
+  auto run = [&](auto mask) {
     for (int t = 0; t < nsteps; t += 2) {
-      compute(t, na);
+      compute(t, mask);
       lstore(t + 2, va);
       __builtin_amdgcn_sched_barrier(0);
       gload(t + 4, va);
       __builtin_amdgcn_sched_barrier(0);
       DR_LDS_SYNC();
-      compute(t + 1, na);   // past the last step its stage holds zeros: the products add 0
+      compute(t + 1, mask);   // past the last step its stage holds zeros: the products add 0
       lstore(t + 3, vb);
       __builtin_amdgcn_sched_barrier(0);
       gload(t + 5, vb);
@@ -310,18 +312,30 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_lds_kernel(GramArgs a) 
       DR_LDS_SYNC();
     }
   };
-  // A blocks wholly outside the problem take no products (I >= J, so these
-  // are the rows past n of the last tile row, which for n + 1 = 64 t + 1 holds
-  // the target mean alone); their accumulators stay zero.  The count is
-  // uniform over the wave, so each wave runs one variant of the loop.
-  const int arow = I * kTile + wr * 32;
-  const int na = (arow < a.rows) + (arow + 16 < a.rows);
-  if (na == 2)
-    run(std::integral_constant<int, 2>{});
-  else if (na == 1)
-    run(std::integral_constant<int, 1>{});
-  else
+  // Blocks the reduction never reads take no products and keep zero
+  // accumulators: A rows wholly past the last row (I >= J, so these are the
+  // last tile row's, which for n + 1 = 64 t + 1 holds the target mean alone),
+  // and on a diagonal tile the blocks wholly above the diagonal.  The mask is
+  // uniform over the wave; it is rounded up to the smallest of five loop
+  // variants that contains it (extra products are harmless).
+  int live = 0;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int rb = I * kTile + wr * 32 + 16 * i, cb = J * kTile + wc * 32 + 16 * j;
+      if (rb < a.rows && cb <= rb + 15) live |= 1 << (i * 2 + j);
+    }
+  if (live == 0)
     run(std::integral_constant<int, 0>{});
+  else if ((live & ~1) == 0)
+    run(std::integral_constant<int, 1>{});    // (0, 0)
+  else if ((live & ~3) == 0)
+    run(std::integral_constant<int, 3>{});    // A block 0 only
+  else if ((live & ~13) == 0)
+    run(std::integral_constant<int, 13>{});   // lower triangle of the wave's 2 x 2
+  else
+    run(std::integral_constant<int, 15>{});
 
   float* out = a.partial + (((long long)p * a.pairs + q) * a.maxchunks + chunk) * (kTile * kTile);
 #pragma unroll
