@@ -13,15 +13,19 @@
 //                        from memory straight into registers.
 //   gram_tile_lds_kernel : fp32 rows, the same tiles and chunks on fp32
 //                        16x16x4 MFMA, the workgroup's rows staged once per
-//                        step through a three-stage LDS ring.
+//                        step through a three-stage LDS ring.  A diagonal
+//                        tile stages its rows once plus the target mean, and
+//                        its wave above the diagonal forms s_p for the
+//                        tile's rows (tile 0 also t2_p), so the same pass
+//                        yields them.
 //   gram_reduce_kernel : sums the chunk partials of a tile in chunk order and
 //                        writes the lower triangle and its mirror, so K is
-//                        exactly symmetric.  For fp32 sketches the target
-//                        mean joins the tiles as row n, so the same pass
-//                        yields s_p (row n) and t2_p (element (n, n)).
-//   score_kernel       : bf16 sketches only: s_p[i] = <G_p[i], gbar_p> and
-//                        t2_p against the fp32 mean, fp64 accumulation,
-//                        fixed-order block reduction.
+//                        exactly symmetric, and for fp32 sketches s_p and
+//                        t2_p from the diagonal tiles.
+//   score_kernel       : s_p[i] = <G_p[i], gbar_p> and t2_p against the fp32
+//                        mean, fp64 accumulation, fixed-order block
+//                        reduction: bf16 sketches, and t2_p of fp32 ones
+//                        with n = 0.
 // Large bf16 problems (at least kBigMinTiles 256x256 lower-triangle tiles):
 //   gram_big_kernel    : one 256x256 tile of K_p per workgroup over all of
 //                        the group's columns (no split): 64-column steps
@@ -200,16 +204,26 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_kernel(GramArgs a) {
 }
 
 
-// fp32 rows, n + 1 > 128: the same 64x64 tile pairs and chunk partials as
-// gram_tile_kernel, with the operands staged through LDS: per step of 32
-// columns the workgroup's 64 + 64 rows (16 KB) are loaded once into
-// registers (each thread 4 segments of 16 bytes), written to a three-stage
-// LDS ring in the conflict-free operand layout, and read by the four waves
-// as fp32 MFMA fragments.  Loads run two steps ahead of their LDS writes,
-// and the LDS writes one step ahead of the products.
+// fp32 rows, n + 1 > 128: 64 x 64 tile pairs over the n general rows, with
+// the operands staged through LDS.  Per step of 32 columns the workgroup's
+// rows are loaded once into registers (16-byte segments), written to a
+// three-stage LDS ring in the conflict-free operand layout, and read by the
+// four waves as fp32 MFMA fragments; loads run two steps ahead of their LDS
+// writes, and the LDS writes one step ahead of the products.
+//   off-diagonal pair (I > J): tile I's 64 rows, then tile J's 64 rows;
+//   diagonal pair (I = J): tile I's 64 rows once (they are both operands),
+//     then the target mean as a 16-row block whose other rows are zero.
+//     Waves (0, 0), (1, 0) and (1, 1) take the tile's lower triangle; wave
+//     (0, 1), whose quadrant lies above the diagonal, takes the target mean
+//     against the 64 rows (the scores s), and in tile 0 wave (0, 0) also
+//     takes the target mean against itself (t2).  Both land in the partial
+//     tile's upper triangle, which holds nothing else: s of tile row
+//     16 b + l at (16 (b / 2), 32 + 16 (b % 2) + l), t2 at (0, 16).
 constexpr int kLS = 32;                          // fp32 columns per step (128-byte rows)
 constexpr int kLNS = 3;                          // ring stages
-constexpr int kLStage = 2 * kTile * kLS * 4;     // 64 A rows + 64 B rows
+constexpr int kLStage = 2 * kTile * kLS * 4;     // 128 rows of 128 bytes
+constexpr int kLMeanRow = kTile;                 // diagonal pairs: the target mean's stage row
+constexpr int kKindS = 16, kKindT2 = 17;         // wave tasks beyond the block masks 0..15
 
 __global__ __launch_bounds__(kThreads, 2) void gram_tile_lds_kernel(GramArgs a) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[kLNS * kLStage];
@@ -221,42 +235,48 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_lds_kernel(GramArgs a) 
   const int nsteps = (int)((c1 - c0 + kLS - 1) / kLS);
   int I, J;
   pair_to_tiles(q, I, J);
+  const bool diag = I == J;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int wr = w >> 1, wc = w & 1;
-  // loader: segment e = tid + 256 u of a stage is row e / 8 (A rows 0..63,
-  // B rows 64..127), segment e % 8; row n of the augmented problem is the
-  // target mean.  An entry outside the problem reads the target mean's
-  // first 16 bytes instead (every call has them; G may be empty) and is
-  // zeroed, so the loads are unconditional and their waits counted.
-  const unsigned char* dummy = reinterpret_cast<const unsigned char*>(a.gbar);
+  // loader: segment e = tid + 256 u of a stage is stage row e / 8, segment
+  // e % 8 (an off-diagonal pair loads u = 0..3, a diagonal one u = 0..2).
+  // An entry outside the problem reads the target mean's first 16 bytes
+  // instead and is zeroed at the LDS write, so the loads are unconditional
+  // and their waits counted.
+  const unsigned char* mean = reinterpret_cast<const unsigned char*>(a.gbar);   // by absolute column
   const unsigned char* src[4];
   bool rok[4];
   int sseg[4];
   unsigned loff[4];
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const int e = tid + kThreads * u, R = e >> 3, s = e & 7;
-    const int grow = R < kTile ? I * kTile + R : J * kTile + (R - kTile);
-    rok[u] = grow < a.rows;
-    src[u] = grow < a.n ? a.G + (long long)grow * a.ldG * 4 : dummy;   // row n: the target mean (by column)
-    sseg[u] = s;
-    loff[u] = (unsigned)(R * 128 + ((s ^ ((R >> 1) & 7)) * 16));
+    const int e = tid + kThreads * u, R = e >> 3, sg = e & 7;
+    if (R < kTile || !diag) {
+      const int grow = R < kTile ? I * kTile + R : J * kTile + (R - kTile);
+      rok[u] = grow < a.n;
+      src[u] = rok[u] ? a.G + (long long)grow * a.ldG * 4 : mean;
+    } else {
+      rok[u] = R == kLMeanRow;
+      src[u] = mean;
+    }
+    sseg[u] = sg;
+    loff[u] = (unsigned)(R * 128 + ((sg ^ ((R >> 1) & 7)) * 16));
   }
   auto seg_ok = [&](int t, int u) { return rok[u] && c0 + (long long)t * kLS + sseg[u] * 4 < c1; };
   // the zeroing happens at the LDS write, so nothing waits for the loads
   // until then
-  auto gload = [&](int t, u32x4 (&v)[4]) {
+  auto gload = [&](int t, u32x4 (&v)[4], auto nu) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < decltype(nu)::value; ++u) {
       const long long c = c0 + (long long)t * kLS + sseg[u] * 4;
-      v[u] = *reinterpret_cast<const u32x4*>(seg_ok(t, u) ? src[u] + c * 4 : dummy);
+      v[u] = *reinterpret_cast<const u32x4*>(seg_ok(t, u) ? src[u] + c * 4 : mean);
     }
   };
-  auto lstore = [&](int t, const u32x4 (&v)[4]) {
+  auto lstore = [&](int t, const u32x4 (&v)[4], auto nu) {
     unsigned char* sb = lds + (t % kLNS) * kLStage;
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < decltype(nu)::value; ++u)
       *reinterpret_cast<u32x4*>(sb + loff[u]) = seg_ok(t, u) ? v[u] : u32x4{0u, 0u, 0u, 0u};
   };
   f32x4 acc[2][2];
@@ -264,78 +284,115 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_lds_kernel(GramArgs a) 
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // products of the wave's 16 x 16 blocks (i, j) whose bit i * 2 + j is set
-  // in M (A block i against B block j)
-  auto compute = [&](int t, auto mask) {
-    constexpr int M = decltype(mask)::value;
-    constexpr bool ra0 = (M & 3) != 0, ra1 = (M & 12) != 0, rb0 = (M & 5) != 0, rb1 = (M & 10) != 0;
-    if constexpr (M != 0) {
+  // the wave's products of step t.  Kind 0..15: the 16 x 16 blocks (i, j)
+  // whose bit i * 2 + j is set (A block i against B block j); kKindT2: mask
+  // 13 plus the target mean against itself into acc[0][1]; kKindS: the
+  // target mean against the tile's four 16-row blocks into acc[b / 2][b % 2]
+  auto compute = [&](int t, auto kind, auto dg) {
+    constexpr int KD = decltype(kind)::value;
+    constexpr bool DG = decltype(dg)::value;
+    if constexpr (KD != 0) {
       const unsigned char* sb = lds + (t % kLNS) * kLStage;
+      const unsigned char* bb = sb + (DG ? 0 : kTile * 128);   // B operand rows
 #pragma unroll
       for (int kh = 0; kh < 2; ++kh) {
-        u32x4 fa[2], fb[2];
-        if constexpr (ra0) fa[0] = swz_read(sb + (wr * 32) * 128, lr, 4 * kh + lg);
-        if constexpr (ra1) fa[1] = swz_read(sb + (wr * 32 + 16) * 128, lr, 4 * kh + lg);
-        if constexpr (rb0) fb[0] = swz_read(sb + (kTile + wc * 32) * 128, lr, 4 * kh + lg);
-        if constexpr (rb1) fb[1] = swz_read(sb + (kTile + wc * 32 + 16) * 128, lr, 4 * kh + lg);
-        if constexpr ((M & 1) != 0) acc[0][0] = mma_v<false>(fa[0], fb[0], acc[0][0]);
-        if constexpr ((M & 2) != 0) acc[0][1] = mma_v<false>(fa[0], fb[1], acc[0][1]);
-        if constexpr ((M & 4) != 0) acc[1][0] = mma_v<false>(fa[1], fb[0], acc[1][0]);
-        if constexpr ((M & 8) != 0) acc[1][1] = mma_v<false>(fa[1], fb[1], acc[1][1]);
+        const int sg = 4 * kh + lg;
+        if constexpr (KD == kKindS) {
+          const u32x4 fm = swz_read(sb + kLMeanRow * 128, lr, sg);
+          u32x4 fb[4];
+#pragma unroll
+          for (int b = 0; b < 4; ++b) fb[b] = swz_read(sb + 16 * b * 128, lr, sg);
+          acc[0][0] = mma_v<false>(fm, fb[0], acc[0][0]);
+          acc[0][1] = mma_v<false>(fm, fb[1], acc[0][1]);
+          acc[1][0] = mma_v<false>(fm, fb[2], acc[1][0]);
+          acc[1][1] = mma_v<false>(fm, fb[3], acc[1][1]);
+        } else {
+          constexpr int M = KD == kKindT2 ? 13 : KD;
+          constexpr bool ra0 = (M & 3) != 0, ra1 = (M & 12) != 0, rb0 = (M & 5) != 0, rb1 = (M & 10) != 0;
+          u32x4 fa[2], fb[2];
+          if constexpr (ra0) fa[0] = swz_read(sb + (wr * 32) * 128, lr, sg);
+          if constexpr (ra1) fa[1] = swz_read(sb + (wr * 32 + 16) * 128, lr, sg);
+          if constexpr (rb0) fb[0] = swz_read(bb + (wc * 32) * 128, lr, sg);
+          if constexpr (rb1) fb[1] = swz_read(bb + (wc * 32 + 16) * 128, lr, sg);
+          if constexpr ((M & 1) != 0) acc[0][0] = mma_v<false>(fa[0], fb[0], acc[0][0]);
+          if constexpr ((M & 2) != 0) acc[0][1] = mma_v<false>(fa[0], fb[1], acc[0][1]);
+          if constexpr ((M & 4) != 0) acc[1][0] = mma_v<false>(fa[1], fb[0], acc[1][0]);
+          if constexpr ((M & 8) != 0) acc[1][1] = mma_v<false>(fa[1], fb[1], acc[1][1]);
+          if constexpr (KD == kKindT2) {
+            const u32x4 fm = swz_read(sb + kLMeanRow * 128, lr, sg);
+            acc[0][1] = mma_v<false>(fm, fm, acc[0][1]);
+          }
+        }
       }
     }
   };
-  u32x4 va[4], vb[4];
-  gload(0, va);
-  gload(1, vb);
-  lstore(0, va);
-  lstore(1, vb);
-  gload(2, va);
-  gload(3, vb);
-  __syncthreads();
   // step t: products from stage t % 3; the data of step t + 2 (loaded two
   // steps ago) into stage (t + 2) % 3, last read at step t - 1; the loads of
   // step t + 4; one barrier
-  auto run = [&](auto mask) {
+  auto run = [&](auto dg, auto kind) {
+    constexpr bool DG = decltype(dg)::value;
+    const std::integral_constant<int, DG ? 3 : 4> nu;
+    u32x4 va[4], vb[4];
+    gload(0, va, nu);
+    gload(1, vb, nu);
+    lstore(0, va, nu);
+    lstore(1, vb, nu);
+    gload(2, va, nu);
+    gload(3, vb, nu);
+    __syncthreads();
     for (int t = 0; t < nsteps; t += 2) {
-      compute(t, mask);
-      lstore(t + 2, va);
+      compute(t, kind, dg);
+      lstore(t + 2, va, nu);
       __builtin_amdgcn_sched_barrier(0);
-      gload(t + 4, va);
+      gload(t + 4, va, nu);
       __builtin_amdgcn_sched_barrier(0);
       DR_LDS_SYNC();
-      compute(t + 1, mask);   // past the last step its stage holds zeros: the products add 0
-      lstore(t + 3, vb);
+      compute(t + 1, kind, dg);   // past the last step its stage holds zeros: the products add 0
+      lstore(t + 3, vb, nu);
       __builtin_amdgcn_sched_barrier(0);
-      gload(t + 5, vb);
+      gload(t + 5, vb, nu);
       __builtin_amdgcn_sched_barrier(0);
       DR_LDS_SYNC();
     }
   };
   // Blocks the reduction never reads take no products and keep zero
-  // accumulators: A rows wholly past the last row (I >= J, so these are the
-  // last tile row's, which for n + 1 = 64 t + 1 holds the target mean alone),
-  // and on a diagonal tile the blocks wholly above the diagonal.  The mask is
-  // uniform over the wave; it is rounded up to the smallest of five loop
-  // variants that contains it (extra products are harmless).
+  // accumulators: A rows wholly past row n - 1 (I >= J, so these are the
+  // last tile's), and on a diagonal tile the blocks wholly above the
+  // diagonal.  The mask is uniform over the wave and is rounded up to the
+  // smallest loop variant that contains it (extra products are harmless).
   int live = 0;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int rb = I * kTile + wr * 32 + 16 * i, cb = J * kTile + wc * 32 + 16 * j;
-      if (rb < a.rows && cb <= rb + 15) live |= 1 << (i * 2 + j);
+      if (rb < a.n && cb <= rb + 15) live |= 1 << (i * 2 + j);
     }
-  if (live == 0)
-    run(std::integral_constant<int, 0>{});
-  else if ((live & ~1) == 0)
-    run(std::integral_constant<int, 1>{});    // (0, 0)
-  else if ((live & ~3) == 0)
-    run(std::integral_constant<int, 3>{});    // A block 0 only
-  else if ((live & ~13) == 0)
-    run(std::integral_constant<int, 13>{});   // lower triangle of the wave's 2 x 2
-  else
-    run(std::integral_constant<int, 15>{});
+  using F = std::false_type;
+  using T = std::true_type;
+  if (!diag) {
+    // J < I: every B block lies below the A rows, so live is 0, 3 or 15
+    if (live == 0)
+      run(F{}, std::integral_constant<int, 0>{});
+    else if ((live & ~3) == 0)
+      run(F{}, std::integral_constant<int, 3>{});
+    else
+      run(F{}, std::integral_constant<int, 15>{});
+  } else if (wr == 0 && wc == 1) {
+    run(T{}, std::integral_constant<int, kKindS>{});
+  } else if (I == 0 && wr == 0 && wc == 0) {
+    run(T{}, std::integral_constant<int, kKindT2>{});   // its live blocks are within mask 13
+  } else if (live == 0) {
+    run(T{}, std::integral_constant<int, 0>{});
+  } else if ((live & ~1) == 0) {
+    run(T{}, std::integral_constant<int, 1>{});
+  } else if ((live & ~3) == 0) {
+    run(T{}, std::integral_constant<int, 3>{});
+  } else if ((live & ~13) == 0) {
+    run(T{}, std::integral_constant<int, 13>{});
+  } else {
+    run(T{}, std::integral_constant<int, 15>{});
+  }
 
   float* out = a.partial + (((long long)p * a.pairs + q) * a.maxchunks + chunk) * (kTile * kTile);
 #pragma unroll
@@ -670,8 +727,9 @@ bool gram_use_big(int64_t n, int P, dr_dtype dtype) {
 }
 
 // One thread per element of a 64x64 tile: sums the chunk partials in chunk
-// order and writes K (lower triangle and its mirror) and, for the augmented
-// fp32 problem, s (row n) and t2 (element (n, n)).
+// order and writes K (lower triangle and its mirror) and, for fp32 rows, s
+// and t2 from the upper triangle of the diagonal tiles (where
+// gram_tile_lds_kernel puts them).
 __global__ __launch_bounds__(kThreads) void gram_reduce_kernel(GramArgs a, float* K, float* s, float* t2,
                                                                long long pbase) {
   const int q = blockIdx.x, p = blockIdx.y;
@@ -680,8 +738,20 @@ __global__ __launch_bounds__(kThreads) void gram_reduce_kernel(GramArgs a, float
   const int nvalid = (int)((width + a.CK - 1) / a.CK);
   int I, J;
   pair_to_tiles(q, I, J);
-  const int r = I * kTile + e / kTile, c = J * kTile + e % kTile;
-  if (r >= a.rows || c > r) return;
+  const int tr = e / kTile, tc = e % kTile;
+  const int r = I * kTile + tr, c = J * kTile + tc;
+  int srow = -1;   // >= 0: this element is s[srow]; -2: t2
+  if (c <= r) {
+    if (r >= a.n) return;
+  } else if (a.rows > a.n && I == J) {
+    if ((tr == 0 || tr == 16) && tc >= 32)
+      srow = I * kTile + 2 * tr + (tc - 32);
+    else if (I == 0 && tr == 0 && tc == 16)
+      srow = -2;
+    if (srow == -1 || srow >= a.n) return;
+  } else {
+    return;
+  }
   const float* src = a.partial + ((long long)p * a.pairs + q) * a.maxchunks * (kTile * kTile) + e;
   float acc = 0.f;
   int ch = 0;
@@ -693,12 +763,12 @@ __global__ __launch_bounds__(kThreads) void gram_reduce_kernel(GramArgs a, float
     for (int u = 0; u < 8; ++u) acc += v[u];
   }
   for (; ch < nvalid; ++ch) acc += src[(long long)ch * (kTile * kTile)];
-  if (r < a.n) {
+  if (srow == -1) {
     float* Kp = K + (pbase + p) * (long long)a.n * a.n;
     Kp[(long long)r * a.n + c] = acc;
     Kp[(long long)c * a.n + r] = acc;
-  } else if (c < a.n) {
-    s[(pbase + p) * (long long)a.n + c] = acc;
+  } else if (srow >= 0) {
+    s[(pbase + p) * (long long)a.n + srow] = acc;
   } else {
     t2[pbase + p] = acc;
   }
@@ -782,9 +852,10 @@ bool gram_use_small(int64_t n, dr_dtype dtype) { return dtype == DR_F32 && n >= 
 // kTargetWGs workgroups; identical for every launch of a call.
 GramPlan gram_plan(int64_t n, const int64_t* goff, int P, dr_dtype dtype) {
   GramPlan g;
-  // fp32 sketches: gbar joins as row n, so s and t2 come out of the same pass
+  // fp32 sketches: gbar joins as row n, so s and t2 come out of the same
+  // pass (the tiles cover the n general rows; the diagonal tiles carry gbar)
   const int64_t rows = dtype == DR_F32 ? n + 1 : n;
-  g.NT = (int)((rows + kTile - 1) / kTile);
+  g.NT = (int)((n + kTile - 1) / kTile);
   g.pairs = g.NT * (g.NT + 1) / 2;
   int64_t maxw = 0;
   for (int p = 0; p < P; ++p) maxw = goff[p + 1] - goff[p] > maxw ? goff[p + 1] - goff[p] : maxw;
@@ -909,7 +980,7 @@ dr_status gram_run(const GramPlan& g, const void* G, int64_t n, int64_t ldG, con
       hipLaunchKernelGGL(gram_small_reduce_kernel, dim3((nr * (nr + 1) / 2 + kThreads / 64 - 1) / (kThreads / 64), gp),
                          dim3(kThreads), 0, hs, a, g.NRP, g.maxchunks, K, s, t2, (long long)p0);
       if ((st = launch_status()) != DR_OK) return st;
-    } else if (g.rows > 0) {
+    } else if (g.pairs > 0) {
       dim3 grid(g.maxchunks, g.pairs, gp);
       if (bf)
         hipLaunchKernelGGL(gram_tile_kernel<true>, grid, dim3(kThreads), 0, hs, a);
@@ -923,6 +994,10 @@ dr_status gram_run(const GramPlan& g, const void* G, int64_t n, int64_t ldG, con
     if (bf) {
       // bf16 sketches: s and t2 against the fp32 target mean in a separate pass
       hipLaunchKernelGGL(score_kernel<true>, dim3(n + 1, gp), dim3(kThreads), 0, hs, a, gbar, s, t2, (long long)p0);
+      if ((st = launch_status()) != DR_OK) return st;
+    } else if (g.pairs == 0) {
+      // fp32 with no general rows: t2 alone
+      hipLaunchKernelGGL(score_kernel<false>, dim3(1, gp), dim3(kThreads), 0, hs, a, gbar, s, t2, (long long)p0);
       if ((st = launch_status()) != DR_OK) return st;
     }
   }

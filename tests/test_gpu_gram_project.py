@@ -32,6 +32,8 @@ def rand(shape, seed, dtype=torch.float32, scale=1.0):
     (64, 2048 + 512 + 68, [0, 512, 512, 2628], torch.float32),   # one-pass small path: groups, one empty, ragged chunk
     (127, 8192, None, torch.float32),                 # largest n of the one-pass path
     (150, 1068, [0, 604, 1068], torch.float32),       # LDS-staged tiles: ragged 32-column steps in both groups
+    (128, 2048, None, torch.float32),                 # LDS-staged tiles: two full row tiles
+    (178, 1568, [0, 768, 1568], torch.float32),       # LDS-staged tiles: 50 rows in the third row tile
 ])
 def test_gram_matches_oracle(n, kappa, goff, dtype):
     G = rand((n, kappa), 10 + n, dtype)
