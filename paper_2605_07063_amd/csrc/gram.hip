@@ -753,8 +753,16 @@ __global__ __launch_bounds__(kThreads) void gram_reduce_kernel(GramArgs a, float
     return;
   }
   const float* src = a.partial + ((long long)p * a.pairs + q) * a.maxchunks * (kTile * kTile) + e;
+  // chunks in batches of 32 loads in flight, summed in chunk order
   float acc = 0.f;
   int ch = 0;
+  for (; ch + 32 <= nvalid; ch += 32) {
+    float v[32];
+#pragma unroll
+    for (int u = 0; u < 32; ++u) v[u] = src[(long long)(ch + u) * (kTile * kTile)];
+#pragma unroll
+    for (int u = 0; u < 32; ++u) acc += v[u];
+  }
   for (; ch + 8 <= nvalid; ch += 8) {
     float v[8];
 #pragma unroll
@@ -780,17 +788,25 @@ __global__ __launch_bounds__(kThreads) void target_mean_kernel(const unsigned ch
                                                                long long c_lo, long long c_hi, float* gbar) {
   const long long c = c_lo + (long long)blockIdx.x * kThreads + threadIdx.x;
   if (c >= c_hi) return;
-  double acc = 0.0;
-  for (int j = 0; j < m; ++j) {
-    float v;
+  auto ld = [&](int j) -> float {
     if constexpr (BF16) {
       const unsigned short h = reinterpret_cast<const unsigned short*>(Gt)[(long long)j * ldGt + c];
-      v = __uint_as_float((unsigned)h << 16);
+      return __uint_as_float((unsigned)h << 16);
     } else {
-      v = reinterpret_cast<const float*>(Gt)[(long long)j * ldGt + c];
+      return reinterpret_cast<const float*>(Gt)[(long long)j * ldGt + c];
     }
-    acc += (double)v;
+  };
+  // rows in batches of 8 loads in flight, summed in row order
+  double acc = 0.0;
+  int j = 0;
+  for (; j + 8 <= m; j += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = ld(j + u);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc += (double)v[u];
   }
+  for (; j < m; ++j) acc += (double)ld(j);
   gbar[c] = (float)(acc / (double)m);
 }
 

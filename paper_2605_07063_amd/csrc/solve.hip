@@ -148,44 +148,45 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
   const float* sp = s + (long long)p * n;
   const int nt = (n + 15) >> 4;
 
-  // K into the tiles (lower triangle, padded to a multiple of 16 with the
-  // identity), the finiteness of every entry of K (tile (I, J) and its
-  // mirror (J, I)) and of s, and the trace; loads with clamped addresses and
-  // masked values, four tiles' worth in flight per lane
+  // K into the tiles: wave w reads rows w, w + 16, ... of K whole (lanes
+  // across the row, coalesced, 32 loads in flight per lane), checks every
+  // entry for finiteness, adds the diagonal to the trace and stores the
+  // entries of the lower block triangle (block column <= block row, so the
+  // diagonal tiles hold both of their triangles); rows and columns from n up
+  // to 16 nt are padded with the identity
   if (tid == 0) flag = 0;
   double tr = 0.0;
   bool bad = false;
   for (int i = tid; i < n; i += kSpanThreads) bad |= !isfinite(sp[i]);
-  constexpr int LB = 4;
-  for (int q0 = wid; q0 < nt * (nt + 1) / 2; q0 += LB * NW) {
-    float v[LB][4], vm[LB][4];
-    int I[LB], J[LB];
+  {
+    constexpr int RB = 8, C4 = kSpanMaxN / 64;
+    for (int r0 = wid; r0 < n; r0 += RB * NW) {
+      float v[RB][C4];
 #pragma unroll
-    for (int h = 0; h < LB; ++h) {
-      const int q = min(q0 + h * NW, nt * (nt + 1) / 2 - 1);
-      tri_pair(q, I[h], J[h]);
+      for (int t = 0; t < RB; ++t) {
+        const int i = min(r0 + NW * t, n - 1);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int e = lane + 64 * u, rr = e >> 4, c = e & 15;
-        const int i = min(16 * I[h] + rr, n - 1), j = min(16 * J[h] + c, n - 1);
-        v[h][u] = Kp[(long long)i * n + j];
-        const int im = min(16 * J[h] + rr, n - 1), jm = min(16 * I[h] + c, n - 1);
-        vm[h][u] = Kp[(long long)im * n + jm];
+        for (int c = 0; c < C4; ++c) v[t][c] = Kp[(long long)i * n + min(lane + 64 * c, n - 1)];
+      }
+#pragma unroll
+      for (int t = 0; t < RB; ++t) {
+        const int i = r0 + NW * t;
+        if (i >= n) break;
+#pragma unroll
+        for (int c = 0; c < C4; ++c) {
+          const int j = lane + 64 * c;
+          if (j >= n) continue;
+          bad |= !isfinite(v[t][c]);
+          if (i == j) tr += (double)v[t][c];
+          if ((j >> 4) <= (i >> 4)) Lt[row_at(i) + col_off(j)] = v[t][c];
+        }
       }
     }
-#pragma unroll
-    for (int h = 0; h < LB; ++h) {
-      if (q0 + h * NW >= nt * (nt + 1) / 2) break;
-      float* T = Lt + (q0 + h * NW) * 256;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int e = lane + 64 * u, rr = e >> 4, c = e & 15;
-        const int i = 16 * I[h] + rr, j = 16 * J[h] + c;
-        const bool in = i < n && j < n;
-        const bool inm = 16 * J[h] + rr < n && 16 * I[h] + c < n;
-        bad |= (in && !isfinite(v[h][u])) || (inm && !isfinite(vm[h][u]));
-        if (in && i == j) tr += (double)v[h][u];
-        T[rperm(rr) * 16 + c] = in ? v[h][u] : (i == j ? 1.f : 0.f);
+    if (n & 15) {
+      const int I = nt - 1;
+      for (int e = tid; e < 16 * 16 * nt; e += kSpanThreads) {
+        const int i = 16 * I + (e >> 4) / nt, j = 16 * ((e >> 4) % nt) + (e & 15);
+        if (i >= n || j >= n) Lt[row_at(i) + col_off(j)] = i == j ? 1.f : 0.f;
       }
     }
   }
