@@ -748,16 +748,18 @@ __global__ __launch_bounds__(kThreads, 2) void sketch_packed_kernel(PackArgs a) 
 }
 
 // Examples spread over several tiles: sum their per-tile partials in tile
-// order; empty examples get zeros.  Four workgroups per (layer, example),
-// one float4 of the sketch block per thread.
-constexpr int kReduceSplit = 4;
+// order (eight tiles' loads in flight); empty examples get zeros.  One float4
+// of the sketch block per thread, kPackReduceWGs workgroups per (layer,
+// example).
+template <int KIN, int KOUT>
+constexpr int kPackReduceWGs = (KOUT * KIN / 4 + kThreads - 1) / kThreads;
 
 template <int KIN, int KOUT>
 __global__ __launch_bounds__(kThreads) void sketch_packed_reduce_kernel(PackArgs a) {
   constexpr int V4 = KOUT * KIN / 4;
-  constexpr int PER = (V4 + kReduceSplit * kThreads - 1) / (kReduceSplit * kThreads);
-  const int part = blockIdx.x % kReduceSplit;
-  const int pair = blockIdx.x / kReduceSplit;
+  constexpr int NP = kPackReduceWGs<KIN, KOUT>;
+  const int part = blockIdx.x % NP;
+  const int pair = blockIdx.x / NP;
   const int li = pair / a.N, e = pair % a.N;
   const int ce = a.cum[e], ce1 = a.cum[e + 1];
   const int R = a.cum[a.N + 1];
@@ -765,26 +767,33 @@ __global__ __launch_bounds__(kThreads) void sketch_packed_reduce_kernel(PackArgs
   const int t0 = (ce / R) * a.KS + (ce % R) / kTokTile;
   const int t1 = ((ce1 - 1) / R) * a.KS + ((ce1 - 1) % R) / kTokTile;
   if (ce1 > ce && t0 == t1) return;   // written by its only tile
-  float* out = a.S + (long long)e * a.ldS + a.L[li].col_offset;
+  const int e4 = part * kThreads + threadIdx.x;
+  if (e4 >= V4) return;
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (ce1 > ce) {
+    // partial of tile tt, slot sl: [layer][tile][slot][KOUT * KIN]
+    const f32x4* base = reinterpret_cast<const f32x4*>(a.partial + (long long)li * a.max_tiles * 2 * (KOUT * KIN)) + e4;
+    for (int tb = t0; tb <= t1; tb += 8) {
+      int ex[8];
 #pragma unroll
-  for (int u = 0; u < PER; ++u) {
-    const int e4 = (part * PER + u) * kThreads + threadIdx.x;
-    if (e4 >= V4) break;
-    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (ce1 > ce) {
-      for (int tt = t0; tt <= t1; ++tt) {
-        if (a.tile_ex[tt] < 0) continue;   // slot past the end of a workgroup's range
-        const int slot = a.tile_ex[tt] == e ? 0 : 1;
-        acc += reinterpret_cast<const f32x4*>(a.partial + (((long long)li * a.max_tiles + tt) * 2 + slot) *
-                                                              (KOUT * KIN))[e4];
-      }
+      for (int u = 0; u < 8; ++u) ex[u] = tb + u <= t1 ? a.tile_ex[tb + u] : -1;   // < 0: no partial
+      f32x4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        v[u] = ex[u] >= 0 ? base[(long long)((tb + u) * 2 + (ex[u] == e ? 0 : 1)) * V4] : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (ex[u] >= 0) acc += v[u];
     }
-    out[4 * e4 + 0] = acc[0];
-    out[4 * e4 + 1] = acc[1];
-    out[4 * e4 + 2] = acc[2];
-    out[4 * e4 + 3] = acc[3];
   }
+  float* out = a.S + (long long)e * a.ldS + a.L[li].col_offset;
+  out[4 * e4 + 0] = acc[0];
+  out[4 * e4 + 1] = acc[1];
+  out[4 * e4 + 2] = acc[2];
+  out[4 * e4 + 3] = acc[3];
 }
+
+constexpr int kReduceSplit = 4;   // workgroups per (layer, example) of sketch_reduce_kernel
 
 // Sum the chunk partials of every (layer, example) in chunk order (register
 // kernel path): four workgroups per (layer, example), one float4 per thread.
@@ -953,7 +962,7 @@ void launch_t(const Launch& l, const SketchArgs& a, const PackArgs& pa, hipStrea
   if (l.packed) {
     if (pa.max_tiles > 0)
       hipLaunchKernelGGL((sketch_packed_kernel<BF16, KIN, KOUT>), dim3(l.count * pa.WL), dim3(kThreads), 0, st, pa);
-    hipLaunchKernelGGL((sketch_packed_reduce_kernel<KIN, KOUT>), dim3(l.count * pa.N * kReduceSplit), dim3(kThreads),
+    hipLaunchKernelGGL((sketch_packed_reduce_kernel<KIN, KOUT>), dim3(l.count * pa.N * kPackReduceWGs<KIN, KOUT>), dim3(kThreads),
                        0, st, pa);
     return;
   }
