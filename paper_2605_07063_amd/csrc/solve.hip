@@ -343,15 +343,26 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
         for (int jj = 0; jj < 4; ++jj) {
           const int J = 4 * mb + jj;
           if (J >= nt) break;
-          float xrow[16];   // row kc of X_J
+          // The LDS reads of the block depend on J only: X_J's row and the
+          // first register's row of block column J go out before the
+          // broadcasts, and each later register's row while the previous
+          // one is applied.  Registers mb + 1.. always hold rows below the
+          // block; register mb does unless jj = 3.
+          const int m0 = jj < 3 ? mb : mb + 1;
+          auto lrow_at = [&](int m) { return Lt + row_at(lane + 64 * m) + J * 256; };   // row k of tile (k / 16, J)
+          auto ld16 = [](const float* p, float (&o)[16]) {
 #pragma unroll
-          for (int c = 0; c < 16; c += 4) {
-            const float4 t4 = *reinterpret_cast<const float4*>(&Xt[J * 256 + kc * 16 + c]);
-            xrow[c] = t4.x;
-            xrow[c + 1] = t4.y;
-            xrow[c + 2] = t4.z;
-            xrow[c + 3] = t4.w;
-          }
+            for (int c = 0; c < 16; c += 4) {
+              const float4 t4 = *reinterpret_cast<const float4*>(p + c);
+              o[c] = t4.x;
+              o[c + 1] = t4.y;
+              o[c + 2] = t4.z;
+              o[c + 3] = t4.w;
+            }
+          };
+          float xrow[16], lcur[16], lnext[16];   // row kc of X_J; rows of block column J
+          ld16(&Xt[J * 256 + kc * 16], xrow);
+          if (m0 < R) ld16(lrow_at(m0), lcur);
           float acc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int c = 0; c < 16; ++c) acc[c & 3] = fmaf(xrow[c], readlane_f(v[mb], 16 * jj + c), acc[c & 3]);
@@ -361,19 +372,17 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
           for (int c = 0; c < 16; ++c) yb[c] = readlane_f(v[mb], 16 * jj + c);
 #pragma unroll
           for (int m = mb; m < R; ++m) {
+            if (m < m0) continue;
+            if (m + 1 < R) ld16(lrow_at(m + 1), lnext);
             const int k = lane + 64 * m;
-            if (64 * m + 63 < 16 * J + 16) continue;   // no row of this register lies below the block
-            const float* Lr = Lt + row_at(k) + J * 256;   // row k of tile (k / 16, J)
             float d[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int c = 0; c < 16; c += 4) {
-              const float4 l4 = *reinterpret_cast<const float4*>(Lr + c);
-              d[0] = fmaf(l4.x, yb[c], d[0]);
-              d[1] = fmaf(l4.y, yb[c + 1], d[1]);
-              d[2] = fmaf(l4.z, yb[c + 2], d[2]);
-              d[3] = fmaf(l4.w, yb[c + 3], d[3]);
-            }
+            for (int c = 0; c < 16; ++c) d[c & 3] = fmaf(lcur[c], yb[c], d[c & 3]);
             v[m] = (k >> 4) > J ? v[m] - ((d[0] + d[1]) + (d[2] + d[3])) : v[m];
+            if (m + 1 < R) {
+#pragma unroll
+              for (int c = 0; c < 16; ++c) lcur[c] = lnext[c];
+            }
           }
         }
       }
@@ -383,9 +392,21 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
         for (int jj = 3; jj >= 0; --jj) {
           const int J = 4 * mb + jj;
           if (J >= nt) continue;
-          float xcol[16];   // column kc of X_J
+          // As in the forward sweep: X_J's column and the first register's
+          // column of block row J before the broadcasts, each later one
+          // while the previous is applied.  Registers 0..mb - 1 always hold
+          // rows above the block; register mb does unless jj = 0.
+          const int m1 = jj > 0 ? mb : mb - 1;   // last register with rows above the block
+          auto lcol_at = [&](int m, float (&o)[16]) {
+            const int k = lane + 64 * m;
+            const float* Lc = Lt + tile_at(J, min(k >> 4, J)) + (k & 15);   // column k of block row J
+#pragma unroll
+            for (int c = 0; c < 16; ++c) o[c] = Lc[rperm(c) * 16];
+          };
+          float xcol[16], lcur[16], lnext[16];   // column kc of X_J; columns of block row J
 #pragma unroll
           for (int c = 0; c < 16; ++c) xcol[c] = Xt[J * 256 + c * 16 + kc];
+          if (m1 >= 0) lcol_at(0, lcur);
           float acc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int c = 0; c < 16; ++c) acc[c & 3] = fmaf(xcol[c], readlane_f(v[mb], 16 * jj + c), acc[c & 3]);
@@ -395,13 +416,17 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
           for (int c = 0; c < 16; ++c) zb[c] = readlane_f(v[mb], 16 * jj + c);
 #pragma unroll
           for (int m = 0; m <= mb; ++m) {
+            if (m > m1) continue;
+            if (m + 1 <= m1) lcol_at(m + 1, lnext);
             const int k = lane + 64 * m;
-            if (64 * m >= 16 * J) continue;   // no row of this register lies above the block
-            const float* Lc = Lt + tile_at(J, min(k >> 4, J)) + (k & 15);   // column k of block row J
             float d[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int c = 0; c < 16; ++c) d[c & 3] = fmaf(Lc[rperm(c) * 16], zb[c], d[c & 3]);
+            for (int c = 0; c < 16; ++c) d[c & 3] = fmaf(lcur[c], zb[c], d[c & 3]);
             v[m] = (k >> 4) < J ? v[m] - ((d[0] + d[1]) + (d[2] + d[3])) : v[m];
+            if (m + 1 <= m1) {
+#pragma unroll
+              for (int c = 0; c < 16; ++c) lcur[c] = lnext[c];
+            }
           }
         }
       }
