@@ -61,7 +61,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kTile = 64;
-constexpr int kMaxGroups = 128;   // groups per launch (more groups -> more launches)
+constexpr int kMaxGroups = 256;   // groups per launch (more groups -> more launches)
 constexpr int kTargetWGs = 1024;
 
 struct GramArgs {

@@ -34,6 +34,7 @@ def rand(shape, seed, dtype=torch.float32, scale=1.0):
     (150, 1068, [0, 604, 1068], torch.float32),       # LDS-staged tiles: ragged 32-column steps in both groups
     (128, 2048, None, torch.float32),                 # LDS-staged tiles: two full row tiles
     (178, 1568, [0, 768, 1568], torch.float32),       # LDS-staged tiles: 50 rows in the third row tile
+    (130, 2400, [8 * i for i in range(301)], torch.float32),   # 300 groups: two launches (256 + 44 groups)
 ])
 def test_gram_matches_oracle(n, kappa, goff, dtype):
     G = rand((n, kappa), 10 + n, dtype)
