@@ -63,6 +63,7 @@ constexpr int kThreads = 256;
 constexpr int kTile = 64;
 constexpr int kMaxGroups = 256;   // groups per launch (more groups -> more launches)
 constexpr int kTargetWGs = 1024;
+constexpr int kLdsSlots = 256 * 3;   // gram_tile_lds_kernel workgroups resident at once: 256 CUs x 3 (48 KB of LDS each)
 
 struct GramArgs {
   const unsigned char* G;
@@ -864,8 +865,9 @@ struct GramPlan {
 
 bool gram_use_small(int64_t n, dr_dtype dtype) { return dtype == DR_F32 && n >= 1 && n + 1 <= kSmMaxRows; }
 
-// Chunk length: a multiple of 256 columns, shrunk until a launch has about
-// kTargetWGs workgroups; identical for every launch of a call.
+// Chunk length: a multiple of 256 columns; for bf16 tiles shrunk until a
+// launch has about kTargetWGs workgroups, for fp32 tiles sized to two
+// rounds of kLdsSlots; identical for every launch of a call.
 GramPlan gram_plan(int64_t n, const int64_t* goff, int P, dr_dtype dtype) {
   GramPlan g;
   // fp32 sketches: gbar joins as row n, so s and t2 come out of the same
@@ -877,7 +879,17 @@ GramPlan gram_plan(int64_t n, const int64_t* goff, int P, dr_dtype dtype) {
   for (int p = 0; p < P; ++p) maxw = goff[p + 1] - goff[p] > maxw ? goff[p + 1] - goff[p] : maxw;
   const int gp = P < kMaxGroups ? P : kMaxGroups;
   int64_t ck = align_up((size_t)(maxw > 0 ? maxw : 1), 256);
-  while (ck > 256 && (int64_t)g.pairs * gp * ((maxw + ck - 1) / ck) < kTargetWGs) ck = align_up((size_t)(ck / 2), 256);
+  if (dtype == DR_F32) {
+    // fp32 tiles: the chunk length that keeps the launch just within two
+    // rounds of the workgroups the chip holds at once (kLdsSlots), so the
+    // second round is nearly full (the fixed count keeps the chunking, and
+    // with it the summation order, the same on every device)
+    const int64_t want = ((int64_t)maxw * g.pairs * gp + 2 * kLdsSlots - 1) / (2 * kLdsSlots);
+    const int64_t c2 = (int64_t)align_up((size_t)(want > 256 ? want : 256), 256);
+    if (c2 < ck) ck = c2;
+  } else {
+    while (ck > 256 && (int64_t)g.pairs * gp * ((maxw + ck - 1) / ck) < kTargetWGs) ck = align_up((size_t)(ck / 2), 256);
+  }
   g.CK = (int)ck;
   g.maxchunks = (int)((maxw + ck - 1) / ck);
   if (g.maxchunks < 1) g.maxchunks = 1;
