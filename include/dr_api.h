@@ -175,8 +175,8 @@ size_t dr_gram_workspace_size(int64_t n, int64_t m, const int64_t* goff, int P, 
  * routine); its first call on a device looks up that device's array.
  *   Returns DR_ERR_TOO_LARGE, before any HIP call, when
  *   dr_gram_workspace_size(n, m, goff, P, dtype) > DR_GRAM_NOALLOC_MAX_BYTES
- *   (every workload shape here needs at most half of it: 32 MB for 256
- *   rows over 229376 fp32 columns).
+ *   (the largest workload shape here needs 36 MiB: 256 fp32 rows over
+ *   229376 columns in 224 groups; 24 MiB as one group).
  * All calls on one GPU share its array (and it keeps the last call's
  * contents; nothing in it needs to start at zero): calls that overlap on one
  * GPU -- on different streams, or from different host threads without
