@@ -63,6 +63,15 @@ def test_gram_no_general_rows_and_determinism():
     torch.cuda.synchronize()
     for x, y in zip(a, b):
         assert torch.equal(x, y)
+    # the LDS-staged tile path (n + 1 > 128), with the scores formed in the
+    # diagonal tiles: bit-identical on a repeat
+    G = rand((200, 6144), 7)
+    Gt2 = rand((5, 6144), 8)
+    a = api.gram(G, Gt2, [0, 1024, 6144])
+    b = api.gram(G, Gt2, [0, 1024, 6144])
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
 
 
 def test_gram_dominated_full_size_sampled():
