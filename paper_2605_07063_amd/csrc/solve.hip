@@ -140,6 +140,11 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
   __shared__ double x[kSpanMaxN], y[kSpanMaxN];
   __shared__ double scratch[kSpanThreads / 64 + 1];
   __shared__ int flag;
+  // q -> (I, J) of the lower block triangle, q = I (I + 1) / 2 + J, as a
+  // table (the trailing update would otherwise take a square root and two
+  // correction loops per tile)
+  constexpr int kTriQ = kSpanTiles * (kSpanTiles + 1) / 2;
+  __shared__ unsigned char tri_tab[2][kTriQ];
   const int p = blockIdx.x, tid = threadIdx.x;
   const int wid = tid >> 6, lane = tid & 63;
   const int lr = lane & 15, lq = lane >> 4;
@@ -155,6 +160,12 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
   // diagonal tiles hold both of their triangles); rows and columns from n up
   // to 16 nt are padded with the identity
   if (tid == 0) flag = 0;
+  if (tid < kTriQ) {
+    int I, J;
+    tri_pair(tid, I, J);
+    tri_tab[0][tid] = (unsigned char)I;
+    tri_tab[1][tid] = (unsigned char)J;
+  }
   double tr = 0.0;
   bool bad = false;
   for (int i = tid; i < n; i += kSpanThreads) bad |= !isfinite(sp[i]);
@@ -282,10 +293,8 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
         int C[2];
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          int I, Kt;
-          tri_pair(min(q0 + h * (NW - 1), nrest - 1), I, Kt);
-          I += J + 1;
-          Kt += J + 1;
+          const int qq = min(q0 + h * (NW - 1), nrest - 1);   // nrest <= kTriQ
+          const int I = tri_tab[0][qq] + J + 1, Kt = tri_tab[1][qq] + J + 1;
           av[h] = *reinterpret_cast<const float4*>(&Lt[tile_at(I, J) + rperm(lr) * 16 + 4 * lq]);
           bv[h] = *reinterpret_cast<const float4*>(&Lt[tile_at(Kt, J) + rperm(lr) * 16 + 4 * lq]);
           C[h] = tile_at(I, Kt);
