@@ -137,7 +137,7 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
                                                                   float* lam_eff_out, float* resid2, int* info) {
   __shared__ __attribute__((aligned(16))) float Lt[kSpanTiles * (kSpanTiles + 1) / 2 * 256];
   __shared__ __attribute__((aligned(16))) float Xt[kSpanTiles * 256];   // inverses of the diagonal tiles
-  __shared__ double x[kSpanMaxN], y[kSpanMaxN];
+  __shared__ double x[kSpanMaxN], y[kSpanMaxN], sd[kSpanMaxN];   // sd: s, staged once
   __shared__ double scratch[kSpanThreads / 64 + 1];
   __shared__ int flag;
   // q -> (I, J) of the lower block triangle, q = I (I + 1) / 2 + J, as a
@@ -475,7 +475,7 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
     }
   };
 
-  for (int i = tid; i < n; i += kSpanThreads) y[i] = (double)sp[i];
+  for (int i = tid; i < n; i += kSpanThreads) y[i] = sd[i] = (double)sp[i];
   __syncthreads();
   chol_solve();
   double x0m = 0.0;
@@ -492,7 +492,7 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
   // the refinement converged, and it stops as soon as they do
   bool converged = false;
   for (int it = 0; it < 2 && !converged; ++it) {
-    kx_rows([&](int i, double kx) { y[i] = (double)sp[i] - (double)lam * x[i] - kx; });
+    kx_rows([&](int i, double kx) { y[i] = sd[i] - (double)lam * x[i] - kx; });
     __syncthreads();
     chol_solve();
     double dm = 0.0, xm = 0.0;
@@ -508,7 +508,7 @@ __global__ __launch_bounds__(kSpanThreads) void span_small_kernel(const float* K
 
   // resid2 = t2 - 2 s.x + x.K.x
   double part = 0.0;
-  kx_rows([&](int i, double kx) { part += x[i] * kx - 2.0 * (double)sp[i] * x[i]; });
+  kx_rows([&](int i, double kx) { part += x[i] * kx - 2.0 * sd[i] * x[i]; });
   const double q = block_sum<kSpanThreads>(part, scratch);
   for (int i = tid; i < n; i += kSpanThreads) w[(long long)p * n + i] = (float)x[i];
   if (tid == 0) {
