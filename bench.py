@@ -452,12 +452,14 @@ def run_small(args, api, _lib, workloads, dev, peaks, with_cpu, with_next):
     u = torch.empty(ktot, device=dev)
     cb_ws = torch.empty(max(1, api.dr_combine_workspace_size(n, goff)), dtype=torch.uint8, device=dev)
     G, Gt = S[:n], S[n:]
-    main = torch.cuda.current_stream()
     side = torch.cuda.Stream()
     gram_done = torch.cuda.Event()
     side_done = torch.cuda.Event()
+    sp_ws = torch.empty(max(1, api.dr_span_workspace_size(n, 1)), dtype=torch.uint8, device=dev)
 
     def step(ev=None):
+        main = torch.cuda.current_stream()   # the capture stream when a graph records the step
+
         def mark(i, stream):
             if ev is not None:
                 ev[i].record(stream)
@@ -473,7 +475,8 @@ def run_small(args, api, _lib, workloads, dev, peaks, with_cpu, with_next):
         api.dr_combine(G, goff, wc, u, workspace=cb_ws, stream=main)
         mark(4, main)
         mark(5, side)
-        api.dr_project_span(K, s, t2, lam, _lib.DR_RIDGE_REL_TRACE, ws_, le, r2s, infos, stream=side)
+        api.dr_project_span(K, s, t2, lam, _lib.DR_RIDGE_REL_TRACE, ws_, le, r2s, infos, workspace=sp_ws,
+                            stream=side)
         mark(6, side)
         api.dr_select_topk(s, k_top, idx, wt, infot, stream=side)
         mark(7, side)
@@ -488,7 +491,31 @@ def run_small(args, api, _lib, workloads, dev, peaks, with_cpu, with_next):
     for _ in range(steps):
         step()
     torch.cuda.synchronize()
-    ms_per_step = (time.perf_counter() - t0) * 1e3 / steps
+    ms_eager = (time.perf_counter() - t0) * 1e3 / steps
+    # The step captured once in a HIP graph and replayed: the same kernels
+    # with the host's launch cost taken out (the eager step enqueues about ten
+    # kernels, four events and two stream joins, which a slow host cannot
+    # always keep ahead of 0.4 ms of GPU work).  Falls back to the eager rate.
+    ms_graph, graph_note = None, None
+    try:
+        graph = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.graph(graph, stream=cap):
+            step()
+        torch.cuda.synchronize()
+        for _ in range(5):
+            graph.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            graph.replay()
+        torch.cuda.synchronize()
+        ms_graph = (time.perf_counter() - t0) * 1e3 / steps
+    except Exception as exc:   # noqa: BLE001 (report and keep the eager rate)
+        graph_note = f"graph capture failed ({type(exc).__name__}: {exc}); eager rate reported"
+        torch.cuda.synchronize()
+    ms_per_step = ms_graph if ms_graph is not None else ms_eager
     # per-stage breakdown from a second run of the same steps with events
     # (an event between two kernels costs this stream about 4-5 us)
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(8)] for _ in range(steps)]
@@ -507,6 +534,8 @@ def run_small(args, api, _lib, workloads, dev, peaks, with_cpu, with_next):
                     "U{128..512}, 64x64 Gaussian sketches per layer (32768 columns), cone NNLS 200 iterations + "
                     "ridge span + top-32 + combine on the same Gram",
         "ms_per_step": ms_per_step, "sketched_grads_per_s": N / (ms_per_step * 1e-3),
+        "timing": ("HIP graph replay of the whole step" if ms_graph is not None else graph_note),
+        "ms_per_step_eager": ms_eager,
         "projection_steps_per_s": 1e3 / proj_ms, "projection_ms": proj_ms, "stages_ms": stage_ms,
         "valid_tokens": int(lens.sum()),
         "roofline": _roofline("dr_sketch_grads (sketch_plan_kernel + sketch_packed_kernel + "
