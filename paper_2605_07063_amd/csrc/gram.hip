@@ -75,6 +75,10 @@ struct GramArgs {
   int P;
   int NT, pairs, CK, maxchunks;
   float* partial;                   // [P][pairs][maxchunks][kTile*kTile]
+  float* K;                         // outputs (gram_tile_lds_kernel writes them itself when
+  float* s;                         // maxchunks == 1); group p of the launch is pbase + p
+  float* t2;
+  long long pbase;
 };
 
 template <bool BF16>
@@ -231,9 +235,12 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_lds_kernel(GramArgs a) 
   const int chunk = blockIdx.x, q = blockIdx.y, p = blockIdx.z;
   const long long g0 = a.goff[p], g1 = a.goff[p + 1];
   const long long c0 = g0 + (long long)chunk * a.CK;
-  if (c0 >= g1) return;
+  // with one chunk per group the tile is final and written here, so an
+  // empty group still writes its zeros (no steps)
+  const bool direct = a.maxchunks == 1;
+  if (c0 >= g1 && !direct) return;
   const long long c1 = c0 + a.CK < g1 ? c0 + a.CK : g1;
-  const int nsteps = (int)((c1 - c0 + kLS - 1) / kLS);
+  const int nsteps = c1 > c0 ? (int)((c1 - c0 + kLS - 1) / kLS) : 0;
   int I, J;
   pair_to_tiles(q, I, J);
   const bool diag = I == J;
@@ -395,6 +402,36 @@ __global__ __launch_bounds__(kThreads, 2) void gram_tile_lds_kernel(GramArgs a) 
     run(T{}, std::integral_constant<int, 15>{});
   }
 
+  if (direct) {
+    // the reduction's writes for a single chunk: K's lower triangle and
+    // mirror, and from a diagonal tile the scores and t2 in its upper
+    // triangle
+    float* Kp = a.K + (a.pbase + p) * (long long)a.n * a.n;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int tr = wr * 32 + i * 16 + lg * 4 + r, tc = wc * 32 + j * 16 + lr;
+          const int row = I * kTile + tr, col = J * kTile + tc;
+          const float v = acc[i][j][r];
+          if (col <= row) {
+            if (row < a.n) {
+              Kp[(long long)row * a.n + col] = v;
+              Kp[(long long)col * a.n + row] = v;
+            }
+          } else if (diag) {
+            if ((tr == 0 || tr == 16) && tc >= 32) {
+              const int srow = I * kTile + 2 * tr + (tc - 32);
+              if (srow < a.n) a.s[(a.pbase + p) * (long long)a.n + srow] = v;
+            } else if (I == 0 && tr == 0 && tc == 16) {
+              a.t2[a.pbase + p] = v;
+            }
+          }
+        }
+    return;
+  }
   float* out = a.partial + (((long long)p * a.pairs + q) * a.maxchunks + chunk) * (kTile * kTile);
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -986,6 +1023,10 @@ dr_status gram_run(const GramPlan& g, const void* G, int64_t n, int64_t ldG, con
     a.CK = g.CK;
     a.maxchunks = g.maxchunks;
     a.partial = partial;
+    a.K = K;
+    a.s = s;
+    a.t2 = t2;
+    a.pbase = p0;
     if (gram_use_big(n, P, dtype)) {
       BigArgs b = {};
       b.G = static_cast<const unsigned char*>(G);
@@ -1015,9 +1056,11 @@ dr_status gram_run(const GramPlan& g, const void* G, int64_t n, int64_t ldG, con
       else
         hipLaunchKernelGGL(gram_tile_lds_kernel, grid, dim3(kThreads), 0, hs, a);
       if ((st = launch_status()) != DR_OK) return st;
-      hipLaunchKernelGGL(gram_reduce_kernel, dim3(g.pairs, gp, kTile * kTile / kThreads), dim3(kThreads), 0, hs, a,
-                         K, s, t2, (long long)p0);
-      if ((st = launch_status()) != DR_OK) return st;
+      if (bf || g.maxchunks > 1) {   // fp32 tiles of a single chunk are written by the tile kernel
+        hipLaunchKernelGGL(gram_reduce_kernel, dim3(g.pairs, gp, kTile * kTile / kThreads), dim3(kThreads), 0, hs,
+                           a, K, s, t2, (long long)p0);
+        if ((st = launch_status()) != DR_OK) return st;
+      }
     }
     if (bf) {
       // bf16 sketches: s and t2 against the fp32 target mean in a separate pass

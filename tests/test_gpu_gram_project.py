@@ -2,6 +2,8 @@
 dr_combine against the oracle, on identical inputs, plus the invariants the
 paper's problem statement fixes."""
 
+import itertools
+
 import numpy as np
 import pytest
 import torch
@@ -35,6 +37,9 @@ def rand(shape, seed, dtype=torch.float32, scale=1.0):
     (128, 2048, None, torch.float32),                 # LDS-staged tiles: two full row tiles
     (178, 1568, [0, 768, 1568], torch.float32),       # LDS-staged tiles: 50 rows in the third row tile
     (130, 2400, [8 * i for i in range(301)], torch.float32),   # 300 groups: two launches (256 + 44 groups)
+    # 300 groups of one chunk each (tiles written without the reduction), two of them empty
+    (130, 2400, [0] + list(itertools.accumulate([0 if g in (5, 100) else (16 if g in (6, 101) else 8)
+                                                 for g in range(300)])), torch.float32),
 ])
 def test_gram_matches_oracle(n, kappa, goff, dtype):
     G = rand((n, kappa), 10 + n, dtype)
